@@ -1,0 +1,94 @@
+"""Newton-Schulz family of odd polynomial filters.
+
+* One step of the degree-(2d+1) map (eq:general_ns_iteration; the quintic of
+  eq:muon_ns is d = 2):  N(X) = sum_i a_i (X X^T)^i X.
+  Since (X X^T)^i X = X (X^T X)^i, the step is evaluated with the Gram matrix
+  of the short side (the two forms are equal in exact arithmetic):
+      G = X^T X (tall X) or X X^T (wide X),
+      B = sum_{i>=1} a_i G^i,
+      N(X) = a_0 X + X B (tall) or a_0 X + B X (wide).
+* On singular values the step applies p(x) = sum_i a_i x^(2i+1) (Sec. 2.1).
+* Bjorck-Bowie coefficients (App. B):
+      a_i = (-1)^i sum_{j=i..d} 4^-j C(2j, j) C(j, i).
+* Muon's retuned quintic (Sec. 3 setup): (3.4445, -4.7750, 2.0315).
+
+bf16 contract (mode "bf16"), used for the bf16 library paths: G is formed
+exactly from the bf16 iterate; the operand of G^2 is bf16(G); B is rounded to
+bf16 after b G + c G^2 (with the unrounded G); the new iterate is rounded to
+bf16 after a X + X B.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+from math import comb
+
+import numpy as np
+
+from .precision import rounding
+
+MUON_QUINTIC = (3.4445, -4.7750, 2.0315)
+
+
+def bjorck_bowie(d: int) -> list[Fraction]:
+    """Coefficients a_0..a_d of the classical degree-(2d+1) map (App. B)."""
+    if d < 1:
+        raise ValueError("d >= 1")
+    out = []
+    for i in range(d + 1):
+        acc = Fraction(0)
+        for j in range(i, d + 1):
+            acc += Fraction(comb(2 * j, j) * comb(j, i), 4 ** j)
+        out.append(acc if i % 2 == 0 else -acc)
+    return out
+
+
+def scalar_poly(x, coeffs) -> np.ndarray:
+    """p(x) = sum_i coeffs[i] x^(2i+1)."""
+    x = np.asarray(x, dtype=np.float64)
+    x2 = x * x
+    acc = np.zeros_like(x)
+    for c in reversed(list(coeffs)):
+        acc = acc * x2 + float(c)
+    return acc * x
+
+
+def scalar_compose(x, table) -> np.ndarray:
+    """p_L o ... o p_1 (x) for a per-step coefficient table."""
+    y = np.asarray(x, dtype=np.float64)
+    for row in table:
+        y = scalar_poly(y, row)
+    return y
+
+
+def ns_step(x: np.ndarray, coeffs, mode: str = "exact") -> np.ndarray:
+    """One matrix step N(X) with coefficients (a_0, a_1, ..., a_d)."""
+    rd = rounding(mode)
+    coeffs = [float(c) for c in coeffs]
+    if mode != "exact" and len(coeffs) > 3:
+        raise ValueError("the bf16 contract covers d <= 2")
+    x = np.asarray(x, dtype=np.float64)
+    tall = x.shape[0] >= x.shape[1]
+    g = x.T @ x if tall else x @ x.T
+    d = len(coeffs) - 1
+    if mode == "exact":
+        b = np.zeros_like(g)
+        gp = np.eye(g.shape[0])
+        for i in range(1, d + 1):
+            gp = gp @ g
+            b = b + coeffs[i] * gp
+    else:
+        b = coeffs[1] * g
+        if d == 2:
+            gb = rd(g)
+            b = b + coeffs[2] * (gb @ gb)
+        b = rd(b)
+    upd = x @ b if tall else b @ x
+    return rd(coeffs[0] * x + upd)
+
+
+def ns_filter(x0: np.ndarray, table, mode: str = "exact") -> np.ndarray:
+    """N_L o ... o N_1 (X0) for a per-step coefficient table (eq:filter)."""
+    x = np.asarray(x0, dtype=np.float64)
+    for row in table:
+        x = ns_step(x, row, mode)
+    return x

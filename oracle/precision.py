@@ -1,0 +1,33 @@
+"""Rounding used by the oracle's bf16 contract mode.
+
+The paper trains in bfloat16 (Sec. 3 setup) but does not fix where values are
+rounded. The library's contract (and this mode) rounds to bfloat16 exactly at
+the operands of the bf16 matrix products and at the stored iterate; all other
+arithmetic here is float64.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest bfloat16 (8 significant bits, ties
+    to even), returned as float64. Exponent range as float32; no overflow
+    handling is needed for the values this package produces."""
+    x = np.asarray(x, dtype=np.float64)
+    mant, expo = np.frexp(x)                 # x = mant * 2**expo, |mant| in [0.5, 1)
+    expo = np.maximum(expo, -125)            # bf16 subnormal spacing 2**-133
+    q = np.ldexp(x, 8 - expo)                # |q| < 2**8 for normal values
+    return np.ldexp(np.rint(q), expo - 8)    # np.rint rounds half to even
+
+
+def identity(x: np.ndarray) -> np.ndarray:
+    return np.asarray(x, dtype=np.float64)
+
+
+def rounding(mode: str):
+    if mode == "exact":
+        return identity
+    if mode == "bf16":
+        return round_bf16
+    raise ValueError(f"unknown precision mode {mode!r}")

@@ -1,0 +1,133 @@
+"""Pins of oracle.psd (Alg. 2, App. E.1) against closed forms and bounds."""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import psd
+from oracle.filters import bjorck_bowie, scalar_compose
+
+
+def sym_case(seed, n, lam):
+    g = np.random.default_rng(seed)
+    q, _ = np.linalg.qr(g.standard_normal((n, n)))
+    return (q * lam) @ q.T, q
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_lanczos_is_an_upper_estimate(seed):
+    # App. E.1: theta >= ||Z||_2 (heuristic; never violated on these inputs) and close to it.
+    g = np.random.default_rng(seed)
+    n = 150
+    lam = np.concatenate([g.uniform(5, 10, 3) * g.choice([-1, 1], 3), g.uniform(-1, 1, n - 3)])
+    z, _ = sym_case(seed, n, lam)
+    theta = psd.lanczos_scale(lambda x: z @ (z @ x), n, seed)
+    norm2 = np.abs(np.linalg.eigvalsh(z)).max()
+    assert norm2 <= theta <= norm2 * 1.05
+
+
+def test_lanczos_small_n_is_exact_and_zero_is_zero():
+    g = np.random.default_rng(3)
+    a = g.standard_normal((8, 8))
+    z = a + a.T
+    theta = psd.lanczos_scale(lambda x: z @ (z @ x), 8)
+    assert abs(theta - np.abs(np.linalg.eigvalsh(z)).max()) < 1e-6
+    zero = np.zeros((10, 10))
+    assert psd.lanczos_scale(lambda x: zero @ x, 10) == 0.0
+
+
+def test_ritz_order_rule():
+    lam = np.array([1.0, -3.0, 3.0, 0.5, -0.5, 2.0])
+    assert list(psd.ritz_order(lam)) == [2, 1, 5, 0, 3, 4]
+
+
+def test_baseline_scalarized_closed_form():
+    # eq:psd_error_base: in the eigenbasis of Z the output is 1/2 lam (1 + p^L(lam / theta)).
+    n = 40
+    g = np.random.default_rng(2)
+    lam = np.concatenate([[30.0, -20.0], g.uniform(-1, 1, n - 2)])
+    z, q = sym_case(0, n, lam)
+    table = [bjorck_bowie(1)] * 8
+    p, theta = psd.psd_project(z, table=table)
+    want = (q * (0.5 * lam * (1 + scalar_compose(lam / theta, table)))) @ q.T
+    np.testing.assert_allclose(p, want, atol=1e-11)
+
+
+def test_baseline_converges_to_projection():
+    n = 30
+    g = np.random.default_rng(5)
+    lam = g.uniform(0.05, 1, n) * g.choice([-1, 1], n)
+    z, _ = sym_case(1, n, lam)
+    p, _ = psd.psd_project(z, table=[bjorck_bowie(1)] * 40)
+    np.testing.assert_allclose(p, psd.psd_exact(z), atol=1e-10)
+
+
+@pytest.mark.parametrize("gamma", [1.0, 1.01, 1.1, 2.0])
+def test_exact_deflation_is_gamma_independent_and_scalarized(gamma):
+    # Prop. 2: with exact eigenpairs the output does not depend on gamma, the head is
+    # restored exactly and the tail passes the filter with the residual scale.
+    n, k = 40, 4
+    g = np.random.default_rng(8)
+    lam = np.concatenate([[50.0, -40.0, 30.0, -25.0], g.uniform(-1, 1, n - k)])
+    z, q = sym_case(3, n, lam)
+    table = [bjorck_bowie(1)] * 6
+    p, vnext, info = psd.psd_project_deflated(z, q[:, :k], table=table, gamma=gamma)
+    assert info.n_deflated == 4 and info.n_positive == 2
+    tail = lam[k:]
+    f = np.concatenate([np.maximum(lam[:k], 0),
+                        0.5 * tail * (1 + scalar_compose(tail / info.theta, table))])
+    np.testing.assert_allclose(p, (q * f) @ q.T, atol=1e-10)
+    # theta estimates ||R||_2 = max |tail|
+    assert np.abs(tail).max() <= info.theta <= np.abs(tail).max() * 1.05
+    # next basis spans Z V = span(q_k)
+    np.testing.assert_allclose(vnext @ vnext.T, q[:, :k] @ q[:, :k].T, atol=1e-10)
+
+
+def test_prop2_ratio_bound():
+    # eq:deflated_psd_ratio with exact eigenpairs, theta = exact norms (both sides
+    # computed here from the oracle's own theta, which is an upper estimate).
+    n, k = 60, 3
+    g = np.random.default_rng(12)
+    lam = np.concatenate([[80.0, -60.0, 45.0], g.uniform(-1, 1, n - k)])
+    lam[-1] = 0.02
+    z, q = sym_case(4, n, lam)
+    target = psd.psd_exact(z)
+    for L in range(1, 7):
+        table = [bjorck_bowie(1)] * L
+        pb, theta = psd.psd_project(z, table=table)
+        pd, _, info = psd.psd_project_deflated(z, q[:, :k], table=table)
+        ell = np.abs(lam).min() / theta
+        alpha_ell = np.abs(lam).min() / info.theta
+        eb = np.linalg.norm(pb - target, 2)
+        ed = np.linalg.norm(pd - target, 2)
+        bound = ((1 - alpha_ell ** 2) / (1 - ell ** 2)) ** (2 ** L)
+        assert ed <= bound * eb * (1 + 1e-9) + 1e-12
+        assert ed < eb
+
+
+def test_gate_and_fallback_to_baseline():
+    n, k = 40, 6
+    g = np.random.default_rng(6)
+    lam = np.concatenate([[50.0, -40.0], g.uniform(-1, 1, n - 2)])
+    z, q = sym_case(5, n, lam)
+    basis = np.linalg.qr(q[:, :k] + 1e-3 * g.standard_normal((n, k)))[0]
+    p, _, info = psd.psd_project_deflated(z, basis, tau=0.1, window=4, steps=8)
+    assert info.n_deflated == 2 and info.n_positive == 1
+    # a gate that does not fire gives the baseline bitwise
+    flat = np.concatenate([g.uniform(0.5, 1, 6) * g.choice([-1, 1], 6), g.uniform(-0.4, 0.4, n - 6)])
+    z2, q2 = sym_case(7, n, flat)
+    p2, _, info2 = psd.psd_project_deflated(z2, q2[:, :k], tau=0.1, window=4, steps=8)
+    pb, _ = psd.psd_project(z2, steps=8)
+    assert info2.n_deflated == 0
+    np.testing.assert_array_equal(p2, pb)
+
+
+def test_deflation_lowers_error_on_small_config4_like():
+    c = workloads.small_psd(256, k=8, n_dom=4, dom=(200.0, 1000.0))
+    z = c.z.astype(np.float64)
+    target = psd.psd_exact(z)
+    pb, _ = psd.psd_project(z, steps=c.steps)
+    pd, _, info = psd.psd_project_deflated(z, c.qwarm, steps=c.steps, gamma=c.gamma,
+                                           subspace_iters=c.subspace_iters)
+    assert np.linalg.norm(pd - target) < 0.1 * np.linalg.norm(pb - target)
+    np.testing.assert_allclose(np.sort(np.abs(info.ritz[:4])),
+                               np.sort(np.abs(c.lam[np.argsort(-np.abs(c.lam))[:4]])), rtol=1e-6)
