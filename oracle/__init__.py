@@ -14,7 +14,7 @@ Modules
   filters    Newton-Schulz family: Bjorck-Bowie coefficients (App. B), the
              scalar odd polynomials and one matrix step (eq:muon_ns,
              eq:general_ns_iteration).
-  linalg     CholeskyQR / CholeskyQR2 of a tall panel.
+  linalg     CholeskyQR of a tall panel.
   muon       Batched randomized SVD (Alg. 3), the deflated polar factor
              (Alg. 1), the undeflated baseline and the exact polar factor.
   psd        Lanczos scale estimate (App. E.1), the deflated PSD projection

@@ -34,7 +34,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from .filters import ns_filter
-from .linalg import cholqr2
+from .linalg import cholqr
 from .precision import rounding
 from .rng import sketch
 
@@ -58,10 +58,10 @@ def tall_view(m: np.ndarray) -> tuple[np.ndarray, bool]:
 def randomized_svd(a, r, rprime, power_iters, omega, mode="exact"):
     """Alg. 3 for one tall matrix a (n x m). Returns U (n x r), s (r), V (m x r)."""
     rd = rounding(mode)
-    q = cholqr2(a @ rd(omega))
+    q = cholqr(a @ rd(omega))
     for _ in range(power_iters):
-        y = cholqr2(a.T @ rd(q))
-        q = cholqr2(a @ rd(y))
+        y = cholqr(a.T @ rd(q))
+        q = cholqr(a @ rd(y))
     g = rd(q).T @ a
     ug, s, vt = np.linalg.svd(g, full_matrices=False)
     u = q @ ug

@@ -35,7 +35,7 @@ from dataclasses import dataclass
 import numpy as np
 
 from .filters import ns_filter
-from .linalg import cholqr2
+from .linalg import cholqr
 from .rng import lanczos_start
 
 CUBIC = (1.5, -0.5)
@@ -95,7 +95,7 @@ def psd_project_deflated(z, basis, *, table=None, steps=10, gamma=1.1, tau=0.0,
     n, kk = v.shape
     table = [CUBIC] * steps if table is None else table
     for _ in range(subspace_iters - 1):
-        v = cholqr2(z @ v)
+        v = cholqr(z @ v)
     zt = z @ v
     t = v.T @ zt
     t = 0.5 * (t + t.T)
@@ -125,7 +125,7 @@ def psd_project_deflated(z, basis, *, table=None, steps=10, gamma=1.1, tau=0.0,
         p = 0.5 * (z + z @ g)
         n_pos = 0
     p = 0.5 * (p + p.T)
-    return p, cholqr2(zt), PSDInfo(n_def, n_pos, theta, lam)
+    return p, cholqr(zt), PSDInfo(n_def, n_pos, theta, lam)
 
 
 def psd_project(z, *, table=None, steps=10, seed=0, lanczos_steps=20):
