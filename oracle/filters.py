@@ -12,10 +12,12 @@
       a_i = (-1)^i sum_{j=i..d} 4^-j C(2j, j) C(j, i).
 * Muon's retuned quintic (Sec. 3 setup): (3.4445, -4.7750, 2.0315).
 
-bf16 contract (mode "bf16"), used for the bf16 library paths: G is formed
-exactly from the bf16 iterate; the operand of G^2 is bf16(G); B is rounded to
-bf16 after b G + c G^2 (with the unrounded G); the new iterate is rounded to
-bf16 after a X + X B.
+bf16 contract (mode "bf16"), used for the bf16 library paths ("bfloat16
+mixed precision" of Sec. 3: bf16 operands, wider accumulation and state): the
+iterate X stays wide; every matrix product takes bf16-rounded operands, so
+G = bf16(X)^T bf16(X); the operand of G^2 is bf16(G); B = bf16(b G + c G^2)
+(with the unrounded G) is a product operand; the new iterate a X + bf16(X) B
+is not rounded.
 """
 from __future__ import annotations
 
@@ -68,7 +70,8 @@ def ns_step(x: np.ndarray, coeffs, mode: str = "exact") -> np.ndarray:
         raise ValueError("the bf16 contract covers d <= 2")
     x = np.asarray(x, dtype=np.float64)
     tall = x.shape[0] >= x.shape[1]
-    g = x.T @ x if tall else x @ x.T
+    xo = rd(x)                                  # product operand
+    g = xo.T @ xo if tall else xo @ xo.T
     d = len(coeffs) - 1
     if mode == "exact":
         b = np.zeros_like(g)
@@ -82,8 +85,8 @@ def ns_step(x: np.ndarray, coeffs, mode: str = "exact") -> np.ndarray:
             gb = rd(g)
             b = b + coeffs[2] * (gb @ gb)
         b = rd(b)
-    upd = x @ b if tall else b @ x
-    return rd(coeffs[0] * x + upd)
+    upd = xo @ b if tall else b @ xo
+    return coeffs[0] * x + upd
 
 
 def ns_filter(x0: np.ndarray, table, mode: str = "exact") -> np.ndarray:

@@ -24,8 +24,9 @@ Degenerate scales (no epsilon is added, the paper has none): a zero nu or a
 zero ||A||_F drops that term (a zero matrix maps to zero).
 
 Modes: "exact" (float64 throughout) and "bf16" (the bf16 contract: the sketch
-products take bf16 operands Omega, Q and Y; X0 and every iterate are rounded
-to bf16; see filters.ns_step for the step itself).
+products take bf16 operands Omega, Q and Y; X0 and the iterates stay wide and
+every filter product takes bf16 operands (filters.ns_step); the output is
+rounded to bf16).
 """
 from __future__ import annotations
 
@@ -80,18 +81,17 @@ def deflation_rank(s: np.ndarray, k: int, tau: float) -> int:
     return 0
 
 
-def deflated_init(a, u, s, v, k_eff, gamma, mode="exact"):
+def deflated_init(a, u, s, v, k_eff, gamma):
     """Padded initialization X0 of Alg. 1 and the residual norm used."""
-    rd = rounding(mode)
     if k_eff == 0:
         nrm = float(np.linalg.norm(a))
         x0 = a / nrm if nrm > 0 else np.zeros_like(a)
-        return rd(x0), nrm
+        return x0, nrm
     uk, sk, vk = u[:, :k_eff], s[:k_eff], v[:, :k_eff]
     r = a - (uk * sk) @ vk.T
     nu = float(np.linalg.norm(r))
     x0 = (r / nu if nu > 0 else np.zeros_like(r)) + (uk @ vk.T) / gamma
-    return rd(x0), nu
+    return x0, nu
 
 
 def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
@@ -114,8 +114,8 @@ def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
         else:
             u = s = v = None
             k_eff = 0
-        x0, nu = deflated_init(a, u, s, v, k_eff, gamma, mode)
-        xl = ns_filter(x0, coeffs, mode)
+        x0, nu = deflated_init(a, u, s, v, k_eff, gamma)
+        xl = rounding(mode)(ns_filter(x0, coeffs, mode))
         outs.append(xl.T if transposed else xl)
         keff.append(k_eff)
         nus.append(nu)
