@@ -149,4 +149,4 @@ def test_bf16_mode_outputs_are_bf16_and_close():
     b, _ = muon.msign_deflated(c.x64, 4, c.coeffs, mode="bf16")
     np.testing.assert_array_equal(round_bf16(b), b)
     rel = np.linalg.norm(b - e) / np.linalg.norm(e)
-    assert 1e-6 < rel < 1e-2
+    assert 1e-6 < rel < 3e-2
