@@ -1,0 +1,165 @@
+#!/usr/bin/env python3
+"""Benchmark of the deflated polar factor on one MI355X.
+
+Workload (one "step" = one call that runs the whole path): 24 matrices of
+768 x 3072 in bfloat16 (the largest group of a GPT-2-small-shaped Muon
+batch), spectra with 8 spikes geometric from 50 down to 5 over a log-uniform
+bulk in [1e-4, 1]; deflation rank k = 8, oversample 8, one power iteration,
+5 steps of Muon's quintic (3.4445, -4.7750, 2.0315), gamma = 1.01. Inputs are
+seeded and synthetic and are resident in HBM before the timed region.
+
+Prints one JSON line: matrices/s (value), the achieved TFLOP/s against the
+bf16 MFMA peak, a roofline entry for the dominant kernel (the iterate update
+X <- a X + B X, timed with HIP events inside the timed region) and the CPU
+oracle timed on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+HBM_PEAK_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def ns_flops_per_matrix(s: int, l: int, steps: int) -> float:
+    """Algorithmic flops of the filter for one s x l matrix: per step the Gram
+    X X^T and A^2 counted once per symmetric entry, plus the 2 s^2 l update."""
+    return steps * (s * (s + 1) * (l + s) + 2.0 * s * s * l)
+
+
+def front_flops_per_matrix(s: int, l: int, k: int, rp: int, power_iters: int) -> float:
+    """Sketch, power and projection products (2 s l r' each) plus the two
+    rank-k passes (residual norm and start)."""
+    return (2 + 2 * power_iters) * 2.0 * s * l * rp + 2 * 2.0 * s * l * k
+
+
+def cpu_baseline(case, seconds: float) -> dict:
+    from threadpoolctl import threadpool_info
+    from oracle import muon as omuon
+    from oracle import rng as orng
+    s = min(case.x.shape[1:])
+    rp = min(s, case.k + case.oversample)
+    threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
+    done, t0 = 0, time.perf_counter()
+    while done < case.x.shape[0]:
+        x64 = case.x64[done:done + 1]
+        omuon.msign_deflated(x64, case.k, case.coeffs, oversample=case.oversample,
+                             power_iters=case.power_iters, gamma=case.gamma, mode="bf16",
+                             sketches=[orng.sketch(0, done, s, rp)])
+        done += 1
+        if time.perf_counter() - t0 >= seconds:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": done / dt, "unit": "matrices/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{done} of {case.x.shape[0]} matrices 768x3072, float64 oracle in bf16-contract "
+                      f"mode, {dt:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--baseline", action="store_true", help="time the undeflated filter (k = 0) instead")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        log("bench.py: this build runs on a single GPU; --gpus must be 1 "
+            "(the method shards by matrix across GPUs, which is not built here)")
+        return 2
+
+    import torch
+    import paper_2609_21102_amd as sd
+    import workloads
+
+    case = workloads.config2("768x3072")
+    b, m, n = case.x.shape
+    k = 0 if args.baseline else case.k
+    s, l = min(m, n), max(m, n)
+    rp = min(s, k + case.oversample) if k else 0
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    x = torch.from_numpy(case.x.view(np.int16).copy()).view(torch.bfloat16).to(dev)
+    out = torch.empty_like(x)
+    ws = torch.empty(sd.msign_workspace_bytes(b, m, n, k, sd.SD_DTYPE_BF16), dtype=torch.uint8, device=dev)
+    coeffs = case.coeffs
+
+    def step():
+        sd.msign(x, k, case.steps, coeffs, oversample=case.oversample, power_iters=case.power_iters,
+                 gamma=case.gamma, out=out, workspace=ws)
+
+    log(f"bench: {b} x {m} x {n} bf16, k={k}, warmup {args.warmup}, steps {args.steps}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    sd.profile_reset()
+    sd.profile_set("ns_update")
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    sd.profile_set()
+    ms_total = start.elapsed_time(end)
+    upd_ms, upd_n = sd.profile_read("ns_update")
+    ms_per_step = ms_total / args.steps
+    value = b * args.steps / (ms_total / 1e3)
+    flops = b * (ns_flops_per_matrix(s, l, case.steps) + (front_flops_per_matrix(s, l, k, rp, case.power_iters)
+                                                          if k else 0.0))
+    tflops = flops / (ms_per_step / 1e3) / 1e12
+    upd_flops = 2.0 * s * s * l * b
+    upd_avg_ms = upd_ms / max(upd_n, 1)
+    upd_tflops = upd_flops / (upd_avg_ms / 1e3) / 1e12
+    log(f"bench: {ms_per_step:.3f} ms/step, {value:.0f} matrices/s, {tflops:.1f} TFLOP/s; "
+        f"update kernel {upd_avg_ms * 1e3:.1f} us avg over {upd_n} launches ({upd_tflops:.1f} TFLOP/s)")
+
+    result = {
+        "metric": "deflated msign matrices/s + TFLOP/s (% MFMA peak), batched 768x3072 bf16",
+        "value": value,
+        "unit": "matrices/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"deflated msign, {b} x {m} x {n} bf16, k={k}, oversample {case.oversample}, "
+                               f"{case.power_iters} power iteration, {case.steps} Muon quintic steps",
+                   "batch": b, "m": m, "n": n, "k": k, "steps": case.steps, "parallelism": "single GPU"},
+        "tflops": tflops,
+        "mfma_frac": tflops / MFMA_BF16_PEAK_TFLOPS,
+        "roofline": {"bound": "mfma", "kernel": "gemm_kernel<bf16, NN> (X <- a X + B X)",
+                     "achieved": upd_tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": upd_tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
+                     "avg_launch_us": upd_avg_ms * 1e3, "flops_per_launch": upd_flops},
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a sample")
+        result["cpu_baseline"] = cpu_baseline(case, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

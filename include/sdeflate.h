@@ -1,0 +1,214 @@
+/*
+ * sdeflate: spectrally deflated fixed-depth polynomial matrix filters on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: "Spectral Deflation for Factorization-Free Matrix Filtering in Muon
+ * and Semidefinite Programming" (arXiv 2609.21102). A fixed-depth polynomial
+ * filter X_t = p_t(X_{t-1}) started from a normalized input (eq:filter) is
+ * run on the residual left after removing an estimated dominant rank-k part;
+ * the removed part is padded back into the start (Muon) or restored after the
+ * filter (PSD projection). Deflation leaves the target matrix function
+ * unchanged (eq:identities).
+ *
+ * Conventions shared by every entry point
+ *   - Data pointers are DEVICE pointers owned by the caller. Matrices are
+ *     dense, row-major and contiguous. Coefficient tables are HOST pointers,
+ *     read before the call returns.
+ *   - Work is enqueued on `stream` (0 = the null stream) and never waits for
+ *     the device; results are ready when the stream reaches that point.
+ *   - Return value: SD_OK, or a negative sd_status. Argument errors are
+ *     reported synchronously and nothing is enqueued. SD_ERR_HIP reports a
+ *     failed allocation or launch. Numerical events found on the device are
+ *     reported through the optional `status_dev` word of the options.
+ *   - Without a caller workspace the library allocates one per call from the
+ *     device's stream-ordered memory pool (hipMallocAsync / hipFreeAsync on
+ *     `stream`), so calls on different streams do not share scratch memory.
+ *   - `in` may equal `out`: the input is fully consumed before the output is
+ *     written.
+ *   - Random numbers (the Gaussian sketch of Alg. 3, the Lanczos start vector)
+ *     come from Philox4x32-10 with key = seed and counter = (call, matrix,
+ *     stream, 0) and a float64 Box-Muller transform; identical seeds give
+ *     identical results, run to run.
+ */
+#ifndef SDEFLATE_H
+#define SDEFLATE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SD_OK = 0,
+  SD_ERR_INVALID_ARG = -1, /* bad sizes, null pointers, options out of range */
+  SD_ERR_UNSUPPORTED = -2, /* valid but outside this build (e.g. sketch wider than 64) */
+  SD_ERR_HIP = -3,         /* HIP allocation or launch failure */
+  SD_ERR_NUMERIC = -4,     /* reserved: numerical failures are flagged in status_dev */
+  SD_ERR_WORKSPACE = -5    /* caller workspace smaller than the *_workspace_bytes query */
+} sd_status;
+
+enum { SD_DTYPE_F32 = 0, SD_DTYPE_BF16 = 1 };
+
+/* Bits set (atomically OR-ed) in *status_dev when the device meets them. */
+enum { SD_FLAG_PIVOT_FLOOR = 2 /* a CholeskyQR pivot hit its floor: a rank-deficient panel */ };
+
+/* ------------------------------------------------------------------ Muon --
+ * Deflated polar factor, batched (Alg. 1 with the batched randomized SVD of
+ * Alg. 3). For every matrix M of the batch [batch, m, n]:
+ *   - orientation: a matrix with m > n is processed as M^T and its result
+ *     transposed back, polar(M^T) = polar(M)^T (App. D, grouping);
+ *   - head estimate: Alg. 3 with r' = min(min(m, n), k + oversample) sketch
+ *     columns and power_iters subspace iterations, one CholeskyQR pass after
+ *     every product (float64 Gram and factorization), thin SVD of the
+ *     r' x min(m,n) reduced matrix;
+ *   - deflation rank: k (fixed rank, tau = 0), or the gate of Alg. 1 on the
+ *     k estimated values: if s_k < tau s_1 deflate max{i : s_i > tau s_1}
+ *     components, else none;
+ *   - start: X0 = R / ||R||_F + gamma^-1 U_k V_k^T with R = M - U_k S_k V_k^T
+ *     (Alg. 1), or X0 = M / ||M||_F when nothing is deflated; a zero norm
+ *     drops its term, so a zero matrix maps to zero;
+ *   - filter: L = steps steps X <- a_t X + (b_t A + c_t A^2) X with A the Gram
+ *     of the short side (eq:muon_ns; Polar-Express-style tables give one row
+ *     per step).
+ * coeffs: HOST float[steps][3] (a_t, b_t, c_t), or NULL for Muon's retuned
+ *   quintic (3.4445, -4.7750, 2.0315) at every step (Sec. 3 setup).
+ * Precision: the f32 entry points compute in float32 (MFMA fp32, float32
+ *   accumulation). The bf16 entry points take bfloat16 input and output
+ *   (uint16_t bit patterns); every matrix product takes bf16 operands with
+ *   float32 accumulation, the iterate is stored in bf16, the Gram A in float32
+ *   (and rounded to bf16 where it is a product operand), b A + c A^2 is
+ *   rounded to bf16, and the sketch panels, norms and small factorizations are
+ *   float32 / float64.
+ * Requirements: batch >= 1, m, n >= 1, 0 <= k < min(m, n), k + oversample
+ *   capped at min(m, n) must not exceed 64 (else SD_ERR_UNSUPPORTED),
+ *   0 <= steps <= 1000. k = 0 is the undeflated baseline, and the gated
+ *   variant that deflates nothing returns the baseline bit for bit (Sec. 2.2).
+ */
+typedef struct {
+  int oversample;          /* p >= 0, default 8 */
+  int power_iters;         /* J >= 0, default 1 */
+  float gamma;             /* padding, > 0, default 1.01 */
+  float tau;               /* 0 = fixed rank k (default); in (0, 1): gate of Alg. 1 */
+  uint64_t seed;           /* Philox key, default 0 */
+  const float* sketch;     /* optional device [batch][r'][min(m,n)]: Omega column j of
+                              matrix b at sketch + (b * r' + j) * min(m,n); NULL = Philox */
+  void* workspace;         /* optional device scratch, >= sd_msign_workspace_bytes() */
+  size_t workspace_bytes;
+  int* k_eff_out;          /* optional device int[batch]: deflated components */
+  float* nu_out;           /* optional device float[batch]: norm X0 was scaled by */
+  float* s_out;            /* optional device float[batch][k]: estimated singular values */
+  int* status_dev;         /* optional device int: SD_FLAG_* bits are OR-ed in */
+} sd_msign_opts;
+
+void sd_msign_opts_default(sd_msign_opts* opts);
+
+int sd_msign(int batch, int m, int n, int steps, const float* coeffs, const float* in, float* out,
+             hipStream_t stream);
+int sd_msign_deflated(int batch, int m, int n, int k, int steps, const float* coeffs, const float* in,
+                      float* out, hipStream_t stream);
+int sd_msign_bf16(int batch, int m, int n, int steps, const float* coeffs, const uint16_t* in,
+                  uint16_t* out, hipStream_t stream);
+int sd_msign_deflated_bf16(int batch, int m, int n, int k, int steps, const float* coeffs,
+                           const uint16_t* in, uint16_t* out, hipStream_t stream);
+/* dtype: SD_DTYPE_F32 or SD_DTYPE_BF16 for both in and out; opts may be NULL. */
+int sd_msign_deflated_ex(int batch, int m, int n, int k, int steps, const float* coeffs, int dtype,
+                         const void* in, void* out, const sd_msign_opts* opts, hipStream_t stream);
+/* Workspace an _ex call with these arguments needs (0 on invalid arguments). */
+size_t sd_msign_workspace_bytes(int batch, int m, int n, int k, int dtype, const sd_msign_opts* opts);
+/* The Gaussian sketch Alg. 3 draws (Omega ~ N(0, 1)^{s x r'} per matrix): out[b][j][i]
+ * is entry (i, j) of matrix b's sketch, Gaussian number j * s + i of Philox stream 1.
+ * sd_sketch fills a DEVICE buffer on `stream`; sd_sketch_host computes the same
+ * numbers on the host into a HOST buffer (batch * rp * s floats). */
+int sd_sketch(int batch, int s, int rp, uint64_t seed, float* out, hipStream_t stream);
+int sd_sketch_host(int batch, int s, int rp, uint64_t seed, float* out);
+
+/* ------------------------------------------------------------------- PSD --
+ * Deflated projection onto the PSD cone of a symmetric X (n x n, float32),
+ * one projection of Alg. 2:
+ *   - (subspace_iters - 1) pre-steps V <- CholeskyQR(X V) on the basis V =
+ *     Qwarm (n x k, orthonormal columns, row-major);
+ *   - Zt = X V; Rayleigh-Ritz on V^T Zt; Ritz pairs ordered by |lambda|
+ *     descending (ties: larger lambda, then lower index);
+ *   - deflated set: all k pairs (tau = 0), or the gate of Alg. 2 with window
+ *     r: if s_r < tau s_1, the pairs with |lambda| > tau s_1, else none;
+ *   - R = X - sum lambda u u^T; theta = Lanczos upper estimate of ||R||_2
+ *     (App. E.1: lanczos_steps steps on R^2, largest Ritz pair (rho, v),
+ *     theta = sqrt(rho + ||R^2 v - rho v||)); X0 = R / theta + gamma^-1
+ *     sum sign(lambda) u u^T;
+ *   - g = steps steps of the odd polynomial filter X <- a X + (b A + c A^2) X,
+ *     A = X^2 (cubic: c = 0; default (a, b) = (3/2, -1/2), the d = 1
+ *     Newton-Schulz map of eq:general_ns_iteration);
+ *   - P = R (I + g) / 2 + sum_{lambda > 0} lambda u u^T, then (P + P^T) / 2;
+ *     with nothing deflated, P = X (I + g(X / theta)) / 2 symmetrized
+ *     (eq:baseline_projection);
+ *   - Qwarm <- CholeskyQR(Zt) (the basis for the next call).
+ * Everything is float32 (MFMA fp32), small factorizations float64.
+ * Requirements: n >= 1, 0 <= k < n, k <= 64, 0 <= steps <= 1000; Qwarm is
+ * required when k > 0 and must not overlap X or out. k = 0 is the baseline
+ * (Qwarm unused, may be NULL).
+ */
+typedef struct {
+  int subspace_iters;      /* J >= 1, default 1 */
+  int lanczos_steps;       /* 1..64, default 20 */
+  float gamma;             /* padding, > 0, default 1.1 */
+  float tau;               /* 0 = deflate all k Ritz pairs (default); in (0, 1): gate */
+  int window;              /* r of the gate, 1..k (used when tau > 0) */
+  int poly_degree;         /* 3 (default) or 5 */
+  const float* poly;       /* HOST float[steps][(poly_degree + 1) / 2] or NULL = (1.5, -0.5) */
+  uint64_t seed;           /* Philox key of the Lanczos start, default 0 */
+  void* workspace;
+  size_t workspace_bytes;
+  int* n_deflated_out;     /* optional device int */
+  int* n_positive_out;     /* optional device int */
+  float* theta_out;        /* optional device float */
+  float* ritz_out;         /* optional device float[k], Ritz values in deflation order */
+  int* status_dev;         /* optional device int */
+} sd_psd_opts;
+
+void sd_psd_opts_default(sd_psd_opts* opts);
+
+int sd_psd_project(int n, int steps, const float* X, float* out, hipStream_t stream);
+int sd_psd_project_deflated(int n, int k, int steps, const float* X, float* Qwarm, float* out,
+                            hipStream_t stream);
+int sd_psd_project_deflated_ex(int n, int k, int steps, const float* X, float* Qwarm, float* out,
+                               const sd_psd_opts* opts, hipStream_t stream);
+size_t sd_psd_workspace_bytes(int n, int k, const sd_psd_opts* opts);
+
+/* ---------------------------------------------------------- stage timing --
+ * Benchmark instrumentation (tracing). While a stage's bit (1 << stage) is set
+ * in the mask, the library brackets every launch of that stage with a pair of
+ * HIP events recorded on the call's stream; this adds two event records per
+ * launch and nothing else. sd_profile_read waits for the recorded events
+ * (a host synchronization), adds their elapsed times to the running totals
+ * and returns the totals of one stage. sd_profile_reset clears the totals.
+ * The instrumentation state is process-wide.
+ */
+enum {
+  SD_STAGE_NS_GRAM = 0,    /* A = X X^T (symmetric tiles) */
+  SD_STAGE_NS_POLY = 1,    /* B = b A + c A^2 */
+  SD_STAGE_NS_UPDATE = 2,  /* X <- a X + B X */
+  SD_STAGE_SKETCH = 3,     /* tall-skinny products of Alg. 3 / the subspace step */
+  SD_STAGE_CHOLQR = 4,     /* CholeskyQR of the panels */
+  SD_STAGE_SMALL = 5,      /* small SVD / Rayleigh-Ritz / rotations */
+  SD_STAGE_LOWRANK = 6,    /* residual norm, padded start, PSD residual */
+  SD_STAGE_LANCZOS = 7,    /* Lanczos scale estimate */
+  SD_STAGE_RESTORE = 8,    /* PSD restore product and symmetrized output */
+  SD_STAGE_COUNT = 9
+};
+void sd_profile_set(unsigned mask);
+int sd_profile_read(int stage, double* total_ms, long long* launches);
+void sd_profile_reset(void);
+
+/* ---------------------------------------------------------------- misc ---- */
+const char* sd_status_string(int status);
+int sd_version(void); /* major * 10000 + minor * 100 + patch */
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SDEFLATE_H */

@@ -1,0 +1,199 @@
+// Host-side helpers: workspace carving, stream-ordered scratch allocation and
+// kernel dispatch by compile-time widths.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <vector>
+
+#include "../../include/sdeflate.h"
+#include "common.hpp"
+#include "gemm.hpp"
+#include "lowrank.hpp"
+#include "skinny.hpp"
+#include "small.hpp"
+
+namespace sd {
+
+// Bump allocator over one block; with base == nullptr it only measures.
+struct Arena {
+  char* base = nullptr;
+  size_t off = 0;
+  template <typename T>
+  T* take(size_t count) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += count * sizeof(T);
+    return p;
+  }
+};
+
+// Scratch for one call: the caller's workspace, or a block from the device's
+// stream-ordered pool (released on the same stream at the end of the call).
+struct Scratch {
+  void* ptr = nullptr;
+  bool owned = false;
+  hipStream_t stream = nullptr;
+  int acquire(void* user, size_t user_bytes, size_t need, hipStream_t st) {
+    stream = st;
+    if (user) {
+      if (user_bytes < need) return SD_ERR_WORKSPACE;
+      ptr = user;
+      return SD_OK;
+    }
+    if (need == 0) return SD_OK;
+    static std::once_flag once[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return SD_ERR_HIP;
+    if (dev >= 0 && dev < 64)
+      std::call_once(once[dev], [dev]() {
+        hipMemPool_t pool;
+        if (hipDeviceGetDefaultMemPool(&pool, dev) == hipSuccess) {
+          uint64_t keep = ~0ull;   // keep freed blocks cached in the pool
+          (void)hipMemPoolSetAttribute(pool, hipMemPoolAttrReleaseThreshold, &keep);
+        }
+      });
+    if (hipMallocAsync(&ptr, need, st) != hipSuccess) {
+      ptr = nullptr;
+      (void)hipGetLastError();
+      return SD_ERR_HIP;
+    }
+    owned = true;
+    return SD_OK;
+  }
+  void release() {
+    if (owned && ptr) (void)hipFreeAsync(ptr, stream);
+    ptr = nullptr;
+    owned = false;
+  }
+  ~Scratch() { release(); }
+};
+
+// ------------------------------------------------------ stage timing ------
+// When a stage's bit is set (sd_profile_set), every launch of that stage is
+// bracketed by two HIP events on the call's stream. sd_profile_read waits for
+// the recorded events and accumulates their elapsed times per stage.
+struct Profiler {
+  std::mutex mu;
+  unsigned mask = 0;
+  struct Rec {
+    int stage;
+    hipEvent_t a, b;
+  };
+  std::vector<Rec> pending;
+  std::vector<hipEvent_t> pool;
+  double total_ms[SD_STAGE_COUNT] = {};
+  long long launches[SD_STAGE_COUNT] = {};
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  void drain() {
+    for (auto& r : pending) {
+      float ms = 0.f;
+      if (hipEventSynchronize(r.b) == hipSuccess && hipEventElapsedTime(&ms, r.a, r.b) == hipSuccess) {
+        total_ms[r.stage] += ms;
+        launches[r.stage] += 1;
+      }
+      pool.push_back(r.a);
+      pool.push_back(r.b);
+    }
+    pending.clear();
+  }
+};
+inline Profiler& profiler() {
+  static Profiler p;
+  return p;
+}
+struct ProfScope {
+  int stage;
+  hipStream_t st;
+  hipEvent_t a = nullptr;
+  ProfScope(int s, hipStream_t stream) : stage(s), st(stream) {
+    Profiler& p = profiler();
+    if (!(p.mask & (1u << s))) return;
+    std::lock_guard<std::mutex> g(p.mu);
+    a = p.get();
+    if (a) (void)hipEventRecord(a, st);
+  }
+  ~ProfScope() {
+    if (!a) return;
+    Profiler& p = profiler();
+    std::lock_guard<std::mutex> g(p.mu);
+    hipEvent_t b = p.get();
+    if (!b) return;
+    (void)hipEventRecord(b, st);
+    p.pending.push_back({stage, a, b});
+  }
+};
+
+inline int hip_status() { return hipGetLastError() == hipSuccess ? SD_OK : SD_ERR_HIP; }
+
+inline dim3 grid1(long long n, int block) { return dim3((unsigned)((n + block - 1) / block)); }
+
+inline void fill(float* p, long long n, float v, hipStream_t st) {
+  if (n > 0) hipLaunchKernelGGL(fill_kernel, grid1(n, 256), dim3(256), 0, st, p, n, v);
+}
+
+// ----------------------------------------------------------- dispatch -----
+template <typename T>
+void ts_xtw(const T* X, long long sx, int ldx, int s_pad, int l_pad, const float* Wt, long long sw, int ldw,
+            int rp, float* Pt, long long sp, int ldp, int batch, hipStream_t st) {
+  ProfScope ps(SD_STAGE_SKETCH, st);
+  const dim3 g((l_pad / 128) * batch), b(256);
+  switch (cdiv(rp, 16)) {
+    case 1: hipLaunchKernelGGL((ts_xtw_kernel<T, 1>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 2: hipLaunchKernelGGL((ts_xtw_kernel<T, 2>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 3: hipLaunchKernelGGL((ts_xtw_kernel<T, 3>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    default: hipLaunchKernelGGL((ts_xtw_kernel<T, 4>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+  }
+}
+
+template <typename T>
+void ts_xw(const T* X, long long sx, int ldx, int s_pad, int l_pad, const float* Wt, long long sw, int ldw,
+           int rp, float* Pt, long long sp, int ldp, int batch, hipStream_t st) {
+  ProfScope ps(SD_STAGE_SKETCH, st);
+  const dim3 g((s_pad / 16) * batch), b(256);
+  switch (cdiv(rp, 16)) {
+    case 1: hipLaunchKernelGGL((ts_xw_kernel<T, 1>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 2: hipLaunchKernelGGL((ts_xw_kernel<T, 2>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 3: hipLaunchKernelGGL((ts_xw_kernel<T, 3>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    default: hipLaunchKernelGGL((ts_xw_kernel<T, 4>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+  }
+}
+
+inline void cholqr(float* Pt, long long sp, int ld, int c, int len_pad, int batch, int* status, hipStream_t st) {
+  ProfScope ps(SD_STAGE_CHOLQR, st);
+  const dim3 g(batch), b(SM_THREADS);
+  if (c <= 16) hipLaunchKernelGGL((cholqr_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, status);
+  else if (c <= 32) hipLaunchKernelGGL((cholqr_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, status);
+  else hipLaunchKernelGGL((cholqr_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, status);
+}
+
+inline void rotate(const float* in, long long si, int ldi, const float* E, long long se, const float* scale,
+                   long long ssc, float* out, long long so, int ldo, int kin, int kout, int len, int batch,
+                   hipStream_t st) {
+  ProfScope ps(SD_STAGE_SMALL, st);
+  const dim3 g((len / 128) * batch), b(128);
+  if (kin <= 16) hipLaunchKernelGGL((rotate_kernel<16>), g, b, 0, st, in, si, ldi, E, se, scale, ssc, out, so, ldo, kin, kout, len, batch);
+  else if (kin <= 32) hipLaunchKernelGGL((rotate_kernel<32>), g, b, 0, st, in, si, ldi, E, se, scale, ssc, out, so, ldo, kin, kout, len, batch);
+  else hipLaunchKernelGGL((rotate_kernel<64>), g, b, 0, st, in, si, ldi, E, se, scale, ssc, out, so, ldo, kin, kout, len, batch);
+}
+
+template <typename TX, typename TO>
+void lowrank(const LowRankArgs& a, hipStream_t st) {
+  ProfScope ps(SD_STAGE_LOWRANK, st);
+  const dim3 g((a.rows_pad / 128) * (a.cols_pad / 128) * a.batch), b(256);
+  if (a.kmax <= 16) hipLaunchKernelGGL((lowrank_kernel<TX, TO, 16>), g, b, 0, st, a);
+  else if (a.kmax <= 32) hipLaunchKernelGGL((lowrank_kernel<TX, TO, 32>), g, b, 0, st, a);
+  else hipLaunchKernelGGL((lowrank_kernel<TX, TO, 64>), g, b, 0, st, a);
+}
+
+}  // namespace sd

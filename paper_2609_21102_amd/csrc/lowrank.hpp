@@ -1,0 +1,226 @@
+// Element-wise passes with a low-rank term, streamed once through HBM:
+//
+//   out[i][n] = alpha * x[i][n] + sum_{j < kk} L[j][i] c[j] Rr[j][n]
+//
+// over a padded rows x cols domain (multiples of 128). Used for the residual
+// norm of the deflated polar factor (sum of out^2 per tile, no output), the
+// padded start X0 of Alg. 1 and Alg. 2 and the PSD residual R of Alg. 2.
+// Per-matrix alpha, c and kk are read from device memory so that gate
+// decisions never leave the GPU.
+#pragma once
+
+#include "common.hpp"
+
+namespace sd {
+
+struct LowRankArgs {
+  const void* x;
+  long long sx;
+  int ldx;
+  const float* L;     // [b][j][ld_l]
+  long long sl;
+  int ldl;
+  const float* Rr;    // [b][j][ld_r]
+  long long sr;
+  int ldr;
+  const float* coef;  // [b][kmax]
+  const int* kk;      // [b] or null (then kconst)
+  int kconst;
+  const float* alpha; // [b] or null (then 1)
+  void* out;          // null: no output
+  long long so;
+  int ldo;
+  float* sumsq;       // [b][tiles] or null
+  int rows_pad, cols_pad, kmax, batch;
+};
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, float v[8]);
+template <>
+__device__ __forceinline__ void load8<bf16_t>(const bf16_t* p, float v[8]) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+template <>
+__device__ __forceinline__ void load8<float>(const float* p, float v[8]) {
+  const float4 a = *reinterpret_cast<const float4*>(p);
+  const float4 b = *reinterpret_cast<const float4*>(p + 4);
+  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+}
+template <typename T>
+__device__ __forceinline__ void store8(T* p, const float v[8]);
+template <>
+__device__ __forceinline__ void store8<bf16_t>(bf16_t* p, const float v[8]) {
+  *reinterpret_cast<uint4*>(p) = make_uint4(pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]),
+                                            pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7]));
+}
+template <>
+__device__ __forceinline__ void store8<float>(float* p, const float v[8]) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
+}
+
+// 128 x 128 tile per work-group; thread t owns rows 8 (t / 16) .. +7 and
+// columns 8 (t % 16) .. +7.
+template <typename TX, typename TO, int KM>
+__global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
+  __shared__ __attribute__((aligned(16))) float ls[KM][128];
+  __shared__ __attribute__((aligned(16))) float rs[KM][128];
+  __shared__ float red[4];
+  const int tr = a.rows_pad / 128, tc = a.cols_pad / 128, per = tr * tc;
+  const int lid = xcd_remap(blockIdx.x, per * a.batch);
+  const int b = lid / per, t = lid - b * per;
+  const int i0 = (t / tc) * 128, n0 = (t % tc) * 128;
+  const int kk = a.kk ? a.kk[b] : a.kconst;
+  const float alpha = a.alpha ? a.alpha[b] : 1.f;
+  const int tid = threadIdx.x;
+  for (int e = tid; e < kk * 128; e += 256) {
+    const int j = e >> 7, x = e & 127;
+    ls[j][x] = a.L[b * a.sl + (long long)j * a.ldl + i0 + x] * a.coef[b * a.kmax + j];
+    rs[j][x] = a.Rr[b * a.sr + (long long)j * a.ldr + n0 + x];
+  }
+  __syncthreads();
+  const int rg = tid >> 4, cg = tid & 15;
+  float acc[8][8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[r][c] = 0.f;
+  for (int j = 0; j < kk; ++j) {
+    const float4 l0 = *reinterpret_cast<const float4*>(&ls[j][rg * 8]);
+    const float4 l1 = *reinterpret_cast<const float4*>(&ls[j][rg * 8 + 4]);
+    const float4 r0 = *reinterpret_cast<const float4*>(&rs[j][cg * 8]);
+    const float4 r1 = *reinterpret_cast<const float4*>(&rs[j][cg * 8 + 4]);
+    const float lv[8] = {l0.x, l0.y, l0.z, l0.w, l1.x, l1.y, l1.z, l1.w};
+    const float rv[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) acc[r][c] = fmaf(lv[r], rv[c], acc[r][c]);
+  }
+  const TX* xb = reinterpret_cast<const TX*>(a.x) + b * a.sx;
+  TO* ob = a.out ? reinterpret_cast<TO*>(a.out) + b * a.so : nullptr;
+  float ss = 0.f;
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int i = i0 + rg * 8 + r;
+    float v[8];
+    load8<TX>(xb + (long long)i * a.ldx + n0 + cg * 8, v);
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      v[c] = fmaf(alpha, v[c], acc[r][c]);
+      ss = fmaf(v[c], v[c], ss);
+    }
+    if (ob) store8<TO>(ob + (long long)i * a.ldo + n0 + cg * 8, v);
+  }
+  if (a.sumsq) {
+    ss = block_sum(ss, red);
+    if (tid == 0) a.sumsq[(long long)b * per + t] = ss;
+  }
+}
+
+// nu = sqrt(sum of the residual tiles) (in tile order, float64); alpha = 1/nu
+// (0 for nu = 0) and the start coefficients c_j = -(s_j / nu - 1 / gamma) of
+//   X0 = alpha X + sum_j L_j c_j R_j^T  =  R / nu + gamma^-1 L R^T.
+static __global__ void muon_finalize_kernel(const float* sumsq, int tiles, const float* sv, const int* keff,
+                                     int kmax, float inv_gamma, float* alpha, float* coef_b, float* nu_dev,
+                                     float* nu_user, int batch) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= batch) return;
+  double acc = 0.0;
+  for (int t = 0; t < tiles; ++t) acc += (double)sumsq[(long long)b * tiles + t];
+  const double nu = sqrt(acc);
+  const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
+  alpha[b] = (float)inv;
+  nu_dev[b] = (float)nu;
+  if (nu_user) nu_user[b] = (float)nu;
+  const int ke = keff ? keff[b] : 0;
+  for (int j = 0; j < kmax; ++j)
+    coef_b[b * kmax + j] = j < ke ? (float)(-((double)sv[b * kmax + j] * inv - (double)inv_gamma)) : 0.f;
+}
+
+static __global__ void fill_kernel(float* p, long long n, float v) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+static __global__ void fill_int_kernel(int* p, long long n, int v) {
+  const long long i = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+// Padded canonical iterate -> caller layout (rows x cols, or its transpose).
+template <typename TX, typename TO>
+__global__ void store_out_kernel(const TX* x, long long sx, int ldx, TO* out, long long so, int rows, int cols,
+                                 int transpose, int batch) {
+  const long long per = (long long)rows * cols;
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= per * batch) return;
+  const int b = (int)(gid / per);
+  const long long r = gid - (long long)b * per;
+  if (!transpose) {
+    const int i = (int)(r / cols), n = (int)(r - (long long)i * cols);
+    out[b * so + r] = Cvt<TO>::from_f(Cvt<TX>::to_f(x[b * sx + (long long)i * ldx + n]));
+  } else {
+    // out is cols x rows: out[n][i] = x[i][n]
+    const int n = (int)(r / rows), i = (int)(r - (long long)n * rows);
+    out[b * so + r] = Cvt<TO>::from_f(Cvt<TX>::to_f(x[b * sx + (long long)i * ldx + n]));
+  }
+}
+
+// Panel (c x ld, transposed storage) -> caller matrix (len x c, row-major).
+static __global__ void panel_to_rows_kernel(const float* pt, int ld, int c, int len, float* out) {
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= (long long)len * c) return;
+  const int x = (int)(gid / c), j = (int)(gid - (long long)x * c);
+  out[gid] = pt[(long long)j * ld + x];
+}
+
+// Caller matrix (len x c, row-major) -> panel (c x ld), zero beyond len.
+static __global__ void rows_to_panel_kernel(const float* in, int c, int len, int ld, float* pt) {
+  const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (gid >= (long long)c * ld) return;
+  const int j = (int)(gid / ld), x = (int)(gid - (long long)j * ld);
+  pt[gid] = x < len ? in[(long long)x * c + j] : 0.f;
+}
+
+// PSD output (Alg. 2 restore and symmetrization):
+//   P[i][j] = R[i][j] / 2 + (C[i][j] + C[j][i]) / 4 + sum_{p < kk} U[p][i] cp[p] U[p][j]
+// with C = R g(X0). 64 x 64 tiles; the transposed tile of C goes through LDS.
+template <int KM>
+__global__ __launch_bounds__(256) void psd_out_kernel(const float* R, const float* C, int ld, const float* Ut,
+                                                      int ldu, const float* coef_p, const int* kk_dev, int n,
+                                                      int n_pad, float* out) {
+  __shared__ float ct[64][65];
+  __shared__ float ui[KM][64];
+  __shared__ float uj[KM][64];
+  const int tiles = n_pad / 64;
+  const int i0 = (blockIdx.x / tiles) * 64, j0 = (blockIdx.x % tiles) * 64;
+  const int tid = threadIdx.x;
+  const int kk = kk_dev ? *kk_dev : 0;
+  for (int e = tid; e < 64 * 64; e += 256) {
+    const int r = e >> 6, c = e & 63;
+    ct[c][r] = C[(long long)(j0 + r) * ld + i0 + c];   // ct[x][y] = C[j0 + y][i0 + x]
+  }
+  for (int e = tid; e < kk * 64; e += 256) {
+    const int p = e >> 6, x = e & 63;
+    ui[p][x] = Ut[(long long)p * ldu + i0 + x] * coef_p[p];
+    uj[p][x] = Ut[(long long)p * ldu + j0 + x];
+  }
+  __syncthreads();
+  const int tx = tid & 63, ty = tid >> 6;
+  for (int r = ty; r < 64; r += 4) {
+    const int i = i0 + r, j = j0 + tx;
+    float h = 0.f;
+    for (int p = 0; p < kk; ++p) h = fmaf(ui[p][r], uj[p][tx], h);
+    const float v = 0.5f * R[(long long)i * ld + j] + 0.25f * (C[(long long)i * ld + j] + ct[r][tx]) + h;
+    if (i < n && j < n) out[(long long)i * n + j] = v;
+  }
+}
+
+}  // namespace sd

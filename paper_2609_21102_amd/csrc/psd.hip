@@ -1,0 +1,508 @@
+// Deflated PSD projection (Alg. 2) with the Lanczos scale of App. E.1: host
+// orchestration, the Lanczos kernels and the C entry points.
+//
+//   (J - 1) x [Zt = Z V, CholQR]  ->  Zt = Z V  ->  Rayleigh-Ritz (float64)
+//   R = Z - U_I diag(lam_I) U_I^T            (one streaming pass)
+//   theta = Lanczos upper estimate of ||R||_2 (GEMVs with R, float64 recurrences)
+//   X0 = R / theta + gamma^-1 U_I sign(lam_I) U_I^T
+//   g = L steps of X <- a X + (b A + c A^2) X, A = X X (symmetric tiles only)
+//   C = R g  ->  P = R / 2 + (C + C^T) / 4 + U_I max(lam_I, 0) U_I^T
+//   Qwarm <- CholQR(Zt)
+// With nothing deflated the same kernels run with R = Z, which is the
+// baseline projection of eq:baseline_projection.
+#include "host.hpp"
+
+namespace sd {
+
+constexpr int LZ_MAX = 64;   // largest Lanczos step count
+
+// y[i] = sum_j A[i][j] x[j]; one wave per row, four rows per work-group.
+__global__ __launch_bounds__(256) void gemv_kernel(const float* __restrict__ A, int ld, int n_pad,
+                                                   const float* __restrict__ x, float* __restrict__ y) {
+  const int wave = threadIdx.x / WAVE, lane = threadIdx.x & (WAVE - 1);
+  const int row = blockIdx.x * 4 + wave;
+  if (row >= n_pad) return;
+  const float* a = A + (long long)row * ld;
+  float acc = 0.f;
+  for (int c = lane * 4; c < n_pad; c += 4 * WAVE) {
+    const float4 av = *reinterpret_cast<const float4*>(a + c);
+    const float4 xv = *reinterpret_cast<const float4*>(x + c);
+    acc = fmaf(av.x, xv.x, acc);
+    acc = fmaf(av.y, xv.y, acc);
+    acc = fmaf(av.z, xv.z, acc);
+    acc = fmaf(av.w, xv.w, acc);
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) y[row] = acc;
+}
+
+struct LanczosState {
+  double alpha[LZ_MAX];
+  double beta[LZ_MAX];
+  int active;      // number of Lanczos vectors that may be used
+  int steps;       // alpha entries computed
+  double rho;
+};
+
+// q_0 = g / ||g|| with g the Philox Gaussians of stream 2 (n entries, zero
+// padding). One work-group of 1024 threads.
+__global__ __launch_bounds__(1024) void lanczos_init_kernel(float* Q, int n, int n_pad, int m, uint64_t seed,
+                                                            LanczosState* st) {
+  __shared__ double red[16];
+  const int tid = threadIdx.x;
+  double ss = 0.0;
+  for (int c = tid; 4 * c < n_pad; c += 1024) {
+    float z[4];
+    Philox::normals(z, (uint32_t)c, 0u, 2u, seed);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      const int i = 4 * c + t;
+      const float v = i < n ? z[t] : 0.f;
+      Q[i] = v;
+      ss += (double)v * v;
+    }
+  }
+  ss = block_sum(ss, red);
+  const float inv = (float)(1.0 / sqrt(ss));
+  for (int i = tid; i < n_pad; i += 1024) Q[i] = (float)((double)Q[i] / sqrt(ss));
+  (void)inv;
+  if (tid == 0) {
+    st->active = m;
+    st->steps = 0;
+    st->rho = 0.0;
+  }
+}
+
+// One Lanczos step on B = R^2 with w = B q_j already computed:
+//   alpha_j = q_j . w;  w -= alpha_j q_j + beta_{j-1} q_{j-1};
+//   two classical Gram-Schmidt passes against q_0..q_j;
+//   beta_j = ||w||; q_{j+1} = w / beta_j (a zero beta ends the run).
+__global__ __launch_bounds__(1024) void lanczos_step_kernel(float* Q, int n_pad, float* w, int j, int m,
+                                                            LanczosState* st) {
+  __shared__ double red[16];
+  __shared__ double h[LZ_MAX];
+  const int tid = threadIdx.x;
+  if (j >= st->active) return;
+  const float* qj = Q + (long long)j * n_pad;
+  double acc = 0.0;
+  for (int i = tid; i < n_pad; i += 1024) acc += (double)qj[i] * w[i];
+  const double a = block_sum(acc, red);
+  const double bprev = j > 0 ? st->beta[j - 1] : 0.0;
+  const float* qp = j > 0 ? Q + (long long)(j - 1) * n_pad : qj;
+  for (int i = tid; i < n_pad; i += 1024)
+    w[i] = (float)((double)w[i] - a * qj[i] - (j > 0 ? bprev * qp[i] : 0.0));
+  __syncthreads();
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int v = 0; v <= j; ++v) {
+      const float* qv = Q + (long long)v * n_pad;
+      double d = 0.0;
+      for (int i = tid; i < n_pad; i += 1024) d += (double)qv[i] * w[i];
+      d = block_sum(d, red);
+      if (tid == 0) h[v] = d;
+    }
+    __syncthreads();
+    for (int i = tid; i < n_pad; i += 1024) {
+      double t = w[i];
+      for (int v = 0; v <= j; ++v) t -= h[v] * Q[(long long)v * n_pad + i];
+      w[i] = (float)t;
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    st->alpha[j] = a;
+    st->steps = j + 1;
+  }
+  if (j == m - 1) return;
+  double nn = 0.0;
+  for (int i = tid; i < n_pad; i += 1024) nn += (double)w[i] * w[i];
+  const double beta = sqrt(block_sum(nn, red));
+  if (beta == 0.0) {
+    if (tid == 0) st->active = j + 1;
+    return;
+  }
+  float* qn = Q + (long long)(j + 1) * n_pad;
+  for (int i = tid; i < n_pad; i += 1024) qn[i] = (float)((double)w[i] / beta);
+  if (tid == 0) st->beta[j] = beta;
+}
+
+// Largest Ritz pair of the tridiagonal matrix: rho and v = Q y.
+__global__ __launch_bounds__(SM_THREADS) void lanczos_ritz_kernel(const float* Q, int n_pad, float* v,
+                                                                  LanczosState* st) {
+  __shared__ SmallLds s;
+  const int tid = threadIdx.x;
+  const int kk = st->steps;
+  for (int e = tid; e < kk * kk; e += SM_THREADS) {
+    const int i = e / kk, j = e - i * kk;
+    double val = 0.0;
+    if (i == j) val = st->alpha[i];
+    else if (j == i + 1) val = st->beta[i];
+    else if (i == j + 1) val = st->beta[j];
+    s.h[i][j] = val;
+  }
+  __syncthreads();
+  jacobi_eig(s, kk);
+  if (tid == 0) {
+    int best = 0;
+    for (int i = 1; i < kk; ++i)
+      if (s.h[i][i] > s.h[best][best]) best = i;
+    s.perm[0] = best;
+    st->rho = s.h[best][best];
+  }
+  __syncthreads();
+  const int best = s.perm[0];
+  for (int i = tid; i < n_pad; i += SM_THREADS) {
+    double t = 0.0;
+    for (int a = 0; a < kk; ++a) t += s.e[a][best] * (double)Q[(long long)a * n_pad + i];
+    v[i] = (float)t;
+  }
+}
+
+// theta = sqrt(rho + ||B v - rho v||); alpha_x0 = 1 / theta (0 for theta = 0).
+__global__ __launch_bounds__(1024) void lanczos_theta_kernel(const float* bv, const float* v, int n_pad,
+                                                             const LanczosState* st, float* theta_dev,
+                                                             float* alpha_x0, float* theta_user) {
+  __shared__ double red[16];
+  const int tid = threadIdx.x;
+  const double rho = st->rho;
+  double acc = 0.0;
+  for (int i = tid; i < n_pad; i += 1024) {
+    const double d = (double)bv[i] - rho * v[i];
+    acc += d * d;
+  }
+  const double res = sqrt(block_sum(acc, red));
+  if (tid == 0) {
+    const double t = rho + res;
+    const double th = t > 0.0 ? sqrt(t) : 0.0;
+    *theta_dev = (float)th;
+    *alpha_x0 = th > 0.0 ? (float)(1.0 / th) : 0.f;
+    if (theta_user) *theta_user = (float)th;
+  }
+}
+
+struct PsdPlan {
+  int n, k, steps, n_pad, K, lz;
+  bool copy_in, quintic;
+  float *zp, *r, *xa, *xb, *s32, *bm, *c;
+  float *vt, *zt, *E, *lam, *ut, *coefR, *coefX, *coefP;
+  int* ndef;
+  float *qlan, *w, *t, *v, *theta, *alpha_x0;
+  LanczosState* lst;
+};
+
+static void plan_psd(PsdPlan& p, Arena& ar) {
+  const size_t nn = (size_t)p.n_pad * p.n_pad;
+  p.zp = p.copy_in ? ar.take<float>(nn) : nullptr;
+  p.r = ar.take<float>(nn);
+  p.xa = ar.take<float>(nn);
+  p.xb = ar.take<float>(nn);
+  p.s32 = p.quintic ? ar.take<float>(nn) : nullptr;
+  p.bm = ar.take<float>(nn);
+  p.c = p.bm;   // the restore product reuses B's buffer after the filter
+  const int kq = p.K > 0 ? p.K : 1;
+  const int kr = round_up(kq, 32);
+  p.vt = ar.take<float>((size_t)kr * p.n_pad);
+  p.zt = ar.take<float>((size_t)kr * p.n_pad);
+  p.E = ar.take<float>((size_t)kq * kq);
+  p.lam = ar.take<float>(kq);
+  p.ut = ar.take<float>((size_t)kq * p.n_pad);
+  p.coefR = ar.take<float>(kq);
+  p.coefX = ar.take<float>(kq);
+  p.coefP = ar.take<float>(kq);
+  p.ndef = ar.take<int>(1);
+  p.qlan = ar.take<float>((size_t)(p.lz + 1) * p.n_pad);
+  p.w = ar.take<float>(p.n_pad);
+  p.t = ar.take<float>(p.n_pad);
+  p.v = ar.take<float>(p.n_pad);
+  p.theta = ar.take<float>(1);
+  p.alpha_x0 = ar.take<float>(1);
+  p.lst = ar.take<LanczosState>(1);
+}
+
+static int validate_psd(int n, int k, int steps, const float* X, const float* Qwarm, const float* out,
+                        const sd_psd_opts& o) {
+  if (n < 1 || k < 0 || k >= n || steps < 0 || steps > 1000 || !X || !out) return SD_ERR_INVALID_ARG;
+  if (k > SM_MAX) return SD_ERR_UNSUPPORTED;
+  if (k > 0 && !Qwarm) return SD_ERR_INVALID_ARG;
+  if (o.subspace_iters < 1 || o.subspace_iters > 100) return SD_ERR_INVALID_ARG;
+  if (o.lanczos_steps < 1 || o.lanczos_steps > LZ_MAX) return SD_ERR_INVALID_ARG;
+  if (!(o.gamma > 0.f) || !(o.tau >= 0.f) || !(o.tau < 1.f)) return SD_ERR_INVALID_ARG;
+  if (o.tau > 0.f && (o.window < 1 || o.window > k)) return SD_ERR_INVALID_ARG;
+  if (o.poly_degree != 3 && o.poly_degree != 5) return SD_ERR_INVALID_ARG;
+  if ((long long)n * n > (1ll << 34)) return SD_ERR_UNSUPPORTED;
+  if (k > 0) {
+    const char* q0 = reinterpret_cast<const char*>(Qwarm);
+    const char* q1 = q0 + (size_t)n * k * sizeof(float);
+    const char* x0 = reinterpret_cast<const char*>(X);
+    const char* x1 = x0 + (size_t)n * n * sizeof(float);
+    const char* o0 = reinterpret_cast<const char*>(out);
+    const char* o1 = o0 + (size_t)n * n * sizeof(float);
+    if ((q0 < x1 && x0 < q1) || (q0 < o1 && o0 < q1)) return SD_ERR_INVALID_ARG;
+  }
+  return SD_OK;
+}
+
+static void make_psd_plan(PsdPlan& p, int n, int k, int steps, const float* X, const sd_psd_opts& o) {
+  p.n = n;
+  p.k = k;
+  p.K = k;
+  p.steps = steps;
+  p.n_pad = round_up(n, 128);
+  p.lz = o.lanczos_steps < n ? o.lanczos_steps : n;
+  p.quintic = o.poly_degree == 5;
+  const bool aligned = X && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
+  p.copy_in = p.n != p.n_pad || !aligned;
+}
+
+static void lanczos(const PsdPlan& p, const float* R, uint64_t seed, float* theta_user, hipStream_t st) {
+  ProfScope ps(SD_STAGE_LANCZOS, st);
+  const int np = p.n_pad;
+  fill(p.qlan, (long long)(p.lz + 1) * np, 0.f, st);
+  hipLaunchKernelGGL(lanczos_init_kernel, dim3(1), dim3(1024), 0, st, p.qlan, p.n, np, p.lz, seed, p.lst);
+  const dim3 gg(np / 4), gb(256);
+  for (int j = 0; j < p.lz; ++j) {
+    hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.qlan + (long long)j * np, p.t);
+    hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.t, p.w);
+    hipLaunchKernelGGL(lanczos_step_kernel, dim3(1), dim3(1024), 0, st, p.qlan, np, p.w, j, p.lz, p.lst);
+  }
+  hipLaunchKernelGGL(lanczos_ritz_kernel, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst);
+  hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.v, p.t);
+  hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.t, p.w);
+  hipLaunchKernelGGL(lanczos_theta_kernel, dim3(1), dim3(1024), 0, st, p.w, p.v, np, p.lst, p.theta, p.alpha_x0,
+                     theta_user);
+}
+
+static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, const sd_psd_opts& o,
+                   hipStream_t st) {
+  const int np = p.n_pad, n = p.n, K = p.K;
+  const long long nn = (long long)np * np;
+  const float* z;
+  if (p.copy_in) {
+    const int blocks = (np / 32) * (np / 32);
+    hipLaunchKernelGGL((canon_copy_kernel<float>), dim3(blocks), dim3(256), 0, st, p.zp, nn, np, np, np, X, nn, n,
+                       n, 0, 1);
+    z = p.zp;
+  } else {
+    z = X;
+  }
+  LowRankArgs la{};
+  la.rows_pad = np;
+  la.cols_pad = np;
+  la.batch = 1;
+  la.ldx = np;
+  la.ldo = np;
+  la.ldl = la.ldr = np;
+  if (K > 0) {
+    hipLaunchKernelGGL(rows_to_panel_kernel, grid1((long long)K * np, 256), dim3(256), 0, st, Qwarm, K, n, np, p.vt);
+    float* vt = p.vt;
+    float* zt = p.zt;
+    for (int j = 0; j + 1 < o.subspace_iters; ++j) {
+      ts_xw<float>(z, nn, np, np, np, vt, 0, np, K, zt, 0, np, 1, st);
+      cholqr(zt, 0, np, K, np, 1, o.status_dev, st);
+      float* tmp = vt;
+      vt = zt;
+      zt = tmp;
+    }
+    ts_xw<float>(z, nn, np, np, np, vt, 0, np, K, zt, 0, np, 1, st);   // Zt = Z V
+    {
+      ProfScope ps(SD_STAGE_SMALL, st);
+      hipLaunchKernelGGL(ritz_kernel, dim3(1), dim3(SM_THREADS), 0, st, vt, zt, np, np, K, o.tau, o.window, o.gamma,
+                       p.E, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out, o.n_deflated_out,
+                         o.n_positive_out);
+    }
+    rotate(vt, 0, np, p.E, 0, nullptr, 0, p.ut, 0, np, K, K, np, 1, st);
+    // R = Z - U diag(lam) U^T
+    la.x = z;
+    la.L = p.ut;
+    la.Rr = p.ut;
+    la.coef = p.coefR;
+    la.kk = p.ndef;
+    la.kmax = K;
+    la.alpha = nullptr;
+    la.out = p.r;
+    lowrank<float, float>(la, st);
+    // next basis: CholQR(Zt), written back after the filter
+    cholqr(zt, 0, np, K, np, 1, o.status_dev, st);
+    hipLaunchKernelGGL(panel_to_rows_kernel, grid1((long long)n * K, 256), dim3(256), 0, st, zt, np, K, n, Qwarm);
+  } else {
+    la.x = z;
+    la.L = la.Rr = p.ut;
+    la.coef = p.coefR;
+    la.kk = nullptr;
+    la.kconst = 0;
+    la.kmax = 1;
+    la.out = p.r;
+    lowrank<float, float>(la, st);
+    if (o.n_deflated_out) hipLaunchKernelGGL(fill_int_kernel, dim3(1), dim3(64), 0, st, o.n_deflated_out, 1ll, 0);
+    if (o.n_positive_out) hipLaunchKernelGGL(fill_int_kernel, dim3(1), dim3(64), 0, st, o.n_positive_out, 1ll, 0);
+  }
+  lanczos(p, p.r, o.seed, o.theta_out, st);
+  // X0 = R / theta + gamma^-1 U sign(lam) U^T
+  la.x = p.r;
+  la.coef = p.coefX;
+  la.alpha = p.alpha_x0;
+  la.out = p.xa;
+  lowrank<float, float>(la, st);
+
+  float* cur = p.xa;
+  float* nxt = p.xb;
+  const int nc = (o.poly_degree + 1) / 2;
+  for (int t = 0; t < p.steps; ++t) {
+    const float a = o.poly ? o.poly[nc * t] : 1.5f;
+    const float b = o.poly ? o.poly[nc * t + 1] : -0.5f;
+    const float c = (o.poly && nc == 3) ? o.poly[nc * t + 2] : 0.f;
+    GemmShape g{np, np, np, np, np, nn, nn, 1};
+    EpiGram eg{};
+    eg.stride = nn;
+    eg.ld = np;
+    if (c != 0.f) {
+      eg.out32 = p.s32 ? p.s32 : p.bm;
+      eg.scale32 = 1.f;
+    } else {
+      eg.out32 = p.bm;
+      eg.scale32 = b;
+    }
+    {
+      ProfScope ps(SD_STAGE_NS_GRAM, st);
+      launch_gemm<float, false, true>(cur, cur, g, eg, st);
+    }
+    if (c != 0.f) {
+      ProfScope ps(SD_STAGE_NS_POLY, st);
+      EpiPoly<float> ep{p.s32, p.bm, b, c, nn, np};
+      launch_gemm<float, false, true>(p.s32, p.s32, g, ep, st);
+    }
+    EpiUpdate<float, float> eu{};
+    eu.x = cur;
+    eu.xstride = nn;
+    eu.ldx = np;
+    eu.ac = a;
+    eu.out = nxt;
+    eu.ostride = nn;
+    eu.ldo = np;
+    {
+      ProfScope ps(SD_STAGE_NS_UPDATE, st);
+      launch_gemm<float, false, true>(p.bm, cur, g, eu, st);
+    }
+    float* tmp = cur;
+    cur = nxt;
+    nxt = tmp;
+  }
+  // C = R g (g symmetric, so the NT form reads rows of g)
+  ProfScope ps(SD_STAGE_RESTORE, st);
+  GemmShape g{np, np, np, np, np, nn, nn, 1};
+  EpiStore es{p.c, nn, np};
+  launch_gemm<float, false, false>(p.r, cur, g, es, st);
+  const int tiles = (np / 64) * (np / 64);
+  const float* ut = K > 0 ? p.ut : nullptr;
+  const int* kk = K > 0 ? p.ndef : nullptr;
+  if (K <= 16)
+    hipLaunchKernelGGL((psd_out_kernel<16>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
+  else if (K <= 32)
+    hipLaunchKernelGGL((psd_out_kernel<32>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
+  else
+    hipLaunchKernelGGL((psd_out_kernel<64>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
+  return hip_status();
+}
+
+}  // namespace sd
+
+using namespace sd;
+
+extern "C" {
+
+void sd_psd_opts_default(sd_psd_opts* o) {
+  if (!o) return;
+  *o = sd_psd_opts{};
+  o->subspace_iters = 1;
+  o->lanczos_steps = 20;
+  o->gamma = 1.1f;
+  o->tau = 0.f;
+  o->window = 1;
+  o->poly_degree = 3;
+  o->poly = nullptr;
+  o->seed = 0;
+}
+
+size_t sd_psd_workspace_bytes(int n, int k, const sd_psd_opts* opts) {
+  sd_psd_opts o;
+  sd_psd_opts_default(&o);
+  if (opts) o = *opts;
+  if (n < 1 || k < 0 || k >= n || k > SM_MAX) return 0;
+  PsdPlan p{};
+  make_psd_plan(p, n, k, 0, nullptr, o);
+  Arena ar;
+  plan_psd(p, ar);
+  return ar.off + 256;
+}
+
+int sd_psd_project_deflated_ex(int n, int k, int steps, const float* X, float* Qwarm, float* out,
+                               const sd_psd_opts* opts, hipStream_t stream) {
+  sd_psd_opts o;
+  sd_psd_opts_default(&o);
+  if (opts) o = *opts;
+  int rc = validate_psd(n, k, steps, X, Qwarm, out, o);
+  if (rc != SD_OK) return rc;
+  PsdPlan p{};
+  make_psd_plan(p, n, k, steps, X, o);
+  Arena sizing;
+  plan_psd(p, sizing);
+  Scratch scratch;
+  rc = scratch.acquire(o.workspace, o.workspace_bytes, sizing.off + 256, stream);
+  if (rc != SD_OK) return rc;
+  Arena ar;
+  ar.base = reinterpret_cast<char*>(scratch.ptr);
+  plan_psd(p, ar);
+  rc = run_psd(p, X, Qwarm, out, o, stream);
+  scratch.release();
+  return rc;
+}
+
+int sd_psd_project(int n, int steps, const float* X, float* out, hipStream_t stream) {
+  return sd_psd_project_deflated_ex(n, 0, steps, X, nullptr, out, nullptr, stream);
+}
+
+int sd_psd_project_deflated(int n, int k, int steps, const float* X, float* Qwarm, float* out,
+                            hipStream_t stream) {
+  return sd_psd_project_deflated_ex(n, k, steps, X, Qwarm, out, nullptr, stream);
+}
+
+const char* sd_status_string(int status) {
+  switch (status) {
+    case SD_OK: return "ok";
+    case SD_ERR_INVALID_ARG: return "invalid argument";
+    case SD_ERR_UNSUPPORTED: return "unsupported size or option";
+    case SD_ERR_HIP: return "HIP runtime error";
+    case SD_ERR_NUMERIC: return "numerical failure";
+    case SD_ERR_WORKSPACE: return "workspace too small";
+    default: return "unknown status";
+  }
+}
+
+int sd_version(void) { return 100; }
+
+void sd_profile_set(unsigned mask) {
+  Profiler& p = profiler();
+  std::lock_guard<std::mutex> g(p.mu);
+  p.mask = mask;
+}
+
+int sd_profile_read(int stage, double* total_ms, long long* launches) {
+  if (stage < 0 || stage >= SD_STAGE_COUNT) return SD_ERR_INVALID_ARG;
+  Profiler& p = profiler();
+  std::lock_guard<std::mutex> g(p.mu);
+  p.drain();
+  if (total_ms) *total_ms = p.total_ms[stage];
+  if (launches) *launches = p.launches[stage];
+  return SD_OK;
+}
+
+void sd_profile_reset(void) {
+  Profiler& p = profiler();
+  std::lock_guard<std::mutex> g(p.mu);
+  p.drain();
+  for (int i = 0; i < SD_STAGE_COUNT; ++i) {
+    p.total_ms[i] = 0.0;
+    p.launches[i] = 0;
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,231 @@
+"""GPU parity of the (deflated) polar factor against the CPU oracle.
+
+Tolerances (relative Frobenius error of the output): 1e-4 for the float32
+paths against the float64 oracle; 2e-2 for the bf16 paths against the
+oracle's bf16 contract mode. Deflation ranks must match exactly.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2609_21102_amd as sd
+import workloads
+from oracle import muon as omuon
+from oracle import rng as orng
+from tests.gpu_util import dev_tensor, host64, rel_fro, say
+
+pytestmark = pytest.mark.gpu
+
+F32_TOL = 1e-4
+BF16_TOL = 2e-2
+
+
+def run_case(case, k=None, steps=None, **kw):
+    k = case.k if k is None else k
+    steps = case.steps if steps is None else steps
+    x = dev_tensor(case.x, case.dtype)
+    out, info = sd.msign(x, k, steps, case.coeffs[:steps], oversample=case.oversample,
+                         power_iters=case.power_iters, gamma=case.gamma, info=True, **kw)
+    torch.cuda.synchronize()
+    return out, info
+
+
+def oracle_case(case, k=None, steps=None, idx=None, **kw):
+    k = case.k if k is None else k
+    steps = case.steps if steps is None else steps
+    x64 = case.x64 if idx is None else case.x64[idx]
+    mode = "bf16" if case.dtype == "bf16" else "exact"
+    sketches = None
+    if idx is not None and k > 0:
+        # the oracle numbers matrices from 0; pass the sketches of the sampled ones
+        s = min(case.x.shape[1:])
+        rp = min(s, k + case.oversample)
+        sketches = [orng.sketch(kw.get("seed", 0), int(b), s, rp) for b in idx]
+    return omuon.msign_deflated(x64, k, case.coeffs[:steps], oversample=case.oversample,
+                                power_iters=case.power_iters, gamma=case.gamma, mode=mode,
+                                sketches=sketches, tau=kw.get("tau", 0.0), seed=kw.get("seed", 0))
+
+
+def test_one_step_fp32():
+    case = workloads.small_muon(1, 64, 200, k=0)
+    say("one step fp32 64x200")
+    out, _ = run_case(case, k=0, steps=1)
+    want, _ = oracle_case(case, k=0, steps=1)
+    assert rel_fro(host64(out), want) < 1e-5
+
+
+SHAPES = [(1, 8, 17), (3, 17, 64), (2, 64, 17), (1, 130, 300), (2, 256, 129), (1, 300, 130), (2, 128, 384)]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("k", [0, 1, 4])
+def test_fp32_shapes(shape, k):
+    # Ragged, tall and wide shapes over several tiles. The bulk floor is 1e-2:
+    # on matrices this small a deeper bulk lets the filter amplify float32
+    # rounding of the deflated residual past 1e-4 (config 1 keeps 1e-3).
+    b, m, n = shape
+    if k >= min(m, n):
+        pytest.skip("k must be below min(m, n)")
+    case = workloads.small_muon(b, m, n, k=max(k, 1), power_iters=1, bulk=(1e-2, 1.0))
+    say(f"fp32 {shape} k={k}")
+    out, info = run_case(case, k=k)
+    want, oinfo = oracle_case(case, k=k)
+    err = rel_fro(host64(out), want)
+    say(f"  rel err {err:.3e}")
+    assert err < F32_TOL
+    assert info["k_eff"].cpu().tolist() == oinfo.k_eff
+
+
+def test_config1_fp32():
+    case = workloads.config1()
+    for k in (0, case.k):
+        say(f"config1 k={k}")
+        out, info = run_case(case, k=k)
+        want, oinfo = oracle_case(case, k=k)
+        err = rel_fro(host64(out), want)
+        say(f"  rel err {err:.3e}")
+        assert err < F32_TOL
+        assert info["k_eff"].cpu().tolist() == oinfo.k_eff
+        np.testing.assert_allclose(info["nu"].cpu().numpy(), oinfo.nu, rtol=1e-4)
+        if k:
+            np.testing.assert_allclose(info["s"].cpu().numpy()[0], oinfo.s[0], rtol=1e-5)
+
+
+@pytest.mark.parametrize("shape", [(2, 64, 200), (1, 96, 96), (3, 200, 70), (1, 128, 1000)],
+                         ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("k", [0, 4])
+def test_bf16_shapes(shape, k):
+    b, m, n = shape
+    case = workloads.small_muon(b, m, n, dtype="bf16", k=max(k, 1), bulk=(1e-3, 1.0))
+    say(f"bf16 {shape} k={k}")
+    out, info = run_case(case, k=k)
+    want, oinfo = oracle_case(case, k=k)
+    err = rel_fro(host64(out), want)
+    say(f"  rel err {err:.3e}")
+    assert err < BF16_TOL
+    assert info["k_eff"].cpu().tolist() == oinfo.k_eff
+
+
+def test_headline_768x3072_bf16_sampled():
+    # The benchmark's launch: 24 matrices of 768 x 3072 in one call; the oracle
+    # checks a sample of them.
+    case = workloads.config2("768x3072")
+    out, info = run_case(case)
+    got = host64(out)
+    for idx in ([0], [13], [23]):
+        want, oinfo = oracle_case(case, idx=idx)
+        err = rel_fro(got[idx[0]], want[0])
+        say(f"config2 768x3072 matrix {idx[0]}: rel err {err:.3e}")
+        assert err < BF16_TOL
+        assert int(info["k_eff"][idx[0]]) == oinfo.k_eff[0]
+
+
+@pytest.mark.parametrize("group", ["768x768", "768x2304"])
+def test_config2_other_groups_sampled(group):
+    case = workloads.config2(group)
+    out, info = run_case(case)
+    got = host64(out)
+    for idx in ([0], [11]):
+        want, _ = oracle_case(case, idx=idx)
+        err = rel_fro(got[idx[0]], want[0])
+        say(f"config2 {group} matrix {idx[0]}: rel err {err:.3e}")
+        assert err < BF16_TOL
+
+
+def test_config3_polar_express_table_sampled():
+    case = workloads.config3("768x3072", batch=4)
+    out, _ = run_case(case)
+    got = host64(out)
+    for idx in ([0], [3]):
+        want, _ = oracle_case(case, idx=idx)
+        err = rel_fro(got[idx[0]], want[0])
+        say(f"config3 matrix {idx[0]}: rel err {err:.3e}")
+        assert err < BF16_TOL
+
+
+def test_gate_off_equals_baseline_bitwise():
+    # Sec. 2.2: when the gate does not fire the method reduces exactly to Muon.
+    case = workloads.small_muon(2, 96, 160, k=3, spikes=[2.0, 1.9, 1.8])
+    x = dev_tensor(case.x, "f32")
+    base = sd.msign(x, 0, 5)
+    gated, info = sd.msign(x, 3, 5, tau=0.1, info=True)
+    torch.cuda.synchronize()
+    assert info["k_eff"].cpu().tolist() == [0, 0]
+    assert torch.equal(base, gated)
+
+
+def test_gate_fires_with_margin():
+    case = workloads.small_muon(2, 96, 160, k=6, spikes=[50, 30, 20, 1.0, 0.9, 0.8], bulk=(1e-3, 0.5))
+    x = dev_tensor(case.x, "f32")
+    out, info = sd.msign(x, 6, 5, tau=0.1, info=True)
+    torch.cuda.synchronize()
+    want, oinfo = omuon.msign_deflated(case.x64, 6, case.coeffs, tau=0.1)
+    assert info["k_eff"].cpu().tolist() == oinfo.k_eff == [3, 3]
+    assert rel_fro(host64(out), want) < F32_TOL
+
+
+def test_deterministic_and_transpose_exact():
+    case = workloads.small_muon(2, 100, 260, dtype="bf16", k=4)
+    x = dev_tensor(case.x, "bf16")
+    a = sd.msign(x, 4, 5)
+    b = sd.msign(x, 4, 5)
+    xt = x.transpose(1, 2).contiguous()
+    c = sd.msign(xt, 4, 5)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    assert torch.equal(a, c.transpose(1, 2))
+
+
+def test_device_sketch_matches_host_generator():
+    for (b, s, rp, seed) in [(3, 80, 12, 5), (24, 768, 16, 0), (2, 17, 5, 2**40 + 7)]:
+        dev = sd.sketch(b, s, rp, seed).cpu().numpy()
+        host = sd.sketch_host(b, s, rp, seed)
+        bad = np.count_nonzero(dev != host)
+        say(f"sketch {b}x{s}x{rp}: {bad} mismatches, max diff {np.abs(dev - host).max():.3e}")
+        assert bad == 0
+
+
+def test_sketch_hook_matches_internal_generator():
+    case = workloads.small_muon(3, 80, 150, k=4)
+    x = dev_tensor(case.x, "f32")
+    rp = min(80, 4 + 8)
+    om = np.ascontiguousarray(np.stack([orng.sketch(5, b, 80, rp).T for b in range(3)]), dtype=np.float32)
+    sk = torch.from_numpy(om).cuda()
+    a = sd.msign(x, 4, 5, seed=5)
+    b = sd.msign(x, 4, 5, seed=5, sketch=sk)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_zero_matrix_and_in_place():
+    z = torch.zeros(2, 40, 72, device="cuda")
+    for k in (0, 3):
+        assert torch.count_nonzero(sd.msign(z, k, 5)) == 0
+    case = workloads.small_muon(1, 64, 128, k=2)
+    x = dev_tensor(case.x, "f32")
+    ref = sd.msign(x, 2, 5)
+    sd.msign(x, 2, 5, out=x)
+    torch.cuda.synchronize()
+    assert torch.equal(ref, x)
+
+
+def test_caller_workspace():
+    case = workloads.small_muon(2, 128, 256, dtype="bf16", k=4)
+    x = dev_tensor(case.x, "bf16")
+    nbytes = sd.msign_workspace_bytes(2, 128, 256, 4, sd.SD_DTYPE_BF16)
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    a = sd.msign(x, 4, 5)
+    b = sd.msign(x, 4, 5, workspace=ws)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+    with pytest.raises(sd.SdError):
+        sd.msign(x, 4, 5, workspace=ws[: nbytes // 2])
+
+
+def test_steps_zero_returns_start():
+    case = workloads.small_muon(1, 64, 96, k=2)
+    x = dev_tensor(case.x, "f32")
+    out = sd.msign(x, 2, 0)
+    torch.cuda.synchronize()
+    want, _ = omuon.msign_deflated(case.x64, 2, np.zeros((0, 3)))
+    assert rel_fro(host64(out), want) < 1e-5
