@@ -189,14 +189,18 @@ static __global__ void rows_to_panel_kernel(const float* in, int c, int len, int
   pt[gid] = x < len ? in[(long long)x * c + j] : 0.f;
 }
 
-// PSD output (Alg. 2 restore and symmetrization):
-//   P[i][j] = R[i][j] / 2 + (C[i][j] + C[j][i]) / 4 + sum_{p < kk} U[p][i] cp[p] U[p][j]
-// with C = R g(X0). 64 x 64 tiles; the transposed tile of C goes through LDS.
+// PSD output (Alg. 2 restore and symmetrization): with C = R g(X0) and the
+// restored head H = sum_{p < kk} cp[p] u_p u_p^T, P_raw = R / 2 + C / 2 + H and
+//   P = (P_raw + P_raw^T) / 2 = (R + R^T) / 4 + (C + C^T) / 4 + H.
+// Every term is evaluated so that P[i][j] and P[j][i] see the same operations
+// on swapped operands (sums are commutative, H uses cp * (u_i u_j)), hence P
+// is exactly symmetric. 64 x 64 tiles; the transposed tiles go through LDS.
 template <int KM>
 __global__ __launch_bounds__(256) void psd_out_kernel(const float* R, const float* C, int ld, const float* Ut,
                                                       int ldu, const float* coef_p, const int* kk_dev, int n,
                                                       int n_pad, float* out) {
   __shared__ float ct[64][65];
+  __shared__ float rt[64][65];
   __shared__ float ui[KM][64];
   __shared__ float uj[KM][64];
   const int tiles = n_pad / 64;
@@ -205,11 +209,13 @@ __global__ __launch_bounds__(256) void psd_out_kernel(const float* R, const floa
   const int kk = kk_dev ? *kk_dev : 0;
   for (int e = tid; e < 64 * 64; e += 256) {
     const int r = e >> 6, c = e & 63;
-    ct[c][r] = C[(long long)(j0 + r) * ld + i0 + c];   // ct[x][y] = C[j0 + y][i0 + x]
+    const long long src = (long long)(j0 + r) * ld + i0 + c;   // element (j0 + r, i0 + c)
+    ct[c][r] = C[src];
+    rt[c][r] = R[src];
   }
   for (int e = tid; e < kk * 64; e += 256) {
     const int p = e >> 6, x = e & 63;
-    ui[p][x] = Ut[(long long)p * ldu + i0 + x] * coef_p[p];
+    ui[p][x] = Ut[(long long)p * ldu + i0 + x];
     uj[p][x] = Ut[(long long)p * ldu + j0 + x];
   }
   __syncthreads();
@@ -217,8 +223,9 @@ __global__ __launch_bounds__(256) void psd_out_kernel(const float* R, const floa
   for (int r = ty; r < 64; r += 4) {
     const int i = i0 + r, j = j0 + tx;
     float h = 0.f;
-    for (int p = 0; p < kk; ++p) h = fmaf(ui[p][r], uj[p][tx], h);
-    const float v = 0.5f * R[(long long)i * ld + j] + 0.25f * (C[(long long)i * ld + j] + ct[r][tx]) + h;
+    for (int p = 0; p < kk; ++p) h = fmaf(coef_p[p], ui[p][r] * uj[p][tx], h);
+    const long long ij = (long long)i * ld + j;
+    const float v = 0.25f * (R[ij] + rt[r][tx]) + 0.25f * (C[ij] + ct[r][tx]) + h;
     if (i < n && j < n) out[(long long)i * n + j] = v;
   }
 }
