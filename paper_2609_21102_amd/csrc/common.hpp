@@ -19,17 +19,15 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 constexpr int WAVE = 64;
 
 // ---------------------------------------------------------------- bf16 ----
-// float -> bfloat16, round to nearest even (NaN maps to a quiet NaN).
-__device__ __forceinline__ bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)0x7fc0;
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
-__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+// float -> bfloat16 with round to nearest even, two at a time through the
+// gfx950 conversion instruction (v_cvt_pk_bf16_f32); NaN stays NaN.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
-  return (uint32_t)f2bf(lo) | ((uint32_t)f2bf(hi) << 16);
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
 }
+__device__ __forceinline__ bf16_t f2bf(float f) { return (bf16_t)(pack_bf2(f, 0.f) & 0xffffu); }
+__device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
 // Component i (a compile-time constant after unrolling) of a 16-byte value.
 __device__ __forceinline__ uint32_t u4c(const u32x4_t& u, int i) { return u[i]; }

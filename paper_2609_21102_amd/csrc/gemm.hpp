@@ -23,13 +23,14 @@
 // and writes each value at (r, c) and (c, r); diagonal tiles write c >= r.
 #pragma once
 
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace sd {
 
-constexpr int G_BM = 128, G_BN = 128, G_THREADS = 256;
 constexpr int G_ROWB = 144;                    // LDS bytes per tile row
-constexpr int G_TILEB = 128 * G_ROWB;          // one operand tile
+constexpr int G_TILEB = 128 * G_ROWB;          // one 128-row operand tile
 
 template <typename T> struct GemmK;
 template <> struct GemmK<bf16_t> { static constexpr int BK = 64; };
@@ -134,6 +135,7 @@ struct EpiUpdate {
   int final_out;       // 0: padded iterate (same layout as x); 1: caller output
   int transpose_out;   // caller output is the transpose of the canonical iterate
   int rows_valid, cols_valid;
+  bf16_t* out16;       // optional bf16 copy of the padded iterate (operand of the next products)
   __device__ void operator()(int b, int r0, int c, float v[4], int mode) const {
     const TX* xb = x + b * xstride;
 #pragma unroll
@@ -141,6 +143,7 @@ struct EpiUpdate {
     TO* ob = out + b * ostride;
     if (!final_out) {
       emit4(ob, ldo, r0, c, v, mode);
+      if (out16) emit4(out16 + b * ostride, ldo, r0, c, v, mode);
       return;
     }
     if (c >= cols_valid) return;
@@ -156,6 +159,48 @@ struct EpiUpdate {
   }
 };
 
+// Iterate update in transposed form: the kernel computes C^T = X^T B (B
+// symmetric), so v[j] is element (c, r0 + j) of the new iterate: a lane owns
+// four consecutive columns of one row and moves them as 16-byte vectors.
+// out = ac * X + C, into the padded iterate (plus its bf16 copy), or (final
+// step) the caller's output with the same rules as EpiUpdate.
+template <typename TO>
+struct EpiUpdateT {
+  const float* x;
+  long long xstride;
+  int ldx;
+  float ac;
+  TO* out;
+  long long ostride;
+  int ldo;
+  int final_out;
+  int transpose_out;
+  int rows_valid, cols_valid;
+  bf16_t* out16;
+  __device__ void operator()(int b, int r0, int c, float v[4], int mode) const {
+    const int row = c, col0 = r0;
+    const f32x4_t xv = *reinterpret_cast<const f32x4_t*>(x + b * xstride + (long long)row * ldx + col0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = ac * xv[j] + v[j];
+    TO* ob = out + b * ostride;
+    if (!final_out) {
+      st_row4(ob, ldo, row, col0, v);
+      if (out16) st_row4(out16 + b * ostride, ldo, row, col0, v);
+      return;
+    }
+    if (row >= rows_valid) return;
+    if (!transpose_out) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (col0 + j < cols_valid) ob[(long long)row * ldo + col0 + j] = Cvt<TO>::from_f(v[j]);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (col0 + j < cols_valid) ob[(long long)(col0 + j) * ldo + row] = Cvt<TO>::from_f(v[j]);
+    }
+  }
+};
+
 // Plain fp32 store of C.
 struct EpiStore {
   float* out;
@@ -167,206 +212,165 @@ struct EpiStore {
 };
 
 // ------------------------------------------------------- staging ----------
-// Four 16-byte registers of one thread's share of a tile. Members are named
-// and indexed only with compile-time constants so that they stay in VGPRs.
-struct Stage4 {
-  u32x4_t v0, v1, v2, v3;
+// Tile configuration: NWM x NWN waves, each computing WM x WN MFMA blocks of
+// 32 x 32, so a work-group owns a (32 WM NWM) x (32 WN NWN) tile of C.
+// STAGES = 2 double-buffers the LDS tiles (one barrier per K step); 1 keeps a
+// single LDS buffer (two barriers per K step) so that two work-groups fit on
+// a CU and one's epilogue overlaps the other's main loop.
+template <int NWM_, int NWN_, int WM_, int WN_, int STAGES_ = 2>
+struct GemmCfg {
+  static constexpr int NWM = NWM_, NWN = NWN_, WM = WM_, WN = WN_, STAGES = STAGES_;
+  static constexpr int BM = 32 * WM * NWM, BN = 32 * WN * NWN;
+  static constexpr int NT = 64 * NWM * NWN;
 };
-template <int I>
-__device__ __forceinline__ u32x4_t& sget(Stage4& r) {
-  if constexpr (I == 0) return r.v0;
-  else if constexpr (I == 1) return r.v1;
-  else if constexpr (I == 2) return r.v2;
-  else return r.v3;
-}
-template <int I>
-__device__ __forceinline__ const u32x4_t& sget(const Stage4& r) {
-  if constexpr (I == 0) return r.v0;
-  else if constexpr (I == 1) return r.v1;
-  else if constexpr (I == 2) return r.v2;
-  else return r.v3;
-}
+using CfgTile128 = GemmCfg<2, 2, 2, 2>;          // 128 x 128, 256 threads
+using CfgTile256 = GemmCfg<2, 4, 4, 2>;          // 256 x 256, 512 threads
+using CfgTile256s = GemmCfg<2, 4, 4, 2, 1>;      // 256 x 256, single LDS stage
+using CfgTile256x128 = GemmCfg<2, 2, 4, 2, 2>;   // 256 x 128, 256 threads
 
-// A-type tile (rows x K, K contiguous): 1024 chunks of 16 B, 4 per thread;
-// thread t owns rows t / 8 + 32 i, chunk t % 8.
-template <int I, typename T>
-__device__ __forceinline__ void load_row1(Stage4& r, const T* base, int ld, int row0, int k0) {
-  const int t = threadIdx.x;
-  const int row = (t >> 3) + 32 * I, ch = t & 7;
-  const char* p = reinterpret_cast<const char*>(base + (long long)(row0 + row) * ld + k0) + ch * 16;
-  sget<I>(r) = ld16(p);
-}
-template <typename T>
-__device__ __forceinline__ void load_rows(Stage4& r, const T* base, int ld, int row0, int k0) {
-  load_row1<0>(r, base, ld, row0, k0);
-  load_row1<1>(r, base, ld, row0, k0);
-  load_row1<2>(r, base, ld, row0, k0);
-  load_row1<3>(r, base, ld, row0, k0);
-}
-template <int I>
-__device__ __forceinline__ void store_row1(char* lds, const Stage4& r) {
-  const int t = threadIdx.x;
-  const int row = (t >> 3) + 32 * I, ch = t & 7;
-  st16(lds + row * G_ROWB + ch * 16, sget<I>(r));
-}
-__device__ __forceinline__ void store_rows(char* lds, const Stage4& r) {
-  store_row1<0>(lds, r);
-  store_row1<1>(lds, r);
-  store_row1<2>(lds, r);
-  store_row1<3>(lds, r);
-}
-
-// NN B tile: global [K rows][N cols] (N contiguous) -> LDS [N rows][K].
-// bf16: 64 x 128 tile, thread block 4 (k) x 8 (n): kb = t % 16, nb = t / 16.
-__device__ __forceinline__ void load_nn(Stage4& r, const bf16_t* base, int ld, int k0, int n0) {
-  const int t = threadIdx.x, kb = t & 15, nb = t >> 4;
-  const bf16_t* p = base + (long long)(k0 + 4 * kb) * ld + n0 + 8 * nb;
-  r.v0 = ld16(p);
-  r.v1 = ld16(p + ld);
-  r.v2 = ld16(p + 2 * (long long)ld);
-  r.v3 = ld16(p + 3 * (long long)ld);
-}
-template <int P>
-__device__ __forceinline__ void store_nn_pair(char* lds, const Stage4& r, int kb, int nb) {
-  // column 2P: low halves of word P of rows k..k+3; column 2P + 1: high halves
-  const uint32_t v0 = u4c(r.v0, P), v1 = u4c(r.v1, P), v2 = u4c(r.v2, P), v3 = u4c(r.v3, P);
-  const u32x2_t lo = {__builtin_amdgcn_perm(v1, v0, 0x05040100u), __builtin_amdgcn_perm(v3, v2, 0x05040100u)};
-  const u32x2_t hi = {__builtin_amdgcn_perm(v1, v0, 0x07060302u), __builtin_amdgcn_perm(v3, v2, 0x07060302u)};
-  *reinterpret_cast<u32x2_t*>(lds + (8 * nb + 2 * P) * G_ROWB + 8 * kb) = lo;
-  *reinterpret_cast<u32x2_t*>(lds + (8 * nb + 2 * P + 1) * G_ROWB + 8 * kb) = hi;
-}
-__device__ __forceinline__ void store_nn(char* lds, const Stage4& r, bf16_t) {
-  const int t = threadIdx.x, kb = t & 15, nb = t >> 4;
-  store_nn_pair<0>(lds, r, kb, nb);
-  store_nn_pair<1>(lds, r, kb, nb);
-  store_nn_pair<2>(lds, r, kb, nb);
-  store_nn_pair<3>(lds, r, kb, nb);
-}
-// fp32: 32 x 128 tile, thread block 4 (k) x 4 (n): kb = t % 8, nb = t / 8.
-__device__ __forceinline__ void load_nn(Stage4& r, const float* base, int ld, int k0, int n0) {
-  const int t = threadIdx.x, kb = t & 7, nb = t >> 3;
-  const float* p = base + (long long)(k0 + 4 * kb) * ld + n0 + 4 * nb;
-  r.v0 = ld16(p);
-  r.v1 = ld16(p + ld);
-  r.v2 = ld16(p + 2 * (long long)ld);
-  r.v3 = ld16(p + 3 * (long long)ld);
-}
-template <int J>
-__device__ __forceinline__ void store_nn_col(char* lds, const Stage4& r, int kb, int nb) {
-  const u32x4_t w = {r.v0[J], r.v1[J], r.v2[J], r.v3[J]};
-  st16(lds + (4 * nb + J) * G_ROWB + 16 * kb, w);
-}
-__device__ __forceinline__ void store_nn(char* lds, const Stage4& r, float) {
-  const int t = threadIdx.x, kb = t & 7, nb = t >> 3;
-  store_nn_col<0>(lds, r, kb, nb);
-  store_nn_col<1>(lds, r, kb, nb);
-  store_nn_col<2>(lds, r, kb, nb);
-  store_nn_col<3>(lds, r, kb, nb);
-}
-
-// fp32 source -> bf16 LDS (the bf16 filter keeps its iterate in fp32 and
-// rounds it when it becomes a product operand). A thread holds two 16-byte
-// halves per row: lo = floats 0..3, hi = floats 4..7 of its 8-element chunk.
-struct Stage8 {
-  Stage4 lo, hi;
-};
-template <int I>
-__device__ __forceinline__ void load_row1_f(Stage8& r, const float* base, int ld, int row0, int k0) {
-  const int t = threadIdx.x;
-  const int row = (t >> 3) + 32 * I, ch = t & 7;
-  const float* p = base + (long long)(row0 + row) * ld + k0 + 8 * ch;
-  sget<I>(r.lo) = ld16(p);
-  sget<I>(r.hi) = ld16(p + 4);
-}
 __device__ __forceinline__ u32x4_t pack8(const u32x4_t& a, const u32x4_t& b) {
   return u32x4_t{pack_bf2(__uint_as_float(a[0]), __uint_as_float(a[1])),
                  pack_bf2(__uint_as_float(a[2]), __uint_as_float(a[3])),
                  pack_bf2(__uint_as_float(b[0]), __uint_as_float(b[1])),
                  pack_bf2(__uint_as_float(b[2]), __uint_as_float(b[3]))};
 }
-template <int I>
-__device__ __forceinline__ void store_row1_f(char* lds, const Stage8& r) {
-  const int t = threadIdx.x;
-  const int row = (t >> 3) + 32 * I, ch = t & 7;
-  st16(lds + row * G_ROWB + ch * 16, pack8(sget<I>(r.lo), sget<I>(r.hi)));
-}
-// NN, fp32 source: 64 (k) x 128 (n) tile, thread block 4 (k) x 8 (n).
-template <int I>
-__device__ __forceinline__ float nnf(const Stage8& r, int c) {
-  return __uint_as_float(c < 4 ? sget<I>(r.lo)[c] : sget<I>(r.hi)[c - 4]);
-}
-template <int P>
-__device__ __forceinline__ void store_nn_pair_f(char* lds, const Stage8& r, int kb, int nb) {
-  const u32x2_t lo = {pack_bf2(nnf<0>(r, 2 * P), nnf<1>(r, 2 * P)), pack_bf2(nnf<2>(r, 2 * P), nnf<3>(r, 2 * P))};
-  const u32x2_t hi = {pack_bf2(nnf<0>(r, 2 * P + 1), nnf<1>(r, 2 * P + 1)),
-                      pack_bf2(nnf<2>(r, 2 * P + 1), nnf<3>(r, 2 * P + 1))};
-  *reinterpret_cast<u32x2_t*>(lds + (8 * nb + 2 * P) * G_ROWB + 8 * kb) = lo;
-  *reinterpret_cast<u32x2_t*>(lds + (8 * nb + 2 * P + 1) * G_ROWB + 8 * kb) = hi;
-}
 
-// Staging policy per (LDS/MFMA type T, source type S).
-template <typename T, typename S> struct Stager;
-template <typename T> struct Stager<T, T> {
-  using Reg = Stage4;
-  __device__ __forceinline__ static void rows(Reg& r, const T* b, int ld, int row0, int k0) {
-    load_rows(r, b, ld, row0, k0);
+// Rows x K tile with K contiguous in memory (the A operand, and B in NT form):
+// ROWS rows of 8 LDS chunks of 16 bytes; chunk id = t + NT u -> row id / 8,
+// chunk id % 8. An fp32 source feeding bf16 MFMAs loads 32 bytes per chunk
+// and rounds them while writing LDS.
+template <int ROWS, int NT, typename T, typename S>
+struct RowStager {
+  static constexpr bool CONV = sizeof(S) != sizeof(T);
+  static constexpr int UNITS = ROWS * 8 / NT;
+  static constexpr int LOADS = UNITS * (CONV ? 2 : 1);
+  u32x4_t r[LOADS];
+  __device__ __forceinline__ void load(const S* base, int ld, int row0, int k0) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < UNITS; ++u) {
+      const int id = t + NT * u, row = id >> 3, ch = id & 7;
+      const S* p = base + (long long)(row0 + row) * ld + k0 + ch * (CONV ? 8 : 16 / (int)sizeof(S));
+      if constexpr (CONV) {
+        r[2 * u] = ld16(p);
+        r[2 * u + 1] = ld16(p + 4);
+      } else {
+        r[u] = ld16(p);
+      }
+    }
   }
-  __device__ __forceinline__ static void rows_st(char* lds, const Reg& r) { store_rows(lds, r); }
-  __device__ __forceinline__ static void nn(Reg& r, const T* b, int ld, int k0, int n0) { load_nn(r, b, ld, k0, n0); }
-  __device__ __forceinline__ static void nn_st(char* lds, const Reg& r) { store_nn(lds, r, T{}); }
+  __device__ __forceinline__ void store(char* lds) const {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < UNITS; ++u) {
+      const int id = t + NT * u, row = id >> 3, ch = id & 7;
+      if constexpr (CONV) st16(lds + row * G_ROWB + ch * 16, pack8(r[2 * u], r[2 * u + 1]));
+      else st16(lds + row * G_ROWB + ch * 16, r[u]);
+    }
+  }
 };
-template <> struct Stager<bf16_t, float> {
-  using Reg = Stage8;
-  __device__ __forceinline__ static void rows(Reg& r, const float* b, int ld, int row0, int k0) {
-    load_row1_f<0>(r, b, ld, row0, k0);
-    load_row1_f<1>(r, b, ld, row0, k0);
-    load_row1_f<2>(r, b, ld, row0, k0);
-    load_row1_f<3>(r, b, ld, row0, k0);
+
+// K x COLS tile with COLS contiguous in memory (B in NN form), transposed into
+// LDS rows of K. A thread block covers 4 consecutive k and 8 (bf16 LDS) or 4
+// (fp32 LDS) consecutive columns; block id = t + NT u -> kb = id % KB,
+// nb = id / KB.
+template <int COLS, int NT, typename T, typename S>
+struct NNStager;
+
+template <int COLS, int NT, typename S>
+struct NNStager<COLS, NT, bf16_t, S> {       // 64 x COLS tile, bf16 LDS
+  static constexpr bool CONV = sizeof(S) == 4;
+  static constexpr int KB = 16;
+  static constexpr int UNITS = KB * (COLS / 8) / NT;
+  static constexpr int PER = CONV ? 8 : 4;    // 16-byte loads per unit
+  u32x4_t r[UNITS * PER];
+  __device__ __forceinline__ void load(const S* base, int ld, int k0, int n0) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < UNITS; ++u) {
+      const int id = t + NT * u, kb = id % KB, nb = id / KB;
+      const S* p = base + (long long)(k0 + 4 * kb) * ld + n0 + 8 * nb;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        if constexpr (CONV) {
+          r[u * PER + 2 * i] = ld16(p + i * (long long)ld);
+          r[u * PER + 2 * i + 1] = ld16(p + i * (long long)ld + 4);
+        } else {
+          r[u * PER + i] = ld16(p + i * (long long)ld);
+        }
+      }
+    }
   }
-  __device__ __forceinline__ static void rows_st(char* lds, const Reg& r) {
-    store_row1_f<0>(lds, r);
-    store_row1_f<1>(lds, r);
-    store_row1_f<2>(lds, r);
-    store_row1_f<3>(lds, r);
+  // 16-bit element c (0..7) of row i of unit u
+  __device__ __forceinline__ uint32_t half_bits(int u, int i, int c) const {
+    if constexpr (CONV) {
+      const float f = __uint_as_float(r[u * PER + 2 * i + (c >> 2)][c & 3]);
+      return (uint32_t)f2bf(f);
+    } else {
+      const uint32_t w = r[u * PER + i][c >> 1];
+      return (c & 1) ? (w >> 16) : (w & 0xffffu);
+    }
   }
-  __device__ __forceinline__ static void nn(Reg& r, const float* b, int ld, int k0, int n0) {
-    const int t = threadIdx.x, kb = t & 15, nb = t >> 4;
-    const float* p = b + (long long)(k0 + 4 * kb) * ld + n0 + 8 * nb;
-    r.lo.v0 = ld16(p);
-    r.hi.v0 = ld16(p + 4);
-    r.lo.v1 = ld16(p + ld);
-    r.hi.v1 = ld16(p + ld + 4);
-    r.lo.v2 = ld16(p + 2 * (long long)ld);
-    r.hi.v2 = ld16(p + 2 * (long long)ld + 4);
-    r.lo.v3 = ld16(p + 3 * (long long)ld);
-    r.hi.v3 = ld16(p + 3 * (long long)ld + 4);
+  __device__ __forceinline__ void store(char* lds) const {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < UNITS; ++u) {
+      const int id = t + NT * u, kb = id % KB, nb = id / KB;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const u32x2_t v = {half_bits(u, 0, c) | (half_bits(u, 1, c) << 16),
+                           half_bits(u, 2, c) | (half_bits(u, 3, c) << 16)};
+        *reinterpret_cast<u32x2_t*>(lds + (8 * nb + c) * G_ROWB + 8 * kb) = v;
+      }
+    }
   }
-  __device__ __forceinline__ static void nn_st(char* lds, const Reg& r) {
-    const int t = threadIdx.x, kb = t & 15, nb = t >> 4;
-    store_nn_pair_f<0>(lds, r, kb, nb);
-    store_nn_pair_f<1>(lds, r, kb, nb);
-    store_nn_pair_f<2>(lds, r, kb, nb);
-    store_nn_pair_f<3>(lds, r, kb, nb);
+};
+
+template <int COLS, int NT>
+struct NNStager<COLS, NT, float, float> {    // 32 x COLS tile, fp32 LDS
+  static constexpr int KB = 8;
+  static constexpr int UNITS = KB * (COLS / 4) / NT;
+  u32x4_t r[UNITS * 4];
+  __device__ __forceinline__ void load(const float* base, int ld, int k0, int n0) {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < UNITS; ++u) {
+      const int id = t + NT * u, kb = id % KB, nb = id / KB;
+      const float* p = base + (long long)(k0 + 4 * kb) * ld + n0 + 4 * nb;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) r[u * 4 + i] = ld16(p + i * (long long)ld);
+    }
+  }
+  __device__ __forceinline__ void store(char* lds) const {
+    const int t = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < UNITS; ++u) {
+      const int id = t + NT * u, kb = id % KB, nb = id / KB;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const u32x4_t w = {r[u * 4][j], r[u * 4 + 1][j], r[u * 4 + 2][j], r[u * 4 + 3][j]};
+        st16(lds + (4 * nb + j) * G_ROWB + 16 * kb, w);
+      }
+    }
   }
 };
 
 // ---------------------------------------------------------- compute -------
-template <typename T>
-__device__ __forceinline__ void tile_mma(const char* la, const char* lb, f32x16_t acc[2][2],
-                                         int wm, int wn, int lane) {
+template <typename T, int WM, int WN>
+__device__ __forceinline__ void tile_mma(const char* la, const char* lb, f32x16_t (&acc)[WM][WN], int wm,
+                                         int wn, int lane) {
   const int r32 = lane & 31, h = lane >> 5;
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    u32x4_t a[2], b[2];
+    u32x4_t a[WM], b[WN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      a[i] = ld16(la + (wm * 64 + i * 32 + r32) * G_ROWB + (2 * g + h) * 16);
-      b[i] = ld16(lb + (wn * 64 + i * 32 + r32) * G_ROWB + (2 * g + h) * 16);
-    }
+    for (int i = 0; i < WM; ++i) a[i] = ld16(la + (wm * WM * 32 + i * 32 + r32) * G_ROWB + (2 * g + h) * 16);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
+    for (int i = 0; i < WN; ++i) b[i] = ld16(lb + (wn * WN * 32 + i * 32 + r32) * G_ROWB + (2 * g + h) * 16);
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
+    for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < WN; ++ni) {
         if constexpr (sizeof(T) == 2) {
           acc[mi][ni] = mfma32_bf16(a[mi], b[ni], acc[mi][ni]);
         } else {
@@ -390,15 +394,17 @@ __device__ __forceinline__ void sym_tile(int t, int nt, int& tm, int& tn) {
 
 // T: MFMA / LDS element type; SA, SB: element types of A and B in memory
 // (fp32 sources feed bf16 MFMAs through rounding in the staging step).
-template <typename T, typename SA, typename SB, bool B_NN, bool SYM, typename Epi>
-__global__ __launch_bounds__(G_THREADS, 2) void gemm_kernel(const SA* __restrict__ A,
-                                                            const SB* __restrict__ B,
-                                                            GemmShape sh, Epi epi) {
-  using StA = Stager<T, SA>;
-  using StB = Stager<T, SB>;
+// A_KN: A is stored K x M (M contiguous) and transposed while staging, as B
+// is in NN form.
+template <typename Cfg, typename T, typename SA, typename SB, bool A_KN, bool B_NN, bool SYM, typename Epi>
+__global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const SA* __restrict__ A, const SB* __restrict__ B,
+                                                       GemmShape sh, Epi epi) {
   constexpr int BK = GemmK<T>::BK;
-  __shared__ __attribute__((aligned(16))) char lds[4 * G_TILEB];
-  const int tiles_m = sh.M / G_BM, tiles_n = sh.N / G_BN;
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, NT = Cfg::NT, WM = Cfg::WM, WN = Cfg::WN;
+  constexpr int TA = BM * G_ROWB, TB = BN * G_ROWB, STAGE = TA + TB;
+  static_assert(!SYM || BM == BN, "symmetric tiling needs square tiles");
+  __shared__ __attribute__((aligned(16))) char lds[Cfg::STAGES * STAGE];
+  const int tiles_m = sh.M / BM, tiles_n = sh.N / BN;
   const int per = SYM ? tiles_m * (tiles_m + 1) / 2 : tiles_m * tiles_n;
   const int lid = xcd_remap(blockIdx.x, per * sh.batch);
   const int b = lid / per;
@@ -409,72 +415,82 @@ __global__ __launch_bounds__(G_THREADS, 2) void gemm_kernel(const SA* __restrict
     tm = t / tiles_n;
     tn = t - tm * tiles_n;
   }
-  const int m0 = tm * G_BM, n0 = tn * G_BN;
+  const int m0 = tm * BM, n0 = tn * BN;
   const SA* Ab = A + b * sh.sa;
   const SB* Bb = B + b * sh.sb;
   const int wave = threadIdx.x / WAVE, lane = threadIdx.x & (WAVE - 1);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / Cfg::NWN, wn = wave % Cfg::NWN;
 
-  f32x16_t acc[2][2];
+  f32x16_t acc[WM][WN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < WM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16_t{};
+    for (int j = 0; j < WN; ++j) acc[i][j] = f32x16_t{};
 
-  typename StA::Reg ra;
-  typename StB::Reg rb;
+  using AStager = typename std::conditional<A_KN, NNStager<BM, NT, T, SA>, RowStager<BM, NT, T, SA>>::type;
+  using BStager = typename std::conditional<B_NN, NNStager<BN, NT, T, SB>, RowStager<BN, NT, T, SB>>::type;
+  AStager sa;
+  BStager sb;
+  auto load_tiles = [&](int k0) {
+    if constexpr (A_KN) sa.load(Ab, sh.lda, k0, m0);
+    else sa.load(Ab, sh.lda, m0, k0);
+    if constexpr (B_NN) sb.load(Bb, sh.ldb, k0, n0);
+    else sb.load(Bb, sh.ldb, n0, k0);
+  };
   const int nk = sh.K / BK;
-  StA::rows(ra, Ab, sh.lda, m0, 0);
-  if constexpr (B_NN) StB::nn(rb, Bb, sh.ldb, 0, n0);
-  else StB::rows(rb, Bb, sh.ldb, n0, 0);
-  StA::rows_st(lds, ra);
-  if constexpr (B_NN) StB::nn_st(lds + G_TILEB, rb);
-  else StB::rows_st(lds + G_TILEB, rb);
-  __syncthreads();
-
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < nk;
-    if (more) {
-      const int k0 = (kt + 1) * BK;
-      StA::rows(ra, Ab, sh.lda, m0, k0);
-      if constexpr (B_NN) StB::nn(rb, Bb, sh.ldb, k0, n0);
-      else StB::rows(rb, Bb, sh.ldb, n0, k0);
-    }
-    tile_mma<T>(lds + cur * 2 * G_TILEB, lds + cur * 2 * G_TILEB + G_TILEB, acc, wm, wn, lane);
-    if (more) {
-      char* nxt = lds + (cur ^ 1) * 2 * G_TILEB;
-      StA::rows_st(nxt, ra);
-      if constexpr (B_NN) StB::nn_st(nxt + G_TILEB, rb);
-      else StB::rows_st(nxt + G_TILEB, rb);
-    }
+  load_tiles(0);
+  if constexpr (Cfg::STAGES == 2) {
+    sa.store(lds);
+    sb.store(lds + TA);
     __syncthreads();
+    for (int kt = 0; kt < nk; ++kt) {
+      const int cur = kt & 1;
+      const bool more = kt + 1 < nk;
+      if (more) load_tiles((kt + 1) * BK);
+      tile_mma<T, WM, WN>(lds + cur * STAGE, lds + cur * STAGE + TA, acc, wm, wn, lane);
+      if (more) {
+        char* nxt = lds + (cur ^ 1) * STAGE;
+        sa.store(nxt);
+        sb.store(nxt + TA);
+      }
+      __syncthreads();
+    }
+  } else {
+    for (int kt = 0; kt < nk; ++kt) {
+      sa.store(lds);
+      sb.store(lds + TA);
+      __syncthreads();
+      if (kt + 1 < nk) load_tiles((kt + 1) * BK);
+      tile_mma<T, WM, WN>(lds, lds + TA, acc, wm, wn, lane);
+      __syncthreads();
+    }
   }
 
   const int mode = SYM ? (tm == tn ? EMIT_SYM_DIAG : EMIT_SYM_OFF) : EMIT_FULL;
   const int r32 = lane & 31, h = lane >> 5;
 #pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
+  for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+    for (int ni = 0; ni < WN; ++ni)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         float v[4] = {acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2],
                       acc[mi][ni][4 * i + 3]};
-        const int r0 = m0 + wm * 64 + mi * 32 + 8 * i + 4 * h;
-        const int c = n0 + wn * 64 + ni * 32 + r32;
+        const int r0 = m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h;
+        const int c = n0 + wn * WN * 32 + ni * 32 + r32;
         epi(b, r0, c, v, mode);
       }
 }
 
 // Host launcher (errors surface through hipGetLastError at the end of a call).
-template <typename T, bool B_NN, bool SYM, typename SA, typename SB, typename Epi>
+// M, N must be multiples of the tile and K of the K step.
+template <typename Cfg, typename T, bool B_NN, bool SYM, typename SA, typename SB, typename Epi, bool A_KN = false>
 void launch_gemm(const SA* A, const SB* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
-  const int tm = sh.M / G_BM, tn = sh.N / G_BN;
+  const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;
   const long long blocks = per * sh.batch;
   if (blocks <= 0) return;
-  hipLaunchKernelGGL((gemm_kernel<T, SA, SB, B_NN, SYM, Epi>), dim3((unsigned)blocks), dim3(G_THREADS), 0,
+  hipLaunchKernelGGL((gemm_kernel<Cfg, T, SA, SB, A_KN, B_NN, SYM, Epi>), dim3((unsigned)blocks), dim3(Cfg::NT), 0,
                      stream, A, B, sh, epi);
 }
 

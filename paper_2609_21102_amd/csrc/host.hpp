@@ -169,12 +169,31 @@ void ts_xw(const T* X, long long sx, int ldx, int s_pad, int l_pad, const float*
   }
 }
 
-inline void cholqr(float* Pt, long long sp, int ld, int c, int len_pad, int batch, int* status, hipStream_t st) {
+// Float64 partial Grams of panel rows over 128-position chunks.
+inline void gram_partials(const float* A, long long sa, int lda, const float* B, long long sb, int ldb, int ca,
+                          int cb, int len_pad, bool sym, double* part, int batch, hipStream_t st) {
+  const dim3 g((len_pad / GP_CHUNK) * batch), b(256);
+  const int cm = ca > cb ? ca : cb;
+  if (cm <= 16) hipLaunchKernelGGL((gram_partial_kernel<16>), g, b, 0, st, A, sa, lda, B, sb, ldb, ca, cb, len_pad, sym, part, batch);
+  else if (cm <= 32) hipLaunchKernelGGL((gram_partial_kernel<32>), g, b, 0, st, A, sa, lda, B, sb, ldb, ca, cb, len_pad, sym, part, batch);
+  else hipLaunchKernelGGL((gram_partial_kernel<64>), g, b, 0, st, A, sa, lda, B, sb, ldb, ca, cb, len_pad, sym, part, batch);
+}
+
+// Scratch of the panel factorizations: partial Grams and the factors.
+inline size_t gram_part_elems(int batch, int len_pad, int ca, int cb, bool sym) {
+  return (size_t)batch * (len_pad / GP_CHUNK) * gram_items(ca, cb, sym);
+}
+
+// One CholeskyQR pass on every panel of the batch, in place.
+inline void cholqr(float* Pt, long long sp, int ld, int c, int len_pad, int batch, double* part, double* fac,
+                   int* status, hipStream_t st) {
   ProfScope ps(SD_STAGE_CHOLQR, st);
-  const dim3 g(batch), b(SM_THREADS);
-  if (c <= 16) hipLaunchKernelGGL((cholqr_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, status);
-  else if (c <= 32) hipLaunchKernelGGL((cholqr_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, status);
-  else hipLaunchKernelGGL((cholqr_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, status);
+  gram_partials(Pt, sp, ld, Pt, sp, ld, c, c, len_pad, true, part, batch, st);
+  hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac, status);
+  const dim3 g((len_pad / 128) * batch), b(128);
+  if (c <= 16) hipLaunchKernelGGL((chol_apply_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch);
+  else if (c <= 32) hipLaunchKernelGGL((chol_apply_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch);
+  else hipLaunchKernelGGL((chol_apply_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch);
 }
 
 inline void rotate(const float* in, long long si, int ldi, const float* E, long long se, const float* scale,

@@ -30,6 +30,7 @@ struct LowRankArgs {
   void* out;          // null: no output
   long long so;
   int ldo;
+  bf16_t* out16;      // optional bf16 copy of out (same layout)
   float* sumsq;       // [b][tiles] or null
   int rows_pad, cols_pad, kmax, batch;
 };
@@ -118,6 +119,7 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
       ss = fmaf(v[c], v[c], ss);
     }
     if (ob) store8<TO>(ob + (long long)i * a.ldo + n0 + cg * 8, v);
+    if (a.out16) store8<bf16_t>(a.out16 + b * a.so + (long long)i * a.ldo + n0 + cg * 8, v);
   }
   if (a.sumsq) {
     ss = block_sum(ss, red);

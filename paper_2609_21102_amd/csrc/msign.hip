@@ -20,9 +20,11 @@ struct MsignPlan {
   // buffers
   void *xc, *bm;
   float *xa, *xb;
+  bf16_t *xa16, *xb16;   // bf16 copies of the iterates (bf16 path)
   float *a32;
   bf16_t* a16;
   float *om, *yl, *ys, *E, *sv, *invsv, *coefA, *coefB, *Ls, *Ll, *sumsq, *alpha, *nu;
+  double *part, *fac;
   int* keff;
   int tiles;
 };
@@ -33,6 +35,8 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   p.xc = p.copy_in ? ar.take<char>(B * sl * p.esz) : nullptr;
   p.xa = ar.take<float>(B * sl);   // iterates are float32 for both dtypes
   p.xb = ar.take<float>(B * sl);
+  p.xa16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * sl) : nullptr;
+  p.xb16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * sl) : nullptr;
   p.a32 = ar.take<float>(B * ss);
   p.a16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * ss) : nullptr;
   p.bm = ar.take<char>(B * ss * p.esz);
@@ -49,6 +53,8 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   p.Ls = ar.take<float>(B * kq * p.s_pad);
   p.Ll = ar.take<float>(B * kq * p.l_pad);
   p.keff = ar.take<int>(B);
+  p.part = ar.take<double>(gram_part_elems(p.batch, p.l_pad > p.s_pad ? p.l_pad : p.s_pad, rq, rq, true));
+  p.fac = ar.take<double>(B * rq * rq);
   p.tiles = (p.s_pad / 128) * (p.l_pad / 128);
   p.sumsq = ar.take<float>(B * p.tiles);
   p.alpha = ar.take<float>(B);
@@ -91,6 +97,17 @@ static void make_plan(MsignPlan& p, int batch, int m, int n, int k, int steps, i
   p.copy_in = p.tall || p.s != p.s_pad || p.l != p.l_pad || !aligned;
 }
 
+// Iterate update X <- a X + B X: 256 x 256 tiles when the padded shape allows.
+// The X operand is the bf16 copy (bf16 path) or the fp32 iterate itself.
+template <typename T, typename SX, typename Epi>
+static void update_gemm(const MsignPlan& p, const T* bm, const SX* xop, const GemmShape& g, const Epi& eu,
+                        hipStream_t st) {
+  if (p.s_pad % 256 == 0 && p.l_pad % 256 == 0)
+    launch_gemm<CfgTile256, T, true, false>(bm, xop, g, eu, st);
+  else
+    launch_gemm<CfgTile128, T, true, false>(bm, xop, g, eu, st);
+}
+
 template <typename T>
 static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opts& o, const T* in, T* out,
                      hipStream_t st) {
@@ -127,18 +144,19 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
       hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, p.s, rp, o.seed, B);
     }
     ts_xtw<T>(xc, sx, ldx, s_pad, l_pad, p.om, so, s_pad, rp, p.yl, sl_, l_pad, B, st);
-    cholqr(p.yl, sl_, l_pad, rp, l_pad, B, o.status_dev, st);
+    cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st);
     for (int j = 0; j < o.power_iters; ++j) {
       ts_xw<T>(xc, sx, ldx, s_pad, l_pad, p.yl, sl_, l_pad, rp, p.ys, so, s_pad, B, st);
-      cholqr(p.ys, so, s_pad, rp, s_pad, B, o.status_dev, st);
+      cholqr(p.ys, so, s_pad, rp, s_pad, B, p.part, p.fac, o.status_dev, st);
       ts_xtw<T>(xc, sx, ldx, s_pad, l_pad, p.ys, so, s_pad, rp, p.yl, sl_, l_pad, B, st);
-      cholqr(p.yl, sl_, l_pad, rp, l_pad, B, o.status_dev, st);
+      cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st);
     }
     ts_xw<T>(xc, sx, ldx, s_pad, l_pad, p.yl, sl_, l_pad, rp, p.ys, so, s_pad, B, st);   // G = (X Q)^T
     {
       ProfScope ps(SD_STAGE_SMALL, st);
-      hipLaunchKernelGGL(svd_head_kernel, dim3(B), dim3(SM_THREADS), 0, st, p.ys, so, s_pad, s_pad, rp, p.k, o.tau,
-                         p.E, p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out);
+      gram_partials(p.ys, so, s_pad, p.ys, so, s_pad, rp, rp, s_pad, true, p.part, B, st);   // G G^T
+      hipLaunchKernelGGL(svd_head_kernel, dim3(B), dim3(64), 0, st, p.part, s_pad / GP_CHUNK, rp, p.k, o.tau, p.E,
+                         p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out);
     }
     // V = G^T E / s (short side), U = Q E (long side)
     rotate(p.ys, so, s_pad, p.E, (long long)rp * p.k, p.invsv, p.k, p.Ls, (long long)p.k * s_pad, s_pad, rp, p.k,
@@ -179,6 +197,7 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   la.coef = p.coefB;
   la.alpha = p.alpha;
   la.out = p.xa;
+  la.out16 = p.xa16;
   la.so = sl;
   la.ldo = p.l_pad;
   la.sumsq = nullptr;
@@ -187,7 +206,14 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   // fixed-depth filter: float32 iterate; bf16 path rounds operands at staging
   float* cur = p.xa;
   float* nxt = p.xb;
+  bf16_t* cur16 = p.xa16;
+  bf16_t* nxt16 = p.xb16;
   T* bm = reinterpret_cast<T*>(p.bm);
+  // operand view of the current iterate: bf16 copy or the fp32 iterate
+  auto xop = [&]() -> const T* {
+    if constexpr (sizeof(T) == 2) return reinterpret_cast<const T*>(cur16);
+    else return reinterpret_cast<const T*>(cur);
+  };
   constexpr bool BF = sizeof(T) == 2;
   for (int t = 0; t < p.steps; ++t) {
     const float a = coeffs ? coeffs[3 * t] : 3.4445f;
@@ -211,14 +237,14 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     }
     {
       ProfScope ps(SD_STAGE_NS_GRAM, st);
-      launch_gemm<T, false, true>(cur, cur, g1, eg, st);
+      launch_gemm<CfgTile128, T, false, true>(xop(), xop(), g1, eg, st);
     }
     if (c != 0.f) {
       GemmShape g2{p.s_pad, p.s_pad, p.s_pad, p.s_pad, p.s_pad, ss, ss, B};
       EpiPoly<T> ep{p.a32, bm, b, c, ss, p.s_pad};
       const T* aop = BF ? reinterpret_cast<const T*>(p.a16) : reinterpret_cast<const T*>(p.a32);
       ProfScope ps(SD_STAGE_NS_POLY, st);
-      launch_gemm<T, false, true>(aop, aop, g2, ep, st);
+      launch_gemm<CfgTile128, T, false, true>(aop, aop, g2, ep, st);
     }
     GemmShape g3{p.s_pad, p.l_pad, p.s_pad, p.s_pad, p.l_pad, ss, sl, B};
     const bool last = t + 1 == p.steps;
@@ -229,11 +255,12 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
       eu.ldx = p.l_pad;
       eu.ac = a;
       eu.out = nxt;
+      eu.out16 = nxt16;
       eu.ostride = sl;
       eu.ldo = p.l_pad;
       eu.final_out = 0;
       ProfScope ps(SD_STAGE_NS_UPDATE, st);
-      launch_gemm<T, true, false>(bm, cur, g3, eu, st);
+      update_gemm<T>(p, bm, xop(), g3, eu, st);
     } else {
       EpiUpdate<float, T> eu{};
       eu.x = cur;
@@ -248,11 +275,14 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
       eu.rows_valid = p.s;
       eu.cols_valid = p.l;
       ProfScope ps(SD_STAGE_NS_UPDATE, st);
-      launch_gemm<T, true, false>(bm, cur, g3, eu, st);
+      update_gemm<T>(p, bm, xop(), g3, eu, st);
     }
     float* tmp = cur;
     cur = nxt;
     nxt = tmp;
+    bf16_t* tmp16 = cur16;
+    cur16 = nxt16;
+    nxt16 = tmp16;
   }
   if (p.steps == 0) {
     const long long tot = (long long)p.m * p.n * B;

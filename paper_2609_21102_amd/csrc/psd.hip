@@ -185,6 +185,7 @@ struct PsdPlan {
   float *zp, *r, *xa, *xb, *s32, *bm, *c;
   float *vt, *zt, *E, *lam, *ut, *coefR, *coefX, *coefP;
   int* ndef;
+  double *part, *fac;
   float *qlan, *w, *t, *v, *theta, *alpha_x0;
   LanczosState* lst;
 };
@@ -209,6 +210,8 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
   p.coefX = ar.take<float>(kq);
   p.coefP = ar.take<float>(kq);
   p.ndef = ar.take<int>(1);
+  p.part = ar.take<double>(gram_part_elems(1, p.n_pad, kq, kq, false));
+  p.fac = ar.take<double>((size_t)kq * kq);
   p.qlan = ar.take<float>((size_t)(p.lz + 1) * p.n_pad);
   p.w = ar.take<float>(p.n_pad);
   p.t = ar.take<float>(p.n_pad);
@@ -297,7 +300,7 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     float* zt = p.zt;
     for (int j = 0; j + 1 < o.subspace_iters; ++j) {
       ts_xw<float>(z, nn, np, np, np, vt, 0, np, K, zt, 0, np, 1, st);
-      cholqr(zt, 0, np, K, np, 1, o.status_dev, st);
+      cholqr(zt, 0, np, K, np, 1, p.part, p.fac, o.status_dev, st);
       float* tmp = vt;
       vt = zt;
       zt = tmp;
@@ -305,8 +308,9 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     ts_xw<float>(z, nn, np, np, np, vt, 0, np, K, zt, 0, np, 1, st);   // Zt = Z V
     {
       ProfScope ps(SD_STAGE_SMALL, st);
-      hipLaunchKernelGGL(ritz_kernel, dim3(1), dim3(SM_THREADS), 0, st, vt, zt, np, np, K, o.tau, o.window, o.gamma,
-                       p.E, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out, o.n_deflated_out,
+      gram_partials(vt, 0, np, zt, 0, np, K, K, np, false, p.part, 1, st);   // V^T (Z V)
+      hipLaunchKernelGGL(ritz_kernel, dim3(1), dim3(64), 0, st, p.part, np / GP_CHUNK, K, o.tau, o.window, o.gamma,
+                         p.E, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out, o.n_deflated_out,
                          o.n_positive_out);
     }
     rotate(vt, 0, np, p.E, 0, nullptr, 0, p.ut, 0, np, K, K, np, 1, st);
@@ -321,7 +325,7 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     la.out = p.r;
     lowrank<float, float>(la, st);
     // next basis: CholQR(Zt), written back after the filter
-    cholqr(zt, 0, np, K, np, 1, o.status_dev, st);
+    cholqr(zt, 0, np, K, np, 1, p.part, p.fac, o.status_dev, st);
     hipLaunchKernelGGL(panel_to_rows_kernel, grid1((long long)n * K, 256), dim3(256), 0, st, zt, np, K, n, Qwarm);
   } else {
     la.x = z;
@@ -363,12 +367,12 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     }
     {
       ProfScope ps(SD_STAGE_NS_GRAM, st);
-      launch_gemm<float, false, true>(cur, cur, g, eg, st);
+      launch_gemm<CfgTile128, float, false, true>(cur, cur, g, eg, st);
     }
     if (c != 0.f) {
       ProfScope ps(SD_STAGE_NS_POLY, st);
       EpiPoly<float> ep{p.s32, p.bm, b, c, nn, np};
-      launch_gemm<float, false, true>(p.s32, p.s32, g, ep, st);
+      launch_gemm<CfgTile128, float, false, true>(p.s32, p.s32, g, ep, st);
     }
     EpiUpdate<float, float> eu{};
     eu.x = cur;
@@ -380,7 +384,7 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     eu.ldo = np;
     {
       ProfScope ps(SD_STAGE_NS_UPDATE, st);
-      launch_gemm<float, false, true>(p.bm, cur, g, eu, st);
+      launch_gemm<CfgTile128, float, false, true>(p.bm, cur, g, eu, st);
     }
     float* tmp = cur;
     cur = nxt;
@@ -390,7 +394,7 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   ProfScope ps(SD_STAGE_RESTORE, st);
   GemmShape g{np, np, np, np, np, nn, nn, 1};
   EpiStore es{p.c, nn, np};
-  launch_gemm<float, false, false>(p.r, cur, g, es, st);
+  launch_gemm<CfgTile128, float, false, false>(p.r, cur, g, es, st);
   const int tiles = (np / 64) * (np / 64);
   const float* ut = K > 0 ? p.ut : nullptr;
   const int* kk = K > 0 ? p.ndef : nullptr;

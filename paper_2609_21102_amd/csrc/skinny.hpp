@@ -45,16 +45,16 @@ __global__ __launch_bounds__(256) void ts_xtw_kernel(const T* __restrict__ X, lo
 #pragma unroll
   for (int m = 0; m < MJ; ++m) acc[m][0] = acc[m][1] = f32x4_t{};
 
-  Stage4 rb;
+  NNStager<128, 256, T, T> rb;
   const int nk = s_pad / BK;
-  load_nn(rb, Xb, ldx, 0, n0);
-  store_nn(lds, rb, T{});
+  rb.load(Xb, ldx, 0, n0);
+  rb.store(lds);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     const int i0 = kt * BK;
     const bool more = kt + 1 < nk;
-    if (more) load_nn(rb, Xb, ldx, i0 + BK, n0);
+    if (more) rb.load(Xb, ldx, i0 + BK, n0);
     const char* ls = lds + cur * G_TILEB;
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
@@ -80,7 +80,7 @@ __global__ __launch_bounds__(256) void ts_xtw_kernel(const T* __restrict__ X, lo
         }
       }
     }
-    if (more) store_nn(lds + (cur ^ 1) * G_TILEB, rb, T{});
+    if (more) rb.store(lds + (cur ^ 1) * G_TILEB);
     __syncthreads();
   }
   float* Pb = Pt + b * sp;

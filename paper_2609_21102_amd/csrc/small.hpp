@@ -1,6 +1,8 @@
 // Small dense linear algebra on one work-group per matrix, in float64:
-//   * Gram of panel rows (Pt[a][:] . Pt[b][:])
-//   * CholeskyQR of a panel (one pass; pivots floored at c u tr(Gram))
+//   * Gram of panel rows (Pt[a][:] . Pt[b][:]) as float64 partial sums over
+//     128-position chunks (many work-groups), reduced in chunk order
+//   * CholeskyQR of a panel (one pass; pivots floored at c u tr(Gram)):
+//     factor on one wave, triangular apply over many work-groups
 //   * symmetric eigendecomposition by cyclic Jacobi with a round-robin
 //     (parallel) ordering, used for the thin SVD of the reduced matrix of the
 //     randomized SVD, for the Rayleigh-Ritz step and for the Lanczos
@@ -14,84 +16,17 @@ namespace sd {
 
 constexpr int SM_MAX = 64;        // largest panel width / eigenproblem
 constexpr int SM_THREADS = 256;
-constexpr int SM_CHUNK = 128;     // panel positions staged per pass
 constexpr int SM_LD = SM_MAX + 1;
 
 struct SmallLds {
   double h[SM_MAX][SM_LD];
   double e[SM_MAX][SM_LD];
-  float cha[SM_MAX][SM_CHUNK + 1];
-  float chb[SM_MAX][SM_CHUNK + 1];
   double rot_c[SM_MAX / 2], rot_s[SM_MAX / 2];
   int rot_i[SM_MAX / 2], rot_j[SM_MAX / 2];
   double red[SM_THREADS / WAVE];
   double key[SM_MAX];
   int perm[SM_MAX];
 };
-
-// out[a][b] = sum_x A[a][x] B[b][x] for a < ca, b < cb over x < len (len a
-// multiple of SM_CHUNK). sym: A == B, only a <= b is summed, then mirrored.
-// Each entry is accumulated in position order, so the result is
-// deterministic.
-static __device__ void panel_gram(SmallLds& s, const float* A, int lda, const float* B, int ldb, int ca,
-                           int cb, int len, bool sym) {
-  constexpr int IPT = SM_MAX * SM_MAX / SM_THREADS;   // items per thread
-  const int tid = threadIdx.x;
-  const int items = sym ? ca * (ca + 1) / 2 : ca * cb;
-  double acc[IPT];
-  int ia[IPT], ib[IPT];
-#pragma unroll
-  for (int u = 0; u < IPT; ++u) {
-    acc[u] = 0.0;
-    int p = tid + u * SM_THREADS;
-    ia[u] = -1;
-    ib[u] = -1;
-    if (p < items) {
-      if (sym) {
-        int a = 0;
-        while (p >= ca - a) {
-          p -= ca - a;
-          ++a;
-        }
-        ia[u] = a;
-        ib[u] = a + p;
-      } else {
-        ia[u] = p / cb;
-        ib[u] = p - ia[u] * cb;
-      }
-    }
-  }
-  for (int x0 = 0; x0 < len; x0 += SM_CHUNK) {
-    for (int e = tid; e < ca * SM_CHUNK; e += SM_THREADS) {
-      const int a = e / SM_CHUNK, x = e - a * SM_CHUNK;
-      s.cha[a][x] = A[(long long)a * lda + x0 + x];
-    }
-    if (!sym)
-      for (int e = tid; e < cb * SM_CHUNK; e += SM_THREADS) {
-        const int a = e / SM_CHUNK, x = e - a * SM_CHUNK;
-        s.chb[a][x] = B[(long long)a * ldb + x0 + x];
-      }
-    __syncthreads();
-    float(*cb_)[SM_CHUNK + 1] = sym ? s.cha : s.chb;
-#pragma unroll
-    for (int u = 0; u < IPT; ++u) {
-      if (ia[u] < 0) continue;
-      const float* ra = s.cha[ia[u]];
-      const float* rb = cb_[ib[u]];
-      double t = acc[u];
-      for (int x = 0; x < SM_CHUNK; ++x) t += (double)ra[x] * (double)rb[x];
-      acc[u] = t;
-    }
-    __syncthreads();
-  }
-#pragma unroll
-  for (int u = 0; u < IPT; ++u) {
-    if (ia[u] < 0) continue;
-    s.h[ia[u]][ib[u]] = acc[u];
-    if (sym) s.h[ib[u]][ia[u]] = acc[u];
-  }
-  __syncthreads();
-}
 
 // ------------------------------------------------------------- Jacobi -----
 // Eigendecomposition of the symmetric n x n matrix in s.h. On return the
@@ -100,8 +35,8 @@ static __device__ void panel_gram(SmallLds& s, const float* A, int lda, const fl
 // disjoint pairs at a time (circle-method ordering); sweeps stop when the
 // off-diagonal mass is below 1e-30 of the total, or after 60 sweeps.
 static __device__ void jacobi_eig(SmallLds& s, int n) {
-  const int tid = threadIdx.x;
-  for (int e = tid; e < n * n; e += SM_THREADS) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  for (int e = tid; e < n * n; e += nt) {
     const int i = e / n, j = e - i * n;
     s.e[i][j] = (i == j) ? 1.0 : 0.0;
   }
@@ -111,7 +46,7 @@ static __device__ void jacobi_eig(SmallLds& s, int n) {
   const int half = N / 2;
   for (int sweep = 0; sweep < 60; ++sweep) {
     double off = 0.0, tot = 0.0;
-    for (int e = tid; e < n * n; e += SM_THREADS) {
+    for (int e = tid; e < n * n; e += nt) {
       const int i = e / n, j = e - i * n;
       const double v = s.h[i][j] * s.h[i][j];
       tot += v;
@@ -146,7 +81,7 @@ static __device__ void jacobi_eig(SmallLds& s, int n) {
       }
       __syncthreads();
       // columns: H <- H J, E <- E J
-      for (int e = tid; e < n * half; e += SM_THREADS) {
+      for (int e = tid; e < n * half; e += nt) {
         const int row = e / half, p = e - row * half;
         const int i = s.rot_i[p], j = s.rot_j[p];
         if (i < 0) continue;
@@ -160,7 +95,7 @@ static __device__ void jacobi_eig(SmallLds& s, int n) {
       }
       __syncthreads();
       // rows: H <- J^T H
-      for (int e = tid; e < n * half; e += SM_THREADS) {
+      for (int e = tid; e < n * half; e += nt) {
         const int col = e / half, p = e - col * half;
         const int i = s.rot_i[p], j = s.rot_j[p];
         if (i < 0) continue;
@@ -190,26 +125,95 @@ static __device__ void sort_desc(SmallLds& s, int n) {
   __syncthreads();
 }
 
-// --------------------------------------------------------- CholeskyQR -----
-// One work-group per panel; Pt[b] is c x ld (fp32), updated in place.
+// ------------------------------------------------------ Gram partials -----
+// part[b][chunk][item] = sum over the chunk's 128 positions of A[a][x] B[bb][x]
+// for the items of gram_item (upper pairs when sym, all pairs otherwise), in
+// float64 and position order. Grid: (len_pad / 128) * batch; 256 threads.
+constexpr int GP_CHUNK = 128;
+
+__host__ __device__ inline int gram_items(int ca, int cb, bool sym) { return sym ? ca * (ca + 1) / 2 : ca * cb; }
+
+__device__ __forceinline__ void gram_item(int p, int ca, int cb, bool sym, int& a, int& bb) {
+  if (sym) {
+    int r = 0;
+    while (p >= ca - r) {
+      p -= ca - r;
+      ++r;
+    }
+    a = r;
+    bb = r + p;
+  } else {
+    a = p / cb;
+    bb = p - a * cb;
+  }
+}
+
 template <int CM>
-__global__ __launch_bounds__(SM_THREADS) void cholqr_kernel(float* Pt, long long sp, int ld, int c,
-                                                            int len_pad, int* status) {
+__global__ __launch_bounds__(256) void gram_partial_kernel(const float* A, long long sa, int lda, const float* B,
+                                                           long long sb, int ldb, int ca, int cb, int len_pad,
+                                                           bool sym, double* part, int batch) {
+  __shared__ float ta[CM][GP_CHUNK + 1];
+  __shared__ float tb[CM][GP_CHUNK + 1];
+  const int nch = len_pad / GP_CHUNK;
+  const int b = blockIdx.x / nch, ch = blockIdx.x - b * nch;
+  const int x0 = ch * GP_CHUNK;
+  const float* Ab = A + b * sa;
+  for (int e = threadIdx.x; e < ca * GP_CHUNK; e += 256) {
+    const int a = e / GP_CHUNK, x = e - a * GP_CHUNK;
+    ta[a][x] = Ab[(long long)a * lda + x0 + x];
+  }
+  if (!sym) {
+    const float* Bb = B + b * sb;
+    for (int e = threadIdx.x; e < cb * GP_CHUNK; e += 256) {
+      const int a = e / GP_CHUNK, x = e - a * GP_CHUNK;
+      tb[a][x] = Bb[(long long)a * ldb + x0 + x];
+    }
+  }
+  __syncthreads();
+  const int items = gram_items(ca, cb, sym);
+  double* out = part + ((long long)b * nch + ch) * items;
+  for (int p = threadIdx.x; p < items; p += 256) {
+    int a, bb;
+    gram_item(p, ca, cb, sym, a, bb);
+    const float* ra = ta[a];
+    const float* rb = sym ? ta[bb] : tb[bb];
+    double t = 0.0;
+    for (int x = 0; x < GP_CHUNK; ++x) t += (double)ra[x] * (double)rb[x];
+    out[p] = t;
+  }
+}
+
+// s.h[a][bb] = sum of the chunk partials in chunk order (mirrored when sym).
+static __device__ void gram_reduce(SmallLds& s, const double* part, int nch, int ca, int cb, bool sym) {
+  const int items = gram_items(ca, cb, sym);
+  for (int p = threadIdx.x; p < items; p += blockDim.x) {
+    double t = 0.0;
+    for (int c = 0; c < nch; ++c) t += part[(long long)c * items + p];
+    int a, bb;
+    gram_item(p, ca, cb, sym, a, bb);
+    s.h[a][bb] = t;
+    if (sym) s.h[bb][a] = t;
+  }
+  __syncthreads();
+}
+
+// --------------------------------------------------------- CholeskyQR -----
+// Factor: Gram = L L^T (right-looking, pivots floored at c u tr(Gram)); L is
+// written to fac[b] (c x c, float64, lower). A zero trace writes L = 0, which
+// the apply kernel turns into a zero panel. One wave per panel.
+static __global__ __launch_bounds__(64) void chol_factor_kernel(const double* part, int nch, int c, double* fac,
+                                                         int* status) {
   __shared__ SmallLds s;
-  const int tid = threadIdx.x;
-  float* P = Pt + blockIdx.x * sp;
-  panel_gram(s, P, ld, P, ld, c, c, len_pad, true);
+  const int b = blockIdx.x, tid = threadIdx.x;
+  gram_reduce(s, part + (long long)b * nch * gram_items(c, c, true), nch, c, c, true);
   double tr = 0.0;
   for (int a = 0; a < c; ++a) tr += s.h[a][a];
+  double* L = fac + (long long)b * c * c;
   if (tr == 0.0) {
-    for (int e = tid; e < c * len_pad; e += SM_THREADS) {
-      const int a = e / len_pad, x = e - a * len_pad;
-      P[(long long)a * ld + x] = 0.f;
-    }
+    for (int e = tid; e < c * c; e += 64) L[e] = 0.0;
     return;
   }
   const double floor_ = (double)c * 1.1102230246251565e-16 * tr;
-  // right-looking Cholesky: lower factor L in s.h (lower triangle)
   for (int j = 0; j < c; ++j) {
     if (tid == 0) {
       double d = s.h[j][j];
@@ -220,96 +224,114 @@ __global__ __launch_bounds__(SM_THREADS) void cholqr_kernel(float* Pt, long long
       s.h[j][j] = sqrt(d);
     }
     __syncthreads();
-    for (int i = j + 1 + tid; i < c; i += SM_THREADS) s.h[i][j] /= s.h[j][j];
+    for (int i = j + 1 + tid; i < c; i += 64) s.h[i][j] /= s.h[j][j];
     __syncthreads();
     const int m = c - j - 1;
-    for (int e = tid; e < m * m; e += SM_THREADS) {
+    for (int e = tid; e < m * m; e += 64) {
       const int i = j + 1 + e / m, k = j + 1 + e % m;
       if (k <= i) s.h[i][k] -= s.h[i][j] * s.h[k][j];
     }
     __syncthreads();
   }
-  // Q = P R^-1 with R = L^T: forward substitution per position.
-  for (int x = tid; x < len_pad; x += SM_THREADS) {
-    double q[CM];
-#pragma unroll
-    for (int jj = 0; jj < CM; ++jj) {
-      if (jj < c) {
-        double v = (double)P[(long long)jj * ld + x];
-#pragma unroll
-        for (int i = 0; i < jj; ++i) v -= q[i] * s.h[jj][i];
-        q[jj] = v / s.h[jj][jj];
-      }
-    }
-#pragma unroll
-    for (int jj = 0; jj < CM; ++jj)
-      if (jj < c) P[(long long)jj * ld + x] = (float)q[jj];
+  for (int e = tid; e < c * c; e += 64) {
+    const int i = e / c, k = e - i * c;
+    L[e] = k <= i ? s.h[i][k] : 0.0;
   }
 }
 
+// Apply: Q = P R^-1 with R = L^T, by forward substitution per position, in
+// place. Grid: (len_pad / 128) * batch; one thread per position.
+template <int CM>
+__global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp, int ld, int c, int len_pad,
+                                                         const double* fac, int batch) {
+  __shared__ double L[CM][CM + 1];
+  __shared__ double inv_d[CM];
+  const int per = len_pad / 128;
+  const int b = blockIdx.x / per;
+  const int x = (blockIdx.x - b * per) * 128 + threadIdx.x;
+  const double* F = fac + (long long)b * c * c;
+  for (int e = threadIdx.x; e < c * c; e += 128) L[e / c][e % c] = F[e];
+  __syncthreads();
+  if (threadIdx.x < c) inv_d[threadIdx.x] = L[threadIdx.x][threadIdx.x] != 0.0 ? 1.0 / L[threadIdx.x][threadIdx.x] : 0.0;
+  __syncthreads();
+  float* P = Pt + b * sp;
+  double q[CM];
+#pragma unroll
+  for (int jj = 0; jj < CM; ++jj) {
+    if (jj < c) {
+      double v = (double)P[(long long)jj * ld + x];
+#pragma unroll
+      for (int i = 0; i < jj; ++i) v -= q[i] * L[jj][i];
+      q[jj] = v * inv_d[jj];
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < CM; ++jj)
+    if (jj < c) P[(long long)jj * ld + x] = (float)q[jj];
+}
+
 // ----------------------------------------------- thin SVD of G (Alg. 3) ---
-// G = Pt (rp x ld, rows of Q^T A). Eigen-decompose H = G G^T, order the
-// eigenvalues decreasingly, and emit for the leading k: singular values, the
-// eigenvector matrix E (rp x k), 1/s (0 for s = 0) and the deflation rank
-// (fixed k, or the gate of Alg. 1 when tau > 0) with the subtraction
-// coefficients -s_j used by the residual pass.
-static __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const float* G, long long sg, int ldg,
-                                                              int len_pad, int rp, int k, float tau,
-                                                              float* E, float* sv, float* inv_sv,
-                                                              int* keff, float* coef_a, float* s_user,
-                                                              int* keff_user) {
+// From the partials of H = G G^T (G = Q^T A, rp x s): eigen-decompose H, order
+// the eigenvalues decreasingly, and emit for the leading k: singular values,
+// the eigenvector matrix E (rp x k), 1/s (0 for s = 0), and the deflation
+// rank (fixed k, or the gate of Alg. 1 when tau > 0) with the subtraction
+// coefficients -s_j used by the residual pass. One wave per matrix.
+static __global__ __launch_bounds__(64) void svd_head_kernel(const double* part, int nch, int rp, int k, float tau,
+                                                             float* E, float* sv, float* inv_sv, int* keff,
+                                                             float* coef_a, float* s_user, int* keff_user) {
   __shared__ SmallLds s;
   const int tid = threadIdx.x, b = blockIdx.x;
-  panel_gram(s, G + b * sg, ldg, nullptr, 0, rp, rp, len_pad, true);
+  gram_reduce(s, part + (long long)b * nch * gram_items(rp, rp, true), nch, rp, rp, true);
   jacobi_eig(s, rp);
   if (tid < rp) s.key[tid] = s.h[tid][tid];
   __syncthreads();
   sort_desc(s, rp);
-  for (int e = tid; e < rp * k; e += SM_THREADS) {
+  for (int e = tid; e < rp * k; e += 64) {
     const int a = e / k, j = e - a * k;
     E[(long long)b * rp * k + e] = (float)s.e[a][s.perm[j]];
   }
+  if (tid < k) {
+    const double lam = s.h[s.perm[tid]][s.perm[tid]];
+    s.key[tid] = lam > 0.0 ? sqrt(lam) : 0.0;   // reuse: singular values
+  }
+  __syncthreads();
   if (tid == 0) {
-    double sval[SM_MAX];
-    for (int j = 0; j < k; ++j) {
-      const double lam = s.h[s.perm[j]][s.perm[j]];
-      sval[j] = lam > 0.0 ? sqrt(lam) : 0.0;
-    }
     int ke = k;
     if (tau > 0.f) {
-      const double thr = (double)tau * sval[0];
+      const double thr = (double)tau * s.key[0];
       ke = 0;
-      if (sval[k - 1] < thr)
-        for (int j = 0; j < k; ++j) ke += (sval[j] > thr) ? 1 : 0;
+      if (s.key[k - 1] < thr)
+        for (int j = 0; j < k; ++j) ke += (s.key[j] > thr) ? 1 : 0;
     }
     keff[b] = ke;
     if (keff_user) keff_user[b] = ke;
-    for (int j = 0; j < k; ++j) {
-      const float sj = (float)sval[j];
-      sv[b * k + j] = sj;
-      inv_sv[b * k + j] = sval[j] > 0.0 ? (float)(1.0 / sval[j]) : 0.f;
-      coef_a[b * k + j] = j < ke ? -sj : 0.f;
-      if (s_user) s_user[b * k + j] = sj;
-    }
+    s.perm[SM_MAX - 1] = ke;
+  }
+  __syncthreads();
+  const int ke = s.perm[SM_MAX - 1];
+  if (tid < k) {
+    const double sj = s.key[tid];
+    sv[b * k + tid] = (float)sj;
+    inv_sv[b * k + tid] = sj > 0.0 ? (float)(1.0 / sj) : 0.f;
+    coef_a[b * k + tid] = tid < ke ? -(float)sj : 0.f;
+    if (s_user) s_user[b * k + tid] = (float)sj;
   }
 }
 
 // ------------------------------------------- Rayleigh-Ritz (Alg. 2) -------
-// T = V^T (Z V) (K x K, symmetrized), T = E diag(lam) E^T, Ritz pairs ordered
-// by |lam| descending (ties: larger lam, then lower index). Deflated set I:
-// all K (tau = 0) or the gate of Alg. 2 on the magnitudes. Coefficients for
-// the residual (-lam), the padded start (sign(lam) / gamma) and the restore
-// (max(lam, 0)).
-static __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const float* Vt, const float* Zt, int ld, int len_pad,
-                                                          int K, float tau, int window, float gamma, float* E,
-                                                          float* lam_sorted, int* ndef, float* coef_r,
-                                                          float* coef_x, float* coef_p, float* ritz_user,
-                                                          int* ndef_user, int* npos_user) {
+// From the partials of T = V^T (Z V) (K x K, symmetrized): T = E diag(lam) E^T,
+// Ritz pairs ordered by |lam| descending (ties: larger lam, then lower index).
+// Deflated set I: all K (tau = 0) or the gate of Alg. 2 on the magnitudes.
+// Coefficients for the residual (-lam), the padded start (sign(lam) / gamma)
+// and the restore (max(lam, 0)). One wave.
+static __global__ __launch_bounds__(64) void ritz_kernel(const double* part, int nch, int K, float tau, int window,
+                                                         float gamma, float* E, float* lam_sorted, int* ndef,
+                                                         float* coef_r, float* coef_x, float* coef_p,
+                                                         float* ritz_user, int* ndef_user, int* npos_user) {
   __shared__ SmallLds s;
   const int tid = threadIdx.x;
-  panel_gram(s, Vt, ld, Zt, ld, K, K, len_pad, false);
-  // symmetrize: T = (T + T^T) / 2
-  for (int e = tid; e < K * K; e += SM_THREADS) {
+  gram_reduce(s, part, nch, K, K, false);
+  for (int e = tid; e < K * K; e += 64) {
     const int i = e / K, j = e - i * K;
     if (i < j) {
       const double v = 0.5 * (s.h[i][j] + s.h[j][i]);
@@ -319,11 +341,7 @@ static __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const float* Vt
   }
   __syncthreads();
   jacobi_eig(s, K);
-  // key: |lam| first, then lam; index ties are broken by sort_desc
-  if (tid < K) {
-    const double lam = s.h[tid][tid];
-    s.key[tid] = fabs(lam);
-  }
+  if (tid < K) s.key[tid] = fabs(s.h[tid][tid]);
   __syncthreads();
   if (tid < K) {
     const double k0 = s.key[tid], lam = s.h[tid][tid];
@@ -335,35 +353,40 @@ static __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const float* Vt
     s.perm[rank] = tid;
   }
   __syncthreads();
-  for (int e = tid; e < K * K; e += SM_THREADS) {
+  for (int e = tid; e < K * K; e += 64) {
     const int a = e / K, j = e - a * K;
     E[e] = (float)s.e[a][s.perm[j]];
   }
   if (tid == 0) {
-    double lam[SM_MAX];
-    for (int j = 0; j < K; ++j) lam[j] = s.h[s.perm[j]][s.perm[j]];
+    const double l0 = fabs(s.h[s.perm[0]][s.perm[0]]);
     int nd = K;
     if (tau > 0.f) {
-      const double thr = (double)tau * fabs(lam[0]);
-      int r = window < 1 ? 1 : (window > K ? K : window);
+      const double thr = (double)tau * l0;
+      const int r = window < 1 ? 1 : (window > K ? K : window);
       nd = 0;
-      if (fabs(lam[r - 1]) < thr)
-        for (int j = 0; j < K; ++j) nd += (fabs(lam[j]) > thr) ? 1 : 0;
+      if (fabs(s.h[s.perm[r - 1]][s.perm[r - 1]]) < thr)
+        for (int j = 0; j < K; ++j) nd += (fabs(s.h[s.perm[j]][s.perm[j]]) > thr) ? 1 : 0;
     }
     int np = 0;
     for (int j = 0; j < K; ++j) {
-      const bool on = j < nd;
-      const double l = lam[j];
-      lam_sorted[j] = (float)l;
-      if (ritz_user) ritz_user[j] = (float)l;
-      coef_r[j] = on ? (float)(-l) : 0.f;
-      coef_x[j] = on ? (float)((l > 0.0 ? 1.0 : (l < 0.0 ? -1.0 : 0.0)) / (double)gamma) : 0.f;
-      coef_p[j] = (on && l > 0.0) ? (float)l : 0.f;
-      if (on && l > 0.0) ++np;
+      const double l = s.h[s.perm[j]][s.perm[j]];
+      if (j < nd && l > 0.0) ++np;
     }
     *ndef = nd;
     if (ndef_user) *ndef_user = nd;
     if (npos_user) *npos_user = np;
+    s.perm[SM_MAX - 1] = nd;
+  }
+  __syncthreads();
+  const int nd = s.perm[SM_MAX - 1];
+  if (tid < K) {
+    const double l = s.h[s.perm[tid]][s.perm[tid]];
+    const bool on = tid < nd;
+    lam_sorted[tid] = (float)l;
+    if (ritz_user) ritz_user[tid] = (float)l;
+    coef_r[tid] = on ? (float)(-l) : 0.f;
+    coef_x[tid] = on ? (float)((l > 0.0 ? 1.0 : (l < 0.0 ? -1.0 : 0.0)) / (double)gamma) : 0.f;
+    coef_p[tid] = (on && l > 0.0) ? (float)l : 0.f;
   }
 }
 
