@@ -87,6 +87,7 @@ __device__ __forceinline__ void emit4(T* p, int ld, int r0, int c, const float v
 // Gram: out32 = scale32 * C (fp32, optional), out16 = bf16(scale16 * C)
 // (optional).
 struct EpiGram {
+  static constexpr bool PRE = false;
   float* out32;
   bf16_t* out16;
   float scale32, scale16;
@@ -107,6 +108,7 @@ struct EpiGram {
 // Polynomial in the Gram: out = bc * A32 + cc * C.
 template <typename TO>
 struct EpiPoly {
+  static constexpr bool PRE = false;
   const float* a32;
   TO* out;
   float bc, cc;
@@ -123,8 +125,11 @@ struct EpiPoly {
 // Iterate update: out = ac * X + C into the next padded iterate, or (final
 // step) into the caller's output: rows < rows_valid, cols < cols_valid, in
 // row-major [rows x cols] or transposed [cols x rows] with its own dtype.
+// The X values are prefetched into registers before the main loop (pre), so
+// their HBM reads overlap the products.
 template <typename TX, typename TO>
 struct EpiUpdate {
+  static constexpr bool PRE = true;
   const TX* x;
   long long xstride;
   int ldx;
@@ -136,10 +141,10 @@ struct EpiUpdate {
   int transpose_out;   // caller output is the transpose of the canonical iterate
   int rows_valid, cols_valid;
   bf16_t* out16;       // optional bf16 copy of the padded iterate (operand of the next products)
-  __device__ void operator()(int b, int r0, int c, float v[4], int mode) const {
-    const TX* xb = x + b * xstride;
+  __device__ float pre(int b, int r, int c) const { return Cvt<TX>::to_f(x[b * xstride + (long long)r * ldx + c]); }
+  __device__ void apply(int b, int r0, int c, float v[4], int mode, const float* xv) const {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) v[j] = ac * Cvt<TX>::to_f(xb[(long long)(r0 + j) * ldx + c]) + v[j];
+    for (int j = 0; j < 4; ++j) v[j] = ac * xv[j] + v[j];
     TO* ob = out + b * ostride;
     if (!final_out) {
       emit4(ob, ldo, r0, c, v, mode);
@@ -166,6 +171,7 @@ struct EpiUpdate {
 // step) the caller's output with the same rules as EpiUpdate.
 template <typename TO>
 struct EpiUpdateT {
+  static constexpr bool PRE = false;
   const float* x;
   long long xstride;
   int ldx;
@@ -203,6 +209,7 @@ struct EpiUpdateT {
 
 // Plain fp32 store of C.
 struct EpiStore {
+  static constexpr bool PRE = false;
   float* out;
   long long stride;
   int ld;
@@ -217,16 +224,21 @@ struct EpiStore {
 // STAGES = 2 double-buffers the LDS tiles (one barrier per K step); 1 keeps a
 // single LDS buffer (two barriers per K step) so that two work-groups fit on
 // a CU and one's epilogue overlaps the other's main loop.
-template <int NWM_, int NWN_, int WM_, int WN_, int STAGES_ = 2>
+// OCC: minimum waves per SIMD the register allocation must allow (0: the
+// compiler's choice for the block size).
+template <int NWM_, int NWN_, int WM_, int WN_, int STAGES_ = 2, int OCC_ = 0>
 struct GemmCfg {
   static constexpr int NWM = NWM_, NWN = NWN_, WM = WM_, WN = WN_, STAGES = STAGES_;
+  static constexpr int OCC = OCC_ ? OCC_ : (64 * NWM_ * NWN_ + 255) / 256;
   static constexpr int BM = 32 * WM * NWM, BN = 32 * WN * NWN;
   static constexpr int NT = 64 * NWM * NWN;
 };
 using CfgTile128 = GemmCfg<2, 2, 2, 2>;          // 128 x 128, 256 threads
 using CfgTile256 = GemmCfg<2, 4, 4, 2>;          // 256 x 256, 512 threads
-using CfgTile256s = GemmCfg<2, 4, 4, 2, 1>;      // 256 x 256, single LDS stage
-using CfgTile256x128 = GemmCfg<2, 2, 4, 2, 2>;   // 256 x 128, 256 threads
+// Single-stage tiles with registers capped for two work-groups per CU, so
+// that one's epilogue (HBM traffic) overlaps the other's main loop.
+using CfgTile256x128s = GemmCfg<2, 2, 4, 2, 1, 2>;   // 256 x 128, 256 threads
+using CfgTile128s = GemmCfg<2, 2, 2, 2, 1, 2>;       // 128 x 128, 256 threads
 
 __device__ __forceinline__ u32x4_t pack8(const u32x4_t& a, const u32x4_t& b) {
   return u32x4_t{pack_bf2(__uint_as_float(a[0]), __uint_as_float(a[1])),
@@ -301,15 +313,14 @@ struct NNStager<COLS, NT, bf16_t, S> {       // 64 x COLS tile, bf16 LDS
       }
     }
   }
-  // 16-bit element c (0..7) of row i of unit u
+  // 16-bit element c (0..7) of row i of unit u (bf16 source)
   __device__ __forceinline__ uint32_t half_bits(int u, int i, int c) const {
-    if constexpr (CONV) {
-      const float f = __uint_as_float(r[u * PER + 2 * i + (c >> 2)][c & 3]);
-      return (uint32_t)f2bf(f);
-    } else {
-      const uint32_t w = r[u * PER + i][c >> 1];
-      return (c & 1) ? (w >> 16) : (w & 0xffffu);
-    }
+    const uint32_t w = r[u * PER + i][c >> 1];
+    return (c & 1) ? (w >> 16) : (w & 0xffffu);
+  }
+  // fp32 element c (0..7) of row i of unit u (fp32 source)
+  __device__ __forceinline__ float elem(int u, int i, int c) const {
+    return __uint_as_float(r[u * PER + 2 * i + (c >> 2)][c & 3]);
   }
   __device__ __forceinline__ void store(char* lds) const {
     const int t = threadIdx.x;
@@ -318,8 +329,12 @@ struct NNStager<COLS, NT, bf16_t, S> {       // 64 x COLS tile, bf16 LDS
       const int id = t + NT * u, kb = id % KB, nb = id / KB;
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
-        const u32x2_t v = {half_bits(u, 0, c) | (half_bits(u, 1, c) << 16),
-                           half_bits(u, 2, c) | (half_bits(u, 3, c) << 16)};
+        u32x2_t v;
+        if constexpr (CONV) {
+          v = u32x2_t{pack_bf2(elem(u, 0, c), elem(u, 1, c)), pack_bf2(elem(u, 2, c), elem(u, 3, c))};
+        } else {
+          v = u32x2_t{half_bits(u, 0, c) | (half_bits(u, 1, c) << 16), half_bits(u, 2, c) | (half_bits(u, 3, c) << 16)};
+        }
         *reinterpret_cast<u32x2_t*>(lds + (8 * nb + c) * G_ROWB + 8 * kb) = v;
       }
     }
@@ -397,7 +412,7 @@ __device__ __forceinline__ void sym_tile(int t, int nt, int& tm, int& tn) {
 // A_KN: A is stored K x M (M contiguous) and transposed while staging, as B
 // is in NN form.
 template <typename Cfg, typename T, typename SA, typename SB, bool A_KN, bool B_NN, bool SYM, typename Epi>
-__global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const SA* __restrict__ A, const SB* __restrict__ B,
+__global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void gemm_kernel(const SA* __restrict__ A, const SB* __restrict__ B,
                                                        GemmShape sh, Epi epi) {
   constexpr int BK = GemmK<T>::BK;
   constexpr int BM = Cfg::BM, BN = Cfg::BN, NT = Cfg::NT, WM = Cfg::WM, WN = Cfg::WN;
@@ -426,6 +441,23 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const SA* __restrict__ A,
   for (int i = 0; i < WM; ++i)
 #pragma unroll
     for (int j = 0; j < WN; ++j) acc[i][j] = f32x16_t{};
+
+  const int r32 = lane & 31, h = lane >> 5;
+  // epilogue operands this lane will need, loaded before the main loop
+  constexpr bool PRE = Epi::PRE;
+  float px[PRE ? WM * WN * 16 : 1];
+  if constexpr (PRE) {
+#pragma unroll
+    for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            px[(mi * WN + ni) * 16 + 4 * i + j] =
+                epi.pre(b, m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h + j, n0 + wn * WN * 32 + ni * 32 + r32);
+  }
 
   using AStager = typename std::conditional<A_KN, NNStager<BM, NT, T, SA>, RowStager<BM, NT, T, SA>>::type;
   using BStager = typename std::conditional<B_NN, NNStager<BN, NT, T, SB>, RowStager<BN, NT, T, SB>>::type;
@@ -467,7 +499,6 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const SA* __restrict__ A,
   }
 
   const int mode = SYM ? (tm == tn ? EMIT_SYM_DIAG : EMIT_SYM_OFF) : EMIT_FULL;
-  const int r32 = lane & 31, h = lane >> 5;
 #pragma unroll
   for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
@@ -478,13 +509,14 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(const SA* __restrict__ A,
                       acc[mi][ni][4 * i + 3]};
         const int r0 = m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h;
         const int c = n0 + wn * WN * 32 + ni * 32 + r32;
-        epi(b, r0, c, v, mode);
+        if constexpr (PRE) epi.apply(b, r0, c, v, mode, &px[(mi * WN + ni) * 16 + 4 * i]);
+        else epi(b, r0, c, v, mode);
       }
 }
 
 // Host launcher (errors surface through hipGetLastError at the end of a call).
 // M, N must be multiples of the tile and K of the K step.
-template <typename Cfg, typename T, bool B_NN, bool SYM, typename SA, typename SB, typename Epi, bool A_KN = false>
+template <typename Cfg, typename T, bool B_NN, bool SYM, bool A_KN = false, typename SA, typename SB, typename Epi>
 void launch_gemm(const SA* A, const SB* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;

@@ -127,23 +127,29 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
   }
 }
 
-// nu = sqrt(sum of the residual tiles) (in tile order, float64); alpha = 1/nu
-// (0 for nu = 0) and the start coefficients c_j = -(s_j / nu - 1 / gamma) of
+// nu = sqrt(sum of the residual tiles) (float64: per-lane strided partial
+// sums, then lane 0's butterfly total); alpha = 1/nu (0 for nu = 0) and the
+// start coefficients c_j = -(s_j / nu - 1 / gamma) of
 //   X0 = alpha X + sum_j L_j c_j R_j^T  =  R / nu + gamma^-1 L R^T.
-static __global__ void muon_finalize_kernel(const float* sumsq, int tiles, const float* sv, const int* keff,
-                                     int kmax, float inv_gamma, float* alpha, float* coef_b, float* nu_dev,
-                                     float* nu_user, int batch) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= batch) return;
+// One wave per matrix.
+static __global__ __launch_bounds__(64) void muon_finalize_kernel(const float* sumsq, int tiles, const float* sv,
+                                                                  const int* keff, int kmax, float inv_gamma,
+                                                                  float* alpha, float* coef_b, float* nu_dev,
+                                                                  float* nu_user, int batch) {
+  const int b = blockIdx.x, lane = threadIdx.x;
   double acc = 0.0;
-  for (int t = 0; t < tiles; ++t) acc += (double)sumsq[(long long)b * tiles + t];
+  for (int t = lane; t < tiles; t += WAVE) acc += (double)sumsq[(long long)b * tiles + t];
+  acc = wave_sum(acc);
+  acc = __shfl(acc, 0, WAVE);
   const double nu = sqrt(acc);
   const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
-  alpha[b] = (float)inv;
-  nu_dev[b] = (float)nu;
-  if (nu_user) nu_user[b] = (float)nu;
+  if (lane == 0) {
+    alpha[b] = (float)inv;
+    nu_dev[b] = (float)nu;
+    if (nu_user) nu_user[b] = (float)nu;
+  }
   const int ke = keff ? keff[b] : 0;
-  for (int j = 0; j < kmax; ++j)
+  for (int j = lane; j < kmax; j += WAVE)
     coef_b[b * kmax + j] = j < ke ? (float)(-((double)sv[b * kmax + j] * inv - (double)inv_gamma)) : 0.f;
 }
 

@@ -97,15 +97,23 @@ static void make_plan(MsignPlan& p, int batch, int m, int n, int k, int steps, i
   p.copy_in = p.tall || p.s != p.s_pad || p.l != p.l_pad || !aligned;
 }
 
-// Iterate update X <- a X + B X: 256 x 256 tiles when the padded shape allows.
-// The X operand is the bf16 copy (bf16 path) or the fp32 iterate itself.
+// Iterate update X <- a X + B X on 128 x 128 tiles; the epilogue's X reads
+// are issued before the main loop. The X operand is the bf16 copy (bf16
+// path: single-stage LDS, two work-groups per CU) or the fp32 iterate.
 template <typename T, typename SX, typename Epi>
 static void update_gemm(const MsignPlan& p, const T* bm, const SX* xop, const GemmShape& g, const Epi& eu,
                         hipStream_t st) {
-  if (p.s_pad % 256 == 0 && p.l_pad % 256 == 0)
-    launch_gemm<CfgTile256, T, true, false>(bm, xop, g, eu, st);
-  else
-    launch_gemm<CfgTile128, T, true, false>(bm, xop, g, eu, st);
+  (void)p;
+  if constexpr (sizeof(T) == 2) launch_gemm<CfgTile128s, T, true, false>(bm, xop, g, eu, st);
+  else launch_gemm<CfgTile128, T, true, false>(bm, xop, g, eu, st);
+}
+
+// Symmetric products (Gram and A^2): 128 x 128 tiles; single-stage with two
+// work-groups per CU on the bf16 path.
+template <typename T, typename Epi>
+static void sym_gemm(const T* a, const GemmShape& g, const Epi& e, hipStream_t st) {
+  if constexpr (sizeof(T) == 2) launch_gemm<CfgTile128s, T, false, true>(a, a, g, e, st);
+  else launch_gemm<CfgTile128, T, false, true>(a, a, g, e, st);
 }
 
 template <typename T>
@@ -155,7 +163,7 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     {
       ProfScope ps(SD_STAGE_SMALL, st);
       gram_partials(p.ys, so, s_pad, p.ys, so, s_pad, rp, rp, s_pad, true, p.part, B, st);   // G G^T
-      hipLaunchKernelGGL(svd_head_kernel, dim3(B), dim3(64), 0, st, p.part, s_pad / GP_CHUNK, rp, p.k, o.tau, p.E,
+      hipLaunchKernelGGL(svd_head_kernel, dim3(B), dim3(SM_THREADS), 0, st, p.part, s_pad / GP_CHUNK, rp, p.k, o.tau, p.E,
                          p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out);
     }
     // V = G^T E / s (short side), U = Q E (long side)
@@ -191,7 +199,7 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   lowrank<T, T>(la, st);
   {
     ProfScope ps(SD_STAGE_LOWRANK, st);
-    hipLaunchKernelGGL(muon_finalize_kernel, grid1(B, 64), dim3(64), 0, st, p.sumsq, p.tiles, p.sv,
+    hipLaunchKernelGGL(muon_finalize_kernel, dim3(B), dim3(64), 0, st, p.sumsq, p.tiles, p.sv,
                        p.k > 0 ? p.keff : nullptr, la.kmax, 1.f / o.gamma, p.alpha, p.coefB, p.nu, o.nu_out, B);
   }
   la.coef = p.coefB;
@@ -237,14 +245,14 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     }
     {
       ProfScope ps(SD_STAGE_NS_GRAM, st);
-      launch_gemm<CfgTile128, T, false, true>(xop(), xop(), g1, eg, st);
+      sym_gemm<T>(xop(), g1, eg, st);
     }
     if (c != 0.f) {
       GemmShape g2{p.s_pad, p.s_pad, p.s_pad, p.s_pad, p.s_pad, ss, ss, B};
       EpiPoly<T> ep{p.a32, bm, b, c, ss, p.s_pad};
       const T* aop = BF ? reinterpret_cast<const T*>(p.a16) : reinterpret_cast<const T*>(p.a32);
       ProfScope ps(SD_STAGE_NS_POLY, st);
-      launch_gemm<CfgTile128, T, false, true>(aop, aop, g2, ep, st);
+      sym_gemm<T>(aop, g2, ep, st);
     }
     GemmShape g3{p.s_pad, p.l_pad, p.s_pad, p.s_pad, p.l_pad, ss, sl, B};
     const bool last = t + 1 == p.steps;

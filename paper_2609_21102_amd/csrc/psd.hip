@@ -309,7 +309,7 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     {
       ProfScope ps(SD_STAGE_SMALL, st);
       gram_partials(vt, 0, np, zt, 0, np, K, K, np, false, p.part, 1, st);   // V^T (Z V)
-      hipLaunchKernelGGL(ritz_kernel, dim3(1), dim3(64), 0, st, p.part, np / GP_CHUNK, K, o.tau, o.window, o.gamma,
+      hipLaunchKernelGGL(ritz_kernel, dim3(1), dim3(SM_THREADS), 0, st, p.part, np / GP_CHUNK, K, o.tau, o.window, o.gamma,
                          p.E, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out, o.n_deflated_out,
                          o.n_positive_out);
     }

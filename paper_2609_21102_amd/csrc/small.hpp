@@ -21,19 +21,27 @@ constexpr int SM_LD = SM_MAX + 1;
 struct SmallLds {
   double h[SM_MAX][SM_LD];
   double e[SM_MAX][SM_LD];
-  double rot_c[SM_MAX / 2], rot_s[SM_MAX / 2];
-  int rot_i[SM_MAX / 2], rot_j[SM_MAX / 2];
+  double h2[SM_MAX][SM_LD];       // second buffers: a Jacobi round reads one
+  double e2[SM_MAX][SM_LD];       // pair of buffers and writes the other
+  double rot_c[SM_MAX], rot_d[SM_MAX];   // per index: coefficient on itself / on its partner
+  int rot_p[SM_MAX];              // per index: partner in this round
+  int rot_z[SM_MAX];              // per index: its pair is annihilated this round
   double red[SM_THREADS / WAVE];
   double key[SM_MAX];
   int perm[SM_MAX];
+  int rotated;                    // a rotation was applied in this sweep
 };
 
 // ------------------------------------------------------------- Jacobi -----
 // Eigendecomposition of the symmetric n x n matrix in s.h. On return the
 // eigenvalues are on the diagonal of s.h and s.e holds the eigenvectors as
-// columns. Rotations (Golub & Van Loan, sym.schur2) are applied for n/2
-// disjoint pairs at a time (circle-method ordering); sweeps stop when the
-// off-diagonal mass is below 1e-30 of the total, or after 60 sweeps.
+// columns. Each round rotates n/2 disjoint pairs (circle-method ordering;
+// rotation angles as in Golub & Van Loan, sym.schur2) and applies all of them
+// in one pass: with R the round's rotation, H' = R^T H R and E' = E R are
+// written entry by entry into the second buffers, the annihilated pairs as
+// exact zeros. A pair is skipped when |h_ij| <= 2^-50 sqrt(|h_ii h_jj|) or
+// |h_ij| <= 2^-48 ||H||_F (below what the rounding of the rotations leaves
+// behind); sweeps stop after one that rotates nothing, or after 40.
 static __device__ void jacobi_eig(SmallLds& s, int n) {
   const int tid = threadIdx.x, nt = blockDim.x;
   for (int e = tid; e < n * n; e += nt) {
@@ -44,68 +52,81 @@ static __device__ void jacobi_eig(SmallLds& s, int n) {
   if (n <= 1) return;
   const int N = n + (n & 1);
   const int half = N / 2;
-  for (int sweep = 0; sweep < 60; ++sweep) {
-    double off = 0.0, tot = 0.0;
-    for (int e = tid; e < n * n; e += nt) {
-      const int i = e / n, j = e - i * n;
-      const double v = s.h[i][j] * s.h[i][j];
-      tot += v;
-      if (i != j) off += v;
-    }
-    off = block_sum(off, s.red);
-    tot = block_sum(tot, s.red);
-    if (off <= 1e-30 * tot) break;
+  double fro = 0.0;
+  for (int e = tid; e < n * n; e += nt) fro += s.h[e / n][e % n] * s.h[e / n][e % n];
+  fro = block_sum(fro, s.red);
+  const double abs_floor = 0x1p-48 * sqrt(fro);
+  double(*H)[SM_LD] = s.h;
+  double(*E)[SM_LD] = s.e;
+  double(*H2)[SM_LD] = s.h2;
+  double(*E2)[SM_LD] = s.e2;
+  for (int sweep = 0; sweep < 40; ++sweep) {
+    if (tid == 0) s.rotated = 0;
+    __syncthreads();
     for (int r = 0; r < N - 1; ++r) {
       if (tid < half) {
         const int pa = (tid == 0) ? 0 : ((r + tid - 1) % (N - 1)) + 1;
         const int pb = ((r + N - 2 - tid) % (N - 1)) + 1;
-        int i = pa < pb ? pa : pb, j = pa < pb ? pb : pa;
-        double c = 1.0, sn = 0.0;
+        const int i = pa < pb ? pa : pb, j = pa < pb ? pb : pa;
         if (j < n) {
-          const double aij = s.h[i][j];
-          if (aij != 0.0) {
-            const double tau = (s.h[j][j] - s.h[i][i]) / (2.0 * aij);
+          double c = 1.0, sn = 0.0;
+          int rot = 0;
+          const double aij = H[i][j], aii = H[i][i], ajj = H[j][j];
+          if (fabs(aij) > 0x1p-50 * sqrt(fabs(aii) * fabs(ajj)) && fabs(aij) > abs_floor) {
+            const double tau = (ajj - aii) / (2.0 * aij);
             double t;
             if (fabs(tau) > 1e150) t = 0.5 / tau;
             else t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
             c = 1.0 / sqrt(1.0 + t * t);
             sn = t * c;
+            rot = 1;
+            s.rotated = 1;
           }
-        } else {
-          i = j = -1;
+          // column i <- c col_i - s col_j ; column j <- s col_i + c col_j
+          s.rot_p[i] = j;
+          s.rot_c[i] = c;
+          s.rot_d[i] = -sn;
+          s.rot_z[i] = rot;
+          s.rot_p[j] = i;
+          s.rot_c[j] = c;
+          s.rot_d[j] = sn;
+          s.rot_z[j] = rot;
+        } else if (i < n) {   // paired with the padding index: unchanged
+          s.rot_p[i] = i;
+          s.rot_c[i] = 1.0;
+          s.rot_d[i] = 0.0;
+          s.rot_z[i] = 0;
         }
-        s.rot_i[tid] = i;
-        s.rot_j[tid] = j;
-        s.rot_c[tid] = c;
-        s.rot_s[tid] = sn;
       }
       __syncthreads();
-      // columns: H <- H J, E <- E J
-      for (int e = tid; e < n * half; e += nt) {
-        const int row = e / half, p = e - row * half;
-        const int i = s.rot_i[p], j = s.rot_j[p];
-        if (i < 0) continue;
-        const double c = s.rot_c[p], sn = s.rot_s[p];
-        const double hi = s.h[row][i], hj = s.h[row][j];
-        s.h[row][i] = c * hi - sn * hj;
-        s.h[row][j] = sn * hi + c * hj;
-        const double ei = s.e[row][i], ej = s.e[row][j];
-        s.e[row][i] = c * ei - sn * ej;
-        s.e[row][j] = sn * ei + c * ej;
+      for (int e = tid; e < n * n; e += nt) {
+        const int a = e / n, b = e - a * n;
+        const int qa = s.rot_p[a], qb = s.rot_p[b];
+        const double ca = s.rot_c[a], da = s.rot_d[a], cb = s.rot_c[b], db = s.rot_d[b];
+        double v = ca * (cb * H[a][b] + db * H[a][qb]) + da * (cb * H[qa][b] + db * H[qa][qb]);
+        if (s.rot_z[a] && b == qa) v = 0.0;
+        H2[a][b] = v;
+        E2[a][b] = cb * E[a][b] + db * E[a][qb];
       }
       __syncthreads();
-      // rows: H <- J^T H
-      for (int e = tid; e < n * half; e += nt) {
-        const int col = e / half, p = e - col * half;
-        const int i = s.rot_i[p], j = s.rot_j[p];
-        if (i < 0) continue;
-        const double c = s.rot_c[p], sn = s.rot_s[p];
-        const double hi = s.h[i][col], hj = s.h[j][col];
-        s.h[i][col] = c * hi - sn * hj;
-        s.h[j][col] = sn * hi + c * hj;
-      }
-      __syncthreads();
+      double(*t)[SM_LD] = H;
+      H = H2;
+      H2 = t;
+      t = E;
+      E = E2;
+      E2 = t;
     }
+    const int any = s.rotated;
+    __syncthreads();
+    if (!any) break;
+  }
+  if (H != s.h) {
+    for (int e = tid; e < n * n; e += nt) {
+      const int a = e / n, b = e - a * n;
+      s.h[a][b] = H[a][b];
+      s.e[a][b] = E[a][b];
+    }
+    __syncthreads();
   }
 }
 
@@ -184,11 +205,20 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const float* A, long 
 }
 
 // s.h[a][bb] = sum of the chunk partials in chunk order (mirrored when sym).
+// Loads are issued eight chunks at a time; the additions keep chunk order.
 static __device__ void gram_reduce(SmallLds& s, const double* part, int nch, int ca, int cb, bool sym) {
   const int items = gram_items(ca, cb, sym);
   for (int p = threadIdx.x; p < items; p += blockDim.x) {
     double t = 0.0;
-    for (int c = 0; c < nch; ++c) t += part[(long long)c * items + p];
+    int c = 0;
+    for (; c + 8 <= nch; c += 8) {
+      double v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = part[(long long)(c + u) * items + p];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) t += v[u];
+    }
+    for (; c < nch; ++c) t += part[(long long)c * items + p];
     int a, bb;
     gram_item(p, ca, cb, sym, a, bb);
     s.h[a][bb] = t;
@@ -275,8 +305,8 @@ __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp
 // the eigenvalues decreasingly, and emit for the leading k: singular values,
 // the eigenvector matrix E (rp x k), 1/s (0 for s = 0), and the deflation
 // rank (fixed k, or the gate of Alg. 1 when tau > 0) with the subtraction
-// coefficients -s_j used by the residual pass. One wave per matrix.
-static __global__ __launch_bounds__(64) void svd_head_kernel(const double* part, int nch, int rp, int k, float tau,
+// coefficients -s_j used by the residual pass. One work-group per matrix.
+static __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part, int nch, int rp, int k, float tau,
                                                              float* E, float* sv, float* inv_sv, int* keff,
                                                              float* coef_a, float* s_user, int* keff_user) {
   __shared__ SmallLds s;
@@ -286,7 +316,7 @@ static __global__ __launch_bounds__(64) void svd_head_kernel(const double* part,
   if (tid < rp) s.key[tid] = s.h[tid][tid];
   __syncthreads();
   sort_desc(s, rp);
-  for (int e = tid; e < rp * k; e += 64) {
+  for (int e = tid; e < rp * k; e += SM_THREADS) {
     const int a = e / k, j = e - a * k;
     E[(long long)b * rp * k + e] = (float)s.e[a][s.perm[j]];
   }
@@ -323,15 +353,15 @@ static __global__ __launch_bounds__(64) void svd_head_kernel(const double* part,
 // Ritz pairs ordered by |lam| descending (ties: larger lam, then lower index).
 // Deflated set I: all K (tau = 0) or the gate of Alg. 2 on the magnitudes.
 // Coefficients for the residual (-lam), the padded start (sign(lam) / gamma)
-// and the restore (max(lam, 0)). One wave.
-static __global__ __launch_bounds__(64) void ritz_kernel(const double* part, int nch, int K, float tau, int window,
+// and the restore (max(lam, 0)). One work-group.
+static __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const double* part, int nch, int K, float tau, int window,
                                                          float gamma, float* E, float* lam_sorted, int* ndef,
                                                          float* coef_r, float* coef_x, float* coef_p,
                                                          float* ritz_user, int* ndef_user, int* npos_user) {
   __shared__ SmallLds s;
   const int tid = threadIdx.x;
   gram_reduce(s, part, nch, K, K, false);
-  for (int e = tid; e < K * K; e += 64) {
+  for (int e = tid; e < K * K; e += SM_THREADS) {
     const int i = e / K, j = e - i * K;
     if (i < j) {
       const double v = 0.5 * (s.h[i][j] + s.h[j][i]);
@@ -353,7 +383,7 @@ static __global__ __launch_bounds__(64) void ritz_kernel(const double* part, int
     s.perm[rank] = tid;
   }
   __syncthreads();
-  for (int e = tid; e < K * K; e += 64) {
+  for (int e = tid; e < K * K; e += SM_THREADS) {
     const int a = e / K, j = e - a * K;
     E[e] = (float)s.e[a][s.perm[j]];
   }
