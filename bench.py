@@ -10,12 +10,18 @@ seeded and synthetic and are resident in HBM before the timed region.
 
 Prints one JSON line: matrices/s (value), the achieved TFLOP/s against the
 bf16 MFMA peak, a roofline entry for the dominant kernel (the iterate update
-X <- a X + B X, timed with HIP events inside the timed region) and the CPU
-oracle timed on a bounded sample of the same workload.
+X <- a X + B X, timed with HIP events inside the timed region; its
+arithmetic intensity, about 120 flop per byte, is below the bf16 ridge of
+about 310, so it is priced against HBM) and the CPU oracle timed on a bounded
+sample of the same workload.
+
+--copy-calibration adds one plain device copy of 256 MiB before the timed
+region, the reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -47,26 +53,72 @@ def front_flops_per_matrix(s: int, l: int, k: int, rp: int, power_iters: int) ->
     return (2 + 2 * power_iters) * 2.0 * s * l * rp + 2 * 2.0 * s * l * k
 
 
+def update_bytes_per_matrix(s: int, l: int, steps: int) -> float:
+    """Algorithmic HBM bytes of the iterate updates of one s x l matrix,
+    averaged over the call's launches: every step reads B (bf16, s x s), the
+    fp32 iterate and its bf16 copy (s x l); the first steps - 1 write the next
+    fp32 iterate and its bf16 copy, the last writes the bf16 output."""
+    inner = 2.0 * s * s + (4 + 2) * s * l + (4 + 2) * s * l
+    last = 2.0 * s * s + (4 + 2) * s * l + 2 * s * l
+    return ((steps - 1) * inner + last) / steps
+
+
+KERNEL_SOURCES = ("gemm.hpp", "common.hpp", "msign.hip")
+
+
+def kernel_hash() -> str:
+    """Hash of the sources the update kernel is built from."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2609_21102_amd", "csrc")
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(csrc, name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per update launch from the committed counter summary, or
+    None when the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", "ns_update_768x3072_bf16_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_hash") != kernel_hash():
+        return None
+    try:
+        return float(vals["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(case, seconds: float) -> dict:
+    """The oracle (bf16-contract mode, float64) on whole matrices of the same
+    workload, cycling through the batch until `seconds` have passed."""
     from threadpoolctl import threadpool_info
     from oracle import muon as omuon
     from oracle import rng as orng
+    b = case.x.shape[0]
     s = min(case.x.shape[1:])
     rp = min(s, case.k + case.oversample)
     threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
     done, t0 = 0, time.perf_counter()
-    while done < case.x.shape[0]:
-        x64 = case.x64[done:done + 1]
-        omuon.msign_deflated(x64, case.k, case.coeffs, oversample=case.oversample,
+    while True:
+        idx = done % b
+        omuon.msign_deflated(case.x64[idx:idx + 1], case.k, case.coeffs, oversample=case.oversample,
                              power_iters=case.power_iters, gamma=case.gamma, mode="bf16",
-                             sketches=[orng.sketch(0, done, s, rp)])
+                             sketches=[orng.sketch(0, idx, s, rp)])
         done += 1
         if time.perf_counter() - t0 >= seconds:
             break
     dt = time.perf_counter() - t0
     return {"value": done / dt, "unit": "matrices/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} of {case.x.shape[0]} matrices 768x3072, float64 oracle in bf16-contract "
-                      f"mode, {dt:.1f} s"}
+            "sample": f"{done} matrices 768x3072 (cycling through the batch of {b}), float64 oracle in "
+                      f"bf16-contract mode, {dt:.1f} s"}
 
 
 def main() -> int:
@@ -74,9 +126,11 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--baseline", action="store_true", help="time the undeflated filter (k = 0) instead")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one plain 256 MiB device copy before timing (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         log("bench.py: this build runs on a single GPU; --gpus must be 1 "
@@ -104,6 +158,12 @@ def main() -> int:
                  gamma=case.gamma, out=out, workspace=ws)
 
     log(f"bench: {b} x {m} x {n} bf16, k={k}, warmup {args.warmup}, steps {args.steps}")
+    if args.copy_calibration:
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -126,10 +186,13 @@ def main() -> int:
                                                           if k else 0.0))
     tflops = flops / (ms_per_step / 1e3) / 1e12
     upd_flops = 2.0 * s * s * l * b
+    upd_bytes = update_bytes_per_matrix(s, l, case.steps) * b
     upd_avg_ms = upd_ms / max(upd_n, 1)
     upd_tflops = upd_flops / (upd_avg_ms / 1e3) / 1e12
+    upd_gbs = upd_bytes / (upd_avg_ms / 1e3) / 1e9
     log(f"bench: {ms_per_step:.3f} ms/step, {value:.0f} matrices/s, {tflops:.1f} TFLOP/s; "
-        f"update kernel {upd_avg_ms * 1e3:.1f} us avg over {upd_n} launches ({upd_tflops:.1f} TFLOP/s)")
+        f"update kernel {upd_avg_ms * 1e3:.1f} us avg over {upd_n} launches "
+        f"({upd_gbs:.0f} GB/s algorithmic, {upd_tflops:.1f} TFLOP/s)")
 
     result = {
         "metric": "deflated msign matrices/s + TFLOP/s (% MFMA peak), batched 768x3072 bf16",
@@ -149,10 +212,12 @@ def main() -> int:
                    "batch": b, "m": m, "n": n, "k": k, "steps": case.steps, "parallelism": "single GPU"},
         "tflops": tflops,
         "mfma_frac": tflops / MFMA_BF16_PEAK_TFLOPS,
-        "roofline": {"bound": "mfma", "kernel": "gemm_kernel<bf16, NN> (X <- a X + B X)",
-                     "achieved": upd_tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                     "frac": upd_tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": None,
-                     "avg_launch_us": upd_avg_ms * 1e3, "flops_per_launch": upd_flops},
+        "roofline": {"bound": "hbm", "kernel": "iterate update X <- a X + B X (gemm_kernel, EpiUpdate)",
+                     "achieved": upd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": upd_gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
+                     "bytes_per_launch": upd_bytes, "avg_launch_us": upd_avg_ms * 1e3,
+                     "launches": upd_n, "tflops": upd_tflops,
+                     "mfma_frac": upd_tflops / MFMA_BF16_PEAK_TFLOPS, "kernel_hash": kernel_hash()},
     }
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")

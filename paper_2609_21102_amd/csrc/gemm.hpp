@@ -41,6 +41,11 @@ struct GemmShape {
   int lda, ldb;
   long long sa, sb;   // batch strides in elements
   int batch;
+  // Tile order (non-symmetric): 0 walks tile columns fastest, 1 tile rows
+  // fastest. With few tile rows and a small A, rows-fastest makes the
+  // work-groups that share a B column panel run together on one XCD, so the
+  // panel comes from HBM once and from L2 after that.
+  int m_fast = 0;
 };
 
 enum { EMIT_FULL = 0, EMIT_SYM_OFF = 1, EMIT_SYM_DIAG = 2 };
@@ -426,6 +431,9 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_
   int t = lid - b * per, tm, tn;
   if (SYM) {
     sym_tile(t, tiles_m, tm, tn);
+  } else if (sh.m_fast) {
+    tn = t / tiles_m;
+    tm = t - tn * tiles_m;
   } else {
     tm = t / tiles_n;
     tn = t - tm * tiles_n;

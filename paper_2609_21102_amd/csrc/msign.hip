@@ -254,7 +254,7 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
       ProfScope ps(SD_STAGE_NS_POLY, st);
       sym_gemm<T>(aop, g2, ep, st);
     }
-    GemmShape g3{p.s_pad, p.l_pad, p.s_pad, p.s_pad, p.l_pad, ss, sl, B};
+    GemmShape g3{p.s_pad, p.l_pad, p.s_pad, p.s_pad, p.l_pad, ss, sl, B, 1};
     const bool last = t + 1 == p.steps;
     if (!last) {
       EpiUpdate<float, float> eu{};

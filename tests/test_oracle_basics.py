@@ -28,6 +28,26 @@ def test_bf16_matches_library_rounding():
 
 
 # --- Gaussian generator ------------------------------------------------------------
+# Known-answer vectors of Philox4x32-10 published with the generator
+# (Salmon, Moraes, Dror, Shaw, SC 2011; Random123 distribution): counter,
+# key -> output, all words as 32-bit integers.
+PHILOX_KAT = [
+    ((0x00000000, 0x00000000, 0x00000000, 0x00000000), (0x00000000, 0x00000000),
+     (0x6627E8D5, 0xE169C58D, 0xBC57AC4C, 0x9B00DBD8)),
+    ((0xFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF, 0xFFFFFFFF), (0xFFFFFFFF, 0xFFFFFFFF),
+     (0x408F276D, 0x41C83B0E, 0xA20BC7C6, 0x6D5451FD)),
+    ((0x243F6A88, 0x85A308D3, 0x13198A2E, 0x03707344), (0xA4093822, 0x299F31D0),
+     (0xD16CFE09, 0x94FDCCEB, 0x5001E420, 0x24126EA1)),
+]
+
+
+@pytest.mark.parametrize("ctr,key,want", PHILOX_KAT)
+def test_philox_known_answers(ctr, key, want):
+    args = [np.array([v], dtype=np.uint32) for v in (*ctr, *key)]
+    got = [int(np.asarray(w).ravel()[0]) for w in rng.philox4x32_10(*args)]
+    assert got == list(want)
+
+
 def test_gaussians_are_standard_normal():
     z = rng.gaussians(0, 0, rng.STREAM_SKETCH, 200000)
     assert abs(z.mean()) < 0.01 and abs(z.var() - 1) < 0.01
