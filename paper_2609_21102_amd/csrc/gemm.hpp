@@ -244,6 +244,8 @@ using CfgTile256 = GemmCfg<2, 4, 4, 2>;          // 256 x 256, 512 threads
 // that one's epilogue (HBM traffic) overlaps the other's main loop.
 using CfgTile256x128s = GemmCfg<2, 2, 4, 2, 1, 2>;   // 256 x 128, 256 threads
 using CfgTile128s = GemmCfg<2, 2, 2, 2, 1, 2>;       // 128 x 128, 256 threads
+// Direct-to-LDS kernel: 128 x 128, two-stage ring, two work-groups per CU.
+using CfgDma128 = GemmCfg<2, 2, 2, 2, 2, 2>;
 
 __device__ __forceinline__ u32x4_t pack8(const u32x4_t& a, const u32x4_t& b) {
   return u32x4_t{pack_bf2(__uint_as_float(a[0]), __uint_as_float(a[1])),
@@ -520,6 +522,225 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_
         if constexpr (PRE) epi.apply(b, r0, c, v, mode, &px[(mi * WN + ni) * 16 + 4 * i]);
         else epi(b, r0, c, v, mode);
       }
+}
+
+// ------------------------------------------- bf16, direct-to-LDS loads -----
+// gemm_dma_kernel: bf16 operands only. Tiles move from global memory into a
+// ring of STAGES LDS buffers by global_load_lds_dwordx4 (no registers on
+// the way), so STAGES - 1 K steps are in flight while one is multiplied;
+// one barrier per K step.
+//
+// LDS layouts (BK = 64, 16-byte chunks of 8 bf16):
+//   row form (A, and B in NT form): row r holds K in 8 chunks; logical chunk
+//     c sits in slot c ^ ((r >> 1) & 7), so 16 consecutive rows read at one
+//     logical chunk hit 16 distinct 16-byte bank groups.
+//   NN form (B, K x N in memory): row k holds BN columns; chunk c (columns
+//     8c..8c+7) sits in slot c ^ (2 (k & 3)). MFMA fragments are read with
+//     the gfx950 LDS transpose read (ds_read_b64_tr_b16): a group of 16 lanes
+//     whose lane i addresses row k0 + i / 4, columns n0 + 4 (i % 4) .. +3
+//     receives in lane j the four values (k0 .. k0 + 3, n0 + j).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) bf16x4_t* lds_bf16x4_ptr;
+
+__device__ __forceinline__ u32x2_t lds_read_tr16(const char* p) {
+  lds_bf16x4_ptr q = (lds_bf16x4_ptr)(p);
+  return __builtin_bit_cast(u32x2_t, __builtin_amdgcn_ds_read_tr16_b64_v4bf16(q));
+}
+
+// 16 bytes per lane from global memory straight into LDS at base + 16 lane
+// (base wave-uniform).
+__device__ __forceinline__ void lds_dma16(const bf16_t* g, char* base) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(base), 16, 0, 0);
+}
+
+__device__ __forceinline__ int rowform_slot(int r, int c) { return c ^ ((r >> 1) & 7); }
+__device__ __forceinline__ int nnform_slot(int k, int c) { return c ^ (2 * (k & 3)); }
+
+template <int WM, int WN, int BN, bool B_NN>
+__device__ __forceinline__ void tile_mma_dma(const char* la, const char* lb, f32x16_t (&acc)[WM][WN], int wm,
+                                             int wn, int lane) {
+  const int r32 = lane & 31, h = lane >> 5;
+  const int q = lane >> 4, j = lane & 15;
+#pragma unroll
+  for (int g = 0; g < 4; ++g) {
+    u32x4_t a[WM], b[WN];
+    const int c = 2 * g + h;
+#pragma unroll
+    for (int i = 0; i < WM; ++i) {
+      const int row = wm * WM * 32 + i * 32 + r32;
+      a[i] = ld16(la + row * 128 + (rowform_slot(row, c) << 4));
+    }
+    if constexpr (!B_NN) {
+#pragma unroll
+      for (int i = 0; i < WN; ++i) {
+        const int row = wn * WN * 32 + i * 32 + r32;
+        b[i] = ld16(lb + row * 128 + (rowform_slot(row, c) << 4));
+      }
+    } else {
+      const int k0 = 8 * (2 * g + (q >> 1)) + (j >> 2);
+#pragma unroll
+      for (int i = 0; i < WN; ++i) {
+        const int col = wn * WN * 32 + i * 32 + 16 * (q & 1) + 4 * (j & 3);
+        const int off = ((col & 7) << 1);
+        const u32x2_t lo = lds_read_tr16(lb + k0 * (2 * BN) + (nnform_slot(k0, col >> 3) << 4) + off);
+        const u32x2_t hi = lds_read_tr16(lb + (k0 + 4) * (2 * BN) + (nnform_slot(k0 + 4, col >> 3) << 4) + off);
+        b[i] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+      }
+    }
+#pragma unroll
+    for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < WN; ++ni) acc[mi][ni] = mfma32_bf16(a[mi], b[ni], acc[mi][ni]);
+  }
+}
+
+template <typename Cfg, bool B_NN, bool SYM, typename Epi>
+__global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void
+gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, GemmShape sh, Epi epi) {
+  constexpr int BK = 64;
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, WM = Cfg::WM, WN = Cfg::WN, S = Cfg::STAGES;
+  constexpr int NW = Cfg::NWM * Cfg::NWN;
+  constexpr int A_BYTES = BM * 128, STAGE = (BM + BN) * 128;
+  constexpr int LA = BM / 8 / NW;          // A load instructions per wave per stage (8 rows each)
+  constexpr int LB = BN / 8 / NW;          // B: NT 8 rows each; NN 1 KB = 512 / BN rows each
+  constexpr int LT = LA + LB;
+  static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile rows per wave");
+  static_assert(S >= 2 && LT * (S - 2) < 64, "stages");
+  static_assert(!SYM || BM == BN, "symmetric tiling needs square tiles");
+  __shared__ __attribute__((aligned(1024))) char lds[S * STAGE];
+
+  const int tiles_m = sh.M / BM, tiles_n = sh.N / BN;
+  const int per = SYM ? tiles_m * (tiles_m + 1) / 2 : tiles_m * tiles_n;
+  const int lid = xcd_remap(blockIdx.x, per * sh.batch);
+  const int b = lid / per;
+  int t = lid - b * per, tm, tn;
+  if (SYM) {
+    sym_tile(t, tiles_m, tm, tn);
+  } else if (sh.m_fast) {
+    tn = t / tiles_m;
+    tm = t - tn * tiles_m;
+  } else {
+    tm = t / tiles_n;
+    tn = t - tm * tiles_n;
+  }
+  const int m0 = tm * BM, n0 = tn * BN;
+  const int wave = threadIdx.x / WAVE, lane = threadIdx.x & (WAVE - 1);
+  const int wm = wave / Cfg::NWN, wn = wave % Cfg::NWN;
+  const int r32 = lane & 31, h = lane >> 5;
+
+  constexpr bool PRE = Epi::PRE;
+  float px[PRE ? WM * WN * 16 : 1];
+  if constexpr (PRE) {
+#pragma unroll
+    for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            px[(mi * WN + ni) * 16 + 4 * i + jj] =
+                epi.pre(b, m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h + jj, n0 + wn * WN * 32 + ni * 32 + r32);
+  }
+
+  // per-lane global sources (at k = 0) and wave-uniform LDS offsets
+  const bf16_t* ga[LA];
+  int la_off[LA];
+#pragma unroll
+  for (int u = 0; u < LA; ++u) {
+    const int qi = wave + NW * u;
+    const int row = 8 * qi + (lane >> 3);
+    const int ch = rowform_slot(row, lane & 7);   // slot -> logical chunk (xor is its own inverse)
+    ga[u] = A + b * sh.sa + (long long)(m0 + row) * sh.lda + 8 * ch;
+    la_off[u] = 1024 * qi;
+  }
+  const bf16_t* gb[LB];
+  int lb_off[LB];
+#pragma unroll
+  for (int u = 0; u < LB; ++u) {
+    const int qi = wave + NW * u;
+    if constexpr (!B_NN) {
+      const int row = 8 * qi + (lane >> 3);
+      const int ch = rowform_slot(row, lane & 7);
+      gb[u] = B + b * sh.sb + (long long)(n0 + row) * sh.ldb + 8 * ch;
+    } else {
+      constexpr int CPR = BN / 8;            // chunks per LDS row
+      constexpr int RPI = 64 / CPR;          // rows per load instruction
+      const int k = RPI * qi + lane / CPR;
+      const int ch = nnform_slot(k, lane % CPR);
+      gb[u] = B + b * sh.sb + (long long)k * sh.ldb + n0 + 8 * ch;
+    }
+    lb_off[u] = A_BYTES + 1024 * qi;
+  }
+  const long long a_step = BK, b_step = B_NN ? (long long)BK * sh.ldb : (long long)BK;
+
+  auto issue = [&](int slot, int kt) {
+    char* base = lds + slot * STAGE;
+#pragma unroll
+    for (int u = 0; u < LA; ++u) lds_dma16(ga[u] + kt * a_step, base + la_off[u]);
+#pragma unroll
+    for (int u = 0; u < LB; ++u) lds_dma16(gb[u] + kt * b_step, base + lb_off[u]);
+  };
+
+  f32x16_t acc[WM][WN];
+#pragma unroll
+  for (int i = 0; i < WM; ++i)
+#pragma unroll
+    for (int jj = 0; jj < WN; ++jj) acc[i][jj] = f32x16_t{};
+
+  const int nk = sh.K / BK;
+#pragma unroll
+  for (int s0 = 0; s0 < S - 1; ++s0)
+    if (s0 < nk) issue(s0, s0);
+  for (int kt = 0; kt < nk; ++kt) {
+    // stage kt has landed once at most the later stages' loads are pending
+    const int later = nk - 1 - kt < S - 2 ? nk - 1 - kt : S - 2;
+    if constexpr (S >= 4) {
+      if (later >= 2) wait_vmcnt<LT * 2>();
+      else if (later == 1) wait_vmcnt<LT>();
+      else wait_vmcnt<0>();
+    } else if constexpr (S == 3) {
+      if (later >= 1) wait_vmcnt<LT>();
+      else wait_vmcnt<0>();
+    } else {
+      wait_vmcnt<0>();
+    }
+    __builtin_amdgcn_s_barrier();
+    if (kt + S - 1 < nk) issue((kt + S - 1) % S, kt + S - 1);
+    const char* base = lds + (kt % S) * STAGE;
+    tile_mma_dma<WM, WN, BN, B_NN>(base, base + A_BYTES, acc, wm, wn, lane);
+  }
+
+  const int mode = SYM ? (tm == tn ? EMIT_SYM_DIAG : EMIT_SYM_OFF) : EMIT_FULL;
+#pragma unroll
+  for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float v[4] = {acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2],
+                      acc[mi][ni][4 * i + 3]};
+        const int r0 = m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h;
+        const int c = n0 + wn * WN * 32 + ni * 32 + r32;
+        if constexpr (PRE) epi.apply(b, r0, c, v, mode, &px[(mi * WN + ni) * 16 + 4 * i]);
+        else epi(b, r0, c, v, mode);
+      }
+}
+
+template <typename Cfg, bool B_NN, bool SYM, typename Epi>
+void launch_gemm_dma(const bf16_t* A, const bf16_t* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
+  const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
+  const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;
+  const long long blocks = per * sh.batch;
+  if (blocks <= 0) return;
+  hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi>), dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A, B,
+                     sh, epi);
 }
 
 // Host launcher (errors surface through hipGetLastError at the end of a call).

@@ -98,21 +98,22 @@ static void make_plan(MsignPlan& p, int batch, int m, int n, int k, int steps, i
 }
 
 // Iterate update X <- a X + B X on 128 x 128 tiles; the epilogue's X reads
-// are issued before the main loop. The X operand is the bf16 copy (bf16
-// path: single-stage LDS, two work-groups per CU) or the fp32 iterate.
+// are issued before the main loop. bf16 path: operand tiles move into a
+// two-stage LDS ring by direct-to-LDS loads, two work-groups per CU; fp32
+// path: register-staged tiles.
 template <typename T, typename SX, typename Epi>
 static void update_gemm(const MsignPlan& p, const T* bm, const SX* xop, const GemmShape& g, const Epi& eu,
                         hipStream_t st) {
   (void)p;
-  if constexpr (sizeof(T) == 2) launch_gemm<CfgTile128s, T, true, false>(bm, xop, g, eu, st);
+  if constexpr (sizeof(T) == 2) launch_gemm_dma<CfgDma128, true, false>(bm, xop, g, eu, st);
   else launch_gemm<CfgTile128, T, true, false>(bm, xop, g, eu, st);
 }
 
-// Symmetric products (Gram and A^2): 128 x 128 tiles; single-stage with two
-// work-groups per CU on the bf16 path.
+// Symmetric products (Gram and A^2) on 128 x 128 tiles, upper-triangle tiles
+// only; direct-to-LDS loads on the bf16 path.
 template <typename T, typename Epi>
 static void sym_gemm(const T* a, const GemmShape& g, const Epi& e, hipStream_t st) {
-  if constexpr (sizeof(T) == 2) launch_gemm<CfgTile128s, T, false, true>(a, a, g, e, st);
+  if constexpr (sizeof(T) == 2) launch_gemm_dma<CfgDma128, false, true>(a, a, g, e, st);
   else launch_gemm<CfgTile128, T, false, true>(a, a, g, e, st);
 }
 
