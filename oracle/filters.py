@@ -14,10 +14,13 @@
 
 bf16 contract (mode "bf16"), used for the bf16 library paths ("bfloat16
 mixed precision" of Sec. 3: bf16 operands, wider accumulation and state): the
-iterate X stays wide; every matrix product takes bf16-rounded operands, so
-G = bf16(X)^T bf16(X); the operand of G^2 is bf16(G); B = bf16(b G + c G^2)
-(with the unrounded G) is a product operand; the new iterate a X + bf16(X) B
-is not rounded.
+iterate is stored as a pair of bf16 numbers, hi = bf16(X) and
+lo = bf16(X - hi), and carried as hi + lo (about 16 significant bits); every
+matrix product takes bf16 operands, the iterate's being hi, so
+G = hi^T hi; the operand of G^2 is bf16(G); B = bf16(b G + c G^2) (with the
+unrounded G) is a product operand; the new iterate a (hi + lo) + hi B is
+split into a pair again before the next step. ns_filter returns the last
+step's value unsplit; the caller rounds it to its output precision.
 """
 from __future__ import annotations
 
@@ -26,7 +29,7 @@ from math import comb
 
 import numpy as np
 
-from .precision import rounding
+from .precision import round_bf16, rounding
 
 MUON_QUINTIC = (3.4445, -4.7750, 2.0315)
 
@@ -62,15 +65,24 @@ def scalar_compose(x, table) -> np.ndarray:
     return y
 
 
-def ns_step(x: np.ndarray, coeffs, mode: str = "exact") -> np.ndarray:
-    """One matrix step N(X) with coefficients (a_0, a_1, ..., a_d)."""
+def split_bf16(x: np.ndarray):
+    """The stored form of a bf16-contract iterate: hi = bf16(x), lo = bf16(x - hi)."""
+    x = np.asarray(x, dtype=np.float64)
+    hi = round_bf16(x)
+    return hi, round_bf16(x - hi)
+
+
+def ns_step(x: np.ndarray, coeffs, mode: str = "exact", operand=None) -> np.ndarray:
+    """One matrix step N(X) with coefficients (a_0, a_1, ..., a_d). In bf16
+    mode the product operand is `operand` (the stored hi of the iterate) when
+    given, else bf16(X)."""
     rd = rounding(mode)
     coeffs = [float(c) for c in coeffs]
     if mode != "exact" and len(coeffs) > 3:
         raise ValueError("the bf16 contract covers d <= 2")
     x = np.asarray(x, dtype=np.float64)
     tall = x.shape[0] >= x.shape[1]
-    xo = rd(x)                                  # product operand
+    xo = rd(x) if operand is None else np.asarray(operand, dtype=np.float64)   # product operand
     g = xo.T @ xo if tall else xo @ xo.T
     d = len(coeffs) - 1
     if mode == "exact":
@@ -90,8 +102,13 @@ def ns_step(x: np.ndarray, coeffs, mode: str = "exact") -> np.ndarray:
 
 
 def ns_filter(x0: np.ndarray, table, mode: str = "exact") -> np.ndarray:
-    """N_L o ... o N_1 (X0) for a per-step coefficient table (eq:filter)."""
+    """N_L o ... o N_1 (X0) for a per-step coefficient table (eq:filter). In
+    bf16 mode every step starts from the stored pair hi + lo of its input."""
     x = np.asarray(x0, dtype=np.float64)
     for row in table:
-        x = ns_step(x, row, mode)
+        if mode == "exact":
+            x = ns_step(x, row, mode)
+        else:
+            hi, lo = split_bf16(x)
+            x = ns_step(hi + lo, row, mode, operand=hi)
     return x
