@@ -55,11 +55,12 @@ def front_flops_per_matrix(s: int, l: int, k: int, rp: int, power_iters: int) ->
 
 def update_bytes_per_matrix(s: int, l: int, steps: int) -> float:
     """Algorithmic HBM bytes of the iterate updates of one s x l matrix,
-    averaged over the call's launches: every step reads B (bf16, s x s), the
-    fp32 iterate and its bf16 copy (s x l); the first steps - 1 write the next
-    fp32 iterate and its bf16 copy, the last writes the bf16 output."""
-    inner = 2.0 * s * s + (4 + 2) * s * l + (4 + 2) * s * l
-    last = 2.0 * s * s + (4 + 2) * s * l + 2 * s * l
+    averaged over the call's launches. The bf16 iterate is stored as a pair of
+    bf16 arrays hi + lo. Every step reads B (bf16, s x s), the operand hi
+    (s x l) and the pair hi, lo for the a X term; the first steps - 1 write
+    the next pair, the last writes the bf16 output."""
+    inner = 2.0 * s * s + 2 * s * l + 4 * s * l + 4 * s * l
+    last = 2.0 * s * s + 2 * s * l + 4 * s * l + 2 * s * l
     return ((steps - 1) * inner + last) / steps
 
 
@@ -212,7 +213,7 @@ def main() -> int:
                    "batch": b, "m": m, "n": n, "k": k, "steps": case.steps, "parallelism": "single GPU"},
         "tflops": tflops,
         "mfma_frac": tflops / MFMA_BF16_PEAK_TFLOPS,
-        "roofline": {"bound": "hbm", "kernel": "iterate update X <- a X + B X (gemm_kernel, EpiUpdate)",
+        "roofline": {"bound": "hbm", "kernel": "iterate update X <- a X + B X (gemm_dma_kernel, EpiUpdateHL)",
                      "achieved": upd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": upd_gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
                      "bytes_per_launch": upd_bytes, "avg_launch_us": upd_avg_ms * 1e3,

@@ -93,6 +93,7 @@ __device__ __forceinline__ void emit4(T* p, int ld, int r0, int c, const float v
 // (optional).
 struct EpiGram {
   static constexpr bool PRE = false;
+  static constexpr bool ROWWISE = false;
   float* out32;
   bf16_t* out16;
   float scale32, scale16;
@@ -114,6 +115,7 @@ struct EpiGram {
 template <typename TO>
 struct EpiPoly {
   static constexpr bool PRE = false;
+  static constexpr bool ROWWISE = false;
   const float* a32;
   TO* out;
   float bc, cc;
@@ -135,6 +137,7 @@ struct EpiPoly {
 template <typename TX, typename TO>
 struct EpiUpdate {
   static constexpr bool PRE = true;
+  static constexpr bool ROWWISE = false;
   const TX* x;
   long long xstride;
   int ldx;
@@ -169,6 +172,75 @@ struct EpiUpdate {
   }
 };
 
+// Iterate update with the bf16 iterate stored as a pair, X = hi + lo
+// (hi = bf16(X), lo = bf16(X - hi)): out = ac * (hi + lo) + C, written as the
+// next pair, or (final step) into the caller's output with the rules of
+// EpiUpdate. hi is the product operand of the next step.
+// Row-wise epilogue: the kernel hands it eight consecutive columns of one row
+// (the accumulators pass through LDS), so every global access is 16 bytes
+// wide; the pair values are loaded before the main loop (pre8).
+template <typename TO>
+struct EpiUpdateHL {
+  static constexpr bool PRE = true;
+  static constexpr bool ROWWISE = true;
+  const bf16_t* hi;
+  const bf16_t* lo;
+  long long xstride;
+  int ldx;
+  float ac;
+  bf16_t* out_hi;      // next pair (same layout as hi / lo)
+  bf16_t* out_lo;
+  TO* out;             // final step: caller output
+  long long ostride;
+  int ldo;
+  int final_out;
+  int transpose_out;
+  int rows_valid, cols_valid;
+  __device__ void pre8(int b, int r, int c0, u32x4_t& h, u32x4_t& l) const {
+    const long long o = b * xstride + (long long)r * ldx + c0;
+    h = ld16(hi + o);
+    l = ld16(lo + o);
+  }
+  __device__ void apply8(int b, int r, int c0, const float (&acc)[8], const u32x4_t& h, const u32x4_t& l) const {
+    float v[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v[2 * q] = ac * (__uint_as_float(h[q] << 16) + __uint_as_float(l[q] << 16)) + acc[2 * q];
+      v[2 * q + 1] = ac * (__uint_as_float(h[q] & 0xffff0000u) + __uint_as_float(l[q] & 0xffff0000u)) + acc[2 * q + 1];
+    }
+    if (!final_out) {
+      u32x4_t nh, nl;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        nh[q] = pack_bf2(v[2 * q], v[2 * q + 1]);
+        nl[q] = pack_bf2(v[2 * q] - __uint_as_float(nh[q] << 16), v[2 * q + 1] - __uint_as_float(nh[q] & 0xffff0000u));
+      }
+      const long long o = b * xstride + (long long)r * ldx + c0;
+      st16(out_hi + o, nh);
+      st16(out_lo + o, nl);
+      return;
+    }
+    if (r >= rows_valid) return;
+    TO* ob = out + b * ostride;
+    if (!transpose_out) {
+      if constexpr (sizeof(TO) == 2) {
+        if (c0 + 8 <= cols_valid && (ldo & 7) == 0) {
+          st16(ob + (long long)r * ldo + c0,
+               u32x4_t{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])});
+          return;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (c0 + q < cols_valid) ob[(long long)r * ldo + c0 + q] = Cvt<TO>::from_f(v[q]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q)
+        if (c0 + q < cols_valid) ob[(long long)(c0 + q) * ldo + r] = Cvt<TO>::from_f(v[q]);
+    }
+  }
+};
+
 // Iterate update in transposed form: the kernel computes C^T = X^T B (B
 // symmetric), so v[j] is element (c, r0 + j) of the new iterate: a lane owns
 // four consecutive columns of one row and moves them as 16-byte vectors.
@@ -177,6 +249,7 @@ struct EpiUpdate {
 template <typename TO>
 struct EpiUpdateT {
   static constexpr bool PRE = false;
+  static constexpr bool ROWWISE = false;
   const float* x;
   long long xstride;
   int ldx;
@@ -215,6 +288,7 @@ struct EpiUpdateT {
 // Plain fp32 store of C.
 struct EpiStore {
   static constexpr bool PRE = false;
+  static constexpr bool ROWWISE = false;
   float* out;
   long long stride;
   int ld;
@@ -613,7 +687,12 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
   static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile rows per wave");
   static_assert(S >= 2 && LT * (S - 2) < 64, "stages");
   static_assert(!SYM || BM == BN, "symmetric tiling needs square tiles");
-  __shared__ __attribute__((aligned(1024))) char lds[S * STAGE];
+  // the row-wise epilogue reuses the ring for the C tile, rows padded to
+  // BN + 8 floats (the two row groups a store instruction covers fall in
+  // different banks)
+  constexpr int RW_LD = BN + 8;
+  constexpr int RING = S * STAGE, CT = Epi::ROWWISE ? BM * RW_LD * 4 : 0;
+  __shared__ __attribute__((aligned(1024))) char lds[RING > CT ? RING : CT];
 
   const int tiles_m = sh.M / BM, tiles_n = sh.N / BN;
   const int per = SYM ? tiles_m * (tiles_m + 1) / 2 : tiles_m * tiles_n;
@@ -634,8 +713,14 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
   const int wm = wave / Cfg::NWN, wn = wave % Cfg::NWN;
   const int r32 = lane & 31, h = lane >> 5;
 
-  constexpr bool PRE = Epi::PRE;
+  // Epilogue operands this lane will need, loaded before the main loop: in
+  // the MFMA layout (PRE), or 8-column row chunks (ROWWISE: chunk u of thread
+  // t is element group t + NT u of the tile, row = group / (BN / 8)).
+  constexpr bool PRE = Epi::PRE && !Epi::ROWWISE;
+  constexpr bool ROWWISE = Epi::ROWWISE;
+  constexpr int RW_CH = BM * BN / 8 / Cfg::NT;     // row chunks per thread
   float px[PRE ? WM * WN * 16 : 1];
+  u32x4_t rw_h[ROWWISE ? RW_CH : 1], rw_l[ROWWISE ? RW_CH : 1];
   if constexpr (PRE) {
 #pragma unroll
     for (int mi = 0; mi < WM; ++mi)
@@ -647,6 +732,13 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
           for (int jj = 0; jj < 4; ++jj)
             px[(mi * WN + ni) * 16 + 4 * i + jj] =
                 epi.pre(b, m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h + jj, n0 + wn * WN * 32 + ni * 32 + r32);
+  }
+  if constexpr (ROWWISE) {
+#pragma unroll
+    for (int u = 0; u < RW_CH; ++u) {
+      const int e = threadIdx.x + Cfg::NT * u;
+      epi.pre8(b, m0 + e / (BN / 8), n0 + 8 * (e % (BN / 8)), rw_h[u], rw_l[u]);
+    }
   }
 
   // per-lane global sources (at k = 0) and wave-uniform LDS offsets
@@ -717,20 +809,47 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
     tile_mma_dma<WM, WN, BN, B_NN>(base, base + A_BYTES, acc, wm, wn, lane);
   }
 
-  const int mode = SYM ? (tm == tn ? EMIT_SYM_DIAG : EMIT_SYM_OFF) : EMIT_FULL;
+  if constexpr (ROWWISE) {
+    // accumulators -> LDS (row pitch RW_LD floats) -> 8-column row chunks
+    static_assert(!SYM, "row-wise epilogue is for full tiles");
+    float* ct = reinterpret_cast<float*>(lds);
+    __syncthreads();
 #pragma unroll
-  for (int mi = 0; mi < WM; ++mi)
+    for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
-    for (int ni = 0; ni < WN; ++ni)
+      for (int ni = 0; ni < WN; ++ni)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float v[4] = {acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2],
-                      acc[mi][ni][4 * i + 3]};
-        const int r0 = m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h;
-        const int c = n0 + wn * WN * 32 + ni * 32 + r32;
-        if constexpr (PRE) epi.apply(b, r0, c, v, mode, &px[(mi * WN + ni) * 16 + 4 * i]);
-        else epi(b, r0, c, v, mode);
-      }
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int jj = 0; jj < 4; ++jj)
+            ct[(wm * WM * 32 + mi * 32 + 8 * i + 4 * h + jj) * RW_LD + wn * WN * 32 + ni * 32 + r32] =
+                acc[mi][ni][4 * i + jj];
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < RW_CH; ++u) {
+      const int e = threadIdx.x + Cfg::NT * u;
+      const int r = e / (BN / 8), c8 = 8 * (e % (BN / 8));
+      const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(ct + r * RW_LD + c8);
+      const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(ct + r * RW_LD + c8 + 4);
+      const float av[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+      epi.apply8(b, m0 + r, n0 + c8, av, rw_h[u], rw_l[u]);
+    }
+  } else {
+    const int mode = SYM ? (tm == tn ? EMIT_SYM_DIAG : EMIT_SYM_OFF) : EMIT_FULL;
+#pragma unroll
+    for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          float v[4] = {acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2],
+                        acc[mi][ni][4 * i + 3]};
+          const int r0 = m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h;
+          const int c = n0 + wn * WN * 32 + ni * 32 + r32;
+          if constexpr (PRE) epi.apply(b, r0, c, v, mode, &px[(mi * WN + ni) * 16 + 4 * i]);
+          else epi(b, r0, c, v, mode);
+        }
+  }
 }
 
 template <typename Cfg, bool B_NN, bool SYM, typename Epi>

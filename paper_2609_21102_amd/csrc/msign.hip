@@ -19,8 +19,9 @@ struct MsignPlan {
   size_t esz;
   // buffers
   void *xc, *bm;
-  float *xa, *xb;
-  bf16_t *xa16, *xb16;   // bf16 copies of the iterates (bf16 path)
+  float *xa, *xb;        // float32 iterates (fp32 path)
+  bf16_t *xa16, *xb16;   // bf16 path: the iterates as pairs hi + lo; hi is the
+  bf16_t *xalo, *xblo;   // product operand
   float *a32;
   bf16_t* a16;
   float *om, *yl, *ys, *E, *sv, *invsv, *coefA, *coefB, *Ls, *Ll, *sumsq, *alpha, *nu;
@@ -33,10 +34,13 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   const size_t B = p.batch;
   const size_t sl = (size_t)p.s_pad * p.l_pad, ss = (size_t)p.s_pad * p.s_pad;
   p.xc = p.copy_in ? ar.take<char>(B * sl * p.esz) : nullptr;
-  p.xa = ar.take<float>(B * sl);   // iterates are float32 for both dtypes
-  p.xb = ar.take<float>(B * sl);
-  p.xa16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * sl) : nullptr;
-  p.xb16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * sl) : nullptr;
+  const bool bf = p.dtype == SD_DTYPE_BF16;
+  p.xa = bf ? nullptr : ar.take<float>(B * sl);
+  p.xb = bf ? nullptr : ar.take<float>(B * sl);
+  p.xa16 = bf ? ar.take<bf16_t>(B * sl) : nullptr;
+  p.xb16 = bf ? ar.take<bf16_t>(B * sl) : nullptr;
+  p.xalo = bf ? ar.take<bf16_t>(B * sl) : nullptr;
+  p.xblo = bf ? ar.take<bf16_t>(B * sl) : nullptr;
   p.a32 = ar.take<float>(B * ss);
   p.a16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * ss) : nullptr;
   p.bm = ar.take<char>(B * ss * p.esz);
@@ -205,25 +209,28 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   }
   la.coef = p.coefB;
   la.alpha = p.alpha;
-  la.out = p.xa;
-  la.out16 = p.xa16;
+  la.out = p.xa;        // fp32 path: float32 X0
+  la.out16 = p.xa16;    // bf16 path: X0 as the pair hi + lo
+  la.out_lo = p.xalo;
   la.so = sl;
   la.ldo = p.l_pad;
   la.sumsq = nullptr;
   lowrank<T, float>(la, st);
 
-  // fixed-depth filter: float32 iterate; bf16 path rounds operands at staging
+  // fixed-depth filter: float32 iterate (fp32 path) or the bf16 pair hi + lo
+  // whose hi is the product operand (bf16 path)
   float* cur = p.xa;
   float* nxt = p.xb;
   bf16_t* cur16 = p.xa16;
   bf16_t* nxt16 = p.xb16;
+  bf16_t* curlo = p.xalo;
+  bf16_t* nxtlo = p.xblo;
   T* bm = reinterpret_cast<T*>(p.bm);
-  // operand view of the current iterate: bf16 copy or the fp32 iterate
+  constexpr bool BF = sizeof(T) == 2;
   auto xop = [&]() -> const T* {
-    if constexpr (sizeof(T) == 2) return reinterpret_cast<const T*>(cur16);
+    if constexpr (BF) return reinterpret_cast<const T*>(cur16);
     else return reinterpret_cast<const T*>(cur);
   };
-  constexpr bool BF = sizeof(T) == 2;
   for (int t = 0; t < p.steps; ++t) {
     const float a = coeffs ? coeffs[3 * t] : 3.4445f;
     const float b = coeffs ? coeffs[3 * t + 1] : -4.7750f;
@@ -257,18 +264,38 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     }
     GemmShape g3{p.s_pad, p.l_pad, p.s_pad, p.s_pad, p.l_pad, ss, sl, B, 1};
     const bool last = t + 1 == p.steps;
-    if (!last) {
+    ProfScope ps(SD_STAGE_NS_UPDATE, st);
+    if constexpr (BF) {
+      EpiUpdateHL<T> eu{};
+      eu.hi = cur16;
+      eu.lo = curlo;
+      eu.xstride = sl;
+      eu.ldx = p.l_pad;
+      eu.ac = a;
+      if (!last) {
+        eu.out_hi = nxt16;
+        eu.out_lo = nxtlo;
+        eu.final_out = 0;
+      } else {
+        eu.out = out;
+        eu.ostride = (long long)p.m * p.n;
+        eu.ldo = p.tall ? p.s : p.l;
+        eu.final_out = 1;
+        eu.transpose_out = p.tall ? 1 : 0;
+        eu.rows_valid = p.s;
+        eu.cols_valid = p.l;
+      }
+      update_gemm<T>(p, bm, xop(), g3, eu, st);
+    } else if (!last) {
       EpiUpdate<float, float> eu{};
       eu.x = cur;
       eu.xstride = sl;
       eu.ldx = p.l_pad;
       eu.ac = a;
       eu.out = nxt;
-      eu.out16 = nxt16;
       eu.ostride = sl;
       eu.ldo = p.l_pad;
       eu.final_out = 0;
-      ProfScope ps(SD_STAGE_NS_UPDATE, st);
       update_gemm<T>(p, bm, xop(), g3, eu, st);
     } else {
       EpiUpdate<float, T> eu{};
@@ -283,7 +310,6 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
       eu.transpose_out = p.tall ? 1 : 0;
       eu.rows_valid = p.s;
       eu.cols_valid = p.l;
-      ProfScope ps(SD_STAGE_NS_UPDATE, st);
       update_gemm<T>(p, bm, xop(), g3, eu, st);
     }
     float* tmp = cur;
@@ -292,11 +318,19 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     bf16_t* tmp16 = cur16;
     cur16 = nxt16;
     nxt16 = tmp16;
+    tmp16 = curlo;
+    curlo = nxtlo;
+    nxtlo = tmp16;
   }
   if (p.steps == 0) {
+    // the start itself, rounded to the output type (bf16 path: its hi)
     const long long tot = (long long)p.m * p.n * B;
-    hipLaunchKernelGGL((store_out_kernel<float, T>), grid1(tot, 256), dim3(256), 0, st, cur, sl, p.l_pad, out,
-                       (long long)p.m * p.n, p.s, p.l, p.tall ? 1 : 0, B);
+    if constexpr (BF)
+      hipLaunchKernelGGL((store_out_kernel<bf16_t, T>), grid1(tot, 256), dim3(256), 0, st, cur16, sl, p.l_pad, out,
+                         (long long)p.m * p.n, p.s, p.l, p.tall ? 1 : 0, B);
+    else
+      hipLaunchKernelGGL((store_out_kernel<float, T>), grid1(tot, 256), dim3(256), 0, st, cur, sl, p.l_pad, out,
+                         (long long)p.m * p.n, p.s, p.l, p.tall ? 1 : 0, B);
   }
   return hip_status();
 }
