@@ -93,7 +93,19 @@ __device__ __forceinline__ void emit4(T* p, int ld, int r0, int c, const float v
 // (optional).
 struct EpiGram {
   static constexpr bool PRE = false;
-  static constexpr bool ROWWISE = false;
+  static constexpr bool ROWWISE = true;
+  // row-wise form (direct-to-LDS kernel): eight consecutive columns of row r
+  __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&) const {
+    const long long o = b * stride + (long long)r * ld + c0;
+    if (out16)
+      st16(out16 + o, u32x4_t{pack_bf2(v[0] * scale16, v[1] * scale16), pack_bf2(v[2] * scale16, v[3] * scale16),
+                              pack_bf2(v[4] * scale16, v[5] * scale16), pack_bf2(v[6] * scale16, v[7] * scale16)});
+    if (out32) {
+      *reinterpret_cast<f32x4_t*>(out32 + o) = f32x4_t{v[0], v[1], v[2], v[3]} * scale32;
+      *reinterpret_cast<f32x4_t*>(out32 + o + 4) = f32x4_t{v[4], v[5], v[6], v[7]} * scale32;
+    }
+  }
   float* out32;
   bf16_t* out16;
   float scale32, scale16;
@@ -115,12 +127,31 @@ struct EpiGram {
 template <typename TO>
 struct EpiPoly {
   static constexpr bool PRE = false;
-  static constexpr bool ROWWISE = false;
+  static constexpr bool ROWWISE = true;
   const float* a32;
   TO* out;
   float bc, cc;
   long long stride;
   int ld;
+  // row-wise form (direct-to-LDS kernel): eight consecutive columns of row r
+  __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&) const {
+    const long long o = b * stride + (long long)r * ld + c0;
+    const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(a32 + o);
+    const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(a32 + o + 4);
+    float w[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      w[q] = bc * a0[q] + cc * v[q];
+      w[q + 4] = bc * a1[q] + cc * v[q + 4];
+    }
+    if constexpr (sizeof(TO) == 2) {
+      st16(out + o, u32x4_t{pack_bf2(w[0], w[1]), pack_bf2(w[2], w[3]), pack_bf2(w[4], w[5]), pack_bf2(w[6], w[7])});
+    } else {
+      *reinterpret_cast<f32x4_t*>(out + o) = f32x4_t{w[0], w[1], w[2], w[3]};
+      *reinterpret_cast<f32x4_t*>(out + o + 4) = f32x4_t{w[4], w[5], w[6], w[7]};
+    }
+  }
   __device__ void operator()(int b, int r0, int c, float v[4], int mode) const {
     const float* a = a32 + b * stride;
 #pragma unroll
@@ -810,8 +841,10 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
   }
 
   if constexpr (ROWWISE) {
-    // accumulators -> LDS (row pitch RW_LD floats) -> 8-column row chunks
-    static_assert(!SYM, "row-wise epilogue is for full tiles");
+    // accumulators -> LDS (row pitch RW_LD floats) -> 8-column row chunks.
+    // Symmetric tiling: a diagonal tile takes C[r][c] for c >= r and C[c][r]
+    // below (so the result is exactly symmetric); an off-diagonal tile also
+    // writes its transpose at (n0 + c, m0 + r).
     float* ct = reinterpret_cast<float*>(lds);
     __syncthreads();
 #pragma unroll
@@ -825,14 +858,31 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
             ct[(wm * WM * 32 + mi * 32 + 8 * i + 4 * h + jj) * RW_LD + wn * WN * 32 + ni * 32 + r32] =
                 acc[mi][ni][4 * i + jj];
     __syncthreads();
+    const bool diag = SYM && tm == tn;
 #pragma unroll
     for (int u = 0; u < RW_CH; ++u) {
       const int e = threadIdx.x + Cfg::NT * u;
       const int r = e / (BN / 8), c8 = 8 * (e % (BN / 8));
       const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(ct + r * RW_LD + c8);
       const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(ct + r * RW_LD + c8 + 4);
-      const float av[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+      float av[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+      if (diag) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          if (c8 + q < r) av[q] = ct[(c8 + q) * RW_LD + r];
+      }
       epi.apply8(b, m0 + r, n0 + c8, av, rw_h[u], rw_l[u]);
+    }
+    if (SYM && !diag) {
+#pragma unroll
+      for (int u = 0; u < RW_CH; ++u) {
+        const int e = threadIdx.x + Cfg::NT * u;
+        const int c = e / (BM / 8), r8 = 8 * (e % (BM / 8));
+        float av[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) av[q] = ct[(r8 + q) * RW_LD + c];
+        epi.apply8(b, n0 + c, m0 + r8, av, rw_h[0], rw_l[0]);
+      }
     }
   } else {
     const int mode = SYM ? (tm == tn ? EMIT_SYM_DIAG : EMIT_SYM_OFF) : EMIT_FULL;
