@@ -659,10 +659,20 @@ __device__ __forceinline__ u32x2_t lds_read_tr16(const char* p) {
 }
 
 // 16 bytes per lane from global memory straight into LDS at base + 16 lane
-// (base wave-uniform).
+// (base wave-uniform), as inline assembly: the compiler then does not track
+// the load as an LDS write, so it adds no wait on it before later LDS reads;
+// the kernels order every such load with their own vmcnt waits and barriers.
+// m0 carries the LDS address; nothing else in these kernels uses m0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 __device__ __forceinline__ void lds_dma16(const bf16_t* g, char* base) {
-  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(base), 16, 0, 0);
+  const unsigned off = (unsigned)(size_t)((__attribute__((address_space(3))) char*)base);
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(__builtin_amdgcn_readfirstlane(off))
+               : "memory", "m0");
 }
+#pragma clang diagnostic pop
 
 __device__ __forceinline__ int rowform_slot(int r, int c) { return c ^ ((r >> 1) & 7); }
 __device__ __forceinline__ int nnform_slot(int k, int c) { return c ^ (2 * (k & 3)); }
