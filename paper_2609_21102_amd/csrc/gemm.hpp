@@ -94,6 +94,7 @@ __device__ __forceinline__ void emit4(T* p, int ld, int r0, int c, const float v
 struct EpiGram {
   static constexpr bool PRE = false;
   static constexpr bool ROWWISE = true;
+  static constexpr bool HI_FROM_B = false;
   // row-wise form (direct-to-LDS kernel): eight consecutive columns of row r
   __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
   __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&) const {
@@ -128,6 +129,7 @@ template <typename TO>
 struct EpiPoly {
   static constexpr bool PRE = false;
   static constexpr bool ROWWISE = true;
+  static constexpr bool HI_FROM_B = false;
   const float* a32;
   TO* out;
   float bc, cc;
@@ -169,6 +171,7 @@ template <typename TX, typename TO>
 struct EpiUpdate {
   static constexpr bool PRE = true;
   static constexpr bool ROWWISE = false;
+  static constexpr bool HI_FROM_B = false;
   const TX* x;
   long long xstride;
   int ldx;
@@ -209,11 +212,15 @@ struct EpiUpdate {
 // EpiUpdate. hi is the product operand of the next step.
 // Row-wise epilogue: the kernel hands it eight consecutive columns of one row
 // (the accumulators pass through LDS), so every global access is 16 bytes
-// wide; the pair values are loaded before the main loop (pre8).
+// wide. lo is loaded before the main loop (pre8); hi is the product's B
+// operand itself (X, K x N with K = the rows of the iterate), so the kernel
+// copies it out of the LDS ring while the K steps that cover the tile's rows
+// pass through (HI_FROM_B) instead of reading it again from HBM.
 template <typename TO>
 struct EpiUpdateHL {
   static constexpr bool PRE = true;
   static constexpr bool ROWWISE = true;
+  static constexpr bool HI_FROM_B = true;
   const bf16_t* hi;
   const bf16_t* lo;
   long long xstride;
@@ -227,10 +234,8 @@ struct EpiUpdateHL {
   int final_out;
   int transpose_out;
   int rows_valid, cols_valid;
-  __device__ void pre8(int b, int r, int c0, u32x4_t& h, u32x4_t& l) const {
-    const long long o = b * xstride + (long long)r * ldx + c0;
-    h = ld16(hi + o);
-    l = ld16(lo + o);
+  __device__ void pre8(int b, int r, int c0, u32x4_t&, u32x4_t& l) const {
+    l = ld16(lo + b * xstride + (long long)r * ldx + c0);
   }
   __device__ void apply8(int b, int r, int c0, const float (&acc)[8], const u32x4_t& h, const u32x4_t& l) const {
     float v[8];
@@ -281,6 +286,7 @@ template <typename TO>
 struct EpiUpdateT {
   static constexpr bool PRE = false;
   static constexpr bool ROWWISE = false;
+  static constexpr bool HI_FROM_B = false;
   const float* x;
   long long xstride;
   int ldx;
@@ -320,6 +326,7 @@ struct EpiUpdateT {
 struct EpiStore {
   static constexpr bool PRE = false;
   static constexpr bool ROWWISE = false;
+  static constexpr bool HI_FROM_B = false;
   float* out;
   long long stride;
   int ld;
@@ -847,6 +854,21 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
     __builtin_amdgcn_s_barrier();
     if (kt + S - 1 < nk) issue((kt + S - 1) % S, kt + S - 1);
     const char* base = lds + (kt % S) * STAGE;
+    if constexpr (Epi::HI_FROM_B) {
+      // rows [kt BK, kt BK + BK) of the B operand are rows of this tile's
+      // output when they fall in [m0, m0 + BM): copy the epilogue's chunks
+      static_assert(B_NN && !SYM && ROWWISE, "hi from B needs the update's layout");
+      const int kb = kt * BK - m0;
+      if (kb >= 0 && kb < BM) {
+#pragma unroll
+        for (int u = 0; u < RW_CH; ++u) {
+          const int e = threadIdx.x + Cfg::NT * u;
+          const int k = e / (BN / 8) - kb;
+          if (k >= 0 && k < BK)
+            rw_h[u] = ld16(base + A_BYTES + k * (2 * BN) + (nnform_slot(k, e % (BN / 8)) << 4));
+        }
+      }
+    }
     tile_mma_dma<WM, WN, BN, B_NN>(base, base + A_BYTES, acc, wm, wn, lane);
   }
 
