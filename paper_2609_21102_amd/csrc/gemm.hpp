@@ -335,6 +335,22 @@ struct EpiStore {
   }
 };
 
+// Plain fp32 store of C in the row-wise form (direct-to-LDS kernel).
+struct EpiStoreRows {
+  static constexpr bool PRE = false;
+  static constexpr bool ROWWISE = true;
+  static constexpr bool HI_FROM_B = false;
+  float* out;
+  long long stride;
+  int ld;
+  __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&) const {
+    float* p = out + b * stride + (long long)r * ld + c0;
+    *reinterpret_cast<f32x4_t*>(p) = f32x4_t{v[0], v[1], v[2], v[3]};
+    *reinterpret_cast<f32x4_t*>(p + 4) = f32x4_t{v[4], v[5], v[6], v[7]};
+  }
+};
+
 // ------------------------------------------------------- staging ----------
 // Tile configuration: NWM x NWN waves, each computing WM x WN MFMA blocks of
 // 32 x 32, so a work-group owns a (32 WM NWM) x (32 WN NWN) tile of C.

@@ -169,6 +169,28 @@ void ts_xw(const T* X, long long sx, int ldx, int s_pad, int l_pad, const float*
   }
 }
 
+// bf16 tall-skinny products on the direct-to-LDS GEMM. Panels have rq rows
+// (32 or 64; rows past the sketch width are zero) of bf16 operands (W16) and
+// fp32 results (Pt), [batch][rq][len_pad].
+//   ts_xtw_dma:  Pt = (X^T W)^T = W^T X       (M = rq, N = l_pad, K = s_pad, X in NN form)
+//   ts_xw_dma:   Pt = (X W)^T   = W^T X^T     (M = rq, N = s_pad, K = l_pad, X rows in NT form)
+inline void ts_xtw_dma(const bf16_t* X, long long sx, int ldx, int s_pad, int l_pad, const bf16_t* W16, int rq,
+                       float* Pt, int batch, hipStream_t st) {
+  ProfScope ps(SD_STAGE_SKETCH, st);
+  GemmShape g{rq, l_pad, s_pad, s_pad, ldx, (long long)rq * s_pad, sx, batch};
+  EpiStoreRows e{Pt, (long long)rq * l_pad, l_pad};
+  if (rq == 32) launch_gemm_dma<GemmCfg<1, 4, 1, 1, 2, 0>, true, false>(W16, X, g, e, st);
+  else launch_gemm_dma<GemmCfg<1, 4, 2, 1, 2, 0>, true, false>(W16, X, g, e, st);
+}
+inline void ts_xw_dma(const bf16_t* X, long long sx, int ldx, int s_pad, int l_pad, const bf16_t* W16, int rq,
+                      float* Pt, int batch, hipStream_t st) {
+  ProfScope ps(SD_STAGE_SKETCH, st);
+  GemmShape g{rq, s_pad, l_pad, l_pad, ldx, (long long)rq * l_pad, sx, batch};
+  EpiStoreRows e{Pt, (long long)rq * s_pad, s_pad};
+  if (rq == 32) launch_gemm_dma<GemmCfg<1, 2, 1, 1, 2, 0>, false, false>(W16, X, g, e, st);
+  else launch_gemm_dma<GemmCfg<1, 2, 2, 1, 2, 0>, false, false>(W16, X, g, e, st);
+}
+
 // Float64 partial Grams of panel rows over 128-position chunks.
 inline void gram_partials(const float* A, long long sa, int lda, const float* B, long long sb, int ldb, int ca,
                           int cb, int len_pad, bool sym, double* part, int batch, hipStream_t st) {
@@ -186,14 +208,14 @@ inline size_t gram_part_elems(int batch, int len_pad, int ca, int cb, bool sym) 
 
 // One CholeskyQR pass on every panel of the batch, in place.
 inline void cholqr(float* Pt, long long sp, int ld, int c, int len_pad, int batch, double* part, double* fac,
-                   int* status, hipStream_t st) {
+                   int* status, hipStream_t st, bf16_t* Pt16 = nullptr) {
   ProfScope ps(SD_STAGE_CHOLQR, st);
   gram_partials(Pt, sp, ld, Pt, sp, ld, c, c, len_pad, true, part, batch, st);
   hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac, status);
   const dim3 g((len_pad / 128) * batch), b(128);
-  if (c <= 16) hipLaunchKernelGGL((chol_apply_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch);
-  else if (c <= 32) hipLaunchKernelGGL((chol_apply_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch);
-  else hipLaunchKernelGGL((chol_apply_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch);
+  if (c <= 16) hipLaunchKernelGGL((chol_apply_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16);
+  else if (c <= 32) hipLaunchKernelGGL((chol_apply_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16);
+  else hipLaunchKernelGGL((chol_apply_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16);
 }
 
 inline void rotate(const float* in, long long si, int ldi, const float* E, long long se, const float* scale,

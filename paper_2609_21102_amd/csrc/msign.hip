@@ -16,6 +16,7 @@ struct MsignPlan {
   int batch, m, n, k, steps, dtype;
   bool tall, copy_in;
   int s, l, s_pad, l_pad, rp;
+  int rq;                // rows of the sketch panels: rp rounded up to 32 (zero rows past rp)
   size_t esz;
   // buffers
   void *xc, *bm;
@@ -25,6 +26,7 @@ struct MsignPlan {
   float *a32;
   bf16_t* a16;
   float *om, *yl, *ys, *E, *sv, *invsv, *coefA, *coefB, *Ls, *Ll, *sumsq, *alpha, *nu;
+  bf16_t *om16, *yl16, *ys16;   // bf16 copies of the panels: product operands (bf16 path)
   double *part, *fac;
   int* keff;
   int tiles;
@@ -45,10 +47,13 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   p.a16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * ss) : nullptr;
   p.bm = ar.take<char>(B * ss * p.esz);
   const int kq = p.k > 0 ? p.k : 1;
-  const int rq = p.rp > 0 ? p.rp : 1;
+  const int rq = p.rq;
   p.om = ar.take<float>(B * rq * p.s_pad);
   p.yl = ar.take<float>(B * rq * p.l_pad);
   p.ys = ar.take<float>(B * rq * p.s_pad);
+  p.om16 = bf ? ar.take<bf16_t>(B * rq * p.s_pad) : nullptr;
+  p.yl16 = bf ? ar.take<bf16_t>(B * rq * p.l_pad) : nullptr;
+  p.ys16 = bf ? ar.take<bf16_t>(B * rq * p.s_pad) : nullptr;
   p.E = ar.take<float>(B * rq * kq);
   p.sv = ar.take<float>(B * kq);
   p.invsv = ar.take<float>(B * kq);
@@ -96,6 +101,7 @@ static void make_plan(MsignPlan& p, int batch, int m, int n, int k, int steps, i
   p.s_pad = round_up(p.s, 128);
   p.l_pad = round_up(p.l, 128);
   p.rp = k > 0 ? (k + o.oversample < p.s ? k + o.oversample : p.s) : 0;
+  p.rq = p.rp > 32 ? 64 : 32;
   p.esz = dtype == SD_DTYPE_BF16 ? 2 : 4;
   const bool aligned = in && (reinterpret_cast<uintptr_t>(in) % 16 == 0);
   p.copy_in = p.tall || p.s != p.s_pad || p.l != p.l_pad || !aligned;
@@ -144,27 +150,46 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     ldx = p.l;
   }
 
-  // Alg. 3: head estimate
+  // Alg. 3: head estimate. Panels are [B][rq][len_pad] (rows past rp zero);
+  // on the bf16 path the products take the panels' bf16 copies and run on
+  // the direct-to-LDS GEMM.
   if (p.k > 0) {
-    const int rp = p.rp, s_pad = p.s_pad, l_pad = p.l_pad;
-    const long long so = (long long)rp * s_pad, sl_ = (long long)rp * l_pad;
+    const int rp = p.rp, rq = p.rq, s_pad = p.s_pad, l_pad = p.l_pad;
+    const long long so = (long long)rq * s_pad, sl_ = (long long)rq * l_pad;
+    constexpr bool BF = sizeof(T) == 2;
     fill(p.om, so * B, 0.f, st);
+    if constexpr (BF) {
+      // zero bf16 copies (their rows past rp stay zero)
+      fill(reinterpret_cast<float*>(p.om16), so * B / 2, 0.f, st);
+      fill(reinterpret_cast<float*>(p.yl16), sl_ * B / 2, 0.f, st);
+      fill(reinterpret_cast<float*>(p.ys16), so * B / 2, 0.f, st);
+    }
     if (o.sketch) {
       const long long tot = (long long)p.s * rp * B;
-      hipLaunchKernelGGL(sketch_copy_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, o.sketch, p.s, rp, B);
+      hipLaunchKernelGGL(sketch_copy_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, o.sketch, p.s, rp, B,
+                         p.om16);
     } else {
       const long long tot = (((long long)p.s * rp + 3) / 4) * B;
-      hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, p.s, rp, o.seed, B);
+      hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, p.s, rp, o.seed, B,
+                         p.om16);
     }
-    ts_xtw<T>(xc, sx, ldx, s_pad, l_pad, p.om, so, s_pad, rp, p.yl, sl_, l_pad, B, st);
-    cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st);
+    auto xtw = [&](const float* w, const bf16_t* w16, float* out) {
+      if constexpr (BF) ts_xtw_dma(reinterpret_cast<const bf16_t*>(xc), sx, ldx, s_pad, l_pad, w16, rq, out, B, st);
+      else ts_xtw<T>(xc, sx, ldx, s_pad, l_pad, w, so, s_pad, rp, out, sl_, l_pad, B, st);
+    };
+    auto xw = [&](const float* w, const bf16_t* w16, float* out) {
+      if constexpr (BF) ts_xw_dma(reinterpret_cast<const bf16_t*>(xc), sx, ldx, s_pad, l_pad, w16, rq, out, B, st);
+      else ts_xw<T>(xc, sx, ldx, s_pad, l_pad, w, sl_, l_pad, rp, out, so, s_pad, B, st);
+    };
+    xtw(p.om, p.om16, p.yl);
+    cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st, p.yl16);
     for (int j = 0; j < o.power_iters; ++j) {
-      ts_xw<T>(xc, sx, ldx, s_pad, l_pad, p.yl, sl_, l_pad, rp, p.ys, so, s_pad, B, st);
-      cholqr(p.ys, so, s_pad, rp, s_pad, B, p.part, p.fac, o.status_dev, st);
-      ts_xtw<T>(xc, sx, ldx, s_pad, l_pad, p.ys, so, s_pad, rp, p.yl, sl_, l_pad, B, st);
-      cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st);
+      xw(p.yl, p.yl16, p.ys);
+      cholqr(p.ys, so, s_pad, rp, s_pad, B, p.part, p.fac, o.status_dev, st, p.ys16);
+      xtw(p.ys, p.ys16, p.yl);
+      cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st, p.yl16);
     }
-    ts_xw<T>(xc, sx, ldx, s_pad, l_pad, p.yl, sl_, l_pad, rp, p.ys, so, s_pad, B, st);   // G = (X Q)^T
+    xw(p.yl, p.yl16, p.ys);   // G = (X Q)^T
     {
       ProfScope ps(SD_STAGE_SMALL, st);
       gram_partials(p.ys, so, s_pad, p.ys, so, s_pad, rp, rp, s_pad, true, p.part, B, st);   // G G^T
@@ -395,7 +420,7 @@ int sd_sketch(int batch, int s, int rp, uint64_t seed, float* out, hipStream_t s
   if (batch < 1 || s < 1 || rp < 1 || !out) return SD_ERR_INVALID_ARG;
   const long long tot = (((long long)s * rp + 3) / 4) * batch;
   hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, stream, out, (long long)s * rp, s, s, rp, seed,
-                     batch);
+                     batch, (bf16_t*)nullptr);
   return hip_status();
 }
 

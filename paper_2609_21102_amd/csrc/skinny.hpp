@@ -214,7 +214,7 @@ struct Philox {
 // Omega^T [rp][ld] for every matrix: entry (i, j) of the s x rp sketch is
 // Gaussian number j * s + i of stream 1. Rows beyond s are zero.
 static __global__ void sketch_kernel(float* __restrict__ Wt, long long sw, int ld, int s, int rp,
-                              uint64_t seed, int batch) {
+                              uint64_t seed, int batch, bf16_t* __restrict__ Wt16) {
   const long long per = ((long long)s * rp + 3) / 4;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= per * batch) return;
@@ -229,13 +229,14 @@ static __global__ void sketch_kernel(float* __restrict__ Wt, long long sw, int l
     if (g < (long long)s * rp) {
       const int j = (int)(g / s), i = (int)(g - (long long)j * s);
       Wb[(long long)j * ld + i] = z[t];
+      if (Wt16) Wt16[b * sw + (long long)j * ld + i] = f2bf(z[t]);
     }
   }
 }
 
 // Copy a caller-supplied sketch [batch][rp][s] into the padded panel.
 static __global__ void sketch_copy_kernel(float* __restrict__ Wt, long long sw, int ld, const float* __restrict__ src,
-                                   int s, int rp, int batch) {
+                                   int s, int rp, int batch, bf16_t* __restrict__ Wt16) {
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   const long long per = (long long)s * rp;
   if (gid >= per * batch) return;
@@ -243,6 +244,7 @@ static __global__ void sketch_copy_kernel(float* __restrict__ Wt, long long sw, 
   const long long r = gid - (long long)b * per;
   const int j = (int)(r / s), i = (int)(r - (long long)j * s);
   Wt[b * sw + (long long)j * ld + i] = src[gid];
+  if (Wt16) Wt16[b * sw + (long long)j * ld + i] = f2bf(src[gid]);
 }
 
 // ----------------------------------------------------- canonical copy ----

@@ -270,10 +270,11 @@ static __global__ __launch_bounds__(64) void chol_factor_kernel(const double* pa
 }
 
 // Apply: Q = P R^-1 with R = L^T, by forward substitution per position, in
-// place. Grid: (len_pad / 128) * batch; one thread per position.
+// place (plus an optional bf16 copy of Q). Grid: (len_pad / 128) * batch; one
+// thread per position.
 template <int CM>
 __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp, int ld, int c, int len_pad,
-                                                         const double* fac, int batch) {
+                                                         const double* fac, int batch, bf16_t* Pt16) {
   __shared__ double L[CM][CM + 1];
   __shared__ double inv_d[CM];
   const int per = len_pad / 128;
@@ -298,6 +299,12 @@ __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp
 #pragma unroll
   for (int jj = 0; jj < CM; ++jj)
     if (jj < c) P[(long long)jj * ld + x] = (float)q[jj];
+  if (Pt16) {   // bf16 copy: the panel as a product operand
+    bf16_t* P16 = Pt16 + b * sp;
+#pragma unroll
+    for (int jj = 0; jj < CM; ++jj)
+      if (jj < c) P16[(long long)jj * ld + x] = f2bf((float)q[jj]);
+  }
 }
 
 // ----------------------------------------------- thin SVD of G (Alg. 3) ---
