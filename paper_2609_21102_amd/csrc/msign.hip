@@ -51,6 +51,7 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   p.om = ar.take<float>(B * rq * p.s_pad);
   p.yl = ar.take<float>(B * rq * p.l_pad);
   p.ys = ar.take<float>(B * rq * p.s_pad);
+  // (taken back to back: run_msign zeroes om16 .. ys16 with one fill)
   p.om16 = bf ? ar.take<bf16_t>(B * rq * p.s_pad) : nullptr;
   p.yl16 = bf ? ar.take<bf16_t>(B * rq * p.l_pad) : nullptr;
   p.ys16 = bf ? ar.take<bf16_t>(B * rq * p.s_pad) : nullptr;
@@ -159,10 +160,11 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     constexpr bool BF = sizeof(T) == 2;
     fill(p.om, so * B, 0.f, st);
     if constexpr (BF) {
-      // zero bf16 copies (their rows past rp stay zero)
-      fill(reinterpret_cast<float*>(p.om16), so * B / 2, 0.f, st);
-      fill(reinterpret_cast<float*>(p.yl16), sl_ * B / 2, 0.f, st);
-      fill(reinterpret_cast<float*>(p.ys16), so * B / 2, 0.f, st);
+      // zero the bf16 copies (their rows past rp stay zero); plan_msign takes
+      // them back to back, so one fill spans all three
+      char* lo = reinterpret_cast<char*>(p.om16);
+      char* hi = reinterpret_cast<char*>(p.ys16 + so * B);
+      fill(reinterpret_cast<float*>(lo), (long long)(hi - lo) / 4, 0.f, st);
     }
     if (o.sketch) {
       const long long tot = (long long)p.s * rp * B;

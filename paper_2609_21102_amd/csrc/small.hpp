@@ -205,12 +205,20 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const float* A, long 
 }
 
 // s.h[a][bb] = sum of the chunk partials in chunk order (mirrored when sym).
-// Loads are issued eight chunks at a time; the additions keep chunk order.
+// Loads are issued 32 chunks at a time (one round trip for up to 4096
+// positions); the additions keep chunk order.
 static __device__ void gram_reduce(SmallLds& s, const double* part, int nch, int ca, int cb, bool sym) {
   const int items = gram_items(ca, cb, sym);
   for (int p = threadIdx.x; p < items; p += blockDim.x) {
     double t = 0.0;
     int c = 0;
+    for (; c + 32 <= nch; c += 32) {
+      double v[32];
+#pragma unroll
+      for (int u = 0; u < 32; ++u) v[u] = part[(long long)(c + u) * items + p];
+#pragma unroll
+      for (int u = 0; u < 32; ++u) t += v[u];
+    }
     for (; c + 8 <= nch; c += 8) {
       double v[8];
 #pragma unroll
