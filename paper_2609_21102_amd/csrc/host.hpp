@@ -211,7 +211,14 @@ inline void cholqr(float* Pt, long long sp, int ld, int c, int len_pad, int batc
                    int* status, hipStream_t st, bf16_t* Pt16 = nullptr) {
   ProfScope ps(SD_STAGE_CHOLQR, st);
   gram_partials(Pt, sp, ld, Pt, sp, ld, c, c, len_pad, true, part, batch, st);
-  hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac, status);
+  if (c <= 16)
+    hipLaunchKernelGGL((chol_factor_wave_kernel<16>), dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac,
+                       status);
+  else if (c <= 32)
+    hipLaunchKernelGGL((chol_factor_wave_kernel<32>), dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac,
+                       status);
+  else
+    hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac, status);
   const dim3 g((len_pad / 128) * batch), b(128);
   if (c <= 16) hipLaunchKernelGGL((chol_apply_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16);
   else if (c <= 32) hipLaunchKernelGGL((chol_apply_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16);

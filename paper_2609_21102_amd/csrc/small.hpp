@@ -277,6 +277,60 @@ static __global__ __launch_bounds__(64) void chol_factor_kernel(const double* pa
   }
 }
 
+// The same factorization on one wave with rows in registers (c <= CM <= 32):
+// lane i owns row i of the lower triangle; column j takes its pivot from
+// lane j and the multipliers L[k][j] by cross-lane broadcasts, so no step
+// waits on LDS or a barrier.
+template <int CM>
+__global__ __launch_bounds__(64) void chol_factor_wave_kernel(const double* part, int nch, int c, double* fac,
+                                                             int* status) {
+  static_assert(CM <= 32, "one row per lane");
+  __shared__ SmallLds s;
+  const int b = blockIdx.x, lane = threadIdx.x;
+  gram_reduce(s, part + (long long)b * nch * gram_items(c, c, true), nch, c, c, true);
+  double h[CM];
+#pragma unroll
+  for (int k = 0; k < CM; ++k) h[k] = (lane < c && k <= lane) ? s.h[lane][k] : 0.0;
+  double dg = 0.0;
+#pragma unroll
+  for (int k = 0; k < CM; ++k)
+    if (k == lane) dg = h[k];
+  const double tr = __shfl(wave_sum(dg), 0, WAVE);
+  double* L = fac + (long long)b * c * c;
+  if (tr == 0.0) {
+    for (int e = lane; e < c * c; e += WAVE) L[e] = 0.0;
+    return;
+  }
+  const double floor_ = (double)c * 1.1102230246251565e-16 * tr;
+  bool floored = false;
+#pragma unroll
+  for (int j = 0; j < CM; ++j) {
+    if (j < c) {
+      double d = __shfl(h[j], j, WAVE);   // pivot: lane j's updated diagonal
+      if (d <= floor_) {
+        d = floor_;
+        floored = true;
+      }
+      const double piv = sqrt(d), inv = 1.0 / piv;
+      const double lij = lane > j ? h[j] * inv : (lane == j ? piv : 0.0);
+      h[j] = lij;
+#pragma unroll
+      for (int k = j + 1; k < CM; ++k) {
+        if (k < c) {
+          const double lkj = __shfl(lij, k, WAVE);
+          if (lane >= k) h[k] -= lij * lkj;
+        }
+      }
+    }
+  }
+  if (floored && lane == 0 && status) atomicOr(status, 2);
+  if (lane < c) {
+#pragma unroll
+    for (int k = 0; k < CM; ++k)
+      if (k < c) L[(long long)lane * c + k] = k <= lane ? h[k] : 0.0;
+  }
+}
+
 // Apply: Q = P R^-1 with R = L^T, by forward substitution per position, in
 // place (plus an optional bf16 copy of Q). Grid: (len_pad / 128) * batch; one
 // thread per position.
