@@ -186,9 +186,12 @@ def main() -> int:
     flops = b * (ns_flops_per_matrix(s, l, case.steps) + (front_flops_per_matrix(s, l, k, rp, case.power_iters)
                                                           if k else 0.0))
     tflops = flops / (ms_per_step / 1e3) / 1e12
-    upd_flops = 2.0 * s * s * l * b
-    upd_bytes = update_bytes_per_matrix(s, l, case.steps) * b
-    upd_avg_ms = upd_ms / max(upd_n, 1)
+    # totals over the timed calls, divided by the update launches they made
+    # (one per filter step, or two when a call runs its batch in two halves)
+    n_launch = max(upd_n, 1)
+    upd_flops = 2.0 * s * s * l * b * case.steps * args.steps / n_launch
+    upd_bytes = update_bytes_per_matrix(s, l, case.steps) * b * case.steps * args.steps / n_launch
+    upd_avg_ms = upd_ms / n_launch
     upd_tflops = upd_flops / (upd_avg_ms / 1e3) / 1e12
     upd_gbs = upd_bytes / (upd_avg_ms / 1e3) / 1e9
     log(f"bench: {ms_per_step:.3f} ms/step, {value:.0f} matrices/s, {tflops:.1f} TFLOP/s; "
