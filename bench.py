@@ -55,12 +55,13 @@ def front_flops_per_matrix(s: int, l: int, k: int, rp: int, power_iters: int) ->
 
 def update_bytes_per_matrix(s: int, l: int, steps: int) -> float:
     """Algorithmic HBM bytes of the iterate updates of one s x l matrix,
-    averaged over the call's launches. The bf16 iterate is stored as a pair of
-    bf16 arrays hi + lo. Every step reads B (bf16, s x s), the operand hi
-    (s x l) and the pair hi, lo for the a X term; the first steps - 1 write
-    the next pair, the last writes the bf16 output."""
-    inner = 2.0 * s * s + 2 * s * l + 4 * s * l + 4 * s * l
-    last = 2.0 * s * s + 2 * s * l + 4 * s * l + 2 * s * l
+    averaged over the call's launches. The bf16 iterate is stored as hi (bf16)
+    plus an 8-bit residual. Every step reads B (bf16, s x s), the operand hi
+    (s x l; the a X term takes hi from the same tiles) and the residuals; the
+    first steps - 1 write the next hi and residuals, the last writes the bf16
+    output."""
+    inner = 2.0 * s * s + 2 * s * l + 1 * s * l + 3 * s * l
+    last = 2.0 * s * s + 2 * s * l + 1 * s * l + 2 * s * l
     return ((steps - 1) * inner + last) / steps
 
 

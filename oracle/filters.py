@@ -14,13 +14,15 @@
 
 bf16 contract (mode "bf16"), used for the bf16 library paths ("bfloat16
 mixed precision" of Sec. 3: bf16 operands, wider accumulation and state): the
-iterate is stored as a pair of bf16 numbers, hi = bf16(X) and
-lo = bf16(X - hi), and carried as hi + lo (about 16 significant bits); every
-matrix product takes bf16 operands, the iterate's being hi, so
+iterate is stored as hi = bf16(X) plus an 8-bit residual q in units of
+2^-8 ulp(hi), q = clip(rint((X - hi) / (2^-8 ulp(hi))), -127, 127), and carried
+as hi + q 2^-8 ulp(hi) (about 16 significant bits; ulp(hi) = 2^(E - 134) for
+the bf16 exponent field E of hi, E taken as 1 for zero and subnormals);
+every matrix product takes bf16 operands, the iterate's being hi, so
 G = hi^T hi; the operand of G^2 is bf16(G); B = bf16(b G + c G^2) (with the
-unrounded G) is a product operand; the new iterate a (hi + lo) + hi B is
-split into a pair again before the next step. ns_filter returns the last
-step's value unsplit; the caller rounds it to its output precision.
+unrounded G) is a product operand; the new iterate a (carried X) + hi B is
+stored in the same form before the next step. ns_filter returns the last
+step's value as computed; the caller rounds it to its output precision.
 """
 from __future__ import annotations
 
@@ -65,11 +67,15 @@ def scalar_compose(x, table) -> np.ndarray:
     return y
 
 
-def split_bf16(x: np.ndarray):
-    """The stored form of a bf16-contract iterate: hi = bf16(x), lo = bf16(x - hi)."""
+def store_state(x: np.ndarray):
+    """The stored form of a bf16-contract iterate: returns (hi, carried) with
+    hi = bf16(x) and carried = hi + q 2^-8 ulp(hi) for the 8-bit residual q."""
     x = np.asarray(x, dtype=np.float64)
     hi = round_bf16(x)
-    return hi, round_bf16(x - hi)
+    field = (hi.astype(np.float32).view(np.uint32) >> np.uint32(23)) & np.uint32(0xFF)
+    step = np.ldexp(1.0, np.maximum(field.astype(np.int64), 1) - 142)
+    q = np.clip(np.rint((x - hi) / step), -127, 127)
+    return hi, hi + q * step
 
 
 def ns_step(x: np.ndarray, coeffs, mode: str = "exact", operand=None) -> np.ndarray:
@@ -103,12 +109,13 @@ def ns_step(x: np.ndarray, coeffs, mode: str = "exact", operand=None) -> np.ndar
 
 def ns_filter(x0: np.ndarray, table, mode: str = "exact") -> np.ndarray:
     """N_L o ... o N_1 (X0) for a per-step coefficient table (eq:filter). In
-    bf16 mode every step starts from the stored pair hi + lo of its input."""
+    bf16 mode every step starts from the stored form (hi, 8-bit residual) of
+    its input."""
     x = np.asarray(x0, dtype=np.float64)
     for row in table:
         if mode == "exact":
             x = ns_step(x, row, mode)
         else:
-            hi, lo = split_bf16(x)
-            x = ns_step(hi + lo, row, mode, operand=hi)
+            hi, carried = store_state(x)
+            x = ns_step(carried, row, mode, operand=hi)
     return x

@@ -29,6 +29,36 @@ __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
 __device__ __forceinline__ bf16_t f2bf(float f) { return (bf16_t)(pack_bf2(f, 0.f) & 0xffffu); }
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
+// ------------------------------------------------- iterate state ----------
+// The bf16 iterate is stored as hi = bf16(x) plus an 8-bit residual q in
+// units of 2^-8 ulp(hi): q = clamp(rint((x - hi) 2^(142 - E)), -127, 127) for
+// the (bf16 = fp32) exponent field E of hi, E taken as 1 for zero and
+// subnormals, and read back as hi + q 2^(E - 142). The scalings are exact.
+__device__ __forceinline__ int state_exp(float h) {
+  const int f = (int)((__float_as_uint(h) >> 23) & 0xFFu);
+  return f > 0 ? f : 1;
+}
+__device__ __forceinline__ int state_q8(float x, float h) {
+  float t = __builtin_rintf(__builtin_amdgcn_ldexpf(x - h, 142 - state_exp(h)));
+  t = fminf(fmaxf(t, -127.f), 127.f);
+  return (int)t;
+}
+__device__ __forceinline__ float state_value(float h, int q) {
+  return h + __builtin_amdgcn_ldexpf((float)q, state_exp(h) - 142);
+}
+// 8 residuals <-> 8 bytes
+__device__ __forceinline__ u32x2_t pack_q8(const int (&q)[8]) {
+  u32x2_t w;
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+    w[i] = (uint32_t)(q[4 * i] & 0xFF) | ((uint32_t)(q[4 * i + 1] & 0xFF) << 8) |
+           ((uint32_t)(q[4 * i + 2] & 0xFF) << 16) | ((uint32_t)(q[4 * i + 3] & 0xFF) << 24);
+  return w;
+}
+__device__ __forceinline__ int unpack_q8(const u32x2_t& w, int i) {
+  return (int)(int8_t)((w[i >> 2] >> (8 * (i & 3))) & 0xFFu);
+}
+
 // Component i (a compile-time constant after unrolling) of a 16-byte value.
 __device__ __forceinline__ uint32_t u4c(const u32x4_t& u, int i) { return u[i]; }
 __device__ __forceinline__ float u4f(const u32x4_t& u, int i) { return __uint_as_float(u[i]); }

@@ -206,28 +206,28 @@ struct EpiUpdate {
   }
 };
 
-// Iterate update with the bf16 iterate stored as a pair, X = hi + lo
-// (hi = bf16(X), lo = bf16(X - hi)): out = ac * (hi + lo) + C, written as the
-// next pair, or (final step) into the caller's output with the rules of
-// EpiUpdate. hi is the product operand of the next step.
+// Iterate update with the bf16 iterate stored as hi = bf16(X) plus an 8-bit
+// residual q (state_q8 / state_value): out = ac * X + C, written in the same
+// form, or (final step) into the caller's output with the rules of EpiUpdate.
+// hi is the product operand of the next step.
 // Row-wise epilogue: the kernel hands it eight consecutive columns of one row
-// (the accumulators pass through LDS), so every global access is 16 bytes
-// wide. lo is loaded before the main loop (pre8); hi is the product's B
-// operand itself (X, K x N with K = the rows of the iterate), so the kernel
-// copies it out of the LDS ring while the K steps that cover the tile's rows
-// pass through (HI_FROM_B) instead of reading it again from HBM.
+// (the accumulators pass through LDS), so global accesses are 16 bytes (hi)
+// and 8 bytes (q) wide. q is loaded before the main loop (pre8); hi is the
+// product's B operand itself (X, K x N with K = the rows of the iterate), so
+// the kernel copies it out of the LDS ring while the K steps that cover the
+// tile's rows pass through (HI_FROM_B) instead of reading it again from HBM.
 template <typename TO>
 struct EpiUpdateHL {
   static constexpr bool PRE = true;
   static constexpr bool ROWWISE = true;
   static constexpr bool HI_FROM_B = true;
   const bf16_t* hi;
-  const bf16_t* lo;
+  const int8_t* lo;    // residuals, same element layout as hi
   long long xstride;
   int ldx;
   float ac;
-  bf16_t* out_hi;      // next pair (same layout as hi / lo)
-  bf16_t* out_lo;
+  bf16_t* out_hi;      // next state (same layout as hi / lo)
+  int8_t* out_lo;
   TO* out;             // final step: caller output
   long long ostride;
   int ldo;
@@ -235,25 +235,29 @@ struct EpiUpdateHL {
   int transpose_out;
   int rows_valid, cols_valid;
   __device__ void pre8(int b, int r, int c0, u32x4_t&, u32x4_t& l) const {
-    l = ld16(lo + b * xstride + (long long)r * ldx + c0);
+    const u32x2_t w = *reinterpret_cast<const u32x2_t*>(lo + b * xstride + (long long)r * ldx + c0);
+    l = u32x4_t{w[0], w[1], 0u, 0u};
   }
   __device__ void apply8(int b, int r, int c0, const float (&acc)[8], const u32x4_t& h, const u32x4_t& l) const {
+    const u32x2_t lw = {l[0], l[1]};
     float v[8];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      v[2 * q] = ac * (__uint_as_float(h[q] << 16) + __uint_as_float(l[q] << 16)) + acc[2 * q];
-      v[2 * q + 1] = ac * (__uint_as_float(h[q] & 0xffff0000u) + __uint_as_float(l[q] & 0xffff0000u)) + acc[2 * q + 1];
+      v[2 * q] = ac * state_value(__uint_as_float(h[q] << 16), unpack_q8(lw, 2 * q)) + acc[2 * q];
+      v[2 * q + 1] = ac * state_value(__uint_as_float(h[q] & 0xffff0000u), unpack_q8(lw, 2 * q + 1)) + acc[2 * q + 1];
     }
     if (!final_out) {
-      u32x4_t nh, nl;
+      u32x4_t nh;
+      int nq[8];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         nh[q] = pack_bf2(v[2 * q], v[2 * q + 1]);
-        nl[q] = pack_bf2(v[2 * q] - __uint_as_float(nh[q] << 16), v[2 * q + 1] - __uint_as_float(nh[q] & 0xffff0000u));
+        nq[2 * q] = state_q8(v[2 * q], __uint_as_float(nh[q] << 16));
+        nq[2 * q + 1] = state_q8(v[2 * q + 1], __uint_as_float(nh[q] & 0xffff0000u));
       }
       const long long o = b * xstride + (long long)r * ldx + c0;
       st16(out_hi + o, nh);
-      st16(out_lo + o, nl);
+      *reinterpret_cast<u32x2_t*>(out_lo + o) = pack_q8(nq);
       return;
     }
     if (r >= rows_valid) return;

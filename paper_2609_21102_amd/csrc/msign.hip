@@ -21,8 +21,8 @@ struct MsignPlan {
   // buffers
   void *xc, *bm;
   float *xa, *xb;        // float32 iterates (fp32 path)
-  bf16_t *xa16, *xb16;   // bf16 path: the iterates as pairs hi + lo; hi is the
-  bf16_t *xalo, *xblo;   // product operand
+  bf16_t *xa16, *xb16;   // bf16 path: the iterates as hi = bf16(X) (the product
+  int8_t *xalo, *xblo;   // operand) plus 8-bit residuals
   float *a32;
   bf16_t* a16;
   float *om, *yl, *ys, *E, *sv, *invsv, *coefA, *coefB, *Ls, *Ll, *sumsq, *alpha, *nu;
@@ -41,8 +41,8 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   p.xb = bf ? nullptr : ar.take<float>(B * sl);
   p.xa16 = bf ? ar.take<bf16_t>(B * sl) : nullptr;
   p.xb16 = bf ? ar.take<bf16_t>(B * sl) : nullptr;
-  p.xalo = bf ? ar.take<bf16_t>(B * sl) : nullptr;
-  p.xblo = bf ? ar.take<bf16_t>(B * sl) : nullptr;
+  p.xalo = bf ? ar.take<int8_t>(B * sl) : nullptr;
+  p.xblo = bf ? ar.take<int8_t>(B * sl) : nullptr;
   p.a32 = ar.take<float>(B * ss);
   p.a16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * ss) : nullptr;
   p.bm = ar.take<char>(B * ss * p.esz);
@@ -237,21 +237,21 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   la.coef = p.coefB;
   la.alpha = p.alpha;
   la.out = p.xa;        // fp32 path: float32 X0
-  la.out16 = p.xa16;    // bf16 path: X0 as the pair hi + lo
+  la.out16 = p.xa16;    // bf16 path: X0 as hi plus 8-bit residuals
   la.out_lo = p.xalo;
   la.so = sl;
   la.ldo = p.l_pad;
   la.sumsq = nullptr;
   lowrank<T, float>(la, st);
 
-  // fixed-depth filter: float32 iterate (fp32 path) or the bf16 pair hi + lo
-  // whose hi is the product operand (bf16 path)
+  // fixed-depth filter: float32 iterate (fp32 path) or hi = bf16(X) plus
+  // 8-bit residuals, hi being the product operand (bf16 path)
   float* cur = p.xa;
   float* nxt = p.xb;
   bf16_t* cur16 = p.xa16;
   bf16_t* nxt16 = p.xb16;
-  bf16_t* curlo = p.xalo;
-  bf16_t* nxtlo = p.xblo;
+  int8_t* curlo = p.xalo;
+  int8_t* nxtlo = p.xblo;
   T* bm = reinterpret_cast<T*>(p.bm);
   constexpr bool BF = sizeof(T) == 2;
   auto xop = [&]() -> const T* {
@@ -345,9 +345,9 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     bf16_t* tmp16 = cur16;
     cur16 = nxt16;
     nxt16 = tmp16;
-    tmp16 = curlo;
+    int8_t* tmplo = curlo;
     curlo = nxtlo;
-    nxtlo = tmp16;
+    nxtlo = tmplo;
   }
   if (p.steps == 0) {
     // the start itself, rounded to the output type (bf16 path: its hi)
