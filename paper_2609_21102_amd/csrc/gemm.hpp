@@ -704,41 +704,50 @@ __device__ __forceinline__ void lds_dma16(const bf16_t* g, char* base) {
 __device__ __forceinline__ int rowform_slot(int r, int c) { return c ^ ((r >> 1) & 7); }
 __device__ __forceinline__ int nnform_slot(int k, int c) { return c ^ (2 * (k & 3)); }
 
+// One K step (BK = 64) of MFMAs from LDS: four k-chunks, the fragments of
+// chunk g + 1 read while chunk g's MFMAs issue.
+template <int WM, int WN, int BN, bool B_NN>
+__device__ __forceinline__ void load_frags_dma(const char* la, const char* lb, int g, u32x4_t (&a)[WM],
+                                               u32x4_t (&b)[WN], int wm, int wn, int lane) {
+  const int r32 = lane & 31, h = lane >> 5;
+  const int q = lane >> 4, j = lane & 15;
+  const int c = 2 * g + h;
+#pragma unroll
+  for (int i = 0; i < WM; ++i) {
+    const int row = wm * WM * 32 + i * 32 + r32;
+    a[i] = ld16(la + row * 128 + (rowform_slot(row, c) << 4));
+  }
+  if constexpr (!B_NN) {
+#pragma unroll
+    for (int i = 0; i < WN; ++i) {
+      const int row = wn * WN * 32 + i * 32 + r32;
+      b[i] = ld16(lb + row * 128 + (rowform_slot(row, c) << 4));
+    }
+  } else {
+    const int k0 = 8 * (2 * g + (q >> 1)) + (j >> 2);
+#pragma unroll
+    for (int i = 0; i < WN; ++i) {
+      const int col = wn * WN * 32 + i * 32 + 16 * (q & 1) + 4 * (j & 3);
+      const int off = ((col & 7) << 1);
+      const u32x2_t lo = lds_read_tr16(lb + k0 * (2 * BN) + (nnform_slot(k0, col >> 3) << 4) + off);
+      const u32x2_t hi = lds_read_tr16(lb + (k0 + 4) * (2 * BN) + (nnform_slot(k0 + 4, col >> 3) << 4) + off);
+      b[i] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
+    }
+  }
+}
+
 template <int WM, int WN, int BN, bool B_NN>
 __device__ __forceinline__ void tile_mma_dma(const char* la, const char* lb, f32x16_t (&acc)[WM][WN], int wm,
                                              int wn, int lane) {
-  const int r32 = lane & 31, h = lane >> 5;
-  const int q = lane >> 4, j = lane & 15;
+  u32x4_t a[2][WM], b[2][WN];
+  load_frags_dma<WM, WN, BN, B_NN>(la, lb, 0, a[0], b[0], wm, wn, lane);
 #pragma unroll
   for (int g = 0; g < 4; ++g) {
-    u32x4_t a[WM], b[WN];
-    const int c = 2 * g + h;
-#pragma unroll
-    for (int i = 0; i < WM; ++i) {
-      const int row = wm * WM * 32 + i * 32 + r32;
-      a[i] = ld16(la + row * 128 + (rowform_slot(row, c) << 4));
-    }
-    if constexpr (!B_NN) {
-#pragma unroll
-      for (int i = 0; i < WN; ++i) {
-        const int row = wn * WN * 32 + i * 32 + r32;
-        b[i] = ld16(lb + row * 128 + (rowform_slot(row, c) << 4));
-      }
-    } else {
-      const int k0 = 8 * (2 * g + (q >> 1)) + (j >> 2);
-#pragma unroll
-      for (int i = 0; i < WN; ++i) {
-        const int col = wn * WN * 32 + i * 32 + 16 * (q & 1) + 4 * (j & 3);
-        const int off = ((col & 7) << 1);
-        const u32x2_t lo = lds_read_tr16(lb + k0 * (2 * BN) + (nnform_slot(k0, col >> 3) << 4) + off);
-        const u32x2_t hi = lds_read_tr16(lb + (k0 + 4) * (2 * BN) + (nnform_slot(k0 + 4, col >> 3) << 4) + off);
-        b[i] = u32x4_t{lo[0], lo[1], hi[0], hi[1]};
-      }
-    }
+    if (g + 1 < 4) load_frags_dma<WM, WN, BN, B_NN>(la, lb, g + 1, a[(g + 1) & 1], b[(g + 1) & 1], wm, wn, lane);
 #pragma unroll
     for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < WN; ++ni) acc[mi][ni] = mfma32_bf16(a[mi], b[ni], acc[mi][ni]);
+      for (int ni = 0; ni < WN; ++ni) acc[mi][ni] = mfma32_bf16(a[g & 1][mi], b[g & 1][ni], acc[mi][ni]);
   }
 }
 
