@@ -95,17 +95,25 @@ struct EpiGram {
   static constexpr bool PRE = false;
   static constexpr bool ROWWISE = true;
   static constexpr bool HI_FROM_B = false;
-  // row-wise form (direct-to-LDS kernel): eight consecutive columns of row r
+  // Row-wise form (direct-to-LDS kernel): eight consecutive columns of row r.
+  // The transposed (lower-triangle) copy gets out16 only (store8): out32 is
+  // read back only at upper-triangle and diagonal-tile positions.
   __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
-  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&) const {
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&,
+                         float (&mv)[8]) const {
     const long long o = b * stride + (long long)r * ld + c0;
-    if (out16)
-      st16(out16 + o, u32x4_t{pack_bf2(v[0] * scale16, v[1] * scale16), pack_bf2(v[2] * scale16, v[3] * scale16),
-                              pack_bf2(v[4] * scale16, v[5] * scale16), pack_bf2(v[6] * scale16, v[7] * scale16)});
+#pragma unroll
+    for (int q = 0; q < 8; ++q) mv[q] = v[q] * scale16;
+    if (out16) store8(b, r, c0, mv);
     if (out32) {
       *reinterpret_cast<f32x4_t*>(out32 + o) = f32x4_t{v[0], v[1], v[2], v[3]} * scale32;
       *reinterpret_cast<f32x4_t*>(out32 + o + 4) = f32x4_t{v[4], v[5], v[6], v[7]} * scale32;
     }
+  }
+  __device__ void store8(int b, int r, int c0, const float (&v)[8]) const {
+    if (out16)
+      st16(out16 + b * stride + (long long)r * ld + c0,
+           u32x4_t{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])});
   }
   float* out32;
   bf16_t* out16;
@@ -135,18 +143,23 @@ struct EpiPoly {
   float bc, cc;
   long long stride;
   int ld;
-  // row-wise form (direct-to-LDS kernel): eight consecutive columns of row r
+  // Row-wise form (direct-to-LDS kernel): eight consecutive columns of row r.
+  // A32 is read only here; the transposed copy reuses the values (store8).
   __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
-  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&) const {
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&,
+                         float (&w)[8]) const {
     const long long o = b * stride + (long long)r * ld + c0;
     const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(a32 + o);
     const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(a32 + o + 4);
-    float w[8];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       w[q] = bc * a0[q] + cc * v[q];
       w[q + 4] = bc * a1[q] + cc * v[q + 4];
     }
+    store8(b, r, c0, w);
+  }
+  __device__ void store8(int b, int r, int c0, const float (&w)[8]) const {
+    const long long o = b * stride + (long long)r * ld + c0;
     if constexpr (sizeof(TO) == 2) {
       st16(out + o, u32x4_t{pack_bf2(w[0], w[1]), pack_bf2(w[2], w[3]), pack_bf2(w[4], w[5]), pack_bf2(w[6], w[7])});
     } else {
@@ -238,7 +251,8 @@ struct EpiUpdateHL {
     const u32x2_t w = *reinterpret_cast<const u32x2_t*>(lo + b * xstride + (long long)r * ldx + c0);
     l = u32x4_t{w[0], w[1], 0u, 0u};
   }
-  __device__ void apply8(int b, int r, int c0, const float (&acc)[8], const u32x4_t& h, const u32x4_t& l) const {
+  __device__ void apply8(int b, int r, int c0, const float (&acc)[8], const u32x4_t& h, const u32x4_t& l,
+                         float (&)[8]) const {
     const u32x2_t lw = {l[0], l[1]};
     float v[8];
 #pragma unroll
@@ -348,7 +362,8 @@ struct EpiStoreRows {
   long long stride;
   int ld;
   __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
-  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&) const {
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&,
+                         float (&)[8]) const {
     float* p = out + b * stride + (long long)r * ld + c0;
     *reinterpret_cast<f32x4_t*>(p) = f32x4_t{v[0], v[1], v[2], v[3]};
     *reinterpret_cast<f32x4_t*>(p + 4) = f32x4_t{v[4], v[5], v[6], v[7]};
@@ -920,6 +935,7 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
                 acc[mi][ni][4 * i + jj];
     __syncthreads();
     const bool diag = SYM && tm == tn;
+    float mv[RW_CH][8];   // values of the transposed copy (symmetric tilings)
 #pragma unroll
     for (int u = 0; u < RW_CH; ++u) {
       const int e = threadIdx.x + Cfg::NT * u;
@@ -932,17 +948,29 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
         for (int q = 0; q < 8; ++q)
           if (c8 + q < r) av[q] = ct[(c8 + q) * RW_LD + r];
       }
-      epi.apply8(b, m0 + r, n0 + c8, av, rw_h[u], rw_l[u]);
+      epi.apply8(b, m0 + r, n0 + c8, av, rw_h[u], rw_l[u], mv[u]);
     }
-    if (SYM && !diag) {
+    if constexpr (SYM) {
+      if (!diag) {
+        // the values to mirror go back into the C tile, then out transposed
+        __syncthreads();
 #pragma unroll
-      for (int u = 0; u < RW_CH; ++u) {
-        const int e = threadIdx.x + Cfg::NT * u;
-        const int c = e / (BM / 8), r8 = 8 * (e % (BM / 8));
-        float av[8];
+        for (int u = 0; u < RW_CH; ++u) {
+          const int e = threadIdx.x + Cfg::NT * u;
+          const int r = e / (BN / 8), c8 = 8 * (e % (BN / 8));
+          *reinterpret_cast<f32x4_t*>(ct + r * RW_LD + c8) = f32x4_t{mv[u][0], mv[u][1], mv[u][2], mv[u][3]};
+          *reinterpret_cast<f32x4_t*>(ct + r * RW_LD + c8 + 4) = f32x4_t{mv[u][4], mv[u][5], mv[u][6], mv[u][7]};
+        }
+        __syncthreads();
 #pragma unroll
-        for (int q = 0; q < 8; ++q) av[q] = ct[(r8 + q) * RW_LD + c];
-        epi.apply8(b, n0 + c, m0 + r8, av, rw_h[0], rw_l[0]);
+        for (int u = 0; u < RW_CH; ++u) {
+          const int e = threadIdx.x + Cfg::NT * u;
+          const int c = e / (BM / 8), r8 = 8 * (e % (BM / 8));
+          float av[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) av[q] = ct[(r8 + q) * RW_LD + c];
+          epi.store8(b, n0 + c, m0 + r8, av);
+        }
       }
     }
   } else {
