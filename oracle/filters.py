@@ -14,10 +14,12 @@
 
 bf16 contract (mode "bf16"), used for the bf16 library paths ("bfloat16
 mixed precision" of Sec. 3: bf16 operands, wider accumulation and state): the
-iterate is stored as hi = bf16(X) plus an 8-bit residual q in units of
-2^-8 ulp(hi), q = clip(rint((X - hi) / (2^-8 ulp(hi))), -127, 127), and carried
-as hi + q 2^-8 ulp(hi) (about 16 significant bits; ulp(hi) = 2^(E - 134) for
-the bf16 exponent field E of hi, E taken as 1 for zero and subnormals);
+iterate is stored as hi = bf16(X) plus a one-byte residual, the float8 e4m3
+value r = e4m3(clip((X - hi) 2^16, -448, 448)) (round to nearest even), and
+carried as hi + r 2^-16 (the residual keeps 4 significant bits of X - hi, so
+the carried value has about 12 or more significant bits where
+2^-13 <= |X| < 2; smaller entries keep 4 bits of their residual down to the
+format's subnormal range, larger ones a clipped residual);
 every matrix product takes bf16 operands, the iterate's being hi, so
 G = hi^T hi; the operand of G^2 is bf16(G); B = bf16(b G + c G^2) (with the
 unrounded G) is a product operand; the new iterate a (carried X) + hi B is
@@ -31,7 +33,9 @@ from math import comb
 
 import numpy as np
 
-from .precision import round_bf16, rounding
+from .precision import E4M3_MAX, round_bf16, round_e4m3, rounding
+
+STATE_SCALE = 2.0 ** 16   # residual scale of the stored bf16-contract iterate
 
 MUON_QUINTIC = (3.4445, -4.7750, 2.0315)
 
@@ -69,13 +73,12 @@ def scalar_compose(x, table) -> np.ndarray:
 
 def store_state(x: np.ndarray):
     """The stored form of a bf16-contract iterate: returns (hi, carried) with
-    hi = bf16(x) and carried = hi + q 2^-8 ulp(hi) for the 8-bit residual q."""
+    hi = bf16(x) and carried = hi + r 2^-16 for the e4m3 residual
+    r = e4m3(clip((x - hi) 2^16, -448, 448))."""
     x = np.asarray(x, dtype=np.float64)
     hi = round_bf16(x)
-    field = (hi.astype(np.float32).view(np.uint32) >> np.uint32(23)) & np.uint32(0xFF)
-    step = np.ldexp(1.0, np.maximum(field.astype(np.int64), 1) - 142)
-    q = np.clip(np.rint((x - hi) / step), -127, 127)
-    return hi, hi + q * step
+    r = round_e4m3(np.clip((x - hi) * STATE_SCALE, -E4M3_MAX, E4M3_MAX))
+    return hi, hi + r / STATE_SCALE
 
 
 def ns_step(x: np.ndarray, coeffs, mode: str = "exact", operand=None) -> np.ndarray:
@@ -109,7 +112,7 @@ def ns_step(x: np.ndarray, coeffs, mode: str = "exact", operand=None) -> np.ndar
 
 def ns_filter(x0: np.ndarray, table, mode: str = "exact") -> np.ndarray:
     """N_L o ... o N_1 (X0) for a per-step coefficient table (eq:filter). In
-    bf16 mode every step starts from the stored form (hi, 8-bit residual) of
+    bf16 mode every step starts from the stored form (hi, e4m3 residual) of
     its input."""
     x = np.asarray(x0, dtype=np.float64)
     for row in table:

@@ -25,7 +25,7 @@ zero ||A||_F drops that term (a zero matrix maps to zero).
 
 Modes: "exact" (float64 throughout) and "bf16" (the bf16 contract: the sketch
 products take bf16 operands Omega, Q and Y; X0 is formed wide, and X0 and the
-iterates are stored as bf16 hi plus an 8-bit residual, hi being every filter
+iterates are stored as bf16 hi plus an e4m3 residual, hi being every filter
 product's operand (filters.ns_filter); the output is rounded to bf16).
 """
 from __future__ import annotations

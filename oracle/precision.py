@@ -21,6 +21,23 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     return np.ldexp(np.rint(q), expo - 8)    # np.rint rounds half to even
 
 
+E4M3_MAX = 448.0
+
+
+def round_e4m3(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest OCP float8 e4m3 ("fn") value (3
+    fraction bits, exponent bias 7, subnormal spacing 2**-9, largest finite
+    448), ties to even, returned as float64. Inputs must lie in [-448, 448]
+    (callers clamp first; the format has no infinities)."""
+    x = np.asarray(x, dtype=np.float64)
+    if np.any(np.abs(x) > E4M3_MAX):
+        raise ValueError("round_e4m3 takes values in [-448, 448]")
+    mant, expo = np.frexp(x)                 # x = mant * 2**expo, |mant| in [0.5, 1)
+    expo = np.maximum(expo, -5)              # normal range starts at 2**-6
+    q = np.ldexp(x, 4 - expo)                # |q| < 2**4
+    return np.ldexp(np.rint(q), expo - 4)    # np.rint rounds half to even
+
+
 def identity(x: np.ndarray) -> np.ndarray:
     return np.asarray(x, dtype=np.float64)
 

@@ -219,13 +219,13 @@ struct EpiUpdate {
   }
 };
 
-// Iterate update with the bf16 iterate stored as hi = bf16(X) plus an 8-bit
-// residual q (state_q8 / state_value): out = ac * X + C, written in the same
-// form, or (final step) into the caller's output with the rules of EpiUpdate.
-// hi is the product operand of the next step.
+// Iterate update with the bf16 iterate stored as hi = bf16(X) plus an e4m3
+// residual byte (state_pack8 / state_value8): out = ac * X + C, written in the
+// same form, or (final step) into the caller's output with the rules of
+// EpiUpdate. hi is the product operand of the next step.
 // Row-wise epilogue: the kernel hands it eight consecutive columns of one row
 // (the accumulators pass through LDS), so global accesses are 16 bytes (hi)
-// and 8 bytes (q) wide. q is loaded before the main loop (pre8); hi is the
+// and 8 bytes (residuals) wide. The residuals are loaded before the main loop (pre8); hi is the
 // product's B operand itself (X, K x N with K = the rows of the iterate), so
 // the kernel copies it out of the LDS ring while the K steps that cover the
 // tile's rows pass through (HI_FROM_B) instead of reading it again from HBM.
@@ -235,7 +235,7 @@ struct EpiUpdateHL {
   static constexpr bool ROWWISE = true;
   static constexpr bool HI_FROM_B = true;
   const bf16_t* hi;
-  const int8_t* lo;    // residuals, same element layout as hi
+  const int8_t* lo;    // residual bytes, same element layout as hi
   long long xstride;
   int ldx;
   float ac;
@@ -253,25 +253,18 @@ struct EpiUpdateHL {
   }
   __device__ void apply8(int b, int r, int c0, const float (&acc)[8], const u32x4_t& h, const u32x4_t& l,
                          float (&)[8]) const {
-    const u32x2_t lw = {l[0], l[1]};
+    const uint32_t hw[4] = {h[0], h[1], h[2], h[3]};
     float v[8];
+    state_value8(hw, l[0], l[1], v);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      v[2 * q] = ac * state_value(__uint_as_float(h[q] << 16), unpack_q8(lw, 2 * q)) + acc[2 * q];
-      v[2 * q + 1] = ac * state_value(__uint_as_float(h[q] & 0xffff0000u), unpack_q8(lw, 2 * q + 1)) + acc[2 * q + 1];
-    }
+    for (int q = 0; q < 8; ++q) v[q] = ac * v[q] + acc[q];
     if (!final_out) {
-      u32x4_t nh;
-      int nq[8];
+      uint32_t nh[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        nh[q] = pack_bf2(v[2 * q], v[2 * q + 1]);
-        nq[2 * q] = state_q8(v[2 * q], __uint_as_float(nh[q] << 16));
-        nq[2 * q + 1] = state_q8(v[2 * q + 1], __uint_as_float(nh[q] & 0xffff0000u));
-      }
+      for (int q = 0; q < 4; ++q) nh[q] = pack_bf2(v[2 * q], v[2 * q + 1]);
       const long long o = b * xstride + (long long)r * ldx + c0;
-      st16(out_hi + o, nh);
-      *reinterpret_cast<u32x2_t*>(out_lo + o) = pack_q8(nq);
+      st16_nt(out_hi + o, u32x4_t{nh[0], nh[1], nh[2], nh[3]});
+      st8_nt(out_lo + o, state_pack8(v, nh));
       return;
     }
     if (r >= rows_valid) return;
@@ -279,7 +272,7 @@ struct EpiUpdateHL {
     if (!transpose_out) {
       if constexpr (sizeof(TO) == 2) {
         if (c0 + 8 <= cols_valid && (ldo & 7) == 0) {
-          st16(ob + (long long)r * ldo + c0,
+          st16_nt(ob + (long long)r * ldo + c0,
                u32x4_t{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])});
           return;
         }
@@ -378,9 +371,11 @@ struct EpiStoreRows {
 // a CU and one's epilogue overlaps the other's main loop.
 // OCC: minimum waves per SIMD the register allocation must allow (0: the
 // compiler's choice for the block size).
-template <int NWM_, int NWN_, int WM_, int WN_, int STAGES_ = 2, int OCC_ = 0>
+// BK: K step of the direct-to-LDS kernel (64 or 32; the register-staged
+// kernel takes its K step from the element type).
+template <int NWM_, int NWN_, int WM_, int WN_, int STAGES_ = 2, int OCC_ = 0, int BK_ = 64>
 struct GemmCfg {
-  static constexpr int NWM = NWM_, NWN = NWN_, WM = WM_, WN = WN_, STAGES = STAGES_;
+  static constexpr int NWM = NWM_, NWN = NWN_, WM = WM_, WN = WN_, STAGES = STAGES_, BK = BK_;
   static constexpr int OCC = OCC_ ? OCC_ : (64 * NWM_ * NWN_ + 255) / 256;
   static constexpr int BM = 32 * WM * NWM, BN = 32 * WN * NWN;
   static constexpr int NT = 64 * NWM * NWN;
@@ -677,12 +672,14 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_
 // the way), so STAGES - 1 K steps are in flight while one is multiplied;
 // one barrier per K step.
 //
-// LDS layouts (BK = 64, 16-byte chunks of 8 bf16):
-//   row form (A, and B in NT form): row r holds K in 8 chunks; logical chunk
-//     c sits in slot c ^ ((r >> 1) & 7), so 16 consecutive rows read at one
-//     logical chunk hit 16 distinct 16-byte bank groups.
+// LDS layouts (16-byte chunks of 8 bf16; CH = BK / 8 chunks per K row):
+//   row form (A, and B in NT form): row r holds K in CH chunks; logical chunk
+//     c sits in slot c ^ ((r / (16 / CH)) % CH), so 16 consecutive rows read
+//     at one logical chunk hit 16 distinct 16-byte bank groups.
 //   NN form (B, K x N in memory): row k holds BN columns; chunk c (columns
-//     8c..8c+7) sits in slot c ^ (2 (k & 3)). MFMA fragments are read with
+//     8c..8c+7) sits in slot c ^ (4 (k & 3)), so the 32 lanes of one
+//     transpose read (4 rows x 4 chunks each) meet 16 distinct 16-byte bank
+//     groups. MFMA fragments are read with
 //     the gfx950 LDS transpose read (ds_read_b64_tr_b16): a group of 16 lanes
 //     whose lane i addresses row k0 + i / 4, columns n0 + 4 (i % 4) .. +3
 //     receives in lane j the four values (k0 .. k0 + 3, n0 + j).
@@ -716,27 +713,32 @@ __device__ __forceinline__ void lds_dma16(const bf16_t* g, char* base) {
 }
 #pragma clang diagnostic pop
 
-__device__ __forceinline__ int rowform_slot(int r, int c) { return c ^ ((r >> 1) & 7); }
-__device__ __forceinline__ int nnform_slot(int k, int c) { return c ^ (2 * (k & 3)); }
+template <int CH>
+__device__ __forceinline__ int rowform_slot(int r, int c) {
+  static_assert(CH == 4 || CH == 8, "K row of 4 or 8 chunks");
+  return c ^ ((r / (16 / CH)) & (CH - 1));
+}
+__device__ __forceinline__ int nnform_slot(int k, int c) { return c ^ (4 * (k & 3)); }
 
-// One K step (BK = 64) of MFMAs from LDS: four k-chunks, the fragments of
-// chunk g + 1 read while chunk g's MFMAs issue.
-template <int WM, int WN, int BN, bool B_NN>
+// One K step of MFMAs from LDS: BK / 16 k-chunks, the fragments of chunk
+// g + 1 read while chunk g's MFMAs issue.
+template <int WM, int WN, int BN, int BK, bool B_NN>
 __device__ __forceinline__ void load_frags_dma(const char* la, const char* lb, int g, u32x4_t (&a)[WM],
                                                u32x4_t (&b)[WN], int wm, int wn, int lane) {
+  constexpr int RB = 2 * BK, CH = BK / 8;   // bytes and chunks per K row
   const int r32 = lane & 31, h = lane >> 5;
   const int q = lane >> 4, j = lane & 15;
   const int c = 2 * g + h;
 #pragma unroll
   for (int i = 0; i < WM; ++i) {
     const int row = wm * WM * 32 + i * 32 + r32;
-    a[i] = ld16(la + row * 128 + (rowform_slot(row, c) << 4));
+    a[i] = ld16(la + row * RB + (rowform_slot<CH>(row, c) << 4));
   }
   if constexpr (!B_NN) {
 #pragma unroll
     for (int i = 0; i < WN; ++i) {
       const int row = wn * WN * 32 + i * 32 + r32;
-      b[i] = ld16(lb + row * 128 + (rowform_slot(row, c) << 4));
+      b[i] = ld16(lb + row * RB + (rowform_slot<CH>(row, c) << 4));
     }
   } else {
     const int k0 = 8 * (2 * g + (q >> 1)) + (j >> 2);
@@ -751,14 +753,16 @@ __device__ __forceinline__ void load_frags_dma(const char* la, const char* lb, i
   }
 }
 
-template <int WM, int WN, int BN, bool B_NN>
+template <int WM, int WN, int BN, int BK, bool B_NN>
 __device__ __forceinline__ void tile_mma_dma(const char* la, const char* lb, f32x16_t (&acc)[WM][WN], int wm,
                                              int wn, int lane) {
+  constexpr int G = BK / 16;
   u32x4_t a[2][WM], b[2][WN];
-  load_frags_dma<WM, WN, BN, B_NN>(la, lb, 0, a[0], b[0], wm, wn, lane);
+  load_frags_dma<WM, WN, BN, BK, B_NN>(la, lb, 0, a[0], b[0], wm, wn, lane);
 #pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    if (g + 1 < 4) load_frags_dma<WM, WN, BN, B_NN>(la, lb, g + 1, a[(g + 1) & 1], b[(g + 1) & 1], wm, wn, lane);
+  for (int g = 0; g < G; ++g) {
+    if (g + 1 < G)
+      load_frags_dma<WM, WN, BN, BK, B_NN>(la, lb, g + 1, a[(g + 1) & 1], b[(g + 1) & 1], wm, wn, lane);
 #pragma unroll
     for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
@@ -766,29 +770,36 @@ __device__ __forceinline__ void tile_mma_dma(const char* la, const char* lb, f32
   }
 }
 
+// LDS bytes of gemm_dma_kernel: the ring, or the row-wise epilogue's C tile
+// (rows padded to BN + 8 floats, so the two row groups a store instruction
+// covers fall in different banks) where that is larger.
+template <typename Cfg, bool ROWWISE>
+struct DmaLds {
+  static constexpr int RW_LD = Cfg::BN + 8;
+  static constexpr int RING = Cfg::STAGES * (Cfg::BM + Cfg::BN) * 2 * Cfg::BK;
+  static constexpr int CT = ROWWISE ? Cfg::BM * RW_LD * 4 : 0;
+  static constexpr int BYTES = RING > CT ? RING : CT;
+};
+
+// One output tile (linear tile id lid over the batch).
 template <typename Cfg, bool B_NN, bool SYM, typename Epi>
-__global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void
-gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, GemmShape sh, Epi epi) {
-  constexpr int BK = 64;
+__device__ __forceinline__ void gemm_dma_tile(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
+                                              const GemmShape& sh, const Epi& epi, char* lds, int lid) {
+  constexpr int BK = Cfg::BK, RB = 2 * BK, CH = BK / 8, RPL = 1024 / RB;   // rows per 1 KB load
   constexpr int BM = Cfg::BM, BN = Cfg::BN, WM = Cfg::WM, WN = Cfg::WN, S = Cfg::STAGES;
   constexpr int NW = Cfg::NWM * Cfg::NWN;
-  constexpr int A_BYTES = BM * 128, STAGE = (BM + BN) * 128;
-  constexpr int LA = BM / 8 / NW;          // A load instructions per wave per stage (8 rows each)
-  constexpr int LB = BN / 8 / NW;          // B: NT 8 rows each; NN 1 KB = 512 / BN rows each
+  constexpr int A_BYTES = BM * RB, STAGE = (BM + BN) * RB;
+  constexpr int LA = BM / RPL / NW;        // A load instructions (1 KB each) per wave per stage
+  constexpr int LB = BN / RPL / NW;        // B: NT RPL rows each; NN 1 KB = 512 / BN K rows each
   constexpr int LT = LA + LB;
-  static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "tile rows per wave");
-  static_assert(S >= 2 && LT * (S - 2) < 64, "stages");
+  static_assert(BK == 32 || BK == 64, "K step");
+  static_assert(BM % (RPL * NW) == 0 && BN % (RPL * NW) == 0, "tile rows per wave");
+  static_assert(S >= 2 && S <= 5 && LT * (S - 2) < 64, "stages");
   static_assert(!SYM || BM == BN, "symmetric tiling needs square tiles");
-  // the row-wise epilogue reuses the ring for the C tile, rows padded to
-  // BN + 8 floats (the two row groups a store instruction covers fall in
-  // different banks)
-  constexpr int RW_LD = BN + 8;
-  constexpr int RING = S * STAGE, CT = Epi::ROWWISE ? BM * RW_LD * 4 : 0;
-  __shared__ __attribute__((aligned(1024))) char lds[RING > CT ? RING : CT];
+  constexpr int RW_LD = DmaLds<Cfg, Epi::ROWWISE>::RW_LD;
 
   const int tiles_m = sh.M / BM, tiles_n = sh.N / BN;
   const int per = SYM ? tiles_m * (tiles_m + 1) / 2 : tiles_m * tiles_n;
-  const int lid = xcd_remap(blockIdx.x, per * sh.batch);
   const int b = lid / per;
   int t = lid - b * per, tm, tn;
   if (SYM) {
@@ -839,8 +850,8 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
 #pragma unroll
   for (int u = 0; u < LA; ++u) {
     const int qi = wave + NW * u;
-    const int row = 8 * qi + (lane >> 3);
-    const int ch = rowform_slot(row, lane & 7);   // slot -> logical chunk (xor is its own inverse)
+    const int row = RPL * qi + lane / CH;
+    const int ch = rowform_slot<CH>(row, lane % CH);   // slot -> logical chunk (xor is its own inverse)
     ga[u] = A + b * sh.sa + (long long)(m0 + row) * sh.lda + 8 * ch;
     la_off[u] = 1024 * qi;
   }
@@ -850,11 +861,12 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
   for (int u = 0; u < LB; ++u) {
     const int qi = wave + NW * u;
     if constexpr (!B_NN) {
-      const int row = 8 * qi + (lane >> 3);
-      const int ch = rowform_slot(row, lane & 7);
+      const int row = RPL * qi + lane / CH;
+      const int ch = rowform_slot<CH>(row, lane % CH);
       gb[u] = B + b * sh.sb + (long long)(n0 + row) * sh.ldb + 8 * ch;
     } else {
       constexpr int CPR = BN / 8;            // chunks per LDS row
+      static_assert(CPR >= 16, "the NN swizzle needs rows of at least 16 chunks");
       constexpr int RPI = 64 / CPR;          // rows per load instruction
       const int k = RPI * qi + lane / CPR;
       const int ch = nnform_slot(k, lane % CPR);
@@ -885,7 +897,12 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
   for (int kt = 0; kt < nk; ++kt) {
     // stage kt has landed once at most the later stages' loads are pending
     const int later = nk - 1 - kt < S - 2 ? nk - 1 - kt : S - 2;
-    if constexpr (S >= 4) {
+    if constexpr (S >= 5) {
+      if (later >= 3) wait_vmcnt<LT * 3>();
+      else if (later == 2) wait_vmcnt<LT * 2>();
+      else if (later == 1) wait_vmcnt<LT>();
+      else wait_vmcnt<0>();
+    } else if constexpr (S == 4) {
       if (later >= 2) wait_vmcnt<LT * 2>();
       else if (later == 1) wait_vmcnt<LT>();
       else wait_vmcnt<0>();
@@ -913,7 +930,7 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
         }
       }
     }
-    tile_mma_dma<WM, WN, BN, B_NN>(base, base + A_BYTES, acc, wm, wn, lane);
+    tile_mma_dma<WM, WN, BN, BK, B_NN>(base, base + A_BYTES, acc, wm, wn, lane);
   }
 
   if constexpr (ROWWISE) {
@@ -991,12 +1008,32 @@ gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, Gemm
   }
 }
 
+// The grid walks the tiles: work-group g takes tiles g, g + G, g + 2G, ...
+// (G = gridDim.x; G a multiple of 8 keeps every work-group on one XCD, and
+// xcd_remap gives each XCD a contiguous range of tiles). With G below the
+// tile count a work-group's stores of one tile drain while it computes the
+// next.
 template <typename Cfg, bool B_NN, bool SYM, typename Epi>
-void launch_gemm_dma(const bf16_t* A, const bf16_t* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
+__global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void
+gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, GemmShape sh, Epi epi) {
+  __shared__ __attribute__((aligned(1024))) char lds[DmaLds<Cfg, Epi::ROWWISE>::BYTES];
+  const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
+  const int total = (SYM ? tm * (tm + 1) / 2 : tm * tn) * sh.batch;
+  for (int it = blockIdx.x; it < total; it += gridDim.x) {
+    if (it != (int)blockIdx.x) __syncthreads();   // the previous tile's LDS reads are done
+    gemm_dma_tile<Cfg, B_NN, SYM, Epi>(A, B, sh, epi, lds, xcd_remap(it, total));
+  }
+}
+
+// max_blocks > 0 caps the grid (rounded down to a multiple of 8).
+template <typename Cfg, bool B_NN, bool SYM, typename Epi>
+void launch_gemm_dma(const bf16_t* A, const bf16_t* B, const GemmShape& sh, const Epi& epi, hipStream_t stream,
+                     int max_blocks = 0) {
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;
-  const long long blocks = per * sh.batch;
+  long long blocks = per * sh.batch;
   if (blocks <= 0) return;
+  if (max_blocks >= 8 && blocks > max_blocks) blocks = max_blocks / 8 * 8;
   hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi>), dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A, B,
                      sh, epi);
 }

@@ -31,7 +31,7 @@ struct LowRankArgs {
   long long so;
   int ldo;
   bf16_t* out16;      // optional bf16 copy of out (same layout)
-  int8_t* out_lo;     // with out16: 8-bit residual of out against bf16(out) (state_q8)
+  int8_t* out_lo;     // with out16: e4m3 residual byte of out against bf16(out) (state_pack8)
   float* sumsq;       // [b][tiles] or null
   int rows_pad, cols_pad, kmax, batch;
 };
@@ -122,10 +122,10 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
     if (ob) store8<TO>(ob + (long long)i * a.ldo + n0 + cg * 8, v);
     if (a.out16) store8<bf16_t>(a.out16 + b * a.so + (long long)i * a.ldo + n0 + cg * 8, v);
     if (a.out_lo) {
-      int q[8];
+      uint32_t nh[4];
 #pragma unroll
-      for (int c = 0; c < 8; ++c) q[c] = state_q8(v[c], bf2f(f2bf(v[c])));
-      *reinterpret_cast<u32x2_t*>(a.out_lo + b * a.so + (long long)i * a.ldo + n0 + cg * 8) = pack_q8(q);
+      for (int q = 0; q < 4; ++q) nh[q] = pack_bf2(v[2 * q], v[2 * q + 1]);
+      *reinterpret_cast<u32x2_t*>(a.out_lo + b * a.so + (long long)i * a.ldo + n0 + cg * 8) = state_pack8(v, nh);
     }
   }
   if (a.sumsq) {

@@ -27,6 +27,82 @@ def test_bf16_matches_library_rounding():
     np.testing.assert_array_equal(precision.round_bf16(x.astype(np.float64)), want)
 
 
+# --- e4m3 rounding (residual of the stored bf16 iterate) -------------------------
+def _e4m3_grid():
+    """Every finite OCP e4m3 ("fn") value from its bit layout: sign, 4-bit
+    exponent field (bias 7), 3-bit fraction; field 0 is subnormal, field 15
+    with fraction 7 is NaN."""
+    vals, codes = [], []
+    for b in range(256):
+        e, m = (b >> 3) & 0xF, b & 7
+        if e == 0xF and m == 7:
+            continue
+        v = (m / 8) * 2.0 ** -6 if e == 0 else (1 + m / 8) * 2.0 ** (e - 7)
+        vals.append(-v if b & 0x80 else v)
+        codes.append(b)
+    return np.array(vals), np.array(codes)
+
+
+def test_e4m3_matches_nearest_grid_value():
+    grid, codes = _e4m3_grid()
+    assert grid.max() == 448.0 and np.sort(np.abs(grid))[2] == 2.0 ** -9
+    g = np.random.default_rng(3)
+    pos = np.unique(np.abs(grid))
+    mids = (pos[1:] + pos[:-1]) / 2
+    x = np.concatenate([g.uniform(-448, 448, 20000), g.standard_normal(20000) * 10.0 ** g.uniform(-4, 2, 20000),
+                        mids, -mids, np.nextafter(mids, 0), np.nextafter(mids, 1e9), pos, -pos])
+    x = np.clip(x, -448, 448)
+    d = np.abs(x[:, None] - grid[None, :])
+    best = d.min(axis=1, keepdims=True)
+    tie_ok = (d == best)
+    # ties go to the even fraction (lowest code bit clear)
+    pick = np.where(tie_ok & ((codes[None, :] & 1) == 0), 1, 0) + np.where(tie_ok, 1, 0)
+    want = grid[np.argmax(pick, axis=1)]
+    got = precision.round_e4m3(x)
+    np.testing.assert_array_equal(np.abs(got), np.abs(want))
+    assert np.all((got == 0) | (np.sign(got) == np.sign(x)))
+
+
+def test_e4m3_matches_library_rounding():
+    g = np.random.default_rng(4)
+    x = np.clip(g.standard_normal(100000) * 10.0 ** g.uniform(-4, 2.5, 100000), -448, 448).astype(np.float32)
+    want = torch.from_numpy(x).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    np.testing.assert_array_equal(precision.round_e4m3(x.astype(np.float64)), want)
+    with pytest.raises(ValueError):
+        precision.round_e4m3(np.array([449.0]))
+
+
+def test_stored_state_residual():
+    from oracle.filters import STATE_SCALE, store_state
+    g = np.random.default_rng(5)
+    x = g.standard_normal(50000) * 10.0 ** g.uniform(-3, 0.2, 50000)
+    hi, carried = store_state(x)
+    np.testing.assert_array_equal(hi, precision.round_bf16(x))
+    r = (carried - hi) * STATE_SCALE
+    # the residual is an e4m3 value, within half a unit in its 4th bit of (x - hi) 2^16
+    grid, _ = _e4m3_grid()
+    assert np.isin(r, grid).all()
+    d = (x - hi) * STATE_SCALE
+    inside = np.abs(d) <= 448
+    normal = inside & (np.abs(d) >= 2.0 ** -6)
+    assert np.all(np.abs(r - d)[normal] <= np.abs(d)[normal] * 2.0 ** -4 * (1 + 1e-12))
+    assert np.all(np.abs(r - d)[np.abs(d) < 2.0 ** -6] <= 2.0 ** -10)
+    np.testing.assert_array_equal(r[~inside], np.sign(d[~inside]) * 448.0)
+    assert inside.mean() > 0.9
+    # round trip: an iterate already in stored form keeps its value (and its
+    # split, unless the residual rounded to half a bf16 unit, a tie of bf16)
+    hi2, carried2 = store_state(carried)
+    np.testing.assert_array_equal(carried2, carried)
+    half_ulp = np.abs(hi) * 2.0 ** -8   # at or above half a unit of hi
+    split_kept = np.abs(carried - hi) < np.ldexp(1.0, np.frexp(hi)[1] - 9)
+    assert split_kept.mean() > 0.9 and np.all(np.abs(carried - hi) <= half_ulp + 1e-300)
+    np.testing.assert_array_equal(hi2[split_kept], hi[split_kept])
+    # residuals past the format's range are clipped to +-448 2^-16
+    big = np.array([3.0 + 0.45 * 2.0 ** -6, -(3.0 + 0.45 * 2.0 ** -6)])   # residual 0.45 units of 2^-6
+    hb, cb = store_state(big)
+    np.testing.assert_array_equal(cb - hb, np.sign(big) * 448.0 / STATE_SCALE)
+
+
 # --- Gaussian generator ------------------------------------------------------------
 # Known-answer vectors of Philox4x32-10 published with the generator
 # (Salmon, Moraes, Dror, Shaw, SC 2011; Random123 distribution): counter,
