@@ -187,8 +187,10 @@ inline void ts_xw_dma(const bf16_t* X, long long sx, int ldx, int s_pad, int l_p
   ProfScope ps(SD_STAGE_SKETCH, st);
   GemmShape g{rq, s_pad, l_pad, l_pad, ldx, (long long)rq * l_pad, sx, batch};
   EpiStoreRows e{Pt, (long long)rq * s_pad, s_pad};
-  if (rq == 32) launch_gemm_dma<GemmCfg<1, 2, 1, 1, 2, 0>, false, false>(W16, X, g, e, st);
-  else launch_gemm_dma<GemmCfg<1, 2, 2, 1, 2, 0>, false, false>(W16, X, g, e, st);
+  // one wave per 32-column tile and a four-stage ring: the K loop is long
+  // (l_pad) and the grid small, so more loads per work-group stay in flight
+  if (rq == 32) launch_gemm_dma<GemmCfg<1, 1, 1, 1, 4, 0>, false, false>(W16, X, g, e, st);
+  else launch_gemm_dma<GemmCfg<1, 1, 2, 1, 4, 0>, false, false>(W16, X, g, e, st);
 }
 
 // Float64 partial Grams of panel rows over 128-position chunks.

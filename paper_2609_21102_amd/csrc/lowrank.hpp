@@ -37,25 +37,6 @@ struct LowRankArgs {
 };
 
 template <typename T>
-__device__ __forceinline__ void load8(const T* p, float v[8]);
-template <>
-__device__ __forceinline__ void load8<bf16_t>(const bf16_t* p, float v[8]) {
-  const uint4 u = *reinterpret_cast<const uint4*>(p);
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    v[2 * i] = __uint_as_float(w[i] << 16);
-    v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
-  }
-}
-template <>
-__device__ __forceinline__ void load8<float>(const float* p, float v[8]) {
-  const float4 a = *reinterpret_cast<const float4*>(p);
-  const float4 b = *reinterpret_cast<const float4*>(p + 4);
-  v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
-  v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
-}
-template <typename T>
 __device__ __forceinline__ void store8(T* p, const float v[8]);
 template <>
 __device__ __forceinline__ void store8<bf16_t>(bf16_t* p, const float v[8]) {
@@ -68,8 +49,38 @@ __device__ __forceinline__ void store8<float>(float* p, const float v[8]) {
   *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
 }
 
+// Eight consecutive elements as loaded (raw bits), converted after the wait.
+template <typename T>
+struct Raw8;
+template <>
+struct Raw8<bf16_t> {
+  uint4 u;
+  __device__ __forceinline__ void load(const bf16_t* p) { u = *reinterpret_cast<const uint4*>(p); }
+  __device__ __forceinline__ void get(float v[8]) const {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+    }
+  }
+};
+template <>
+struct Raw8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* p) {
+    a = *reinterpret_cast<const float4*>(p);
+    b = *reinterpret_cast<const float4*>(p + 4);
+  }
+  __device__ __forceinline__ void get(float v[8]) const {
+    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+  }
+};
+
 // 128 x 128 tile per work-group; thread t owns rows 8 (t / 16) .. +7 and
-// columns 8 (t % 16) .. +7.
+// columns 8 (t % 16) .. +7. The thread's X values are loaded first, so their
+// latency overlaps the staging of the low-rank panels.
 template <typename TX, typename TO, int KM>
 __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
   __shared__ __attribute__((aligned(16))) float ls[KM][128];
@@ -82,13 +93,17 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
   const int kk = a.kk ? a.kk[b] : a.kconst;
   const float alpha = a.alpha ? a.alpha[b] : 1.f;
   const int tid = threadIdx.x;
+  const int rg = tid >> 4, cg = tid & 15;
+  const TX* xb = reinterpret_cast<const TX*>(a.x) + b * a.sx;
+  Raw8<TX> xr[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) xr[r].load(xb + (long long)(i0 + rg * 8 + r) * a.ldx + n0 + cg * 8);
   for (int e = tid; e < kk * 128; e += 256) {
     const int j = e >> 7, x = e & 127;
     ls[j][x] = a.L[b * a.sl + (long long)j * a.ldl + i0 + x] * a.coef[b * a.kmax + j];
     rs[j][x] = a.Rr[b * a.sr + (long long)j * a.ldr + n0 + x];
   }
   __syncthreads();
-  const int rg = tid >> 4, cg = tid & 15;
   float acc[8][8];
 #pragma unroll
   for (int r = 0; r < 8; ++r)
@@ -106,26 +121,26 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
 #pragma unroll
       for (int c = 0; c < 8; ++c) acc[r][c] = fmaf(lv[r], rv[c], acc[r][c]);
   }
-  const TX* xb = reinterpret_cast<const TX*>(a.x) + b * a.sx;
   TO* ob = a.out ? reinterpret_cast<TO*>(a.out) + b * a.so : nullptr;
   float ss = 0.f;
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
     const int i = i0 + rg * 8 + r;
     float v[8];
-    load8<TX>(xb + (long long)i * a.ldx + n0 + cg * 8, v);
+    xr[r].get(v);
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
       v[c] = fmaf(alpha, v[c], acc[r][c]);
       ss = fmaf(v[c], v[c], ss);
     }
     if (ob) store8<TO>(ob + (long long)i * a.ldo + n0 + cg * 8, v);
-    if (a.out16) store8<bf16_t>(a.out16 + b * a.so + (long long)i * a.ldo + n0 + cg * 8, v);
-    if (a.out_lo) {
+    if (a.out16) {
       uint32_t nh[4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) nh[q] = pack_bf2(v[2 * q], v[2 * q + 1]);
-      *reinterpret_cast<u32x2_t*>(a.out_lo + b * a.so + (long long)i * a.ldo + n0 + cg * 8) = state_pack8(v, nh);
+      const long long o = b * a.so + (long long)i * a.ldo + n0 + cg * 8;
+      st16_nt(a.out16 + o, u32x4_t{nh[0], nh[1], nh[2], nh[3]});
+      if (a.out_lo) st8_nt(a.out_lo + o, state_pack8(v, nh));
     }
   }
   if (a.sumsq) {
