@@ -24,8 +24,6 @@ struct SmallLds {
   double h2[SM_MAX][SM_LD];       // second buffers: a Jacobi round reads one
   double e2[SM_MAX][SM_LD];       // pair of buffers and writes the other
   double rot_c[SM_MAX], rot_d[SM_MAX];   // per index: coefficient on itself / on its partner
-  int rot_p[SM_MAX];              // per index: partner in this round
-  int rot_z[SM_MAX];              // per index: its pair is annihilated this round
   double red[SM_THREADS / WAVE];
   double key[SM_MAX];
   int perm[SM_MAX];
@@ -38,11 +36,49 @@ struct SmallLds {
 // columns. Each round rotates n/2 disjoint pairs (circle-method ordering;
 // rotation angles as in Golub & Van Loan, sym.schur2) and applies all of them
 // in one pass: with R the round's rotation, H' = R^T H R and E' = E R are
-// written entry by entry into the second buffers, the annihilated pairs as
-// exact zeros. A pair is skipped when |h_ij| <= 2^-50 sqrt(|h_ii h_jj|) or
-// |h_ij| <= 2^-48 ||H||_F (below what the rounding of the rotations leaves
-// behind); sweeps stop after one that rotates nothing, or after 40.
-static __device__ void jacobi_eig(SmallLds& s, int n) {
+// written entry by entry into the second buffers. A pair is skipped when
+// h_ij^2 <= 2^-100 |h_ii h_jj| or |h_ij| <= 2^tol_exp ||H||_F (the default
+// 2^-48 is below what the rounding of the rotations leaves behind); sweeps
+// stop after one that rotates nothing, or after 40.
+// The angle is chosen in float32 (the round's serial latency is this chain;
+// float64 square roots and divisions made it several times longer) on the
+// pair's entries scaled by a power of two, and (c, s) are then renormalized
+// in float64 by one Newton step for 1 / sqrt(c^2 + s^2), so every rotation is
+// orthogonal to float64 rounding. The annihilated entry is left to the
+// rotation (about 1e-7 of its size instead of zero); later sweeps take it out.
+__device__ __forceinline__ void jacobi_angle(double aii, double ajj, double aij, double& c, double& sn) {
+  const double d = ajj - aii;
+  const double m = fmax(fabs(d), fabs(2.0 * aij));
+  const int ex = __builtin_amdgcn_frexp_exp(m);   // m = f 2^ex, f in [0.5, 1)
+  const float df = (float)__builtin_amdgcn_ldexp(d, -ex), af = (float)__builtin_amdgcn_ldexp(aij, -ex);
+  // df^2 + 4 af^2 lies in [0.25, 2]: the raw square root and reciprocal apply
+  const float r = __builtin_amdgcn_sqrtf(df * df + 4.f * af * af);
+  const float t = (df >= 0.f ? 2.f * af : -2.f * af) * __builtin_amdgcn_rcpf(fabsf(df) + r);
+  const float cf = __builtin_amdgcn_rsqf(1.f + t * t);
+  c = (double)cf;
+  sn = (double)t * c;
+  const double q = 1.5 - 0.5 * (c * c + sn * sn);   // Newton step of 1 / sqrt(c^2 + s^2) from 1
+  c *= q;
+  sn *= q;
+}
+
+// Partner of index a in round r of the circle method over N (even) indices:
+// index 0 meets 1 + (r - 1) mod (N - 1); indices x + 1, y + 1 (x != y) meet
+// when x + y = 2 (r - 1) mod (N - 1); the one with 2x = 2(r - 1) meets 0.
+// (No integer division: r and a - 1 lie in [0, N - 2], so y starts in
+// [-N, 2N - 6] and two conditional additions and one subtraction reduce it.)
+__device__ __forceinline__ int jacobi_partner(int a, int r, int N) {
+  const int m = N - 1;
+  if (a == 0) return r == 0 ? m : r;
+  const int x = a - 1;
+  int y = 2 * r - 2 - x;
+  y += y < 0 ? m : 0;
+  y += y < 0 ? m : 0;
+  y -= y >= m ? m : 0;
+  return y == x ? 0 : y + 1;
+}
+
+static __device__ void jacobi_eig(SmallLds& s, int n, int tol_exp = -48) {
   const int tid = threadIdx.x, nt = blockDim.x;
   for (int e = tid; e < n * n; e += nt) {
     const int i = e / n, j = e - i * n;
@@ -55,57 +91,51 @@ static __device__ void jacobi_eig(SmallLds& s, int n) {
   double fro = 0.0;
   for (int e = tid; e < n * n; e += nt) fro += s.h[e / n][e % n] * s.h[e / n][e % n];
   fro = block_sum(fro, s.red);
-  const double abs_floor = 0x1p-48 * sqrt(fro);
+  const double abs_floor = __builtin_amdgcn_ldexp(sqrt(fro), tol_exp);
   double(*H)[SM_LD] = s.h;
   double(*E)[SM_LD] = s.e;
   double(*H2)[SM_LD] = s.h2;
   double(*E2)[SM_LD] = s.e2;
+  // this thread's entries in the update: column b of rows a0, a0 + rows_per_pass, ...
+  const int rows_per_pass = nt / n, b = tid % n;
+  const int a0 = tid < rows_per_pass * n ? tid / n : n;
   for (int sweep = 0; sweep < 40; ++sweep) {
     if (tid == 0) s.rotated = 0;
     __syncthreads();
     for (int r = 0; r < N - 1; ++r) {
       if (tid < half) {
-        const int pa = (tid == 0) ? 0 : ((r + tid - 1) % (N - 1)) + 1;
-        const int pb = ((r + N - 2 - tid) % (N - 1)) + 1;
+        // pair of this thread: 1 + (r + tid - 1) mod (N - 1) (0 for thread 0)
+        // and 1 + (r + N - 2 - tid) mod (N - 1); both sums lie in [0, 2N - 4]
+        const int m = N - 1;
+        int u = r + tid - 1, w = r + m - 1 - tid;
+        u -= u >= m ? m : 0;
+        w -= w >= m ? m : 0;
+        const int pa = tid == 0 ? 0 : u + 1, pb = w + 1;
         const int i = pa < pb ? pa : pb, j = pa < pb ? pb : pa;
         if (j < n) {
           double c = 1.0, sn = 0.0;
-          int rot = 0;
           const double aij = H[i][j], aii = H[i][i], ajj = H[j][j];
-          if (fabs(aij) > 0x1p-50 * sqrt(fabs(aii) * fabs(ajj)) && fabs(aij) > abs_floor) {
-            const double tau = (ajj - aii) / (2.0 * aij);
-            double t;
-            if (fabs(tau) > 1e150) t = 0.5 / tau;
-            else t = (tau >= 0.0 ? 1.0 : -1.0) / (fabs(tau) + sqrt(1.0 + tau * tau));
-            c = 1.0 / sqrt(1.0 + t * t);
-            sn = t * c;
-            rot = 1;
+          if (aij * aij > 0x1p-100 * fabs(aii * ajj) && fabs(aij) > abs_floor) {
+            jacobi_angle(aii, ajj, aij, c, sn);
             s.rotated = 1;
           }
           // column i <- c col_i - s col_j ; column j <- s col_i + c col_j
-          s.rot_p[i] = j;
           s.rot_c[i] = c;
           s.rot_d[i] = -sn;
-          s.rot_z[i] = rot;
-          s.rot_p[j] = i;
           s.rot_c[j] = c;
           s.rot_d[j] = sn;
-          s.rot_z[j] = rot;
         } else if (i < n) {   // paired with the padding index: unchanged
-          s.rot_p[i] = i;
           s.rot_c[i] = 1.0;
           s.rot_d[i] = 0.0;
-          s.rot_z[i] = 0;
         }
       }
       __syncthreads();
-      for (int e = tid; e < n * n; e += nt) {
-        const int a = e / n, b = e - a * n;
-        const int qa = s.rot_p[a], qb = s.rot_p[b];
+      for (int a = a0; a < n; a += rows_per_pass) {
+        int qa = jacobi_partner(a, r, N), qb = jacobi_partner(b, r, N);
+        qa = qa < n ? qa : a;   // paired with the padding index: unchanged
+        qb = qb < n ? qb : b;
         const double ca = s.rot_c[a], da = s.rot_d[a], cb = s.rot_c[b], db = s.rot_d[b];
-        double v = ca * (cb * H[a][b] + db * H[a][qb]) + da * (cb * H[qa][b] + db * H[qa][qb]);
-        if (s.rot_z[a] && b == qa) v = 0.0;
-        H2[a][b] = v;
+        H2[a][b] = ca * (cb * H[a][b] + db * H[a][qb]) + da * (cb * H[qa][b] + db * H[qa][qb]);
         E2[a][b] = cb * E[a][b] + db * E[a][qb];
       }
       __syncthreads();
@@ -381,7 +411,9 @@ static __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const doubl
   __shared__ SmallLds s;
   const int tid = threadIdx.x, b = blockIdx.x;
   gram_reduce(s, part + (long long)b * nch * gram_items(rp, rp, true), nch, rp, rp, true);
-  jacobi_eig(s, rp);
+  // off-diagonal floor 2^-40 ||H||_F: the outputs are float32, and the
+  // leading eigenvectors move by at most that over the gap to the rest
+  jacobi_eig(s, rp, -40);
   if (tid < rp) s.key[tid] = s.h[tid][tid];
   __syncthreads();
   sort_desc(s, rp);
