@@ -106,14 +106,15 @@ struct EpiGram {
     for (int q = 0; q < 8; ++q) mv[q] = v[q] * scale16;
     if (out16) store8(b, r, c0, mv);
     if (out32) {
-      *reinterpret_cast<f32x4_t*>(out32 + o) = f32x4_t{v[0], v[1], v[2], v[3]} * scale32;
-      *reinterpret_cast<f32x4_t*>(out32 + o + 4) = f32x4_t{v[4], v[5], v[6], v[7]} * scale32;
+      const f32x4_t w0 = f32x4_t{v[0], v[1], v[2], v[3]} * scale32, w1 = f32x4_t{v[4], v[5], v[6], v[7]} * scale32;
+      st16_nt(out32 + o, __builtin_bit_cast(u32x4_t, w0));
+      st16_nt(out32 + o + 4, __builtin_bit_cast(u32x4_t, w1));
     }
   }
   __device__ void store8(int b, int r, int c0, const float (&v)[8]) const {
     if (out16)
-      st16(out16 + b * stride + (long long)r * ld + c0,
-           u32x4_t{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])});
+      st16_nt(out16 + b * stride + (long long)r * ld + c0,
+              u32x4_t{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])});
   }
   float* out32;
   bf16_t* out16;
@@ -144,24 +145,27 @@ struct EpiPoly {
   long long stride;
   int ld;
   // Row-wise form (direct-to-LDS kernel): eight consecutive columns of row r.
-  // A32 is read only here; the transposed copy reuses the values (store8).
-  __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
-  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&,
-                         float (&w)[8]) const {
+  // The A32 values are loaded before the main loop (pre8: columns c0..c0+3
+  // in the first word group, c0+4..c0+7 in the second); the transposed copy
+  // reuses the values (store8).
+  __device__ void pre8(int b, int r, int c0, u32x4_t& h, u32x4_t& l) const {
     const long long o = b * stride + (long long)r * ld + c0;
-    const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(a32 + o);
-    const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(a32 + o + 4);
+    h = ld16(a32 + o);
+    l = ld16(a32 + o + 4);
+  }
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t& h, const u32x4_t& l,
+                         float (&w)[8]) const {
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      w[q] = bc * a0[q] + cc * v[q];
-      w[q + 4] = bc * a1[q] + cc * v[q + 4];
+      w[q] = bc * __uint_as_float(h[q]) + cc * v[q];
+      w[q + 4] = bc * __uint_as_float(l[q]) + cc * v[q + 4];
     }
     store8(b, r, c0, w);
   }
   __device__ void store8(int b, int r, int c0, const float (&w)[8]) const {
     const long long o = b * stride + (long long)r * ld + c0;
     if constexpr (sizeof(TO) == 2) {
-      st16(out + o, u32x4_t{pack_bf2(w[0], w[1]), pack_bf2(w[2], w[3]), pack_bf2(w[4], w[5]), pack_bf2(w[6], w[7])});
+      st16_nt(out + o, u32x4_t{pack_bf2(w[0], w[1]), pack_bf2(w[2], w[3]), pack_bf2(w[4], w[5]), pack_bf2(w[6], w[7])});
     } else {
       *reinterpret_cast<f32x4_t*>(out + o) = f32x4_t{w[0], w[1], w[2], w[3]};
       *reinterpret_cast<f32x4_t*>(out + o + 4) = f32x4_t{w[4], w[5], w[6], w[7]};
@@ -1008,32 +1012,25 @@ __device__ __forceinline__ void gemm_dma_tile(const bf16_t* __restrict__ A, cons
   }
 }
 
-// The grid walks the tiles: work-group g takes tiles g, g + G, g + 2G, ...
-// (G = gridDim.x; G a multiple of 8 keeps every work-group on one XCD, and
-// xcd_remap gives each XCD a contiguous range of tiles). With G below the
-// tile count a work-group's stores of one tile drain while it computes the
-// next.
+// One work-group per tile (xcd_remap gives each XCD a contiguous range of
+// tiles, so work-groups that share operand panels share an L2). A variant
+// that walked several tiles per work-group measured no faster and needed
+// about 20-100 more VGPRs.
 template <typename Cfg, bool B_NN, bool SYM, typename Epi>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void
 gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, GemmShape sh, Epi epi) {
   __shared__ __attribute__((aligned(1024))) char lds[DmaLds<Cfg, Epi::ROWWISE>::BYTES];
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const int total = (SYM ? tm * (tm + 1) / 2 : tm * tn) * sh.batch;
-  for (int it = blockIdx.x; it < total; it += gridDim.x) {
-    if (it != (int)blockIdx.x) __syncthreads();   // the previous tile's LDS reads are done
-    gemm_dma_tile<Cfg, B_NN, SYM, Epi>(A, B, sh, epi, lds, xcd_remap(it, total));
-  }
+  gemm_dma_tile<Cfg, B_NN, SYM, Epi>(A, B, sh, epi, lds, xcd_remap(blockIdx.x, total));
 }
 
-// max_blocks > 0 caps the grid (rounded down to a multiple of 8).
 template <typename Cfg, bool B_NN, bool SYM, typename Epi>
-void launch_gemm_dma(const bf16_t* A, const bf16_t* B, const GemmShape& sh, const Epi& epi, hipStream_t stream,
-                     int max_blocks = 0) {
+void launch_gemm_dma(const bf16_t* A, const bf16_t* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;
-  long long blocks = per * sh.batch;
+  const long long blocks = per * sh.batch;
   if (blocks <= 0) return;
-  if (max_blocks >= 8 && blocks > max_blocks) blocks = max_blocks / 8 * 8;
   hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi>), dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A, B,
                      sh, epi);
 }
