@@ -208,23 +208,22 @@ inline size_t gram_part_elems(int batch, int len_pad, int ca, int cb, bool sym) 
   return (size_t)batch * (len_pad / GP_CHUNK) * gram_items(ca, cb, sym);
 }
 
-// One CholeskyQR pass on every panel of the batch, in place.
+// One CholeskyQR pass on every panel of the batch, in place (plus the bf16
+// copy of Q, with rows c .. c16 - 1 zero).
 inline void cholqr(float* Pt, long long sp, int ld, int c, int len_pad, int batch, double* part, double* fac,
-                   int* status, hipStream_t st, bf16_t* Pt16 = nullptr) {
+                   int* status, hipStream_t st, bf16_t* Pt16 = nullptr, int c16 = 0) {
   ProfScope ps(SD_STAGE_CHOLQR, st);
   gram_partials(Pt, sp, ld, Pt, sp, ld, c, c, len_pad, true, part, batch, st);
-  if (c <= 16)
-    hipLaunchKernelGGL((chol_factor_wave_kernel<16>), dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac,
-                       status);
-  else if (c <= 32)
-    hipLaunchKernelGGL((chol_factor_wave_kernel<32>), dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac,
-                       status);
-  else
-    hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(64), 0, st, part, len_pad / GP_CHUNK, c, fac, status);
+  const int nch = len_pad / GP_CHUNK;
   const dim3 g((len_pad / 128) * batch), b(128);
-  if (c <= 16) hipLaunchKernelGGL((chol_apply_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16);
-  else if (c <= 32) hipLaunchKernelGGL((chol_apply_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16);
-  else hipLaunchKernelGGL((chol_apply_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16);
+  if (c <= 16) {
+    hipLaunchKernelGGL((chol_qr_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, part, nch, status, Pt16, c16);
+  } else if (c <= 32) {
+    hipLaunchKernelGGL((chol_qr_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, part, nch, status, Pt16, c16);
+  } else {
+    hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(64), 0, st, part, nch, c, fac, status);
+    hipLaunchKernelGGL((chol_apply_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16, c16);
+  }
 }
 
 inline void rotate(const float* in, long long si, int ldi, const float* E, long long se, const float* scale,

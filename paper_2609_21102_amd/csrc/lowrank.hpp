@@ -98,10 +98,24 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
   Raw8<TX> xr[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) xr[r].load(xb + (long long)(i0 + rg * 8 + r) * a.ldx + n0 + cg * 8);
-  for (int e = tid; e < kk * 128; e += 256) {
-    const int j = e >> 7, x = e & 127;
-    ls[j][x] = a.L[b * a.sl + (long long)j * a.ldl + i0 + x] * a.coef[b * a.kmax + j];
-    rs[j][x] = a.Rr[b * a.sr + (long long)j * a.ldr + n0 + x];
+  // low-rank panels: every load is issued before the first LDS store
+  {
+    constexpr int PER = KM * 128 / 256;
+    float lv[PER], rv[PER];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + 256 * u, j = e >> 7, x = e & 127;
+      lv[u] = j < kk ? a.L[b * a.sl + (long long)j * a.ldl + i0 + x] * a.coef[b * a.kmax + j] : 0.f;
+      rv[u] = j < kk ? a.Rr[b * a.sr + (long long)j * a.ldr + n0 + x] : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int e = tid + 256 * u, j = e >> 7, x = e & 127;
+      if (j < kk) {
+        ls[j][x] = lv[u];
+        rs[j][x] = rv[u];
+      }
+    }
   }
   __syncthreads();
   float acc[8][8];

@@ -51,7 +51,6 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   p.om = ar.take<float>(B * rq * p.s_pad);
   p.yl = ar.take<float>(B * rq * p.l_pad);
   p.ys = ar.take<float>(B * rq * p.s_pad);
-  // (taken back to back: run_msign zeroes om16 .. ys16 with one fill)
   p.om16 = bf ? ar.take<bf16_t>(B * rq * p.s_pad) : nullptr;
   p.yl16 = bf ? ar.take<bf16_t>(B * rq * p.l_pad) : nullptr;
   p.ys16 = bf ? ar.take<bf16_t>(B * rq * p.s_pad) : nullptr;
@@ -158,22 +157,17 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     const int rp = p.rp, rq = p.rq, s_pad = p.s_pad, l_pad = p.l_pad;
     const long long so = (long long)rq * s_pad, sl_ = (long long)rq * l_pad;
     constexpr bool BF = sizeof(T) == 2;
-    fill(p.om, so * B, 0.f, st);
-    if constexpr (BF) {
-      // zero the bf16 copies (their rows past rp stay zero); plan_msign takes
-      // them back to back, so one fill spans all three
-      char* lo = reinterpret_cast<char*>(p.om16);
-      char* hi = reinterpret_cast<char*>(p.ys16 + so * B);
-      fill(reinterpret_cast<float*>(lo), (long long)(hi - lo) / 4, 0.f, st);
-    }
+    // the sketch kernels write the whole padded panels (zero rows past rp,
+    // zero columns past s); the CholQR passes write the bf16 copies of Q
+    // likewise, so no panel needs clearing first
     if (o.sketch) {
-      const long long tot = (long long)p.s * rp * B;
-      hipLaunchKernelGGL(sketch_copy_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, o.sketch, p.s, rp, B,
-                         p.om16);
+      const long long tot = (long long)rq * s_pad * B;
+      hipLaunchKernelGGL(sketch_copy_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, o.sketch, p.s, rp, rq,
+                         B, BF ? p.om16 : nullptr);
     } else {
-      const long long tot = (((long long)p.s * rp + 3) / 4) * B;
-      hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, p.s, rp, o.seed, B,
-                         p.om16);
+      const long long tot = (long long)rq * (s_pad / 4) * B;
+      hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, p.s, rp, rq, o.seed, B,
+                         BF ? p.om16 : nullptr);
     }
     auto xtw = [&](const float* w, const bf16_t* w16, float* out) {
       if constexpr (BF) ts_xtw_dma(reinterpret_cast<const bf16_t*>(xc), sx, ldx, s_pad, l_pad, w16, rq, out, B, st);
@@ -184,25 +178,30 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
       else ts_xw<T>(xc, sx, ldx, s_pad, l_pad, w, sl_, l_pad, rp, out, so, s_pad, B, st);
     };
     xtw(p.om, p.om16, p.yl);
-    cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st, p.yl16);
+    cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st, p.yl16, rq);
     for (int j = 0; j < o.power_iters; ++j) {
       xw(p.yl, p.yl16, p.ys);
-      cholqr(p.ys, so, s_pad, rp, s_pad, B, p.part, p.fac, o.status_dev, st, p.ys16);
+      cholqr(p.ys, so, s_pad, rp, s_pad, B, p.part, p.fac, o.status_dev, st, p.ys16, rq);
       xtw(p.ys, p.ys16, p.yl);
-      cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st, p.yl16);
+      cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st, p.yl16, rq);
     }
     xw(p.yl, p.yl16, p.ys);   // G = (X Q)^T
     {
       ProfScope ps(SD_STAGE_SMALL, st);
       gram_partials(p.ys, so, s_pad, p.ys, so, s_pad, rp, rp, s_pad, true, p.part, B, st);   // G G^T
-      hipLaunchKernelGGL(svd_head_kernel, dim3(B), dim3(SM_THREADS), 0, st, p.part, s_pad / GP_CHUNK, rp, p.k, o.tau, p.E,
-                         p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out);
+#define SD_HEAD(NPV)                                                                                       \
+  hipLaunchKernelGGL(svd_head_kernel<NPV>, dim3(B), dim3(SM_THREADS), 0, st, p.part, s_pad / GP_CHUNK, rp, p.k, \
+                     o.tau, p.E, p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out, p.ys, so, s_pad, p.yl, sl_,  \
+                     l_pad, p.Ls, p.Ll)
+      switch (jacobi_class(rp)) {
+        case 4: SD_HEAD(4); break;
+        case 8: SD_HEAD(8); break;
+        case 12: SD_HEAD(12); break;
+        case 16: SD_HEAD(16); break;
+        default: SD_HEAD(0); break;
+      }
+#undef SD_HEAD
     }
-    // V = G^T E / s (short side), U = Q E (long side)
-    rotate(p.ys, so, s_pad, p.E, (long long)rp * p.k, p.invsv, p.k, p.Ls, (long long)p.k * s_pad, s_pad, rp, p.k,
-           s_pad, B, st);
-    rotate(p.yl, sl_, l_pad, p.E, (long long)rp * p.k, nullptr, 0, p.Ll, (long long)p.k * l_pad, l_pad, rp, p.k,
-           l_pad, B, st);
   } else if (o.k_eff_out) {
     hipLaunchKernelGGL(fill_int_kernel, grid1(B, 256), dim3(256), 0, st, o.k_eff_out, (long long)B, 0);
   }
@@ -212,10 +211,10 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   la.x = xc;
   la.sx = sx;
   la.ldx = ldx;
-  la.L = p.Ls;
+  la.L = p.Ls;   // V = G^T E / s, [k][s_pad]
   la.sl = (long long)p.k * p.s_pad;
   la.ldl = p.s_pad;
-  la.Rr = p.Ll;
+  la.Rr = p.Ll;  // U = Q E, [k][l_pad]
   la.sr = (long long)p.k * p.l_pad;
   la.ldr = p.l_pad;
   la.kk = p.k > 0 ? p.keff : nullptr;
@@ -420,8 +419,8 @@ int sd_msign_deflated_ex(int batch, int m, int n, int k, int steps, const float*
 
 int sd_sketch(int batch, int s, int rp, uint64_t seed, float* out, hipStream_t stream) {
   if (batch < 1 || s < 1 || rp < 1 || !out) return SD_ERR_INVALID_ARG;
-  const long long tot = (((long long)s * rp + 3) / 4) * batch;
-  hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, stream, out, (long long)s * rp, s, s, rp, seed,
+  const long long tot = (long long)rp * ((s + 3) / 4) * batch;
+  hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, stream, out, (long long)s * rp, s, s, rp, rp, seed,
                      batch, (bf16_t*)nullptr);
   return hip_status();
 }

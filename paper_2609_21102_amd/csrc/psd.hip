@@ -126,6 +126,7 @@ __global__ __launch_bounds__(1024) void lanczos_step_kernel(float* Q, int n_pad,
 }
 
 // Largest Ritz pair of the tridiagonal matrix: rho and v = Q y.
+template <int NP>
 __global__ __launch_bounds__(SM_THREADS) void lanczos_ritz_kernel(const float* Q, int n_pad, float* v,
                                                                   LanczosState* st) {
   __shared__ SmallLds s;
@@ -140,7 +141,7 @@ __global__ __launch_bounds__(SM_THREADS) void lanczos_ritz_kernel(const float* Q
     s.h[i][j] = val;
   }
   __syncthreads();
-  jacobi_eig(s, kk);
+  jacobi_eig_any<NP>(s, kk);
   if (tid == 0) {
     int best = 0;
     for (int i = 1; i < kk; ++i)
@@ -267,7 +268,13 @@ static void lanczos(const PsdPlan& p, const float* R, uint64_t seed, float* thet
     hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.t, p.w);
     hipLaunchKernelGGL(lanczos_step_kernel, dim3(1), dim3(1024), 0, st, p.qlan, np, p.w, j, p.lz, p.lst);
   }
-  hipLaunchKernelGGL(lanczos_ritz_kernel, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst);
+  switch (jacobi_class(p.lz)) {   // the run may stop early: kk <= lz
+    case 4: hipLaunchKernelGGL(lanczos_ritz_kernel<4>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
+    case 8: hipLaunchKernelGGL(lanczos_ritz_kernel<8>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
+    case 12: hipLaunchKernelGGL(lanczos_ritz_kernel<12>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
+    case 16: hipLaunchKernelGGL(lanczos_ritz_kernel<16>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
+    default: hipLaunchKernelGGL(lanczos_ritz_kernel<0>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
+  }
   hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.v, p.t);
   hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.t, p.w);
   hipLaunchKernelGGL(lanczos_theta_kernel, dim3(1), dim3(1024), 0, st, p.w, p.v, np, p.lst, p.theta, p.alpha_x0,
@@ -309,9 +316,18 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     {
       ProfScope ps(SD_STAGE_SMALL, st);
       gram_partials(vt, 0, np, zt, 0, np, K, K, np, false, p.part, 1, st);   // V^T (Z V)
-      hipLaunchKernelGGL(ritz_kernel, dim3(1), dim3(SM_THREADS), 0, st, p.part, np / GP_CHUNK, K, o.tau, o.window, o.gamma,
-                         p.E, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out, o.n_deflated_out,
-                         o.n_positive_out);
+#define SD_RITZ(NPV)                                                                                            \
+  hipLaunchKernelGGL(ritz_kernel<NPV>, dim3(1), dim3(SM_THREADS), 0, st, p.part, np / GP_CHUNK, K, o.tau, o.window, \
+                     o.gamma, p.E, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out, o.n_deflated_out,          \
+                     o.n_positive_out)
+      switch (jacobi_class(K)) {
+        case 4: SD_RITZ(4); break;
+        case 8: SD_RITZ(8); break;
+        case 12: SD_RITZ(12); break;
+        case 16: SD_RITZ(16); break;
+        default: SD_RITZ(0); break;
+      }
+#undef SD_RITZ
     }
     rotate(vt, 0, np, p.E, 0, nullptr, 0, p.ut, 0, np, K, K, np, 1, st);
     // R = Z - U diag(lam) U^T

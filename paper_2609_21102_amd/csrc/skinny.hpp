@@ -211,40 +211,52 @@ struct Philox {
   }
 };
 
-// Omega^T [rp][ld] for every matrix: entry (i, j) of the s x rp sketch is
-// Gaussian number j * s + i of stream 1. Rows beyond s are zero.
-static __global__ void sketch_kernel(float* __restrict__ Wt, long long sw, int ld, int s, int rp,
-                              uint64_t seed, int batch, bf16_t* __restrict__ Wt16) {
-  const long long per = ((long long)s * rp + 3) / 4;
+// Omega^T as a [rows][ld] panel for every matrix: entry (i, j) of the s x rp
+// sketch is Gaussian number j * s + i of stream 1 (four per Philox call);
+// every other entry of the panel (rows rp .. rows - 1, columns s .. ld - 1)
+// is written as zero. One thread per four consecutive columns of a row.
+static __global__ void sketch_kernel(float* __restrict__ Wt, long long sw, int ld, int s, int rp, int rows,
+                                     uint64_t seed, int batch, bf16_t* __restrict__ Wt16) {
+  const int quads = (ld + 3) / 4;
+  const long long per = (long long)rows * quads;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= per * batch) return;
   const int b = (int)(gid / per);
-  const uint32_t call = (uint32_t)(gid - (long long)b * per);
-  float z[4];
-  Philox::normals(z, call, (uint32_t)b, 1u, seed);
-  float* Wb = Wt + b * sw;
+  const int rem = (int)(gid - (long long)b * per);
+  const int j = rem / quads, i0 = 4 * (rem - j * quads);
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  if (j < rp && i0 < s) {
+    const long long g0 = (long long)j * s + i0;
+    const uint32_t c0 = (uint32_t)(g0 >> 2);
+    const int off = (int)(g0 & 3), nv = s - i0 < 4 ? s - i0 : 4;
+    float z[8];
+    Philox::normals(z, c0, (uint32_t)b, 1u, seed);
+    if (off + nv > 4) Philox::normals(z + 4, c0 + 1, (uint32_t)b, 1u, seed);
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const long long g = 4ll * call + t;
-    if (g < (long long)s * rp) {
-      const int j = (int)(g / s), i = (int)(g - (long long)j * s);
-      Wb[(long long)j * ld + i] = z[t];
-      if (Wt16) Wt16[b * sw + (long long)j * ld + i] = f2bf(z[t]);
-    }
+    for (int t = 0; t < 4; ++t)
+      if (t < nv) v[t] = z[off + t];
   }
+  const long long o = b * sw + (long long)j * ld + i0;
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    if (i0 + t < ld) {
+      Wt[o + t] = v[t];
+      if (Wt16) Wt16[o + t] = f2bf(v[t]);
+    }
 }
 
-// Copy a caller-supplied sketch [batch][rp][s] into the padded panel.
+// A caller-supplied sketch [batch][rp][s] as the same zero-padded panel.
 static __global__ void sketch_copy_kernel(float* __restrict__ Wt, long long sw, int ld, const float* __restrict__ src,
-                                   int s, int rp, int batch, bf16_t* __restrict__ Wt16) {
+                                          int s, int rp, int rows, int batch, bf16_t* __restrict__ Wt16) {
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  const long long per = (long long)s * rp;
+  const long long per = (long long)rows * ld;
   if (gid >= per * batch) return;
   const int b = (int)(gid / per);
   const long long r = gid - (long long)b * per;
-  const int j = (int)(r / s), i = (int)(r - (long long)j * s);
-  Wt[b * sw + (long long)j * ld + i] = src[gid];
-  if (Wt16) Wt16[b * sw + (long long)j * ld + i] = f2bf(src[gid]);
+  const int j = (int)(r / ld), i = (int)(r - (long long)j * ld);
+  const float v = (j < rp && i < s) ? src[((long long)b * rp + j) * s + i] : 0.f;
+  Wt[b * sw + r] = v;
+  if (Wt16) Wt16[b * sw + r] = f2bf(v);
 }
 
 // ----------------------------------------------------- canonical copy ----

@@ -46,20 +46,30 @@ struct SmallLds {
 // in float64 by one Newton step for 1 / sqrt(c^2 + s^2), so every rotation is
 // orthogonal to float64 rounding. The annihilated entry is left to the
 // rotation (about 1e-7 of its size instead of zero); later sweeps take it out.
-__device__ __forceinline__ void jacobi_angle(double aii, double ajj, double aij, double& c, double& sn) {
+__device__ __forceinline__ void jacobi_angle_f(double aii, double ajj, double aij, float& cf, float& tf) {
   const double d = ajj - aii;
   const double m = fmax(fabs(d), fabs(2.0 * aij));
   const int ex = __builtin_amdgcn_frexp_exp(m);   // m = f 2^ex, f in [0.5, 1)
   const float df = (float)__builtin_amdgcn_ldexp(d, -ex), af = (float)__builtin_amdgcn_ldexp(aij, -ex);
   // df^2 + 4 af^2 lies in [0.25, 2]: the raw square root and reciprocal apply
   const float r = __builtin_amdgcn_sqrtf(df * df + 4.f * af * af);
-  const float t = (df >= 0.f ? 2.f * af : -2.f * af) * __builtin_amdgcn_rcpf(fabsf(df) + r);
-  const float cf = __builtin_amdgcn_rsqf(1.f + t * t);
+  tf = (df >= 0.f ? 2.f * af : -2.f * af) * __builtin_amdgcn_rcpf(fabsf(df) + r);
+  cf = __builtin_amdgcn_rsqf(1.f + tf * tf);
+}
+// (c, s) in float64 from the float32 cosine and tangent: one Newton step of
+// 1 / sqrt(c^2 + s^2) from 1. Every caller that starts from the same (cf, tf)
+// gets the same (c, s); (1, 0) stays exactly (1, 0).
+__device__ __forceinline__ void jacobi_rot64(float cf, float tf, double& c, double& sn) {
   c = (double)cf;
-  sn = (double)t * c;
-  const double q = 1.5 - 0.5 * (c * c + sn * sn);   // Newton step of 1 / sqrt(c^2 + s^2) from 1
+  sn = (double)tf * c;
+  const double q = 1.5 - 0.5 * (c * c + sn * sn);
   c *= q;
   sn *= q;
+}
+__device__ __forceinline__ void jacobi_angle(double aii, double ajj, double aij, double& c, double& sn) {
+  float cf, tf;
+  jacobi_angle_f(aii, ajj, aij, cf, tf);
+  jacobi_rot64(cf, tf, c, sn);
 }
 
 // Partner of index a in round r of the circle method over N (even) indices:
@@ -78,7 +88,7 @@ __device__ __forceinline__ int jacobi_partner(int a, int r, int N) {
   return y == x ? 0 : y + 1;
 }
 
-static __device__ void jacobi_eig(SmallLds& s, int n, int tol_exp = -48) {
+static __device__ __forceinline__ void jacobi_eig(SmallLds& s, int n, int tol_exp = -48) {
   const int tid = threadIdx.x, nt = blockDim.x;
   for (int e = tid; e < n * n; e += nt) {
     const int i = e / n, j = e - i * n;
@@ -160,9 +170,201 @@ static __device__ void jacobi_eig(SmallLds& s, int n, int tol_exp = -48) {
   }
 }
 
+// ---------------------------------------------------- one-wave Jacobi -----
+// The same eigendecomposition for n <= 2 NP <= 32 on one wave, with no
+// work-group barrier: the small eigenproblems sit on the critical path of the
+// call, so the latency of a round is what counts.
+//   * The N = 2 NP indices sit in slots T_p = p and B_p = NP + p. A round
+//     rotates the NP disjoint pairs (T_p, B_p) (angles and skip rules as in
+//     jacobi_eig), then every slot but T_0 moves one step along the ring
+//     T_1 -> ... -> T_{NP-1} -> B_{NP-1} -> ... -> B_0 -> T_1 (circle method:
+//     N - 1 consecutive rounds pair every two indices once).
+//   * Lane l holds the 2 x 2 blocks (p, q) of H in slot coordinates (rows
+//     T_p, B_p; columns T_q, B_q) with p NP + q = l + 64 u, so a round's row
+//     and column rotations are both local to the lane. Each lane also holds
+//     the diagonal blocks' entries of pairs p and q and chooses their angles
+//     itself (every lane holding a pair computes the same angle from the same
+//     values), so the angles need no exchange. E (rows: indices, columns:
+//     slots) is held as 2 x 2 units (rows 2p, 2p + 1; columns T_q, B_q).
+//   * The ring step goes through LDS (s.h2, s.e2): one round trip per round.
+//   * Stop after N - 1 consecutive rounds without a rotation (every pair was
+//     checked with nothing changed in between), or after 40 sweeps.
+// Input: s.h (n x n). Output as jacobi_eig: eigenvalues on the diagonal of
+// s.h (off-diagonal entries are left as they were) and eigenvectors as the
+// columns of s.e; returns the number of rounds. Only the calling wave may
+// touch s meanwhile; wave_sync orders its LDS accesses (a single wave's LDS
+// operations complete in order).
+__device__ __forceinline__ void wave_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+template <int NP>
+__device__ __forceinline__ int jw_slot(int r, int p) { return r ? NP + p : p; }
+
+// Slot whose content moves into slot (r, p) on a ring step.
+template <int NP>
+__device__ __forceinline__ int jw_src(int r, int p) {
+  if (r == 0) return p == 0 ? 0 : (p == 1 ? NP : p - 1);
+  return p == NP - 1 ? NP - 1 : NP + p + 1;
+}
+
+// Index in slot `slot` after R ring steps from the identity placement.
+template <int NP>
+__device__ __forceinline__ int jw_index(int slot, int R) {
+  if (slot == 0) return 0;
+  constexpr int M = 2 * NP - 1;   // ring length
+  const int k = slot < NP ? slot - 1 : 3 * NP - 2 - slot;   // ring position
+  int k0 = (k - R % M) % M;
+  k0 += k0 < 0 ? M : 0;
+  return k0 <= NP - 2 ? k0 + 1 : 3 * NP - 2 - k0;
+}
+
+template <int NP>
+__device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) {
+  constexpr int N = 2 * NP, NB = NP * NP, U = (NB + WAVE - 1) / WAVE;
+  static_assert(N <= 32, "one wave holds at most 16 x 16 blocks");
+  const int lane = threadIdx.x & (WAVE - 1);
+  double h[U][4], e[U][4];
+  double tp[U][3], tq[U][3];   // (H[T][T], H[B][B], H[T][B]) of pairs p and q
+  int bp[U], bq[U];
+  bool act[U];
+  double fro = 0.0;
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int id = lane + WAVE * u;
+    act[u] = id < NB;
+    bp[u] = act[u] ? id / NP : 0;
+    bq[u] = act[u] ? id - bp[u] * NP : 0;
+#pragma unroll
+    for (int r1 = 0; r1 < 2; ++r1)
+#pragma unroll
+      for (int r2 = 0; r2 < 2; ++r2) {
+        const int a = jw_slot<NP>(r1, bp[u]), b = jw_slot<NP>(r2, bq[u]);
+        const double v = (act[u] && a < n && b < n) ? s.h[a][b] : 0.0;
+        h[u][2 * r1 + r2] = v;
+        fro += v * v;
+        e[u][2 * r1 + r2] = (act[u] && 2 * bp[u] + r1 == b) ? 1.0 : 0.0;
+      }
+    const int pt = jw_slot<NP>(0, bp[u]), pb = jw_slot<NP>(1, bp[u]);
+    const int qt = jw_slot<NP>(0, bq[u]), qb = jw_slot<NP>(1, bq[u]);
+    tp[u][0] = pt < n ? s.h[pt][pt] : 0.0;
+    tp[u][1] = pb < n ? s.h[pb][pb] : 0.0;
+    tp[u][2] = pb < n ? s.h[pt][pb] : 0.0;
+    tq[u][0] = qt < n ? s.h[qt][qt] : 0.0;
+    tq[u][1] = qb < n ? s.h[qb][qb] : 0.0;
+    tq[u][2] = qb < n ? s.h[qt][qb] : 0.0;
+  }
+  fro = wave_sum(fro);
+  const double abs_floor = __builtin_amdgcn_ldexp(sqrt(fro), tol_exp);
+  int idle = 0, R = 0;
+  while (idle < N - 1 && R < 40 * (N - 1)) {
+    // every lane chooses the angles of its own pairs p and q from their
+    // diagonal blocks (the same inputs give the same angles in every lane)
+    bool rot = false;
+    double cp[U], sp[U], cq[U], sq[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float cf = 1.f, tf = 0.f, cg = 1.f, tg = 0.f;
+      if (tp[u][2] * tp[u][2] > 0x1p-100 * fabs(tp[u][0] * tp[u][1]) && fabs(tp[u][2]) > abs_floor) {
+        jacobi_angle_f(tp[u][0], tp[u][1], tp[u][2], cf, tf);
+        rot = act[u];
+      }
+      if (tq[u][2] * tq[u][2] > 0x1p-100 * fabs(tq[u][0] * tq[u][1]) && fabs(tq[u][2]) > abs_floor)
+        jacobi_angle_f(tq[u][0], tq[u][1], tq[u][2], cg, tg);
+      jacobi_rot64(cf, tf, cp[u], sp[u]);
+      jacobi_rot64(cg, tg, cq[u], sq[u]);
+    }
+    if (__any(rot)) {   // every pair is some active lane's p
+      idle = 0;
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        // columns of pair q: T <- c T - s B, B <- s T + c B; then the rows of pair p
+        const double x00 = cq[u] * h[u][0] - sq[u] * h[u][1], x01 = sq[u] * h[u][0] + cq[u] * h[u][1];
+        const double x10 = cq[u] * h[u][2] - sq[u] * h[u][3], x11 = sq[u] * h[u][2] + cq[u] * h[u][3];
+        h[u][0] = cp[u] * x00 - sp[u] * x10;
+        h[u][2] = sp[u] * x00 + cp[u] * x10;
+        h[u][1] = cp[u] * x01 - sp[u] * x11;
+        h[u][3] = sp[u] * x01 + cp[u] * x11;
+        const double y00 = cq[u] * e[u][0] - sq[u] * e[u][1], y01 = sq[u] * e[u][0] + cq[u] * e[u][1];
+        const double y10 = cq[u] * e[u][2] - sq[u] * e[u][3], y11 = sq[u] * e[u][2] + cq[u] * e[u][3];
+        e[u][0] = y00;
+        e[u][1] = y01;
+        e[u][2] = y10;
+        e[u][3] = y11;
+      }
+    } else {
+      ++idle;
+    }
+    // ring step; each lane also picks up the diagonal blocks of its new p, q
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (act[u])
+#pragma unroll
+        for (int r1 = 0; r1 < 2; ++r1)
+#pragma unroll
+          for (int r2 = 0; r2 < 2; ++r2) {
+            const int b = jw_slot<NP>(r2, bq[u]);
+            s.h2[jw_slot<NP>(r1, bp[u])][b] = h[u][2 * r1 + r2];
+            s.e2[2 * bp[u] + r1][b] = e[u][2 * r1 + r2];
+          }
+    wave_sync();
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (act[u]) {
+#pragma unroll
+        for (int r1 = 0; r1 < 2; ++r1)
+#pragma unroll
+          for (int r2 = 0; r2 < 2; ++r2) {
+            const int b = jw_src<NP>(r2, bq[u]);
+            h[u][2 * r1 + r2] = s.h2[jw_src<NP>(r1, bp[u])][b];
+            e[u][2 * r1 + r2] = s.e2[2 * bp[u] + r1][b];
+          }
+        const int pt = jw_src<NP>(0, bp[u]), pb = jw_src<NP>(1, bp[u]);
+        const int qt = jw_src<NP>(0, bq[u]), qb = jw_src<NP>(1, bq[u]);
+        tp[u][0] = s.h2[pt][pt];
+        tp[u][1] = s.h2[pb][pb];
+        tp[u][2] = s.h2[pt][pb];
+        tq[u][0] = s.h2[qt][qt];
+        tq[u][1] = s.h2[qb][qb];
+        tq[u][2] = s.h2[qt][qb];
+      }
+    wave_sync();
+    ++R;
+  }
+  // back to index coordinates: slot -> index after R ring steps
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+    if (act[u])
+#pragma unroll
+      for (int r2 = 0; r2 < 2; ++r2) {
+        const int col = jw_index<NP>(jw_slot<NP>(r2, bq[u]), R);
+        if (col < n) {
+#pragma unroll
+          for (int r1 = 0; r1 < 2; ++r1)
+            if (2 * bp[u] + r1 < n) s.e[2 * bp[u] + r1][col] = e[u][2 * r1 + r2];
+          if (bp[u] == bq[u]) s.h[col][col] = h[u][3 * r2];
+        }
+      }
+  wave_sync();
+  return R;
+}
+
+// jacobi_eig for a whole work-group: with NP > 0 (n <= 2 NP) on its first
+// wave, otherwise block-wide.
+template <int NP>
+__device__ __forceinline__ void jacobi_eig_any(SmallLds& s, int n, int tol_exp = -48) {
+  if constexpr (NP == 0) {
+    jacobi_eig(s, n, tol_exp);
+  } else {
+    __syncthreads();
+    if (threadIdx.x < WAVE) jacobi_eig_wave<NP>(s, n, tol_exp);
+    __syncthreads();
+  }
+}
+// Wave size class of an n x n eigenproblem (0: block-wide solver).
+__host__ __device__ inline int jacobi_class(int n) { return n <= 8 ? 4 : n <= 16 ? 8 : n <= 24 ? 12 : n <= 32 ? 16 : 0; }
+
 // Rank of each key under "larger key first, then smaller index": s.perm[rank]
 // = index. Keys must be set in s.key[0..n).
-static __device__ void sort_desc(SmallLds& s, int n) {
+static __device__ __forceinline__ void sort_desc(SmallLds& s, int n) {
   const int tid = threadIdx.x;
   if (tid < n) {
     const double k = s.key[tid];
@@ -208,17 +410,22 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const float* A, long 
   const int nch = len_pad / GP_CHUNK;
   const int b = blockIdx.x / nch, ch = blockIdx.x - b * nch;
   const int x0 = ch * GP_CHUNK;
+  // every load of the chunk is issued before the first LDS store
+  constexpr int PER = CM * GP_CHUNK / 256;
   const float* Ab = A + b * sa;
-  for (int e = threadIdx.x; e < ca * GP_CHUNK; e += 256) {
-    const int a = e / GP_CHUNK, x = e - a * GP_CHUNK;
-    ta[a][x] = Ab[(long long)a * lda + x0 + x];
+  const float* Bb = B + b * sb;
+  float va[PER], vb[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + 256 * u, a = e / GP_CHUNK, x = e - a * GP_CHUNK;
+    va[u] = a < ca ? Ab[(long long)a * lda + x0 + x] : 0.f;
+    vb[u] = (!sym && a < cb) ? Bb[(long long)a * ldb + x0 + x] : 0.f;
   }
-  if (!sym) {
-    const float* Bb = B + b * sb;
-    for (int e = threadIdx.x; e < cb * GP_CHUNK; e += 256) {
-      const int a = e / GP_CHUNK, x = e - a * GP_CHUNK;
-      tb[a][x] = Bb[(long long)a * ldb + x0 + x];
-    }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + 256 * u, a = e / GP_CHUNK, x = e - a * GP_CHUNK;
+    ta[a][x] = va[u];
+    if (!sym) tb[a][x] = vb[u];
   }
   __syncthreads();
   const int items = gram_items(ca, cb, sym);
@@ -237,7 +444,7 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const float* A, long 
 // s.h[a][bb] = sum of the chunk partials in chunk order (mirrored when sym).
 // Loads are issued 32 chunks at a time (one round trip for up to 4096
 // positions); the additions keep chunk order.
-static __device__ void gram_reduce(SmallLds& s, const double* part, int nch, int ca, int cb, bool sym) {
+static __device__ __forceinline__ void gram_reduce(SmallLds& s, const double* part, int nch, int ca, int cb, bool sym) {
   const int items = gram_items(ca, cb, sym);
   for (int p = threadIdx.x; p < items; p += blockDim.x) {
     double t = 0.0;
@@ -307,66 +514,12 @@ static __global__ __launch_bounds__(64) void chol_factor_kernel(const double* pa
   }
 }
 
-// The same factorization on one wave with rows in registers (c <= CM <= 32):
-// lane i owns row i of the lower triangle; column j takes its pivot from
-// lane j and the multipliers L[k][j] by cross-lane broadcasts, so no step
-// waits on LDS or a barrier.
-template <int CM>
-__global__ __launch_bounds__(64) void chol_factor_wave_kernel(const double* part, int nch, int c, double* fac,
-                                                             int* status) {
-  static_assert(CM <= 32, "one row per lane");
-  __shared__ SmallLds s;
-  const int b = blockIdx.x, lane = threadIdx.x;
-  gram_reduce(s, part + (long long)b * nch * gram_items(c, c, true), nch, c, c, true);
-  double h[CM];
-#pragma unroll
-  for (int k = 0; k < CM; ++k) h[k] = (lane < c && k <= lane) ? s.h[lane][k] : 0.0;
-  double dg = 0.0;
-#pragma unroll
-  for (int k = 0; k < CM; ++k)
-    if (k == lane) dg = h[k];
-  const double tr = __shfl(wave_sum(dg), 0, WAVE);
-  double* L = fac + (long long)b * c * c;
-  if (tr == 0.0) {
-    for (int e = lane; e < c * c; e += WAVE) L[e] = 0.0;
-    return;
-  }
-  const double floor_ = (double)c * 1.1102230246251565e-16 * tr;
-  bool floored = false;
-#pragma unroll
-  for (int j = 0; j < CM; ++j) {
-    if (j < c) {
-      double d = __shfl(h[j], j, WAVE);   // pivot: lane j's updated diagonal
-      if (d <= floor_) {
-        d = floor_;
-        floored = true;
-      }
-      const double piv = sqrt(d), inv = 1.0 / piv;
-      const double lij = lane > j ? h[j] * inv : (lane == j ? piv : 0.0);
-      h[j] = lij;
-#pragma unroll
-      for (int k = j + 1; k < CM; ++k) {
-        if (k < c) {
-          const double lkj = __shfl(lij, k, WAVE);
-          if (lane >= k) h[k] -= lij * lkj;
-        }
-      }
-    }
-  }
-  if (floored && lane == 0 && status) atomicOr(status, 2);
-  if (lane < c) {
-#pragma unroll
-    for (int k = 0; k < CM; ++k)
-      if (k < c) L[(long long)lane * c + k] = k <= lane ? h[k] : 0.0;
-  }
-}
-
 // Apply: Q = P R^-1 with R = L^T, by forward substitution per position, in
-// place (plus an optional bf16 copy of Q). Grid: (len_pad / 128) * batch; one
-// thread per position.
+// place (plus an optional bf16 copy of Q, rows c .. c16 - 1 zero). Grid:
+// (len_pad / 128) * batch; one thread per position.
 template <int CM>
 __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp, int ld, int c, int len_pad,
-                                                         const double* fac, int batch, bf16_t* Pt16) {
+                                                         const double* fac, int batch, bf16_t* Pt16, int c16) {
   __shared__ double L[CM][CM + 1];
   __shared__ double inv_d[CM];
   const int per = len_pad / 128;
@@ -396,30 +549,204 @@ __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp
 #pragma unroll
     for (int jj = 0; jj < CM; ++jj)
       if (jj < c) P16[(long long)jj * ld + x] = f2bf((float)q[jj]);
+    for (int jj = c; jj < c16; ++jj) P16[(long long)jj * ld + x] = 0;
+  }
+}
+
+// Factor and apply in one launch (c <= CM <= 32). Every work-group reduces the
+// partials, factors Gram = L L^T on its first wave and applies Q = P R^-1
+// (R = L^T) to its 128 positions, so no work-group waits for another; all of
+// them compute the same L from the same partials in the same order.
+//   * Factor: lane i holds row i of the lower triangle in registers; column
+//     j takes its pivot from lane j and the multipliers L[k][j] from lane k
+//     by lane reads (the lane indices are compile-time constants), so a step
+//     waits on no LDS access. 1 / sqrt(pivot) is the hardware estimate with
+//     one Newton step (within an ulp or two of float64 rounding).
+//   * Pivots below c u tr(Gram) are raised to it (flag 2 in status, set by
+//     the matrix's first work-group); a zero trace gives a zero panel.
+//   * Apply: forward substitution per position, in place, plus an optional
+//     bf16 copy of Q whose rows c .. c16 - 1 are written as zeros.
+// Grid: (len_pad / 128) * batch; 128 threads.
+__device__ __forceinline__ double lane_read(double v, int lane) {
+  const uint64_t u = __double_as_longlong(v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+template <int CM>
+__global__ __launch_bounds__(128) void chol_qr_kernel(float* Pt, long long sp, int ld, int c, int len_pad,
+                                                      const double* part, int nch, int* status, bf16_t* Pt16,
+                                                      int c16) {
+  static_assert(CM <= 32, "one row per lane");
+  __shared__ double G[CM][CM + 1];
+  __shared__ double L[CM][CM + 1];
+  __shared__ double inv_d[CM];
+  const int per = len_pad / 128;
+  const int b = blockIdx.x / per, tile = blockIdx.x - b * per;
+  const int tid = threadIdx.x;
+  // this thread's panel column, loaded first: its latency overlaps the
+  // reduction and the factorization
+  const int x = tile * 128 + tid;
+  float* P = Pt + b * sp;
+  float pv[CM];
+#pragma unroll
+  for (int jj = 0; jj < CM; ++jj) pv[jj] = jj < c ? P[(long long)jj * ld + x] : 0.f;
+  // Gram from the chunk partials, in chunk order
+  {
+    const int items = c * (c + 1) / 2;
+    const double* pb = part + (long long)b * nch * items;
+    for (int q = tid; q < items; q += 128) {
+      double t = 0.0;
+      int ch = 0;
+      for (; ch + 8 <= nch; ch += 8) {
+        double v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = pb[(long long)(ch + u) * items + q];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) t += v[u];
+      }
+      for (; ch < nch; ++ch) t += pb[(long long)ch * items + q];
+      int a, bb;
+      gram_item(q, c, c, true, a, bb);
+      G[a][bb] = t;
+      G[bb][a] = t;
+    }
+  }
+  __syncthreads();
+  if (tid < WAVE) {
+    const int lane = tid;
+    double h[CM];
+#pragma unroll
+    for (int k = 0; k < CM; ++k) h[k] = (lane < c && k <= lane) ? G[lane][k] : 0.0;
+    double tr = 0.0;
+#pragma unroll
+    for (int k = 0; k < CM; ++k)
+      if (k < c) tr += G[k][k];
+    const double floor_ = (double)c * 1.1102230246251565e-16 * tr;
+    bool floored = false;
+    if (tr == 0.0) {
+#pragma unroll
+      for (int k = 0; k < CM; ++k) h[k] = 0.0;
+    } else {
+#pragma unroll
+      for (int j = 0; j < CM; ++j) {
+        if (j < c) {
+          double d = lane_read(h[j], j);   // pivot: lane j's updated diagonal
+          if (d <= floor_) {
+            d = floor_;
+            floored = true;
+          }
+          double r = __builtin_amdgcn_rsq(d);
+          r = r * (1.5 - 0.5 * d * r * r);
+          const double lij = lane > j ? h[j] * r : (lane == j ? d * r : 0.0);
+          h[j] = lij;
+          if (lane == j) inv_d[j] = r;
+#pragma unroll
+          for (int k = j + 1; k < CM; ++k)
+            if (k < c) {
+              const double lkj = lane_read(lij, k);
+              if (lane >= k) h[k] -= lij * lkj;
+            }
+        }
+      }
+    }
+    if (tr == 0.0 && lane < c) inv_d[lane] = 0.0;
+    if (lane < c) {
+#pragma unroll
+      for (int k = 0; k < CM; ++k) L[lane][k] = h[k];
+    }
+    if (floored && lane == 0 && tile == 0 && status) atomicOr(status, 2);
+  }
+  __syncthreads();
+  double q[CM];
+#pragma unroll
+  for (int jj = 0; jj < CM; ++jj) {
+    if (jj < c) {
+      double v = (double)pv[jj];
+#pragma unroll
+      for (int i = 0; i < jj; ++i) v -= q[i] * L[jj][i];
+      q[jj] = v * inv_d[jj];
+    }
+  }
+#pragma unroll
+  for (int jj = 0; jj < CM; ++jj)
+    if (jj < c) P[(long long)jj * ld + x] = (float)q[jj];
+  if (Pt16) {   // bf16 copy: the panel as a product operand (zero rows up to c16)
+    bf16_t* P16 = Pt16 + b * sp;
+#pragma unroll
+    for (int jj = 0; jj < CM; ++jj)
+      if (jj < c) P16[(long long)jj * ld + x] = f2bf((float)q[jj]);
+    for (int jj = c; jj < c16; ++jj) P16[(long long)jj * ld + x] = 0;
   }
 }
 
 // ----------------------------------------------- thin SVD of G (Alg. 3) ---
-// From the partials of H = G G^T (G = Q^T A, rp x s): eigen-decompose H, order
-// the eigenvalues decreasingly, and emit for the leading k: singular values,
-// the eigenvector matrix E (rp x k), 1/s (0 for s = 0), and the deflation
-// rank (fixed k, or the gate of Alg. 1 when tau > 0) with the subtraction
-// coefficients -s_j used by the residual pass. One work-group per matrix.
-static __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part, int nch, int rp, int k, float tau,
-                                                             float* E, float* sv, float* inv_sv, int* keff,
-                                                             float* coef_a, float* s_user, int* keff_user) {
+// out[j][x] = scale[j] * sum_{a < rp} es[a][j] P[a][x] (j < k, x < len), by
+// the whole work-group in float32, the terms added in order of a. es holds RM
+// rows (rows rp .. RM - 1 zero), so every read is unconditional: each thread
+// loads the panel values of PB positions, and a factor's RM coefficients,
+// before it uses any of them.
+template <int RM>
+__device__ __forceinline__ void rotate_panel(const float* P, int ldp, int len, int rp, int k, const float* es,
+                                             const float* scale, float* out, int ldo) {
+  constexpr int PB = RM <= 16 ? 64 / RM : 1;
+  for (int x0 = threadIdx.x; x0 < len; x0 += PB * SM_THREADS) {
+    float v[PB][RM];
+#pragma unroll
+    for (int i = 0; i < PB; ++i) {
+      const int x = x0 + i * SM_THREADS;
+#pragma unroll
+      for (int r = 0; r < RM; ++r) v[i][r] = (r < rp && x < len) ? P[(long long)r * ldp + x] : 0.f;
+    }
+    for (int j = 0; j < k; ++j) {
+      float ev[RM];
+#pragma unroll
+      for (int r = 0; r < RM; ++r) ev[r] = es[r * k + j];
+      const float sc = scale ? scale[j] : 1.f;
+#pragma unroll
+      for (int i = 0; i < PB; ++i) {
+        const int x = x0 + i * SM_THREADS;
+        float acc = 0.f;
+#pragma unroll
+        for (int r = 0; r < RM; ++r) acc += ev[r] * v[i][r];
+        if (x < len) out[(long long)j * ldo + x] = scale ? sc * acc : acc;
+      }
+    }
+  }
+}
+
+// From the partials of H = G G^T (G = Q^T A, rp x s), in float64: eigen-
+// decompose H, order the eigenvalues decreasingly, and emit for the leading
+// k: singular values, the eigenvector matrix E (rp x k), 1/s (0 for s = 0),
+// the deflation rank (fixed k, or the gate of Alg. 1 when tau > 0) with the
+// subtraction coefficients -s_j used by the residual pass, and the factors
+// V = G^T E / s (k x s_pad, from the G^T panel Gt) and U = Q E (k x l_pad,
+// from the Q panel Qt). One work-group per matrix; NP = jacobi_class(rp).
+template <int NP>
+__global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part, int nch, int rp, int k, float tau,
+                                                              float* E, float* sv, float* inv_sv, int* keff,
+                                                              float* coef_a, float* s_user, int* keff_user,
+                                                              const float* Gt, long long sg, int s_pad,
+                                                              const float* Qt, long long sq, int l_pad, float* Vt,
+                                                              float* Ut) {
   __shared__ SmallLds s;
   const int tid = threadIdx.x, b = blockIdx.x;
   gram_reduce(s, part + (long long)b * nch * gram_items(rp, rp, true), nch, rp, rp, true);
   // off-diagonal floor 2^-40 ||H||_F: the outputs are float32, and the
   // leading eigenvectors move by at most that over the gap to the rest
-  jacobi_eig(s, rp, -40);
+  jacobi_eig_any<NP>(s, rp, -40);
   if (tid < rp) s.key[tid] = s.h[tid][tid];
   __syncthreads();
   sort_desc(s, rp);
-  for (int e = tid; e < rp * k; e += SM_THREADS) {
+  constexpr int RM = NP > 0 ? 2 * NP : SM_MAX;
+  float* es = reinterpret_cast<float*>(&s.h2[0][0]);   // E as float32, [RM][k] (rows past rp zero)
+  float* isv = es + RM * k;                            // 1/s as float32
+  for (int e = tid; e < RM * k; e += SM_THREADS) {
     const int a = e / k, j = e - a * k;
-    E[(long long)b * rp * k + e] = (float)s.e[a][s.perm[j]];
+    const float v = a < rp ? (float)s.e[a][s.perm[j]] : 0.f;
+    if (a < rp) E[(long long)b * rp * k + e] = v;
+    es[e] = v;
   }
   if (tid < k) {
     const double lam = s.h[s.perm[tid]][s.perm[tid]];
@@ -442,11 +769,16 @@ static __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const doubl
   const int ke = s.perm[SM_MAX - 1];
   if (tid < k) {
     const double sj = s.key[tid];
+    const float inv = sj > 0.0 ? (float)(1.0 / sj) : 0.f;
     sv[b * k + tid] = (float)sj;
-    inv_sv[b * k + tid] = sj > 0.0 ? (float)(1.0 / sj) : 0.f;
+    inv_sv[b * k + tid] = inv;
+    isv[tid] = inv;
     coef_a[b * k + tid] = tid < ke ? -(float)sj : 0.f;
     if (s_user) s_user[b * k + tid] = (float)sj;
   }
+  __syncthreads();
+  rotate_panel<RM>(Gt + b * sg, s_pad, s_pad, rp, k, es, isv, Vt + (long long)b * k * s_pad, s_pad);
+  rotate_panel<RM>(Qt + b * sq, l_pad, l_pad, rp, k, es, nullptr, Ut + (long long)b * k * l_pad, l_pad);
 }
 
 // ------------------------------------------- Rayleigh-Ritz (Alg. 2) -------
@@ -455,7 +787,8 @@ static __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const doubl
 // Deflated set I: all K (tau = 0) or the gate of Alg. 2 on the magnitudes.
 // Coefficients for the residual (-lam), the padded start (sign(lam) / gamma)
 // and the restore (max(lam, 0)). One work-group.
-static __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const double* part, int nch, int K, float tau, int window,
+template <int NP>
+__global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const double* part, int nch, int K, float tau, int window,
                                                          float gamma, float* E, float* lam_sorted, int* ndef,
                                                          float* coef_r, float* coef_x, float* coef_p,
                                                          float* ritz_user, int* ndef_user, int* npos_user) {
@@ -471,7 +804,7 @@ static __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const double* p
     }
   }
   __syncthreads();
-  jacobi_eig(s, K);
+  jacobi_eig_any<NP>(s, K);
   if (tid < K) s.key[tid] = fabs(s.h[tid][tid]);
   __syncthreads();
   if (tid < K) {
