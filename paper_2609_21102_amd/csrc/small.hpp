@@ -553,35 +553,30 @@ __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp
   }
 }
 
-// Factor and apply in one launch (c <= CM <= 32). Every work-group reduces the
+// Factor and apply in one launch (c <= CM <= 16). Every work-group reduces the
 // partials, factors Gram = L L^T on its first wave and applies Q = P R^-1
 // (R = L^T) to its 128 positions, so no work-group waits for another; all of
 // them compute the same L from the same partials in the same order.
-//   * Factor: lane i holds row i of the lower triangle in registers; column
-//     j takes its pivot from lane j and the multipliers L[k][j] from lane k
-//     by lane reads (the lane indices are compile-time constants), so a step
-//     waits on no LDS access. 1 / sqrt(pivot) is the hardware estimate with
-//     one Newton step (within an ulp or two of float64 rounding).
+//   * Factor: lane i holds row i of the lower triangle in registers; at step
+//     j every lane publishes its entry of column j in LDS and reads the column
+//     back, so one LDS round trip gives every lane the pivot and the
+//     multipliers L[k][j] = G'[k][j] / sqrt(pivot), computed alike in every
+//     lane. 1 / sqrt(pivot) is the hardware estimate with one Newton step
+//     (within an ulp or two of float64 rounding).
 //   * Pivots below c u tr(Gram) are raised to it (flag 2 in status, set by
 //     the matrix's first work-group); a zero trace gives a zero panel.
 //   * Apply: forward substitution per position, in place, plus an optional
 //     bf16 copy of Q whose rows c .. c16 - 1 are written as zeros.
 // Grid: (len_pad / 128) * batch; 128 threads.
-__device__ __forceinline__ double lane_read(double v, int lane) {
-  const uint64_t u = __double_as_longlong(v);
-  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
-  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
-  return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
-}
-
 template <int CM>
 __global__ __launch_bounds__(128) void chol_qr_kernel(float* Pt, long long sp, int ld, int c, int len_pad,
                                                       const double* part, int nch, int* status, bf16_t* Pt16,
                                                       int c16) {
-  static_assert(CM <= 32, "one row per lane");
+  static_assert(CM <= 16, "rows in registers: wider panels use the two-kernel path");
   __shared__ double G[CM][CM + 1];
   __shared__ double L[CM][CM + 1];
   __shared__ double inv_d[CM];
+  __shared__ double colv[CM];
   const int per = len_pad / 128;
   const int b = blockIdx.x / per, tile = blockIdx.x - b * per;
   const int tid = threadIdx.x;
@@ -615,50 +610,58 @@ __global__ __launch_bounds__(128) void chol_qr_kernel(float* Pt, long long sp, i
   }
   __syncthreads();
   if (tid < WAVE) {
+    // The Gram is padded to CM x CM with tr(Gram) on the diagonal past c
+    // (above the floor, and independent of the leading block), so every loop
+    // below has compile-time bounds.
     const int lane = tid;
-    double h[CM];
-#pragma unroll
-    for (int k = 0; k < CM; ++k) h[k] = (lane < c && k <= lane) ? G[lane][k] : 0.0;
     double tr = 0.0;
 #pragma unroll
     for (int k = 0; k < CM; ++k)
       if (k < c) tr += G[k][k];
     const double floor_ = (double)c * 1.1102230246251565e-16 * tr;
+    double h[CM];
+#pragma unroll
+    for (int k = 0; k < CM; ++k)
+      h[k] = (lane < c && k <= lane) ? G[lane][k] : (k == lane ? tr : 0.0);
     bool floored = false;
-    if (tr == 0.0) {
+    if (tr == 0.0) {   // zero panel: L = 0 and zero reciprocals
 #pragma unroll
       for (int k = 0; k < CM; ++k) h[k] = 0.0;
+      if (lane < CM) inv_d[lane] = 0.0;
     } else {
 #pragma unroll
       for (int j = 0; j < CM; ++j) {
-        if (j < c) {
-          double d = lane_read(h[j], j);   // pivot: lane j's updated diagonal
-          if (d <= floor_) {
-            d = floor_;
-            floored = true;
-          }
-          double r = __builtin_amdgcn_rsq(d);
-          r = r * (1.5 - 0.5 * d * r * r);
-          const double lij = lane > j ? h[j] * r : (lane == j ? d * r : 0.0);
-          h[j] = lij;
-          if (lane == j) inv_d[j] = r;
+        // column j (lane i: entry (i, j) of the updated matrix) through LDS;
+        // every lane then forms the pivot and the multipliers itself
+        if (lane < CM) colv[lane] = h[j];
+        wave_sync();
+        double cv[CM];
 #pragma unroll
-          for (int k = j + 1; k < CM; ++k)
-            if (k < c) {
-              const double lkj = lane_read(lij, k);
-              if (lane >= k) h[k] -= lij * lkj;
-            }
+        for (int k = j; k < CM; ++k) cv[k] = colv[k];
+        wave_sync();
+        double d = cv[j];
+        if (d <= floor_) {
+          d = floor_;
+          floored = true;
         }
+        double r = __builtin_amdgcn_rsq(d);
+        r = r * (1.5 - 0.5 * d * r * r);
+        const double lij = lane > j ? h[j] * r : (lane == j ? d * r : 0.0);
+        h[j] = lij;
+        if (lane == j) inv_d[j] = r;
+#pragma unroll
+        for (int k = j + 1; k < CM; ++k)
+          if (lane >= k) h[k] -= lij * (cv[k] * r);
       }
     }
-    if (tr == 0.0 && lane < c) inv_d[lane] = 0.0;
-    if (lane < c) {
+    if (lane < CM) {
 #pragma unroll
       for (int k = 0; k < CM; ++k) L[lane][k] = h[k];
     }
     if (floored && lane == 0 && tile == 0 && status) atomicOr(status, 2);
   }
   __syncthreads();
+  // (the runtime bound keeps the compiler from hoisting all of L's reads)
   double q[CM];
 #pragma unroll
   for (int jj = 0; jj < CM; ++jj) {
