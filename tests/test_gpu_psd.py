@@ -3,6 +3,8 @@
 Tolerance: relative Frobenius error 1e-4 (float32 path against the float64
 oracle); deflated and positive counts must match exactly.
 """
+import math
+
 import numpy as np
 import pytest
 import torch
@@ -98,3 +100,98 @@ def test_config4_full():
     assert err < TOL
     assert int(info["n_deflated"]) == oinfo.n_deflated
     assert int(info["n_positive"]) == oinfo.n_positive
+
+
+def test_config5_chain_scaled():
+    """Config 5's call pattern at n = 1024 (same spectrum recipe, k = 32, one
+    subspace step per call): 20 chained projections, each warm-started from
+    the previous call's basis while X drifts by 1e-3 ||X||_F; every call is
+    compared with the oracle run on the same chain."""
+    n, k, calls = 1024, 32, 20
+    case = workloads.config5_first(n)
+    z = case.z.copy()
+    q = torch.from_numpy(case.qwarm).cuda()
+    v = case.qwarm.astype(np.float64)
+    errs = []
+    for call in range(calls):
+        out, info = sd.psd_project(torch.from_numpy(z).cuda(), k, case.steps, q, subspace_iters=1,
+                                   gamma=case.gamma, info=True)
+        torch.cuda.synchronize()
+        want, v, oinfo = opsd.psd_project_deflated(z.astype(np.float64), v, steps=case.steps, gamma=case.gamma,
+                                                   subspace_iters=1)
+        err = rel_fro(host64(out), want)
+        errs.append(err)
+        assert err < TOL, (call, err)
+        assert int(info["n_deflated"]) == oinfo.n_deflated == k
+        assert int(info["n_positive"]) == oinfo.n_positive
+        assert rel_fro(host64(q), v) < 1e-4
+        assert abs(float(info["theta"]) - oinfo.theta) <= 1e-4 * oinfo.theta
+        z = workloads.psd_drift(z, 1e-3, call)
+    say(f"config5 chain n={n}: rel err per call {min(errs):.2e} .. {max(errs):.2e}")
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(900)
+def test_config5_full_chain():
+    """Config 5 at n = 16384: the 20-call chain with drift, warm-started from
+    the previous call's basis. The oracle cannot run at this size, so each
+    call is checked on what holds at any size:
+      * the output is exactly symmetric, finite;
+      * bookkeeping: all 32 pairs deflated, and the positive count equals the
+        number of positive dominant eigenvalues (the drift moves them by far
+        less than their size);
+      * the Ritz values match the dominant eigenvalues (first call: the
+        generator's; the drift moves them by at most ||E||_2 per call);
+      * the returned basis spans the dominant eigenspace: within 1e-3 of the
+        first input's after the first call (the warm start is 1e-2 away, and
+        one block step shrinks that by |bulk| / |dominant| <= 1/500), and
+        within 1e-2 of it over the chain (the drift turns the eigenspace by
+        about ||E||_2 / 500 per call);
+      * the first call's output matches the exact projection Q max(lam, 0) Q^T
+        on random probe vectors to the accuracy the method reaches from this
+        warm start (the oracle on the same recipe at n = 1024: 1.3e-2);
+      * once the basis has converged, the Lanczos scale is that of the bulk
+        (|bulk| <= 1 plus the drift), not of the dominant eigenvalues."""
+    import time
+    n, k, calls = 16384, 32, 20
+    t0 = time.time()
+    z, lam, qf, qwarm = workloads.config5_device(n)
+    torch.cuda.synchronize()
+    say(f"config5 n={n}: input built in {time.time() - t0:.1f} s")
+    order = np.argsort(-np.abs(lam), kind="stable")
+    dom = lam[order[:k]]
+    n_pos = int((dom > 0).sum())
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    probes = torch.randn((n, 8), generator=gen, device="cuda", dtype=torch.float64)
+    top = qf[:, torch.from_numpy(order[:k]).cuda()]
+    exact_probe = qf @ (torch.from_numpy(np.maximum(lam, 0.0)).cuda().unsqueeze(1) * (qf.T @ probes))
+    times = []
+    for call in range(calls):
+        t1 = time.time()
+        out, info = sd.psd_project(z, k, 10, qwarm, subspace_iters=1, gamma=1.1, info=True)
+        torch.cuda.synchronize()
+        times.append(time.time() - t1)
+        assert torch.equal(out, out.T)
+        assert bool(torch.isfinite(out).all())
+        assert int(info["n_deflated"]) == k
+        assert int(info["n_positive"]) == n_pos
+        ritz = np.sort(info["ritz"].double().cpu().numpy())
+        # warm-start error eps^2 |lam| (first call) plus ||E||_2 <= 0.3 per drift step
+        assert np.allclose(ritz, np.sort(dom), rtol=0, atol=1.0 + 1e-4 * np.abs(dom).max() + 0.3 * call), call
+        # basis: distance of the first input's dominant eigenspace from span(qwarm)
+        resid = top - qwarm.double() @ (qwarm.double().T @ top)
+        dist = float(torch.linalg.norm(resid) / math.sqrt(k))
+        assert dist < (1e-3 if call == 0 else 1e-2), (call, dist)
+        theta = float(info["theta"])
+        if call == 0:
+            got = out.double() @ probes
+            perr = float(torch.linalg.norm(got - exact_probe) / torch.linalg.norm(exact_probe))
+            say(f"  call 0: probe error vs exact {perr:.2e}, basis distance {dist:.2e}, theta {theta:.4g}, "
+                f"{times[-1] * 1e3:.0f} ms")
+            assert perr < 5e-2, perr
+        elif call == calls - 1:
+            say(f"  call {call}: basis distance {dist:.2e}, theta {theta:.4g}, {times[-1] * 1e3:.0f} ms")
+            assert theta < 3.0, theta
+        z = workloads.psd_drift_device(z, 1e-3, call)
+    say(f"config5 chain: median call {1e3 * sorted(times)[len(times) // 2]:.0f} ms")

@@ -284,3 +284,51 @@ def config5_first(n: int = 16384) -> PSDCase:
 
     Building it needs an n x n QR (minutes of host time at n = 16384)."""
     return psd_case(f"c5_{n}_f32", n, 32, (500.0, 5000.0), 32, 1, 10, 1.1, ids=(5,))
+
+
+def config5_device(n: int = 16384, device: str = "cuda"):
+    """Config 5 at full size, assembled on the GPU.
+
+    Same recipe as config5_first (32 dominant eigenvalues +-U[500, 5000] over
+    a bulk U[-1, 1], warm start at eps = 1e-2), drawn from the same seeded
+    host generator, but the n x n orthogonal factor comes from a float64
+    Householder QR on the GPU and Q diag(lam) Q^T from a float64 product
+    there: at n = 16384 the host QR takes minutes. Returns (z, lam, q, qwarm):
+    z float32 [n, n] exactly symmetric, lam float64 numpy [n], q float64
+    [n, n] (device), qwarm float32 [n, 32] (device)."""
+    import torch
+    rng = rng_for(5)
+    lam = psd_spectrum(rng, n, 32, 500.0, 5000.0)
+    g = torch.from_numpy(rng.standard_normal((n, n))).to(device)
+    q, r = torch.linalg.qr(g)
+    del g
+    q *= torch.sign(torch.diagonal(r)).unsqueeze(0)
+    del r
+    lam_d = torch.from_numpy(lam).to(device)
+    z64 = (q * lam_d) @ q.T
+    z64 = 0.5 * (z64 + z64.T)
+    z = z64.float()
+    del z64
+    z = torch.triu(z) + torch.triu(z, 1).T   # exactly symmetric storage
+    order = np.argsort(-np.abs(lam), kind="stable")
+    top = q[:, torch.from_numpy(order[:32]).to(device)]
+    w = top + 1e-2 * torch.from_numpy(rng.standard_normal((n, 32))).to(device) / math.sqrt(n)
+    qq, rr = torch.linalg.qr(w)
+    qwarm = (qq * torch.sign(torch.diagonal(rr)).unsqueeze(0)).float().contiguous()
+    return z.contiguous(), lam, q, qwarm
+
+
+def psd_drift_device(z, rel: float, call: int, case_id: int = 5):
+    """psd_drift on the GPU: E = (G + G^T) / sqrt(2) from a seeded device
+    generator, scaled to ||E||_F = rel ||Z||_F; z + E stored exactly
+    symmetric (float32)."""
+    import torch
+    gen = torch.Generator(device=z.device)
+    gen.manual_seed(MASTER_SEED * 1000003 + case_id * 1009 + call)
+    n = z.shape[0]
+    e = torch.randn((n, n), generator=gen, device=z.device, dtype=torch.float32)
+    e = (e + e.T) / math.sqrt(2.0)
+    e *= (rel * torch.linalg.norm(z.double()) / torch.linalg.norm(e.double())).float()
+    out = z + e
+    return (torch.triu(out) + torch.triu(out, 1).T).contiguous()
+
