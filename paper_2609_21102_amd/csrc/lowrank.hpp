@@ -79,8 +79,7 @@ struct Raw8<float> {
 };
 
 // 128 x 128 tile per work-group; thread t owns rows 8 (t / 16) .. +7 and
-// columns 8 (t % 16) .. +7. The thread's X values are loaded first, so their
-// latency overlaps the staging of the low-rank panels.
+// columns 8 (t % 16) .. +7.
 template <typename TX, typename TO, int KM>
 __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
   __shared__ __attribute__((aligned(16))) float ls[KM][128];
@@ -90,31 +89,32 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
   const int lid = xcd_remap(blockIdx.x, per * a.batch);
   const int b = lid / per, t = lid - b * per;
   const int i0 = (t / tc) * 128, n0 = (t % tc) * 128;
-  const int kk = a.kk ? a.kk[b] : a.kconst;
-  const float alpha = a.alpha ? a.alpha[b] : 1.f;
   const int tid = threadIdx.x;
   const int rg = tid >> 4, cg = tid & 15;
+  // Loads in the order they are needed: the low-rank panels (all kmax rows:
+  // the coefficients past the per-matrix count are zero, so no load waits on
+  // that count), then the thread's X values, whose latency overlaps the
+  // low-rank product.
+  constexpr int PER = KM * 128 / 256;
+  float lv[PER], rv[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = tid + 256 * u, j = e >> 7, x = e & 127;
+    lv[u] = j < a.kmax ? a.L[b * a.sl + (long long)j * a.ldl + i0 + x] * a.coef[b * a.kmax + j] : 0.f;
+    rv[u] = j < a.kmax ? a.Rr[b * a.sr + (long long)j * a.ldr + n0 + x] : 0.f;
+  }
   const TX* xb = reinterpret_cast<const TX*>(a.x) + b * a.sx;
   Raw8<TX> xr[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) xr[r].load(xb + (long long)(i0 + rg * 8 + r) * a.ldx + n0 + cg * 8);
-  // low-rank panels: every load is issued before the first LDS store
-  {
-    constexpr int PER = KM * 128 / 256;
-    float lv[PER], rv[PER];
+  const int kk = a.kk ? a.kk[b] : a.kconst;
+  const float alpha = a.alpha ? a.alpha[b] : 1.f;
 #pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int e = tid + 256 * u, j = e >> 7, x = e & 127;
-      lv[u] = j < kk ? a.L[b * a.sl + (long long)j * a.ldl + i0 + x] * a.coef[b * a.kmax + j] : 0.f;
-      rv[u] = j < kk ? a.Rr[b * a.sr + (long long)j * a.ldr + n0 + x] : 0.f;
-    }
-#pragma unroll
-    for (int u = 0; u < PER; ++u) {
-      const int e = tid + 256 * u, j = e >> 7, x = e & 127;
-      if (j < kk) {
-        ls[j][x] = lv[u];
-        rs[j][x] = rv[u];
-      }
+  for (int u = 0; u < PER; ++u) {
+    const int e = tid + 256 * u, j = e >> 7, x = e & 127;
+    if (j < a.kmax) {
+      ls[j][x] = lv[u];
+      rs[j][x] = rv[u];
     }
   }
   __syncthreads();
