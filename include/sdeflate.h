@@ -117,6 +117,30 @@ int sd_msign_deflated_bf16(int batch, int m, int n, int k, int steps, const floa
 /* dtype: SD_DTYPE_F32 or SD_DTYPE_BF16 for both in and out; opts may be NULL. */
 int sd_msign_deflated_ex(int batch, int m, int n, int k, int steps, const float* coeffs, int dtype,
                          const void* in, void* out, const sd_msign_opts* opts, hipStream_t stream);
+/* One shape group of a Muon step: the arguments of one sd_msign_deflated_ex
+ * call (opts may be NULL; a workspace in opts serves that group alone). */
+typedef struct {
+  int batch, m, n, k, steps;
+  const float* coeffs;        /* HOST [steps][3] or NULL */
+  int dtype;                  /* SD_DTYPE_F32 or SD_DTYPE_BF16 */
+  const void* in;
+  void* out;
+  const sd_msign_opts* opts;
+} sd_msign_group;
+
+/* The deflated polar factors of a whole Muon step: a parameter list grouped
+ * by shape, one batched call per group (App. D, "Grouping"; the grouping
+ * itself, wide vs tall and equal shapes, is the caller's). Every group is
+ * validated first: on an argument error nothing is enqueued and the error of
+ * the first bad group is returned. The groups then run concurrently on
+ * library-owned streams (default priority, at most three per device) that
+ * wait for `stream` and are joined back into it, so the results are ready
+ * when `stream` reaches that point, as with one call. Each group's result is
+ * the one sd_msign_deflated_ex gives for it alone, bit for bit. Scratch comes
+ * from the pool on the group's stream unless its opts bring a workspace.
+ * The output buffers of different groups must not overlap. */
+int sd_msign_groups(int ngroups, const sd_msign_group* groups, hipStream_t stream);
+
 /* Workspace an _ex call with these arguments needs (0 on invalid arguments). */
 size_t sd_msign_workspace_bytes(int batch, int m, int n, int k, int dtype, const sd_msign_opts* opts);
 /* The Gaussian sketch Alg. 3 draws (Omega ~ N(0, 1)^{s x r'} per matrix): out[b][j][i]

@@ -2,6 +2,7 @@
 MI355X). Argument marshalling only: every step runs in the HIP library.
 
     msign(x, k, steps, coeffs=None, ...)        -> sd_msign_deflated_ex
+    msign_groups([{x, k, steps, ...}, ...])      -> sd_msign_groups
     psd_project(X, k, steps, qwarm=None, ...)    -> sd_psd_project_deflated_ex
 
 Tensors are torch CUDA (ROCm) tensors; torch provides device memory and the
@@ -46,6 +47,21 @@ class MsignOpts(ctypes.Structure):
     ]
 
 
+class MsignGroup(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int),
+        ("m", ctypes.c_int),
+        ("n", ctypes.c_int),
+        ("k", ctypes.c_int),
+        ("steps", ctypes.c_int),
+        ("coeffs", ctypes.c_void_p),
+        ("dtype", ctypes.c_int),
+        ("input", ctypes.c_void_p),
+        ("out", ctypes.c_void_p),
+        ("opts", ctypes.POINTER(MsignOpts)),
+    ]
+
+
 class PsdOpts(ctypes.Structure):
     _fields_ = [
         ("subspace_iters", ctypes.c_int),
@@ -78,6 +94,7 @@ def _declare(lib):
         "sd_msign_deflated_bf16": (i, [i, i, i, i, i, vp, vp, vp, vp]),
         "sd_msign_deflated_ex": (i, [i, i, i, i, i, vp, i, vp, vp, ctypes.POINTER(MsignOpts), vp]),
         "sd_msign_workspace_bytes": (sz, [i, i, i, i, i, ctypes.POINTER(MsignOpts)]),
+        "sd_msign_groups": (i, [i, ctypes.POINTER(MsignGroup), vp]),
         "sd_msign_opts_default": (None, [ctypes.POINTER(MsignOpts)]),
         "sd_psd_project": (i, [i, i, vp, vp, vp]),
         "sd_psd_project_deflated": (i, [i, i, i, vp, vp, vp, vp]),
@@ -210,6 +227,42 @@ def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, po
     if info:
         return res, {"k_eff": keff, "nu": nu, "s": sv[:, :k]}
     return res
+
+
+def msign_groups(groups, *, stream=None):
+    """One Muon step over several shape groups (sd_msign_groups): groups is a
+    list of dicts with keys x ([B, m, n] bf16 or float32 CUDA tensor), k,
+    steps, and optionally coeffs, out, oversample, power_iters, gamma, tau,
+    seed. The groups run concurrently inside the library; returns the list of
+    outputs."""
+    import torch
+    n = len(groups)
+    arr = (MsignGroup * n)()
+    keep = []
+    outs = []
+    for i, g in enumerate(groups):
+        x = g["x"]
+        if x.dim() != 3 or not x.is_cuda or not x.is_contiguous():
+            raise ValueError("every x must be a contiguous CUDA tensor [B, m, n]")
+        if x.dtype == torch.bfloat16:
+            dtype = SD_DTYPE_BF16
+        elif x.dtype == torch.float32:
+            dtype = SD_DTYPE_F32
+        else:
+            raise TypeError("x must be bfloat16 or float32")
+        b, m, nn = x.shape
+        steps = int(g.get("steps", 5))
+        out = g.get("out")
+        out = torch.empty_like(x) if out is None else out
+        table, tptr = _host_table(g.get("coeffs"), steps, 3)
+        o = msign_opts(**{key: g[key] for key in ("oversample", "power_iters", "gamma", "tau", "seed") if key in g})
+        keep += [table, o]
+        arr[i] = MsignGroup(b, m, nn, int(g.get("k", 0)), steps, tptr.value if tptr is not None else None, dtype,
+                            x.data_ptr(), out.data_ptr(), ctypes.pointer(o))
+        outs.append(out)
+    _check(lib().sd_msign_groups(n, arr, _stream(stream)), "sd_msign_groups")
+    del keep
+    return outs
 
 
 def sketch_host(batch: int, s: int, rp: int, seed: int = 0) -> np.ndarray:

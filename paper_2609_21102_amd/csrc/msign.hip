@@ -361,6 +361,9 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   return hip_status();
 }
 
+static int msign_enqueue(int batch, int m, int n, int k, int steps, const float* coeffs, int dtype,
+                         const void* in, void* out, const sd_msign_opts& o, hipStream_t stream);
+
 }  // namespace sd
 
 using namespace sd;
@@ -398,6 +401,15 @@ int sd_msign_deflated_ex(int batch, int m, int n, int k, int steps, const float*
   if (opts) o = *opts;
   int rc = validate_msign(batch, m, n, k, steps, dtype, in, out, o);
   if (rc != SD_OK) return rc;
+  return sd::msign_enqueue(batch, m, n, k, steps, coeffs, dtype, in, out, o, stream);
+}
+}  // extern "C"
+
+namespace sd {
+// Enqueue one validated call.
+static int msign_enqueue(int batch, int m, int n, int k, int steps, const float* coeffs, int dtype,
+                         const void* in, void* out, const sd_msign_opts& o, hipStream_t stream) {
+  int rc;
   MsignPlan p{};
   make_plan(p, batch, m, n, k, steps, dtype, in, o);
   Arena sizing;
@@ -414,6 +426,75 @@ int sd_msign_deflated_ex(int batch, int m, int n, int k, int steps, const float*
   else
     rc = run_msign<float>(p, coeffs, o, reinterpret_cast<const float*>(in), reinterpret_cast<float*>(out), stream);
   scratch.release();
+  return rc;
+}
+
+// Library-owned streams for concurrent groups: per device, created on first
+// use (non-blocking, default priority) and kept until the process ends, with
+// one fork event and one join event per stream.
+struct GroupStreams {
+  static constexpr int N = 3;
+  hipStream_t s[N] = {};
+  hipEvent_t fork = nullptr, join[N] = {};
+  bool ready = false;
+};
+
+static int group_streams(GroupStreams*& gs) {
+  static std::mutex mu;
+  static GroupStreams per_dev[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return SD_ERR_HIP;
+  std::lock_guard<std::mutex> g(mu);
+  GroupStreams& d = per_dev[dev];
+  if (!d.ready) {
+    for (int i = 0; i < GroupStreams::N; ++i) {
+      if (hipStreamCreateWithFlags(&d.s[i], hipStreamNonBlocking) != hipSuccess) return SD_ERR_HIP;
+      if (hipEventCreateWithFlags(&d.join[i], hipEventDisableTiming) != hipSuccess) return SD_ERR_HIP;
+    }
+    if (hipEventCreateWithFlags(&d.fork, hipEventDisableTiming) != hipSuccess) return SD_ERR_HIP;
+    d.ready = true;
+  }
+  gs = &d;
+  return SD_OK;
+}
+}  // namespace sd
+
+extern "C" {
+
+int sd_msign_groups(int ngroups, const sd_msign_group* groups, hipStream_t stream) {
+  if (ngroups < 1 || !groups) return SD_ERR_INVALID_ARG;
+  std::vector<sd_msign_opts> opts(ngroups);
+  for (int i = 0; i < ngroups; ++i) {
+    const sd_msign_group& g = groups[i];
+    sd_msign_opts_default(&opts[i]);
+    if (g.opts) opts[i] = *g.opts;
+    const int rc = validate_msign(g.batch, g.m, g.n, g.k, g.steps, g.dtype, g.in, g.out, opts[i]);
+    if (rc != SD_OK) return rc;
+  }
+  if (ngroups == 1) {
+    const sd_msign_group& g = groups[0];
+    return msign_enqueue(g.batch, g.m, g.n, g.k, g.steps, g.coeffs, g.dtype, g.in, g.out, opts[0], stream);
+  }
+  GroupStreams* gs = nullptr;
+  int rc = group_streams(gs);
+  if (rc != SD_OK) return rc;
+  // one host thread at a time enqueues on the shared streams and events
+  static std::mutex enqueue_mu;
+  std::lock_guard<std::mutex> lock(enqueue_mu);
+  const int used = ngroups < GroupStreams::N ? ngroups : GroupStreams::N;
+  if (hipEventRecord(gs->fork, stream) != hipSuccess) return SD_ERR_HIP;
+  for (int i = 0; i < used; ++i)
+    if (hipStreamWaitEvent(gs->s[i], gs->fork, 0) != hipSuccess) return SD_ERR_HIP;
+  for (int i = 0; i < ngroups && rc == SD_OK; ++i) {
+    const sd_msign_group& g = groups[i];
+    rc = msign_enqueue(g.batch, g.m, g.n, g.k, g.steps, g.coeffs, g.dtype, g.in, g.out, opts[i],
+                       gs->s[i % GroupStreams::N]);
+  }
+  // join every used stream back, also after a failure, so `stream` never runs ahead
+  for (int i = 0; i < used; ++i) {
+    if (hipEventRecord(gs->join[i], gs->s[i]) != hipSuccess || hipStreamWaitEvent(stream, gs->join[i], 0) != hipSuccess)
+      return SD_ERR_HIP;
+  }
   return rc;
 }
 

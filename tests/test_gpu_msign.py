@@ -229,3 +229,56 @@ def test_steps_zero_returns_start():
     torch.cuda.synchronize()
     want, _ = omuon.msign_deflated(case.x64, 2, np.zeros((0, 3)))
     assert rel_fro(host64(out), want) < 1e-5
+
+
+def _group_args(case):
+    return dict(x=dev_tensor(case.x, case.dtype), k=case.k, steps=case.steps, coeffs=case.coeffs,
+                oversample=case.oversample, power_iters=case.power_iters, gamma=case.gamma)
+
+
+def test_groups_match_single_calls_bitwise():
+    """sd_msign_groups runs the groups concurrently on the library's streams;
+    each group's result must be the single call's, bit for bit."""
+    cases = [workloads.config2(g, batch=3) for g in ("768x768", "768x2304", "768x3072")]
+    cases.append(workloads.small_muon(2, 300, 200, dtype="f32", k=4, case_id=31))
+    groups = [_group_args(c) for c in cases]
+    outs = sd.msign_groups(groups)
+    outs2 = sd.msign_groups(groups)
+    torch.cuda.synchronize()
+    for g, c, o, o2 in zip(groups, cases, outs, outs2):
+        ref = sd.msign(g["x"], c.k, c.steps, c.coeffs, oversample=c.oversample, power_iters=c.power_iters,
+                       gamma=c.gamma)
+        torch.cuda.synchronize()
+        say(f"group {c.name}: equal {torch.equal(o, ref)}")
+        assert torch.equal(o, ref)
+        assert torch.equal(o, o2)
+
+
+def test_groups_reject_bad_group_without_enqueueing():
+    case = workloads.config2("768x768", batch=2)
+    good = _group_args(case)
+    out = torch.full_like(good["x"], 7.0)
+    bad = dict(good, k=768)          # k >= min(m, n)
+    with pytest.raises(sd.SdError):
+        sd.msign_groups([dict(good, out=out), bad])
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all())  # nothing ran
+
+
+@pytest.mark.slow
+@pytest.mark.timeout(600)
+def test_paper_scale_groups_sampled():
+    """The paper's GPT-2 Large groups in one grouped call (144 x 1280 x 1280
+    and 72 x 5120 x 1280, tall, k = 32, r' = 64); the oracle checks two
+    batch positions of each group (each position draws its own sketch)."""
+    cases = [workloads.paper_scale_group(g) for g in ("1280x1280", "5120x1280")]
+    groups = [_group_args(c) for c in cases]
+    outs = sd.msign_groups(groups)
+    torch.cuda.synchronize()
+    for c, o in zip(cases, outs):
+        got = host64(o)
+        for b in (1, c.x.shape[0] - 1):
+            want, oinfo = oracle_case(c, idx=[b])
+            err = rel_fro(got[b], want[0])
+            say(f"{c.name} matrix {b}: rel err {err:.3e}")
+            assert err < BF16_TOL

@@ -192,6 +192,30 @@ def config3(group: str = "768x3072", batch: int | None = None) -> MuonCase:
     return c
 
 
+# The paper's GPT-2 Large Muon groups (App. D): 144 square 1280 x 1280 and 72
+# tall 5120 x 1280 matrices, deflation rank 32 with 64 sketch columns.
+PAPER_GROUPS = {"1280x1280": (144, 1280, 1280), "5120x1280": (72, 5120, 1280)}
+
+
+def paper_scale_group(group: str, distinct: int = 6) -> MuonCase:
+    """A paper-scale bf16 group: 32 spikes geometric from 50 down to 5 over a
+    log-uniform bulk in [1e-4, 1]; k = 32, oversample 32 (r' = 64), 1 power
+    iteration, 5 steps of Muon's quintic. The batch cycles through `distinct`
+    seeded matrices (matrix b is matrix b mod distinct); every batch position
+    still draws its own sketch, so each position is an independent case."""
+    b, m, n = PAPER_GROUPS[group]
+    spikes = [50.0 * 10.0 ** (-i / 31.0) for i in range(32)]
+    gid = list(PAPER_GROUPS).index(group)
+    pool = muon_batch(f"paper_{group}_pool", distinct, m, n, dtype="bf16", spikes=spikes,
+                      bulk=(1e-4, 1.0), k=32, oversample=32, power_iters=1, steps=5,
+                      coeffs=muon_coeff_table(5), gamma=1.01, ids=(6, gid))
+    idx = np.arange(b) % distinct
+    pool.name = f"paper_{b}x{group}_bf16"
+    pool.x = np.ascontiguousarray(pool.x[idx])
+    pool.spectra = [pool.spectra[i] for i in idx]
+    return pool
+
+
 def small_muon(b, m, n, *, dtype="f32", k=4, spikes=None, bulk=(1e-3, 1.0),
                oversample=8, power_iters=1, steps=5, coeffs=None, gamma=1.01,
                case_id=0) -> MuonCase:
