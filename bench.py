@@ -123,6 +123,103 @@ def cpu_baseline(case, seconds: float) -> dict:
                       f"bf16-contract mode, {dt:.1f} s"}
 
 
+def _timed(step, steps: int, warmup: int) -> float:
+    """Milliseconds per step over `steps` timed calls after `warmup` calls."""
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / steps
+
+
+def other_workload(args) -> int:
+    """Throughput of the configurations other than the benchmark line."""
+    import torch
+    import paper_2609_21102_amd as sd
+    import workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def muon_groups(cases):
+        groups = []
+        for c in cases:
+            x = torch.from_numpy(c.x.view(np.int16).copy()).view(torch.bfloat16).to(dev)
+            groups.append(dict(x=x, out=torch.empty_like(x), k=c.k, steps=c.steps, coeffs=c.coeffs,
+                               oversample=c.oversample, power_iters=c.power_iters, gamma=c.gamma))
+        flops = 0.0
+        for c in cases:
+            b, m, n = c.x.shape
+            s, l = min(m, n), max(m, n)
+            rp = min(s, c.k + c.oversample)
+            flops += b * (ns_flops_per_matrix(s, l, c.steps) + front_flops_per_matrix(s, l, c.k, rp, c.power_iters))
+        return groups, flops
+
+    if args.workload in ("c2-step", "paper-step", "c3"):
+        if args.workload == "c2-step":
+            cases = [workloads.config2(g) for g in ("768x768", "768x2304", "768x3072")]
+        elif args.workload == "paper-step":
+            cases = [workloads.paper_scale_group(g) for g in ("1280x1280", "5120x1280")]
+        else:
+            cases = [workloads.config3("768x3072")]
+        groups, flops = muon_groups(cases)
+        nmat = sum(c.x.shape[0] for c in cases)
+        if args.sequential:
+            def step():
+                for g in groups:
+                    sd.msign(g["x"], g["k"], g["steps"], g["coeffs"], oversample=g["oversample"],
+                             power_iters=g["power_iters"], gamma=g["gamma"], out=g["out"])
+        else:
+            def step():
+                sd.msign_groups(groups)
+        ms = _timed(step, args.steps, args.warmup)
+        desc = " + ".join(f"{c.x.shape[0]} x {c.x.shape[1]} x {c.x.shape[2]}" for c in cases)
+        res = {"metric": f"deflated msign matrices/s ({args.workload}: {desc} bf16)", "value": nmat / (ms / 1e3),
+               "unit": "matrices/s", "ms_per_step": ms, "tflops": flops / (ms / 1e3) / 1e12,
+               "mfma_frac": flops / (ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, "steps": args.steps,
+               "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
+               "config": {"workload": args.workload, "groups": desc,
+                          "launch": "one call per group" if args.sequential else "sd_msign_groups",
+                          "k": [c.k for c in cases], "filter_steps": [c.steps for c in cases]}}
+    else:
+        if args.workload == "c4":
+            case = workloads.config4()
+            z = torch.from_numpy(case.z).to(dev)
+            lam, q0 = None, torch.from_numpy(np.ascontiguousarray(case.qwarm)).to(dev)
+            n, k, steps, sub = case.z.shape[0], case.k, case.steps, case.subspace_iters
+        else:
+            z, lam, _, q0 = workloads.config5_device(16384)
+            n, k, steps, sub = 16384, 32, 10, 1
+        q = q0.clone()
+        out = torch.empty_like(z)
+        ws = torch.empty(sd.psd_workspace_bytes(n, k), dtype=torch.uint8, device=dev)
+
+        def call():
+            q.copy_(q0)   # every timed call starts from the same warm basis
+            sd.psd_project(z, k, steps, q, subspace_iters=sub, gamma=1.1, out=out, workspace=ws)
+
+        ms = _timed(call, args.steps, args.warmup)
+        # cubic filter: X^2 and X X^2 are both symmetric and computed on upper-triangle
+        # tiles (n^3 each per step); the restore product R g is a full 2 n^3
+        flops = 2.0 * n ** 3 * steps + 2.0 * n ** 3
+        res = {"metric": f"deflated PSD projections/s ({args.workload}: n = {n} fp32, k = {k})",
+               "value": 1e3 / ms, "unit": "projections/s", "ms_per_step": ms,
+               "tflops": flops / (ms / 1e3) / 1e12, "fp32_mfma_frac": flops / (ms / 1e3) / 1e12 / 157.3,
+               "steps": args.steps, "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
+               "config": {"workload": args.workload, "n": n, "k": k, "filter_steps": steps,
+                          "subspace_iters": sub}}
+    log(f"bench {args.workload}: {res['ms_per_step']:.3f} ms per call, {res['value']:.1f} {res['unit']}, "
+        f"{res['tflops']:.1f} TFLOP/s")
+    print(json.dumps(res), flush=True)
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -133,6 +230,12 @@ def main() -> int:
     ap.add_argument("--baseline", action="store_true", help="time the undeflated filter (k = 0) instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 256 MiB device copy before timing (counter calibration)")
+    ap.add_argument("--workload", default="headline",
+                    choices=["headline", "c2-step", "c3", "paper-step", "c4", "c5"],
+                    help="headline: the benchmark line; the others time further configurations "
+                         "(one JSON line each, no roofline or CPU baseline)")
+    ap.add_argument("--sequential", action="store_true",
+                    help="c2-step / paper-step: one call per group on one stream instead of sd_msign_groups")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         log("bench.py: this build runs on a single GPU; --gpus must be 1 "
@@ -142,6 +245,9 @@ def main() -> int:
     import torch
     import paper_2609_21102_amd as sd
     import workloads
+
+    if args.workload != "headline":
+        return other_workload(args)
 
     case = workloads.config2("768x3072")
     b, m, n = case.x.shape
