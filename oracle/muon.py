@@ -20,6 +20,9 @@ Deflated polar factor (Alg. 1):
                 X0 = R / nu + gamma^-1 U_k V_k^T
     k_eff = 0:  X0 = A / ||A||_F
     return N_L o ... o N_1 (X0).
+Explicit restore (restore="explicit", the gamma -> infinity form of the
+exact split polar(M) = U_k V_k^T + polar(R_k), eq:identities in Sec. 1):
+    X0 = R / nu (no head term),  return U_k V_k^T + N_L o ... o N_1 (X0).
 Degenerate scales (no epsilon is added, the paper has none): a zero nu or a
 zero ||A||_F drops that term (a zero matrix maps to zero).
 
@@ -81,8 +84,9 @@ def deflation_rank(s: np.ndarray, k: int, tau: float) -> int:
     return 0
 
 
-def deflated_init(a, u, s, v, k_eff, gamma):
-    """Padded initialization X0 of Alg. 1 and the residual norm used."""
+def deflated_init(a, u, s, v, k_eff, gamma, restore="padded"):
+    """Start X0 of Alg. 1 (padded: the head enters at gamma^-1) or of the
+    explicit restore (residual only), and the residual norm used."""
     if k_eff == 0:
         nrm = float(np.linalg.norm(a))
         x0 = a / nrm if nrm > 0 else np.zeros_like(a)
@@ -90,15 +94,21 @@ def deflated_init(a, u, s, v, k_eff, gamma):
     uk, sk, vk = u[:, :k_eff], s[:k_eff], v[:, :k_eff]
     r = a - (uk * sk) @ vk.T
     nu = float(np.linalg.norm(r))
-    x0 = (r / nu if nu > 0 else np.zeros_like(r)) + (uk @ vk.T) / gamma
+    x0 = r / nu if nu > 0 else np.zeros_like(r)
+    if restore == "padded":
+        x0 = x0 + (uk @ vk.T) / gamma
     return x0, nu
 
 
 def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
-                   tau=0.0, seed=0, mode="exact", sketches=None):
+                   tau=0.0, seed=0, mode="exact", sketches=None, restore="padded"):
     """Deflated polar factor of every matrix of x [B, rows, cols] (float64
     values). coeffs: per-step table [L, 3]. Returns (out [B, rows, cols], info).
-    sketches: optional list of Omega (m x r') overriding the generator."""
+    sketches: optional list of Omega (m x r') overriding the generator.
+    restore: "padded" (Alg. 1) or "explicit" (U_k V_k^T added after the
+    filter; gamma is then unused)."""
+    if restore not in ("padded", "explicit"):
+        raise ValueError(f"unknown restore {restore!r}")
     x = np.asarray(x, dtype=np.float64)
     outs, keff, nus, svals = [], [], [], []
     rprime = 0
@@ -114,8 +124,11 @@ def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
         else:
             u = s = v = None
             k_eff = 0
-        x0, nu = deflated_init(a, u, s, v, k_eff, gamma)
-        xl = rounding(mode)(ns_filter(x0, coeffs, mode))
+        x0, nu = deflated_init(a, u, s, v, k_eff, gamma, restore)
+        xl = ns_filter(x0, coeffs, mode)
+        if restore == "explicit" and k_eff > 0:
+            xl = xl + u[:, :k_eff] @ v[:, :k_eff].T
+        xl = rounding(mode)(xl)
         outs.append(xl.T if transposed else xl)
         keff.append(k_eff)
         nus.append(nu)

@@ -128,6 +128,42 @@ def test_pipeline_with_exact_head_matches_scalarized_closed_form():
     np.testing.assert_allclose(info.nu[0], nu, rtol=1e-12)
 
 
+def test_explicit_restore_matches_scalarized_closed_form():
+    # Explicit restore (eq:identities): the head is added after the filter, so
+    # its singular values are exactly 1 and the tail's are p^L(sigma_i / ||R||_F).
+    g = np.random.default_rng(19)
+    n, m, k = 50, 12, 3
+    sig = np.array([40.0, 20.0, 10.0, 1.0, 0.8, 0.5, 0.3, 0.2, 0.1, 0.05, 0.02, 0.01])
+    u, v = haar(g, n, m), haar(g, m, m)
+    a = (u * sig) @ v.T
+    table = [bjorck_bowie(2)] * 5
+    out, info = muon.msign_deflated(a[None], k, table, oversample=9, power_iters=2, restore="explicit")
+    nu = np.linalg.norm(sig[k:])
+    x = np.concatenate([np.ones(k), scalar_compose(sig[k:] / nu, table)])
+    want = (u * x) @ v.T
+    np.testing.assert_allclose(out[0], want, atol=1e-9)
+    # the padded form with a huge gamma leaves the head out of the filter: it
+    # differs from the explicit form by exactly U_k V_k^T
+    pad, _ = muon.msign_deflated(a[None], k, table, oversample=9, power_iters=2, gamma=1e30)
+    np.testing.assert_allclose(out[0] - pad[0], u[:, :k] @ v[:, :k].T, atol=1e-9)
+
+
+def test_explicit_restore_converges_to_polar_and_k0_is_baseline():
+    g = np.random.default_rng(23)
+    a, *_ = spiked(g, 40, 16, [30.0, 10.0], tail_lo=0.05)
+    # 20 classical steps resolve the tail (sigma_min / ||R||_F = 0.056). Many more
+    # would not stay converged: the head directions of R / nu are rounding-level
+    # (1e-16), the filter grows them by about 1.5 per step, and after ~60 steps
+    # they rejoin the restored head. The padded form has no such drift.
+    table = [bjorck_bowie(1)] * 20
+    # r' = m: the estimated head is exact, so the split is the exact one of eq:identities
+    out, _ = muon.msign_deflated(a[None], 2, table, oversample=14, restore="explicit")
+    np.testing.assert_allclose(out[0], muon.polar_exact(a[None])[0], atol=1e-8)
+    base = muon.msign(a[None], table[:5])
+    expl, _ = muon.msign_deflated(a[None], 0, table[:5], restore="explicit")
+    assert np.array_equal(base, expl)
+
+
 def test_deflation_lowers_error_on_config1():
     # Sec. 3 claim (empirical with Muon's coefficients): deflation lowers the error to polar(M).
     c = workloads.config1()
