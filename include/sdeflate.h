@@ -88,6 +88,14 @@ enum { SD_FLAG_PIVOT_FLOOR = 2 /* a CholeskyQR pivot hit its floor: a rank-defic
  *   0 <= steps <= 1000. k = 0 is the undeflated baseline, and the gated
  *   variant that deflates nothing returns the baseline bit for bit (Sec. 2.2).
  */
+/* How the deflated head returns (eq:identities: polar(M) = U_k V_k^T + polar(R_k)):
+ *   PADDED (Alg. 1): X0 = R / ||R||_F + gamma^-1 U_k V_k^T, and the filter
+ *     itself drives the head toward 1;
+ *   EXPLICIT (the gamma -> infinity form): X0 = R / ||R||_F, and U_k V_k^T is
+ *     added to the filter's output (in float32, before the final rounding).
+ *     gamma is unused. Needs steps >= 1 (SD_ERR_UNSUPPORTED otherwise). */
+enum { SD_RESTORE_PADDED = 0, SD_RESTORE_EXPLICIT = 1 };
+
 typedef struct {
   int oversample;          /* p >= 0, default 8 */
   int power_iters;         /* J >= 0, default 1 */
@@ -102,6 +110,7 @@ typedef struct {
   float* nu_out;           /* optional device float[batch]: norm X0 was scaled by */
   float* s_out;            /* optional device float[batch][k]: estimated singular values */
   int* status_dev;         /* optional device int: SD_FLAG_* bits are OR-ed in */
+  int restore;             /* SD_RESTORE_PADDED (default) or SD_RESTORE_EXPLICIT */
 } sd_msign_opts;
 
 void sd_msign_opts_default(sd_msign_opts* opts);

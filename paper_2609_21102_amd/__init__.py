@@ -24,6 +24,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "sdeflate.h")
 SD_OK = 0
 SD_DTYPE_F32 = 0
 SD_DTYPE_BF16 = 1
+SD_RESTORE = {"padded": 0, "explicit": 1}
 MUON_QUINTIC = (3.4445, -4.7750, 2.0315)
 
 _c_int_p = ctypes.POINTER(ctypes.c_int)
@@ -44,6 +45,7 @@ class MsignOpts(ctypes.Structure):
         ("nu_out", ctypes.c_void_p),
         ("s_out", ctypes.c_void_p),
         ("status_dev", ctypes.c_void_p),
+        ("restore", ctypes.c_int),
     ]
 
 
@@ -180,11 +182,12 @@ def psd_opts(**kw) -> PsdOpts:
 
 def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, power_iters: int = 1,
           gamma: float = 1.01, tau: float = 0.0, seed: int = 0, sketch=None, out=None, workspace=None,
-          info: bool = False, stream=None):
+          restore: str = "padded", info: bool = False, stream=None):
     """(Deflated) polar factor of every matrix of x ([B, m, n] or [m, n], bf16 or
     float32, contiguous, on the GPU). k = 0 is the undeflated baseline.
     Returns out (same shape and dtype), and with info=True a dict of device
-    tensors k_eff [B], nu [B], s [B, k]."""
+    tensors k_eff [B], nu [B], s [B, k]. restore: "padded" (Alg. 1) or
+    "explicit" (U_k V_k^T added after the filter)."""
     import torch
     squeeze = x.dim() == 2
     xb = x.unsqueeze(0) if squeeze else x
@@ -206,7 +209,8 @@ def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, po
     keff = torch.empty(b, dtype=torch.int32, device=dev) if info else None
     nu = torch.empty(b, dtype=torch.float32, device=dev) if info else None
     sv = torch.empty((b, max(k, 1)), dtype=torch.float32, device=dev) if info else None
-    o = msign_opts(oversample=oversample, power_iters=power_iters, gamma=gamma, tau=tau, seed=seed)
+    o = msign_opts(oversample=oversample, power_iters=power_iters, gamma=gamma, tau=tau, seed=seed,
+                   restore=SD_RESTORE[restore])
     if sketch is not None:
         s_ = min(m, n)
         rp = min(s_, k + oversample)
@@ -233,7 +237,7 @@ def msign_groups(groups, *, stream=None):
     """One Muon step over several shape groups (sd_msign_groups): groups is a
     list of dicts with keys x ([B, m, n] bf16 or float32 CUDA tensor), k,
     steps, and optionally coeffs, out, oversample, power_iters, gamma, tau,
-    seed. The groups run concurrently inside the library; returns the list of
+    seed, restore. The groups run concurrently inside the library; returns the list of
     outputs."""
     import torch
     n = len(groups)
@@ -256,6 +260,7 @@ def msign_groups(groups, *, stream=None):
         out = torch.empty_like(x) if out is None else out
         table, tptr = _host_table(g.get("coeffs"), steps, 3)
         o = msign_opts(**{key: g[key] for key in ("oversample", "power_iters", "gamma", "tau", "seed") if key in g})
+        o.restore = SD_RESTORE[g.get("restore", "padded")]
         keep += [table, o]
         arr[i] = MsignGroup(b, m, nn, int(g.get("k", 0)), steps, tptr.value if tptr is not None else None, dtype,
                             x.data_ptr(), out.data_ptr(), ctypes.pointer(o))

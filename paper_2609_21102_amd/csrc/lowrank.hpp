@@ -166,12 +166,14 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
 // nu = sqrt(sum of the residual tiles) (float64: per-lane strided partial
 // sums, then lane 0's butterfly total); alpha = 1/nu (0 for nu = 0) and the
 // start coefficients c_j = -(s_j / nu - 1 / gamma) of
-//   X0 = alpha X + sum_j L_j c_j R_j^T  =  R / nu + gamma^-1 L R^T.
-// One wave per matrix.
+//   X0 = alpha X + sum_j L_j c_j R_j^T  =  R / nu + gamma^-1 L R^T
+// (1 / gamma = 0 for the explicit restore). With coef_one, also the restore
+// coefficients: 1 for the deflated components, 0 past them. One wave per
+// matrix.
 static __global__ __launch_bounds__(64) void muon_finalize_kernel(const float* sumsq, int tiles, const float* sv,
                                                                   const int* keff, int kmax, float inv_gamma,
                                                                   float* alpha, float* coef_b, float* nu_dev,
-                                                                  float* nu_user, int batch) {
+                                                                  float* nu_user, float* coef_one, int batch) {
   const int b = blockIdx.x, lane = threadIdx.x;
   double acc = 0.0;
   for (int t = lane; t < tiles; t += WAVE) acc += (double)sumsq[(long long)b * tiles + t];
@@ -185,8 +187,10 @@ static __global__ __launch_bounds__(64) void muon_finalize_kernel(const float* s
     if (nu_user) nu_user[b] = (float)nu;
   }
   const int ke = keff ? keff[b] : 0;
-  for (int j = lane; j < kmax; j += WAVE)
+  for (int j = lane; j < kmax; j += WAVE) {
     coef_b[b * kmax + j] = j < ke ? (float)(-((double)sv[b * kmax + j] * inv - (double)inv_gamma)) : 0.f;
+    if (coef_one) coef_one[b * kmax + j] = j < ke ? 1.f : 0.f;
+  }
 }
 
 static __global__ void fill_kernel(float* p, long long n, float v) {

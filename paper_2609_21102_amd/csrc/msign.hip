@@ -15,6 +15,7 @@ namespace sd {
 struct MsignPlan {
   int batch, m, n, k, steps, dtype;
   bool tall, copy_in;
+  bool explicit_restore;  // head added after the filter (k > 0)
   int s, l, s_pad, l_pad, rp;
   int rq;                // rows of the sketch panels: rp rounded up to 32 (zero rows past rp)
   size_t esz;
@@ -25,7 +26,8 @@ struct MsignPlan {
   int8_t *xalo, *xblo;   // operand) plus 8-bit residuals
   float *a32;
   bf16_t* a16;
-  float *om, *yl, *ys, *E, *sv, *invsv, *coefA, *coefB, *Ls, *Ll, *sumsq, *alpha, *nu;
+  float *om, *yl, *ys, *E, *sv, *invsv, *coefA, *coefB, *coefR, *Ls, *Ll, *sumsq, *alpha, *nu;
+  float* xl32;           // explicit restore, bf16 path: the filter output in float32
   bf16_t *om16, *yl16, *ys16;   // bf16 copies of the panels: product operands (bf16 path)
   double *part, *fac;
   int* keff;
@@ -59,6 +61,8 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   p.invsv = ar.take<float>(B * kq);
   p.coefA = ar.take<float>(B * kq);
   p.coefB = ar.take<float>(B * kq);
+  p.coefR = p.explicit_restore ? ar.take<float>(B * kq) : nullptr;
+  p.xl32 = (p.explicit_restore && bf) ? ar.take<float>(B * sl) : nullptr;
   p.Ls = ar.take<float>(B * kq * p.s_pad);
   p.Ll = ar.take<float>(B * kq * p.l_pad);
   p.keff = ar.take<int>(B);
@@ -79,6 +83,8 @@ static int validate_msign(int batch, int m, int n, int k, int steps, int dtype, 
   if (k >= s) return SD_ERR_INVALID_ARG;
   if (o.oversample < 0 || o.power_iters < 0 || o.power_iters > 100) return SD_ERR_INVALID_ARG;
   if (!(o.gamma > 0.f) || !(o.tau >= 0.f) || !(o.tau < 1.f)) return SD_ERR_INVALID_ARG;
+  if (o.restore != SD_RESTORE_PADDED && o.restore != SD_RESTORE_EXPLICIT) return SD_ERR_INVALID_ARG;
+  if (o.restore == SD_RESTORE_EXPLICIT && steps == 0) return SD_ERR_UNSUPPORTED;
   if ((long long)m * n > (1ll << 31) || (long long)batch * m * n > (1ll << 40)) return SD_ERR_UNSUPPORTED;
   if (k > 0) {
     const long long rp = (long long)k + o.oversample < s ? (long long)k + o.oversample : s;
@@ -105,6 +111,7 @@ static void make_plan(MsignPlan& p, int batch, int m, int n, int k, int steps, i
   p.esz = dtype == SD_DTYPE_BF16 ? 2 : 4;
   const bool aligned = in && (reinterpret_cast<uintptr_t>(in) % 16 == 0);
   p.copy_in = p.tall || p.s != p.s_pad || p.l != p.l_pad || !aligned;
+  p.explicit_restore = o.restore == SD_RESTORE_EXPLICIT && k > 0;
 }
 
 // Iterate update X <- a X + B X on 128 x 128 tiles; the epilogue's X reads
@@ -231,7 +238,8 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   {
     ProfScope ps(SD_STAGE_LOWRANK, st);
     hipLaunchKernelGGL(muon_finalize_kernel, dim3(B), dim3(64), 0, st, p.sumsq, p.tiles, p.sv,
-                       p.k > 0 ? p.keff : nullptr, la.kmax, 1.f / o.gamma, p.alpha, p.coefB, p.nu, o.nu_out, B);
+                       p.k > 0 ? p.keff : nullptr, la.kmax, p.explicit_restore ? 0.f : 1.f / o.gamma, p.alpha,
+                       p.coefB, p.nu, o.nu_out, p.coefR, B);
   }
   la.coef = p.coefB;
   la.alpha = p.alpha;
@@ -292,6 +300,24 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     const bool last = t + 1 == p.steps;
     ProfScope ps(SD_STAGE_NS_UPDATE, st);
     if constexpr (BF) {
+      if (last && p.explicit_restore) {
+        // the filter output stays float32 (canonical layout) for the restore
+        EpiUpdateHL<float> ef{};
+        ef.hi = cur16;
+        ef.lo = curlo;
+        ef.xstride = sl;
+        ef.ldx = p.l_pad;
+        ef.ac = a;
+        ef.out = p.xl32;
+        ef.ostride = sl;
+        ef.ldo = p.l_pad;
+        ef.final_out = 1;
+        ef.transpose_out = 0;
+        ef.rows_valid = p.s_pad;
+        ef.cols_valid = p.l_pad;
+        update_gemm<T>(p, bm, xop(), g3, ef, st);
+        continue;
+      }
       EpiUpdateHL<T> eu{};
       eu.hi = cur16;
       eu.lo = curlo;
@@ -312,7 +338,7 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
         eu.cols_valid = p.l;
       }
       update_gemm<T>(p, bm, xop(), g3, eu, st);
-    } else if (!last) {
+    } else if (!last || p.explicit_restore) {
       EpiUpdate<float, float> eu{};
       eu.x = cur;
       eu.xstride = sl;
@@ -347,6 +373,31 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     int8_t* tmplo = curlo;
     curlo = nxtlo;
     nxtlo = tmplo;
+  }
+  if (p.explicit_restore) {
+    // out = X_L + U_k V_k^T (eq:identities), rounded once to the output type:
+    // straight into the caller's buffer when its layout is the canonical one,
+    // else through the canonical input buffer (free after the front end)
+    LowRankArgs ra = la;
+    if constexpr (BF) ra.x = p.xl32;
+    else ra.x = cur;   // the last update's target (the buffers were swapped after it)
+    ra.sx = sl;
+    ra.ldx = p.l_pad;
+    ra.coef = p.coefR;
+    ra.alpha = nullptr;
+    ra.out16 = nullptr;
+    ra.out_lo = nullptr;
+    ra.sumsq = nullptr;
+    const bool direct = !p.copy_in && reinterpret_cast<uintptr_t>(out) % 16 == 0;
+    ra.out = direct ? static_cast<void*>(out) : p.xc;
+    ra.so = direct ? (long long)p.m * p.n : sl;
+    ra.ldo = direct ? p.l : p.l_pad;
+    lowrank<float, T>(ra, st);
+    if (!direct) {
+      const long long tot = (long long)p.m * p.n * B;
+      hipLaunchKernelGGL((store_out_kernel<T, T>), grid1(tot, 256), dim3(256), 0, st, reinterpret_cast<const T*>(p.xc),
+                         sl, p.l_pad, out, (long long)p.m * p.n, p.s, p.l, p.tall ? 1 : 0, B);
+    }
   }
   if (p.steps == 0) {
     // the start itself, rounded to the output type (bf16 path: its hi)
@@ -385,7 +436,7 @@ size_t sd_msign_workspace_bytes(int batch, int m, int n, int k, int dtype, const
   sd_msign_opts_default(&o);
   if (opts) o = *opts;
   const char dummy[16] __attribute__((aligned(16))) = {0};
-  if (validate_msign(batch, m, n, k, 0, dtype, dummy, dummy, o) != SD_OK) return 0;
+  if (validate_msign(batch, m, n, k, 1, dtype, dummy, dummy, o) != SD_OK) return 0;
   MsignPlan p{};
   // assume the input needs a copy (upper bound over alignments)
   make_plan(p, batch, m, n, k, 0, dtype, nullptr, o);

@@ -46,7 +46,11 @@ int main(void) {
   F(sd_msign_opts, oversample) F(sd_msign_opts, power_iters) F(sd_msign_opts, gamma)
   F(sd_msign_opts, tau) F(sd_msign_opts, seed) F(sd_msign_opts, sketch) F(sd_msign_opts, workspace)
   F(sd_msign_opts, workspace_bytes) F(sd_msign_opts, k_eff_out) F(sd_msign_opts, nu_out)
-  F(sd_msign_opts, s_out) F(sd_msign_opts, status_dev)
+  F(sd_msign_opts, s_out) F(sd_msign_opts, status_dev) F(sd_msign_opts, restore)
+  printf("sd_msign_group %zu\n", sizeof(sd_msign_group));
+  F(sd_msign_group, batch) F(sd_msign_group, m) F(sd_msign_group, n) F(sd_msign_group, k)
+  F(sd_msign_group, steps) F(sd_msign_group, coeffs) F(sd_msign_group, dtype) F(sd_msign_group, in)
+  F(sd_msign_group, out) F(sd_msign_group, opts)
   F(sd_psd_opts, subspace_iters) F(sd_psd_opts, lanczos_steps) F(sd_psd_opts, gamma) F(sd_psd_opts, tau)
   F(sd_psd_opts, window) F(sd_psd_opts, poly_degree) F(sd_psd_opts, poly) F(sd_psd_opts, seed)
   F(sd_psd_opts, workspace) F(sd_psd_opts, workspace_bytes) F(sd_psd_opts, n_deflated_out)
@@ -72,9 +76,12 @@ def test_option_struct_layout_matches_header():
         got[parts[0]] = tuple(int(p) for p in parts[1:])
     assert got["sd_msign_opts"][0] == ctypes.sizeof(sd.MsignOpts)
     assert got["sd_psd_opts"][0] == ctypes.sizeof(sd.PsdOpts)
-    for cls, cname in ((sd.MsignOpts, "sd_msign_opts"), (sd.PsdOpts, "sd_psd_opts")):
+    assert got["sd_msign_group"][0] == ctypes.sizeof(sd.MsignGroup)
+    for cls, cname in ((sd.MsignOpts, "sd_msign_opts"), (sd.PsdOpts, "sd_psd_opts"),
+                       (sd.MsignGroup, "sd_msign_group")):
         for name, ctype in cls._fields_:
-            off, size = got[f"{cname}.{name}"]
+            cfield = "in" if name == "input" else name   # `in` is a Python keyword
+            off, size = got[f"{cname}.{cfield}"]
             assert getattr(cls, name).offset == off, name
             assert ctypes.sizeof(ctype) == size, name
 
@@ -109,11 +116,25 @@ def test_msign_invalid_options_and_pointers(lib):
     assert lib.sd_msign_deflated_ex(1, 8, 8, 0, 5, None, 7, FAKE, FAKE, None, None) == -1
     assert lib.sd_msign_deflated_ex(1, 8, 8, 0, 5, None, 0, None, FAKE, None, None) == -1
     assert lib.sd_msign_deflated_ex(1, 8, 8, 0, 5, None, 0, FAKE, None, None, None) == -1
-    for bad in (dict(gamma=0.0), dict(tau=1.0), dict(tau=-0.1), dict(oversample=-1), dict(power_iters=-1)):
+    for bad in (dict(gamma=0.0), dict(tau=1.0), dict(tau=-0.1), dict(oversample=-1), dict(power_iters=-1),
+                dict(restore=2), dict(restore=-1)):
         o = sd.msign_opts(**bad)
         assert lib.sd_msign_deflated_ex(1, 8, 8, 2, 5, None, 0, FAKE, FAKE, ctypes.byref(o), None) == -1
     # sketch wider than 64 columns is outside this build
     assert lib.sd_msign_deflated_ex(1, 256, 256, 60, 5, None, 0, FAKE, FAKE, None, None) == -2
+    # the explicit restore needs at least one filter step
+    o = sd.msign_opts(restore=sd.SD_RESTORE["explicit"])
+    assert lib.sd_msign_deflated_ex(1, 8, 8, 2, 0, None, 0, FAKE, FAKE, ctypes.byref(o), None) == -2
+    assert lib.sd_msign_workspace_bytes(1, 8, 8, 2, 0, ctypes.byref(o)) > 0
+
+
+def test_groups_invalid_arguments(lib):
+    ok = sd.MsignGroup(1, 8, 8, 2, 5, None, 0, FAKE.value, FAKE.value, None)
+    bad = sd.MsignGroup(1, 8, 8, 8, 5, None, 0, FAKE.value, FAKE.value, None)   # k >= min(m, n)
+    arr = (sd.MsignGroup * 2)(ok, bad)
+    assert lib.sd_msign_groups(2, arr, None) == -1
+    assert lib.sd_msign_groups(0, arr, None) == -1
+    assert lib.sd_msign_groups(1, None, None) == -1
 
 
 def test_psd_invalid_arguments(lib):
