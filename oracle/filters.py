@@ -25,6 +25,11 @@ G = hi^T hi; the operand of G^2 is bf16(G); B = bf16(b G + c G^2) (with the
 unrounded G) is a product operand; the new iterate a (carried X) + hi B is
 stored in the same form before the next step. ns_filter returns the last
 step's value as computed; the caller rounds it to its output precision.
+
+fp16 contract (mode "f16"), used for the PSD sign filter in fp16 (the paper's
+SDP experiments run the filter in fp16, App. E): every product operand is
+rounded to fp16 (X for G = X X, G for G^2, and B = b G + c G^2), the products
+accumulate wide, and the iterate is stored wide.
 """
 from __future__ import annotations
 
@@ -88,7 +93,7 @@ def ns_step(x: np.ndarray, coeffs, mode: str = "exact", operand=None) -> np.ndar
     rd = rounding(mode)
     coeffs = [float(c) for c in coeffs]
     if mode != "exact" and len(coeffs) > 3:
-        raise ValueError("the bf16 contract covers d <= 2")
+        raise ValueError("the rounding contracts cover d <= 2")
     x = np.asarray(x, dtype=np.float64)
     tall = x.shape[0] >= x.shape[1]
     xo = rd(x) if operand is None else np.asarray(operand, dtype=np.float64)   # product operand
@@ -116,7 +121,7 @@ def ns_filter(x0: np.ndarray, table, mode: str = "exact") -> np.ndarray:
     its input."""
     x = np.asarray(x0, dtype=np.float64)
     for row in table:
-        if mode == "exact":
+        if mode in ("exact", "f16"):
             x = ns_step(x, row, mode)
         else:
             hi, carried = store_state(x)

@@ -1,4 +1,4 @@
-"""Rounding used by the oracle's bf16 contract mode.
+"""Rounding used by the oracle's bf16 and fp16 contract modes.
 
 The paper trains in bfloat16 (Sec. 3 setup) but does not fix where values are
 rounded. The library's contract (and this mode) rounds to bfloat16 exactly at
@@ -38,6 +38,22 @@ def round_e4m3(x: np.ndarray) -> np.ndarray:
     return np.ldexp(np.rint(q), expo - 4)    # np.rint rounds half to even
 
 
+F16_MAX = 65504.0
+
+
+def round_f16(x: np.ndarray) -> np.ndarray:
+    """Round float64 values to the nearest IEEE binary16 value (10 fraction
+    bits, subnormal spacing 2**-24), ties to even, returned as float64. Inputs
+    must lie within the format's finite range (the filter's operands do)."""
+    x = np.asarray(x, dtype=np.float64)
+    if np.any(np.abs(x) > F16_MAX):
+        raise ValueError("round_f16 takes values in [-65504, 65504]")
+    mant, expo = np.frexp(x)                 # x = mant * 2**expo, |mant| in [0.5, 1)
+    expo = np.maximum(expo, -13)             # normal range starts at 2**-14
+    q = np.ldexp(x, 11 - expo)               # |q| < 2**11
+    return np.ldexp(np.rint(q), expo - 11)   # np.rint rounds half to even
+
+
 def identity(x: np.ndarray) -> np.ndarray:
     return np.asarray(x, dtype=np.float64)
 
@@ -47,4 +63,6 @@ def rounding(mode: str):
         return identity
     if mode == "bf16":
         return round_bf16
+    if mode == "f16":
+        return round_f16
     raise ValueError(f"unknown precision mode {mode!r}")

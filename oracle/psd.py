@@ -87,8 +87,9 @@ def ritz_order(lam: np.ndarray) -> np.ndarray:
 
 
 def psd_project_deflated(z, basis, *, table=None, steps=10, gamma=1.1, tau=0.0,
-                         window=0, subspace_iters=1, seed=0, lanczos_steps=20):
+                         window=0, subspace_iters=1, seed=0, lanczos_steps=20, mode="exact"):
     """Alg. 2. z: symmetric (n x n); basis: orthonormal (n x K).
+    mode: the sign filter's arithmetic, "exact" or "f16" (filters.ns_filter).
     Returns (P, V_next, info)."""
     z = np.asarray(z, dtype=np.float64)
     v = np.asarray(basis, dtype=np.float64)
@@ -115,26 +116,26 @@ def psd_project_deflated(z, basis, *, table=None, steps=10, gamma=1.1, tau=0.0,
         theta = lanczos_scale(lambda x: res @ (res @ x), n, seed, lanczos_steps)
         x0 = (res / theta if theta > 0 else np.zeros_like(res)) \
             + (ui * np.sign(li)) @ ui.T / gamma
-        g = ns_filter(x0, table)
+        g = ns_filter(x0, table, mode)
         p = 0.5 * (res + res @ g) + (ui * np.maximum(li, 0.0)) @ ui.T
         n_pos = int(np.count_nonzero(li > 0))
     else:
         theta = lanczos_scale(lambda x: z @ (z @ x), n, seed, lanczos_steps)
         x0 = z / theta if theta > 0 else np.zeros_like(z)
-        g = ns_filter(x0, table)
+        g = ns_filter(x0, table, mode)
         p = 0.5 * (z + z @ g)
         n_pos = 0
     p = 0.5 * (p + p.T)
     return p, cholqr(zt), PSDInfo(n_def, n_pos, theta, lam)
 
 
-def psd_project(z, *, table=None, steps=10, seed=0, lanczos_steps=20):
+def psd_project(z, *, table=None, steps=10, seed=0, lanczos_steps=20, mode="exact"):
     """Undeflated baseline projection (eq:baseline_projection), symmetrized."""
     z = np.asarray(z, dtype=np.float64)
     table = [CUBIC] * steps if table is None else table
     theta = lanczos_scale(lambda x: z @ (z @ x), z.shape[0], seed, lanczos_steps)
     x0 = z / theta if theta > 0 else np.zeros_like(z)
-    g = ns_filter(x0, table)
+    g = ns_filter(x0, table, mode)
     p = 0.5 * (z + z @ g)
     return 0.5 * (p + p.T), theta
 

@@ -27,6 +27,28 @@ def test_bf16_matches_library_rounding():
     np.testing.assert_array_equal(precision.round_bf16(x.astype(np.float64)), want)
 
 
+# --- fp16 rounding (operands of the fp16 sign filter) ---------------------------
+def test_f16_ties_subnormals_and_exact_values():
+    r = precision.round_f16
+    assert r(np.array([1 + 2.0 ** -11]))[0] == 1.0                        # tie -> even
+    assert r(np.array([1 + 3 * 2.0 ** -11]))[0] == 1 + 2.0 ** -9          # tie -> even
+    assert r(np.array([-(1 + 2.0 ** -11 + 2.0 ** -40)]))[0] == -(1 + 2.0 ** -10)
+    assert r(np.array([2.0 ** -24]))[0] == 2.0 ** -24                     # smallest subnormal
+    assert r(np.array([2.0 ** -25]))[0] == 0.0                            # tie -> even (zero)
+    assert r(np.array([3 * 2.0 ** -25]))[0] == 2.0 ** -23                 # tie -> even
+    assert r(np.array([65504.0]))[0] == 65504.0
+    with pytest.raises(ValueError):
+        r(np.array([65505.0]))
+
+
+def test_f16_matches_library_rounding():
+    g = np.random.default_rng(5)
+    x = (g.standard_normal(200000) * 10.0 ** g.uniform(-9, 4, 200000)).astype(np.float32)
+    x = np.clip(x, -65504, 65504)
+    want = torch.from_numpy(x).to(torch.float16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(precision.round_f16(x.astype(np.float64)), want)
+
+
 # --- e4m3 rounding (residual of the stored bf16 iterate) -------------------------
 def _e4m3_grid():
     """Every finite OCP e4m3 ("fn") value from its bit layout: sign, 4-bit

@@ -131,3 +131,34 @@ def test_deflation_lowers_error_on_small_config4_like():
     assert np.linalg.norm(pd - target) < 0.1 * np.linalg.norm(pb - target)
     np.testing.assert_allclose(np.sort(np.abs(info.ritz[:4])),
                                np.sort(np.abs(c.lam[np.argsort(-np.abs(c.lam))[:4]])), rtol=1e-6)
+
+
+# --- fp16 contract of the sign filter ----------------------------------------------
+def test_f16_filter_step_is_exact_on_dyadic_input():
+    # A diagonal X with dyadic entries keeps every operand, product and
+    # coefficient combination exactly representable: the fp16 contract must
+    # then equal exact arithmetic bit for bit (no rounding point is missing
+    # an operand, and none is applied to a wide value).
+    from oracle.filters import ns_filter
+    x = np.diag([0.5, -0.25, 0.75, 0.125, 0.0, -1.0])
+    for table in ([(1.5, -0.5)], [(1.875, -1.25, 0.375)]):
+        np.testing.assert_array_equal(ns_filter(x, table, "f16"), ns_filter(x, table))
+
+
+def test_f16_projection_within_the_fp16_error_of_exact():
+    # Operand rounding of 2^-11 relative, grown by the filter's slope, moves
+    # the output far less than the filter's own error: on a deflated case the
+    # fp16-contract projection stays within 1e-2 of the exact-arithmetic one
+    # and shares its bookkeeping, and differs from it (the contract is applied).
+    case = workloads.small_psd(160, k=8, case_id=12)
+    z = case.z.astype(np.float64)
+    q = case.qwarm.astype(np.float64)
+    p64, v64, i64 = psd.psd_project_deflated(z, q, steps=case.steps, gamma=case.gamma,
+                                             subspace_iters=case.subspace_iters)
+    p16, v16, i16 = psd.psd_project_deflated(z, q, steps=case.steps, gamma=case.gamma,
+                                             subspace_iters=case.subspace_iters, mode="f16")
+    err = np.linalg.norm(p16 - p64) / np.linalg.norm(p64)
+    assert 0 < err < 1e-2
+    assert (i16.n_deflated, i16.n_positive) == (i64.n_deflated, i64.n_positive)
+    np.testing.assert_array_equal(v16, v64)   # the basis update does not involve the filter
+
