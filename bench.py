@@ -202,16 +202,19 @@ def other_workload(args) -> int:
 
         def call():
             q.copy_(q0)   # every timed call starts from the same warm basis
-            sd.psd_project(z, k, steps, q, subspace_iters=sub, gamma=1.1, out=out, workspace=ws)
+            sd.psd_project(z, k, steps, q, subspace_iters=sub, gamma=1.1, out=out, workspace=ws,
+                           precision=args.precision)
 
         ms = _timed(call, args.steps, args.warmup)
         # cubic filter: X^2 and X X^2 are both symmetric and computed on upper-triangle
         # tiles (n^3 each per step); the restore product R g is a full 2 n^3
         flops = 2.0 * n ** 3 * steps + 2.0 * n ** 3
-        res = {"metric": f"deflated PSD projections/s ({args.workload}: n = {n} fp32, k = {k})",
+        peak = 157.3 if args.precision == "f32" else MFMA_BF16_PEAK_TFLOPS   # fp16 dense = bf16 dense
+        res = {"metric": f"deflated PSD projections/s ({args.workload}: n = {n}, k = {k}, "
+                         f"{args.precision} filter products)",
                "value": 1e3 / ms, "unit": "projections/s", "ms_per_step": ms,
-               "tflops": flops / (ms / 1e3) / 1e12, "fp32_mfma_frac": flops / (ms / 1e3) / 1e12 / 157.3,
-               "steps": args.steps, "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
+               "tflops": flops / (ms / 1e3) / 1e12, "mfma_frac": flops / (ms / 1e3) / 1e12 / peak,
+               "steps": args.steps, "warmup": args.warmup, "dtype": args.precision, "data": "synthetic",
                "config": {"workload": args.workload, "n": n, "k": k, "filter_steps": steps,
                           "subspace_iters": sub}}
     log(f"bench {args.workload}: {res['ms_per_step']:.3f} ms per call, {res['value']:.1f} {res['unit']}, "
@@ -234,6 +237,8 @@ def main() -> int:
                     choices=["headline", "c2-step", "c3", "paper-step", "c4", "c5"],
                     help="headline: the benchmark line; the others time further configurations "
                          "(one JSON line each, no roofline or CPU baseline)")
+    ap.add_argument("--precision", default="f32", choices=["f32", "f16"],
+                    help="c4 / c5: arithmetic of the sign filter's products")
     ap.add_argument("--sequential", action="store_true",
                     help="c2-step / paper-step: one call per group on one stream instead of sd_msign_groups")
     args = ap.parse_args()

@@ -184,6 +184,14 @@ int sd_sketch_host(int batch, int s, int rp, uint64_t seed, float* out);
  * required when k > 0 and must not overlap X or out. k = 0 is the baseline
  * (Qwarm unused, may be NULL).
  */
+/* Arithmetic of the sign filter's products (the paper's SDP experiments run
+ * the filter in fp16, App. E): SD_PREC_F32 computes them in float32 (fp32
+ * MFMA); SD_PREC_F16 rounds every product operand to fp16 (round to nearest
+ * even) and accumulates in float32 (fp16 MFMA). The iterate, the Gram and
+ * b A + c A^2 are stored in float32 either way, and the residual, the Lanczos
+ * scale and the restore product stay float32. */
+enum { SD_PREC_F32 = 0, SD_PREC_F16 = 1 };
+
 typedef struct {
   int subspace_iters;      /* J >= 1, default 1 */
   int lanczos_steps;       /* 1..64, default 20 */
@@ -200,6 +208,7 @@ typedef struct {
   float* theta_out;        /* optional device float */
   float* ritz_out;         /* optional device float[k], Ritz values in deflation order */
   int* status_dev;         /* optional device int */
+  int precision;           /* SD_PREC_F32 (default) or SD_PREC_F16, see below */
 } sd_psd_opts;
 
 void sd_psd_opts_default(sd_psd_opts* opts);

@@ -25,6 +25,7 @@ SD_OK = 0
 SD_DTYPE_F32 = 0
 SD_DTYPE_BF16 = 1
 SD_RESTORE = {"padded": 0, "explicit": 1}
+SD_PREC = {"f32": 0, "f16": 1}
 MUON_QUINTIC = (3.4445, -4.7750, 2.0315)
 
 _c_int_p = ctypes.POINTER(ctypes.c_int)
@@ -81,6 +82,7 @@ class PsdOpts(ctypes.Structure):
         ("theta_out", ctypes.c_void_p),
         ("ritz_out", ctypes.c_void_p),
         ("status_dev", ctypes.c_void_p),
+        ("precision", ctypes.c_int),
     ]
 
 
@@ -292,11 +294,12 @@ def msign_workspace_bytes(batch, m, n, k, dtype=SD_DTYPE_BF16, **kw) -> int:
 
 def psd_project(X, k: int = 0, steps: int = 10, qwarm=None, *, subspace_iters: int = 1,
                 lanczos_steps: int = 20, gamma: float = 1.1, tau: float = 0.0, window: int = 1,
-                poly=None, poly_degree: int = 3, seed: int = 0, out=None, workspace=None,
-                info: bool = False, stream=None):
+                poly=None, poly_degree: int = 3, seed: int = 0, precision: str = "f32", out=None,
+                workspace=None, info: bool = False, stream=None):
     """(Deflated) projection of the symmetric float32 X [n, n] onto the PSD cone.
     qwarm [n, k] (float32) is the warm-start basis and is overwritten with the
-    next basis. Returns out, and with info=True a dict of device tensors
+    next basis. precision: "f32", or "f16" (the sign filter's products take
+    fp16 operands). Returns out, and with info=True a dict of device tensors
     n_deflated, n_positive, theta, ritz."""
     import torch
     if X.dim() != 2 or X.shape[0] != X.shape[1] or X.dtype != torch.float32 or not X.is_contiguous():
@@ -308,7 +311,7 @@ def psd_project(X, k: int = 0, steps: int = 10, qwarm=None, *, subspace_iters: i
     table, tptr = _host_table(poly, steps, width)
     dev = X.device
     o = psd_opts(subspace_iters=subspace_iters, lanczos_steps=lanczos_steps, gamma=gamma, tau=tau,
-                 window=window, poly_degree=poly_degree, seed=seed)
+                 window=window, poly_degree=poly_degree, seed=seed, precision=SD_PREC[precision])
     if tptr is not None:
         o.poly = tptr.value
     if workspace is not None:

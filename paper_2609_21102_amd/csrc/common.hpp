@@ -29,6 +29,18 @@ __device__ __forceinline__ uint32_t pack_bf2(float lo, float hi) {
 __device__ __forceinline__ bf16_t f2bf(float f) { return (bf16_t)(pack_bf2(f, 0.f) & 0xffffu); }
 __device__ __forceinline__ float bf2f(bf16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
 
+// ---------------------------------------------------------------- fp16 ----
+// IEEE binary16 product operands (a tag type: the bits live in packed words).
+// float -> fp16 rounds to nearest even.
+struct f16_t {
+  uint16_t bits;
+};
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ uint32_t pack_h2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, f16x2_t));
+}
+
 // ------------------------------------------------- iterate state ----------
 // The bf16 iterate is stored as hi = bf16(x) plus one residual byte: the OCP
 // float8 e4m3 ("fn") code of (x - hi) 2^16, clamped to +-448 and rounded to
@@ -108,6 +120,28 @@ __device__ __forceinline__ f32x16_t mfma32_bf16(const u32x4_t& a, const u32x4_t&
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, a),
                                                  __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
 }
+__device__ __forceinline__ f32x16_t mfma32_f16(const u32x4_t& a, const u32x4_t& b, f32x16_t c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8_t, a), __builtin_bit_cast(f16x8_t, b), c, 0,
+                                                0, 0);
+}
+// The 16-bit operand types of the MFMA GEMMs: packing of two floats and the
+// 32 x 32 x 16 product with float32 accumulation.
+template <typename T>
+struct Op16;
+template <>
+struct Op16<bf16_t> {
+  __device__ __forceinline__ static uint32_t pack2(float lo, float hi) { return pack_bf2(lo, hi); }
+  __device__ __forceinline__ static f32x16_t mma(const u32x4_t& a, const u32x4_t& b, f32x16_t c) {
+    return mfma32_bf16(a, b, c);
+  }
+};
+template <>
+struct Op16<f16_t> {
+  __device__ __forceinline__ static uint32_t pack2(float lo, float hi) { return pack_h2(lo, hi); }
+  __device__ __forceinline__ static f32x16_t mma(const u32x4_t& a, const u32x4_t& b, f32x16_t c) {
+    return mfma32_f16(a, b, c);
+  }
+};
 __device__ __forceinline__ f32x16_t mfma32_f32(float a, float b, f32x16_t c) {
   return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
 }

@@ -34,6 +34,7 @@ constexpr int G_TILEB = 128 * G_ROWB;          // one 128-row operand tile
 
 template <typename T> struct GemmK;
 template <> struct GemmK<bf16_t> { static constexpr int BK = 64; };
+template <> struct GemmK<f16_t> { static constexpr int BK = 64; };
 template <> struct GemmK<float> { static constexpr int BK = 32; };
 
 struct GemmShape {
@@ -393,17 +394,19 @@ using CfgTile128s = GemmCfg<2, 2, 2, 2, 1, 2>;       // 128 x 128, 256 threads
 // Direct-to-LDS kernel: 128 x 128, two-stage ring, two work-groups per CU.
 using CfgDma128 = GemmCfg<2, 2, 2, 2, 2, 2>;
 
+// Eight floats (two 16-byte words) rounded to eight 16-bit operands of type T.
+template <typename T>
 __device__ __forceinline__ u32x4_t pack8(const u32x4_t& a, const u32x4_t& b) {
-  return u32x4_t{pack_bf2(__uint_as_float(a[0]), __uint_as_float(a[1])),
-                 pack_bf2(__uint_as_float(a[2]), __uint_as_float(a[3])),
-                 pack_bf2(__uint_as_float(b[0]), __uint_as_float(b[1])),
-                 pack_bf2(__uint_as_float(b[2]), __uint_as_float(b[3]))};
+  return u32x4_t{Op16<T>::pack2(__uint_as_float(a[0]), __uint_as_float(a[1])),
+                 Op16<T>::pack2(__uint_as_float(a[2]), __uint_as_float(a[3])),
+                 Op16<T>::pack2(__uint_as_float(b[0]), __uint_as_float(b[1])),
+                 Op16<T>::pack2(__uint_as_float(b[2]), __uint_as_float(b[3]))};
 }
 
 // Rows x K tile with K contiguous in memory (the A operand, and B in NT form):
 // ROWS rows of 8 LDS chunks of 16 bytes; chunk id = t + NT u -> row id / 8,
-// chunk id % 8. An fp32 source feeding bf16 MFMAs loads 32 bytes per chunk
-// and rounds them while writing LDS.
+// chunk id % 8. An fp32 source feeding 16-bit MFMAs (bf16 or fp16) loads 32
+// bytes per chunk and rounds them while writing LDS.
 template <int ROWS, int NT, typename T, typename S>
 struct RowStager {
   static constexpr bool CONV = sizeof(S) != sizeof(T);
@@ -429,7 +432,7 @@ struct RowStager {
 #pragma unroll
     for (int u = 0; u < UNITS; ++u) {
       const int id = t + NT * u, row = id >> 3, ch = id & 7;
-      if constexpr (CONV) st16(lds + row * G_ROWB + ch * 16, pack8(r[2 * u], r[2 * u + 1]));
+      if constexpr (CONV) st16(lds + row * G_ROWB + ch * 16, pack8<T>(r[2 * u], r[2 * u + 1]));
       else st16(lds + row * G_ROWB + ch * 16, r[u]);
     }
   }
@@ -540,7 +543,7 @@ __device__ __forceinline__ void tile_mma(const char* la, const char* lb, f32x16_
 #pragma unroll
       for (int ni = 0; ni < WN; ++ni) {
         if constexpr (sizeof(T) == 2) {
-          acc[mi][ni] = mfma32_bf16(a[mi], b[ni], acc[mi][ni]);
+          acc[mi][ni] = Op16<T>::mma(a[mi], b[ni], acc[mi][ni]);
         } else {
 #pragma unroll
           for (int t = 0; t < 4; ++t) acc[mi][ni] = mfma32_f32(u4f(a[mi], t), u4f(b[ni], t), acc[mi][ni]);

@@ -232,6 +232,7 @@ static int validate_psd(int n, int k, int steps, const float* X, const float* Qw
   if (!(o.gamma > 0.f) || !(o.tau >= 0.f) || !(o.tau < 1.f)) return SD_ERR_INVALID_ARG;
   if (o.tau > 0.f && (o.window < 1 || o.window > k)) return SD_ERR_INVALID_ARG;
   if (o.poly_degree != 3 && o.poly_degree != 5) return SD_ERR_INVALID_ARG;
+  if (o.precision != SD_PREC_F32 && o.precision != SD_PREC_F16) return SD_ERR_INVALID_ARG;
   if ((long long)n * n > (1ll << 34)) return SD_ERR_UNSUPPORTED;
   if (k > 0) {
     const char* q0 = reinterpret_cast<const char*>(Qwarm);
@@ -366,6 +367,13 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   float* cur = p.xa;
   float* nxt = p.xb;
   const int nc = (o.poly_degree + 1) / 2;
+  // the filter's products: float32 operands, or fp16 operands rounded while
+  // they are staged from the float32 buffers
+  const bool f16 = o.precision == SD_PREC_F16;
+  auto sym_gemm = [&](const float* A, const float* B, const GemmShape& g, const auto& epi) {
+    if (f16) launch_gemm<CfgTile128, f16_t, false, true>(A, B, g, epi, st);
+    else launch_gemm<CfgTile128, float, false, true>(A, B, g, epi, st);
+  };
   for (int t = 0; t < p.steps; ++t) {
     const float a = o.poly ? o.poly[nc * t] : 1.5f;
     const float b = o.poly ? o.poly[nc * t + 1] : -0.5f;
@@ -383,12 +391,12 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     }
     {
       ProfScope ps(SD_STAGE_NS_GRAM, st);
-      launch_gemm<CfgTile128, float, false, true>(cur, cur, g, eg, st);
+      sym_gemm(cur, cur, g, eg);
     }
     if (c != 0.f) {
       ProfScope ps(SD_STAGE_NS_POLY, st);
       EpiPoly<float> ep{p.s32, p.bm, b, c, nn, np};
-      launch_gemm<CfgTile128, float, false, true>(p.s32, p.s32, g, ep, st);
+      sym_gemm(p.s32, p.s32, g, ep);
     }
     EpiUpdate<float, float> eu{};
     eu.x = cur;
@@ -400,7 +408,7 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     eu.ldo = np;
     {
       ProfScope ps(SD_STAGE_NS_UPDATE, st);
-      launch_gemm<CfgTile128, float, false, true>(p.bm, cur, g, eu, st);
+      sym_gemm(p.bm, cur, g, eu);
     }
     float* tmp = cur;
     cur = nxt;

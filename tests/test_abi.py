@@ -55,7 +55,7 @@ int main(void) {
   F(sd_psd_opts, window) F(sd_psd_opts, poly_degree) F(sd_psd_opts, poly) F(sd_psd_opts, seed)
   F(sd_psd_opts, workspace) F(sd_psd_opts, workspace_bytes) F(sd_psd_opts, n_deflated_out)
   F(sd_psd_opts, n_positive_out) F(sd_psd_opts, theta_out) F(sd_psd_opts, ritz_out)
-  F(sd_psd_opts, status_dev)
+  F(sd_psd_opts, status_dev) F(sd_psd_opts, precision)
   return 0;
 }
 """

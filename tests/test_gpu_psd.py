@@ -17,6 +17,10 @@ from tests.gpu_util import host64, rel_fro, say
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-4
+# fp16 filter against the oracle's fp16 contract: both sides round the same
+# operands to fp16, so what differs is float32 against float64 accumulation
+# and the rare operand near a rounding tie; measured 4e-6 - 2.4e-5.
+F16_TOL = 1e-4
 
 
 def gpu_psd(case, k=None, **kw):
@@ -195,3 +199,38 @@ def test_config5_full_chain():
             assert theta < 3.0, theta
         z = workloads.psd_drift_device(z, 1e-3, call)
     say(f"config5 chain: median call {1e3 * sorted(times)[len(times) // 2]:.0f} ms")
+
+
+@pytest.mark.parametrize("n,k,degree", [(256, 8, 3), (300, 16, 3), (129, 4, 3), (180, 8, 5)])
+def test_f16_filter(n, k, degree):
+    """precision="f16": the sign filter's products take fp16 operands (the
+    paper's SDP runs), against the oracle's fp16 contract."""
+    case = workloads.small_psd(n, k=k, case_id=n + 1000)
+    table = None
+    if degree == 5:
+        table = np.array([[1.875, -1.25, 0.375]] * case.steps, dtype=np.float32)
+    out, info, q = gpu_psd(case, k, precision="f16", poly=table, poly_degree=degree)
+    want, vnext, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm[:, :k].astype(np.float64),
+                                                   steps=case.steps, gamma=case.gamma,
+                                                   subspace_iters=case.subspace_iters, mode="f16",
+                                                   table=None if table is None else table.astype(np.float64))
+    err = rel_fro(host64(out), want)
+    say(f"psd f16 n={n} k={k} degree {degree}: rel err {err:.3e}")
+    assert err < F16_TOL
+    assert int(info["n_deflated"]) == oinfo.n_deflated
+    assert int(info["n_positive"]) == oinfo.n_positive
+    o = out.cpu().numpy()
+    assert np.array_equal(o, o.T)
+
+
+@pytest.mark.slow
+def test_config4_f16():
+    case = workloads.config4()
+    out, info, _ = gpu_psd(case, precision="f16")
+    want, _, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm.astype(np.float64),
+                                               steps=case.steps, gamma=case.gamma,
+                                               subspace_iters=case.subspace_iters, mode="f16")
+    err = rel_fro(host64(out), want)
+    say(f"config4 f16: rel err {err:.3e}")
+    assert err < F16_TOL
+    assert int(info["n_deflated"]) == oinfo.n_deflated
