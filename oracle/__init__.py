@@ -20,9 +20,11 @@ Modules
   psd        Lanczos scale estimate (App. E.1), the deflated PSD projection
              (Alg. 2), the undeflated baseline (eq:baseline_projection) and the
              exact projection (eq:psd_sign).
+  admm       Three-block ADMM for SDPs with diagonal constraints (the max-cut
+             relaxation; eq:admm_iter) and its KKT residual (eq:admm_eta).
 
 Pins: every function is checked in tests/test_oracle_*.py against values the
 paper prints, closed forms, invariants or brute force; none is "parity
 unpinned".
 """
-from . import filters, linalg, muon, precision, psd, rng  # noqa: F401
+from . import admm, filters, linalg, muon, precision, psd, rng  # noqa: F401

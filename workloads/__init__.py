@@ -356,3 +356,35 @@ def psd_drift_device(z, rel: float, call: int, case_id: int = 5):
     out = z + e
     return (torch.triu(out) + torch.triu(out, 1).T).contiguous()
 
+
+# ----------------------------------------------------------------- ADMM -----
+@dataclass
+class MaxCutCase:
+    name: str
+    w: np.ndarray            # symmetric 0/1 weights, zero diagonal (float64)
+    c: np.ndarray            # cost -L / 4 of the relaxation min <C, X>, diag(X) = 1 (float32)
+    b: np.ndarray            # ones (float32)
+    basis0: np.ndarray       # float32 [n, K]: orthonormalized Gaussian start of the tracked basis
+    k: int                   # K = ceil(0.05 n) tracked columns (Sec. 3.3: w' = 0.05)
+    window: int              # r = ceil(0.025 n) (w = 0.025)
+
+
+def planted_maxcut(n: int, case_id: int = 0, p_in: float = 0.01, p_out: float = 0.15) -> MaxCutCase:
+    """Max-cut relaxation of a random graph with a planted bisection (edges
+    across the two halves with probability p_out, inside with p_in): a
+    stand-in for the Gset max-cut instances of the paper's SDP runs (Sec. 3.3),
+    whose ADMM iterates have a dominant head over a bulk."""
+    rng = rng_for(7, case_id, n)
+    lab = np.arange(n) % 2
+    prob = np.where(lab[:, None] == lab[None, :], p_in, p_out)
+    a = np.triu((rng.uniform(size=(n, n)) < prob).astype(np.float64), 1)
+    w = a + a.T
+    lap = np.diag(w.sum(axis=1)) - w
+    c = (-0.25 * lap).astype(np.float32)
+    k = math.ceil(0.05 * n)
+    g = rng.standard_normal((n, k))
+    q, r = np.linalg.qr(g)
+    basis0 = (q * np.sign(np.diag(r))).astype(np.float32)
+    return MaxCutCase(f"maxcut_planted_{n}", w, c, np.ones(n, dtype=np.float32), basis0, k,
+                      math.ceil(0.025 * n))
+
