@@ -47,7 +47,7 @@ def test_projector_schedule():
     p = proj(z)                                    # then Alg. 2 with the tracked basis
     want, vnext, info = psd.psd_project_deflated(z, v, steps=10, gamma=1.1, tau=0.1, window=case.window)
     np.testing.assert_array_equal(p, want)
-    np.testing.assert_array_equal(proj.basis, vnext)
+    np.testing.assert_allclose(proj.basis, vnext, rtol=0, atol=1e-12)   # BLAS rounding may differ
     assert proj.n_deflated[-1] == info.n_deflated
 
 
