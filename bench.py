@@ -187,6 +187,35 @@ def other_workload(args) -> int:
                "config": {"workload": args.workload, "groups": desc,
                           "launch": "one call per group" if args.sequential else "sd_msign_groups",
                           "k": [c.k for c in cases], "filter_steps": [c.steps for c in cases]}}
+    elif args.workload == "admm":
+        # ADMM on a max-cut relaxation of the size of the paper's n = 5000
+        # instances (planted-bisection random graph), tracked basis K = 64
+        # (the widest Rayleigh-Ritz block this build solves), r = 32, tau = 0.1;
+        # one step = 10 iterations with the gate open, continuing the state.
+        n, k, r, chunk, steps = 5000, 64, 32, 10, 10
+        case = workloads.planted_maxcut(n, case_id=0)
+        C = torch.from_numpy(case.c).to(dev)
+        bvec = torch.from_numpy(case.b).to(dev)
+        g = np.random.default_rng(11).standard_normal((n, k))
+        q = torch.from_numpy(np.linalg.qr(g)[0].astype(np.float32)).to(dev)
+        X, S, y = torch.zeros_like(C), torch.zeros_like(C), torch.zeros(n, dtype=torch.float32, device=dev)
+        last = {}
+
+        def call():
+            _, _, _, eta, ndef = sd.admm_diag(C, bvec, chunk, k, q, X=X, S=S, y=y, steps=steps, warmup=0,
+                                              tau=0.1, window=r, precision=args.precision)
+            last.update(eta=eta, ndef=ndef)
+
+        ms = _timed(call, args.steps, args.warmup)
+        flops = chunk * (2.0 * n ** 3 * steps + 2.0 * n ** 3)
+        peak = 157.3 if args.precision == "f32" else MFMA_BF16_PEAK_TFLOPS
+        res = {"metric": f"ADMM iterations/s (max-cut SDP, n = {n}, K = {k}, {args.precision} filter products)",
+               "value": chunk * 1e3 / ms, "unit": "iterations/s", "ms_per_step": ms,
+               "tflops": flops / (ms / 1e3) / 1e12, "mfma_frac": flops / (ms / 1e3) / 1e12 / peak,
+               "steps": args.steps, "warmup": args.warmup, "dtype": args.precision, "data": "synthetic",
+               "config": {"workload": "admm", "n": n, "k": k, "window": r, "tau": 0.1, "filter_steps": steps,
+                          "iterations_per_step": chunk, "final_eta": float(last["eta"][-1]),
+                          "final_n_deflated": int(last["ndef"][-1])}}
     else:
         if args.workload == "c4":
             case = workloads.config4()
@@ -234,11 +263,11 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 256 MiB device copy before timing (counter calibration)")
     ap.add_argument("--workload", default="headline",
-                    choices=["headline", "c2-step", "c3", "paper-step", "c4", "c5"],
+                    choices=["headline", "c2-step", "c3", "paper-step", "c4", "c5", "admm"],
                     help="headline: the benchmark line; the others time further configurations "
                          "(one JSON line each, no roofline or CPU baseline)")
     ap.add_argument("--precision", default="f32", choices=["f32", "f16"],
-                    help="c4 / c5: arithmetic of the sign filter's products")
+                    help="c4 / c5 / admm: arithmetic of the sign filter's products")
     ap.add_argument("--sequential", action="store_true",
                     help="c2-step / paper-step: one call per group on one stream instead of sd_msign_groups")
     args = ap.parse_args()

@@ -220,6 +220,29 @@ int sd_psd_project_deflated_ex(int n, int k, int steps, const float* X, float* Q
                                const sd_psd_opts* opts, hipStream_t stream);
 size_t sd_psd_workspace_bytes(int n, int k, const sd_psd_opts* opts);
 
+/* ------------------------------------------------------------------ ADMM --
+ * Three-block ADMM (App. E.1, eq:admm_iter) for the standard-form SDP pair
+ * with diagonal constraints, min <C, X> s.t. diag(X) = b, X PSD (the max-cut
+ * relaxation; A X = diag(X), A* y = Diag(y), A A* = I, so the y-update is
+ * elementwise), penalty sigma > 0, for `iters` iterations:
+ *     y = b / sigma - diag(X / sigma + S - C),   Z = C - Diag(y) - X / sigma,
+ *     S = projection of Z,                       X = X + sigma (S + Diag(y) - C).
+ * The projection is sd_psd_project_deflated_ex with `opts` (filter steps,
+ * gamma, gate tau / window, precision, ...) on the tracked basis Qwarm
+ * [n, k] (in/out: one block step and CholQR per iteration, Alg. 2), with the
+ * gate held closed for the first `warmup` iterations while the basis settles
+ * (Sec. 3.3); k = 0 projects with the undeflated baseline.
+ * C, b: device [n, n] (symmetric) and [n]. X, S [n, n] and y [n]: device,
+ * in/out (the iteration continues from them; zeros start it afresh).
+ * eta_out: optional device float[iters], the eigenvalue-free KKT residual
+ * after each iteration (the first three terms of eq:admm_eta). ndef_out:
+ * optional device int[iters], the deflated count of each projection.
+ * Scratch: opts->workspace of sd_admm_workspace_bytes(), or the pool. */
+int sd_admm_diag(int n, int iters, int steps, float sigma, const float* C, const float* b, float* X, float* S,
+                 float* y, int k, float* Qwarm, int warmup, const sd_psd_opts* opts, float* eta_out, int* ndef_out,
+                 hipStream_t stream);
+size_t sd_admm_workspace_bytes(int n, int k, int steps, const sd_psd_opts* opts);
+
 /* ---------------------------------------------------------- stage timing --
  * Benchmark instrumentation (tracing). While a stage's bit (1 << stage) is set
  * in the mask, the library brackets every launch of that stage with a pair of

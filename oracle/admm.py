@@ -54,6 +54,7 @@ class DeflatedProjector:
     mode: str = "exact"
     calls: int = 0
     n_deflated: list = field(default_factory=list)
+    ritz: list = field(default_factory=list)
 
     def __call__(self, z: np.ndarray) -> np.ndarray:
         if self.basis is None:
@@ -64,6 +65,7 @@ class DeflatedProjector:
             p, self.basis, info = psd_project_deflated(z, self.basis, steps=self.steps, gamma=self.gamma, tau=tau,
                                                        window=self.window, mode=self.mode)
             self.n_deflated.append(info.n_deflated)
+            self.ritz.append(info.ritz)
         self.calls += 1
         return p
 

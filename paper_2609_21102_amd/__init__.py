@@ -4,6 +4,7 @@ MI355X). Argument marshalling only: every step runs in the HIP library.
     msign(x, k, steps, coeffs=None, ...)        -> sd_msign_deflated_ex
     msign_groups([{x, k, steps, ...}, ...])      -> sd_msign_groups
     psd_project(X, k, steps, qwarm=None, ...)    -> sd_psd_project_deflated_ex
+    admm_diag(C, b, iters, k, qwarm, ...)        -> sd_admm_diag
 
 Tensors are torch CUDA (ROCm) tensors; torch provides device memory and the
 current stream. The library must be built (paper_2609_21102_amd/build.py);
@@ -104,6 +105,9 @@ def _declare(lib):
         "sd_psd_project_deflated": (i, [i, i, i, vp, vp, vp, vp]),
         "sd_psd_project_deflated_ex": (i, [i, i, i, vp, vp, vp, ctypes.POINTER(PsdOpts), vp]),
         "sd_psd_workspace_bytes": (sz, [i, i, ctypes.POINTER(PsdOpts)]),
+        "sd_admm_diag": (i, [i, i, i, ctypes.c_float, vp, vp, vp, vp, vp, i, vp, i, ctypes.POINTER(PsdOpts), vp, vp,
+                             vp]),
+        "sd_admm_workspace_bytes": (sz, [i, i, i, ctypes.POINTER(PsdOpts)]),
         "sd_psd_opts_default": (None, [ctypes.POINTER(PsdOpts)]),
         "sd_sketch": (i, [i, i, i, ctypes.c_uint64, vp, vp]),
         "sd_sketch_host": (i, [i, i, i, ctypes.c_uint64, vp]),
@@ -338,6 +342,29 @@ def psd_project(X, k: int = 0, steps: int = 10, qwarm=None, *, subspace_iters: i
         res["ritz"] = res["ritz"][:k]
         return out, res
     return out
+
+
+def admm_diag(C, b, iters: int, k: int = 0, qwarm=None, *, X=None, S=None, y=None, steps: int = 10,
+              sigma: float = 1.0, warmup: int = 100, tau: float = 0.1, window: int = 1, gamma: float = 1.1,
+              precision: str = "f32", seed: int = 0, stream=None):
+    """`iters` ADMM iterations (sd_admm_diag) for min <C, X> s.t. diag(X) = b,
+    X PSD, continuing from X, S, y (zeros when None; updated in place).
+    qwarm [n, k] is the tracked basis (updated in place). Returns
+    (X, S, y, eta [iters], n_deflated [iters]) as device tensors."""
+    import torch
+    n = C.shape[0]
+    dev = C.device
+    X = torch.zeros_like(C) if X is None else X
+    S = torch.zeros_like(C) if S is None else S
+    y = torch.zeros(n, dtype=torch.float32, device=dev) if y is None else y
+    eta = torch.empty(max(iters, 1), dtype=torch.float32, device=dev)
+    ndef = torch.empty(max(iters, 1), dtype=torch.int32, device=dev)
+    o = psd_opts(gamma=gamma, tau=tau, window=window, precision=SD_PREC[precision], seed=seed)
+    rc = lib().sd_admm_diag(n, iters, steps, sigma, _ptr(C), _ptr(b), _ptr(X), _ptr(S), _ptr(y), k,
+                            _ptr(qwarm) if k > 0 else None, warmup, ctypes.byref(o), _ptr(eta), _ptr(ndef),
+                            _stream(stream))
+    _check(rc, "sd_admm_diag")
+    return X, S, y, eta[:iters], ndef[:iters]
 
 
 STAGES = {"ns_gram": 0, "ns_poly": 1, "ns_update": 2, "sketch": 3, "cholqr": 4, "small": 5,

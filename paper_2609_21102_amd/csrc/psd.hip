@@ -431,6 +431,121 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   return hip_status();
 }
 
+// ------------------------------------------------------------------ ADMM --
+// Three-block ADMM (eq:admm_iter) for SDPs with diagonal constraints,
+// A X = diag(X): A* y = Diag(y) and A A* = I, so the y-update is elementwise.
+// Matrices are n x n, row-major, contiguous.
+constexpr int ADMM_BLOCKS = 1024;   // fixed grid of the reducing kernels (fixed summation order)
+
+// y_i = b_i / sigma - (X_ii / sigma + S_ii - C_ii)
+__global__ __launch_bounds__(256) void admm_y_kernel(const float* __restrict__ X, const float* __restrict__ S,
+                                                     const float* __restrict__ C, const float* __restrict__ b, int n,
+                                                     float inv_sigma, float* __restrict__ y) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const long long d = (long long)i * n + i;
+  y[i] = b[i] * inv_sigma - (X[d] * inv_sigma + S[d] - C[d]);
+}
+
+// Z = C - Diag(y) - X / sigma
+__global__ __launch_bounds__(256) void admm_z_kernel(const float* __restrict__ C, const float* __restrict__ X,
+                                                     const float* __restrict__ y, int n, float inv_sigma,
+                                                     float* __restrict__ Z) {
+  const long long nn = (long long)n * n;
+  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < nn; e += (long long)gridDim.x * blockDim.x) {
+    const int i = (int)(e / n), j = (int)(e - (long long)i * n);
+    Z[e] = C[e] - (i == j ? y[i] : 0.f) - X[e] * inv_sigma;
+  }
+}
+
+// X <- X + sigma (S + Diag(y) - C), and per-block float64 partial sums of
+// ||Diag(y) + S - C||_F^2, <C, X_new> and ||diag(X_new) - b||^2.
+__global__ __launch_bounds__(256) void admm_x_kernel(float* __restrict__ X, const float* __restrict__ S,
+                                                     const float* __restrict__ C, const float* __restrict__ y,
+                                                     const float* __restrict__ b, int n, float sigma,
+                                                     double* __restrict__ part) {
+  __shared__ double red[4];
+  const long long nn = (long long)n * n;
+  double dual = 0.0, cx = 0.0, prim = 0.0;
+  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < nn; e += (long long)gridDim.x * blockDim.x) {
+    const int i = (int)(e / n), j = (int)(e - (long long)i * n);
+    const float r = S[e] + (i == j ? y[i] : 0.f) - C[e];
+    const float xn = X[e] + sigma * r;
+    X[e] = xn;
+    dual += (double)r * r;
+    cx += (double)C[e] * xn;
+    if (i == j) {
+      const double pr = (double)xn - b[i];
+      prim += pr * pr;
+    }
+  }
+  dual = block_sum(dual, red);
+  cx = block_sum(cx, red);
+  prim = block_sum(prim, red);
+  if (threadIdx.x == 0) {
+    part[3 * blockIdx.x] = dual;
+    part[3 * blockIdx.x + 1] = cx;
+    part[3 * blockIdx.x + 2] = prim;
+  }
+}
+
+// ||C||_F^2 partial sums (once per call)
+__global__ __launch_bounds__(256) void admm_cnorm_kernel(const float* __restrict__ C, int n, double* __restrict__ part) {
+  __shared__ double red[4];
+  const long long nn = (long long)n * n;
+  double acc = 0.0;
+  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < nn; e += (long long)gridDim.x * blockDim.x)
+    acc += (double)C[e] * C[e];
+  acc = block_sum(acc, red);
+  if (threadIdx.x == 0) part[blockIdx.x] = acc;
+}
+
+// Scratch of an ADMM call: Z, the partial sums, then the projection's own
+// workspace (planned for Z, which the arena aligns to 256 bytes).
+static void admm_plan(PsdPlan& p, Arena& ar, int n, int k, int steps, const sd_psd_opts& o, float** Z = nullptr,
+                      double** part = nullptr, double** cpart = nullptr) {
+  float* z = ar.take<float>((size_t)n * n);
+  double* pa = ar.take<double>(3 * ADMM_BLOCKS);
+  double* cp = ar.take<double>(ADMM_BLOCKS);
+  // sizing (no base) plans with an aligned stand-in address: same copy-in decision
+  make_psd_plan(p, n, k, steps, ar.base ? z : reinterpret_cast<const float*>(uintptr_t(256)), o);
+  plan_psd(p, ar);
+  if (Z) *Z = z;
+  if (part) *part = pa;
+  if (cpart) *cpart = cp;
+}
+
+// eta: the eigenvalue-free terms of eq:admm_eta from the partial sums. One
+// work-group; the partials are added in block order.
+__global__ __launch_bounds__(256) void admm_eta_kernel(const double* __restrict__ part, const double* __restrict__ cpart,
+                                                       const float* __restrict__ b, const float* __restrict__ y, int n,
+                                                       float* __restrict__ eta) {
+  __shared__ double red[4];
+  __shared__ double sums[6];
+  const int tid = threadIdx.x;
+  double bb = 0.0, by = 0.0;
+  for (int i = tid; i < n; i += 256) {
+    bb += (double)b[i] * b[i];
+    by += (double)b[i] * y[i];
+  }
+  bb = block_sum(bb, red);
+  by = block_sum(by, red);
+  if (tid == 0) {
+    double dual = 0.0, cx = 0.0, prim = 0.0, cc = 0.0;
+    for (int k = 0; k < ADMM_BLOCKS; ++k) {
+      dual += part[3 * k];
+      cx += part[3 * k + 1];
+      prim += part[3 * k + 2];
+      cc += cpart[k];
+    }
+    const double nb = sqrt(bb), nc = sqrt(cc);
+    const double e1 = sqrt(prim) / (1.0 + nb);
+    const double e2 = sqrt(dual) / (1.0 + nc);
+    const double e3 = fabs(cx - by) / (1.0 + fabs(cx) + fabs(by));
+    *eta = (float)fmax(e1, fmax(e2, e3));
+  }
+}
+
 }  // namespace sd
 
 using namespace sd;
@@ -521,6 +636,62 @@ int sd_profile_read(int stage, double* total_ms, long long* launches) {
   if (total_ms) *total_ms = p.total_ms[stage];
   if (launches) *launches = p.launches[stage];
   return SD_OK;
+}
+
+size_t sd_admm_workspace_bytes(int n, int k, int steps, const sd_psd_opts* opts) {
+  sd_psd_opts o;
+  sd_psd_opts_default(&o);
+  if (opts) o = *opts;
+  if (n < 1 || k < 0 || k >= n || k > SM_MAX || steps < 0) return 0;
+  PsdPlan p{};
+  Arena ar;
+  admm_plan(p, ar, n, k, steps, o);
+  return ar.off + 256;
+}
+
+int sd_admm_diag(int n, int iters, int steps, float sigma, const float* C, const float* b, float* X, float* S,
+                 float* y, int k, float* Qwarm, int warmup, const sd_psd_opts* opts, float* eta_out, int* ndef_out,
+                 hipStream_t stream) {
+  sd_psd_opts o;
+  sd_psd_opts_default(&o);
+  if (opts) o = *opts;
+  if (iters < 0 || warmup < 0 || !(sigma > 0.f) || !C || !b || !X || !S || !y) return SD_ERR_INVALID_ARG;
+  // the projection reads Z (library scratch) and writes S
+  int rc = validate_psd(n, k, steps, C, Qwarm, S, o);
+  if (rc != SD_OK) return rc;
+  if (iters == 0) return SD_OK;
+  const long long nn = (long long)n * n;
+  PsdPlan p{};
+  Arena sizing;
+  admm_plan(p, sizing, n, k, steps, o);
+  Scratch scratch;
+  rc = scratch.acquire(o.workspace, o.workspace_bytes, sizing.off + 256, stream);
+  if (rc != SD_OK) return rc;
+  Arena ar;
+  ar.base = reinterpret_cast<char*>(scratch.ptr);
+  float* Z;
+  double *part, *cpart;
+  admm_plan(p, ar, n, k, steps, o, &Z, &part, &cpart);
+  const float inv_sigma = 1.f / sigma;
+  hipLaunchKernelGGL(admm_cnorm_kernel, dim3(ADMM_BLOCKS), dim3(256), 0, stream, C, n, cpart);
+  for (int it = 0; it < iters && rc == SD_OK; ++it) {
+    hipLaunchKernelGGL(admm_y_kernel, grid1(n, 256), dim3(256), 0, stream, X, S, C, b, n, inv_sigma, y);
+    hipLaunchKernelGGL(admm_z_kernel, dim3(ADMM_BLOCKS), dim3(256), 0, stream, C, X, y, n, inv_sigma, Z);
+    sd_psd_opts oi = o;
+    if (it < warmup) oi.tau = 1e-30f;   // gate held closed: s_r < tau s_1 cannot hold
+    oi.n_deflated_out = ndef_out ? ndef_out + it : nullptr;
+    oi.n_positive_out = nullptr;
+    oi.theta_out = nullptr;
+    oi.ritz_out = nullptr;
+    if (k > 0 && it < warmup && oi.window < 1) oi.window = 1;
+    rc = run_psd(p, Z, Qwarm, S, oi, stream);
+    hipLaunchKernelGGL(admm_x_kernel, dim3(ADMM_BLOCKS), dim3(256), 0, stream, X, S, C, y, b, n, sigma, part);
+    if (eta_out)
+      hipLaunchKernelGGL(admm_eta_kernel, dim3(1), dim3(256), 0, stream, part, cpart, b, y, n, eta_out + it);
+  }
+  scratch.release();
+  if (rc != SD_OK) return rc;
+  return hip_status();
 }
 
 void sd_profile_reset(void) {
