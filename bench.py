@@ -227,7 +227,8 @@ def other_workload(args) -> int:
             n, k, steps, sub = 16384, 32, 10, 1
         q = q0.clone()
         out = torch.empty_like(z)
-        ws = torch.empty(sd.psd_workspace_bytes(n, k), dtype=torch.uint8, device=dev)
+        ws = torch.empty(sd.psd_workspace_bytes(n, k, precision=sd.SD_PREC[args.precision]), dtype=torch.uint8,
+                         device=dev)
 
         def call():
             q.copy_(q0)   # every timed call starts from the same warm basis

@@ -112,6 +112,10 @@ template <> struct Cvt<bf16_t> {
   __device__ __forceinline__ static float to_f(bf16_t v) { return bf2f(v); }
   __device__ __forceinline__ static bf16_t from_f(float v) { return f2bf(v); }
 };
+template <> struct Cvt<f16_t> {
+  __device__ __forceinline__ static float to_f(f16_t v) { return (float)__builtin_bit_cast(_Float16, v.bits); }
+  __device__ __forceinline__ static f16_t from_f(float v) { return f16_t{(uint16_t)(pack_h2(v, 0.f) & 0xffffu)}; }
+};
 
 // ---------------------------------------------------------------- MFMA ----
 // 32x32 output block, accumulator layout (CDNA3/CDNA4): lane l holds column

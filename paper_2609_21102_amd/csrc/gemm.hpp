@@ -90,9 +90,10 @@ __device__ __forceinline__ void emit4(T* p, int ld, int r0, int c, const float v
 }
 
 // ------------------------------------------------------- epilogues --------
-// Gram: out32 = scale32 * C (fp32, optional), out16 = bf16(scale16 * C)
-// (optional).
-struct EpiGram {
+// Gram: out32 = scale32 * C (fp32, optional), out16 = T16(scale16 * C)
+// (optional; bf16 or fp16, rounded to nearest even).
+template <typename T16>
+struct EpiGramT {
   static constexpr bool PRE = false;
   static constexpr bool ROWWISE = true;
   static constexpr bool HI_FROM_B = false;
@@ -115,10 +116,11 @@ struct EpiGram {
   __device__ void store8(int b, int r, int c0, const float (&v)[8]) const {
     if (out16)
       st16_nt(out16 + b * stride + (long long)r * ld + c0,
-              u32x4_t{pack_bf2(v[0], v[1]), pack_bf2(v[2], v[3]), pack_bf2(v[4], v[5]), pack_bf2(v[6], v[7])});
+              u32x4_t{Op16<T16>::pack2(v[0], v[1]), Op16<T16>::pack2(v[2], v[3]), Op16<T16>::pack2(v[4], v[5]),
+                      Op16<T16>::pack2(v[6], v[7])});
   }
   float* out32;
-  bf16_t* out16;
+  T16* out16;
   float scale32, scale16;
   long long stride;
   int ld;
@@ -133,6 +135,7 @@ struct EpiGram {
     }
   }
 };
+using EpiGram = EpiGramT<bf16_t>;
 
 // Polynomial in the Gram: out = bc * A32 + cc * C.
 template <typename TO>
@@ -166,7 +169,8 @@ struct EpiPoly {
   __device__ void store8(int b, int r, int c0, const float (&w)[8]) const {
     const long long o = b * stride + (long long)r * ld + c0;
     if constexpr (sizeof(TO) == 2) {
-      st16_nt(out + o, u32x4_t{pack_bf2(w[0], w[1]), pack_bf2(w[2], w[3]), pack_bf2(w[4], w[5]), pack_bf2(w[6], w[7])});
+      st16_nt(out + o, u32x4_t{Op16<TO>::pack2(w[0], w[1]), Op16<TO>::pack2(w[2], w[3]), Op16<TO>::pack2(w[4], w[5]),
+                               Op16<TO>::pack2(w[6], w[7])});
     } else {
       *reinterpret_cast<f32x4_t*>(out + o) = f32x4_t{w[0], w[1], w[2], w[3]};
       *reinterpret_cast<f32x4_t*>(out + o + 4) = f32x4_t{w[4], w[5], w[6], w[7]};
@@ -222,6 +226,45 @@ struct EpiUpdate {
         if (r0 + j < rows_valid) ob[(long long)c * ldo + r0 + j] = Cvt<TO>::from_f(v[j]);
     }
   }
+};
+
+// Iterate update of a symmetric filter (X and the polynomial in X commute,
+// so X_next = ac X + B X is symmetric and computed on upper-triangle tiles):
+// row-wise, out = ac * x + C in fp32 and its T16 copy (the next products'
+// operand). The x values are loaded before the main loop (pre8).
+template <typename T16>
+struct EpiUpdateSym {
+  static constexpr bool PRE = true;
+  static constexpr bool ROWWISE = true;
+  static constexpr bool HI_FROM_B = false;
+  const float* x;
+  float ac;
+  float* out;
+  T16* out16;
+  long long stride;
+  int ld;
+  __device__ void pre8(int b, int r, int c0, u32x4_t& h, u32x4_t& l) const {
+    const long long o = b * stride + (long long)r * ld + c0;
+    h = ld16(x + o);
+    l = ld16(x + o + 4);
+  }
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t& h, const u32x4_t& l,
+                         float (&w)[8]) const {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      w[q] = ac * __uint_as_float(h[q]) + v[q];
+      w[q + 4] = ac * __uint_as_float(l[q]) + v[q + 4];
+    }
+    store8(b, r, c0, w);
+  }
+  __device__ void store8(int b, int r, int c0, const float (&w)[8]) const {
+    const long long o = b * stride + (long long)r * ld + c0;
+    st16_nt(out + o, __builtin_bit_cast(u32x4_t, f32x4_t{w[0], w[1], w[2], w[3]}));
+    st16_nt(out + o + 4, __builtin_bit_cast(u32x4_t, f32x4_t{w[4], w[5], w[6], w[7]}));
+    st16_nt(out16 + o, u32x4_t{Op16<T16>::pack2(w[0], w[1]), Op16<T16>::pack2(w[2], w[3]),
+                               Op16<T16>::pack2(w[4], w[5]), Op16<T16>::pack2(w[6], w[7])});
+  }
+  __device__ void operator()(int, int, int, float*, int) const {}
 };
 
 // Iterate update with the bf16 iterate stored as hi = bf16(X) plus an e4m3
@@ -711,7 +754,7 @@ __device__ __forceinline__ u32x2_t lds_read_tr16(const char* p) {
 // m0 carries the LDS address; nothing else in these kernels uses m0.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void lds_dma16(const bf16_t* g, char* base) {
+__device__ __forceinline__ void lds_dma16(const void* g, char* base) {
   const unsigned off = (unsigned)(size_t)((__attribute__((address_space(3))) char*)base);
   asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
                :
@@ -760,7 +803,7 @@ __device__ __forceinline__ void load_frags_dma(const char* la, const char* lb, i
   }
 }
 
-template <int WM, int WN, int BN, int BK, bool B_NN>
+template <typename T, int WM, int WN, int BN, int BK, bool B_NN>
 __device__ __forceinline__ void tile_mma_dma(const char* la, const char* lb, f32x16_t (&acc)[WM][WN], int wm,
                                              int wn, int lane) {
   constexpr int G = BK / 16;
@@ -773,7 +816,7 @@ __device__ __forceinline__ void tile_mma_dma(const char* la, const char* lb, f32
 #pragma unroll
     for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < WN; ++ni) acc[mi][ni] = mfma32_bf16(a[g & 1][mi], b[g & 1][ni], acc[mi][ni]);
+      for (int ni = 0; ni < WN; ++ni) acc[mi][ni] = Op16<T>::mma(a[g & 1][mi], b[g & 1][ni], acc[mi][ni]);
   }
 }
 
@@ -788,9 +831,10 @@ struct DmaLds {
   static constexpr int BYTES = RING > CT ? RING : CT;
 };
 
-// One output tile (linear tile id lid over the batch).
-template <typename Cfg, bool B_NN, bool SYM, typename Epi>
-__device__ __forceinline__ void gemm_dma_tile(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B,
+// One output tile (linear tile id lid over the batch). T: the 16-bit operand
+// type (bf16 or fp16; the loads move bytes, only the MFMA differs).
+template <typename Cfg, typename T, bool B_NN, bool SYM, typename Epi>
+__device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* __restrict__ B,
                                               const GemmShape& sh, const Epi& epi, char* lds, int lid) {
   constexpr int BK = Cfg::BK, RB = 2 * BK, CH = BK / 8, RPL = 1024 / RB;   // rows per 1 KB load
   constexpr int BM = Cfg::BM, BN = Cfg::BN, WM = Cfg::WM, WN = Cfg::WN, S = Cfg::STAGES;
@@ -852,7 +896,7 @@ __device__ __forceinline__ void gemm_dma_tile(const bf16_t* __restrict__ A, cons
   }
 
   // per-lane global sources (at k = 0) and wave-uniform LDS offsets
-  const bf16_t* ga[LA];
+  const T* ga[LA];
   int la_off[LA];
 #pragma unroll
   for (int u = 0; u < LA; ++u) {
@@ -862,7 +906,7 @@ __device__ __forceinline__ void gemm_dma_tile(const bf16_t* __restrict__ A, cons
     ga[u] = A + b * sh.sa + (long long)(m0 + row) * sh.lda + 8 * ch;
     la_off[u] = 1024 * qi;
   }
-  const bf16_t* gb[LB];
+  const T* gb[LB];
   int lb_off[LB];
 #pragma unroll
   for (int u = 0; u < LB; ++u) {
@@ -937,7 +981,7 @@ __device__ __forceinline__ void gemm_dma_tile(const bf16_t* __restrict__ A, cons
         }
       }
     }
-    tile_mma_dma<WM, WN, BN, BK, B_NN>(base, base + A_BYTES, acc, wm, wn, lane);
+    tile_mma_dma<T, WM, WN, BN, BK, B_NN>(base, base + A_BYTES, acc, wm, wn, lane);
   }
 
   if constexpr (ROWWISE) {
@@ -1019,23 +1063,24 @@ __device__ __forceinline__ void gemm_dma_tile(const bf16_t* __restrict__ A, cons
 // tiles, so work-groups that share operand panels share an L2). A variant
 // that walked several tiles per work-group measured no faster and needed
 // about 20-100 more VGPRs.
-template <typename Cfg, bool B_NN, bool SYM, typename Epi>
+template <typename Cfg, bool B_NN, bool SYM, typename Epi, typename T>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void
-gemm_dma_kernel(const bf16_t* __restrict__ A, const bf16_t* __restrict__ B, GemmShape sh, Epi epi) {
+gemm_dma_kernel(const T* __restrict__ A, const T* __restrict__ B, GemmShape sh, Epi epi) {
   __shared__ __attribute__((aligned(1024))) char lds[DmaLds<Cfg, Epi::ROWWISE>::BYTES];
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const int total = (SYM ? tm * (tm + 1) / 2 : tm * tn) * sh.batch;
-  gemm_dma_tile<Cfg, B_NN, SYM, Epi>(A, B, sh, epi, lds, xcd_remap(blockIdx.x, total));
+  gemm_dma_tile<Cfg, T, B_NN, SYM, Epi>(A, B, sh, epi, lds, xcd_remap(blockIdx.x, total));
 }
 
-template <typename Cfg, bool B_NN, bool SYM, typename Epi>
-void launch_gemm_dma(const bf16_t* A, const bf16_t* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
+template <typename Cfg, bool B_NN, bool SYM, typename Epi, typename T>
+void launch_gemm_dma(const T* A, const T* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
+  static_assert(sizeof(T) == 2, "16-bit operands");
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;
   const long long blocks = per * sh.batch;
   if (blocks <= 0) return;
-  hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi>), dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A, B,
-                     sh, epi);
+  hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi, T>), dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A,
+                     B, sh, epi);
 }
 
 // Host launcher (errors surface through hipGetLastError at the end of a call).

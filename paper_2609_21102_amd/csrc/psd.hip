@@ -180,10 +180,23 @@ __global__ __launch_bounds__(1024) void lanczos_theta_kernel(const float* bv, co
   }
 }
 
+// out = fp16(x), eight elements per thread (n8 groups of eight)
+__global__ void to_f16_kernel(const float* __restrict__ x, long long n8, f16_t* __restrict__ out) {
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < n8; i += (long long)gridDim.x * blockDim.x) {
+    const u32x4_t lo = ld16(x + 8 * i), hi = ld16(x + 8 * i + 4);
+    const u32x4_t h = {pack_h2(__uint_as_float(lo[0]), __uint_as_float(lo[1])),
+                       pack_h2(__uint_as_float(lo[2]), __uint_as_float(lo[3])),
+                       pack_h2(__uint_as_float(hi[0]), __uint_as_float(hi[1])),
+                       pack_h2(__uint_as_float(hi[2]), __uint_as_float(hi[3]))};
+    *reinterpret_cast<u32x4_t*>(out + 8 * i) = h;
+  }
+}
+
 struct PsdPlan {
   int n, k, steps, n_pad, K, lz;
-  bool copy_in, quintic;
+  bool copy_in, quintic, f16;
   float *zp, *r, *xa, *xb, *s32, *bm, *c;
+  f16_t *xh0, *xh1, *bh, *ah;   // fp16 filter: operand copies of X (current, next), B and (quintic) A
   float *vt, *zt, *E, *lam, *ut, *coefR, *coefX, *coefP;
   int* ndef;
   double *part, *fac;
@@ -200,6 +213,10 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
   p.s32 = p.quintic ? ar.take<float>(nn) : nullptr;
   p.bm = ar.take<float>(nn);
   p.c = p.bm;   // the restore product reuses B's buffer after the filter
+  p.xh0 = p.f16 ? ar.take<f16_t>(nn) : nullptr;
+  p.xh1 = p.f16 ? ar.take<f16_t>(nn) : nullptr;
+  p.bh = p.f16 ? ar.take<f16_t>(nn) : nullptr;
+  p.ah = p.f16 && p.quintic ? ar.take<f16_t>(nn) : nullptr;
   const int kq = p.K > 0 ? p.K : 1;
   const int kr = round_up(kq, 32);
   p.vt = ar.take<float>((size_t)kr * p.n_pad);
@@ -254,6 +271,7 @@ static void make_psd_plan(PsdPlan& p, int n, int k, int steps, const float* X, c
   p.n_pad = round_up(n, 128);
   p.lz = o.lanczos_steps < n ? o.lanczos_steps : n;
   p.quintic = o.poly_degree == 5;
+  p.f16 = o.precision == SD_PREC_F16;
   const bool aligned = X && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
   p.copy_in = p.n != p.n_pad || !aligned;
 }
@@ -367,14 +385,59 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   float* cur = p.xa;
   float* nxt = p.xb;
   const int nc = (o.poly_degree + 1) / 2;
-  // the filter's products: float32 operands, or fp16 operands rounded while
-  // they are staged from the float32 buffers
-  const bool f16 = o.precision == SD_PREC_F16;
+  if (p.f16 && p.steps > 0) {
+    // fp16 products on the direct-to-LDS kernel: every epilogue also writes
+    // the fp16 copy of what the next product reads (X, B, A), rounded from
+    // the same fp32 value the fp32 buffers hold
+    f16_t* hc = p.xh0;
+    f16_t* hn = p.xh1;
+    const long long n8 = (long long)np * np / 8;
+    hipLaunchKernelGGL(to_f16_kernel, grid1(n8, 256), dim3(256), 0, st, cur, n8, hc);
+    for (int t = 0; t < p.steps; ++t) {
+      const float a = o.poly ? o.poly[nc * t] : 1.5f;
+      const float b = o.poly ? o.poly[nc * t + 1] : -0.5f;
+      const float c = (o.poly && nc == 3) ? o.poly[nc * t + 2] : 0.f;
+      GemmShape g{np, np, np, np, np, nn, nn, 1};
+      EpiGramT<f16_t> eg{};
+      eg.stride = nn;
+      eg.ld = np;
+      if (c != 0.f) {
+        eg.out32 = p.s32;   // A, for the b A term
+        eg.scale32 = 1.f;
+        eg.out16 = p.ah;    // A, the operand of A^2
+        eg.scale16 = 1.f;
+      } else {
+        eg.out32 = nullptr;
+        eg.out16 = p.bh;    // B = b A
+        eg.scale16 = b;
+      }
+      {
+        ProfScope ps(SD_STAGE_NS_GRAM, st);
+        launch_gemm_dma<CfgDma128, false, true>(hc, hc, g, eg, st);
+      }
+      if (c != 0.f) {
+        ProfScope ps(SD_STAGE_NS_POLY, st);
+        EpiPoly<f16_t> ep{p.s32, p.bh, b, c, nn, np};
+        launch_gemm_dma<CfgDma128, false, true>(p.ah, p.ah, g, ep, st);
+      }
+      {
+        ProfScope ps(SD_STAGE_NS_UPDATE, st);
+        // B X = B X^T: the NT form on rows of X; symmetric tiles
+        EpiUpdateSym<f16_t> eu{cur, a, nxt, hn, nn, np};
+        launch_gemm_dma<CfgDma128, false, true>(p.bh, hc, g, eu, st);
+      }
+      float* tmp = cur;
+      cur = nxt;
+      nxt = tmp;
+      f16_t* th = hc;
+      hc = hn;
+      hn = th;
+    }
+  }
   auto sym_gemm = [&](const float* A, const float* B, const GemmShape& g, const auto& epi) {
-    if (f16) launch_gemm<CfgTile128, f16_t, false, true>(A, B, g, epi, st);
-    else launch_gemm<CfgTile128, float, false, true>(A, B, g, epi, st);
+    launch_gemm<CfgTile128, float, false, true>(A, B, g, epi, st);
   };
-  for (int t = 0; t < p.steps; ++t) {
+  for (int t = 0; t < (p.f16 ? 0 : p.steps); ++t) {
     const float a = o.poly ? o.poly[nc * t] : 1.5f;
     const float b = o.poly ? o.poly[nc * t + 1] : -0.5f;
     const float c = (o.poly && nc == 3) ? o.poly[nc * t + 2] : 0.f;
