@@ -205,6 +205,7 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
         case 8: SD_HEAD(8); break;
         case 12: SD_HEAD(12); break;
         case 16: SD_HEAD(16); break;
+        case 32: SD_HEAD(32); break;
         default: SD_HEAD(0); break;
       }
 #undef SD_HEAD

@@ -292,6 +292,7 @@ static void lanczos(const PsdPlan& p, const float* R, uint64_t seed, float* thet
     case 8: hipLaunchKernelGGL(lanczos_ritz_kernel<8>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
     case 12: hipLaunchKernelGGL(lanczos_ritz_kernel<12>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
     case 16: hipLaunchKernelGGL(lanczos_ritz_kernel<16>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
+    case 32: hipLaunchKernelGGL(lanczos_ritz_kernel<32>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
     default: hipLaunchKernelGGL(lanczos_ritz_kernel<0>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
   }
   hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.v, p.t);
@@ -344,6 +345,7 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
         case 8: SD_RITZ(8); break;
         case 12: SD_RITZ(12); break;
         case 16: SD_RITZ(16); break;
+        case 32: SD_RITZ(32); break;
         default: SD_RITZ(0); break;
       }
 #undef SD_RITZ

@@ -28,6 +28,7 @@ struct SmallLds {
   double key[SM_MAX];
   int perm[SM_MAX];
   int rotated;                    // a rotation was applied in this sweep
+  int count;                      // a count broadcast from thread 0 (deflation rank)
 };
 
 // ------------------------------------------------------------- Jacobi -----
@@ -194,6 +195,11 @@ static __device__ __forceinline__ void jacobi_eig(SmallLds& s, int n, int tol_ex
 // columns of s.e; returns the number of rounds. Only the calling wave may
 // touch s meanwhile; wave_sync orders its LDS accesses (a single wave's LDS
 // operations complete in order).
+// NW > 1 (n <= 64): the same scheme on NW waves (the whole work-group, which
+// must have 64 NW threads): lane t of the group holds blocks t + 64 NW u, the
+// ring step is ordered by work-group barriers, and the "any rotation" vote is
+// taken at the first of them (__syncthreads_or); every lane applies its
+// rotations unconditionally, which is exact for a skipped pair ((1, 0)).
 __device__ __forceinline__ void wave_sync() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
 template <int NP>
@@ -217,11 +223,11 @@ __device__ __forceinline__ int jw_index(int slot, int R) {
   return k0 <= NP - 2 ? k0 + 1 : 3 * NP - 2 - k0;
 }
 
-template <int NP>
+template <int NP, int NW = 1>
 __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) {
-  constexpr int N = 2 * NP, NB = NP * NP, U = (NB + WAVE - 1) / WAVE;
-  static_assert(N <= 32, "one wave holds at most 16 x 16 blocks");
-  const int lane = threadIdx.x & (WAVE - 1);
+  constexpr int N = 2 * NP, NB = NP * NP, L = WAVE * NW, U = (NB + L - 1) / L;
+  static_assert(N <= SM_MAX && U <= 4, "at most four 2 x 2 blocks per lane");
+  const int lane = NW == 1 ? (int)(threadIdx.x & (WAVE - 1)) : (int)threadIdx.x;
   double h[U][4], e[U][4];
   double tp[U][3], tq[U][3];   // (H[T][T], H[B][B], H[T][B]) of pairs p and q
   int bp[U], bq[U];
@@ -229,7 +235,7 @@ __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) 
   double fro = 0.0;
 #pragma unroll
   for (int u = 0; u < U; ++u) {
-    const int id = lane + WAVE * u;
+    const int id = lane + L * u;
     act[u] = id < NB;
     bp[u] = act[u] ? id / NP : 0;
     bq[u] = act[u] ? id - bp[u] * NP : 0;
@@ -252,7 +258,8 @@ __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) 
     tq[u][1] = qb < n ? s.h[qb][qb] : 0.0;
     tq[u][2] = qb < n ? s.h[qt][qb] : 0.0;
   }
-  fro = wave_sum(fro);
+  if constexpr (NW == 1) fro = wave_sum(fro);
+  else fro = block_sum(fro, s.red);
   const double abs_floor = __builtin_amdgcn_ldexp(sqrt(fro), tol_exp);
   int idle = 0, R = 0;
   while (idle < N - 1 && R < 40 * (N - 1)) {
@@ -272,8 +279,8 @@ __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) 
       jacobi_rot64(cf, tf, cp[u], sp[u]);
       jacobi_rot64(cg, tg, cq[u], sq[u]);
     }
-    if (__any(rot)) {   // every pair is some active lane's p
-      idle = 0;
+    if (NW > 1 || __any(rot)) {   // every pair is some active lane's p
+      if constexpr (NW == 1) idle = 0;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         // columns of pair q: T <- c T - s B, B <- s T + c B; then the rows of pair p
@@ -290,7 +297,7 @@ __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) 
         e[u][2] = y10;
         e[u][3] = y11;
       }
-    } else {
+    } else if constexpr (NW == 1) {
       ++idle;
     }
     // ring step; each lane also picks up the diagonal blocks of its new p, q
@@ -305,7 +312,12 @@ __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) 
             s.h2[jw_slot<NP>(r1, bp[u])][b] = h[u][2 * r1 + r2];
             s.e2[2 * bp[u] + r1][b] = e[u][2 * r1 + r2];
           }
-    wave_sync();
+    if constexpr (NW == 1) {
+      wave_sync();
+    } else {
+      const bool any = __syncthreads_or(rot);
+      idle = any ? 0 : idle + 1;
+    }
 #pragma unroll
     for (int u = 0; u < U; ++u)
       if (act[u]) {
@@ -326,7 +338,8 @@ __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) 
         tq[u][1] = s.h2[qb][qb];
         tq[u][2] = s.h2[qt][qb];
       }
-    wave_sync();
+    if constexpr (NW == 1) wave_sync();
+    else __syncthreads();
     ++R;
   }
   // back to index coordinates: slot -> index after R ring steps
@@ -343,16 +356,22 @@ __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) 
           if (bp[u] == bq[u]) s.h[col][col] = h[u][3 * r2];
         }
       }
-  wave_sync();
+  if constexpr (NW == 1) wave_sync();
+  else __syncthreads();
   return R;
 }
 
-// jacobi_eig for a whole work-group: with NP > 0 (n <= 2 NP) on its first
-// wave, otherwise block-wide.
+// jacobi_eig for a whole work-group of SM_THREADS: with 0 < NP <= 16 (n <= 2 NP)
+// on its first wave, NP = 32 on all four waves, otherwise block-wide.
 template <int NP>
 __device__ __forceinline__ void jacobi_eig_any(SmallLds& s, int n, int tol_exp = -48) {
   if constexpr (NP == 0) {
     jacobi_eig(s, n, tol_exp);
+  } else if constexpr (NP > 16) {
+    static_assert(SM_THREADS == 4 * WAVE, "four waves");
+    __syncthreads();
+    jacobi_eig_wave<NP, 4>(s, n, tol_exp);
+    __syncthreads();
   } else {
     __syncthreads();
     if (threadIdx.x < WAVE) jacobi_eig_wave<NP>(s, n, tol_exp);
@@ -360,7 +379,9 @@ __device__ __forceinline__ void jacobi_eig_any(SmallLds& s, int n, int tol_exp =
   }
 }
 // Wave size class of an n x n eigenproblem (0: block-wide solver).
-__host__ __device__ inline int jacobi_class(int n) { return n <= 8 ? 4 : n <= 16 ? 8 : n <= 24 ? 12 : n <= 32 ? 16 : 0; }
+__host__ __device__ inline int jacobi_class(int n) {
+  return n <= 8 ? 4 : n <= 16 ? 8 : n <= 24 ? 12 : n <= 32 ? 16 : n <= 64 ? 32 : 0;
+}
 
 // Rank of each key under "larger key first, then smaller index": s.perm[rank]
 // = index. Keys must be set in s.key[0..n).
@@ -766,10 +787,10 @@ __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part
     }
     keff[b] = ke;
     if (keff_user) keff_user[b] = ke;
-    s.perm[SM_MAX - 1] = ke;
+    s.count = ke;
   }
   __syncthreads();
-  const int ke = s.perm[SM_MAX - 1];
+  const int ke = s.count;
   if (tid < k) {
     const double sj = s.key[tid];
     const float inv = sj > 0.0 ? (float)(1.0 / sj) : 0.f;
@@ -842,10 +863,10 @@ __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const double* part, in
     *ndef = nd;
     if (ndef_user) *ndef_user = nd;
     if (npos_user) *npos_user = np;
-    s.perm[SM_MAX - 1] = nd;
+    s.count = nd;
   }
   __syncthreads();
-  const int nd = s.perm[SM_MAX - 1];
+  const int nd = s.count;
   if (tid < K) {
     const double l = s.h[s.perm[tid]][s.perm[tid]];
     const bool on = tid < nd;

@@ -33,7 +33,7 @@ def gpu_psd(case, k=None, **kw):
     return out, info, q
 
 
-@pytest.mark.parametrize("n,k", [(100, 0), (100, 8), (256, 8), (300, 16), (129, 4)])
+@pytest.mark.parametrize("n,k", [(100, 0), (100, 8), (256, 8), (300, 16), (129, 4), (200, 40), (300, 64)])
 def test_small(n, k):
     case = workloads.small_psd(n, k=max(k, 1), case_id=n)
     say(f"psd n={n} k={k}")
