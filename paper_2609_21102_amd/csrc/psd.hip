@@ -75,13 +75,16 @@ __global__ __launch_bounds__(1024) void lanczos_init_kernel(float* Q, int n, int
 
 // One Lanczos step on B = R^2 with w = B q_j already computed:
 //   alpha_j = q_j . w;  w -= alpha_j q_j + beta_{j-1} q_{j-1};
-//   two classical Gram-Schmidt passes against q_0..q_j;
+//   two classical Gram-Schmidt passes against q_0..q_j (each pass takes all
+//   j + 1 products with the same w: wave v computes those of q_v, q_{v+16},
+//   ..., so a pass needs one work-group barrier, not one per vector);
 //   beta_j = ||w||; q_{j+1} = w / beta_j (a zero beta ends the run).
 __global__ __launch_bounds__(1024) void lanczos_step_kernel(float* Q, int n_pad, float* w, int j, int m,
                                                             LanczosState* st) {
   __shared__ double red[16];
   __shared__ double h[LZ_MAX];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, wave = tid / WAVE, lane = tid & (WAVE - 1);
+  constexpr int NWAVES = 1024 / WAVE;
   if (j >= st->active) return;
   const float* qj = Q + (long long)j * n_pad;
   double acc = 0.0;
@@ -93,12 +96,12 @@ __global__ __launch_bounds__(1024) void lanczos_step_kernel(float* Q, int n_pad,
     w[i] = (float)((double)w[i] - a * qj[i] - (j > 0 ? bprev * qp[i] : 0.0));
   __syncthreads();
   for (int pass = 0; pass < 2; ++pass) {
-    for (int v = 0; v <= j; ++v) {
+    for (int v = wave; v <= j; v += NWAVES) {
       const float* qv = Q + (long long)v * n_pad;
       double d = 0.0;
-      for (int i = tid; i < n_pad; i += 1024) d += (double)qv[i] * w[i];
-      d = block_sum(d, red);
-      if (tid == 0) h[v] = d;
+      for (int i = lane; i < n_pad; i += WAVE) d += (double)qv[i] * w[i];
+      d = wave_sum(d);
+      if (lane == 0) h[v] = d;
     }
     __syncthreads();
     for (int i = tid; i < n_pad; i += 1024) {
