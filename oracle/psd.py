@@ -27,6 +27,11 @@ Deflated projection (Alg. 2), one call:
 g is the Newton-Schulz composition (filters.ns_filter) with a per-step
 coefficient table; the default is the cubic Bjorck-Bowie map (3/2, -1/2).
 A zero theta drops the R / theta term.
+fp16 mode (the fp16 projection of the paper's SDP runs): every product of the
+filter stage takes fp16 operands, the restore product R g included, whose
+operands are R / theta (entries in [-1, 1], since theta >= ||R||_2) and g,
+rounded to fp16; the product is scaled back by theta. R, the Ritz step, the
+Lanczos scale and every sum stay wide.
 """
 from __future__ import annotations
 
@@ -36,6 +41,7 @@ import numpy as np
 
 from .filters import ns_filter
 from .linalg import cholqr
+from .precision import round_f16
 from .rng import lanczos_start
 
 CUBIC = (1.5, -0.5)
@@ -117,13 +123,13 @@ def psd_project_deflated(z, basis, *, table=None, steps=10, gamma=1.1, tau=0.0,
         x0 = (res / theta if theta > 0 else np.zeros_like(res)) \
             + (ui * np.sign(li)) @ ui.T / gamma
         g = ns_filter(x0, table, mode)
-        p = 0.5 * (res + res @ g) + (ui * np.maximum(li, 0.0)) @ ui.T
+        p = 0.5 * (res + restore_product(res, g, theta, mode)) + (ui * np.maximum(li, 0.0)) @ ui.T
         n_pos = int(np.count_nonzero(li > 0))
     else:
         theta = lanczos_scale(lambda x: z @ (z @ x), n, seed, lanczos_steps)
         x0 = z / theta if theta > 0 else np.zeros_like(z)
         g = ns_filter(x0, table, mode)
-        p = 0.5 * (z + z @ g)
+        p = 0.5 * (z + restore_product(z, g, theta, mode))
         n_pos = 0
     p = 0.5 * (p + p.T)
     return p, cholqr(zt), PSDInfo(n_def, n_pos, theta, lam)
@@ -136,8 +142,18 @@ def psd_project(z, *, table=None, steps=10, seed=0, lanczos_steps=20, mode="exac
     theta = lanczos_scale(lambda x: z @ (z @ x), z.shape[0], seed, lanczos_steps)
     x0 = z / theta if theta > 0 else np.zeros_like(z)
     g = ns_filter(x0, table, mode)
-    p = 0.5 * (z + z @ g)
+    p = 0.5 * (z + restore_product(z, g, theta, mode))
     return 0.5 * (p + p.T), theta
+
+
+def restore_product(r: np.ndarray, g: np.ndarray, theta: float, mode: str) -> np.ndarray:
+    """R g, the product that restores the sign filter's output (Alg. 2,
+    eq:baseline_projection); in fp16 mode theta fp16(R / theta) fp16(g)."""
+    if mode != "f16":
+        return r @ g
+    if theta <= 0.0:
+        return np.zeros_like(r)
+    return theta * (round_f16(r / theta) @ round_f16(g))
 
 
 def psd_exact(z: np.ndarray) -> np.ndarray:

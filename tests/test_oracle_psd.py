@@ -162,3 +162,36 @@ def test_f16_projection_within_the_fp16_error_of_exact():
     assert (i16.n_deflated, i16.n_positive) == (i64.n_deflated, i64.n_positive)
     np.testing.assert_array_equal(v16, v64)   # the basis update does not involve the filter
 
+
+
+def test_f16_restore_product_rounds_normalized_operands():
+    # The fp16 restore product rounds R / theta (not R) and g. With R = 3 F,
+    # theta = 3 and F, g on the fp16 grid, both operands survive rounding,
+    # so the product equals the exact one bit for bit; rounding R itself
+    # would not (3 F needs up to 13 significant bits).
+    from oracle.precision import round_f16
+    rng = np.random.default_rng(7)
+    f = round_f16(rng.uniform(-1, 1, (24, 24)))
+    g = round_f16(rng.uniform(-1, 1, (24, 24)))
+    r = 3.0 * f
+    assert not np.array_equal(round_f16(r), r)
+    np.testing.assert_array_equal(psd.restore_product(r, g, 3.0, "f16"), r @ g)
+    # a zero scale gives a zero product; exact mode is the plain product
+    np.testing.assert_array_equal(psd.restore_product(r, g, 0.0, "f16"), np.zeros_like(r))
+    np.testing.assert_array_equal(psd.restore_product(r, g, 3.0, "exact"), r @ g)
+
+
+def test_f16_restore_product_within_the_operand_rounding_bound():
+    # |fl16(a) - a| <= 2^-11 |a| per operand, so
+    # ||theta (R~ g~) - R g||_F <= 2^-11 theta (||R/theta||_F ||g~||_2 + ||R/theta||_2 ||g||_F);
+    # the error is nonzero on generic operands (the rounding is applied).
+    rng = np.random.default_rng(8)
+    a = rng.standard_normal((64, 64))
+    r = a + a.T
+    theta = 1.01 * np.linalg.norm(r, 2)
+    g = np.tanh(rng.standard_normal((64, 64)))
+    err = np.linalg.norm(psd.restore_product(r, g, theta, "f16") - r @ g)
+    from oracle.precision import round_f16
+    bound = 2.0 ** -11 * theta * (np.linalg.norm(r / theta) * np.linalg.norm(round_f16(g), 2)
+                                  + np.linalg.norm(r / theta, 2) * np.linalg.norm(g))
+    assert 0 < err <= bound
