@@ -228,6 +228,31 @@ struct EpiUpdate {
   }
 };
 
+// Full product scaled by a device scalar: out = (*scale) C, fp32, row-wise.
+struct EpiScaleStore {
+  static constexpr bool PRE = false;
+  static constexpr bool ROWWISE = true;
+  static constexpr bool HI_FROM_B = false;
+  float* out;
+  const float* scale;
+  long long stride;
+  int ld;
+  __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&,
+                         float (&w)[8]) const {
+    const float s = *scale;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) w[q] = v[q] * s;
+    store8(b, r, c0, w);
+  }
+  __device__ void store8(int b, int r, int c0, const float (&w)[8]) const {
+    const long long o = b * stride + (long long)r * ld + c0;
+    *reinterpret_cast<f32x4_t*>(out + o) = f32x4_t{w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<f32x4_t*>(out + o + 4) = f32x4_t{w[4], w[5], w[6], w[7]};
+  }
+  __device__ void operator()(int, int, int, float*, int) const {}
+};
+
 // Iterate update of a symmetric filter (X and the polynomial in X commute,
 // so X_next = ac X + B X is symmetric and computed on upper-triangle tiles):
 // row-wise, out = ac * x + C in fp32 and its T16 copy (the next products'

@@ -32,6 +32,7 @@ struct LowRankArgs {
   int ldo;
   bf16_t* out16;      // optional bf16 copy of out (same layout)
   int8_t* out_lo;     // with out16: e4m3 residual byte of out against bf16(out) (state_pack8)
+  f16_t* xs16;        // optional fp16(alpha * x) (same layout as out)
   float* sumsq;       // [b][tiles] or null
   int rows_pad, cols_pad, kmax, batch;
 };
@@ -91,17 +92,21 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
   const int i0 = (t / tc) * 128, n0 = (t % tc) * 128;
   const int tid = threadIdx.x;
   const int rg = tid >> 4, cg = tid & 15;
-  // Loads in the order they are needed: the low-rank panels (all kmax rows:
-  // the coefficients past the per-matrix count are zero, so no load waits on
-  // that count), then the thread's X values, whose latency overlaps the
-  // low-rank product.
+  // Every load is issued before any of them is used: the low-rank panels
+  // and their coefficients (all kmax rows: the coefficients past the
+  // per-matrix count are zero, so no load waits on that count; rows past
+  // kmax load row kmax - 1 and are not stored), then the thread's X values,
+  // whose latency overlaps the low-rank product. (Scaling a panel value as
+  // it arrives made every panel load wait for the one before.)
   constexpr int PER = KM * 128 / 256;
-  float lv[PER], rv[PER];
+  float lv[PER], cv[PER], rv[PER];
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
     const int e = tid + 256 * u, j = e >> 7, x = e & 127;
-    lv[u] = j < a.kmax ? a.L[b * a.sl + (long long)j * a.ldl + i0 + x] * a.coef[b * a.kmax + j] : 0.f;
-    rv[u] = j < a.kmax ? a.Rr[b * a.sr + (long long)j * a.ldr + n0 + x] : 0.f;
+    const int jc = j < a.kmax ? j : a.kmax - 1;
+    lv[u] = a.L[b * a.sl + (long long)jc * a.ldl + i0 + x];
+    cv[u] = a.coef[b * a.kmax + jc];
+    rv[u] = a.Rr[b * a.sr + (long long)jc * a.ldr + n0 + x];
   }
   const TX* xb = reinterpret_cast<const TX*>(a.x) + b * a.sx;
   Raw8<TX> xr[8];
@@ -113,7 +118,7 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
   for (int u = 0; u < PER; ++u) {
     const int e = tid + 256 * u, j = e >> 7, x = e & 127;
     if (j < a.kmax) {
-      ls[j][x] = lv[u];
+      ls[j][x] = lv[u] * cv[u];
       rs[j][x] = rv[u];
     }
   }
@@ -142,6 +147,12 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
     const int i = i0 + rg * 8 + r;
     float v[8];
     xr[r].get(v);
+    if (a.xs16) {
+      const long long o = b * a.so + (long long)i * a.ldo + n0 + cg * 8;
+      *reinterpret_cast<u32x4_t*>(a.xs16 + o) =
+          u32x4_t{pack_h2(alpha * v[0], alpha * v[1]), pack_h2(alpha * v[2], alpha * v[3]),
+                  pack_h2(alpha * v[4], alpha * v[5]), pack_h2(alpha * v[6], alpha * v[7])};
+    }
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
       v[c] = fmaf(alpha, v[c], acc[r][c]);

@@ -200,6 +200,7 @@ struct PsdPlan {
   bool copy_in, quintic, f16;
   float *zp, *r, *xa, *xb, *s32, *bm, *c;
   f16_t *xh0, *xh1, *bh, *ah;   // fp16 filter: operand copies of X (current, next), B and (quintic) A
+  f16_t* rh;                    // fp16 filter: R / theta, the restore product's operand
   float *vt, *zt, *E, *lam, *ut, *coefR, *coefX, *coefP;
   int* ndef;
   double *part, *fac;
@@ -220,6 +221,7 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
   p.xh1 = p.f16 ? ar.take<f16_t>(nn) : nullptr;
   p.bh = p.f16 ? ar.take<f16_t>(nn) : nullptr;
   p.ah = p.f16 && p.quintic ? ar.take<f16_t>(nn) : nullptr;
+  p.rh = p.f16 ? ar.take<f16_t>(nn) : nullptr;
   const int kq = p.K > 0 ? p.K : 1;
   const int kr = round_up(kq, 32);
   p.vt = ar.take<float>((size_t)kr * p.n_pad);
@@ -385,12 +387,14 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   la.coef = p.coefX;
   la.alpha = p.alpha_x0;
   la.out = p.xa;
+  la.xs16 = p.rh;   // fp16 path: R / theta, the restore product's operand
   lowrank<float, float>(la, st);
+  la.xs16 = nullptr;
 
   float* cur = p.xa;
   float* nxt = p.xb;
   const int nc = (o.poly_degree + 1) / 2;
-  if (p.f16 && p.steps > 0) {
+  if (p.f16) {
     // fp16 products on the direct-to-LDS kernel: every epilogue also writes
     // the fp16 copy of what the next product reads (X, B, A), rounded from
     // the same fp32 value the fp32 buffers hold
@@ -482,11 +486,17 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     cur = nxt;
     nxt = tmp;
   }
-  // C = R g (g symmetric, so the NT form reads rows of g)
+  // C = R g (g symmetric, so the NT form reads rows of g); fp16 path:
+  // C = theta fp16(R / theta) fp16(g), the operands the filter left behind
   ProfScope ps(SD_STAGE_RESTORE, st);
   GemmShape g{np, np, np, np, np, nn, nn, 1};
-  EpiStore es{p.c, nn, np};
-  launch_gemm<CfgTile128, float, false, false>(p.r, cur, g, es, st);
+  if (p.f16) {
+    EpiScaleStore es{p.c, p.theta, nn, np};
+    launch_gemm_dma<CfgDma128, false, false>(p.rh, p.steps % 2 ? p.xh1 : p.xh0, g, es, st);
+  } else {
+    EpiStore es{p.c, nn, np};
+    launch_gemm<CfgTile128, float, false, false>(p.r, cur, g, es, st);
+  }
   const int tiles = (np / 64) * (np / 64);
   const float* ut = K > 0 ? p.ut : nullptr;
   const int* kk = K > 0 ? p.ndef : nullptr;

@@ -236,11 +236,15 @@ def test_config4_f16():
     assert int(info["n_deflated"]) == oinfo.n_deflated
 
 
-# fp32 ADMM: the 1e-4 fp32 contract. fp16 filter: each projection carries the
-# fp16 filter's 1e-4 contract and the iteration accumulates it (40 steps at
-# most 1e-3 relative in practice: measured 4.3e-4 on S).
+# fp32 ADMM: the 1e-4 fp32 contract. fp16 products: each projection meets
+# the fp16 contract's 1e-4 against the oracle (F16_TOL) and the iterations
+# add those differences up, so T iterations are held to T x 1e-4 (measured
+# after 40 iterations: 8.7e-4 on S; after 12: 4.7e-4).
 ADMM_F32_TOL = 1e-4
-ADMM_F16_TOL = 1e-3
+
+
+def admm_f16_tol(iters: int) -> float:
+    return iters * F16_TOL
 
 
 def _admm_compare(case, iters, warmup, precision, x0=None, s0=None, y0=None, basis=None):
@@ -279,7 +283,7 @@ def test_admm_maxcut_warmup_against_oracle(precision):
     (ex, es, ey), eta, etas, ndef, proj = _admm_compare(case, 40, 10, precision)
     say(f"admm warm-up {precision}: X {ex:.2e} S {es:.2e} y {ey:.2e}; eta {eta[-1]:.4e} vs {etas[-1]:.4e}")
     assert ndef == proj.n_deflated == [0] * 40
-    assert max(ex, es, ey) < (ADMM_F32_TOL if precision == "f32" else ADMM_F16_TOL)
+    assert max(ex, es, ey) < (ADMM_F32_TOL if precision == "f32" else admm_f16_tol(40))
     np.testing.assert_allclose(eta, etas, rtol=1e-2)
 
 
@@ -302,5 +306,5 @@ def test_admm_maxcut_deflating_against_oracle(precision):
         f"deflated {ndef}")
     assert ndef == proj.n_deflated
     assert min(ndef) > 0
-    assert max(ex, es, ey) < (ADMM_F32_TOL if precision == "f32" else ADMM_F16_TOL)
+    assert max(ex, es, ey) < (ADMM_F32_TOL if precision == "f32" else admm_f16_tol(12))
     np.testing.assert_allclose(eta, etas, rtol=1e-2)
