@@ -138,8 +138,41 @@ def _timed(step, steps: int, warmup: int) -> float:
     return start.elapsed_time(end) / steps
 
 
+def _psd_update_roofline(sd, step, steps: int, n: int, precision: str) -> dict:
+    """Roofline of the filter's update product X B (symmetric tiles: the
+    n (n + 1) / 2 entries of the upper triangle, 2 n flops each, counted once)
+    against the dense MFMA peak of its operand type."""
+    ms, launches = _stage_time(sd, step, steps, "ns_update")
+    n_pad = -(-n // 128) * 128
+    flops = float(n_pad) * (n_pad + 1) * n_pad
+    avg_ms = ms / max(launches, 1)
+    tf = flops / (avg_ms / 1e3) / 1e12
+    peak = 157.3 if precision == "f32" else MFMA_BF16_PEAK_TFLOPS   # fp16 dense = bf16 dense
+    return {"bound": "mfma", "kernel": "filter update X <- a X + X B, symmetric tiles "
+            + ("(gemm_dma_kernel, fp16 operands)" if precision == "f16" else "(gemm_kernel, fp32)"),
+            "achieved": tf, "peak": peak, "unit": "TFLOP/s", "frac": tf / peak, "traffic": None,
+            "flops_per_launch": flops, "avg_launch_us": avg_ms * 1e3, "launches": launches}
+
+
+def _stage_time(sd, step, steps: int, stage: str) -> tuple[float, int]:
+    """(milliseconds, launches) of one stage over `steps` further calls, each
+    launch bracketed by HIP events on the library's stream."""
+    import torch
+    torch.cuda.synchronize()
+    sd.profile_reset()
+    sd.profile_set(stage)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    sd.profile_set()
+    return sd.profile_read(stage)
+
+
 def other_workload(args) -> int:
-    """Throughput of the configurations other than the benchmark line."""
+    """Throughput of the configurations other than the benchmark line, each
+    with the roofline of its dominant kernel: the bf16 iterate update (HBM)
+    for the Muon groups, the symmetric filter update (MFMA) for the PSD and
+    ADMM workloads."""
     import torch
     import paper_2609_21102_amd as sd
     import workloads
@@ -179,6 +212,26 @@ def other_workload(args) -> int:
             def step():
                 sd.msign_groups(groups)
         ms = _timed(step, args.steps, args.warmup)
+        # the update of every group, summed: bytes and flops over launch time
+        # (grouped calls run groups concurrently, so launch times overlap)
+        upd_ms, upd_n = _stage_time(sd, step, args.steps, "ns_update")
+        upd_bytes = upd_flops = 0.0
+        for c in cases:
+            b_, s_, l_ = c.x.shape[0], min(c.x.shape[1:]), max(c.x.shape[1:])
+            upd_bytes += b_ * update_bytes_per_matrix(s_, l_, c.steps) * c.steps * args.steps
+            upd_flops += b_ * 2.0 * s_ * s_ * l_ * c.steps * args.steps
+        sec = upd_ms / 1e3
+        if upd_flops / upd_bytes > MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
+            ach = upd_flops / sec / 1e12
+            roof = {"bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": ach / MFMA_BF16_PEAK_TFLOPS, "flops_per_launch": upd_flops / max(upd_n, 1)}
+        else:
+            ach = upd_bytes / sec / 1e9
+            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
+                    "bytes_per_launch": upd_bytes / max(upd_n, 1)}
+        roof.update({"kernel": "iterate update X <- a X + B X (gemm_dma_kernel, EpiUpdateHL), all groups",
+                     "traffic": None, "avg_launch_us": upd_ms * 1e3 / max(upd_n, 1), "launches": upd_n,
+                     "flop_per_byte": upd_flops / upd_bytes})
         desc = " + ".join(f"{c.x.shape[0]} x {c.x.shape[1]} x {c.x.shape[2]}" for c in cases)
         res = {"metric": f"deflated msign matrices/s ({args.workload}: {desc} bf16)", "value": nmat / (ms / 1e3),
                "unit": "matrices/s", "ms_per_step": ms, "tflops": flops / (ms / 1e3) / 1e12,
@@ -186,7 +239,8 @@ def other_workload(args) -> int:
                "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
                "config": {"workload": args.workload, "groups": desc,
                           "launch": "one call per group" if args.sequential else "sd_msign_groups",
-                          "k": [c.k for c in cases], "filter_steps": [c.steps for c in cases]}}
+                          "k": [c.k for c in cases], "filter_steps": [c.steps for c in cases]},
+               "roofline": roof}
     elif args.workload == "admm":
         # ADMM on a max-cut relaxation of the size of the paper's n = 5000
         # instances (planted-bisection random graph), tracked basis K = 64
@@ -207,6 +261,7 @@ def other_workload(args) -> int:
             last.update(eta=eta, ndef=ndef)
 
         ms = _timed(call, args.steps, args.warmup)
+        roof = _psd_update_roofline(sd, call, args.steps, n, args.precision)
         flops = chunk * (2.0 * n ** 3 * steps + 2.0 * n ** 3)
         peak = 157.3 if args.precision == "f32" else MFMA_BF16_PEAK_TFLOPS
         res = {"metric": f"ADMM iterations/s (max-cut SDP, n = {n}, K = {k}, {args.precision} filter products)",
@@ -215,7 +270,8 @@ def other_workload(args) -> int:
                "steps": args.steps, "warmup": args.warmup, "dtype": args.precision, "data": "synthetic",
                "config": {"workload": "admm", "n": n, "k": k, "window": r, "tau": 0.1, "filter_steps": steps,
                           "iterations_per_step": chunk, "final_eta": float(last["eta"][-1]),
-                          "final_n_deflated": int(last["ndef"][-1])}}
+                          "final_n_deflated": int(last["ndef"][-1])},
+               "roofline": roof}
     else:
         if args.workload == "c4":
             case = workloads.config4()
@@ -236,6 +292,7 @@ def other_workload(args) -> int:
                            precision=args.precision)
 
         ms = _timed(call, args.steps, args.warmup)
+        roof = _psd_update_roofline(sd, call, args.steps, n, args.precision)
         # cubic filter: X^2 and X X^2 are both symmetric and computed on upper-triangle
         # tiles (n^3 each per step); the restore product R g is a full 2 n^3
         flops = 2.0 * n ** 3 * steps + 2.0 * n ** 3
@@ -246,9 +303,12 @@ def other_workload(args) -> int:
                "tflops": flops / (ms / 1e3) / 1e12, "mfma_frac": flops / (ms / 1e3) / 1e12 / peak,
                "steps": args.steps, "warmup": args.warmup, "dtype": args.precision, "data": "synthetic",
                "config": {"workload": args.workload, "n": n, "k": k, "filter_steps": steps,
-                          "subspace_iters": sub}}
+                          "subspace_iters": sub},
+               "roofline": roof}
+    r = res["roofline"]
     log(f"bench {args.workload}: {res['ms_per_step']:.3f} ms per call, {res['value']:.1f} {res['unit']}, "
-        f"{res['tflops']:.1f} TFLOP/s")
+        f"{res['tflops']:.1f} TFLOP/s; {r['kernel']}: {r['avg_launch_us']:.1f} us avg over {r['launches']} launches, "
+        f"{r['achieved']:.0f} {r['unit']} ({100 * r['frac']:.1f}% of peak)")
     print(json.dumps(res), flush=True)
     return 0
 
