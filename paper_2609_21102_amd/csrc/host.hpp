@@ -219,7 +219,7 @@ inline void cholqr(float* Pt, long long sp, int ld, int c, int len_pad, int batc
   if (c <= 16) {
     hipLaunchKernelGGL((chol_qr_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, part, nch, status, Pt16, c16);
   } else {   // wider panels: factor on one work-group per panel, then apply
-    hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(64), 0, st, part, nch, c, fac, status);
+    hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(256), 0, st, part, nch, c, fac, status);
     if (c <= 32) hipLaunchKernelGGL((chol_apply_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16, c16);
     else hipLaunchKernelGGL((chol_apply_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16, c16);
   }

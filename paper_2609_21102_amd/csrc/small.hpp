@@ -496,17 +496,19 @@ static __device__ __forceinline__ void gram_reduce(SmallLds& s, const double* pa
 // --------------------------------------------------------- CholeskyQR -----
 // Factor: Gram = L L^T (right-looking, pivots floored at c u tr(Gram)); L is
 // written to fac[b] (c x c, float64, lower). A zero trace writes L = 0, which
-// the apply kernel turns into a zero panel. One wave per panel.
-static __global__ __launch_bounds__(64) void chol_factor_kernel(const double* part, int nch, int c, double* fac,
-                                                         int* status) {
+// the apply kernel turns into a zero panel. One work-group (four waves) per
+// panel: all of them reduce the partials and update the trailing triangle.
+static __global__ __launch_bounds__(256) void chol_factor_kernel(const double* part, int nch, int c, double* fac,
+                                                          int* status) {
   __shared__ SmallLds s;
-  const int b = blockIdx.x, tid = threadIdx.x;
+  const int b = blockIdx.x, tid = threadIdx.x, nt = blockDim.x;
+  const int lane = tid & (WAVE - 1), w = tid / WAVE, nw = nt / WAVE;
   gram_reduce(s, part + (long long)b * nch * gram_items(c, c, true), nch, c, c, true);
   double tr = 0.0;
   for (int a = 0; a < c; ++a) tr += s.h[a][a];
   double* L = fac + (long long)b * c * c;
   if (tr == 0.0) {
-    for (int e = tid; e < c * c; e += 64) L[e] = 0.0;
+    for (int e = tid; e < c * c; e += nt) L[e] = 0.0;
     return;
   }
   const double floor_ = (double)c * 1.1102230246251565e-16 * tr;
@@ -520,16 +522,16 @@ static __global__ __launch_bounds__(64) void chol_factor_kernel(const double* pa
       s.h[j][j] = sqrt(d);
     }
     __syncthreads();
-    for (int i = j + 1 + tid; i < c; i += 64) s.h[i][j] /= s.h[j][j];
+    for (int i = j + 1 + tid; i < c; i += nt) s.h[i][j] /= s.h[j][j];
     __syncthreads();
-    const int m = c - j - 1;
-    for (int e = tid; e < m * m; e += 64) {
-      const int i = j + 1 + e / m, k = j + 1 + e % m;
+    // trailing update of the lower triangle: wave w takes rows j + 1 + w,
+    // j + 1 + w + nw, ...; lane l column j + 1 + l (c <= 64 = one wave)
+    const int k = j + 1 + lane;
+    for (int i = j + 1 + w; i < c; i += nw)
       if (k <= i) s.h[i][k] -= s.h[i][j] * s.h[k][j];
-    }
     __syncthreads();
   }
-  for (int e = tid; e < c * c; e += 64) {
+  for (int e = tid; e < c * c; e += nt) {
     const int i = e / c, k = e - i * c;
     L[e] = k <= i ? s.h[i][k] : 0.0;
   }
