@@ -359,7 +359,8 @@ def admm_diag(C, b, iters: int, k: int = 0, qwarm=None, *, X=None, S=None, y=Non
     y = torch.zeros(n, dtype=torch.float32, device=dev) if y is None else y
     eta = torch.empty(max(iters, 1), dtype=torch.float32, device=dev)
     ndef = torch.empty(max(iters, 1), dtype=torch.int32, device=dev)
-    o = psd_opts(gamma=gamma, tau=tau, window=window, precision=SD_PREC[precision], seed=seed)
+    # no tracked basis (k = 0): the undeflated projection, no gate
+    o = psd_opts(gamma=gamma, tau=tau if k > 0 else 0.0, window=window, precision=SD_PREC[precision], seed=seed)
     rc = lib().sd_admm_diag(n, iters, steps, sigma, _ptr(C), _ptr(b), _ptr(X), _ptr(S), _ptr(y), k,
                             _ptr(qwarm) if k > 0 else None, warmup, ctypes.byref(o), _ptr(eta), _ptr(ndef),
                             _stream(stream))

@@ -155,6 +155,28 @@ def test_psd_invalid_arguments(lib):
         assert rc == -1, bad
 
 
+def test_admm_invalid_arguments_and_empty_run(lib):
+    f = ctypes.c_float
+    P = [ctypes.c_void_p(0x100000 * (i + 1)) for i in range(6)]   # never dereferenced
+    C, b, X, S, y, Q = P
+    o = sd.psd_opts()
+    call = lambda n, iters, sigma, k, q, warmup=0, opts=None, C=C: lib.sd_admm_diag(
+        n, iters, 5, f(sigma), C, b, X, S, y, k, q, warmup, opts, None, None, None)
+    assert call(0, 3, 1.0, 0, None) == -1                 # n < 1
+    assert call(16, -1, 1.0, 0, None) == -1               # negative iteration count
+    assert call(16, 3, 0.0, 0, None) == -1                # sigma must be positive
+    assert call(16, 3, 1.0, 4, None) == -1                # deflation without a basis
+    assert call(16, 3, 1.0, 16, Q) == -1                  # k >= n
+    assert call(16, 3, 1.0, 0, None, warmup=-1) == -1
+    assert call(16, 3, 1.0, 0, None, C=None) == -1        # missing matrix
+    assert call(200, 3, 1.0, 65, Q) == -2                 # K beyond the supported Rayleigh-Ritz block
+    bad = sd.psd_opts(tau=0.1, window=0)
+    assert call(64, 3, 1.0, 4, Q, opts=ctypes.byref(bad)) == -1
+    # zero iterations: validated, nothing launched, success
+    assert call(64, 0, 1.0, 4, Q, opts=ctypes.byref(o)) == 0
+    assert sd.lib().sd_admm_workspace_bytes(4096, 16, 10, None) > sd.psd_workspace_bytes(4096, 16)
+
+
 def test_workspace_queries(lib):
     big = sd.msign_workspace_bytes(24, 768, 3072, 8, sd.SD_DTYPE_BF16)
     base = sd.msign_workspace_bytes(24, 768, 3072, 0, sd.SD_DTYPE_BF16)

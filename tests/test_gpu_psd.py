@@ -308,3 +308,40 @@ def test_admm_maxcut_deflating_against_oracle(precision):
     assert min(ndef) > 0
     assert max(ex, es, ey) < (ADMM_F32_TOL if precision == "f32" else admm_f16_tol(12))
     np.testing.assert_allclose(eta, etas, rtol=1e-2)
+
+
+def test_admm_baseline_projection_against_oracle():
+    """K = 0: ADMM with the undeflated projection (eq:baseline_projection)
+    in every iteration, 25 iterations from zero, against the oracle."""
+    from oracle import admm as oadmm
+    case = workloads.planted_maxcut(160, case_id=4)
+    C = torch.from_numpy(case.c).cuda()
+    b = torch.from_numpy(case.b).cuda()
+    X, S, y, eta, ndef = sd.admm_diag(C, b, 25, 0, None)
+    torch.cuda.synchronize()
+    proj = oadmm.DeflatedProjector(None)
+    xo, so, yo, etas = oadmm.admm_diag(case.c.astype(np.float64), case.b.astype(np.float64), 25, proj)
+    ex, es, ey = rel_fro(host64(X), xo), rel_fro(host64(S), so), rel_fro(host64(y), yo)
+    say(f"admm baseline: X {ex:.2e} S {es:.2e} y {ey:.2e}; eta {float(eta[-1]):.4e} vs {etas[-1]:.4e}")
+    assert ndef.cpu().tolist() == [0] * 25
+    assert max(ex, es, ey) < ADMM_F32_TOL
+    np.testing.assert_allclose(eta.cpu().numpy(), etas, rtol=1e-3)
+
+
+def test_admm_split_calls_equal_one_call_bitwise():
+    """The iteration state is X, S, y and the tracked basis, all caller-owned:
+    12 iterations in one call equal 5 + 7 iterations in two calls bit for bit
+    (gate open from the start, so the warm-up counter plays no part)."""
+    case = workloads.planted_maxcut(160, case_id=5)
+    C = torch.from_numpy(case.c).cuda()
+    b = torch.from_numpy(case.b).cuda()
+    kw = dict(warmup=0, tau=0.1, window=case.window)
+    q1 = torch.from_numpy(case.basis0).cuda()
+    X1, S1, y1, e1, d1 = sd.admm_diag(C, b, 12, case.k, q1, **kw)
+    q2 = torch.from_numpy(case.basis0).cuda()
+    X2, S2, y2, e2a, d2a = sd.admm_diag(C, b, 5, case.k, q2, **kw)
+    X2, S2, y2, e2b, d2b = sd.admm_diag(C, b, 7, case.k, q2, X=X2, S=S2, y=y2, **kw)
+    torch.cuda.synchronize()
+    for u, v in ((X1, X2), (S1, S2), (y1, y2), (q1, q2)):
+        assert torch.equal(u, v)
+    assert torch.equal(e1, torch.cat([e2a, e2b])) and torch.equal(d1, torch.cat([d2a, d2b]))
