@@ -91,6 +91,51 @@ def test_config1_fp32():
             np.testing.assert_allclose(info["s"].cpu().numpy()[0], oinfo.s[0], rtol=1e-5)
 
 
+@pytest.mark.parametrize("shape", [(2, 1, 37), (3, 45, 1)], ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_vector_inputs_closed_form(shape, dtype):
+    # A 1 x n (or n x 1) input has one singular value; X0 = X / ||X||_F puts
+    # it at 1, so the filter returns p^L(1) v / ||v|| with p^L the scalar
+    # composition of the coefficient table (eq:general_ns_iteration). The
+    # bf16 contract rounds every product operand (the 1 x 1 Gram is then
+    # 1 + O(2^-8) and the error grows over the steps), so in bf16 only the
+    # oracle's bf16 contract is the reference.
+    case = workloads.small_muon(*shape, dtype=dtype, k=0, case_id=7)
+    say(f"vector input {shape} {dtype}")
+    out, _ = run_case(case, k=0)
+    v = case.x64.reshape(shape[0], -1)
+    scale = 1.0
+    for row in case.coeffs:
+        scale = sum(c * scale ** (2 * i + 1) for i, c in enumerate(row))
+    want = scale * v / np.linalg.norm(v, axis=1, keepdims=True)
+    got = host64(out).reshape(shape[0], -1)
+    tol = F32_TOL if dtype == "f32" else BF16_TOL
+    if dtype == "f32":
+        for b in range(shape[0]):
+            assert rel_fro(got[b], want[b]) < tol
+    want_o, _ = oracle_case(case, k=0)
+    assert rel_fro(host64(out), want_o) < tol
+
+
+@pytest.mark.parametrize("shape", [(2, 2, 50), (2, 50, 3)], ids=lambda s: "x".join(map(str, s)))
+def test_full_rank_sketch_fp32(shape):
+    # r' = min(s, k + p) = s: the sketch spans the whole short side, so the
+    # head is exact and only rounding is left in R (Sec. 2.2 exact deflation).
+    # A moderate spike over the bulk: float32 resolves the residual's
+    # singular values to about 1e-7 of the spike, so a spike 5000 times the
+    # bulk leaves 5e-4 in R against the float64 oracle (measured), past the
+    # 1e-4 contract; a ratio of at most 40 keeps that below 1e-5.
+    case = workloads.small_muon(*shape, k=1, spikes=[4.0], bulk=(0.1, 1.0), case_id=8)
+    say(f"full-rank sketch {shape}")
+    out, info = run_case(case, k=1)
+    want, oinfo = oracle_case(case, k=1)
+    assert rel_fro(host64(out), want) < F32_TOL
+    assert info["k_eff"].cpu().tolist() == oinfo.k_eff
+    got_s = info["s"].cpu().numpy().reshape(shape[0], -1)
+    for b in range(shape[0]):
+        np.testing.assert_allclose(got_s[b][0], oinfo.s[b][0], rtol=1e-5)
+
+
 @pytest.mark.parametrize("shape", [(2, 64, 200), (1, 96, 96), (3, 200, 70), (1, 128, 1000)],
                          ids=lambda s: "x".join(map(str, s)))
 @pytest.mark.parametrize("k", [0, 4])
