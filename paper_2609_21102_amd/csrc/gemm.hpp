@@ -69,6 +69,13 @@ __device__ __forceinline__ void st_row4(bf16_t* p, int ld, int r, int c0, const 
   *reinterpret_cast<uint2*>(p + (long long)r * ld + c0) = w;
 }
 
+__device__ __forceinline__ void st_row4(f16_t* p, int ld, int r, int c0, const float v[4]) {
+  uint2 w;
+  w.x = pack_h2(v[0], v[1]);
+  w.y = pack_h2(v[2], v[3]);
+  *reinterpret_cast<uint2*>(p + (long long)r * ld + c0) = w;
+}
+
 // Store v (rows r0..r0+3, column c) into a symmetric-or-full matrix.
 template <typename T>
 __device__ __forceinline__ void emit4(T* p, int ld, int r0, int c, const float v[4], int mode) {
@@ -91,11 +98,12 @@ __device__ __forceinline__ void emit4(T* p, int ld, int r0, int c, const float v
 
 // ------------------------------------------------------- epilogues --------
 // Gram: out32 = scale32 * C (fp32, optional), out16 = T16(scale16 * C)
-// (optional; bf16 or fp16, rounded to nearest even).
-template <typename T16>
+// (optional; bf16 or fp16, rounded to nearest even). RW = false: stores from
+// the MFMA layout (for tiles whose C tile does not fit in LDS).
+template <typename T16, bool RW = true>
 struct EpiGramT {
   static constexpr bool PRE = false;
-  static constexpr bool ROWWISE = true;
+  static constexpr bool ROWWISE = RW;
   static constexpr bool HI_FROM_B = false;
   // Row-wise form (direct-to-LDS kernel): eight consecutive columns of row r.
   // The transposed (lower-triangle) copy gets out16 only (store8): out32 is
@@ -228,10 +236,12 @@ struct EpiUpdate {
   }
 };
 
-// Full product scaled by a device scalar: out = (*scale) C, fp32, row-wise.
+// Full product scaled by a device scalar: out = (*scale) C, fp32; row-wise,
+// or from the MFMA layout (RW = false).
+template <bool RW = true>
 struct EpiScaleStore {
   static constexpr bool PRE = false;
-  static constexpr bool ROWWISE = true;
+  static constexpr bool ROWWISE = RW;
   static constexpr bool HI_FROM_B = false;
   float* out;
   const float* scale;
@@ -250,7 +260,11 @@ struct EpiScaleStore {
     *reinterpret_cast<f32x4_t*>(out + o) = f32x4_t{w[0], w[1], w[2], w[3]};
     *reinterpret_cast<f32x4_t*>(out + o + 4) = f32x4_t{w[4], w[5], w[6], w[7]};
   }
-  __device__ void operator()(int, int, int, float*, int) const {}
+  __device__ void operator()(int b, int r0, int c, float v[4], int mode) const {
+    const float s = *scale;
+    float w[4] = {v[0] * s, v[1] * s, v[2] * s, v[3] * s};
+    emit4(out + b * stride, ld, r0, c, w, mode);
+  }
 };
 
 // Iterate update of a symmetric filter (X and the polynomial in X commute,
@@ -290,6 +304,34 @@ struct EpiUpdateSym {
                                Op16<T16>::pack2(w[4], w[5]), Op16<T16>::pack2(w[6], w[7])});
   }
   __device__ void operator()(int, int, int, float*, int) const {}
+};
+
+// EpiUpdateSym from the MFMA layout, for tiles whose C tile does not fit in
+// LDS: x is read after the main loop (the long K loops this form serves
+// leave that read negligible), both outputs through emit4 (mirrored on
+// off-diagonal tiles).
+template <typename T16>
+struct EpiUpdateSymNR {
+  static constexpr bool PRE = false;
+  static constexpr bool ROWWISE = false;
+  static constexpr bool HI_FROM_B = false;
+  const float* x;
+  float ac;
+  float* out;
+  T16* out16;
+  long long stride;
+  int ld;
+  __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
+  __device__ void apply8(int, int, int, const float (&)[8], const u32x4_t&, const u32x4_t&, float (&)[8]) const {}
+  __device__ void store8(int, int, int, const float (&)[8]) const {}
+  __device__ void operator()(int b, int r0, int c, float v[4], int mode) const {
+    const float* xb = x + b * stride;
+    float w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = ac * xb[(long long)(r0 + j) * ld + c] + v[j];
+    emit4(out + b * stride, ld, r0, c, w, mode);
+    emit4(out16 + b * stride, ld, r0, c, w, mode);
+  }
 };
 
 // Iterate update with the bf16 iterate stored as hi = bf16(X) plus an e4m3
@@ -461,6 +503,7 @@ using CfgTile256x128s = GemmCfg<2, 2, 4, 2, 1, 2>;   // 256 x 128, 256 threads
 using CfgTile128s = GemmCfg<2, 2, 2, 2, 1, 2>;       // 128 x 128, 256 threads
 // Direct-to-LDS kernel: 128 x 128, two-stage ring, two work-groups per CU.
 using CfgDma128 = GemmCfg<2, 2, 2, 2, 2, 2>;
+using CfgDma256 = GemmCfg<2, 4, 4, 2, 2, 2>;   // 256 x 256, eight waves, one work-group per CU
 
 // Eight floats (two 16-byte words) rounded to eight 16-bit operands of type T.
 template <typename T>

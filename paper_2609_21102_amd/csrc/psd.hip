@@ -198,6 +198,7 @@ __global__ void to_f16_kernel(const float* __restrict__ x, long long n8, f16_t* 
 struct PsdPlan {
   int n, k, steps, n_pad, K, lz;
   bool copy_in, quintic, f16;
+  bool wide;   // fp16 products on 256 x 256 tiles (n_pad a multiple of 256, at least 4096)
   float *zp, *r, *xa, *xb, *s32, *bm, *c;
   f16_t *xh0, *xh1, *bh, *ah;   // fp16 filter: operand copies of X (current, next), B and (quintic) A
   f16_t* rh;                    // fp16 filter: R / theta, the restore product's operand
@@ -277,6 +278,7 @@ static void make_psd_plan(PsdPlan& p, int n, int k, int steps, const float* X, c
   p.lz = o.lanczos_steps < n ? o.lanczos_steps : n;
   p.quintic = o.poly_degree == 5;
   p.f16 = o.precision == SD_PREC_F16;
+  p.wide = p.f16 && p.n_pad % 256 == 0 && p.n_pad >= 4096;
   const bool aligned = X && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
   p.copy_in = p.n != p.n_pad || !aligned;
 }
@@ -400,6 +402,12 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     // the same fp32 value the fp32 buffers hold
     f16_t* hc = p.xh0;
     f16_t* hn = p.xh1;
+    // 256 x 256 tiles (epilogues from the MFMA layout) for n_pad a multiple
+    // of 256 from 4096 up (measured faster there: fewer operand bytes per
+    // flop on these long K loops); 128 x 128 otherwise. The
+    // quintic's Gram and A^2 keep 128 (its fp32 A copy is written on, and
+    // read back from, the same tiles).
+    const bool wide = p.wide;
     const long long n8 = (long long)np * np / 8;
     hipLaunchKernelGGL(to_f16_kernel, grid1(n8, 256), dim3(256), 0, st, cur, n8, hc);
     for (int t = 0; t < p.steps; ++t) {
@@ -422,7 +430,16 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
       }
       {
         ProfScope ps(SD_STAGE_NS_GRAM, st);
-        launch_gemm_dma<CfgDma128, false, true>(hc, hc, g, eg, st);
+        if (wide && c == 0.f) {
+          EpiGramT<f16_t, false> ew{};
+          ew.out16 = eg.out16;
+          ew.scale16 = eg.scale16;
+          ew.stride = eg.stride;
+          ew.ld = eg.ld;
+          launch_gemm_dma<CfgDma256, false, true>(hc, hc, g, ew, st);
+        } else {
+          launch_gemm_dma<CfgDma128, false, true>(hc, hc, g, eg, st);
+        }
       }
       if (c != 0.f) {
         ProfScope ps(SD_STAGE_NS_POLY, st);
@@ -432,8 +449,13 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
       {
         ProfScope ps(SD_STAGE_NS_UPDATE, st);
         // B X = B X^T: the NT form on rows of X; symmetric tiles
-        EpiUpdateSym<f16_t> eu{cur, a, nxt, hn, nn, np};
-        launch_gemm_dma<CfgDma128, false, true>(p.bh, hc, g, eu, st);
+        if (wide) {
+          EpiUpdateSymNR<f16_t> eu{cur, a, nxt, hn, nn, np};
+          launch_gemm_dma<CfgDma256, false, true>(p.bh, hc, g, eu, st);
+        } else {
+          EpiUpdateSym<f16_t> eu{cur, a, nxt, hn, nn, np};
+          launch_gemm_dma<CfgDma128, false, true>(p.bh, hc, g, eu, st);
+        }
       }
       float* tmp = cur;
       cur = nxt;
@@ -490,8 +512,11 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   // C = theta fp16(R / theta) fp16(g), the operands the filter left behind
   ProfScope ps(SD_STAGE_RESTORE, st);
   GemmShape g{np, np, np, np, np, nn, nn, 1};
-  if (p.f16) {
-    EpiScaleStore es{p.c, p.theta, nn, np};
+  if (p.f16 && p.wide) {
+    EpiScaleStore<false> es{p.c, p.theta, nn, np};
+    launch_gemm_dma<CfgDma256, false, false>(p.rh, p.steps % 2 ? p.xh1 : p.xh0, g, es, st);
+  } else if (p.f16) {
+    EpiScaleStore<> es{p.c, p.theta, nn, np};
     launch_gemm_dma<CfgDma128, false, false>(p.rh, p.steps % 2 ? p.xh1 : p.xh0, g, es, st);
   } else {
     EpiStore es{p.c, nn, np};

@@ -201,6 +201,35 @@ def test_config5_full_chain():
     say(f"config5 chain: median call {1e3 * sorted(times)[len(times) // 2]:.0f} ms")
 
 
+def test_config5_full_f16():
+    """Config 5 at n = 16384 with fp16 products (the 256 x 256 tile path):
+    three chained calls, checked like the fp32 chain on what holds at any
+    size, the probe error against the exact projection with the same bound
+    (fp16 operand rounding adds about 1e-3 to the method's 1.3e-2)."""
+    n, k = 16384, 32
+    z, lam, qf, qwarm = workloads.config5_device(n)
+    order = np.argsort(-np.abs(lam), kind="stable")
+    dom = lam[order[:k]]
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+    probes = torch.randn((n, 8), generator=gen, device="cuda", dtype=torch.float64)
+    exact_probe = qf @ (torch.from_numpy(np.maximum(lam, 0.0)).cuda().unsqueeze(1) * (qf.T @ probes))
+    for call in range(3):
+        out, info = sd.psd_project(z, k, 10, qwarm, subspace_iters=1, gamma=1.1, info=True, precision="f16")
+        torch.cuda.synchronize()
+        assert torch.equal(out, out.T)
+        assert bool(torch.isfinite(out).all())
+        assert int(info["n_deflated"]) == k
+        assert int(info["n_positive"]) == int((dom > 0).sum())
+        ritz = np.sort(info["ritz"].double().cpu().numpy())
+        assert np.allclose(ritz, np.sort(dom), rtol=0, atol=1.0 + 1e-4 * np.abs(dom).max() + 0.3 * call), call
+        if call == 0:
+            perr = float(torch.linalg.norm(out.double() @ probes - exact_probe) / torch.linalg.norm(exact_probe))
+            say(f"config5 f16 call 0: probe error vs exact {perr:.2e}, theta {float(info['theta']):.4g}")
+            assert perr < 5e-2, perr
+        z = workloads.psd_drift_device(z, 1e-3, call)
+
+
 @pytest.mark.parametrize("n,k,degree", [(256, 8, 3), (300, 16, 3), (129, 4, 3), (180, 8, 5)])
 def test_f16_filter(n, k, degree):
     """precision="f16": the sign filter's products take fp16 operands (the
@@ -225,6 +254,8 @@ def test_f16_filter(n, k, degree):
 
 @pytest.mark.slow
 def test_config4_f16():
+    # n = 4096: the fp16 products run on 256 x 256 tiles (n_pad a multiple of
+    # 256 from 4096 up), the smaller cases above on 128 x 128
     case = workloads.config4()
     out, info, _ = gpu_psd(case, precision="f16")
     want, _, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm.astype(np.float64),
