@@ -73,7 +73,8 @@ __global__ __launch_bounds__(1024) void lanczos_init_kernel(float* Q, int n, int
   }
 }
 
-// One Lanczos step on B = R^2 with w = B q_j already computed:
+// One Lanczos step on B = R^2 with w = B q_j already computed, on one
+// work-group (n_pad below 8192: one launch instead of four):
 //   alpha_j = q_j . w;  w -= alpha_j q_j + beta_{j-1} q_{j-1};
 //   two classical Gram-Schmidt passes against q_0..q_j (each pass takes all
 //   j + 1 products with the same w: wave v computes those of q_v, q_{v+16},
@@ -126,6 +127,108 @@ __global__ __launch_bounds__(1024) void lanczos_step_kernel(float* Q, int n_pad,
   float* qn = Q + (long long)(j + 1) * n_pad;
   for (int i = tid; i < n_pad; i += 1024) qn[i] = (float)((double)w[i] / beta);
   if (tid == 0) st->beta[j] = beta;
+}
+
+// The same step spread over work-groups of 256 positions (one per thread),
+// for n_pad from 8192 up (the one-work-group step grows with n: 187 us at
+// n = 16384, against about 55 us here), in four launches:
+//   dots:    h_v = q_v . w for v <= j (per-wave partial sums);
+//   pass 1:  w -= sum_v h_v q_v, with alpha_j = h_j (this subtracts the
+//            three-term recurrence's alpha_j q_j and beta_{j-1} q_{j-1} and
+//            a first classical Gram-Schmidt pass in one), then the partial
+//            products of the second pass;
+//   pass 2:  w -= sum_v h'_v q_v, then the partial squares of w;
+//   next:    beta_j = ||w||, q_{j+1} = w / beta_j (a zero beta ends the run).
+// Every work-group reduces the partials itself (fixed order), so the steps
+// need no atomics and are deterministic. A run that has ended (j >= active)
+// returns at once.
+constexpr int LZ_BLOCK = 256;
+constexpr int LZ_MULTI_MIN = 8192;   // n_pad from which the step spreads over work-groups
+
+__host__ __device__ inline int lanczos_partials(int n_pad) { return 4 * ((n_pad + LZ_BLOCK - 1) / LZ_BLOCK); }
+
+// h[v] (LDS) = sum over the partials of row v, v <= j; one wave per row.
+__device__ __forceinline__ void lanczos_reduce(const double* part, int np4, int j, double* h) {
+  const int wave = threadIdx.x / WAVE, lane = threadIdx.x & (WAVE - 1);
+  for (int v = wave; v <= j; v += LZ_BLOCK / WAVE) {
+    double t = 0.0;
+    for (int e = lane; e < np4; e += WAVE) t += part[(long long)v * np4 + e];
+    t = wave_sum(t);
+    if (lane == 0) h[v] = t;
+  }
+  __syncthreads();
+}
+
+// part[v][4 blk + wave] = sum over the wave's positions of q_v[i] y (v <= j).
+__device__ __forceinline__ void lanczos_partial_dots(const float* Q, int n_pad, int j, int i, double y,
+                                                     double* part, int np4) {
+  const int wave = threadIdx.x / WAVE, lane = threadIdx.x & (WAVE - 1);
+  float q[LZ_MAX];
+#pragma unroll
+  for (int v = 0; v < LZ_MAX; ++v) q[v] = (v <= j && i < n_pad) ? Q[(long long)v * n_pad + i] : 0.f;
+#pragma unroll
+  for (int v = 0; v < LZ_MAX; ++v) {
+    if (v > j) break;
+    const double d = wave_sum((double)q[v] * y);
+    if (lane == 0) part[(long long)v * np4 + 4 * blockIdx.x + wave] = d;
+  }
+}
+
+__global__ __launch_bounds__(LZ_BLOCK) void lanczos_dots_kernel(const float* Q, int n_pad, const float* w, int j,
+                                                                double* part, const LanczosState* st) {
+  if (j >= st->active) return;
+  const int i = blockIdx.x * LZ_BLOCK + threadIdx.x;
+  const double y = i < n_pad ? (double)w[i] : 0.0;
+  lanczos_partial_dots(Q, n_pad, j, i, y, part, lanczos_partials(n_pad));
+}
+
+// pass 1 (last = 0): subtract, store alpha_j, partial dots of the result into
+// out; pass 2 (last = 1): subtract, partial squares into out (row 0).
+__global__ __launch_bounds__(LZ_BLOCK) void lanczos_pass_kernel(const float* Q, int n_pad, float* w, int j,
+                                                                const double* in, double* out, int last,
+                                                                LanczosState* st) {
+  __shared__ double h[LZ_MAX];
+  if (j >= st->active) return;
+  const int np4 = lanczos_partials(n_pad);
+  lanczos_reduce(in, np4, j, h);
+  if (!last && blockIdx.x == 0 && threadIdx.x == 0) {
+    st->alpha[j] = h[j];
+    st->steps = j + 1;
+  }
+  const int i = blockIdx.x * LZ_BLOCK + threadIdx.x;
+  float q[LZ_MAX];
+#pragma unroll
+  for (int v = 0; v < LZ_MAX; ++v) q[v] = (v <= j && i < n_pad) ? Q[(long long)v * n_pad + i] : 0.f;
+  double t = i < n_pad ? (double)w[i] : 0.0;
+#pragma unroll
+  for (int v = 0; v < LZ_MAX; ++v) {
+    if (v > j) break;
+    t -= h[v] * q[v];
+  }
+  if (i < n_pad) w[i] = (float)t;
+  const double y = (double)(float)t;   // the stored value
+  if (!last) {
+    lanczos_partial_dots(Q, n_pad, j, i, y, out, np4);
+  } else {
+    const int wave = threadIdx.x / WAVE, lane = threadIdx.x & (WAVE - 1);
+    const double d = wave_sum(y * y);
+    if (lane == 0) out[4 * blockIdx.x + wave] = d;
+  }
+}
+
+__global__ __launch_bounds__(LZ_BLOCK) void lanczos_next_kernel(float* Q, int n_pad, const float* w, int j, int m,
+                                                                const double* sq, LanczosState* st) {
+  __shared__ double h[1];
+  if (j >= st->active || j == m - 1) return;
+  lanczos_reduce(sq, lanczos_partials(n_pad), 0, h);
+  const double beta = sqrt(h[0]);
+  if (beta == 0.0) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) st->active = j + 1;
+    return;
+  }
+  const int i = blockIdx.x * LZ_BLOCK + threadIdx.x;
+  if (i < n_pad) Q[(long long)(j + 1) * n_pad + i] = (float)((double)w[i] / beta);
+  if (blockIdx.x == 0 && threadIdx.x == 0) st->beta[j] = beta;
 }
 
 // Largest Ritz pair of the tridiagonal matrix: rho and v = Q y.
@@ -207,6 +310,7 @@ struct PsdPlan {
   double *part, *fac;
   float *qlan, *w, *t, *v, *theta, *alpha_x0;
   LanczosState* lst;
+  double* lpart;   // Lanczos step partial sums: two blocks of LZ_MAX rows
 };
 
 static void plan_psd(PsdPlan& p, Arena& ar) {
@@ -243,6 +347,7 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
   p.theta = ar.take<float>(1);
   p.alpha_x0 = ar.take<float>(1);
   p.lst = ar.take<LanczosState>(1);
+  p.lpart = ar.take<double>((size_t)2 * LZ_MAX * lanczos_partials(p.n_pad));
 }
 
 static int validate_psd(int n, int k, int steps, const float* X, const float* Qwarm, const float* out,
@@ -292,7 +397,16 @@ static void lanczos(const PsdPlan& p, const float* R, uint64_t seed, float* thet
   for (int j = 0; j < p.lz; ++j) {
     hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.qlan + (long long)j * np, p.t);
     hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.t, p.w);
-    hipLaunchKernelGGL(lanczos_step_kernel, dim3(1), dim3(1024), 0, st, p.qlan, np, p.w, j, p.lz, p.lst);
+    if (np < LZ_MULTI_MIN) {
+      hipLaunchKernelGGL(lanczos_step_kernel, dim3(1), dim3(1024), 0, st, p.qlan, np, p.w, j, p.lz, p.lst);
+      continue;
+    }
+    const dim3 lg((np + LZ_BLOCK - 1) / LZ_BLOCK), lb(LZ_BLOCK);
+    const long long rows = (long long)lanczos_partials(np) * LZ_MAX;
+    hipLaunchKernelGGL(lanczos_dots_kernel, lg, lb, 0, st, p.qlan, np, p.w, j, p.lpart, p.lst);
+    hipLaunchKernelGGL(lanczos_pass_kernel, lg, lb, 0, st, p.qlan, np, p.w, j, p.lpart, p.lpart + rows, 0, p.lst);
+    hipLaunchKernelGGL(lanczos_pass_kernel, lg, lb, 0, st, p.qlan, np, p.w, j, p.lpart + rows, p.lpart, 1, p.lst);
+    hipLaunchKernelGGL(lanczos_next_kernel, lg, lb, 0, st, p.qlan, np, p.w, j, p.lz, p.lpart, p.lst);
   }
   switch (jacobi_class(p.lz)) {   // the run may stop early: kk <= lz
     case 4: hipLaunchKernelGGL(lanczos_ritz_kernel<4>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;

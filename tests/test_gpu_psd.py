@@ -230,6 +230,23 @@ def test_config5_full_f16():
         z = workloads.psd_drift_device(z, 1e-3, call)
 
 
+@pytest.mark.parametrize("n", [8192, 8200])
+def test_lanczos_scale_multi_block(n):
+    """From n_pad = 8192 up the Lanczos steps run over many work-groups
+    (four launches per step); theta against the oracle's estimate on a
+    symmetric Gaussian matrix (no deflation, no filter steps: the call's
+    theta is the Lanczos estimate of ||Z||_2). n = 8200 pads to 8320, a
+    partial last work-group."""
+    z = workloads.sym_gaussian(n, case_id=1)
+    zt = torch.from_numpy(z).cuda()
+    out, info = sd.psd_project(zt, 0, 0, None, info=True)
+    torch.cuda.synchronize()
+    want = opsd.lanczos_scale(lambda x: z.astype(np.float64) @ (z.astype(np.float64) @ x), n, 0, 20)
+    got = float(info["theta"])
+    say(f"lanczos n={n}: theta {got:.7g} vs {want:.7g}")
+    assert abs(got - want) <= 1e-5 * want
+
+
 @pytest.mark.parametrize("n,k,degree", [(256, 8, 3), (300, 16, 3), (129, 4, 3), (180, 8, 5)])
 def test_f16_filter(n, k, degree):
     """precision="f16": the sign filter's products take fp16 operands (the

@@ -291,6 +291,14 @@ def small_psd(n, *, k=8, n_dom=4, dom=(50.0, 200.0), subspace_iters=2, steps=10,
                     gamma, ids=(200, case_id, n, k), eps=eps)
 
 
+def sym_gaussian(n: int, case_id: int = 0) -> np.ndarray:
+    """Seeded symmetric Gaussian matrix (G + G^T) / sqrt(2), float32, exactly
+    symmetric (a semicircle spectrum of radius about 2 sqrt(n))."""
+    g = rng_for(600, case_id, n).standard_normal((n, n)).astype(np.float32)
+    z = (g + g.T) / np.float32(math.sqrt(2.0))
+    return np.triu(z) + np.triu(z, 1).T
+
+
 def psd_drift(z: np.ndarray, rel: float, call: int, case_id: int = 5) -> np.ndarray:
     """Seeded symmetric perturbation E with ||E||_F = rel * ||Z||_F."""
     rng = rng_for(500, case_id, call)
