@@ -253,15 +253,19 @@ static __global__ void rows_to_panel_kernel(const float* in, int c, int len, int
 //   P = (P_raw + P_raw^T) / 2 = (R + R^T) / 4 + (C + C^T) / 4 + H.
 // Every term is evaluated so that P[i][j] and P[j][i] see the same operations
 // on swapped operands (sums are commutative, H uses cp * (u_i u_j)), hence P
-// is exactly symmetric. 64 x 64 tiles; the transposed tiles go through LDS.
+// is exactly symmetric. 64 x 64 tiles; the transposed tiles and the head's
+// coefficients go through LDS (a coefficient read from global memory inside
+// the head sum was re-read after every store, which may alias it).
 template <int KM>
-__global__ __launch_bounds__(256) void psd_out_kernel(const float* R, const float* C, int ld, const float* Ut,
-                                                      int ldu, const float* coef_p, const int* kk_dev, int n,
-                                                      int n_pad, float* out) {
+__global__ __launch_bounds__(256) void psd_out_kernel(const float* __restrict__ R, const float* __restrict__ C,
+                                                      int ld, const float* __restrict__ Ut, int ldu,
+                                                      const float* __restrict__ coef_p, const int* kk_dev, int n,
+                                                      int n_pad, float* __restrict__ out) {
   __shared__ float ct[64][65];
   __shared__ float rt[64][65];
   __shared__ float ui[KM][64];
   __shared__ float uj[KM][64];
+  __shared__ float cps[KM];
   const int tiles = n_pad / 64;
   const int i0 = (blockIdx.x / tiles) * 64, j0 = (blockIdx.x % tiles) * 64;
   const int tid = threadIdx.x;
@@ -277,12 +281,13 @@ __global__ __launch_bounds__(256) void psd_out_kernel(const float* R, const floa
     ui[p][x] = Ut[(long long)p * ldu + i0 + x];
     uj[p][x] = Ut[(long long)p * ldu + j0 + x];
   }
+  if (tid < kk) cps[tid] = coef_p[tid];
   __syncthreads();
   const int tx = tid & 63, ty = tid >> 6;
   for (int r = ty; r < 64; r += 4) {
     const int i = i0 + r, j = j0 + tx;
     float h = 0.f;
-    for (int p = 0; p < kk; ++p) h = fmaf(coef_p[p], ui[p][r] * uj[p][tx], h);
+    for (int p = 0; p < kk; ++p) h = fmaf(cps[p], ui[p][r] * uj[p][tx], h);
     const long long ij = (long long)i * ld + j;
     const float v = 0.25f * (R[ij] + rt[r][tx]) + 0.25f * (C[ij] + ct[r][tx]) + h;
     if (i < n && j < n) out[(long long)i * n + j] = v;

@@ -42,6 +42,7 @@ struct LanczosState {
   int active;      // number of Lanczos vectors that may be used
   int steps;       // alpha entries computed
   double rho;
+  double y[LZ_MAX];   // the largest Ritz vector of the tridiagonal matrix
 };
 
 // q_0 = g / ||g|| with g the Philox Gaussians of stream 2 (n entries, zero
@@ -231,10 +232,10 @@ __global__ __launch_bounds__(LZ_BLOCK) void lanczos_next_kernel(float* Q, int n_
   if (blockIdx.x == 0 && threadIdx.x == 0) st->beta[j] = beta;
 }
 
-// Largest Ritz pair of the tridiagonal matrix: rho and v = Q y.
+// Largest Ritz pair of the tridiagonal matrix: rho and y (v = Q y is formed
+// by lanczos_vec_kernel over many work-groups).
 template <int NP>
-__global__ __launch_bounds__(SM_THREADS) void lanczos_ritz_kernel(const float* Q, int n_pad, float* v,
-                                                                  LanczosState* st) {
+__global__ __launch_bounds__(SM_THREADS) void lanczos_ritz_kernel(LanczosState* st) {
   __shared__ SmallLds s;
   const int tid = threadIdx.x;
   const int kk = st->steps;
@@ -257,11 +258,26 @@ __global__ __launch_bounds__(SM_THREADS) void lanczos_ritz_kernel(const float* Q
   }
   __syncthreads();
   const int best = s.perm[0];
-  for (int i = tid; i < n_pad; i += SM_THREADS) {
-    double t = 0.0;
-    for (int a = 0; a < kk; ++a) t += s.e[a][best] * (double)Q[(long long)a * n_pad + i];
-    v[i] = (float)t;
+  if (tid < kk) st->y[tid] = s.e[tid][best];
+}
+
+// v = Q y (y from lanczos_ritz_kernel), one position per thread, every load
+// issued before the sum.
+__global__ __launch_bounds__(256) void lanczos_vec_kernel(const float* Q, int n_pad, float* v,
+                                                          const LanczosState* st) {
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  const int kk = st->steps;
+  if (i >= n_pad) return;
+  float q[LZ_MAX];
+#pragma unroll
+  for (int a = 0; a < LZ_MAX; ++a) q[a] = a < kk ? Q[(long long)a * n_pad + i] : 0.f;
+  double t = 0.0;
+#pragma unroll
+  for (int a = 0; a < LZ_MAX; ++a) {
+    if (a >= kk) break;
+    t += st->y[a] * (double)q[a];
   }
+  v[i] = (float)t;
 }
 
 // theta = sqrt(rho + ||B v - rho v||); alpha_x0 = 1 / theta (0 for theta = 0).
@@ -409,13 +425,14 @@ static void lanczos(const PsdPlan& p, const float* R, uint64_t seed, float* thet
     hipLaunchKernelGGL(lanczos_next_kernel, lg, lb, 0, st, p.qlan, np, p.w, j, p.lz, p.lpart, p.lst);
   }
   switch (jacobi_class(p.lz)) {   // the run may stop early: kk <= lz
-    case 4: hipLaunchKernelGGL(lanczos_ritz_kernel<4>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
-    case 8: hipLaunchKernelGGL(lanczos_ritz_kernel<8>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
-    case 12: hipLaunchKernelGGL(lanczos_ritz_kernel<12>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
-    case 16: hipLaunchKernelGGL(lanczos_ritz_kernel<16>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
-    case 32: hipLaunchKernelGGL(lanczos_ritz_kernel<32>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
-    default: hipLaunchKernelGGL(lanczos_ritz_kernel<0>, dim3(1), dim3(SM_THREADS), 0, st, p.qlan, np, p.v, p.lst); break;
+    case 4: hipLaunchKernelGGL(lanczos_ritz_kernel<4>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
+    case 8: hipLaunchKernelGGL(lanczos_ritz_kernel<8>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
+    case 12: hipLaunchKernelGGL(lanczos_ritz_kernel<12>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
+    case 16: hipLaunchKernelGGL(lanczos_ritz_kernel<16>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
+    case 32: hipLaunchKernelGGL(lanczos_ritz_kernel<32>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
+    default: hipLaunchKernelGGL(lanczos_ritz_kernel<0>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
   }
+  hipLaunchKernelGGL(lanczos_vec_kernel, dim3((np + 255) / 256), dim3(256), 0, st, p.qlan, np, p.v, p.lst);
   hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.v, p.t);
   hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.t, p.w);
   hipLaunchKernelGGL(lanczos_theta_kernel, dim3(1), dim3(1024), 0, st, p.w, p.v, np, p.lst, p.theta, p.alpha_x0,
