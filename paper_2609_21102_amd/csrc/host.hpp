@@ -229,7 +229,7 @@ inline void rotate(const float* in, long long si, int ldi, const float* E, long 
                    long long ssc, float* out, long long so, int ldo, int kin, int kout, int len, int batch,
                    hipStream_t st) {
   ProfScope ps(SD_STAGE_SMALL, st);
-  const dim3 g((len / 128) * batch), b(128);
+  const dim3 g((len / 128) * batch, ROT_RJ), b(128);
   if (kin <= 16) hipLaunchKernelGGL((rotate_kernel<16>), g, b, 0, st, in, si, ldi, E, se, scale, ssc, out, so, ldo, kin, kout, len, batch);
   else if (kin <= 32) hipLaunchKernelGGL((rotate_kernel<32>), g, b, 0, st, in, si, ldi, E, se, scale, ssc, out, so, ldo, kin, kout, len, batch);
   else hipLaunchKernelGGL((rotate_kernel<64>), g, b, 0, st, in, si, ldi, E, se, scale, ssc, out, so, ldo, kin, kout, len, batch);

@@ -882,22 +882,38 @@ __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const double* part, in
 
 // ------------------------------------------------------------- rotate -----
 // out[b][j][x] = scale[b][j] * sum_{a < kin} E[b][a][j] in[b][a][x] for
-// j < kout, x < len (len a multiple of 128). scale may be null (1).
+// j < kout, x < len (len a multiple of 128). scale may be null (1). Grid:
+// (len / 128) * batch work-groups times RJ column groups of outputs
+// (blockIdx.y: j = y, y + RJ, ...), so wide panels spread over more CUs;
+// every global load of a thread is issued before its first use.
+constexpr int ROT_RJ = 4;
 template <int KM>
-__global__ __launch_bounds__(128) void rotate_kernel(const float* in, long long si, int ldi, const float* E,
-                                                     long long se, const float* scale, long long ssc,
-                                                     float* out, long long so, int ldo, int kin, int kout,
+__global__ __launch_bounds__(128) void rotate_kernel(const float* __restrict__ in, long long si, int ldi,
+                                                     const float* __restrict__ E, long long se,
+                                                     const float* __restrict__ scale, long long ssc,
+                                                     float* __restrict__ out, long long so, int ldo, int kin, int kout,
                                                      int len, int batch) {
   __shared__ float es[KM * KM];
   const int per = len / 128;
   const int b = blockIdx.x / per;
   const int x = (blockIdx.x - b * per) * 128 + threadIdx.x;
-  for (int e = threadIdx.x; e < kin * kout; e += 128) es[e] = E[b * se + e];
-  __syncthreads();
+  constexpr int EL = KM * KM / 128;   // E entries per thread
+  float ev[EL];
+#pragma unroll
+  for (int u = 0; u < EL; ++u) {
+    const int e = threadIdx.x + 128 * u;
+    ev[u] = e < kin * kout ? E[b * se + e] : 0.f;
+  }
   float v[KM];
 #pragma unroll
   for (int a = 0; a < KM; ++a) v[a] = a < kin ? in[b * si + (long long)a * ldi + x] : 0.f;
-  for (int j = 0; j < kout; ++j) {
+#pragma unroll
+  for (int u = 0; u < EL; ++u) {
+    const int e = threadIdx.x + 128 * u;
+    if (e < kin * kout) es[e] = ev[u];
+  }
+  __syncthreads();
+  for (int j = blockIdx.y; j < kout; j += ROT_RJ) {
     float acc = 0.f;
 #pragma unroll
     for (int a = 0; a < KM; ++a)
