@@ -232,36 +232,128 @@ __global__ __launch_bounds__(LZ_BLOCK) void lanczos_next_kernel(float* Q, int n_
   if (blockIdx.x == 0 && threadIdx.x == 0) st->beta[j] = beta;
 }
 
-// Largest Ritz pair of the tridiagonal matrix: rho and y (v = Q y is formed
-// by lanczos_vec_kernel over many work-groups).
-template <int NP>
-__global__ __launch_bounds__(SM_THREADS) void lanczos_ritz_kernel(LanczosState* st) {
-  __shared__ SmallLds s;
-  const int tid = threadIdx.x;
-  const int kk = st->steps;
-  for (int e = tid; e < kk * kk; e += SM_THREADS) {
-    const int i = e / kk, j = e - i * kk;
-    double val = 0.0;
-    if (i == j) val = st->alpha[i];
-    else if (j == i + 1) val = st->beta[i];
-    else if (i == j + 1) val = st->beta[j];
-    s.h[i][j] = val;
+// Largest eigenpair of the Lanczos tridiagonal matrix (alpha on the diagonal,
+// beta beside it, kk = steps entries) on one wave: the eigenvalue by
+// multisection on Sturm counts (the 64 lanes evaluate 64 points of the
+// bracket per round, so it shrinks 65-fold; the Gershgorin interval is the
+// start), then its eigenvector by two steps of inverse iteration (Gaussian
+// elimination with partial pivoting on the tridiagonal matrix, on lane 0).
+// Same result as the full eigendecomposition to rounding, without its
+// sweeps.
+__device__ __forceinline__ int sturm_below(const double* a, const double* b2, int kk, double x, double pivmin) {
+  int cnt = 0;
+  double q = 1.0;
+  for (int i = 0; i < kk; ++i) {
+    q = (a[i] - x) - (i > 0 ? b2[i - 1] / q : 0.0);
+    if (fabs(q) < pivmin) q = -pivmin;
+    cnt += q < 0.0 ? 1 : 0;
   }
-  __syncthreads();
-  jacobi_eig_any<NP>(s, kk);
-  if (tid == 0) {
-    int best = 0;
-    for (int i = 1; i < kk; ++i)
-      if (s.h[i][i] > s.h[best][best]) best = i;
-    s.perm[0] = best;
-    st->rho = s.h[best][best];
-  }
-  __syncthreads();
-  const int best = s.perm[0];
-  if (tid < kk) st->y[tid] = s.e[tid][best];
+  return cnt;
 }
 
-// v = Q y (y from lanczos_ritz_kernel), one position per thread, every load
+__global__ __launch_bounds__(64) void lanczos_top_kernel(LanczosState* st) {
+  __shared__ double a[LZ_MAX], b[LZ_MAX], b2[LZ_MAX];
+  __shared__ double dg[LZ_MAX], u1[LZ_MAX], u2[LZ_MAX], ml[LZ_MAX], y[LZ_MAX];
+  __shared__ int sw[LZ_MAX];
+  const int lane = threadIdx.x;
+  const int kk = st->steps;
+  if (kk < 1) {   // no step taken (cannot happen after lanczos_init): no pair
+    if (lane == 0) st->rho = 0.0;
+    return;
+  }
+  for (int i = lane; i < kk; i += WAVE) {
+    a[i] = st->alpha[i];
+    b[i] = i + 1 < kk ? st->beta[i] : 0.0;
+    b2[i] = b[i] * b[i];
+  }
+  __syncthreads();
+  double lo = 1e300, hi = -1e300, bmax = 0.0;
+  for (int i = lane; i < kk; i += WAVE) {
+    const double r = fabs(b[i]) + (i > 0 ? fabs(b[i - 1]) : 0.0);
+    lo = fmin(lo, a[i] - r);
+    hi = fmax(hi, a[i] + r);
+    bmax = fmax(bmax, b2[i]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    lo = fmin(lo, __shfl_xor(lo, o, WAVE));
+    hi = fmax(hi, __shfl_xor(hi, o, WAVE));
+    bmax = fmax(bmax, __shfl_xor(bmax, o, WAVE));
+  }
+  const double pivmin = 0x1p-1000 * fmax(1.0, bmax);
+  for (int it = 0; it < 16; ++it) {
+    const double w = hi - lo;
+    if (!(w > 0x1p-52 * fmax(fabs(lo), fabs(hi)))) break;
+    const double x = lo + w * (double)(lane + 1) / 65.0;
+    const int c = sturm_below(a, b2, kk, x, pivmin);
+    const unsigned long long m = __ballot(c >= kk);
+    if (m == 0ull) {
+      lo = __shfl(x, WAVE - 1, WAVE);
+    } else {
+      const int f = __ffsll((long long)m) - 1;
+      const double xf = __shfl(x, f, WAVE), xp = __shfl(x, f > 0 ? f - 1 : 0, WAVE);
+      hi = xf;
+      if (f > 0) lo = xp;
+    }
+  }
+  const double lam = 0.5 * (lo + hi);
+  if (lane == 0) {
+    // elimination of T - lam I with partial pivoting (rows i, i + 1)
+    const double eps = 0x1p-52 * fmax(fabs(lo), fabs(hi)) + pivmin;
+    for (int i = 0; i < kk; ++i) {
+      dg[i] = a[i] - lam;
+      u1[i] = b[i];
+      u2[i] = 0.0;
+    }
+    for (int i = 0; i + 1 < kk; ++i) {
+      const double sub = b[i];   // entry (i + 1, i)
+      if (fabs(dg[i]) >= fabs(sub)) {
+        const double d = dg[i] != 0.0 ? dg[i] : eps;
+        dg[i] = d;
+        ml[i] = sub / d;
+        sw[i] = 0;
+        dg[i + 1] -= ml[i] * u1[i];
+      } else {
+        ml[i] = dg[i] / sub;
+        sw[i] = 1;
+        const double d1 = dg[i + 1], e1 = u1[i + 1], o1 = u1[i];
+        dg[i] = sub;
+        u1[i] = d1;
+        u2[i] = e1;
+        dg[i + 1] = o1 - ml[i] * d1;
+        u1[i + 1] = -ml[i] * e1;
+      }
+    }
+    if (dg[kk - 1] == 0.0) dg[kk - 1] = eps;
+    for (int i = 0; i < kk; ++i) y[i] = 1.0;
+    for (int pass = 0; pass < 2; ++pass) {
+      for (int i = 0; i + 1 < kk; ++i) {   // forward: the row operations on y
+        if (sw[i]) {
+          const double t = y[i];
+          y[i] = y[i + 1];
+          y[i + 1] = t - ml[i] * y[i];
+        } else {
+          y[i + 1] -= ml[i] * y[i];
+        }
+      }
+      for (int i = kk - 1; i >= 0; --i) {   // back substitution
+        double t = y[i];
+        if (i + 1 < kk) t -= u1[i] * y[i + 1];
+        if (i + 2 < kk) t -= u2[i] * y[i + 2];
+        y[i] = t / dg[i];
+      }
+      double nrm = 0.0;
+      for (int i = 0; i < kk; ++i) nrm += y[i] * y[i];
+      nrm = sqrt(nrm);
+      for (int i = 0; i < kk; ++i) y[i] /= nrm;
+    }
+    st->rho = lam;
+  }
+  __syncthreads();
+  for (int i = lane; i < kk; i += WAVE) st->y[i] = y[i];
+}
+
+// v = Q y (y from lanczos_top_kernel), one position per thread, every load
 // issued before the sum.
 __global__ __launch_bounds__(256) void lanczos_vec_kernel(const float* Q, int n_pad, float* v,
                                                           const LanczosState* st) {
@@ -424,14 +516,7 @@ static void lanczos(const PsdPlan& p, const float* R, uint64_t seed, float* thet
     hipLaunchKernelGGL(lanczos_pass_kernel, lg, lb, 0, st, p.qlan, np, p.w, j, p.lpart + rows, p.lpart, 1, p.lst);
     hipLaunchKernelGGL(lanczos_next_kernel, lg, lb, 0, st, p.qlan, np, p.w, j, p.lz, p.lpart, p.lst);
   }
-  switch (jacobi_class(p.lz)) {   // the run may stop early: kk <= lz
-    case 4: hipLaunchKernelGGL(lanczos_ritz_kernel<4>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
-    case 8: hipLaunchKernelGGL(lanczos_ritz_kernel<8>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
-    case 12: hipLaunchKernelGGL(lanczos_ritz_kernel<12>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
-    case 16: hipLaunchKernelGGL(lanczos_ritz_kernel<16>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
-    case 32: hipLaunchKernelGGL(lanczos_ritz_kernel<32>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
-    default: hipLaunchKernelGGL(lanczos_ritz_kernel<0>, dim3(1), dim3(SM_THREADS), 0, st, p.lst); break;
-  }
+  hipLaunchKernelGGL(lanczos_top_kernel, dim3(1), dim3(WAVE), 0, st, p.lst);   // kk <= lz: the run may stop early
   hipLaunchKernelGGL(lanczos_vec_kernel, dim3((np + 255) / 256), dim3(256), 0, st, p.qlan, np, p.v, p.lst);
   hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.v, p.t);
   hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.t, p.w);
