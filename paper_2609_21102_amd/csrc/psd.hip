@@ -77,56 +77,145 @@ __global__ __launch_bounds__(1024) void lanczos_init_kernel(float* Q, int n, int
 // One Lanczos step on B = R^2 with w = B q_j already computed, on one
 // work-group (n_pad below 8192: one launch instead of four):
 //   alpha_j = q_j . w;  w -= alpha_j q_j + beta_{j-1} q_{j-1};
-//   two classical Gram-Schmidt passes against q_0..q_j (each pass takes all
-//   j + 1 products with the same w: wave v computes those of q_v, q_{v+16},
-//   ..., so a pass needs one work-group barrier, not one per vector);
+//   two classical Gram-Schmidt passes against q_0..q_j;
 //   beta_j = ||w||; q_{j+1} = w / beta_j (a zero beta ends the run).
+// Thread t keeps the float4 chunks t and t + 1024 of w in registers for the
+// whole step; the basis vectors are read four at a time with every load of
+// a batch issued before its first use (a loop that waited on each load made
+// the step a chain of memory round trips), and a pass's products are
+// reduced per wave, then over the waves, with one barrier.
+constexpr int LS_CH = 2;   // float4 chunks per thread: n_pad / 4 <= 2048
+constexpr int LS_B = 4;    // basis vectors per load batch
+// p[i] when ok, else zeros; the load always reads an in-bounds element (p[0]
+// when not ok) and the zeros are a value select, so the pointer stays a
+// global one (selecting between a global element and a local zero made
+// every load a flat one).
+__device__ __forceinline__ float4 ld4_or0(const float4* __restrict__ p, long long i, bool ok) {
+  const float4 v = p[ok ? i : 0];
+  return ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+}
+__device__ __forceinline__ float ld_or0(const float* __restrict__ p, long long i, bool ok) {
+  const float v = p[ok ? i : 0];
+  return ok ? v : 0.f;
+}
+__device__ __forceinline__ double dot4(const float4& a, const float4& b) {
+  return (double)a.x * b.x + (double)a.y * b.y + (double)a.z * b.z + (double)a.w * b.w;
+}
 __global__ __launch_bounds__(1024) void lanczos_step_kernel(float* Q, int n_pad, float* w, int j, int m,
                                                             LanczosState* st) {
   __shared__ double red[16];
+  __shared__ double part[LZ_MAX][1024 / WAVE];
   __shared__ double h[LZ_MAX];
   const int tid = threadIdx.x, wave = tid / WAVE, lane = tid & (WAVE - 1);
-  constexpr int NWAVES = 1024 / WAVE;
   if (j >= st->active) return;
-  const float* qj = Q + (long long)j * n_pad;
-  double acc = 0.0;
-  for (int i = tid; i < n_pad; i += 1024) acc += (double)qj[i] * w[i];
-  const double a = block_sum(acc, red);
+  const int n4 = n_pad / 4;
+  const float4* Q4 = reinterpret_cast<const float4*>(Q);
+  float4* w4 = reinterpret_cast<float4*>(w);
+  int idx[LS_CH];
+  bool ok[LS_CH];
+  float4 wr[LS_CH], qj[LS_CH], qp[LS_CH];
   const double bprev = j > 0 ? st->beta[j - 1] : 0.0;
-  const float* qp = j > 0 ? Q + (long long)(j - 1) * n_pad : qj;
-  for (int i = tid; i < n_pad; i += 1024)
-    w[i] = (float)((double)w[i] - a * qj[i] - (j > 0 ? bprev * qp[i] : 0.0));
-  __syncthreads();
-  for (int pass = 0; pass < 2; ++pass) {
-    for (int v = wave; v <= j; v += NWAVES) {
-      const float* qv = Q + (long long)v * n_pad;
-      double d = 0.0;
-      for (int i = lane; i < n_pad; i += WAVE) d += (double)qv[i] * w[i];
-      d = wave_sum(d);
-      if (lane == 0) h[v] = d;
-    }
-    __syncthreads();
-    for (int i = tid; i < n_pad; i += 1024) {
-      double t = w[i];
-      for (int v = 0; v <= j; ++v) t -= h[v] * Q[(long long)v * n_pad + i];
-      w[i] = (float)t;
-    }
-    __syncthreads();
+#pragma unroll
+  for (int c = 0; c < LS_CH; ++c) {
+    idx[c] = tid + 1024 * c;
+    ok[c] = idx[c] < n4;
+    wr[c] = ld4_or0(w4, idx[c], ok[c]);
+    qj[c] = ld4_or0(Q4, (long long)j * n4 + idx[c], ok[c]);
+    qp[c] = ld4_or0(Q4, (long long)(j > 0 ? j - 1 : 0) * n4 + idx[c], ok[c] && j > 0);
   }
+  double acc = 0.0;
+#pragma unroll
+  for (int c = 0; c < LS_CH; ++c) acc += dot4(qj[c], wr[c]);
+  const double a = block_sum(acc, red);
+#pragma unroll
+  for (int c = 0; c < LS_CH; ++c) {
+    wr[c].x = (float)((double)wr[c].x - a * qj[c].x - (j > 0 ? bprev * qp[c].x : 0.0));
+    wr[c].y = (float)((double)wr[c].y - a * qj[c].y - (j > 0 ? bprev * qp[c].y : 0.0));
+    wr[c].z = (float)((double)wr[c].z - a * qj[c].z - (j > 0 ? bprev * qp[c].z : 0.0));
+    wr[c].w = (float)((double)wr[c].w - a * qj[c].w - (j > 0 ? bprev * qp[c].w : 0.0));
+  }
+  for (int pass = 0; pass < 2; ++pass) {
+    for (int v0 = 0; v0 <= j; v0 += LS_B) {
+      float4 qa[LS_B][LS_CH];
+#pragma unroll
+      for (int u = 0; u < LS_B; ++u)
+#pragma unroll
+        for (int c = 0; c < LS_CH; ++c)
+          qa[u][c] = ld4_or0(Q4, (long long)(v0 + u) * n4 + idx[c], v0 + u <= j && ok[c]);
+#pragma unroll
+      for (int u = 0; u < LS_B; ++u) {
+        if (v0 + u <= j) {   // uniform over the work-group
+          double d = 0.0;
+#pragma unroll
+          for (int c = 0; c < LS_CH; ++c) d += dot4(qa[u][c], wr[c]);
+          d = wave_sum(d);
+          if (lane == 0) part[v0 + u][wave] = d;
+        }
+      }
+    }
+    __syncthreads();
+    if (tid <= j) {
+      double t = 0.0;
+      for (int q = 0; q < 1024 / WAVE; ++q) t += part[tid][q];
+      h[tid] = t;
+    }
+    __syncthreads();
+    double t[LS_CH][4];
+#pragma unroll
+    for (int c = 0; c < LS_CH; ++c) {
+      t[c][0] = wr[c].x;
+      t[c][1] = wr[c].y;
+      t[c][2] = wr[c].z;
+      t[c][3] = wr[c].w;
+    }
+    for (int v0 = 0; v0 <= j; v0 += LS_B) {
+      float4 qa[LS_B][LS_CH];
+#pragma unroll
+      for (int u = 0; u < LS_B; ++u)
+#pragma unroll
+        for (int c = 0; c < LS_CH; ++c)
+          qa[u][c] = ld4_or0(Q4, (long long)(v0 + u) * n4 + idx[c], v0 + u <= j && ok[c]);
+#pragma unroll
+      for (int u = 0; u < LS_B; ++u) {
+        if (v0 + u <= j) {
+          const double hv = h[v0 + u];
+#pragma unroll
+          for (int c = 0; c < LS_CH; ++c) {
+            t[c][0] -= hv * qa[u][c].x;
+            t[c][1] -= hv * qa[u][c].y;
+            t[c][2] -= hv * qa[u][c].z;
+            t[c][3] -= hv * qa[u][c].w;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int c = 0; c < LS_CH; ++c)
+      wr[c] = make_float4((float)t[c][0], (float)t[c][1], (float)t[c][2], (float)t[c][3]);
+    __syncthreads();   // part and h are reused by the next pass
+  }
+#pragma unroll
+  for (int c = 0; c < LS_CH; ++c)
+    if (ok[c]) w4[idx[c]] = wr[c];
   if (tid == 0) {
     st->alpha[j] = a;
     st->steps = j + 1;
   }
   if (j == m - 1) return;
   double nn = 0.0;
-  for (int i = tid; i < n_pad; i += 1024) nn += (double)w[i] * w[i];
+#pragma unroll
+  for (int c = 0; c < LS_CH; ++c) nn += dot4(wr[c], wr[c]);
   const double beta = sqrt(block_sum(nn, red));
   if (beta == 0.0) {
     if (tid == 0) st->active = j + 1;
     return;
   }
-  float* qn = Q + (long long)(j + 1) * n_pad;
-  for (int i = tid; i < n_pad; i += 1024) qn[i] = (float)((double)w[i] / beta);
+  float4* qn = reinterpret_cast<float4*>(Q + (long long)(j + 1) * n_pad);
+#pragma unroll
+  for (int c = 0; c < LS_CH; ++c)
+    if (ok[c])
+      qn[idx[c]] = make_float4((float)((double)wr[c].x / beta), (float)((double)wr[c].y / beta),
+                               (float)((double)wr[c].z / beta), (float)((double)wr[c].w / beta));
   if (tid == 0) st->beta[j] = beta;
 }
 
@@ -145,6 +234,7 @@ __global__ __launch_bounds__(1024) void lanczos_step_kernel(float* Q, int n_pad,
 // returns at once.
 constexpr int LZ_BLOCK = 256;
 constexpr int LZ_MULTI_MIN = 8192;   // n_pad from which the step spreads over work-groups
+static_assert(LZ_MULTI_MIN / 4 <= LS_CH * 1024, "the one-work-group step holds n_pad / 4 chunks in LS_CH per thread");
 
 __host__ __device__ inline int lanczos_partials(int n_pad) { return 4 * ((n_pad + LZ_BLOCK - 1) / LZ_BLOCK); }
 
@@ -164,14 +254,17 @@ __device__ __forceinline__ void lanczos_reduce(const double* part, int np4, int 
 __device__ __forceinline__ void lanczos_partial_dots(const float* Q, int n_pad, int j, int i, double y,
                                                      double* part, int np4) {
   const int wave = threadIdx.x / WAVE, lane = threadIdx.x & (WAVE - 1);
-  float q[LZ_MAX];
+  for (int v0 = 0; v0 <= j; v0 += 8) {
+    float q[8];
 #pragma unroll
-  for (int v = 0; v < LZ_MAX; ++v) q[v] = (v <= j && i < n_pad) ? Q[(long long)v * n_pad + i] : 0.f;
+    for (int u = 0; u < 8; ++u) q[u] = ld_or0(Q, (long long)(v0 + u) * n_pad + i, v0 + u <= j && i < n_pad);
 #pragma unroll
-  for (int v = 0; v < LZ_MAX; ++v) {
-    if (v > j) break;
-    const double d = wave_sum((double)q[v] * y);
-    if (lane == 0) part[(long long)v * np4 + 4 * blockIdx.x + wave] = d;
+    for (int u = 0; u < 8; ++u) {
+      if (v0 + u <= j) {
+        const double d = wave_sum((double)q[u] * y);
+        if (lane == 0) part[(long long)(v0 + u) * np4 + 4 * blockIdx.x + wave] = d;
+      }
+    }
   }
 }
 
@@ -179,7 +272,7 @@ __global__ __launch_bounds__(LZ_BLOCK) void lanczos_dots_kernel(const float* Q, 
                                                                 double* part, const LanczosState* st) {
   if (j >= st->active) return;
   const int i = blockIdx.x * LZ_BLOCK + threadIdx.x;
-  const double y = i < n_pad ? (double)w[i] : 0.0;
+  const double y = (double)ld_or0(w, i, i < n_pad);
   lanczos_partial_dots(Q, n_pad, j, i, y, part, lanczos_partials(n_pad));
 }
 
@@ -197,14 +290,14 @@ __global__ __launch_bounds__(LZ_BLOCK) void lanczos_pass_kernel(const float* Q, 
     st->steps = j + 1;
   }
   const int i = blockIdx.x * LZ_BLOCK + threadIdx.x;
-  float q[LZ_MAX];
+  double t = (double)ld_or0(w, i, i < n_pad);
+  for (int v0 = 0; v0 <= j; v0 += 8) {
+    float q[8];
 #pragma unroll
-  for (int v = 0; v < LZ_MAX; ++v) q[v] = (v <= j && i < n_pad) ? Q[(long long)v * n_pad + i] : 0.f;
-  double t = i < n_pad ? (double)w[i] : 0.0;
+    for (int u = 0; u < 8; ++u) q[u] = ld_or0(Q, (long long)(v0 + u) * n_pad + i, v0 + u <= j && i < n_pad);
 #pragma unroll
-  for (int v = 0; v < LZ_MAX; ++v) {
-    if (v > j) break;
-    t -= h[v] * q[v];
+    for (int u = 0; u < 8; ++u)
+      if (v0 + u <= j) t -= h[v0 + u] * q[u];
   }
   if (i < n_pad) w[i] = (float)t;
   const double y = (double)(float)t;   // the stored value
@@ -360,14 +453,14 @@ __global__ __launch_bounds__(256) void lanczos_vec_kernel(const float* Q, int n_
   const int i = blockIdx.x * 256 + threadIdx.x;
   const int kk = st->steps;
   if (i >= n_pad) return;
-  float q[LZ_MAX];
-#pragma unroll
-  for (int a = 0; a < LZ_MAX; ++a) q[a] = a < kk ? Q[(long long)a * n_pad + i] : 0.f;
   double t = 0.0;
+  for (int a0 = 0; a0 < kk; a0 += 8) {
+    float q[8];
 #pragma unroll
-  for (int a = 0; a < LZ_MAX; ++a) {
-    if (a >= kk) break;
-    t += st->y[a] * (double)q[a];
+    for (int u = 0; u < 8; ++u) q[u] = ld_or0(Q, (long long)(a0 + u) * n_pad + i, a0 + u < kk);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (a0 + u < kk) t += st->y[a0 + u] * (double)q[u];
   }
   v[i] = (float)t;
 }
