@@ -244,7 +244,7 @@ def other_workload(args) -> int:
     elif args.workload == "admm":
         # ADMM on a max-cut relaxation of the size of the paper's n = 5000
         # instances (planted-bisection random graph), tracked basis K = 64
-        # (the widest Rayleigh-Ritz block this build solves), r = 32, tau = 0.1;
+        # (the widest Rayleigh-Ritz block the library solves), r = 32, tau = 0.1;
         # one step = 10 iterations with the gate open, continuing the state.
         n, k, r, chunk, steps = 5000, 64, 32, 10, 10
         case = workloads.planted_maxcut(n, case_id=0)
@@ -333,8 +333,8 @@ def main() -> int:
                     help="c2-step / paper-step: one call per group on one stream instead of sd_msign_groups")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        log("bench.py: this build runs on a single GPU; --gpus must be 1 "
-            "(the method shards by matrix across GPUs, which is not built here)")
+        log("bench.py: the library runs on a single GPU; --gpus must be 1 "
+            "(sharding the batch by matrix across GPUs is not implemented)")
         return 2
 
     import torch

@@ -45,7 +45,7 @@ extern "C" {
 typedef enum {
   SD_OK = 0,
   SD_ERR_INVALID_ARG = -1, /* bad sizes, null pointers, options out of range */
-  SD_ERR_UNSUPPORTED = -2, /* valid but outside this build (e.g. sketch wider than 64) */
+  SD_ERR_UNSUPPORTED = -2, /* valid but not supported (e.g. sketch wider than 64) */
   SD_ERR_HIP = -3,         /* HIP allocation or launch failure */
   SD_ERR_NUMERIC = -4,     /* reserved: numerical failures are flagged in status_dev */
   SD_ERR_WORKSPACE = -5    /* caller workspace smaller than the *_workspace_bytes query */

@@ -120,7 +120,7 @@ def test_msign_invalid_options_and_pointers(lib):
                 dict(restore=2), dict(restore=-1)):
         o = sd.msign_opts(**bad)
         assert lib.sd_msign_deflated_ex(1, 8, 8, 2, 5, None, 0, FAKE, FAKE, ctypes.byref(o), None) == -1
-    # sketch wider than 64 columns is outside this build
+    # a sketch wider than 64 columns is not supported
     assert lib.sd_msign_deflated_ex(1, 256, 256, 60, 5, None, 0, FAKE, FAKE, None, None) == -2
     # the explicit restore needs at least one filter step
     o = sd.msign_opts(restore=sd.SD_RESTORE["explicit"])
