@@ -373,15 +373,18 @@ def main() -> int:
 
     sd.profile_reset()
     sd.profile_set("ns_update")
-    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # an event after every step on the call's stream: the per-step spread
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
+    marks[0].record()
+    for t in range(args.steps):
         step()
-    end.record()
+        marks[t + 1].record()
     torch.cuda.synchronize()
     sd.profile_set()
-    ms_total = start.elapsed_time(end)
+    ms_total = marks[0].elapsed_time(marks[-1])
+    per_step = sorted(marks[t].elapsed_time(marks[t + 1]) for t in range(args.steps))
+    pct = lambda q: per_step[min(len(per_step) - 1, int(round(q * (len(per_step) - 1))))]
     upd_ms, upd_n = sd.profile_read("ns_update")
     ms_per_step = ms_total / args.steps
     value = b * args.steps / (ms_total / 1e3)
@@ -408,6 +411,7 @@ def main() -> int:
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": ms_per_step,
+        "ms_per_step_p10_p50_p90": [pct(0.1), pct(0.5), pct(0.9)],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
