@@ -237,7 +237,15 @@ size_t sd_psd_workspace_bytes(int n, int k, const sd_psd_opts* opts);
  * eta_out: optional device float[iters], the eigenvalue-free KKT residual
  * after each iteration (the first three terms of eq:admm_eta). ndef_out:
  * optional device int[iters], the deflated count of each projection.
- * Scratch: opts->workspace of sd_admm_workspace_bytes(), or the pool. */
+ * The per-projection outputs of opts (n_deflated_out, n_positive_out,
+ * theta_out, ritz_out) are not used. Scratch: opts->workspace of
+ * sd_admm_workspace_bytes(), or the pool. The caller owns every buffer;
+ * the call is asynchronous on `stream`. Errors, returned with nothing
+ * enqueued: SD_ERR_INVALID_ARG for n < 1, iters < 0, warmup < 0, sigma <= 0,
+ * steps outside 0..1000,
+ * a null C, b, X, S or y, k < 0 or k >= n, k > 0 without Qwarm, a basis
+ * overlapping C or S, or invalid opts; SD_ERR_UNSUPPORTED for k > 64.
+ * iters = 0 validates and returns SD_OK. */
 int sd_admm_diag(int n, int iters, int steps, float sigma, const float* C, const float* b, float* X, float* S,
                  float* y, int k, float* Qwarm, int warmup, const sd_psd_opts* opts, float* eta_out, int* ndef_out,
                  hipStream_t stream);
