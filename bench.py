@@ -168,6 +168,16 @@ def _stage_time(sd, step, steps: int, stage: str) -> tuple[float, int]:
     return sd.profile_read(stage)
 
 
+def _filter_table(args):
+    """(steps, table, degree) of the PSD filter: 10 cubic Bjorck-Bowie steps,
+    or (--poly quintic7) 7 steps of the degree-5 map (15/8, -5/4, 3/8), the
+    shape of the paper's T = 7 degree-5 fp16 composite (whose own
+    coefficients are not printed)."""
+    if args.poly == "quintic7":
+        return 7, [(1.875, -1.25, 0.375)] * 7, 5
+    return 10, None, 3
+
+
 def other_workload(args) -> int:
     """Throughput of the configurations other than the benchmark line, each
     with the roofline of its dominant kernel: the bf16 iterate update (HBM)
@@ -246,7 +256,8 @@ def other_workload(args) -> int:
         # instances (planted-bisection random graph), tracked basis K = 64
         # (the widest Rayleigh-Ritz block the library solves), r = 32, tau = 0.1;
         # one step = 10 iterations with the gate open, continuing the state.
-        n, k, r, chunk, steps = 5000, 64, 32, 10, 10
+        n, k, r, chunk = 5000, 64, 32, 10
+        steps, table, degree = _filter_table(args)
         case = workloads.planted_maxcut(n, case_id=0)
         C = torch.from_numpy(case.c).to(dev)
         bvec = torch.from_numpy(case.b).to(dev)
@@ -257,18 +268,22 @@ def other_workload(args) -> int:
 
         def call():
             _, _, _, eta, ndef = sd.admm_diag(C, bvec, chunk, k, q, X=X, S=S, y=y, steps=steps, warmup=0,
-                                              tau=0.1, window=r, precision=args.precision)
+                                              tau=0.1, window=r, precision=args.precision, poly=table,
+                                              poly_degree=degree)
             last.update(eta=eta, ndef=ndef)
 
         ms = _timed(call, args.steps, args.warmup)
         roof = _psd_update_roofline(sd, call, args.steps, n, args.precision)
-        flops = chunk * (2.0 * n ** 3 * steps + 2.0 * n ** 3)
+        # per step: X^2 and the update (n^3 each, symmetric), plus A^2 for a quintic
+        flops = chunk * ((2.0 if degree == 3 else 3.0) * n ** 3 * steps + 2.0 * n ** 3)
         peak = 157.3 if args.precision == "f32" else MFMA_BF16_PEAK_TFLOPS
-        res = {"metric": f"ADMM iterations/s (max-cut SDP, n = {n}, K = {k}, {args.precision} filter products)",
+        res = {"metric": f"ADMM iterations/s (max-cut SDP, n = {n}, K = {k}, {steps} degree-{degree} steps, "
+                         f"{args.precision} filter products)",
                "value": chunk * 1e3 / ms, "unit": "iterations/s", "ms_per_step": ms,
                "tflops": flops / (ms / 1e3) / 1e12, "mfma_frac": flops / (ms / 1e3) / 1e12 / peak,
                "steps": args.steps, "warmup": args.warmup, "dtype": args.precision, "data": "synthetic",
                "config": {"workload": "admm", "n": n, "k": k, "window": r, "tau": 0.1, "filter_steps": steps,
+                          "filter_degree": degree,
                           "iterations_per_step": chunk, "final_eta": float(last["eta"][-1]),
                           "final_n_deflated": int(last["ndef"][-1])},
                "roofline": roof}
@@ -281,29 +296,33 @@ def other_workload(args) -> int:
         else:
             z, lam, _, q0 = workloads.config5_device(16384)
             n, k, steps, sub = 16384, 32, 10, 1
+        if args.poly != "cubic":
+            steps, table, degree = _filter_table(args)
+        else:
+            table, degree = None, 3
         q = q0.clone()
         out = torch.empty_like(z)
-        ws = torch.empty(sd.psd_workspace_bytes(n, k, precision=sd.SD_PREC[args.precision]), dtype=torch.uint8,
-                         device=dev)
+        ws = torch.empty(sd.psd_workspace_bytes(n, k, precision=sd.SD_PREC[args.precision], poly_degree=degree),
+                         dtype=torch.uint8, device=dev)
 
         def call():
             q.copy_(q0)   # every timed call starts from the same warm basis
             sd.psd_project(z, k, steps, q, subspace_iters=sub, gamma=1.1, out=out, workspace=ws,
-                           precision=args.precision)
+                           precision=args.precision, poly=table, poly_degree=degree)
 
         ms = _timed(call, args.steps, args.warmup)
         roof = _psd_update_roofline(sd, call, args.steps, n, args.precision)
         # cubic filter: X^2 and X X^2 are both symmetric and computed on upper-triangle
-        # tiles (n^3 each per step); the restore product R g is a full 2 n^3
-        flops = 2.0 * n ** 3 * steps + 2.0 * n ** 3
+        # tiles (n^3 each per step), a quintic adds A^2; the restore product R g is a full 2 n^3
+        flops = (2.0 if degree == 3 else 3.0) * n ** 3 * steps + 2.0 * n ** 3
         peak = 157.3 if args.precision == "f32" else MFMA_BF16_PEAK_TFLOPS   # fp16 dense = bf16 dense
-        res = {"metric": f"deflated PSD projections/s ({args.workload}: n = {n}, k = {k}, "
-                         f"{args.precision} filter products)",
+        res = {"metric": f"deflated PSD projections/s ({args.workload}: n = {n}, k = {k}, {steps} degree-{degree} "
+                         f"steps, {args.precision} filter products)",
                "value": 1e3 / ms, "unit": "projections/s", "ms_per_step": ms,
                "tflops": flops / (ms / 1e3) / 1e12, "mfma_frac": flops / (ms / 1e3) / 1e12 / peak,
                "steps": args.steps, "warmup": args.warmup, "dtype": args.precision, "data": "synthetic",
                "config": {"workload": args.workload, "n": n, "k": k, "filter_steps": steps,
-                          "subspace_iters": sub},
+                          "filter_degree": degree, "subspace_iters": sub},
                "roofline": roof}
     r = res["roofline"]
     log(f"bench {args.workload}: {res['ms_per_step']:.3f} ms per call, {res['value']:.1f} {res['unit']}, "
@@ -329,6 +348,9 @@ def main() -> int:
                          "(one JSON line each, no roofline or CPU baseline)")
     ap.add_argument("--precision", default="f32", choices=["f32", "f16"],
                     help="c4 / c5 / admm: arithmetic of the sign filter's products")
+    ap.add_argument("--poly", default="cubic", choices=["cubic", "quintic7"],
+                    help="c4 / c5 / admm: the filter: 10 cubic steps, or 7 steps of the degree-5 map "
+                         "(the shape of the paper's T = 7 fp16 composite)")
     ap.add_argument("--sequential", action="store_true",
                     help="c2-step / paper-step: one call per group on one stream instead of sd_msign_groups")
     args = ap.parse_args()

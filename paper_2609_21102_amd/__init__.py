@@ -346,7 +346,7 @@ def psd_project(X, k: int = 0, steps: int = 10, qwarm=None, *, subspace_iters: i
 
 def admm_diag(C, b, iters: int, k: int = 0, qwarm=None, *, X=None, S=None, y=None, steps: int = 10,
               sigma: float = 1.0, warmup: int = 100, tau: float = 0.1, window: int = 1, gamma: float = 1.1,
-              precision: str = "f32", seed: int = 0, stream=None):
+              precision: str = "f32", seed: int = 0, poly=None, poly_degree: int = 3, stream=None):
     """`iters` ADMM iterations (sd_admm_diag) for min <C, X> s.t. diag(X) = b,
     X PSD, continuing from X, S, y (zeros when None; updated in place).
     qwarm [n, k] is the tracked basis (updated in place). Returns
@@ -360,7 +360,11 @@ def admm_diag(C, b, iters: int, k: int = 0, qwarm=None, *, X=None, S=None, y=Non
     eta = torch.empty(max(iters, 1), dtype=torch.float32, device=dev)
     ndef = torch.empty(max(iters, 1), dtype=torch.int32, device=dev)
     # no tracked basis (k = 0): the undeflated projection, no gate
-    o = psd_opts(gamma=gamma, tau=tau if k > 0 else 0.0, window=window, precision=SD_PREC[precision], seed=seed)
+    o = psd_opts(gamma=gamma, tau=tau if k > 0 else 0.0, window=window, precision=SD_PREC[precision], seed=seed,
+                 poly_degree=poly_degree)
+    table, tptr = _host_table(poly, steps, (poly_degree + 1) // 2)
+    if tptr is not None:
+        o.poly = tptr.value
     rc = lib().sd_admm_diag(n, iters, steps, sigma, _ptr(C), _ptr(b), _ptr(X), _ptr(S), _ptr(y), k,
                             _ptr(qwarm) if k > 0 else None, warmup, ctypes.byref(o), _ptr(eta), _ptr(ndef),
                             _stream(stream))
