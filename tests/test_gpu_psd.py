@@ -284,6 +284,27 @@ def test_config4_f16():
     assert int(info["n_deflated"]) == oinfo.n_deflated
 
 
+def test_config4_f16_quintic_t7():
+    # The shape of the paper's SDP filter: T = 7 degree-5 steps in fp16 (the
+    # map (15/8, -5/4, 3/8); the paper's own composite is not printed). At
+    # n = 4096 the update runs on 256 x 256 tiles while the quintic's Gram and
+    # A^2 keep 128 x 128 (their fp32 A copy shares the tiling).
+    case = workloads.config4()
+    table = [(1.875, -1.25, 0.375)] * 7
+    z = torch.from_numpy(case.z).cuda()
+    q = torch.from_numpy(np.ascontiguousarray(case.qwarm)).cuda()
+    out, info = sd.psd_project(z, case.k, 7, q, subspace_iters=case.subspace_iters, gamma=case.gamma, info=True,
+                               poly=table, poly_degree=5, precision="f16")
+    torch.cuda.synchronize()
+    want, _, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm.astype(np.float64), steps=7,
+                                               table=table, gamma=case.gamma, subspace_iters=case.subspace_iters,
+                                               mode="f16")
+    err = rel_fro(host64(out), want)
+    say(f"config4 f16 quintic T=7: rel err {err:.3e}")
+    assert err < F16_TOL
+    assert int(info["n_deflated"]) == oinfo.n_deflated
+
+
 # fp32 ADMM: the 1e-4 fp32 contract. fp16 products: each projection meets
 # the fp16 contract's 1e-4 against the oracle (F16_TOL) and the iterations
 # add those differences up, so T iterations are held to T x 1e-4 (measured
