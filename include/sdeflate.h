@@ -54,7 +54,12 @@ typedef enum {
 enum { SD_DTYPE_F32 = 0, SD_DTYPE_BF16 = 1 };
 
 /* Bits set (atomically OR-ed) in *status_dev when the device meets them. */
-enum { SD_FLAG_PIVOT_FLOOR = 2 /* a CholeskyQR pivot hit its floor: a rank-deficient panel */ };
+enum {
+  SD_FLAG_PIVOT_FLOOR = 2,   /* a CholeskyQR pivot hit its floor: a rank-deficient panel */
+  SD_FLAG_RESIDUAL_FLOOR = 4 /* Muon: a residual at the head's rounding level was dropped
+                                (nu <= rho ||X||_F, rho = 2^-8 bf16, 2^-16 fp32; the
+                                degenerate case rank(X) <= k_eff) */
+};
 
 /* ------------------------------------------------------------------ Muon --
  * Deflated polar factor, batched (Alg. 1 with the batched randomized SVD of

@@ -25,6 +25,17 @@ exact split polar(M) = U_k V_k^T + polar(R_k), eq:identities in Sec. 1):
     X0 = R / nu (no head term),  return U_k V_k^T + N_L o ... o N_1 (X0).
 Degenerate scales (no epsilon is added, the paper has none): a zero nu or a
 zero ||A||_F drops that term (a zero matrix maps to zero).
+Residual floor (the degenerate case rank(A) <= k_eff): Sec. 2 notes that
+inexact triplets leave components of R along the head directions and pads
+the head at gamma^-1 against them; with exact triplets ||X0||_2 <= 1. When
+nu is itself at the rounding level of the head, those components are not
+small against nu and X0 can leave the filter's convergence interval. So a
+residual with nu <= rho ||A||_F, where ||A||_F^2 = sum_{j < k_eff} s_j^2 +
+nu^2 (U_k S_k V_k^T projects A on the head), is dropped like a zero one:
+X0 = gamma^-1 U_k V_k^T (padded) or 0 (explicit). rho is the resolution
+of the arithmetic that forms the head: 2^-8 for the bf16 contract (bf16
+sketch operands), 2^-16 for the float32 kernels that "exact" mode serves
+as the reference of.
 
 Modes: "exact" (float64 throughout) and "bf16" (the bf16 contract: the sketch
 products take bf16 operands Omega, Q and Y; X0 is formed wide, and X0 and the
@@ -43,6 +54,9 @@ from .precision import rounding
 from .rng import sketch
 
 
+RESIDUAL_FLOOR = {"exact": 2.0 ** -16, "bf16": 2.0 ** -8}
+
+
 @dataclass
 class MuonInfo:
     k_eff: list
@@ -50,6 +64,7 @@ class MuonInfo:
     s: list
     rprime: int
     transposed: bool
+    floored: list
 
 
 def tall_view(m: np.ndarray) -> tuple[np.ndarray, bool]:
@@ -84,33 +99,38 @@ def deflation_rank(s: np.ndarray, k: int, tau: float) -> int:
     return 0
 
 
-def deflated_init(a, u, s, v, k_eff, gamma, restore="padded"):
+def deflated_init(a, u, s, v, k_eff, gamma, restore="padded", rho=0.0):
     """Start X0 of Alg. 1 (padded: the head enters at gamma^-1) or of the
-    explicit restore (residual only), and the residual norm used."""
+    explicit restore (residual only), the residual norm, and whether the
+    residual fell to the floor rho ||A||_F and was dropped."""
     if k_eff == 0:
         nrm = float(np.linalg.norm(a))
         x0 = a / nrm if nrm > 0 else np.zeros_like(a)
-        return x0, nrm
+        return x0, nrm, False
     uk, sk, vk = u[:, :k_eff], s[:k_eff], v[:, :k_eff]
     r = a - (uk * sk) @ vk.T
     nu = float(np.linalg.norm(r))
-    x0 = r / nu if nu > 0 else np.zeros_like(r)
+    floored = nu <= rho * float(np.sqrt(np.sum(sk * sk) + nu * nu))
+    x0 = r / nu if nu > 0 and not floored else np.zeros_like(r)
     if restore == "padded":
         x0 = x0 + (uk @ vk.T) / gamma
-    return x0, nu
+    return x0, nu, floored
 
 
 def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
-                   tau=0.0, seed=0, mode="exact", sketches=None, restore="padded"):
+                   tau=0.0, seed=0, mode="exact", sketches=None, restore="padded", rho=None):
     """Deflated polar factor of every matrix of x [B, rows, cols] (float64
     values). coeffs: per-step table [L, 3]. Returns (out [B, rows, cols], info).
     sketches: optional list of Omega (m x r') overriding the generator.
     restore: "padded" (Alg. 1) or "explicit" (U_k V_k^T added after the
-    filter; gamma is then unused)."""
+    filter; gamma is then unused). rho: residual floor (default
+    RESIDUAL_FLOOR[mode]; 0 turns it off)."""
     if restore not in ("padded", "explicit"):
         raise ValueError(f"unknown restore {restore!r}")
+    if rho is None:
+        rho = RESIDUAL_FLOOR[mode]
     x = np.asarray(x, dtype=np.float64)
-    outs, keff, nus, svals = [], [], [], []
+    outs, keff, nus, svals, floors = [], [], [], [], []
     rprime = 0
     transposed = False
     for b in range(x.shape[0]):
@@ -124,7 +144,7 @@ def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
         else:
             u = s = v = None
             k_eff = 0
-        x0, nu = deflated_init(a, u, s, v, k_eff, gamma, restore)
+        x0, nu, floored = deflated_init(a, u, s, v, k_eff, gamma, restore, rho)
         xl = ns_filter(x0, coeffs, mode)
         if restore == "explicit" and k_eff > 0:
             xl = xl + u[:, :k_eff] @ v[:, :k_eff].T
@@ -133,7 +153,8 @@ def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
         keff.append(k_eff)
         nus.append(nu)
         svals.append(None if s is None else np.asarray(s))
-    return np.stack(outs), MuonInfo(keff, nus, svals, rprime, transposed)
+        floors.append(floored)
+    return np.stack(outs), MuonInfo(keff, nus, svals, rprime, transposed, floors)
 
 
 def msign(x, coeffs, *, mode="exact"):

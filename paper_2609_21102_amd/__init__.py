@@ -192,7 +192,8 @@ def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, po
     """(Deflated) polar factor of every matrix of x ([B, m, n] or [m, n], bf16 or
     float32, contiguous, on the GPU). k = 0 is the undeflated baseline.
     Returns out (same shape and dtype), and with info=True a dict of device
-    tensors k_eff [B], nu [B], s [B, k]. restore: "padded" (Alg. 1) or
+    tensors k_eff [B], nu [B], s [B, k] and status (int32 [1], the SD_FLAG_*
+    bits the call raised). restore: "padded" (Alg. 1) or
     "explicit" (U_k V_k^T added after the filter)."""
     import torch
     squeeze = x.dim() == 2
@@ -215,6 +216,7 @@ def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, po
     keff = torch.empty(b, dtype=torch.int32, device=dev) if info else None
     nu = torch.empty(b, dtype=torch.float32, device=dev) if info else None
     sv = torch.empty((b, max(k, 1)), dtype=torch.float32, device=dev) if info else None
+    status = torch.zeros(1, dtype=torch.int32, device=dev) if info else None
     o = msign_opts(oversample=oversample, power_iters=power_iters, gamma=gamma, tau=tau, seed=seed,
                    restore=SD_RESTORE[restore])
     if sketch is not None:
@@ -229,13 +231,14 @@ def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, po
         o.workspace_bytes = workspace.numel() * workspace.element_size()
     if info:
         o.k_eff_out, o.nu_out, o.s_out = keff.data_ptr(), nu.data_ptr(), sv.data_ptr()
+        o.status_dev = status.data_ptr()
     rc = lib().sd_msign_deflated_ex(b, m, n, k, steps, tptr, dtype, _ptr(xb), _ptr(out), ctypes.byref(o),
                                     _stream(stream))
     _check(rc, "sd_msign_deflated_ex")
     del table
     res = out[0] if squeeze else out
     if info:
-        return res, {"k_eff": keff, "nu": nu, "s": sv[:, :k]}
+        return res, {"k_eff": keff, "nu": nu, "s": sv[:, :k], "status": status}
     return res
 
 
@@ -326,8 +329,10 @@ def psd_project(X, k: int = 0, steps: int = 10, qwarm=None, *, subspace_iters: i
         res = {"n_deflated": torch.empty(1, dtype=torch.int32, device=dev),
                "n_positive": torch.empty(1, dtype=torch.int32, device=dev),
                "theta": torch.empty(1, dtype=torch.float32, device=dev),
-               "ritz": torch.empty(max(k, 1), dtype=torch.float32, device=dev)}
+               "ritz": torch.empty(max(k, 1), dtype=torch.float32, device=dev),
+               "status": torch.zeros(1, dtype=torch.int32, device=dev)}
         o.n_deflated_out = res["n_deflated"].data_ptr()
+        o.status_dev = res["status"].data_ptr()
         o.n_positive_out = res["n_positive"].data_ptr()
         o.theta_out = res["theta"].data_ptr()
         o.ritz_out = res["ritz"].data_ptr()

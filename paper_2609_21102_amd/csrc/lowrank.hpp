@@ -181,23 +181,35 @@ __global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
 // (1 / gamma = 0 for the explicit restore). With coef_one, also the restore
 // coefficients: 1 for the deflated components, 0 past them. One wave per
 // matrix.
+// Residual floor: with k_eff > 0, a residual with nu <= rho ||X||_F, where
+// ||X||_F^2 = sum_{j < k_eff} s_j^2 + nu^2 (U_k S_k V_k^T is the projection
+// of X on the head), is rounding of the head's arithmetic: its components
+// along the head directions are then not small against nu, and R / nu next
+// to the padded head can leave the filter's convergence interval. Such a
+// residual is dropped (alpha = 0: X0 = gamma^-1 L R^T, or 0 for the explicit
+// restore) and flag 4 is raised in status.
 static __global__ __launch_bounds__(64) void muon_finalize_kernel(const float* sumsq, int tiles, const float* sv,
                                                                   const int* keff, int kmax, float inv_gamma,
-                                                                  float* alpha, float* coef_b, float* nu_dev,
-                                                                  float* nu_user, float* coef_one, int batch) {
+                                                                  float rho, float* alpha, float* coef_b,
+                                                                  float* nu_dev, float* nu_user, float* coef_one,
+                                                                  int* status, int batch) {
   const int b = blockIdx.x, lane = threadIdx.x;
   double acc = 0.0;
   for (int t = lane; t < tiles; t += WAVE) acc += (double)sumsq[(long long)b * tiles + t];
   acc = wave_sum(acc);
   acc = __shfl(acc, 0, WAVE);
   const double nu = sqrt(acc);
-  const double inv = nu > 0.0 ? 1.0 / nu : 0.0;
+  const int ke = keff ? keff[b] : 0;
+  double head = 0.0;
+  for (int j = 0; j < ke; ++j) head += (double)sv[b * kmax + j] * (double)sv[b * kmax + j];
+  const bool floored = ke > 0 && nu <= (double)rho * sqrt(head + acc);
+  const double inv = (nu > 0.0 && !floored) ? 1.0 / nu : 0.0;
   if (lane == 0) {
     alpha[b] = (float)inv;
     nu_dev[b] = (float)nu;
     if (nu_user) nu_user[b] = (float)nu;
+    if (floored && status) atomicOr(status, 4);
   }
-  const int ke = keff ? keff[b] : 0;
   for (int j = lane; j < kmax; j += WAVE) {
     coef_b[b * kmax + j] = j < ke ? (float)(-((double)sv[b * kmax + j] * inv - (double)inv_gamma)) : 0.f;
     if (coef_one) coef_one[b * kmax + j] = j < ke ? 1.f : 0.f;

@@ -134,6 +134,16 @@ static void sym_gemm(const T* a, const GemmShape& g, const Epi& e, hipStream_t s
   else launch_gemm<CfgTile128, T, false, true>(a, a, g, e, st);
 }
 
+// Residual floor rho of the padded start, relative to ||X||_F: the
+// resolution of the arithmetic that forms the head. bf16 path: the sketch
+// products take bf16 operands (unit roundoff 2^-9), rho = 2^-8. fp32 path:
+// float32 products over up to thousands of terms and a one-pass CholeskyQR
+// whose orthogonality loss grows with kappa^2, rho = 2^-16 (256 u).
+template <typename T>
+constexpr float kResidualFloor = 0x1p-16f;
+template <>
+constexpr float kResidualFloor<bf16_t> = 0x1p-8f;
+
 template <typename T>
 static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opts& o, const T* in, T* out,
                      hipStream_t st) {
@@ -239,8 +249,8 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   {
     ProfScope ps(SD_STAGE_LOWRANK, st);
     hipLaunchKernelGGL(muon_finalize_kernel, dim3(B), dim3(64), 0, st, p.sumsq, p.tiles, p.sv,
-                       p.k > 0 ? p.keff : nullptr, la.kmax, p.explicit_restore ? 0.f : 1.f / o.gamma, p.alpha,
-                       p.coefB, p.nu, o.nu_out, p.coefR, B);
+                       p.k > 0 ? p.keff : nullptr, la.kmax, p.explicit_restore ? 0.f : 1.f / o.gamma,
+                       kResidualFloor<T>, p.alpha, p.coefB, p.nu, o.nu_out, p.coefR, o.status_dev, B);
   }
   la.coef = p.coefB;
   la.alpha = p.alpha;

@@ -254,6 +254,45 @@ def test_zero_matrix_and_in_place():
     assert torch.equal(ref, x)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_rank_deficient_input(dtype):
+    # rank(X) = 2 (the method's degenerate case rank <= k). With k = 2 the
+    # residual is rounding of the head only: it falls below the residual floor
+    # (flag 4), X0 = gamma^-1 U V^T, and the output matches the oracle, which
+    # drops it alike. With k = 4 the 12-column sketch panel has rank 2, so
+    # CholeskyQR raises pivots to their floor (flag 2); the two extra head
+    # directions are rounding, so only finiteness is checked there. A
+    # full-rank input raises no flag.
+    import dataclasses
+    base = workloads.small_muon(2, 64, 200, dtype=dtype, k=2, case_id=3)
+    x = workloads.low_rank(2, 64, 200, 2, case_id=1)
+    case = dataclasses.replace(base, x=workloads.to_bf16_bits(x) if dtype == "bf16" else x)
+    say(f"rank-deficient {dtype} k=2")
+    out, info = run_case(case)
+    assert int(info["status"][0]) & 4
+    want, oinfo = oracle_case(case)
+    assert oinfo.floored == [True, True]
+    if dtype == "f32":
+        assert rel_fro(host64(out), want) < F32_TOL
+    else:
+        # the bf16 bound is per unit singular value of a full-rank output
+        # (||out||_F = sqrt(q), q = 64); this output has two, so the error is
+        # taken against sqrt(q) rather than ||want||_F = sqrt(2) (measured:
+        # 3.6e-2 of sqrt(2), 6.4e-3 of sqrt(q))
+        assert np.linalg.norm(host64(out) - want) / np.sqrt(64 * 2) < BF16_TOL
+    say(f"rank-deficient {dtype} k=4")
+    out, info = run_case(case, k=4)
+    st = int(info["status"][0])
+    assert st & 4
+    # bf16 rounding of the input leaves the panel of full numerical rank
+    # (trailing pivots near (2^-9)^2 tr(Gram), far above the floor)
+    assert dtype == "bf16" or st & 2
+    assert bool(torch.isfinite(out).all())
+    say(f"full-rank {dtype}")
+    out, info = run_case(workloads.small_muon(2, 64, 200, dtype=dtype, k=4, bulk=(1e-2, 1.0), case_id=2))
+    assert int(info["status"][0]) == 0
+
+
 def test_caller_workspace():
     case = workloads.small_muon(2, 128, 256, dtype="bf16", k=4)
     x = dev_tensor(case.x, "bf16")

@@ -60,8 +60,8 @@ def test_example1_toy_spectrum():
     u, v = haar(rng, 7, 5), haar(rng, 5, 5)
     m = (u * sig) @ v.T
     table = [bjorck_bowie(2)] * gold["steps"]
-    x_base, nrm = muon.deflated_init(m, None, None, None, 0, 1.0)
-    x_def, nu = muon.deflated_init(m, u, sig, v, gold["deflated_rank"], gold["gamma"])
+    x_base, nrm, _ = muon.deflated_init(m, None, None, None, 0, 1.0)
+    x_def, nu, _ = muon.deflated_init(m, u, sig, v, gold["deflated_rank"], gold["gamma"])
     got = {
         "frobenius_norm": nrm,
         "baseline_floor_start": np.linalg.svd(x_base, compute_uv=False).min(),
@@ -111,7 +111,7 @@ def test_short_side_gram_equals_literal_map():
 def test_classical_map_converges_to_polar():
     rng = np.random.default_rng(11)
     m = rng.standard_normal((40, 25))
-    x0, _ = muon.deflated_init(m, None, None, None, 0, 1.0)
+    x0, _, _ = muon.deflated_init(m, None, None, None, 0, 1.0)
     got = ns_filter(x0, [bjorck_bowie(2)] * 40)
     np.testing.assert_allclose(got, muon.polar_exact(m), atol=1e-10)
 
@@ -126,8 +126,8 @@ def test_theorem1_bounds(d, gamma):
     u, v = haar(rng, n, mm), haar(rng, mm, mm)
     m = (u * sig) @ v.T
     target = muon.polar_exact(m)
-    x_base, nrm = muon.deflated_init(m, None, None, None, 0, gamma)
-    x_def, nu = muon.deflated_init(m, u, sig, v, k, gamma)
+    x_base, nrm, _ = muon.deflated_init(m, None, None, None, 0, gamma)
+    x_def, nu, _ = muon.deflated_init(m, u, sig, v, k, gamma)
     ell = sig[-1] / nrm
     alpha = nrm / nu
     phi = min(alpha * ell, 1.0 / gamma)

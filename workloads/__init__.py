@@ -291,6 +291,20 @@ def small_psd(n, *, k=8, n_dom=4, dom=(50.0, 200.0), subspace_iters=2, steps=10,
                     gamma, ids=(200, case_id, n, k), eps=eps)
 
 
+def low_rank(b: int, m: int, n: int, rank: int, case_id: int = 0) -> np.ndarray:
+    """float32 [b, m, n] of exact rank `rank` (U diag(s) V^T, s = 10, 5, ...,
+    U and V orthonormal from Gaussian QR): a degenerate input whose sketch
+    panels are rank-deficient once the sketch is wider than the rank."""
+    rng = rng_for(700, case_id, m, n, rank)
+    out = np.empty((b, m, n), dtype=np.float32)
+    for i in range(b):
+        u, _ = np.linalg.qr(rng.standard_normal((m, rank)))
+        v, _ = np.linalg.qr(rng.standard_normal((n, rank)))
+        sv = 10.0 * 0.5 ** np.arange(rank)
+        out[i] = ((u * sv) @ v.T).astype(np.float32)
+    return out
+
+
 def sym_gaussian(n: int, case_id: int = 0) -> np.ndarray:
     """Seeded symmetric Gaussian matrix (G + G^T) / sqrt(2), float32, exactly
     symmetric (a semicircle spectrum of radius about 2 sqrt(n))."""
