@@ -91,6 +91,36 @@ def test_zero_matrix():
     assert torch.count_nonzero(sd.psd_project(z, 0, 10)) == 0
 
 
+@pytest.mark.parametrize("precision", ["f32", "f16"])
+def test_rank_deficient(precision):
+    # rank(Z) = 3 < K = 8 with a cold orthonormal basis and two block steps:
+    # the panel Z V has rank 3, so CholeskyQR raises pivots to their floor
+    # (flag 2) and five Ritz pairs are rounding. Their sign is arbitrary, but
+    # their eigenvalues are too: the residual is at the rounding level and
+    # the output is the exact projection sum_{lambda > 0} lambda u u^T to
+    # float32 rounding, on both sides; the three true Ritz values match the
+    # oracle's.
+    g = np.random.default_rng(5)
+    n, k = 130, 8
+    u, _ = np.linalg.qr(g.standard_normal((n, 3)))
+    z = ((u * np.array([5.0, -3.0, 2.0])) @ u.T).astype(np.float32)
+    z = np.triu(z) + np.triu(z, 1).T
+    v0 = np.linalg.qr(g.standard_normal((n, k)))[0].astype(np.float32)
+    say(f"psd rank-deficient {precision}")
+    out, info = sd.psd_project(torch.from_numpy(z).cuda(), k, 10, torch.from_numpy(v0).cuda(), subspace_iters=2,
+                               gamma=1.1, info=True, precision=precision)
+    torch.cuda.synchronize()
+    assert int(info["status"][0]) & 2
+    want, _, oinfo = opsd.psd_project_deflated(z.astype(np.float64), v0.astype(np.float64), subspace_iters=2,
+                                               gamma=1.1, mode="exact" if precision == "f32" else "f16")
+    exact = opsd.psd_exact(z.astype(np.float64))
+    assert rel_fro(host64(out), exact) < TOL
+    assert rel_fro(host64(out), want) < TOL
+    np.testing.assert_allclose(info["ritz"].cpu().numpy()[:3], oinfo.ritz[:3], rtol=1e-5)
+    o = out.cpu().numpy()
+    assert np.isfinite(o).all() and np.array_equal(o, o.T)
+
+
 @pytest.mark.slow
 def test_config4_full():
     case = workloads.config4()
