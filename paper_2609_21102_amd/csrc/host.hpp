@@ -239,7 +239,10 @@ template <typename TX, typename TO>
 void lowrank(const LowRankArgs& a, hipStream_t st) {
   ProfScope ps(SD_STAGE_LOWRANK, st);
   const dim3 g((a.rows_pad / 128) * (a.cols_pad / 128) * a.batch), b(256);
-  if (a.kmax <= 16) hipLaunchKernelGGL((lowrank_kernel<TX, TO, 16>), g, b, 0, st, a);
+  if (a.kmax <= 16) {
+    if constexpr (sizeof(TX) == 2) hipLaunchKernelGGL((lowrank_kernel<TX, TO, 16, 4>), g, b, 0, st, a);
+    else hipLaunchKernelGGL((lowrank_kernel<TX, TO, 16>), g, b, 0, st, a);
+  }
   else if (a.kmax <= 32) hipLaunchKernelGGL((lowrank_kernel<TX, TO, 32>), g, b, 0, st, a);
   else hipLaunchKernelGGL((lowrank_kernel<TX, TO, 64>), g, b, 0, st, a);
 }

@@ -80,9 +80,12 @@ struct Raw8<float> {
 };
 
 // 128 x 128 tile per work-group; thread t owns rows 8 (t / 16) .. +7 and
-// columns 8 (t % 16) .. +7.
-template <typename TX, typename TO, int KM>
-__global__ __launch_bounds__(256) void lowrank_kernel(LowRankArgs a) {
+// columns 8 (t % 16) .. +7. WPE: minimum waves per SIMD the register
+// allocation must allow (4 for the bf16 passes of the Muon start, which
+// would otherwise take 130 registers and three waves: the passes are bound
+// by the X loads in flight, and a fourth work-group per CU adds a third).
+template <typename TX, typename TO, int KM, int WPE = 1>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void lowrank_kernel(LowRankArgs a) {
   __shared__ __attribute__((aligned(16))) float ls[KM][128];
   __shared__ __attribute__((aligned(16))) float rs[KM][128];
   __shared__ float red[4];
