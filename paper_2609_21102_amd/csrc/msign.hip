@@ -208,8 +208,7 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
       gram_partials(p.ys, so, s_pad, p.ys, so, s_pad, rp, rp, s_pad, true, p.part, B, st);   // G G^T
 #define SD_HEAD(NPV)                                                                                       \
   hipLaunchKernelGGL(svd_head_kernel<NPV>, dim3(B), dim3(SM_THREADS), 0, st, p.part, s_pad / GP_CHUNK, rp, p.k, \
-                     o.tau, p.E, p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out, p.ys, so, s_pad, p.yl, sl_,  \
-                     l_pad, p.Ls, p.Ll)
+                     o.tau, p.E, p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out)
       switch (jacobi_class(rp)) {
         case 4: SD_HEAD(4); break;
         case 8: SD_HEAD(8); break;
@@ -219,6 +218,16 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
         default: SD_HEAD(0); break;
       }
 #undef SD_HEAD
+      const dim3 gf(((s_pad + l_pad + 255) / 256) * B);
+      if (rp <= 16)
+        hipLaunchKernelGGL(head_factors_kernel<16>, gf, dim3(256), 0, st, p.E, p.invsv, rp, p.k, p.ys, so, s_pad,
+                           p.yl, sl_, l_pad, p.Ls, p.Ll);
+      else if (rp <= 32)
+        hipLaunchKernelGGL(head_factors_kernel<32>, gf, dim3(256), 0, st, p.E, p.invsv, rp, p.k, p.ys, so, s_pad,
+                           p.yl, sl_, l_pad, p.Ls, p.Ll);
+      else
+        hipLaunchKernelGGL(head_factors_kernel<SM_MAX>, gf, dim3(256), 0, st, p.E, p.invsv, rp, p.k, p.ys, so,
+                           s_pad, p.yl, sl_, l_pad, p.Ls, p.Ll);
     }
   } else if (o.k_eff_out) {
     hipLaunchKernelGGL(fill_int_kernel, grid1(B, 256), dim3(256), 0, st, o.k_eff_out, (long long)B, 0);

@@ -708,54 +708,17 @@ __global__ __launch_bounds__(128) void chol_qr_kernel(float* Pt, long long sp, i
 }
 
 // ----------------------------------------------- thin SVD of G (Alg. 3) ---
-// out[j][x] = scale[j] * sum_{a < rp} es[a][j] P[a][x] (j < k, x < len), by
-// the whole work-group in float32, the terms added in order of a. es holds RM
-// rows (rows rp .. RM - 1 zero), so every read is unconditional: each thread
-// loads the panel values of PB positions, and a factor's RM coefficients,
-// before it uses any of them.
-template <int RM>
-__device__ __forceinline__ void rotate_panel(const float* P, int ldp, int len, int rp, int k, const float* es,
-                                             const float* scale, float* out, int ldo) {
-  constexpr int PB = RM <= 16 ? 64 / RM : 1;
-  for (int x0 = threadIdx.x; x0 < len; x0 += PB * SM_THREADS) {
-    float v[PB][RM];
-#pragma unroll
-    for (int i = 0; i < PB; ++i) {
-      const int x = x0 + i * SM_THREADS;
-#pragma unroll
-      for (int r = 0; r < RM; ++r) v[i][r] = (r < rp && x < len) ? P[(long long)r * ldp + x] : 0.f;
-    }
-    for (int j = 0; j < k; ++j) {
-      float ev[RM];
-#pragma unroll
-      for (int r = 0; r < RM; ++r) ev[r] = es[r * k + j];
-      const float sc = scale ? scale[j] : 1.f;
-#pragma unroll
-      for (int i = 0; i < PB; ++i) {
-        const int x = x0 + i * SM_THREADS;
-        float acc = 0.f;
-#pragma unroll
-        for (int r = 0; r < RM; ++r) acc += ev[r] * v[i][r];
-        if (x < len) out[(long long)j * ldo + x] = scale ? sc * acc : acc;
-      }
-    }
-  }
-}
-
 // From the partials of H = G G^T (G = Q^T A, rp x s), in float64: eigen-
 // decompose H, order the eigenvalues decreasingly, and emit for the leading
 // k: singular values, the eigenvector matrix E (rp x k), 1/s (0 for s = 0),
-// the deflation rank (fixed k, or the gate of Alg. 1 when tau > 0) with the
-// subtraction coefficients -s_j used by the residual pass, and the factors
-// V = G^T E / s (k x s_pad, from the G^T panel Gt) and U = Q E (k x l_pad,
-// from the Q panel Qt). One work-group per matrix; NP = jacobi_class(rp).
+// the deflation rank (fixed k, or the gate of Alg. 1 when tau > 0) and the
+// subtraction coefficients -s_j used by the residual pass. One work-group
+// per matrix; NP = jacobi_class(rp). The factors U and V follow in
+// head_factors_kernel.
 template <int NP>
 __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part, int nch, int rp, int k, float tau,
                                                               float* E, float* sv, float* inv_sv, int* keff,
-                                                              float* coef_a, float* s_user, int* keff_user,
-                                                              const float* Gt, long long sg, int s_pad,
-                                                              const float* Qt, long long sq, int l_pad, float* Vt,
-                                                              float* Ut) {
+                                                              float* coef_a, float* s_user, int* keff_user) {
   __shared__ SmallLds s;
   const int tid = threadIdx.x, b = blockIdx.x;
   gram_reduce(s, part + (long long)b * nch * gram_items(rp, rp, true), nch, rp, rp, true);
@@ -765,14 +728,9 @@ __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part
   if (tid < rp) s.key[tid] = s.h[tid][tid];
   __syncthreads();
   sort_desc(s, rp);
-  constexpr int RM = NP > 0 ? 2 * NP : SM_MAX;
-  float* es = reinterpret_cast<float*>(&s.h2[0][0]);   // E as float32, [RM][k] (rows past rp zero)
-  float* isv = es + RM * k;                            // 1/s as float32
-  for (int e = tid; e < RM * k; e += SM_THREADS) {
+  for (int e = tid; e < rp * k; e += SM_THREADS) {
     const int a = e / k, j = e - a * k;
-    const float v = a < rp ? (float)s.e[a][s.perm[j]] : 0.f;
-    if (a < rp) E[(long long)b * rp * k + e] = v;
-    es[e] = v;
+    E[(long long)b * rp * k + e] = (float)s.e[a][s.perm[j]];
   }
   if (tid < k) {
     const double lam = s.h[s.perm[tid]][s.perm[tid]];
@@ -798,13 +756,48 @@ __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part
     const float inv = sj > 0.0 ? (float)(1.0 / sj) : 0.f;
     sv[b * k + tid] = (float)sj;
     inv_sv[b * k + tid] = inv;
-    isv[tid] = inv;
     coef_a[b * k + tid] = tid < ke ? -(float)sj : 0.f;
     if (s_user) s_user[b * k + tid] = (float)sj;
   }
+}
+
+// The head factors V = G^T E / s (k x s_pad, from the G^T panel Gt) and
+// U = Q E (k x l_pad, from the Q panel Qt) of every matrix, from the E
+// (rp x k, row-major) and 1/s of svd_head_kernel. One position per thread:
+// the V positions, then the U positions, over ceil((s_pad + l_pad) / 256)
+// work-groups per matrix, so both panels stream at full width (on the head
+// kernel's single work-group per matrix this product took 16 us of its 65 at
+// 24 x 768 x 3072). Each output sums its rp terms in row order. RM >= rp.
+template <int RM>
+__global__ __launch_bounds__(256) void head_factors_kernel(const float* __restrict__ E,
+                                                           const float* __restrict__ inv_sv, int rp, int k,
+                                                           const float* __restrict__ Gt, long long sg, int s_pad,
+                                                           const float* __restrict__ Qt, long long sq, int l_pad,
+                                                           float* __restrict__ Vt, float* __restrict__ Ut) {
+  __shared__ float es[RM * SM_MAX];
+  __shared__ float isv[SM_MAX];
+  const int per = (s_pad + l_pad + 255) / 256;
+  const int b = blockIdx.x / per;
+  const int x0 = (blockIdx.x - b * per) * 256 + threadIdx.x;
+  const bool valid = x0 < s_pad + l_pad, vside = x0 < s_pad;
+  const int x = !valid ? 0 : (vside ? x0 : x0 - s_pad);
+  const float* P = vside ? Gt + b * sg : Qt + b * sq;
+  const int ld = vside ? s_pad : l_pad;
+  float v[RM];
+#pragma unroll
+  for (int r = 0; r < RM; ++r) v[r] = P[(long long)(r < rp ? r : rp - 1) * ld + x];
+  for (int e = threadIdx.x; e < rp * k; e += 256) es[e] = E[(long long)b * rp * k + e];
+  for (int j = threadIdx.x; j < k; j += 256) isv[j] = inv_sv[b * k + j];
   __syncthreads();
-  rotate_panel<RM>(Gt + b * sg, s_pad, s_pad, rp, k, es, isv, Vt + (long long)b * k * s_pad, s_pad);
-  rotate_panel<RM>(Qt + b * sq, l_pad, l_pad, rp, k, es, nullptr, Ut + (long long)b * k * l_pad, l_pad);
+  if (!valid) return;
+  float* out = (vside ? Vt + (long long)b * k * s_pad : Ut + (long long)b * k * l_pad) + x;
+  for (int j = 0; j < k; ++j) {
+    float acc = 0.f;
+#pragma unroll
+    for (int r = 0; r < RM; ++r)
+      if (r < rp) acc += es[r * k + j] * v[r];
+    out[(long long)j * ld] = vside ? isv[j] * acc : acc;
+  }
 }
 
 // ------------------------------------------- Rayleigh-Ritz (Alg. 2) -------
