@@ -24,23 +24,17 @@ Explicit restore (restore="explicit", the gamma -> infinity form of the
 exact split polar(M) = U_k V_k^T + polar(R_k), eq:identities in Sec. 1):
     X0 = R / nu (no head term),  return U_k V_k^T + N_L o ... o N_1 (X0).
 Degenerate scales (no epsilon is added, the paper has none): a zero nu or a
-zero ||A||_F drops that term (a zero matrix maps to zero).
-Residual floor (the degenerate case rank(A) <= k_eff): Sec. 2 notes that
-inexact triplets leave components of R along the head directions and pads
-the head at gamma^-1 against them; with exact triplets ||X0||_2 <= 1. When
-nu is itself at the rounding level of the head, those components are not
-small against nu and X0 can leave the filter's convergence interval. So a
-residual with nu <= rho ||A||_F, where ||A||_F^2 = sum_{j < k_eff} s_j^2 +
-nu^2 (U_k S_k V_k^T projects A on the head), is dropped like a zero one:
-X0 = gamma^-1 U_k V_k^T (padded) or 0 (explicit). rho is the resolution
-of the arithmetic that forms the head: 2^-8 for the bf16 contract (bf16
-sketch operands), 2^-16 for the float32 kernels that "exact" mode serves
-as the reference of.
+zero ||A||_F drops that term (a zero matrix maps to zero). Alg. 1 requires
+k < rank(M); no other rule applies to nu.
 
-Modes: "exact" (float64 throughout) and "bf16" (the bf16 contract: the sketch
-products take bf16 operands Omega, Q and Y; X0 is formed wide, and X0 and the
-iterates are stored as bf16 hi plus an e4m3 residual, hi being every filter
-product's operand (filters.ns_filter); the output is rounded to bf16).
+Modes: "exact" (float64 throughout) and "bf16" (the bf16 contract). In the
+bf16 contract the front end (randomized SVD, residual, start) is single
+precision or better, as the paper runs its randomized SVD in single
+precision (App. D, accuracy study); the oracle computes it in float64, so
+it equals exact mode there. The filter then follows filters.ns_filter's
+contract: every product takes bf16 operands, X0 and the iterates are stored
+as bf16 hi plus an e4m3 residual (hi is the operand), and the output is
+rounded to bf16.
 """
 from __future__ import annotations
 
@@ -54,8 +48,6 @@ from .precision import rounding
 from .rng import sketch
 
 
-RESIDUAL_FLOOR = {"exact": 2.0 ** -16, "bf16": 2.0 ** -8}
-
 
 @dataclass
 class MuonInfo:
@@ -64,7 +56,6 @@ class MuonInfo:
     s: list
     rprime: int
     transposed: bool
-    floored: list
 
 
 def tall_view(m: np.ndarray) -> tuple[np.ndarray, bool]:
@@ -74,77 +65,78 @@ def tall_view(m: np.ndarray) -> tuple[np.ndarray, bool]:
     return m.T, True
 
 
-def randomized_svd(a, r, rprime, power_iters, omega, mode="exact"):
+def randomized_svd(a, r, rprime, power_iters, omega):
     """Alg. 3 for one tall matrix a (n x m). Returns U (n x r), s (r), V (m x r)."""
-    rd = rounding(mode)
-    q = cholqr(a @ rd(omega))
+    q = cholqr(a @ omega)
     for _ in range(power_iters):
-        y = cholqr(a.T @ rd(q))
-        q = cholqr(a @ rd(y))
-    g = rd(q).T @ a
+        y = cholqr(a.T @ q)
+        q = cholqr(a @ y)
+    g = q.T @ a
     ug, s, vt = np.linalg.svd(g, full_matrices=False)
     u = q @ ug
     return u[:, :r], s[:r], vt.T[:, :r]
 
 
-def deflation_rank(s: np.ndarray, k: int, tau: float) -> int:
-    """Number of deflated components: k in fixed-rank mode, the gate of
-    Alg. 1 on the k estimated values otherwise."""
+def deflation_rank(s: np.ndarray, k: int, tau: float, r: int | None = None) -> int:
+    """Number of deflated components: k in fixed-rank mode; with tau > 0 the
+    gate of Alg. 1 over the first r estimated values (window, default k):
+    when s_r < tau s_1 it deflates max{i : s_i > tau s_1} of them (fewer
+    than r), capped at k; otherwise none."""
     if k == 0:
         return 0
     if tau <= 0.0:
         return k
-    if s[k - 1] < tau * s[0]:
-        return int(np.count_nonzero(s[:k] > tau * s[0]))
+    r = k if r is None else r
+    if s[r - 1] < tau * s[0]:
+        return min(k, int(np.count_nonzero(s[:r] > tau * s[0])))
     return 0
 
 
-def deflated_init(a, u, s, v, k_eff, gamma, restore="padded", rho=0.0):
+def deflated_init(a, u, s, v, k_eff, gamma, restore="padded"):
     """Start X0 of Alg. 1 (padded: the head enters at gamma^-1) or of the
-    explicit restore (residual only), the residual norm, and whether the
-    residual fell to the floor rho ||A||_F and was dropped."""
+    explicit restore (residual only), and the residual norm."""
     if k_eff == 0:
         nrm = float(np.linalg.norm(a))
         x0 = a / nrm if nrm > 0 else np.zeros_like(a)
-        return x0, nrm, False
+        return x0, nrm
     uk, sk, vk = u[:, :k_eff], s[:k_eff], v[:, :k_eff]
     r = a - (uk * sk) @ vk.T
     nu = float(np.linalg.norm(r))
-    floored = nu <= rho * float(np.sqrt(np.sum(sk * sk) + nu * nu))
-    x0 = r / nu if nu > 0 and not floored else np.zeros_like(r)
+    x0 = r / nu if nu > 0 else np.zeros_like(r)
     if restore == "padded":
         x0 = x0 + (uk @ vk.T) / gamma
-    return x0, nu, floored
+    return x0, nu
 
 
 def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
-                   tau=0.0, seed=0, mode="exact", sketches=None, restore="padded", rho=None):
+                   tau=0.0, seed=0, mode="exact", sketches=None, restore="padded", window=None):
     """Deflated polar factor of every matrix of x [B, rows, cols] (float64
     values). coeffs: per-step table [L, 3]. Returns (out [B, rows, cols], info).
     sketches: optional list of Omega (m x r') overriding the generator.
     restore: "padded" (Alg. 1) or "explicit" (U_k V_k^T added after the
-    filter; gamma is then unused). rho: residual floor (default
-    RESIDUAL_FLOOR[mode]; 0 turns it off)."""
+    filter; gamma is then unused). window: the gate's window r (Alg. 1;
+    used only with tau > 0, default k): r triplets are estimated and the
+    gate deflates k_eff = min(k, max{i : s_i > tau s_1}) of them when
+    s_r < tau s_1."""
     if restore not in ("padded", "explicit"):
         raise ValueError(f"unknown restore {restore!r}")
-    if rho is None:
-        rho = RESIDUAL_FLOOR[mode]
     x = np.asarray(x, dtype=np.float64)
-    outs, keff, nus, svals, floors = [], [], [], [], []
+    outs, keff, nus, svals = [], [], [], []
+    r = k if (tau <= 0.0 or not window) else int(window)
     rprime = 0
     transposed = False
     for b in range(x.shape[0]):
         a, transposed = tall_view(x[b])
         m = a.shape[1]
         if k > 0:
-            rprime = min(m, k + oversample)
+            rprime = min(m, r + oversample)
             omega = sketches[b] if sketches is not None else sketch(seed, b, m, rprime)
-            u, s, v = randomized_svd(a, k, rprime, power_iters, omega, mode)
-            k_eff = deflation_rank(s, k, tau)
+            u, s, v = randomized_svd(a, r, rprime, power_iters, omega)
+            k_eff = deflation_rank(s, k, tau, r)
         else:
             u = s = v = None
             k_eff = 0
-        x0, nu, floored = deflated_init(a, u, s, v, k_eff, gamma, restore, rho)
+        x0, nu = deflated_init(a, u, s, v, k_eff, gamma, restore)
         xl = ns_filter(x0, coeffs, mode)
         if restore == "explicit" and k_eff > 0:
             xl = xl + u[:, :k_eff] @ v[:, :k_eff].T
@@ -153,8 +145,7 @@ def msign_deflated(x, k, coeffs, *, oversample=8, power_iters=1, gamma=1.01,
         keff.append(k_eff)
         nus.append(nu)
         svals.append(None if s is None else np.asarray(s))
-        floors.append(floored)
-    return np.stack(outs), MuonInfo(keff, nus, svals, rprime, transposed, floors)
+    return np.stack(outs), MuonInfo(keff, nus, svals, rprime, transposed)
 
 
 def msign(x, coeffs, *, mode="exact"):

@@ -60,8 +60,8 @@ def test_example1_toy_spectrum():
     u, v = haar(rng, 7, 5), haar(rng, 5, 5)
     m = (u * sig) @ v.T
     table = [bjorck_bowie(2)] * gold["steps"]
-    x_base, nrm, _ = muon.deflated_init(m, None, None, None, 0, 1.0)
-    x_def, nu, _ = muon.deflated_init(m, u, sig, v, gold["deflated_rank"], gold["gamma"])
+    x_base, nrm = muon.deflated_init(m, None, None, None, 0, 1.0)
+    x_def, nu = muon.deflated_init(m, u, sig, v, gold["deflated_rank"], gold["gamma"])
     got = {
         "frobenius_norm": nrm,
         "baseline_floor_start": np.linalg.svd(x_base, compute_uv=False).min(),
@@ -111,7 +111,7 @@ def test_short_side_gram_equals_literal_map():
 def test_classical_map_converges_to_polar():
     rng = np.random.default_rng(11)
     m = rng.standard_normal((40, 25))
-    x0, _, _ = muon.deflated_init(m, None, None, None, 0, 1.0)
+    x0, _ = muon.deflated_init(m, None, None, None, 0, 1.0)
     got = ns_filter(x0, [bjorck_bowie(2)] * 40)
     np.testing.assert_allclose(got, muon.polar_exact(m), atol=1e-10)
 
@@ -126,8 +126,8 @@ def test_theorem1_bounds(d, gamma):
     u, v = haar(rng, n, mm), haar(rng, mm, mm)
     m = (u * sig) @ v.T
     target = muon.polar_exact(m)
-    x_base, nrm, _ = muon.deflated_init(m, None, None, None, 0, gamma)
-    x_def, nu, _ = muon.deflated_init(m, u, sig, v, k, gamma)
+    x_base, nrm = muon.deflated_init(m, None, None, None, 0, gamma)
+    x_def, nu = muon.deflated_init(m, u, sig, v, k, gamma)
     ell = sig[-1] / nrm
     alpha = nrm / nu
     phi = min(alpha * ell, 1.0 / gamma)
@@ -150,3 +150,117 @@ def test_theorem1_bounds(d, gamma):
         assert ed <= bound * eb + 1e-12
         if L > 0:
             assert ed < eb
+
+
+# --- bf16 contract of the filter (ns_step / ns_filter, mode "bf16") --------------
+# The contract's rounding points, one step on a stored iterate x:
+#   (a) the product operand is hi = bf16(x) (both factors of G, and the right
+#       factor of B hi);
+#   (b) the iterate is carried as hi + e4m3(clip((x - hi) 2^16)) 2^-16, and
+#       the linear term a x takes that carried value;
+#   (c) the operand of G^2 is bf16(G) (the linear term b G keeps G wide);
+#   (d) B = bf16(b G + c G^2) is the product operand of the update.
+# On a diagonal iterate every product is scalar, so each rounding point can be
+# checked against a scalar computation that rounds with torch's own bfloat16
+# and float8_e4m3fn conversions (a library independent of the oracle's
+# rounding code). torch converts float64 through float32, which equals direct
+# rounding unless the float32 value lands exactly on a tie of the target
+# format; the reference checks that it does not (or that the value is exact
+# in float32).
+def _torch_round(x, dtype):
+    import torch
+    x = np.asarray(x, dtype=np.float64)
+    x32 = x.astype(np.float32)
+    exact = x32.astype(np.float64) == x
+
+    def rnd(v):
+        return torch.from_numpy(np.asarray(v, dtype=np.float32)).to(dtype).to(torch.float64).numpy()
+    # a float32 value strictly between two ties rounds like its neighbours
+    lo = rnd(np.nextafter(x32, np.float32(-np.inf)))
+    hi = rnd(np.nextafter(x32, np.float32(np.inf)))
+    assert np.all(exact | (lo == hi)), "float32 rounding landed on a tie of the target format"
+    return torch.from_numpy(x).to(dtype).to(torch.float64).numpy()
+
+
+def _scalar_contract_step(x, coeffs, drop=None):
+    """One bf16-contract step on the diagonal entries x, with rounding point
+    `drop` left out ("a_operand", "b_residual_none", "b_residual_full",
+    "c_gram_operand", "d_poly")."""
+    import torch
+    a, b, c = (float(v) for v in coeffs)
+    hi = _torch_round(x, torch.bfloat16)
+    res = np.clip((x - hi) * 2.0 ** 16, -448.0, 448.0)
+    carried = hi + _torch_round(res, torch.float8_e4m3fn) * 2.0 ** -16
+    if drop == "b_residual_none":
+        carried = hi
+    elif drop == "b_residual_full":
+        carried = x
+    op = carried if drop == "a_operand" else hi
+    g = op * op
+    gop = g if drop == "c_gram_operand" else _torch_round(g, torch.bfloat16)
+    bw = b * g + c * gop * gop
+    bb = bw if drop == "d_poly" else _torch_round(bw, torch.bfloat16)
+    return a * carried + bb * op
+
+
+DROPS = ["a_operand", "b_residual_none", "b_residual_full", "c_gram_operand", "d_poly"]
+
+
+def test_bf16_contract_step_known_answer_and_each_rounding_point_is_applied():
+    # float32 entries whose bf16 residuals are nonzero and inside e4m3's
+    # normal range, so every rounding point changes some entry
+    x = np.array([0.7, -0.3, 1.05, 0.013, 0.4375, -0.9], dtype=np.float32).astype(np.float64)
+    coeffs = (1.875, -1.25, 0.375)       # few-bit coefficients keep the reference float32-exact
+    want = _scalar_contract_step(x, coeffs)
+    # ns_filter stores the state (a, b) and calls ns_step, which applies (c, d)
+    got = ns_filter(np.diag(x), [coeffs], "bf16")
+    np.testing.assert_array_equal(np.diag(got), want)
+    assert np.count_nonzero(got - np.diag(np.diag(got))) == 0
+    for drop in DROPS:
+        alt = _scalar_contract_step(x, coeffs, drop)
+        assert np.max(np.abs(alt - want)) > 1e-6, f"dropping {drop} left the step unchanged"
+
+
+def test_bf16_contract_two_steps_muon_coefficients():
+    # Muon's quintic (float32 coefficients) over two steps: the second step
+    # starts from the stored form of the first one's result
+    x = np.array([0.61, -0.27, 0.95, 0.05], dtype=np.float32).astype(np.float64)
+    table = np.array([filters.MUON_QUINTIC] * 2, dtype=np.float32).astype(np.float64)
+    y1 = _scalar_contract_step(x, table[0])
+    np.testing.assert_array_equal(np.diag(ns_filter(np.diag(x), table[:1], "bf16")), y1)
+    np.testing.assert_array_equal(np.diag(ns_filter(np.diag(x), table, "bf16")),
+                                  _scalar_contract_step(y1, table[1]))
+
+
+def test_bf16_contract_is_exact_on_dyadic_input():
+    # Entries and coefficients on a coarse dyadic grid keep every operand,
+    # product and polynomial value exactly representable in bf16 and the
+    # state exactly representable as hi plus an e4m3 residual: the contract
+    # must then equal exact arithmetic bit for bit (no rounding point rounds
+    # to a coarser grid or is applied to a wide value inexactly).
+    quintic = np.diag([0.5, -0.25, 1.0, 0.0, -0.5])
+    np.testing.assert_array_equal(ns_filter(quintic, [(1.875, -1.25, 0.375)], "bf16"),
+                                  ns_filter(quintic, [(1.875, -1.25, 0.375)]))
+    cubic = np.diag([1.0, 0.0, -1.0, 0.5, -0.5, 0.75])
+    for table in ([(1.5, -0.5, 0.0)], [(1.5, -0.5, 0.0)] * 2):
+        if len(table) == 2:
+            cubic = cubic[:5, :5]    # 0.75 leaves a 12-bit Gram after one step
+        np.testing.assert_array_equal(ns_filter(cubic, table, "bf16"), ns_filter(cubic, table))
+
+
+def test_bf16_contract_commutes_with_signed_permutations_and_transpose():
+    # Every rounding is elementwise, so for X = P D Q^T with signed
+    # permutations P, Q the contract gives P f(D) Q^T exactly, on the tall
+    # and the wide orientation alike (short-side Gram on both).
+    rng = np.random.default_rng(3)
+    d = np.array([0.81, -0.33, 0.57, 0.12, 0.98], dtype=np.float32).astype(np.float64)
+    table = np.array([filters.MUON_QUINTIC] * 3, dtype=np.float32).astype(np.float64)
+    fd = np.diag(ns_filter(np.diag(d), table, "bf16"))
+    for rows, cols in ((5, 9), (9, 5)):
+        p = np.eye(rows)[rng.permutation(rows)] * rng.choice([-1.0, 1.0], rows)
+        q = np.eye(cols)[rng.permutation(cols)] * rng.choice([-1.0, 1.0], cols)
+        dd = np.zeros((rows, cols))
+        dd[:5, :5] = np.diag(d)
+        ff = np.zeros((rows, cols))
+        ff[:5, :5] = np.diag(fd)
+        np.testing.assert_array_equal(ns_filter(p @ dd @ q.T, table, "bf16"), p @ ff @ q.T)

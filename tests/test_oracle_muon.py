@@ -79,7 +79,7 @@ def test_exact_deflation_preserves_target(gamma):
     # eq:identities: polar(R/||R|| + gamma^-1 U_k V_k^T) = polar(M) for exact triplets.
     g = np.random.default_rng(1)
     a, u, sig, v = spiked(g, 40, 20, [30, 10, 4])
-    x0, _, _ = muon.deflated_init(a, u, sig, v, 3, gamma)
+    x0, _ = muon.deflated_init(a, u, sig, v, 3, gamma)
     np.testing.assert_allclose(muon.polar_exact(x0), muon.polar_exact(a), atol=1e-12)
 
 
@@ -128,62 +128,41 @@ def test_pipeline_with_exact_head_matches_scalarized_closed_form():
     np.testing.assert_allclose(info.nu[0], nu, rtol=1e-12)
 
 
-def test_residual_floor_threshold():
-    # A = U diag(10, 5) V^T + t N with N orthogonal to both head spaces and
-    # ||N||_F = 1, exact triplets: nu = t and ||A||_F = sqrt(125 + t^2). The
-    # residual is dropped iff t <= rho ||A||_F; at t = 0.9 rho sqrt(125) it
-    # is (it would not be against s_1 = 10, or against the head alone at
-    # 0.999), at t = 1.1 rho sqrt(125) it is kept.
-    g = np.random.default_rng(23)
-    n, m, rho = 40, 10, 1e-3
-    u, v = haar(g, n, m), haar(g, m, m)
-    sig = np.array([10.0, 5.0])
-    head = (u[:, :2] * sig) @ v[:, :2].T
-    nmat = u[:, 2:] @ g.standard_normal((m - 2, m - 2)) @ v[:, 2:].T
-    nmat /= np.linalg.norm(nmat)
-    for frac, want in ((0.9, True), (0.999, True), (1.1, False)):
-        t = frac * rho * np.sqrt(125.0)
-        x0, nu, floored = muon.deflated_init(head + t * nmat, u, sig, v, 2, 1.01, "padded", rho)
-        assert floored is want
-        np.testing.assert_allclose(nu, t, rtol=1e-9)
-        if want:
-            np.testing.assert_allclose(x0, u[:, :2] @ v[:, :2].T / 1.01, atol=1e-14)
-        else:
-            np.testing.assert_allclose(np.linalg.norm(x0 - u[:, :2] @ v[:, :2].T / 1.01), 1.0, rtol=1e-9)
+def test_tail_far_below_the_spike_is_kept():
+    # Alg. 1 as written has no floor on nu: a full-rank input whose tail sits
+    # 1e-6 below the spike (64 x 200, spike 1e6 over a tail in [1e-2, 1],
+    # k = 1) keeps its tail. The deflated output is full rank and close to
+    # polar(M); the undeflated filter cannot resolve the tail at all.
+    g = np.random.default_rng(5)
+    m, n = 64, 200
+    sig = np.concatenate([[1e6], np.sort(10 ** g.uniform(-2, 0, m - 1))[::-1]])
+    a = (haar(g, m, m) * sig) @ haar(g, n, m).T
+    table = [filters.MUON_QUINTIC] * 5
+    target = muon.polar_exact(a[None])[0]
+    out, info = muon.msign_deflated(a[None], 1, table, power_iters=2)
+    sv = np.linalg.svd(out[0], compute_uv=False)
+    assert sv.min() > 0.3 and np.linalg.matrix_rank(out[0]) == m
+    err = np.linalg.norm(out[0] - target) / np.linalg.norm(target)
+    base = muon.msign(a[None], table)[0]
+    err_base = np.linalg.norm(base - target) / np.linalg.norm(target)
+    assert err < 0.2 < 0.9 < err_base
+    np.testing.assert_allclose(info.nu[0], np.linalg.norm(sig[1:]), rtol=1e-6)
 
 
-@pytest.mark.parametrize("mode", ["exact", "bf16"])
-def test_rank_deficient_input_drops_rounding_residual(mode):
-    # rank(M) = k = 2 (Sec. 2's degenerate case): the residual is rounding
-    # only, so it falls below the floor, X0 = gamma^-1 U_k V_k^T, and the
-    # output is p^L(1/gamma) U_2 V_2^T (explicit restore: U_2 V_2^T). Without
-    # the floor the bf16 contract's start overshoots the filter's
-    # convergence interval (||X0||_2 about 1.86 here) and overflows.
-    x = workloads.low_rank(1, 64, 200, 2, case_id=1).astype(np.float64)
-    table = [[3.4445, -4.7750, 2.0315]] * 5
-    ut, sv, vt = np.linalg.svd(x[0].T, full_matrices=False)   # tall view 200 x 64
-    polar2 = ut[:, :2] @ vt[:2]
-    # bf16: the contract's product rounding over 5 steps, as for any input
-    # (3e-2, the bound of the bf16-contract closeness pin below)
-    tol = 1e-9 if mode == "exact" else 3e-2
-    out, info = muon.msign_deflated(x, 2, table, mode=mode)
-    assert info.floored == [True] and info.k_eff == [2]
-    want = scalar_compose(np.array([1 / 1.01]), table)[0] * polar2.T
-    assert np.linalg.norm(out[0] - want) / np.linalg.norm(want) < tol
-    out, info = muon.msign_deflated(x, 2, table, mode=mode, restore="explicit")
-    assert np.linalg.norm(out[0] - polar2.T) / np.linalg.norm(polar2) < tol
-    if mode == "bf16":
-        with np.errstate(all="ignore"):
-            raw, _ = muon.msign_deflated(x, 2, table, mode=mode, rho=0.0)
-        assert not np.isfinite(raw).all()
-
-
-def test_residual_floor_off_for_spread_spectra():
-    # Spectra with a bulk under the spikes keep their residual in both modes.
-    case = workloads.small_muon(2, 64, 200, k=4, bulk=(1e-2, 1.0), case_id=2)
-    for mode in ("exact", "bf16"):
-        _, info = muon.msign_deflated(case.x64, 4, case.coeffs, mode=mode)
-        assert info.floored == [False, False]
+def test_gate_window_separate_from_k():
+    # Alg. 1's gate over a window of r estimated values, capped at k.
+    s = np.array([10.0, 5.0, 2.0, 1.5, 0.5, 0.2])
+    assert muon.deflation_rank(s, 6, 0.1, r=6) == 4       # s_6 < 1: the four values above 1
+    assert muon.deflation_rank(s, 2, 0.1, r=6) == 2       # capped at k
+    assert muon.deflation_rank(s, 6, 0.1, r=4) == 0       # s_4 = 1.5 >= 1: no fire
+    assert muon.deflation_rank(s, 3, 0.1) == 0            # window defaults to k
+    # through the pipeline: a window of 6 sketched values deflates the 3 spikes
+    case = workloads.small_muon(1, 60, 150, k=6, spikes=[50, 30, 20, 1.0, 0.9, 0.8], bulk=(1e-3, 0.5),
+                                case_id=44)
+    _, info = muon.msign_deflated(case.x64, 2, case.coeffs, tau=0.1, window=6)
+    assert info.k_eff == [2] and info.rprime == 14
+    _, info = muon.msign_deflated(case.x64, 6, case.coeffs, tau=0.1, window=6)
+    assert info.k_eff == [3]
 
 
 def test_explicit_restore_matches_scalarized_closed_form():
