@@ -113,9 +113,14 @@ typedef struct {
   size_t workspace_bytes;
   int* k_eff_out;          /* optional device int[batch]: deflated components */
   float* nu_out;           /* optional device float[batch]: norm X0 was scaled by */
-  float* s_out;            /* optional device float[batch][k]: estimated singular values */
+  float* s_out;            /* optional device float[batch][r]: estimated singular values
+                              (r = window when the gate's window is set, else k) */
   int* status_dev;         /* optional device int: SD_FLAG_* bits are OR-ed in */
   int restore;             /* SD_RESTORE_PADDED (default) or SD_RESTORE_EXPLICIT */
+  int window;              /* gate window r of Alg. 1, used only with tau > 0: 0 (default) = k;
+                              else 1 <= r <= min(m, n): r values are estimated (r' = min(min(m,n),
+                              r + oversample)) and the gate deflates min(k, max{i : s_i > tau s_1})
+                              of them when s_r < tau s_1 */
 } sd_msign_opts;
 
 void sd_msign_opts_default(sd_msign_opts* opts);
@@ -192,10 +197,19 @@ int sd_sketch_host(int batch, int s, int rp, uint64_t seed, float* out);
 /* Arithmetic of the sign filter's products (the paper's SDP experiments run
  * the filter in fp16, App. E): SD_PREC_F32 computes them in float32 (fp32
  * MFMA); SD_PREC_F16 rounds every product operand to fp16 (round to nearest
- * even) and accumulates in float32 (fp16 MFMA). The iterate, the Gram and
- * b A + c A^2 are stored in float32 either way, and the residual, the Lanczos
- * scale and the restore product stay float32. */
+ * even) and accumulates in float32 (fp16 MFMA), the restore product R g
+ * included, whose operands are fp16(R / theta) and fp16(g) (scaled back by
+ * theta). The iterate, the Gram and b A + c A^2 are stored in float32 either
+ * way, and the residual, the Ritz step and the Lanczos scale stay float32. */
 enum { SD_PREC_F32 = 0, SD_PREC_F16 = 1 };
+
+/* Normalization scale theta of the residual (X0 = R / theta + ...):
+ * SD_SCALE_LANCZOS (default): the Lanczos upper estimate of ||R||_2 of
+ *   App. E.1 (lanczos_steps steps on R^2 from the seeded start);
+ * SD_SCALE_FROBENIUS: theta = ||R||_F (>= ||R||_2, no iteration), the residual
+ *   Frobenius-normalized as Alg. 1 normalizes the Muon residual; it lowers the
+ *   floor of X0's spectrum by up to sqrt(n) against the Lanczos scale. */
+enum { SD_SCALE_LANCZOS = 0, SD_SCALE_FROBENIUS = 1 };
 
 typedef struct {
   int subspace_iters;      /* J >= 1, default 1 */
@@ -214,6 +228,7 @@ typedef struct {
   float* ritz_out;         /* optional device float[k], Ritz values in deflation order */
   int* status_dev;         /* optional device int */
   int precision;           /* SD_PREC_F32 (default) or SD_PREC_F16, see below */
+  int scale_mode;          /* SD_SCALE_LANCZOS (default) or SD_SCALE_FROBENIUS, see below */
 } sd_psd_opts;
 
 void sd_psd_opts_default(sd_psd_opts* opts);

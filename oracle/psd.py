@@ -27,6 +27,9 @@ Deflated projection (Alg. 2), one call:
 g is the Newton-Schulz composition (filters.ns_filter) with a per-step
 coefficient table; the default is the cubic Bjorck-Bowie map (3/2, -1/2).
 A zero theta drops the R / theta term.
+scale "frobenius" replaces the Lanczos estimate by theta = ||R||_F (or
+||Z||_F undeflated), an upper bound on ||R||_2 that needs no iteration: the
+residual is then Frobenius-normalized, as Alg. 1 normalizes its residual.
 fp16 mode (the fp16 projection of the paper's SDP runs): every product of the
 filter stage takes fp16 operands, the restore product R g included, whose
 operands are R / theta (entries in [-1, 1], since theta >= ||R||_2) and g,
@@ -92,11 +95,21 @@ def ritz_order(lam: np.ndarray) -> np.ndarray:
     return np.lexsort((idx, -lam, -np.abs(lam)))
 
 
+def residual_scale(r: np.ndarray, scale: str, seed: int, lanczos_steps: int) -> float:
+    """theta: the Lanczos upper estimate of ||R||_2 (App. E.1) or ||R||_F."""
+    if scale == "lanczos":
+        return lanczos_scale(lambda x: r @ (r @ x), r.shape[0], seed, lanczos_steps)
+    if scale == "frobenius":
+        return float(np.linalg.norm(r))
+    raise ValueError(f"unknown scale {scale!r}")
+
+
 def psd_project_deflated(z, basis, *, table=None, steps=10, gamma=1.1, tau=0.0,
-                         window=0, subspace_iters=1, seed=0, lanczos_steps=20, mode="exact"):
+                         window=0, subspace_iters=1, seed=0, lanczos_steps=20, mode="exact",
+                         scale="lanczos"):
     """Alg. 2. z: symmetric (n x n); basis: orthonormal (n x K).
     mode: the sign filter's arithmetic, "exact" or "f16" (filters.ns_filter).
-    Returns (P, V_next, info)."""
+    scale: "lanczos" (App. E.1) or "frobenius". Returns (P, V_next, info)."""
     z = np.asarray(z, dtype=np.float64)
     v = np.asarray(basis, dtype=np.float64)
     n, kk = v.shape
@@ -119,14 +132,14 @@ def psd_project_deflated(z, basis, *, table=None, steps=10, gamma=1.1, tau=0.0,
     if n_def > 0:
         ui, li = u[:, :n_def], lam[:n_def]
         res = z - (ui * li) @ ui.T
-        theta = lanczos_scale(lambda x: res @ (res @ x), n, seed, lanczos_steps)
+        theta = residual_scale(res, scale, seed, lanczos_steps)
         x0 = (res / theta if theta > 0 else np.zeros_like(res)) \
             + (ui * np.sign(li)) @ ui.T / gamma
         g = ns_filter(x0, table, mode)
         p = 0.5 * (res + restore_product(res, g, theta, mode)) + (ui * np.maximum(li, 0.0)) @ ui.T
         n_pos = int(np.count_nonzero(li > 0))
     else:
-        theta = lanczos_scale(lambda x: z @ (z @ x), n, seed, lanczos_steps)
+        theta = residual_scale(z, scale, seed, lanczos_steps)
         x0 = z / theta if theta > 0 else np.zeros_like(z)
         g = ns_filter(x0, table, mode)
         p = 0.5 * (z + restore_product(z, g, theta, mode))
@@ -135,11 +148,11 @@ def psd_project_deflated(z, basis, *, table=None, steps=10, gamma=1.1, tau=0.0,
     return p, cholqr(zt), PSDInfo(n_def, n_pos, theta, lam)
 
 
-def psd_project(z, *, table=None, steps=10, seed=0, lanczos_steps=20, mode="exact"):
+def psd_project(z, *, table=None, steps=10, seed=0, lanczos_steps=20, mode="exact", scale="lanczos"):
     """Undeflated baseline projection (eq:baseline_projection), symmetrized."""
     z = np.asarray(z, dtype=np.float64)
     table = [CUBIC] * steps if table is None else table
-    theta = lanczos_scale(lambda x: z @ (z @ x), z.shape[0], seed, lanczos_steps)
+    theta = residual_scale(z, scale, seed, lanczos_steps)
     x0 = z / theta if theta > 0 else np.zeros_like(z)
     g = ns_filter(x0, table, mode)
     p = 0.5 * (z + restore_product(z, g, theta, mode))

@@ -27,6 +27,7 @@ SD_DTYPE_F32 = 0
 SD_DTYPE_BF16 = 1
 SD_RESTORE = {"padded": 0, "explicit": 1}
 SD_PREC = {"f32": 0, "f16": 1}
+SD_SCALE = {"lanczos": 0, "frobenius": 1}
 MUON_QUINTIC = (3.4445, -4.7750, 2.0315)
 
 _c_int_p = ctypes.POINTER(ctypes.c_int)
@@ -48,6 +49,7 @@ class MsignOpts(ctypes.Structure):
         ("s_out", ctypes.c_void_p),
         ("status_dev", ctypes.c_void_p),
         ("restore", ctypes.c_int),
+        ("window", ctypes.c_int),
     ]
 
 
@@ -84,6 +86,7 @@ class PsdOpts(ctypes.Structure):
         ("ritz_out", ctypes.c_void_p),
         ("status_dev", ctypes.c_void_p),
         ("precision", ctypes.c_int),
+        ("scale_mode", ctypes.c_int),
     ]
 
 
@@ -188,13 +191,14 @@ def psd_opts(**kw) -> PsdOpts:
 
 def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, power_iters: int = 1,
           gamma: float = 1.01, tau: float = 0.0, seed: int = 0, sketch=None, out=None, workspace=None,
-          restore: str = "padded", info: bool = False, stream=None):
+          restore: str = "padded", window: int = 0, info: bool = False, stream=None):
     """(Deflated) polar factor of every matrix of x ([B, m, n] or [m, n], bf16 or
     float32, contiguous, on the GPU). k = 0 is the undeflated baseline.
     Returns out (same shape and dtype), and with info=True a dict of device
-    tensors k_eff [B], nu [B], s [B, k] and status (int32 [1], the SD_FLAG_*
-    bits the call raised). restore: "padded" (Alg. 1) or
-    "explicit" (U_k V_k^T added after the filter)."""
+    tensors k_eff [B], nu [B], s [B, r] (r = window when tau > 0 and window > 0,
+    else k) and status (int32 [1], the SD_FLAG_* bits the call raised).
+    restore: "padded" (Alg. 1) or "explicit" (U_k V_k^T added after the
+    filter). window: the gate's window r (tau > 0)."""
     import torch
     squeeze = x.dim() == 2
     xb = x.unsqueeze(0) if squeeze else x
@@ -215,13 +219,14 @@ def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, po
     dev = xb.device
     keff = torch.empty(b, dtype=torch.int32, device=dev) if info else None
     nu = torch.empty(b, dtype=torch.float32, device=dev) if info else None
-    sv = torch.empty((b, max(k, 1)), dtype=torch.float32, device=dev) if info else None
+    kw = window if (tau > 0 and window > 0 and k > 0) else k
+    sv = torch.empty((b, max(kw, 1)), dtype=torch.float32, device=dev) if info else None
     status = torch.zeros(1, dtype=torch.int32, device=dev) if info else None
     o = msign_opts(oversample=oversample, power_iters=power_iters, gamma=gamma, tau=tau, seed=seed,
-                   restore=SD_RESTORE[restore])
+                   restore=SD_RESTORE[restore], window=window)
     if sketch is not None:
         s_ = min(m, n)
-        rp = min(s_, k + oversample)
+        rp = min(s_, kw + oversample)
         if (not sketch.is_cuda or sketch.dtype != torch.float32 or not sketch.is_contiguous()
                 or tuple(sketch.shape) != (b, rp, s_)):
             raise ValueError(f"sketch must be a contiguous float32 CUDA tensor of shape {(b, rp, s_)}")
@@ -238,7 +243,7 @@ def msign(x, k: int = 0, steps: int = 5, coeffs=None, *, oversample: int = 8, po
     del table
     res = out[0] if squeeze else out
     if info:
-        return res, {"k_eff": keff, "nu": nu, "s": sv[:, :k], "status": status}
+        return res, {"k_eff": keff, "nu": nu, "s": sv[:, :kw], "status": status}
     return res
 
 
@@ -246,7 +251,7 @@ def msign_groups(groups, *, stream=None):
     """One Muon step over several shape groups (sd_msign_groups): groups is a
     list of dicts with keys x ([B, m, n] bf16 or float32 CUDA tensor), k,
     steps, and optionally coeffs, out, oversample, power_iters, gamma, tau,
-    seed, restore. The groups run concurrently inside the library; returns the list of
+    seed, window, restore. The groups run concurrently inside the library; returns the list of
     outputs."""
     import torch
     n = len(groups)
@@ -268,7 +273,8 @@ def msign_groups(groups, *, stream=None):
         out = g.get("out")
         out = torch.empty_like(x) if out is None else out
         table, tptr = _host_table(g.get("coeffs"), steps, 3)
-        o = msign_opts(**{key: g[key] for key in ("oversample", "power_iters", "gamma", "tau", "seed") if key in g})
+        o = msign_opts(**{key: g[key] for key in ("oversample", "power_iters", "gamma", "tau", "seed", "window")
+                          if key in g})
         o.restore = SD_RESTORE[g.get("restore", "padded")]
         keep += [table, o]
         arr[i] = MsignGroup(b, m, nn, int(g.get("k", 0)), steps, tptr.value if tptr is not None else None, dtype,
@@ -302,11 +308,12 @@ def msign_workspace_bytes(batch, m, n, k, dtype=SD_DTYPE_BF16, **kw) -> int:
 def psd_project(X, k: int = 0, steps: int = 10, qwarm=None, *, subspace_iters: int = 1,
                 lanczos_steps: int = 20, gamma: float = 1.1, tau: float = 0.0, window: int = 1,
                 poly=None, poly_degree: int = 3, seed: int = 0, precision: str = "f32", out=None,
-                workspace=None, info: bool = False, stream=None):
+                workspace=None, info: bool = False, scale: str = "lanczos", stream=None):
     """(Deflated) projection of the symmetric float32 X [n, n] onto the PSD cone.
     qwarm [n, k] (float32) is the warm-start basis and is overwritten with the
     next basis. precision: "f32", or "f16" (the sign filter's products take
-    fp16 operands). Returns out, and with info=True a dict of device tensors
+    fp16 operands). scale: "lanczos" (App. E.1) or "frobenius" (theta =
+    ||R||_F). Returns out, and with info=True a dict of device tensors
     n_deflated, n_positive, theta, ritz."""
     import torch
     if X.dim() != 2 or X.shape[0] != X.shape[1] or X.dtype != torch.float32 or not X.is_contiguous():
@@ -318,7 +325,8 @@ def psd_project(X, k: int = 0, steps: int = 10, qwarm=None, *, subspace_iters: i
     table, tptr = _host_table(poly, steps, width)
     dev = X.device
     o = psd_opts(subspace_iters=subspace_iters, lanczos_steps=lanczos_steps, gamma=gamma, tau=tau,
-                 window=window, poly_degree=poly_degree, seed=seed, precision=SD_PREC[precision])
+                 window=window, poly_degree=poly_degree, seed=seed, precision=SD_PREC[precision],
+                 scale_mode=SD_SCALE[scale])
     if tptr is not None:
         o.poly = tptr.value
     if workspace is not None:

@@ -478,6 +478,42 @@ struct EpiStoreRows {
   }
 };
 
+// Product of a split-operand panel (the bf16 tall-skinny products of float32
+// panels): the A operand holds panel row j < split twice, as hi in row j and
+// lo in row split + j, and the whole M range is one tile. The kernel adds the
+// partner row's values to every row below split (SPLIT), so output row j is
+// the sum of the pair; rows split .. rows_out - 1 are written as zero and
+// rows from rows_out on are not stored.
+struct EpiStoreRowsSplit {
+  static constexpr bool PRE = false;
+  static constexpr bool ROWWISE = true;
+  static constexpr bool HI_FROM_B = false;
+  static constexpr bool SPLIT = true;
+  float* out;
+  long long stride;
+  int ld;
+  int split, rows_out;
+  __device__ void pre8(int, int, int, u32x4_t&, u32x4_t&) const {}
+  __device__ void apply8(int b, int r, int c0, const float (&v)[8], const u32x4_t&, const u32x4_t&,
+                         float (&)[8]) const {
+    if (r >= rows_out) return;
+    float* p = out + b * stride + (long long)r * ld + c0;
+    const bool keep = r < split;
+    *reinterpret_cast<f32x4_t*>(p) = keep ? f32x4_t{v[0], v[1], v[2], v[3]} : f32x4_t{};
+    *reinterpret_cast<f32x4_t*>(p + 4) = keep ? f32x4_t{v[4], v[5], v[6], v[7]} : f32x4_t{};
+  }
+};
+
+// Epilogues that sum split row pairs declare SPLIT = true.
+template <typename E, typename = void>
+struct EpiSplit {
+  static constexpr bool value = false;
+};
+template <typename E>
+struct EpiSplit<E, std::void_t<decltype(E::SPLIT)>> {
+  static constexpr bool value = E::SPLIT;
+};
+
 // ------------------------------------------------------- staging ----------
 // Tile configuration: NWM x NWN waves, each computing WM x WN MFMA blocks of
 // 32 x 32, so a work-group owns a (32 WM NWM) x (32 WN NWN) tile of C.
@@ -1079,6 +1115,13 @@ __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* 
       const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(ct + r * RW_LD + c8);
       const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(ct + r * RW_LD + c8 + 4);
       float av[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+      if constexpr (EpiSplit<Epi>::value) {
+        // one M tile (m0 = 0): row r's partner r + split is in this tile
+        if (r < epi.split) {
+#pragma unroll
+          for (int q = 0; q < 8; ++q) av[q] += ct[(r + epi.split) * RW_LD + c8 + q];
+        }
+      }
       if (diag) {
 #pragma unroll
         for (int q = 0; q < 8; ++q)

@@ -143,55 +143,63 @@ inline void fill(float* p, long long n, float v, hipStream_t st) {
 }
 
 // ----------------------------------------------------------- dispatch -----
-template <typename T>
+template <typename T, bool ACC64 = false>
 void ts_xtw(const T* X, long long sx, int ldx, int s_pad, int l_pad, const float* Wt, long long sw, int ldw,
             int rp, float* Pt, long long sp, int ldp, int batch, hipStream_t st) {
   ProfScope ps(SD_STAGE_SKETCH, st);
   const dim3 g((l_pad / 128) * batch), b(256);
   switch (cdiv(rp, 16)) {
-    case 1: hipLaunchKernelGGL((ts_xtw_kernel<T, 1>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
-    case 2: hipLaunchKernelGGL((ts_xtw_kernel<T, 2>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
-    case 3: hipLaunchKernelGGL((ts_xtw_kernel<T, 3>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
-    default: hipLaunchKernelGGL((ts_xtw_kernel<T, 4>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 1: hipLaunchKernelGGL((ts_xtw_kernel<T, 1, ACC64>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 2: hipLaunchKernelGGL((ts_xtw_kernel<T, 2, ACC64>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 3: hipLaunchKernelGGL((ts_xtw_kernel<T, 3, ACC64>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    default: hipLaunchKernelGGL((ts_xtw_kernel<T, 4, ACC64>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
   }
 }
 
-template <typename T>
+template <typename T, bool ACC64 = false>
 void ts_xw(const T* X, long long sx, int ldx, int s_pad, int l_pad, const float* Wt, long long sw, int ldw,
            int rp, float* Pt, long long sp, int ldp, int batch, hipStream_t st) {
   ProfScope ps(SD_STAGE_SKETCH, st);
   const dim3 g((s_pad / 16) * batch), b(256);
   switch (cdiv(rp, 16)) {
-    case 1: hipLaunchKernelGGL((ts_xw_kernel<T, 1>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
-    case 2: hipLaunchKernelGGL((ts_xw_kernel<T, 2>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
-    case 3: hipLaunchKernelGGL((ts_xw_kernel<T, 3>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
-    default: hipLaunchKernelGGL((ts_xw_kernel<T, 4>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 1: hipLaunchKernelGGL((ts_xw_kernel<T, 1, ACC64>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 2: hipLaunchKernelGGL((ts_xw_kernel<T, 2, ACC64>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    case 3: hipLaunchKernelGGL((ts_xw_kernel<T, 3, ACC64>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
+    default: hipLaunchKernelGGL((ts_xw_kernel<T, 4, ACC64>), g, b, 0, st, X, sx, ldx, s_pad, l_pad, Wt, sw, ldw, rp, Pt, sp, ldp, batch); break;
   }
 }
 
-// bf16 tall-skinny products on the direct-to-LDS GEMM. Panels have rq rows
-// (32 or 64; rows past the sketch width are zero) of bf16 operands (W16) and
-// fp32 results (Pt), [batch][rq][len_pad].
-//   ts_xtw_dma:  Pt = (X^T W)^T = W^T X       (M = rq, N = l_pad, K = s_pad, X in NN form)
-//   ts_xw_dma:   Pt = (X W)^T   = W^T X^T     (M = rq, N = s_pad, K = l_pad, X rows in NT form)
-inline void ts_xtw_dma(const bf16_t* X, long long sx, int ldx, int s_pad, int l_pad, const bf16_t* W16, int rq,
-                       float* Pt, int batch, hipStream_t st) {
+// bf16 tall-skinny products on the direct-to-LDS GEMM. The operand panel W16
+// holds each of the rp panel rows split in two bf16 rows, hi = bf16(w) in row
+// j and lo = bf16(w - hi) in row rp + j (zero rows up to rq16), so that with
+// the exact bf16 X the product of a float32 panel is formed to about 2^-17 of
+// its value instead of bf16's 2^-9; the epilogue adds each row pair. Results
+// are fp32 panels Pt [batch][rq][len_pad] (rows rp .. rq - 1 written as zero).
+//   ts_xtw_dma:  Pt = (X^T W)^T = W^T X       (M = rq16, N = l_pad, K = s_pad, X in NN form)
+//   ts_xw_dma:   Pt = (X W)^T   = W^T X^T     (M = rq16, N = s_pad, K = l_pad, X rows in NT form)
+inline void ts_xtw_dma(const bf16_t* X, long long sx, int ldx, int s_pad, int l_pad, const bf16_t* W16, int rq16,
+                       int rp, float* Pt, int rq, int batch, hipStream_t st) {
   ProfScope ps(SD_STAGE_SKETCH, st);
-  GemmShape g{rq, l_pad, s_pad, s_pad, ldx, (long long)rq * s_pad, sx, batch};
-  EpiStoreRows e{Pt, (long long)rq * l_pad, l_pad};
-  if (rq == 32) launch_gemm_dma<GemmCfg<1, 4, 1, 1, 2, 0>, true, false>(W16, X, g, e, st);
-  else launch_gemm_dma<GemmCfg<1, 4, 2, 1, 2, 0>, true, false>(W16, X, g, e, st);
+  GemmShape g{rq16, l_pad, s_pad, s_pad, ldx, (long long)rq16 * s_pad, sx, batch};
+  EpiStoreRowsSplit e{Pt, (long long)rq * l_pad, l_pad, rp, rq};
+  if (rq16 == 32) launch_gemm_dma<GemmCfg<1, 4, 1, 1, 2, 0>, true, false>(W16, X, g, e, st);
+  else if (rq16 == 64) launch_gemm_dma<GemmCfg<1, 4, 2, 1, 2, 0>, true, false>(W16, X, g, e, st);
+  else launch_gemm_dma<GemmCfg<1, 4, 4, 1, 2, 0>, true, false>(W16, X, g, e, st);
 }
-inline void ts_xw_dma(const bf16_t* X, long long sx, int ldx, int s_pad, int l_pad, const bf16_t* W16, int rq,
-                      float* Pt, int batch, hipStream_t st) {
+inline void ts_xw_dma(const bf16_t* X, long long sx, int ldx, int s_pad, int l_pad, const bf16_t* W16, int rq16,
+                      int rp, float* Pt, int rq, int batch, hipStream_t st) {
   ProfScope ps(SD_STAGE_SKETCH, st);
-  GemmShape g{rq, s_pad, l_pad, l_pad, ldx, (long long)rq * l_pad, sx, batch};
-  EpiStoreRows e{Pt, (long long)rq * s_pad, s_pad};
+  GemmShape g{rq16, s_pad, l_pad, l_pad, ldx, (long long)rq16 * l_pad, sx, batch};
+  EpiStoreRowsSplit e{Pt, (long long)rq * s_pad, s_pad, rp, rq};
   // one wave per 32-column tile and a four-stage ring: the K loop is long
   // (l_pad) and the grid small, so more loads per work-group stay in flight
-  if (rq == 32) launch_gemm_dma<GemmCfg<1, 1, 1, 1, 4, 0>, false, false>(W16, X, g, e, st);
-  else launch_gemm_dma<GemmCfg<1, 1, 2, 1, 4, 0>, false, false>(W16, X, g, e, st);
+  if (rq16 == 32) launch_gemm_dma<GemmCfg<1, 1, 1, 1, 4, 0>, false, false>(W16, X, g, e, st);
+  else if (rq16 == 64) launch_gemm_dma<GemmCfg<1, 1, 2, 1, 4, 0>, false, false>(W16, X, g, e, st);
+  else launch_gemm_dma<GemmCfg<1, 1, 4, 1, 4, 0>, false, false>(W16, X, g, e, st);
 }
+
+// Rows of the split bf16 operand copy of a panel with rp rows.
+inline int split_rows(int rp) { return 2 * rp <= 32 ? 32 : (2 * rp <= 64 ? 64 : 128); }
 
 // Float64 partial Grams of panel rows over 128-position chunks.
 inline void gram_partials(const float* A, long long sa, int lda, const float* B, long long sb, int ldb, int ca,
@@ -208,20 +216,22 @@ inline size_t gram_part_elems(int batch, int len_pad, int ca, int cb, bool sym) 
   return (size_t)batch * (len_pad / GP_CHUNK) * gram_items(ca, cb, sym);
 }
 
-// One CholeskyQR pass on every panel of the batch, in place (plus the bf16
-// copy of Q, with rows c .. c16 - 1 zero).
+// One CholeskyQR pass on every panel of the batch, in place (plus, with Pt16,
+// the split bf16 copy of Q: hi rows 0 .. c - 1, lo rows c .. 2c - 1, zero
+// rows up to c16; [batch][c16][ld]).
 inline void cholqr(float* Pt, long long sp, int ld, int c, int len_pad, int batch, double* part, double* fac,
                    int* status, hipStream_t st, bf16_t* Pt16 = nullptr, int c16 = 0) {
+  const long long sp16 = (long long)c16 * ld;
   ProfScope ps(SD_STAGE_CHOLQR, st);
   gram_partials(Pt, sp, ld, Pt, sp, ld, c, c, len_pad, true, part, batch, st);
   const int nch = len_pad / GP_CHUNK;
   const dim3 g((len_pad / 128) * batch), b(128);
   if (c <= 16) {
-    hipLaunchKernelGGL((chol_qr_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, part, nch, status, Pt16, c16);
+    hipLaunchKernelGGL((chol_qr_kernel<16>), g, b, 0, st, Pt, sp, ld, c, len_pad, part, nch, status, Pt16, c16, sp16);
   } else {   // wider panels: factor on one work-group per panel, then apply
     hipLaunchKernelGGL(chol_factor_kernel, dim3(batch), dim3(256), 0, st, part, nch, c, fac, status);
-    if (c <= 32) hipLaunchKernelGGL((chol_apply_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16, c16);
-    else hipLaunchKernelGGL((chol_apply_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16, c16);
+    if (c <= 32) hipLaunchKernelGGL((chol_apply_kernel<32>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16, c16, sp16);
+    else hipLaunchKernelGGL((chol_apply_kernel<64>), g, b, 0, st, Pt, sp, ld, c, len_pad, fac, batch, Pt16, c16, sp16);
   }
 }
 
@@ -235,10 +245,16 @@ inline void rotate(const float* in, long long si, int ldi, const float* E, long 
   else hipLaunchKernelGGL((rotate_kernel<64>), g, b, 0, st, in, si, ldi, E, se, scale, ssc, out, so, ldo, kin, kout, len, batch);
 }
 
-template <typename TX, typename TO>
+template <typename TX, typename TO, bool ACC64 = false>
 void lowrank(const LowRankArgs& a, hipStream_t st) {
   ProfScope ps(SD_STAGE_LOWRANK, st);
   const dim3 g((a.rows_pad / 128) * (a.cols_pad / 128) * a.batch), b(256);
+  if constexpr (ACC64) {
+    if (a.kmax <= 16) hipLaunchKernelGGL((lowrank_kernel<TX, TO, 16, 1, true>), g, b, 0, st, a);
+    else if (a.kmax <= 32) hipLaunchKernelGGL((lowrank_kernel<TX, TO, 32, 1, true>), g, b, 0, st, a);
+    else hipLaunchKernelGGL((lowrank_kernel<TX, TO, 64, 1, true>), g, b, 0, st, a);
+    return;
+  }
   if (a.kmax <= 16) {
     if constexpr (sizeof(TX) == 2) hipLaunchKernelGGL((lowrank_kernel<TX, TO, 16, 4>), g, b, 0, st, a);
     else hipLaunchKernelGGL((lowrank_kernel<TX, TO, 16>), g, b, 0, st, a);

@@ -7,6 +7,16 @@
 // padded start X0 of Alg. 1 and Alg. 2 and the PSD residual R of Alg. 2.
 // Per-matrix alpha, c and kk are read from device memory so that gate
 // decisions never leave the GPU.
+//
+// The float32 Muon start takes the two-term form (ACC64)
+//
+//   out[i][n] = alpha * (x[i][n] + sum_j L[j][i] c[j] Rr[j][n]) + sum_j L[j][i] c2[j] Rr[j][n]
+//
+// with the first sum and the difference in float64: the float32 factors'
+// products are exact there, so R = x - V S U^T is formed to float32 rounding
+// of R itself instead of the head's (a head s_1 / nu times larger than R
+// otherwise leaves 2^-24 s_1 / nu of rounding in R / nu, which the filter's
+// slope at zero amplifies).
 #pragma once
 
 #include "common.hpp"
@@ -24,6 +34,7 @@ struct LowRankArgs {
   long long sr;
   int ldr;
   const float* coef;  // [b][kmax]
+  const float* coef2; // [b][kmax], two-term form only (ACC64)
   const int* kk;      // [b] or null (then kconst)
   int kconst;
   const float* alpha; // [b] or null (then 1)
@@ -84,10 +95,12 @@ struct Raw8<float> {
 // allocation must allow (4 for the bf16 passes of the Muon start, which
 // would otherwise take 130 registers and three waves: the passes are bound
 // by the X loads in flight, and a fourth work-group per CU adds a third).
-template <typename TX, typename TO, int KM, int WPE = 1>
+template <typename TX, typename TO, int KM, int WPE = 1, bool ACC64 = false>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void lowrank_kernel(LowRankArgs a) {
   __shared__ __attribute__((aligned(16))) float ls[KM][128];
   __shared__ __attribute__((aligned(16))) float rs[KM][128];
+  __shared__ __attribute__((aligned(16))) float l2s[ACC64 ? KM : 1][128];
+  __shared__ float cs[ACC64 ? KM : 1];
   __shared__ float red[4];
   const int tr = a.rows_pad / 128, tc = a.cols_pad / 128, per = tr * tc;
   const int lid = xcd_remap(blockIdx.x, per * a.batch);
@@ -102,7 +115,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void
   // whose latency overlaps the low-rank product. (Scaling a panel value as
   // it arrives made every panel load wait for the one before.)
   constexpr int PER = KM * 128 / 256;
-  float lv[PER], cv[PER], rv[PER];
+  float lv[PER], cv[PER], rv[PER], c2v[ACC64 ? PER : 1];
 #pragma unroll
   for (int u = 0; u < PER; ++u) {
     const int e = tid + 256 * u, j = e >> 7, x = e & 127;
@@ -110,6 +123,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void
     lv[u] = a.L[b * a.sl + (long long)jc * a.ldl + i0 + x];
     cv[u] = a.coef[b * a.kmax + jc];
     rv[u] = a.Rr[b * a.sr + (long long)jc * a.ldr + n0 + x];
+    if constexpr (ACC64) c2v[u] = a.coef2 ? a.coef2[b * a.kmax + jc] : 0.f;
   }
   const TX* xb = reinterpret_cast<const TX*>(a.x) + b * a.sx;
   Raw8<TX> xr[8];
@@ -121,11 +135,69 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void
   for (int u = 0; u < PER; ++u) {
     const int e = tid + 256 * u, j = e >> 7, x = e & 127;
     if (j < a.kmax) {
-      ls[j][x] = lv[u] * cv[u];
+      if constexpr (ACC64) {
+        ls[j][x] = lv[u];            // unscaled: the coefficient is applied in float64
+        l2s[j][x] = lv[u] * c2v[u];
+        if (x == 0) cs[j] = cv[u];
+      } else {
+        ls[j][x] = lv[u] * cv[u];
+      }
       rs[j][x] = rv[u];
     }
   }
   __syncthreads();
+  if constexpr (ACC64) {
+    // two-term float32 start: R = x + sum_j L c R^T in float64, then
+    // out = alpha R + sum_j L c2 R^T
+    double accd[8][8];
+    float acc2[8][8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        accd[r][c] = 0.0;
+        acc2[r][c] = 0.f;
+      }
+    for (int j = 0; j < kk; ++j) {
+      const double cj = (double)cs[j];
+      double ld[8];
+      float l2[8], rv8[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) {
+        ld[r] = (double)ls[j][rg * 8 + r] * cj;
+        l2[r] = l2s[j][rg * 8 + r];
+        rv8[r] = rs[j][cg * 8 + r];
+      }
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          accd[r][c] = fma(ld[r], (double)rv8[c], accd[r][c]);
+          acc2[r][c] = fmaf(l2[r], rv8[c], acc2[r][c]);
+        }
+    }
+    TO* ob = a.out ? reinterpret_cast<TO*>(a.out) + b * a.so : nullptr;
+    double ssd = 0.0;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int i = i0 + rg * 8 + r;
+      float v[8];
+      xr[r].get(v);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const double rr = (double)v[c] + accd[r][c];
+        ssd = fma(rr, rr, ssd);
+        v[c] = (float)((double)alpha * rr) + acc2[r][c];
+      }
+      if (ob) store8<TO>(ob + (long long)i * a.ldo + n0 + cg * 8, v);
+    }
+    if (a.sumsq) {
+      const float ss = (float)ssd;
+      const float tot = block_sum(ss, red);
+      if (tid == 0) a.sumsq[(long long)b * per + t] = tot;
+    }
+    return;
+  }
   float acc[8][8];
 #pragma unroll
   for (int r = 0; r < 8; ++r)
@@ -182,8 +254,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE))) void
 // start coefficients c_j = -(s_j / nu - 1 / gamma) of
 //   X0 = alpha X + sum_j L_j c_j R_j^T  =  R / nu + gamma^-1 L R^T
 // (1 / gamma = 0 for the explicit restore). With coef_one, also the restore
-// coefficients: 1 for the deflated components, 0 past them. One wave per
-// matrix.
+// coefficients: 1 for the deflated components, 0 past them. With coef_g, the
+// head coefficients of the two-term start (ACC64 lowrank_kernel): 1 / gamma
+// for the deflated components. One wave per matrix.
 // Residual floor: with k_eff > 0, a residual with nu <= rho ||X||_F, where
 // ||X||_F^2 = sum_{j < k_eff} s_j^2 + nu^2 (U_k S_k V_k^T is the projection
 // of X on the head), is rounding of the head's arithmetic: its components
@@ -195,7 +268,7 @@ static __global__ __launch_bounds__(64) void muon_finalize_kernel(const float* s
                                                                   const int* keff, int kmax, float inv_gamma,
                                                                   float rho, float* alpha, float* coef_b,
                                                                   float* nu_dev, float* nu_user, float* coef_one,
-                                                                  int* status, int batch) {
+                                                                  float* coef_g, int* status, int batch) {
   const int b = blockIdx.x, lane = threadIdx.x;
   double acc = 0.0;
   for (int t = lane; t < tiles; t += WAVE) acc += (double)sumsq[(long long)b * tiles + t];
@@ -216,6 +289,7 @@ static __global__ __launch_bounds__(64) void muon_finalize_kernel(const float* s
   for (int j = lane; j < kmax; j += WAVE) {
     coef_b[b * kmax + j] = j < ke ? (float)(-((double)sv[b * kmax + j] * inv - (double)inv_gamma)) : 0.f;
     if (coef_one) coef_one[b * kmax + j] = j < ke ? 1.f : 0.f;
+    if (coef_g) coef_g[b * kmax + j] = j < ke ? inv_gamma : 0.f;
   }
 }
 

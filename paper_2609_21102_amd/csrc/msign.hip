@@ -15,20 +15,24 @@ namespace sd {
 struct MsignPlan {
   int batch, m, n, k, steps, dtype;
   bool tall, copy_in;
+  bool square;            // m == n: tall for Alg. 3 (A = M), filtered in place
   bool explicit_restore;  // head added after the filter (k > 0)
   int s, l, s_pad, l_pad, rp;
+  int kw;                // estimated triplets: k, or the gate's window r when tau > 0 and window > 0
   int rq;                // rows of the sketch panels: rp rounded up to 32 (zero rows past rp)
+  int rq16;              // rows of the split bf16 panel copies (hi, lo): 2 rp rounded up to 32
   size_t esz;
   // buffers
   void *xc, *bm;
   float *xa, *xb;        // float32 iterates (fp32 path)
   bf16_t *xa16, *xb16;   // bf16 path: the iterates as hi = bf16(X) (the product
-  int8_t *xalo, *xblo;   // operand) plus 8-bit residuals
+  int8_t *xalo, *xblo;   // operand) plus e4m3 residual bytes
   float *a32;
   bf16_t* a16;
-  float *om, *yl, *ys, *E, *sv, *invsv, *coefA, *coefB, *coefR, *Ls, *Ll, *sumsq, *alpha, *nu;
+  double* E;             // leading eigenvectors of G G^T, [B][rp][kw] (float64)
+  float *om, *yl, *ys, *sv, *invsv, *coefA, *coefB, *coefR, *coefG, *Ls, *Ll, *sumsq, *alpha, *nu;
   float* xl32;           // explicit restore, bf16 path: the filter output in float32
-  bf16_t *om16, *yl16, *ys16;   // bf16 copies of the panels: product operands (bf16 path)
+  bf16_t *om16, *yl16, *ys16;   // split bf16 copies of the panels: product operands (bf16 path)
   double *part, *fac;
   int* keff;
   int tiles;
@@ -48,20 +52,21 @@ static void plan_msign(MsignPlan& p, Arena& ar) {
   p.a32 = ar.take<float>(B * ss);
   p.a16 = p.dtype == SD_DTYPE_BF16 ? ar.take<bf16_t>(B * ss) : nullptr;
   p.bm = ar.take<char>(B * ss * p.esz);
-  const int kq = p.k > 0 ? p.k : 1;
-  const int rq = p.rq;
+  const int kq = p.kw > 0 ? p.kw : 1;
+  const int rq = p.rq, rq16 = p.rq16;
   p.om = ar.take<float>(B * rq * p.s_pad);
   p.yl = ar.take<float>(B * rq * p.l_pad);
   p.ys = ar.take<float>(B * rq * p.s_pad);
-  p.om16 = bf ? ar.take<bf16_t>(B * rq * p.s_pad) : nullptr;
-  p.yl16 = bf ? ar.take<bf16_t>(B * rq * p.l_pad) : nullptr;
-  p.ys16 = bf ? ar.take<bf16_t>(B * rq * p.s_pad) : nullptr;
-  p.E = ar.take<float>(B * rq * kq);
+  p.om16 = bf ? ar.take<bf16_t>(B * rq16 * p.s_pad) : nullptr;
+  p.yl16 = bf ? ar.take<bf16_t>(B * rq16 * p.l_pad) : nullptr;
+  p.ys16 = bf ? ar.take<bf16_t>(B * rq16 * p.s_pad) : nullptr;
+  p.E = ar.take<double>(B * rq * kq);
   p.sv = ar.take<float>(B * kq);
   p.invsv = ar.take<float>(B * kq);
   p.coefA = ar.take<float>(B * kq);
   p.coefB = ar.take<float>(B * kq);
   p.coefR = p.explicit_restore ? ar.take<float>(B * kq) : nullptr;
+  p.coefG = bf ? nullptr : ar.take<float>(B * kq);
   p.xl32 = (p.explicit_restore && bf) ? ar.take<float>(B * sl) : nullptr;
   p.Ls = ar.take<float>(B * kq * p.s_pad);
   p.Ll = ar.take<float>(B * kq * p.l_pad);
@@ -84,10 +89,12 @@ static int validate_msign(int batch, int m, int n, int k, int steps, int dtype, 
   if (o.oversample < 0 || o.power_iters < 0 || o.power_iters > 100) return SD_ERR_INVALID_ARG;
   if (!(o.gamma > 0.f) || !(o.tau >= 0.f) || !(o.tau < 1.f)) return SD_ERR_INVALID_ARG;
   if (o.restore != SD_RESTORE_PADDED && o.restore != SD_RESTORE_EXPLICIT) return SD_ERR_INVALID_ARG;
+  if (o.window < 0 || o.window > s) return SD_ERR_INVALID_ARG;
   if (o.restore == SD_RESTORE_EXPLICIT && steps == 0) return SD_ERR_UNSUPPORTED;
   if ((long long)m * n > (1ll << 31) || (long long)batch * m * n > (1ll << 40)) return SD_ERR_UNSUPPORTED;
   if (k > 0) {
-    const long long rp = (long long)k + o.oversample < s ? (long long)k + o.oversample : s;
+    const long long kw = (o.tau > 0.f && o.window > 0) ? o.window : k;
+    const long long rp = kw + o.oversample < s ? kw + o.oversample : s;
     if (rp > SM_MAX) return SD_ERR_UNSUPPORTED;
   }
   return SD_OK;
@@ -102,12 +109,15 @@ static void make_plan(MsignPlan& p, int batch, int m, int n, int k, int steps, i
   p.steps = steps;
   p.dtype = dtype;
   p.tall = m > n;
+  p.square = m == n;
   p.s = p.tall ? n : m;
   p.l = p.tall ? m : n;
   p.s_pad = round_up(p.s, 128);
   p.l_pad = round_up(p.l, 128);
-  p.rp = k > 0 ? (k + o.oversample < p.s ? k + o.oversample : p.s) : 0;
+  p.kw = k > 0 ? ((o.tau > 0.f && o.window > 0) ? o.window : k) : 0;
+  p.rp = k > 0 ? (p.kw + o.oversample < p.s ? p.kw + o.oversample : p.s) : 0;
   p.rq = p.rp > 32 ? 64 : 32;
+  p.rq16 = split_rows(p.rp);
   p.esz = dtype == SD_DTYPE_BF16 ? 2 : 4;
   const bool aligned = in && (reinterpret_cast<uintptr_t>(in) % 16 == 0);
   p.copy_in = p.tall || p.s != p.s_pad || p.l != p.l_pad || !aligned;
@@ -134,15 +144,15 @@ static void sym_gemm(const T* a, const GemmShape& g, const Epi& e, hipStream_t s
   else launch_gemm<CfgTile128, T, false, true>(a, a, g, e, st);
 }
 
-// Residual floor rho of the padded start, relative to ||X||_F: the
-// resolution of the arithmetic that forms the head. bf16 path: the sketch
-// products take bf16 operands (unit roundoff 2^-9), rho = 2^-8. fp32 path:
-// float32 products over up to thousands of terms and a one-pass CholeskyQR
-// whose orthogonality loss grows with kappa^2, rho = 2^-16 (256 u).
-template <typename T>
-constexpr float kResidualFloor = 0x1p-16f;
-template <>
-constexpr float kResidualFloor<bf16_t> = 0x1p-8f;
+// Residual floor rho of the padded start, relative to ||X||_F: the rounding
+// level of the float32 arithmetic that forms the residual on both paths (the
+// bf16 path's sketch products take split panels, so its head is float32-
+// class too). R = X - V S U^T is a float32 difference of X and a rank-k
+// float32 product whose entries are as large as X's, built from head factors
+// that carry float32 rounding, so its rounding is a few units of 2^-24
+// ||X||_F; a residual within rho = 16 u = 2^-20 of ||X||_F is that rounding
+// (the input has rank <= k_eff, outside Alg. 1's k < rank(M)) and is dropped.
+constexpr float kResidualFloor = 0x1p-20f;
 
 template <typename T>
 static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opts& o, const T* in, T* out,
@@ -177,38 +187,67 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     // the sketch kernels write the whole padded panels (zero rows past rp,
     // zero columns past s); the CholQR passes write the bf16 copies of Q
     // likewise, so no panel needs clearing first
+    const int rq16 = p.rq16, nrow = BF && rq16 > rq ? rq16 : rq;
+    const long long so16 = (long long)rq16 * s_pad;
     if (o.sketch) {
-      const long long tot = (long long)rq * s_pad * B;
+      const long long tot = (long long)nrow * s_pad * B;
       hipLaunchKernelGGL(sketch_copy_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, o.sketch, p.s, rp, rq,
-                         B, BF ? p.om16 : nullptr);
+                         B, BF ? p.om16 : nullptr, so16, rq16);
     } else {
-      const long long tot = (long long)rq * (s_pad / 4) * B;
+      const long long tot = (long long)nrow * (s_pad / 4) * B;
       hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, st, p.om, so, s_pad, p.s, rp, rq, o.seed, B,
-                         BF ? p.om16 : nullptr);
+                         BF ? p.om16 : nullptr, so16, rq16);
     }
+    // bf16 path: split-panel products (float32-class results); fp32 path:
+    // fp64 accumulation
     auto xtw = [&](const float* w, const bf16_t* w16, float* out) {
-      if constexpr (BF) ts_xtw_dma(reinterpret_cast<const bf16_t*>(xc), sx, ldx, s_pad, l_pad, w16, rq, out, B, st);
-      else ts_xtw<T>(xc, sx, ldx, s_pad, l_pad, w, so, s_pad, rp, out, sl_, l_pad, B, st);
+      if constexpr (BF)
+        ts_xtw_dma(reinterpret_cast<const bf16_t*>(xc), sx, ldx, s_pad, l_pad, w16, rq16, rp, out, rq, B, st);
+      else ts_xtw<T, true>(xc, sx, ldx, s_pad, l_pad, w, so, s_pad, rp, out, sl_, l_pad, B, st);
     };
     auto xw = [&](const float* w, const bf16_t* w16, float* out) {
-      if constexpr (BF) ts_xw_dma(reinterpret_cast<const bf16_t*>(xc), sx, ldx, s_pad, l_pad, w16, rq, out, B, st);
-      else ts_xw<T>(xc, sx, ldx, s_pad, l_pad, w, sl_, l_pad, rp, out, so, s_pad, B, st);
+      if constexpr (BF)
+        ts_xw_dma(reinterpret_cast<const bf16_t*>(xc), sx, ldx, s_pad, l_pad, w16, rq16, rp, out, rq, B, st);
+      else ts_xw<T, true>(xc, sx, ldx, s_pad, l_pad, w, sl_, l_pad, rp, out, so, s_pad, B, st);
     };
-    xtw(p.om, p.om16, p.yl);
-    cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st, p.yl16, rq);
+    // Alg. 3 takes A = M for n >= m: the sketch multiplies the columns of the
+    // tall orientation. A wide input (X = M) and a tall one (X = M^T after the
+    // canonical copy) both have A = X^T, so Omega multiplies X's rows: Y
+    // lives on the l side, G = Q^T A on the s side. A square input is tall
+    // (A = M = X) and is sketched from the other side without a copy: Y = X
+    // Omega on the s side, G^T = X^T Q on the l side, and the head factors
+    // change sides (U = Q E on the rows of X, V = G^T E / s on its columns).
+    // The Gram, polynomial and update of the filter are the same either way.
+    const bool sq = p.square;
+    float* pq = sq ? p.ys : p.yl;   // Q and Y (the sketched side)
+    float* pg = sq ? p.yl : p.ys;   // the other side: power-iteration panel, then G^T
+    bf16_t* pq16 = sq ? p.ys16 : p.yl16;
+    bf16_t* pg16 = sq ? p.yl16 : p.ys16;
+    const long long sq_ = sq ? so : sl_, sg_ = sq ? sl_ : so;
+    const int lq = sq ? s_pad : l_pad, lg = sq ? l_pad : s_pad;
+    auto to_q = [&](const float* w, const bf16_t* w16, float* out) {   // product onto the sketched side
+      if (sq) xw(w, w16, out);
+      else xtw(w, w16, out);
+    };
+    auto to_g = [&](const float* w, const bf16_t* w16, float* out) {   // product onto the other side
+      if (sq) xtw(w, w16, out);
+      else xw(w, w16, out);
+    };
+    to_q(p.om, p.om16, pq);
+    cholqr(pq, sq_, lq, rp, lq, B, p.part, p.fac, o.status_dev, st, pq16, rq16);
     for (int j = 0; j < o.power_iters; ++j) {
-      xw(p.yl, p.yl16, p.ys);
-      cholqr(p.ys, so, s_pad, rp, s_pad, B, p.part, p.fac, o.status_dev, st, p.ys16, rq);
-      xtw(p.ys, p.ys16, p.yl);
-      cholqr(p.yl, sl_, l_pad, rp, l_pad, B, p.part, p.fac, o.status_dev, st, p.yl16, rq);
+      to_g(pq, pq16, pg);
+      cholqr(pg, sg_, lg, rp, lg, B, p.part, p.fac, o.status_dev, st, pg16, rq16);
+      to_q(pg, pg16, pq);
+      cholqr(pq, sq_, lq, rp, lq, B, p.part, p.fac, o.status_dev, st, pq16, rq16);
     }
-    xw(p.yl, p.yl16, p.ys);   // G = (X Q)^T
+    to_g(pq, pq16, pg);   // G^T = A^T Q
     {
       ProfScope ps(SD_STAGE_SMALL, st);
-      gram_partials(p.ys, so, s_pad, p.ys, so, s_pad, rp, rp, s_pad, true, p.part, B, st);   // G G^T
+      gram_partials(pg, sg_, lg, pg, sg_, lg, rp, rp, lg, true, p.part, B, st);   // G G^T
 #define SD_HEAD(NPV)                                                                                       \
-  hipLaunchKernelGGL(svd_head_kernel<NPV>, dim3(B), dim3(SM_THREADS), 0, st, p.part, s_pad / GP_CHUNK, rp, p.k, \
-                     o.tau, p.E, p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out)
+  hipLaunchKernelGGL(svd_head_kernel<NPV>, dim3(B), dim3(SM_THREADS), 0, st, p.part, lg / GP_CHUNK, rp, p.kw, \
+                     p.k, o.tau, p.E, p.sv, p.invsv, p.keff, p.coefA, o.s_out, o.k_eff_out)
       switch (jacobi_class(rp)) {
         case 4: SD_HEAD(4); break;
         case 8: SD_HEAD(8); break;
@@ -218,16 +257,20 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
         default: SD_HEAD(0); break;
       }
 #undef SD_HEAD
+      // V = G^T E / s onto the G side's factor, U = Q E onto the Q side's
+      // (Ls: the rows of X, Ll: its columns; s_pad = l_pad when square)
+      float* vt = sq ? p.Ll : p.Ls;
+      float* ut = sq ? p.Ls : p.Ll;
       const dim3 gf(((s_pad + l_pad + 255) / 256) * B);
       if (rp <= 16)
-        hipLaunchKernelGGL(head_factors_kernel<16>, gf, dim3(256), 0, st, p.E, p.invsv, rp, p.k, p.ys, so, s_pad,
-                           p.yl, sl_, l_pad, p.Ls, p.Ll);
+        hipLaunchKernelGGL(head_factors_kernel<16>, gf, dim3(256), 0, st, p.E, p.sv, rp, p.kw, pg, sg_, lg, pq,
+                           sq_, lq, vt, ut);
       else if (rp <= 32)
-        hipLaunchKernelGGL(head_factors_kernel<32>, gf, dim3(256), 0, st, p.E, p.invsv, rp, p.k, p.ys, so, s_pad,
-                           p.yl, sl_, l_pad, p.Ls, p.Ll);
+        hipLaunchKernelGGL(head_factors_kernel<32>, gf, dim3(256), 0, st, p.E, p.sv, rp, p.kw, pg, sg_, lg, pq,
+                           sq_, lq, vt, ut);
       else
-        hipLaunchKernelGGL(head_factors_kernel<SM_MAX>, gf, dim3(256), 0, st, p.E, p.invsv, rp, p.k, p.ys, so,
-                           s_pad, p.yl, sl_, l_pad, p.Ls, p.Ll);
+        hipLaunchKernelGGL(head_factors_kernel<SM_MAX>, gf, dim3(256), 0, st, p.E, p.sv, rp, p.kw, pg, sg_, lg,
+                           pq, sq_, lq, vt, ut);
     }
   } else if (o.k_eff_out) {
     hipLaunchKernelGGL(fill_int_kernel, grid1(B, 256), dim3(256), 0, st, o.k_eff_out, (long long)B, 0);
@@ -238,30 +281,36 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   la.x = xc;
   la.sx = sx;
   la.ldx = ldx;
-  la.L = p.Ls;   // V = G^T E / s, [k][s_pad]
-  la.sl = (long long)p.k * p.s_pad;
+  la.L = p.Ls;   // V = G^T E / s, [kw][s_pad]
+  la.sl = (long long)p.kw * p.s_pad;
   la.ldl = p.s_pad;
-  la.Rr = p.Ll;  // U = Q E, [k][l_pad]
-  la.sr = (long long)p.k * p.l_pad;
+  la.Rr = p.Ll;  // U = Q E, [kw][l_pad]
+  la.sr = (long long)p.kw * p.l_pad;
   la.ldr = p.l_pad;
   la.kk = p.k > 0 ? p.keff : nullptr;
   la.kconst = 0;
-  la.kmax = p.k > 0 ? p.k : 1;
+  la.kmax = p.kw > 0 ? p.kw : 1;
   la.rows_pad = p.s_pad;
   la.cols_pad = p.l_pad;
   la.batch = B;
   la.coef = p.coefA;
+  la.coef2 = nullptr;
   la.alpha = nullptr;
   la.out = nullptr;
   la.sumsq = p.sumsq;
-  lowrank<T, T>(la, st);
+  // fp32 path: R = X - V S U^T formed in float64 (two-term start below)
+  constexpr bool R64 = sizeof(T) == 4;
+  lowrank<T, T, R64>(la, st);
   {
     ProfScope ps(SD_STAGE_LOWRANK, st);
     hipLaunchKernelGGL(muon_finalize_kernel, dim3(B), dim3(64), 0, st, p.sumsq, p.tiles, p.sv,
                        p.k > 0 ? p.keff : nullptr, la.kmax, p.explicit_restore ? 0.f : 1.f / o.gamma,
-                       kResidualFloor<T>, p.alpha, p.coefB, p.nu, o.nu_out, p.coefR, o.status_dev, B);
+                       kResidualFloor, p.alpha, p.coefB, p.nu, o.nu_out, p.coefR, p.coefG, o.status_dev, B);
   }
-  la.coef = p.coefB;
+  // X0 = alpha R + gamma^-1 V U^T: fp32 path as alpha (X - V S U^T) + V (1 / gamma) U^T
+  // (coefA, coefG); bf16 path in one term, alpha X + V (-(s alpha - 1 / gamma)) U^T (coefB)
+  la.coef = R64 ? p.coefA : p.coefB;
+  la.coef2 = R64 ? p.coefG : nullptr;
   la.alpha = p.alpha;
   la.out = p.xa;        // fp32 path: float32 X0
   la.out16 = p.xa16;    // bf16 path: X0 as hi plus 8-bit residuals
@@ -269,10 +318,10 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
   la.so = sl;
   la.ldo = p.l_pad;
   la.sumsq = nullptr;
-  lowrank<T, float>(la, st);
+  lowrank<T, float, R64>(la, st);
 
   // fixed-depth filter: float32 iterate (fp32 path) or hi = bf16(X) plus
-  // 8-bit residuals, hi being the product operand (bf16 path)
+  // e4m3 residual bytes, hi being the product operand (bf16 path)
   float* cur = p.xa;
   float* nxt = p.xb;
   bf16_t* cur16 = p.xa16;
@@ -404,6 +453,7 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
     ra.sx = sl;
     ra.ldx = p.l_pad;
     ra.coef = p.coefR;
+    ra.coef2 = nullptr;
     ra.alpha = nullptr;
     ra.out16 = nullptr;
     ra.out_lo = nullptr;
@@ -573,7 +623,7 @@ int sd_sketch(int batch, int s, int rp, uint64_t seed, float* out, hipStream_t s
   if (batch < 1 || s < 1 || rp < 1 || !out) return SD_ERR_INVALID_ARG;
   const long long tot = (long long)rp * ((s + 3) / 4) * batch;
   hipLaunchKernelGGL(sketch_kernel, grid1(tot, 256), dim3(256), 0, stream, out, (long long)s * rp, s, s, rp, rp, seed,
-                     batch, (bf16_t*)nullptr);
+                     batch, (bf16_t*)nullptr, 0ll, 0);
   return hip_status();
 }
 

@@ -510,6 +510,8 @@ struct PsdPlan {
   int* ndef;
   double *part, *fac;
   float *qlan, *w, *t, *v, *theta, *alpha_x0;
+  bool frob;       // scale_mode: theta = ||R||_F from the residual pass's tile sums
+  float* sumsq;    // [tiles] sums of R^2 per 128 x 128 tile (Frobenius scale)
   LanczosState* lst;
   double* lpart;   // Lanczos step partial sums: two blocks of LZ_MAX rows
 };
@@ -547,6 +549,7 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
   p.v = ar.take<float>(p.n_pad);
   p.theta = ar.take<float>(1);
   p.alpha_x0 = ar.take<float>(1);
+  p.sumsq = p.frob ? ar.take<float>((size_t)(p.n_pad / 128) * (p.n_pad / 128)) : nullptr;
   p.lst = ar.take<LanczosState>(1);
   p.lpart = ar.take<double>((size_t)2 * LZ_MAX * lanczos_partials(p.n_pad));
 }
@@ -562,6 +565,7 @@ static int validate_psd(int n, int k, int steps, const float* X, const float* Qw
   if (o.tau > 0.f && (o.window < 1 || o.window > k)) return SD_ERR_INVALID_ARG;
   if (o.poly_degree != 3 && o.poly_degree != 5) return SD_ERR_INVALID_ARG;
   if (o.precision != SD_PREC_F32 && o.precision != SD_PREC_F16) return SD_ERR_INVALID_ARG;
+  if (o.scale_mode != SD_SCALE_LANCZOS && o.scale_mode != SD_SCALE_FROBENIUS) return SD_ERR_INVALID_ARG;
   if ((long long)n * n > (1ll << 34)) return SD_ERR_UNSUPPORTED;
   if (k > 0) {
     const char* q0 = reinterpret_cast<const char*>(Qwarm);
@@ -585,6 +589,7 @@ static void make_psd_plan(PsdPlan& p, int n, int k, int steps, const float* X, c
   p.quintic = o.poly_degree == 5;
   p.f16 = o.precision == SD_PREC_F16;
   p.wide = p.f16 && p.n_pad % 256 == 0 && p.n_pad >= 4096;
+  p.frob = o.scale_mode == SD_SCALE_FROBENIUS;
   const bool aligned = X && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
   p.copy_in = p.n != p.n_pad || !aligned;
 }
@@ -615,6 +620,21 @@ static void lanczos(const PsdPlan& p, const float* R, uint64_t seed, float* thet
   hipLaunchKernelGGL(gemv_kernel, gg, gb, 0, st, R, np, np, p.t, p.w);
   hipLaunchKernelGGL(lanczos_theta_kernel, dim3(1), dim3(1024), 0, st, p.w, p.v, np, p.lst, p.theta, p.alpha_x0,
                      theta_user);
+}
+
+// theta = ||R||_F from the residual pass's per-tile sums of squares (float64,
+// fixed order over the tiles), and alpha = 1 / theta (0 for theta = 0).
+__global__ __launch_bounds__(WAVE) void frob_scale_kernel(const float* sumsq, int tiles, float* theta_dev,
+                                                          float* alpha_x0, float* theta_user) {
+  double acc = 0.0;
+  for (int t = threadIdx.x; t < tiles; t += WAVE) acc += (double)sumsq[t];
+  acc = wave_sum(acc);
+  if (threadIdx.x == 0) {
+    const double th = sqrt(acc);
+    *theta_dev = (float)th;
+    *alpha_x0 = th > 0.0 ? (float)(1.0 / th) : 0.f;
+    if (theta_user) *theta_user = (float)th;
+  }
 }
 
 static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, const sd_psd_opts& o,
@@ -676,6 +696,7 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     la.kmax = K;
     la.alpha = nullptr;
     la.out = p.r;
+    la.sumsq = p.sumsq;   // Frobenius scale: tile sums of R^2
     lowrank<float, float>(la, st);
     // next basis: CholQR(Zt), written back after the filter
     cholqr(zt, 0, np, K, np, 1, p.part, p.fac, o.status_dev, st);
@@ -688,11 +709,19 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     la.kconst = 0;
     la.kmax = 1;
     la.out = p.r;
+    la.sumsq = p.sumsq;
     lowrank<float, float>(la, st);
     if (o.n_deflated_out) hipLaunchKernelGGL(fill_int_kernel, dim3(1), dim3(64), 0, st, o.n_deflated_out, 1ll, 0);
     if (o.n_positive_out) hipLaunchKernelGGL(fill_int_kernel, dim3(1), dim3(64), 0, st, o.n_positive_out, 1ll, 0);
   }
-  lanczos(p, p.r, o.seed, o.theta_out, st);
+  la.sumsq = nullptr;
+  if (p.frob) {
+    const int tiles = (np / 128) * (np / 128);
+    hipLaunchKernelGGL(frob_scale_kernel, dim3(1), dim3(WAVE), 0, st, p.sumsq, tiles, p.theta, p.alpha_x0,
+                       o.theta_out);
+  } else {
+    lanczos(p, p.r, o.seed, o.theta_out, st);
+  }
   // X0 = R / theta + gamma^-1 U sign(lam) U^T
   la.x = p.r;
   la.coef = p.coefX;

@@ -9,7 +9,13 @@
 //
 // Both stream X once and are bound by HBM; MFMA 16 x 16 blocks carry the
 // products (bf16 operands with fp32 accumulation, or fp32). W is fp32 and is
-// rounded to bf16 when it feeds a bf16 product.
+// rounded to bf16 when it feeds a bf16 product. ACC64 (fp32 X only): the
+// products run on the fp64 MFMA (v_mfma_f64_16x16x4f64) and accumulate in
+// fp64; the results are rounded to fp32 once. Its operands sit in the lanes
+// as the fp32 16 x 16 x 4 form's (A[i][k] in lane i + 16 k, B[k][j] in lane
+// j + 16 k), but result item r of lane l is row 4 r + l / 16 of column
+// l % 16, where the fp32 form has row 4 (l / 16) + r (checked on the GPU
+// with an in-bounds probe over one block).
 #pragma once
 
 #include "common.hpp"
@@ -24,9 +30,30 @@ __device__ __forceinline__ u32x4_t f8_to_bf8(const float* p) {
   return u32x4_t{pack_bf2(a[0], a[1]), pack_bf2(a[2], a[3]), pack_bf2(b[0], b[1]), pack_bf2(b[2], b[3])};
 }
 
+typedef double f64x4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ f64x4_t mfma16_f64(double a, double b, f64x4_t c) {
+  return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+}
+// Accumulator of the fp32 skinny products: four fp32 or fp64 values.
+template <bool ACC64>
+struct SkAcc {
+  typedef f32x4_t V;
+  __device__ __forceinline__ static V mma(float a, float b, V c) { return mfma16_f32(a, b, c); }
+  __device__ __forceinline__ static float get(const V& v, int j) { return v[j]; }
+  // row of result item r in lane group q = lane / 16
+  __device__ __forceinline__ static int row(int q, int r) { return 4 * q + r; }
+};
+template <>
+struct SkAcc<true> {
+  typedef f64x4_t V;
+  __device__ __forceinline__ static V mma(float a, float b, V c) { return mfma16_f64((double)a, (double)b, c); }
+  __device__ __forceinline__ static float get(const V& v, int j) { return (float)v[j]; }
+  __device__ __forceinline__ static int row(int q, int r) { return 4 * r + q; }
+};
+
 // ------------------------------------------------------------ X^T W -------
 // Grid: (l_pad / 128) * batch work-groups of 256 threads. MJ = ceil(rp / 16).
-template <typename T, int MJ>
+template <typename T, int MJ, bool ACC64 = false>
 __global__ __launch_bounds__(256) void ts_xtw_kernel(const T* __restrict__ X, long long sx, int ldx,
                                                      int s_pad, int l_pad, const float* __restrict__ Wt,
                                                      long long sw, int ldw, int rp, float* __restrict__ Pt,
@@ -40,10 +67,12 @@ __global__ __launch_bounds__(256) void ts_xtw_kernel(const T* __restrict__ X, lo
   const float* Wb = Wt + b * sw;
   const int wave = threadIdx.x / WAVE, lane = threadIdx.x & (WAVE - 1);
   const int r16 = lane & 15, q = lane >> 4;
+  static_assert(!ACC64 || sizeof(T) == 4, "fp64 accumulation serves the fp32 products");
+  using Acc = SkAcc<ACC64>;
 
-  f32x4_t acc[MJ][2];
+  typename Acc::V acc[MJ][2];
 #pragma unroll
-  for (int m = 0; m < MJ; ++m) acc[m][0] = acc[m][1] = f32x4_t{};
+  for (int m = 0; m < MJ; ++m) acc[m][0] = acc[m][1] = typename Acc::V{};
 
   NNStager<128, 256, T, T> rb;
   const int nk = s_pad / BK;
@@ -68,14 +97,16 @@ __global__ __launch_bounds__(256) void ts_xtw_kernel(const T* __restrict__ X, lo
           u32x4_t a = {0u, 0u, 0u, 0u};
           if (j < rp) a = f8_to_bf8(Wb + (long long)j * ldw + i0 + 32 * u + 8 * q);
 #pragma unroll
-          for (int nb = 0; nb < 2; ++nb) acc[m][nb] = mfma16_bf16(a, bfr[nb], acc[m][nb]);
+          for (int nb = 0; nb < 2; ++nb) {
+            if constexpr (!ACC64) acc[m][nb] = mfma16_bf16(a, bfr[nb], acc[m][nb]);
+          }
         } else {
           f32x4_t af = {0.f, 0.f, 0.f, 0.f};
           if (j < rp) af = *reinterpret_cast<const f32x4_t*>(Wb + (long long)j * ldw + i0 + 16 * u + 4 * q);
 #pragma unroll
           for (int nb = 0; nb < 2; ++nb) {
 #pragma unroll
-            for (int t = 0; t < 4; ++t) acc[m][nb] = mfma16_f32(af[t], u4f(bfr[nb], t), acc[m][nb]);
+            for (int t = 0; t < 4; ++t) acc[m][nb] = Acc::mma(af[t], u4f(bfr[nb], t), acc[m][nb]);
           }
         }
       }
@@ -90,20 +121,22 @@ __global__ __launch_bounds__(256) void ts_xtw_kernel(const T* __restrict__ X, lo
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const int j = m * 16 + 4 * q + jj;
-        if (j < rp) Pb[(long long)j * ldp + n0 + (2 * wave + nb) * 16 + r16] = acc[m][nb][jj];
+        const int j = m * 16 + Acc::row(q, jj);
+        if (j < rp) Pb[(long long)j * ldp + n0 + (2 * wave + nb) * 16 + r16] = Acc::get(acc[m][nb], jj);
       }
 }
 
 // -------------------------------------------------------------- X W -------
 // Grid: (s_pad / 16) * batch work-groups; the 4 waves split K = l_pad and
 // their partial sums are added in wave order.
-template <typename T, int MJ>
+template <typename T, int MJ, bool ACC64 = false>
 __global__ __launch_bounds__(256) void ts_xw_kernel(const T* __restrict__ X, long long sx, int ldx,
                                                     int s_pad, int l_pad, const float* __restrict__ Wt,
                                                     long long sw, int ldw, int rp, float* __restrict__ Pt,
                                                     long long sp, int ldp, int batch) {
-  __shared__ f32x4_t red[4][MJ][WAVE];
+  static_assert(!ACC64 || sizeof(T) == 4, "fp64 accumulation serves the fp32 products");
+  using Acc = SkAcc<ACC64>;
+  __shared__ typename Acc::V red[4][MJ][WAVE];
   const int nrb = s_pad / 16;
   const int lid = xcd_remap(blockIdx.x, nrb * batch);
   const int b = lid / nrb, i0 = (lid - b * nrb) * 16;
@@ -113,9 +146,9 @@ __global__ __launch_bounds__(256) void ts_xw_kernel(const T* __restrict__ X, lon
   const int r16 = lane & 15, q = lane >> 4;
   const int klen = l_pad / 4, kbeg = wave * klen, kend = kbeg + klen;
 
-  f32x4_t acc[MJ];
+  typename Acc::V acc[MJ];
 #pragma unroll
-  for (int m = 0; m < MJ; ++m) acc[m] = f32x4_t{};
+  for (int m = 0; m < MJ; ++m) acc[m] = typename Acc::V{};
 
   const T* xrow = Xb + (long long)(i0 + r16) * ldx;
   if constexpr (sizeof(T) == 2) {
@@ -126,7 +159,7 @@ __global__ __launch_bounds__(256) void ts_xw_kernel(const T* __restrict__ X, lon
         const int j = m * 16 + r16;
         u32x4_t a = {0u, 0u, 0u, 0u};
         if (j < rp) a = f8_to_bf8(Wb + (long long)j * ldw + k + 8 * q);
-        acc[m] = mfma16_bf16(a, bx, acc[m]);
+        if constexpr (!ACC64) acc[m] = mfma16_bf16(a, bx, acc[m]);
       }
     }
   } else {
@@ -138,7 +171,7 @@ __global__ __launch_bounds__(256) void ts_xw_kernel(const T* __restrict__ X, lon
         f32x4_t af = {0.f, 0.f, 0.f, 0.f};
         if (j < rp) af = *reinterpret_cast<const f32x4_t*>(Wb + (long long)j * ldw + k + 4 * q);
 #pragma unroll
-        for (int t = 0; t < 4; ++t) acc[m] = mfma16_f32(af[t], bf[t], acc[m]);
+        for (int t = 0; t < 4; ++t) acc[m] = Acc::mma(af[t], bf[t], acc[m]);
       }
     }
   }
@@ -149,14 +182,14 @@ __global__ __launch_bounds__(256) void ts_xw_kernel(const T* __restrict__ X, lon
     float* Pb = Pt + b * sp;
 #pragma unroll
     for (int m = 0; m < MJ; ++m) {
-      f32x4_t s = red[0][m][lane];
+      typename Acc::V s = red[0][m][lane];
       s += red[1][m][lane];
       s += red[2][m][lane];
       s += red[3][m][lane];
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        const int j = m * 16 + 4 * q + jj;
-        if (j < rp) Pb[(long long)j * ldp + i0 + r16] = s[jj];
+        const int j = m * 16 + Acc::row(q, jj);
+        if (j < rp) Pb[(long long)j * ldp + i0 + r16] = Acc::get(s, jj);
       }
     }
   }
@@ -211,14 +244,25 @@ struct Philox {
   }
 };
 
+// Split bf16 copy of a panel value: hi = bf16(v) and lo = bf16(v - hi)
+// (v - hi is exact in fp32).
+__device__ __forceinline__ void split_bf16(float v, bf16_t& hi, bf16_t& lo) {
+  hi = f2bf(v);
+  lo = f2bf(v - bf2f(hi));
+}
+
 // Omega^T as a [rows][ld] panel for every matrix: entry (i, j) of the s x rp
 // sketch is Gaussian number j * s + i of stream 1 (four per Philox call);
 // every other entry of the panel (rows rp .. rows - 1, columns s .. ld - 1)
-// is written as zero. One thread per four consecutive columns of a row.
+// is written as zero. With Wt16, also the split bf16 copy [rows16][ld]
+// (stride sw16): hi in row j, lo in row rp + j, zero rows 2 rp .. rows16 - 1.
+// One thread per four consecutive columns of a row of either panel.
 static __global__ void sketch_kernel(float* __restrict__ Wt, long long sw, int ld, int s, int rp, int rows,
-                                     uint64_t seed, int batch, bf16_t* __restrict__ Wt16) {
+                                     uint64_t seed, int batch, bf16_t* __restrict__ Wt16, long long sw16,
+                                     int rows16) {
   const int quads = (ld + 3) / 4;
-  const long long per = (long long)rows * quads;
+  const int nrow = Wt16 && rows16 > rows ? rows16 : rows;
+  const long long per = (long long)nrow * quads;
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
   if (gid >= per * batch) return;
   const int b = (int)(gid / per);
@@ -237,26 +281,47 @@ static __global__ void sketch_kernel(float* __restrict__ Wt, long long sw, int l
       if (t < nv) v[t] = z[off + t];
   }
   const long long o = b * sw + (long long)j * ld + i0;
+  const long long o16 = b * sw16 + (long long)j * ld + i0;
 #pragma unroll
   for (int t = 0; t < 4; ++t)
     if (i0 + t < ld) {
-      Wt[o + t] = v[t];
-      if (Wt16) Wt16[o + t] = f2bf(v[t]);
+      if (j < rows) Wt[o + t] = v[t];
+      if (Wt16) {
+        if (j < rp) {
+          bf16_t hi, lo;
+          split_bf16(v[t], hi, lo);
+          Wt16[o16 + t] = hi;
+          Wt16[o16 + (long long)rp * ld + t] = lo;
+        } else if (j >= 2 * rp && j < rows16) {
+          Wt16[o16 + t] = 0;
+        }
+      }
     }
 }
 
-// A caller-supplied sketch [batch][rp][s] as the same zero-padded panel.
+// A caller-supplied sketch [batch][rp][s] as the same zero-padded panels.
 static __global__ void sketch_copy_kernel(float* __restrict__ Wt, long long sw, int ld, const float* __restrict__ src,
-                                          int s, int rp, int rows, int batch, bf16_t* __restrict__ Wt16) {
+                                          int s, int rp, int rows, int batch, bf16_t* __restrict__ Wt16,
+                                          long long sw16, int rows16) {
   const long long gid = (long long)blockIdx.x * blockDim.x + threadIdx.x;
-  const long long per = (long long)rows * ld;
+  const int nrow = Wt16 && rows16 > rows ? rows16 : rows;
+  const long long per = (long long)nrow * ld;
   if (gid >= per * batch) return;
   const int b = (int)(gid / per);
   const long long r = gid - (long long)b * per;
   const int j = (int)(r / ld), i = (int)(r - (long long)j * ld);
   const float v = (j < rp && i < s) ? src[((long long)b * rp + j) * s + i] : 0.f;
-  Wt[b * sw + r] = v;
-  if (Wt16) Wt16[b * sw + r] = f2bf(v);
+  if (j < rows) Wt[b * sw + r] = v;
+  if (Wt16) {
+    if (j < rp) {
+      bf16_t hi, lo;
+      split_bf16(v, hi, lo);
+      Wt16[b * sw16 + r] = hi;
+      Wt16[b * sw16 + r + (long long)rp * ld] = lo;
+    } else if (j >= 2 * rp && j < rows16) {
+      Wt16[b * sw16 + r] = 0;
+    }
+  }
 }
 
 // ----------------------------------------------------- canonical copy ----

@@ -537,12 +537,28 @@ static __global__ __launch_bounds__(256) void chol_factor_kernel(const double* p
   }
 }
 
+// Split bf16 copy of column x of a panel of c rows (stride sp16): hi rows
+// 0 .. c - 1, lo rows c .. 2c - 1, zero rows 2c .. c16 - 1.
+template <int CM>
+__device__ __forceinline__ void store_split16(bf16_t* P16, int ld, int c, int c16, int x, const double (&q)[CM]) {
+#pragma unroll
+  for (int jj = 0; jj < CM; ++jj)
+    if (jj < c) {
+      const float v = (float)q[jj];
+      const bf16_t hi = f2bf(v);
+      P16[(long long)jj * ld + x] = hi;
+      P16[(long long)(c + jj) * ld + x] = f2bf(v - bf2f(hi));
+    }
+  for (int jj = 2 * c; jj < c16; ++jj) P16[(long long)jj * ld + x] = 0;
+}
+
 // Apply: Q = P R^-1 with R = L^T, by forward substitution per position, in
-// place (plus an optional bf16 copy of Q, rows c .. c16 - 1 zero). Grid:
-// (len_pad / 128) * batch; one thread per position.
+// place (plus an optional split bf16 copy of Q, [batch][c16][ld], stride
+// sp16). Grid: (len_pad / 128) * batch; one thread per position.
 template <int CM>
 __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp, int ld, int c, int len_pad,
-                                                         const double* fac, int batch, bf16_t* Pt16, int c16) {
+                                                         const double* fac, int batch, bf16_t* Pt16, int c16,
+                                                         long long sp16) {
   __shared__ double L[CM][CM + 1];
   __shared__ double inv_d[CM];
   const int per = len_pad / 128;
@@ -567,13 +583,7 @@ __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp
 #pragma unroll
   for (int jj = 0; jj < CM; ++jj)
     if (jj < c) P[(long long)jj * ld + x] = (float)q[jj];
-  if (Pt16) {   // bf16 copy: the panel as a product operand
-    bf16_t* P16 = Pt16 + b * sp;
-#pragma unroll
-    for (int jj = 0; jj < CM; ++jj)
-      if (jj < c) P16[(long long)jj * ld + x] = f2bf((float)q[jj]);
-    for (int jj = c; jj < c16; ++jj) P16[(long long)jj * ld + x] = 0;
-  }
+  if (Pt16) store_split16<CM>(Pt16 + b * sp16, ld, c, c16, x, q);   // the panel as a product operand
 }
 
 // Factor and apply in one launch (c <= CM <= 16). Every work-group reduces the
@@ -589,12 +599,12 @@ __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp
 //   * Pivots below c u tr(Gram) are raised to it (flag 2 in status, set by
 //     the matrix's first work-group); a zero trace gives a zero panel.
 //   * Apply: forward substitution per position, in place, plus an optional
-//     bf16 copy of Q whose rows c .. c16 - 1 are written as zeros.
+//     split bf16 copy of Q (store_split16; [batch][c16][ld], stride sp16).
 // Grid: (len_pad / 128) * batch; 128 threads.
 template <int CM>
 __global__ __launch_bounds__(128) void chol_qr_kernel(float* Pt, long long sp, int ld, int c, int len_pad,
                                                       const double* part, int nch, int* status, bf16_t* Pt16,
-                                                      int c16) {
+                                                      int c16, long long sp16) {
   static_assert(CM <= 16, "rows in registers: wider panels use the two-kernel path");
   __shared__ double G[CM][CM + 1];
   __shared__ double L[CM][CM + 1];
@@ -698,26 +708,22 @@ __global__ __launch_bounds__(128) void chol_qr_kernel(float* Pt, long long sp, i
 #pragma unroll
   for (int jj = 0; jj < CM; ++jj)
     if (jj < c) P[(long long)jj * ld + x] = (float)q[jj];
-  if (Pt16) {   // bf16 copy: the panel as a product operand (zero rows up to c16)
-    bf16_t* P16 = Pt16 + b * sp;
-#pragma unroll
-    for (int jj = 0; jj < CM; ++jj)
-      if (jj < c) P16[(long long)jj * ld + x] = f2bf((float)q[jj]);
-    for (int jj = c; jj < c16; ++jj) P16[(long long)jj * ld + x] = 0;
-  }
+  if (Pt16) store_split16<CM>(Pt16 + b * sp16, ld, c, c16, x, q);   // the panel as a product operand
 }
 
 // ----------------------------------------------- thin SVD of G (Alg. 3) ---
 // From the partials of H = G G^T (G = Q^T A, rp x s), in float64: eigen-
 // decompose H, order the eigenvalues decreasingly, and emit for the leading
 // k: singular values, the eigenvector matrix E (rp x k), 1/s (0 for s = 0),
-// the deflation rank (fixed k, or the gate of Alg. 1 when tau > 0) and the
-// subtraction coefficients -s_j used by the residual pass. One work-group
-// per matrix; NP = jacobi_class(rp). The factors U and V follow in
-// head_factors_kernel.
+// the deflation rank (fixed: kcap = k; or the gate of Alg. 1 when tau > 0
+// over the window of k estimated values, min(kcap, max{i : s_i > tau s_1})
+// when s_k < tau s_1, else 0) and the subtraction coefficients -s_j used by
+// the residual pass. One work-group per matrix; NP = jacobi_class(rp). The
+// factors U and V follow in head_factors_kernel.
 template <int NP>
-__global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part, int nch, int rp, int k, float tau,
-                                                              float* E, float* sv, float* inv_sv, int* keff,
+__global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part, int nch, int rp, int k, int kcap,
+                                                              float tau,
+                                                              double* E, float* sv, float* inv_sv, int* keff,
                                                               float* coef_a, float* s_user, int* keff_user) {
   __shared__ SmallLds s;
   const int tid = threadIdx.x, b = blockIdx.x;
@@ -730,7 +736,7 @@ __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part
   sort_desc(s, rp);
   for (int e = tid; e < rp * k; e += SM_THREADS) {
     const int a = e / k, j = e - a * k;
-    E[(long long)b * rp * k + e] = (float)s.e[a][s.perm[j]];
+    E[(long long)b * rp * k + e] = s.e[a][s.perm[j]];
   }
   if (tid < k) {
     const double lam = s.h[s.perm[tid]][s.perm[tid]];
@@ -738,12 +744,13 @@ __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part
   }
   __syncthreads();
   if (tid == 0) {
-    int ke = k;
+    int ke = kcap;
     if (tau > 0.f) {
       const double thr = (double)tau * s.key[0];
       ke = 0;
       if (s.key[k - 1] < thr)
         for (int j = 0; j < k; ++j) ke += (s.key[j] > thr) ? 1 : 0;
+      ke = ke < kcap ? ke : kcap;
     }
     keff[b] = ke;
     if (keff_user) keff_user[b] = ke;
@@ -762,20 +769,23 @@ __global__ __launch_bounds__(SM_THREADS) void svd_head_kernel(const double* part
 }
 
 // The head factors V = G^T E / s (k x s_pad, from the G^T panel Gt) and
-// U = Q E (k x l_pad, from the Q panel Qt) of every matrix, from the E
-// (rp x k, row-major) and 1/s of svd_head_kernel. One position per thread:
-// the V positions, then the U positions, over ceil((s_pad + l_pad) / 256)
-// work-groups per matrix, so both panels stream at full width (on the head
-// kernel's single work-group per matrix this product took 16 us of its 65 at
-// 24 x 768 x 3072). Each output sums its rp terms in row order. RM >= rp.
+// U = Q E (k x l_pad, from the Q panel Qt) of every matrix, from the float64
+// eigenvectors E (rp x k, row-major) and the singular values of
+// svd_head_kernel. One position per thread: the V positions, then the U
+// positions, over ceil((s_pad + l_pad) / 256) work-groups per matrix, so both
+// panels stream at full width. Each output sums its rp terms in row order in
+// float64 and is rounded to float32 once (with E rounded to float32 first,
+// the factors' columns lose orthogonality at float32 resolution, which the
+// explicit restore's filter amplifies). V divides by the float32 singular
+// value that the residual multiplies back. RM >= rp.
 template <int RM>
-__global__ __launch_bounds__(256) void head_factors_kernel(const float* __restrict__ E,
-                                                           const float* __restrict__ inv_sv, int rp, int k,
+__global__ __launch_bounds__(256) void head_factors_kernel(const double* __restrict__ E,
+                                                           const float* __restrict__ sv, int rp, int k,
                                                            const float* __restrict__ Gt, long long sg, int s_pad,
                                                            const float* __restrict__ Qt, long long sq, int l_pad,
                                                            float* __restrict__ Vt, float* __restrict__ Ut) {
-  __shared__ float es[RM * SM_MAX];
-  __shared__ float isv[SM_MAX];
+  __shared__ double es[RM * SM_MAX];
+  __shared__ double isv[SM_MAX];
   const int per = (s_pad + l_pad + 255) / 256;
   const int b = blockIdx.x / per;
   const int x0 = (blockIdx.x - b * per) * 256 + threadIdx.x;
@@ -787,16 +797,19 @@ __global__ __launch_bounds__(256) void head_factors_kernel(const float* __restri
 #pragma unroll
   for (int r = 0; r < RM; ++r) v[r] = P[(long long)(r < rp ? r : rp - 1) * ld + x];
   for (int e = threadIdx.x; e < rp * k; e += 256) es[e] = E[(long long)b * rp * k + e];
-  for (int j = threadIdx.x; j < k; j += 256) isv[j] = inv_sv[b * k + j];
+  for (int j = threadIdx.x; j < k; j += 256) {
+    const float sj = sv[b * k + j];
+    isv[j] = sj > 0.f ? 1.0 / (double)sj : 0.0;
+  }
   __syncthreads();
   if (!valid) return;
   float* out = (vside ? Vt + (long long)b * k * s_pad : Ut + (long long)b * k * l_pad) + x;
   for (int j = 0; j < k; ++j) {
-    float acc = 0.f;
+    double acc = 0.0;
 #pragma unroll
     for (int r = 0; r < RM; ++r)
-      if (r < rp) acc += es[r * k + j] * v[r];
-    out[(long long)j * ld] = vside ? isv[j] * acc : acc;
+      if (r < rp) acc = fma(es[r * k + j], (double)v[r], acc);
+    out[(long long)j * ld] = (float)(vside ? isv[j] * acc : acc);
   }
 }
 

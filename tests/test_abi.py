@@ -46,7 +46,7 @@ int main(void) {
   F(sd_msign_opts, oversample) F(sd_msign_opts, power_iters) F(sd_msign_opts, gamma)
   F(sd_msign_opts, tau) F(sd_msign_opts, seed) F(sd_msign_opts, sketch) F(sd_msign_opts, workspace)
   F(sd_msign_opts, workspace_bytes) F(sd_msign_opts, k_eff_out) F(sd_msign_opts, nu_out)
-  F(sd_msign_opts, s_out) F(sd_msign_opts, status_dev) F(sd_msign_opts, restore)
+  F(sd_msign_opts, s_out) F(sd_msign_opts, status_dev) F(sd_msign_opts, restore) F(sd_msign_opts, window)
   printf("sd_msign_group %zu\n", sizeof(sd_msign_group));
   F(sd_msign_group, batch) F(sd_msign_group, m) F(sd_msign_group, n) F(sd_msign_group, k)
   F(sd_msign_group, steps) F(sd_msign_group, coeffs) F(sd_msign_group, dtype) F(sd_msign_group, in)
@@ -55,7 +55,7 @@ int main(void) {
   F(sd_psd_opts, window) F(sd_psd_opts, poly_degree) F(sd_psd_opts, poly) F(sd_psd_opts, seed)
   F(sd_psd_opts, workspace) F(sd_psd_opts, workspace_bytes) F(sd_psd_opts, n_deflated_out)
   F(sd_psd_opts, n_positive_out) F(sd_psd_opts, theta_out) F(sd_psd_opts, ritz_out)
-  F(sd_psd_opts, status_dev) F(sd_psd_opts, precision)
+  F(sd_psd_opts, status_dev) F(sd_psd_opts, precision) F(sd_psd_opts, scale_mode)
   return 0;
 }
 """
@@ -194,3 +194,46 @@ def test_host_sketch_matches_oracle_generator(lib):
     got = sd.sketch_host(3, 77, 9, seed=123)
     want = np.stack([rng.sketch(123, b, 77, 9).T for b in range(3)]).astype(np.float32)
     np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.gpu
+def test_plain_entry_points_equal_ex_with_defaults():
+    """The six plain entry points of the header, called through ctypes, give
+    the _ex forms' results with default options (NULL) bit for bit."""
+    import torch
+    import workloads
+    L = sd.lib()
+    vp = ctypes.c_void_p
+    st = vp(torch.cuda.current_stream().cuda_stream)
+    ptr = lambda t: vp(t.data_ptr())
+    case = workloads.small_muon(3, 96, 200, k=4, case_id=51)
+    x32 = torch.from_numpy(case.x.astype(np.float32)).cuda()
+    x16 = x32.to(torch.bfloat16)
+    table = np.ascontiguousarray(case.coeffs, dtype=np.float32)
+    tp = table.ctypes.data_as(vp)
+    b, m, n = x32.shape
+    for name, k, x, dtype in (("sd_msign", 0, x32, sd.SD_DTYPE_F32), ("sd_msign_deflated", 4, x32, sd.SD_DTYPE_F32),
+                              ("sd_msign_bf16", 0, x16, sd.SD_DTYPE_BF16),
+                              ("sd_msign_deflated_bf16", 4, x16, sd.SD_DTYPE_BF16)):
+        a, e = torch.empty_like(x), torch.empty_like(x)
+        fn = getattr(L, name)
+        args = (b, m, n, k, 5, tp) if k else (b, m, n, 5, tp)
+        assert fn(*args, ptr(x), ptr(a), st) == 0
+        assert L.sd_msign_deflated_ex(b, m, n, k, 5, tp, dtype, ptr(x), ptr(e), None, st) == 0
+        torch.cuda.synchronize()
+        print(f"{name}: equal {torch.equal(a, e)}", flush=True)
+        assert torch.equal(a, e) and bool(torch.isfinite(a.float()).all())
+    pc = workloads.small_psd(160, k=8, case_id=52)
+    z = torch.from_numpy(pc.z).cuda()
+    nz = z.shape[0]
+    a, e = torch.empty_like(z), torch.empty_like(z)
+    assert L.sd_psd_project(nz, 10, ptr(z), ptr(a), st) == 0
+    assert L.sd_psd_project_deflated_ex(nz, 0, 10, ptr(z), None, ptr(e), None, st) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(a, e)
+    q0 = torch.from_numpy(np.ascontiguousarray(pc.qwarm[:, :8])).cuda()
+    qa, qe = q0.clone(), q0.clone()
+    assert L.sd_psd_project_deflated(nz, 8, 10, ptr(z), ptr(qa), ptr(a), st) == 0
+    assert L.sd_psd_project_deflated_ex(nz, 8, 10, ptr(z), ptr(qe), ptr(e), None, st) == 0
+    torch.cuda.synchronize()
+    assert torch.equal(a, e) and torch.equal(qa, qe)

@@ -57,6 +57,29 @@ def test_small(n, k):
     assert np.array_equal(o, o.T)
 
 
+@pytest.mark.parametrize("n,k,precision", [(100, 0, "f32"), (256, 8, "f32"), (300, 16, "f32"), (256, 8, "f16")])
+def test_frobenius_scale(n, k, precision):
+    # scale_mode = Frobenius: theta = ||R||_F (||Z||_F undeflated) from the
+    # residual pass, against the oracle's "frobenius" scale
+    case = workloads.small_psd(n, k=max(k, 1), case_id=n + 7)
+    say(f"psd frobenius n={n} k={k} {precision}")
+    out, info, q = gpu_psd(case, k, scale="frobenius", precision=precision)
+    z = case.z.astype(np.float64)
+    mode = "f16" if precision == "f16" else "exact"
+    if k > 0:
+        want, vnext, oinfo = opsd.psd_project_deflated(z, case.qwarm[:, :k].astype(np.float64), steps=case.steps,
+                                                       gamma=case.gamma, subspace_iters=case.subspace_iters,
+                                                       scale="frobenius", mode=mode)
+        assert int(info["n_deflated"]) == oinfo.n_deflated
+        theta = oinfo.theta
+    else:
+        want, theta = opsd.psd_project(z, steps=case.steps, scale="frobenius", mode=mode)
+    err = rel_fro(host64(out), want)
+    say(f"  rel err {err:.3e}  theta {float(info['theta']):.6g} vs {theta:.6g}")
+    assert err < (F16_TOL if precision == "f16" else TOL)
+    assert abs(float(info["theta"]) - theta) <= 1e-5 * theta
+
+
 def test_gate_and_counts():
     case = workloads.small_psd(200, k=8, n_dom=3, dom=(100.0, 300.0), case_id=7)
     out, info, _ = gpu_psd(case, 8, tau=0.1, window=6)

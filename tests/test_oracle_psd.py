@@ -195,3 +195,27 @@ def test_f16_restore_product_within_the_operand_rounding_bound():
     bound = 2.0 ** -11 * theta * (np.linalg.norm(r / theta) * np.linalg.norm(round_f16(g), 2)
                                   + np.linalg.norm(r / theta, 2) * np.linalg.norm(g))
     assert 0 < err <= bound
+
+
+# --- Frobenius scale ----------------------------------------------------------------
+def test_frobenius_scale_closed_form_and_convergence():
+    # With exact Ritz pairs (the basis spans the dominant eigenvectors), the
+    # residual is the rest of the spectrum: theta = sqrt(sum_{i not in I}
+    # lam_i^2) >= ||R||_2, so X0's spectrum lies in [-1, 1] and the classical
+    # filter converges to Pi_+ with enough steps.
+    n, k = 48, 4
+    g = np.random.default_rng(31)
+    lam = np.concatenate([[60.0, -45.0, 30.0, 20.0], g.uniform(-1, 1, n - k)])
+    z, q = sym_case(31, n, lam)
+    order = np.argsort(-np.abs(lam))
+    basis = q[:, order[:k]]
+    p, _, info = psd.psd_project_deflated(z, basis, steps=60, scale="frobenius")
+    tail = np.delete(lam, order[:k])
+    np.testing.assert_allclose(info.theta, np.sqrt(np.sum(tail ** 2)), rtol=1e-12)
+    assert info.theta >= np.max(np.abs(tail))
+    np.testing.assert_allclose(p, psd.psd_exact(z), atol=1e-6 * np.linalg.norm(z))
+    # the undeflated form scales by ||Z||_F
+    pb, theta_b = psd.psd_project(z, steps=5, scale="frobenius")
+    np.testing.assert_allclose(theta_b, np.linalg.norm(z), rtol=1e-12)
+    with pytest.raises(ValueError):
+        psd.psd_project(z, steps=1, scale="spectral")
