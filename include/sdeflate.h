@@ -56,9 +56,10 @@ enum { SD_DTYPE_F32 = 0, SD_DTYPE_BF16 = 1 };
 /* Bits set (atomically OR-ed) in *status_dev when the device meets them. */
 enum {
   SD_FLAG_PIVOT_FLOOR = 2,   /* a CholeskyQR pivot hit its floor: a rank-deficient panel */
-  SD_FLAG_RESIDUAL_FLOOR = 4 /* Muon: a residual at the head's rounding level was dropped
-                                (nu <= rho ||X||_F, rho = 2^-8 bf16, 2^-16 fp32; the
-                                degenerate case rank(X) <= k_eff) */
+  SD_FLAG_RESIDUAL_FLOOR = 4 /* Muon: a residual at the float32 rounding level of the head
+                                was dropped (nu <= 2^-20 ||X||_F: the input has rank
+                                <= k_eff, outside Alg. 1's k < rank(M)); X0 is then
+                                gamma^-1 U_k V_k^T (0 with the explicit restore) */
 };
 
 /* ------------------------------------------------------------------ Muon --
@@ -66,13 +67,13 @@ enum {
  * Alg. 3). For every matrix M of the batch [batch, m, n]:
  *   - orientation: a matrix with m > n is processed as M^T and its result
  *     transposed back, polar(M^T) = polar(M)^T (App. D, grouping);
- *   - head estimate: Alg. 3 with r' = min(min(m, n), k + oversample) sketch
- *     columns and power_iters subspace iterations, one CholeskyQR pass after
- *     every product (float64 Gram and factorization), thin SVD of the
- *     r' x min(m,n) reduced matrix;
+ *   - head estimate: Alg. 3 with r' = min(min(m, n), r + oversample) sketch
+ *     columns (r = k, or the gate's window when set) and power_iters subspace
+ *     iterations, one CholeskyQR pass after every product (float64 Gram and
+ *     factorization), thin SVD of the r' x min(m,n) reduced matrix;
  *   - deflation rank: k (fixed rank, tau = 0), or the gate of Alg. 1 on the
- *     k estimated values: if s_k < tau s_1 deflate max{i : s_i > tau s_1}
- *     components, else none;
+ *     r estimated values: if s_r < tau s_1 deflate min(k, max{i : s_i >
+ *     tau s_1}) components, else none;
  *   - start: X0 = R / ||R||_F + gamma^-1 U_k V_k^T with R = M - U_k S_k V_k^T
  *     (Alg. 1), or X0 = M / ||M||_F when nothing is deflated; a zero norm
  *     drops its term, so a zero matrix maps to zero;
@@ -82,16 +83,23 @@ enum {
  * coeffs: HOST float[steps][3] (a_t, b_t, c_t), or NULL for Muon's retuned
  *   quintic (3.4445, -4.7750, 2.0315) at every step (Sec. 3 setup).
  * Precision: the f32 entry points compute in float32 (MFMA fp32, float32
- *   accumulation). The bf16 entry points take bfloat16 input and output
- *   (uint16_t bit patterns); every matrix product takes bf16 operands with
- *   float32 accumulation, the iterate is stored in bf16, the Gram A in float32
- *   (and rounded to bf16 where it is a product operand), b A + c A^2 is
- *   rounded to bf16, and the sketch panels, norms and small factorizations are
- *   float32 / float64.
+ *   accumulation); their sketch products accumulate in float64 and the
+ *   residual M - U_k S_k V_k^T is formed in float64 (rounded once). The bf16
+ *   entry points take bfloat16 input and output (uint16_t bit patterns). Their
+ *   front end runs at float32 precision: the sketch products take each float32
+ *   panel as two bf16 operands (hi, lo) with float32 accumulation. Every
+ *   product of the filter takes bf16 operands with float32 accumulation. The
+ *   iterate is stored in 3 bytes per element: hi = bf16(X), the product
+ *   operand, plus an OCP float8 e4m3 byte holding (X - hi) 2^16, carried as
+ *   hi + e4m3 2^-16. The Gram A is kept in float32 (rounded to bf16 where it
+ *   is a product operand), b A + c A^2 is rounded to bf16, and the sketch
+ *   panels, norms and small factorizations are float32 / float64.
  * Requirements: batch >= 1, m, n >= 1, 0 <= k < min(m, n), k + oversample
  *   capped at min(m, n) must not exceed 64 (else SD_ERR_UNSUPPORTED),
  *   0 <= steps <= 1000. k = 0 is the undeflated baseline, and the gated
  *   variant that deflates nothing returns the baseline bit for bit (Sec. 2.2).
+ * Orientation of the sketch: Alg. 3 takes A = M for n >= m (square included)
+ *   and A = M^T for a wide M, and sketches A's columns (Y = A Omega).
  */
 /* How the deflated head returns (eq:identities: polar(M) = U_k V_k^T + polar(R_k)):
  *   PADDED (Alg. 1): X0 = R / ||R||_F + gamma^-1 U_k V_k^T, and the filter

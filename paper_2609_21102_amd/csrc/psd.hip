@@ -698,7 +698,8 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     la.out = p.r;
     la.sumsq = p.sumsq;   // Frobenius scale: tile sums of R^2
     lowrank<float, float>(la, st);
-    // next basis: CholQR(Zt), written back after the filter
+    // next basis: CholQR(Zt), written to the caller's Qwarm now (Z V was the
+    // last read of the old basis; nothing after this reads Qwarm)
     cholqr(zt, 0, np, K, np, 1, p.part, p.fac, o.status_dev, st);
     hipLaunchKernelGGL(panel_to_rows_kernel, grid1((long long)n * K, 256), dim3(256), 0, st, zt, np, K, n, Qwarm);
   } else {
