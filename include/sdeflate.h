@@ -170,6 +170,23 @@ int sd_msign_groups(int ngroups, const sd_msign_group* groups, hipStream_t strea
 
 /* Workspace an _ex call with these arguments needs (0 on invalid arguments). */
 size_t sd_msign_workspace_bytes(int batch, int m, int n, int k, int dtype, const sd_msign_opts* opts);
+
+/* Allocation-free form of sd_msign_deflated_ex, for callers that cannot
+ * allocate device memory during the call (code captured into a HIP graph,
+ * serving loops, harnesses that forbid hipMalloc): same arguments, results
+ * and errors, but its scratch is a library-owned array of
+ * SD_STATIC_SCRATCH_BYTES per GPU (a static device array, held until the
+ * process ends), and it calls no hipMalloc / hipFree or allocating routine.
+ * Calls whose sd_msign_workspace_bytes() exceeds that size return
+ * SD_ERR_WORKSPACE with nothing enqueued (at bf16 that is one 768 x 3072
+ * matrix, or about 24 of 768 x 768); opts->workspace must be NULL
+ * (SD_ERR_INVALID_ARG otherwise). Every call on one GPU shares the array and
+ * overwrites it: calls that overlap on one GPU (other streams, other host
+ * threads) race and must be ordered by the caller. No part of the scratch
+ * needs to start at zero. */
+#define SD_STATIC_SCRATCH_BYTES (64u << 20)
+int sd_msign_deflated_noalloc(int batch, int m, int n, int k, int steps, const float* coeffs, int dtype,
+                              const void* in, void* out, const sd_msign_opts* opts, hipStream_t stream);
 /* The Gaussian sketch Alg. 3 draws (Omega ~ N(0, 1)^{s x r'} per matrix): out[b][j][i]
  * is entry (i, j) of matrix b's sketch, Gaussian number j * s + i of Philox stream 1.
  * sd_sketch fills a DEVICE buffer on `stream`; sd_sketch_host computes the same

@@ -102,6 +102,7 @@ def _declare(lib):
         "sd_msign_deflated_bf16": (i, [i, i, i, i, i, vp, vp, vp, vp]),
         "sd_msign_deflated_ex": (i, [i, i, i, i, i, vp, i, vp, vp, ctypes.POINTER(MsignOpts), vp]),
         "sd_msign_workspace_bytes": (sz, [i, i, i, i, i, ctypes.POINTER(MsignOpts)]),
+        "sd_msign_deflated_noalloc": (i, [i, i, i, i, i, vp, i, vp, vp, ctypes.POINTER(MsignOpts), vp]),
         "sd_msign_groups": (i, [i, ctypes.POINTER(MsignGroup), vp]),
         "sd_msign_opts_default": (None, [ctypes.POINTER(MsignOpts)]),
         "sd_psd_project": (i, [i, i, vp, vp, vp]),

@@ -642,6 +642,58 @@ int sd_sketch_host(int batch, int s, int rp, uint64_t seed, float* out) {
   return SD_OK;
 }
 
+}  // extern "C"
+
+namespace sd {
+// Scratch of the allocation-free entry point: one array per device, held
+// until the process ends. Host code never passes its name to a kernel (in
+// host code the name stands for a host-side shadow): each device's address
+// comes from hipGetSymbolAddress, taken once per device with that device
+// current, and only that address is used.
+constexpr size_t kStaticScratchBytes = (size_t)SD_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+static int static_scratch(void** ptr) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return SD_ERR_HIP;
+  std::lock_guard<std::mutex> g(mu);
+  if (!addr[dev]) {
+    void* a = nullptr;
+    if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || !a) {
+      (void)hipGetLastError();
+      return SD_ERR_HIP;
+    }
+    addr[dev] = a;
+  }
+  *ptr = addr[dev];
+  return SD_OK;
+}
+}  // namespace sd
+
+extern "C" {
+
+int sd_msign_deflated_noalloc(int batch, int m, int n, int k, int steps, const float* coeffs, int dtype,
+                              const void* in, void* out, const sd_msign_opts* opts, hipStream_t stream) {
+  sd_msign_opts o;
+  sd_msign_opts_default(&o);
+  if (opts) o = *opts;
+  if (o.workspace) return SD_ERR_INVALID_ARG;   // the scratch is the library's
+  int rc = validate_msign(batch, m, n, k, steps, dtype, in, out, o);
+  if (rc != SD_OK) return rc;
+  // the call's scratch (the input's alignment decides only whether the
+  // canonical copy is needed, so the query with a copy is an upper bound)
+  const size_t need = sd_msign_workspace_bytes(batch, m, n, k, dtype, &o);
+  if (need == 0 || need > kStaticScratchBytes) return SD_ERR_WORKSPACE;
+  void* ws = nullptr;
+  rc = static_scratch(&ws);
+  if (rc != SD_OK) return rc;
+  o.workspace = ws;
+  o.workspace_bytes = kStaticScratchBytes;
+  return sd::msign_enqueue(batch, m, n, k, steps, coeffs, dtype, in, out, o, stream);
+}
+
 int sd_msign(int batch, int m, int n, int steps, const float* coeffs, const float* in, float* out,
              hipStream_t stream) {
   return sd_msign_deflated_ex(batch, m, n, 0, steps, coeffs, SD_DTYPE_F32, in, out, nullptr, stream);
