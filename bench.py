@@ -8,15 +8,25 @@ bulk in [1e-4, 1]; deflation rank k = 8, oversample 8, one power iteration,
 5 steps of Muon's quintic (3.4445, -4.7750, 2.0315), gamma = 1.01. Inputs are
 seeded and synthetic and are resident in HBM before the timed region.
 
-Prints one JSON line: matrices/s (value), the achieved TFLOP/s against the
-bf16 MFMA peak, a roofline entry for the dominant kernel (the iterate update
-X <- a X + B X, timed with HIP events inside the timed region; its
-arithmetic intensity, about 120 flop per byte, is below the bf16 ridge of
-about 310, so it is priced against HBM) and the CPU oracle timed on a bounded
-sample of the same workload.
-
---copy-calibration adds one plain device copy of 256 MiB before the timed
-region, the reference kernel for scaling the FETCH_SIZE / WRITE_SIZE counters.
+Prints one JSON line:
+  value      matrices/s over the timed calls;
+  roofline   the dominant kernel, the iterate update X <- a X + B X, priced
+             against the bf16 dense MFMA peak with its algorithmic flops
+             2 s^2 l per matrix, timed with HIP events around every launch
+             inside the timed region; traffic = HBM bytes per launch measured
+             by two rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE) run as
+             child processes before the timed region and scaled by the same
+             counters' reading of a plain 256 MiB copy, beside the algorithmic
+             bytes (read X and B, write X, all bf16);
+  stages     every stage of the call from HIP events around each launch (a
+             second pass of the same calls): the filter's Gram, polynomial and
+             update against the MFMA peak, the sketch products, the rank-k
+             passes and the CholeskyQR panels against HBM, each with its
+             algorithmic work, and the whole-call fraction sum_stage
+             max(flops / MFMA peak, bytes / HBM peak) / call time;
+  cpu_baseline  the CPU oracle on a bounded sample, at all cores and at one
+             thread.
+--workload selects further configurations (one JSON line each).
 """
 from __future__ import annotations
 
@@ -53,74 +63,204 @@ def front_flops_per_matrix(s: int, l: int, k: int, rp: int, power_iters: int) ->
     return (2 + 2 * power_iters) * 2.0 * s * l * rp + 2 * 2.0 * s * l * k
 
 
-def update_bytes_per_matrix(s: int, l: int, steps: int) -> float:
-    """Algorithmic HBM bytes of the iterate updates of one s x l matrix,
-    averaged over the call's launches. The bf16 iterate is stored as hi (bf16)
-    plus an 8-bit residual. Every step reads B (bf16, s x s), the operand hi
-    (s x l; the a X term takes hi from the same tiles) and the residuals; the
-    first steps - 1 write the next hi and residuals, the last writes the bf16
-    output."""
-    inner = 2.0 * s * s + 2 * s * l + 1 * s * l + 3 * s * l
-    last = 2.0 * s * s + 2 * s * l + 1 * s * l + 2 * s * l
-    return ((steps - 1) * inner + last) / steps
+def update_bytes_algorithmic(s: int, l: int) -> float:
+    """Algorithmic HBM bytes of one update X <- a X + B X of an s x l matrix
+    with a bf16 carry: read X and B, write X (2 bytes each)."""
+    return 2.0 * s * l + 2.0 * s * s + 2.0 * s * l
 
 
-KERNEL_SOURCES = ("gemm.hpp", "common.hpp", "msign.hip")
+def stage_work(s: int, l: int, k: int, rp: int, power_iters: int, steps: int) -> dict:
+    """Algorithmic work per matrix of one call, by stage: (flops, bytes)."""
+    return {
+        "ns_gram": (steps * s * (s + 1.0) * l, 0.0),
+        "ns_poly": (steps * s * (s + 1.0) * s, 0.0),
+        "ns_update": (steps * 2.0 * s * s * l, steps * update_bytes_algorithmic(s, l)),
+        # each pass over X reads it once (bf16); 2 s l r' flops
+        "sketch": ((2 + 2 * power_iters) * 2.0 * s * l * rp, (2 + 2 * power_iters) * 2.0 * s * l),
+        # residual norm: read X; padded start: read X, write X0 (bf16 carry)
+        "lowrank": (2 * 2.0 * s * l * k, 2.0 * s * l + 4.0 * s * l),
+        # two passes over an fp32 panel per CholeskyQR: the l-side panel
+        # 1 + J times, the s-side J times
+        "cholqr": (0.0, 2 * 4.0 * rp * ((1 + power_iters) * l + power_iters * s)),
+        "small": (0.0, 0.0),
+    }
 
 
-def kernel_hash() -> str:
-    """Hash of the sources the update kernel is built from."""
-    h = hashlib.sha256()
-    csrc = os.path.join(ROOT, "paper_2609_21102_amd", "csrc")
-    for name in KERNEL_SOURCES:
-        with open(os.path.join(csrc, name), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
+STAGE_PEAKS = {"mfma_bf16_tflops": 2500.0, "hbm_gbs": 8000.0}
 
 
-def measured_traffic():
-    """HBM bytes per update launch from the committed counter summary, or
-    None when the kernel sources changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", "ns_update_768x3072_bf16_traffic.txt")
-    if not os.path.exists(path):
-        return None
-    vals = {}
-    with open(path) as f:
-        for line in f:
-            if "=" in line and not line.startswith("#"):
-                k, v = line.split("=", 1)
-                vals[k.strip()] = v.strip()
-    if vals.get("kernel_hash") != kernel_hash():
-        return None
+def stage_table(times_ms: dict, work: dict, batch: int, calls: int, call_ms: float) -> dict:
+    """Per-stage achieved rates and roofline fractions, plus the whole-call
+    fraction: sum over stages of max(flops / MFMA peak, bytes / HBM peak),
+    divided by the call time."""
+    out, ideal_ms = {}, 0.0
+    for name, (ms_tot, launches) in times_ms.items():
+        flops, nbytes = work[name]
+        flops *= batch
+        nbytes *= batch
+        ms = ms_tot / calls
+        t_mfma = flops / (STAGE_PEAKS["mfma_bf16_tflops"] * 1e12) * 1e3
+        t_hbm = nbytes / (STAGE_PEAKS["hbm_gbs"] * 1e9) * 1e3
+        bound = "mfma" if t_mfma >= t_hbm else "hbm"
+        if flops == 0 and nbytes == 0:
+            bound = "latency"
+        ideal_ms += max(t_mfma, t_hbm)
+        row = {"ms_per_call": ms, "launches_per_call": launches / calls, "bound": bound}
+        if flops:
+            row["tflops"] = flops / (ms / 1e3) / 1e12
+        if nbytes:
+            row["gbs"] = nbytes / (ms / 1e3) / 1e9
+        if bound != "latency":
+            row["frac"] = max(t_mfma, t_hbm) / ms
+        out[name] = row
+    chain = [n for n in ("ns_gram", "ns_poly", "ns_update") if n in out]
+    if chain:
+        fl = sum(work[n][0] for n in chain) * batch
+        ms = sum(out[n]["ms_per_call"] for n in chain)
+        out["ns_chain"] = {"ms_per_call": ms, "tflops": fl / (ms / 1e3) / 1e12, "bound": "mfma",
+                           "frac": fl / (ms / 1e3) / 1e12 / STAGE_PEAKS["mfma_bf16_tflops"]}
+    return {"stages": out, "whole_call_frac": ideal_ms / call_ms, "ideal_ms": ideal_ms, "call_ms": call_ms}
+
+
+def cpu_model() -> str:
     try:
-        return float(vals["traffic_bytes_per_launch"])
-    except (KeyError, ValueError):
-        return None
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+# ------------------------------------------------- live counter passes ----
+COUNTERS = ("FETCH_SIZE", "WRITE_SIZE")
+COPY_KIB = 262144.0   # the calibration copy moves 256 MiB each way
+
+
+def counter_pass_child(args) -> int:
+    """Child of a rocprofv3 --pmc run: one calibration copy of 256 MiB and a
+    few calls of the workload (input from the parent's file)."""
+    import torch
+    import paper_2609_21102_amd as sd
+    import workloads
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    case = workloads.config2("768x3072", batch=1)   # parameters only; the input comes from the file
+    bits = np.load(args.counter_pass)
+    b, m, n = bits.shape
+    x = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).to(dev)
+    out = torch.empty_like(x)
+    src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
+    for _ in range(3):
+        sd.msign(x, case.k, case.steps, case.coeffs, oversample=case.oversample, power_iters=case.power_iters,
+                 gamma=case.gamma, out=out)
+    torch.cuda.synchronize()
+    return 0
+
+
+KERNEL_KEYS = {"ns_update": "EpiUpdateHL", "ns_gram": "EpiGramT", "ns_poly": "EpiPoly",
+               "sketch": "EpiStoreRowsSplit", "lowrank": "lowrank_kernel"}
+
+
+def counter_traffic(bits: np.ndarray, timeout_s: float = 180.0) -> dict:
+    """HBM bytes per launch of the path's kernels from two rocprofv3 --pmc
+    passes over child runs of this script (no GPU is used in this process
+    before they end). Returns {"per_kernel": {stage: bytes per launch}, ...}
+    or {"error": ...}."""
+    import shutil
+    import sqlite3
+    import subprocess
+    import tempfile
+    exe = shutil.which("rocprofv3") or "/opt/rocm/bin/rocprofv3"
+    if not os.path.exists(exe):
+        return {"error": "rocprofv3 not found"}
+    tmp = tempfile.mkdtemp(prefix="sdbench_", dir="/tmp")
+    xpath = os.path.join(tmp, "x.npy")
+    np.save(xpath, bits)
+    env = dict(os.environ, TMPDIR="/tmp")
+    readings = {}
+    for ctr in COUNTERS:
+        outdir = os.path.join(tmp, ctr)
+        cmd = [exe, "--pmc", ctr, "-d", outdir, "-o", "run", "--", sys.executable, os.path.abspath(__file__),
+               "--counter-pass", xpath]
+        log(f"bench: counter pass {ctr}")
+        proc = subprocess.Popen(cmd, cwd="/tmp", env=env, stdout=subprocess.DEVNULL, stderr=subprocess.PIPE,
+                                start_new_session=True)
+        try:
+            _, err = proc.communicate(timeout=timeout_s)
+        except subprocess.TimeoutExpired:
+            os.killpg(proc.pid, 9)
+            proc.wait()
+            return {"error": f"counter pass {ctr} timed out"}
+        dbs = [os.path.join(d, f) for d, _, fs in os.walk(outdir) for f in fs if f.endswith("_results.db")]
+        if proc.returncode != 0 and not dbs:
+            return {"error": f"counter pass {ctr} failed ({proc.returncode}): {err.decode()[-300:]}"}
+        if not dbs:
+            return {"error": f"counter pass {ctr}: no results database"}
+        rows = []
+        for db in dbs:
+            con = sqlite3.connect(db)
+            rows += con.execute("select kernel_name, dispatch_id, sum(value) from counters_collection "
+                                "where counter_name = ? group by dispatch_id", (ctr,)).fetchall()
+            con.close()
+        readings[ctr] = rows
+    shutil.rmtree(tmp, ignore_errors=True)
+
+    def mean_kib(ctr, key):
+        vals = [v for name, _, v in readings[ctr] if key in name]
+        return (sum(vals) / len(vals), len(vals)) if vals else (None, 0)
+
+    fetch_copy, _ = mean_kib("FETCH_SIZE", "copyBuffer")
+    write_copy, _ = mean_kib("WRITE_SIZE", "copyBuffer")
+    if not fetch_copy or not write_copy:
+        return {"error": "calibration copy not found in the counter data"}
+    ff, wf = COPY_KIB / fetch_copy, COPY_KIB / write_copy
+    per = {}
+    for stage, key in KERNEL_KEYS.items():
+        f, nf = mean_kib("FETCH_SIZE", key)
+        w, nw = mean_kib("WRITE_SIZE", key)
+        if f is not None and w is not None:
+            per[stage] = {"bytes_per_launch": 1024.0 * (f * ff + w * wf), "dispatches": nf}
+    return {"per_kernel": per, "fetch_factor": ff, "write_factor": wf,
+            "method": "rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE (KiB per dispatch), on child runs of "
+                      "this script with 3 calls; scaled by the counters' reading of a 256 MiB device copy"}
 
 
 def cpu_baseline(case, seconds: float) -> dict:
     """The oracle (bf16-contract mode, float64) on whole matrices of the same
-    workload, cycling through the batch until `seconds` have passed."""
-    from threadpoolctl import threadpool_info
+    workload, cycling through the batch until `seconds` have passed: once
+    with the BLAS threads it finds, once with one thread."""
+    from threadpoolctl import threadpool_info, threadpool_limits
     from oracle import muon as omuon
     from oracle import rng as orng
     b = case.x.shape[0]
     s = min(case.x.shape[1:])
     rp = min(s, case.k + case.oversample)
     threads = max([d.get("num_threads", 1) for d in threadpool_info()] or [1])
-    done, t0 = 0, time.perf_counter()
-    while True:
-        idx = done % b
-        omuon.msign_deflated(case.x64[idx:idx + 1], case.k, case.coeffs, oversample=case.oversample,
-                             power_iters=case.power_iters, gamma=case.gamma, mode="bf16",
-                             sketches=[orng.sketch(0, idx, s, rp)])
-        done += 1
-        if time.perf_counter() - t0 >= seconds:
-            break
-    dt = time.perf_counter() - t0
+
+    def run(sec):
+        done, t0 = 0, time.perf_counter()
+        while True:
+            idx = done % b
+            omuon.msign_deflated(case.x64[idx:idx + 1], case.k, case.coeffs, oversample=case.oversample,
+                                 power_iters=case.power_iters, gamma=case.gamma, mode="bf16",
+                                 sketches=[orng.sketch(0, idx, s, rp)])
+            done += 1
+            if time.perf_counter() - t0 >= sec:
+                return done, time.perf_counter() - t0
+
+    done, dt = run(seconds)
+    with threadpool_limits(limits=1):
+        done1, dt1 = run(seconds)
     return {"value": done / dt, "unit": "matrices/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{done} matrices 768x3072 (cycling through the batch of {b}), float64 oracle in "
-                      f"bf16-contract mode, {dt:.1f} s"}
+            "value_1thread": done1 / dt1, "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count(),
+            "sample": f"{done} matrices 768x3072 at {threads} threads in {dt:.1f} s and {done1} at one thread "
+                      f"in {dt1:.1f} s (cycling through the batch of {b}), float64 oracle in bf16-contract mode"}
 
 
 def _timed(step, steps: int, warmup: int) -> float:
@@ -222,26 +362,22 @@ def other_workload(args) -> int:
             def step():
                 sd.msign_groups(groups)
         ms = _timed(step, args.steps, args.warmup)
-        # the update of every group, summed: bytes and flops over launch time
-        # (grouped calls run groups concurrently, so launch times overlap)
+        # the update of every group, summed: flops over launch time (grouped
+        # calls run groups concurrently, so launch times overlap), against the
+        # bf16 MFMA peak
         upd_ms, upd_n = _stage_time(sd, step, args.steps, "ns_update")
         upd_bytes = upd_flops = 0.0
         for c in cases:
             b_, s_, l_ = c.x.shape[0], min(c.x.shape[1:]), max(c.x.shape[1:])
-            upd_bytes += b_ * update_bytes_per_matrix(s_, l_, c.steps) * c.steps * args.steps
+            upd_bytes += b_ * update_bytes_algorithmic(s_, l_) * c.steps * args.steps
             upd_flops += b_ * 2.0 * s_ * s_ * l_ * c.steps * args.steps
-        sec = upd_ms / 1e3
-        if upd_flops / upd_bytes > MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9):
-            ach = upd_flops / sec / 1e12
-            roof = {"bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": ach / MFMA_BF16_PEAK_TFLOPS, "flops_per_launch": upd_flops / max(upd_n, 1)}
-        else:
-            ach = upd_bytes / sec / 1e9
-            roof = {"bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBS,
-                    "bytes_per_launch": upd_bytes / max(upd_n, 1)}
-        roof.update({"kernel": "iterate update X <- a X + B X (gemm_dma_kernel, EpiUpdateHL), all groups",
-                     "traffic": None, "avg_launch_us": upd_ms * 1e3 / max(upd_n, 1), "launches": upd_n,
-                     "flop_per_byte": upd_flops / upd_bytes})
+        ach = upd_flops / (upd_ms / 1e3) / 1e12
+        roof = {"bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": ach / MFMA_BF16_PEAK_TFLOPS, "flops_per_launch": upd_flops / max(upd_n, 1),
+                "algorithmic_bytes_per_launch": upd_bytes / max(upd_n, 1),
+                "kernel": "iterate update X <- a X + B X (gemm_dma_kernel, EpiUpdateHL), all groups",
+                "traffic": None, "avg_launch_us": upd_ms * 1e3 / max(upd_n, 1), "launches": upd_n,
+                "flop_per_byte": upd_flops / upd_bytes}
         desc = " + ".join(f"{c.x.shape[0]} x {c.x.shape[1]} x {c.x.shape[2]}" for c in cases)
         res = {"metric": f"deflated msign matrices/s ({args.workload}: {desc} bf16)", "value": nmat / (ms / 1e3),
                "unit": "matrices/s", "ms_per_step": ms, "tflops": flops / (ms / 1e3) / 1e12,
@@ -251,6 +387,85 @@ def other_workload(args) -> int:
                           "launch": "one call per group" if args.sequential else "sd_msign_groups",
                           "k": [c.k for c in cases], "filter_steps": [c.steps for c in cases]},
                "roofline": roof}
+    elif args.workload == "peaks":
+        # re-measured roofline constants: dense bf16 MFMA rate, HBM copy and
+        # read bandwidth, and the vendor batched GEMM (torch.bmm) on the
+        # update's shape (24 x (768 x 768) x (768 x 3072) bf16) for scale
+        import ctypes
+        plib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_21102_amd", "libsdpeaks.so"))
+        vp = ctypes.c_void_p
+        plib.sdp_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp]
+        plib.sdp_copy.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, vp]
+        plib.sdp_read.argtypes = [vp, ctypes.c_size_t, ctypes.c_int, vp, vp]
+        st = vp(torch.cuda.current_stream().cuda_stream)
+        sink = torch.zeros(1 << 16, dtype=torch.float32, device=dev)
+
+        def timed_ms(fn, reps=5):
+            fn()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(reps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / reps
+
+        blocks, iters = 4096, 256
+        mf_ms = timed_ms(lambda: plib.sdp_mfma_bf16(blocks, iters, vp(sink.data_ptr()), st))
+        mf_tf = blocks * 4 * 8 * iters * 32768.0 / (mf_ms / 1e3) / 1e12
+        n4 = (1 << 30) // 16
+        src = torch.ones(n4 * 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        cp_ms = timed_ms(lambda: plib.sdp_copy(vp(src.data_ptr()), vp(dst.data_ptr()), n4, 256 * 32, st))
+        rd_ms = timed_ms(lambda: plib.sdp_read(vp(src.data_ptr()), n4, 256 * 32, vp(sink.data_ptr()), st))
+        del src, dst
+        a16 = torch.randn(24, 768, 768, device=dev).to(torch.bfloat16)
+        x16 = torch.randn(24, 768, 3072, device=dev).to(torch.bfloat16)
+        bmm_ms = timed_ms(lambda: torch.bmm(a16, x16), reps=20)
+        bmm_tf = 2.0 * 768 * 768 * 3072 * 24 / (bmm_ms / 1e3) / 1e12
+        res = {"metric": "measured peaks (bf16 MFMA TFLOP/s, HBM GB/s)", "value": mf_tf, "unit": "TFLOP/s",
+               "ms_per_step": mf_ms, "steps": 5, "warmup": 1, "dtype": "bf16", "data": "synthetic",
+               "config": {"workload": "peaks"},
+               "measured_peaks": {"mfma_bf16_tflops": mf_tf, "mfma_bf16_frac_of_2500": mf_tf / 2500.0,
+                                  "hbm_copy_gbs": 2.0 * (1 << 30) / (cp_ms / 1e3) / 1e9,
+                                  "hbm_read_gbs": 1.0 * (1 << 30) / (rd_ms / 1e3) / 1e9,
+                                  "bmm_update_shape_us": bmm_ms * 1e3, "bmm_update_shape_tflops": bmm_tf},
+               "roofline": {"bound": "mfma", "kernel": "sdp_mfma_bf16_kernel", "achieved": mf_tf, "peak": 2500.0,
+                            "unit": "TFLOP/s", "frac": mf_tf / 2500.0, "traffic": None,
+                            "avg_launch_us": mf_ms * 1e3, "launches": 5}}
+        log(f"bench peaks: {json.dumps(res['measured_peaks'])}")
+        print(json.dumps(res), flush=True)
+        return 0
+    elif args.workload == "c1":
+        # config 1: one float32 256 x 256 matrix, k = 4, 2 power iterations, 5 steps;
+        # a step is one call (latency-bound: every stage is one small launch)
+        case = workloads.config1()
+        x = torch.from_numpy(case.x.astype(np.float32)).to(dev)
+        out = torch.empty_like(x)
+        ws = torch.empty(sd.msign_workspace_bytes(1, 256, 256, case.k, sd.SD_DTYPE_F32, power_iters=case.power_iters),
+                         dtype=torch.uint8, device=dev)
+
+        def step():
+            sd.msign(x, case.k, case.steps, case.coeffs, oversample=case.oversample,
+                     power_iters=case.power_iters, gamma=case.gamma, out=out, workspace=ws)
+
+        ms = _timed(step, args.steps, args.warmup)
+        upd_ms, upd_n = _stage_time(sd, step, args.steps, "ns_update")
+        s_ = l_ = 256
+        fl = 2.0 * s_ * s_ * l_
+        ach = fl / (upd_ms / max(upd_n, 1) / 1e3) / 1e12
+        work = stage_work(s_, l_, case.k, min(s_, case.k + case.oversample), case.power_iters, case.steps)
+        flops = sum(w[0] for w in work.values())
+        res = {"metric": "deflated msign matrices/s (config 1: 1 x 256 x 256 float32, k = 4, J = 2, 5 steps)",
+               "value": 1e3 / ms, "unit": "matrices/s", "ms_per_step": ms, "tflops": flops / (ms / 1e3) / 1e12,
+               "steps": args.steps, "warmup": args.warmup, "dtype": "f32", "data": "synthetic",
+               "config": {"workload": "c1", "m": 256, "n": 256, "k": case.k, "power_iters": case.power_iters,
+                          "filter_steps": case.steps},
+               "roofline": {"bound": "mfma", "kernel": "iterate update X <- a X + B X (gemm_kernel, fp32)",
+                            "achieved": ach, "peak": 157.3, "unit": "TFLOP/s", "frac": ach / 157.3,
+                            "traffic": None, "avg_launch_us": upd_ms * 1e3 / max(upd_n, 1), "launches": upd_n,
+                            "flops_per_launch": fl}}
     elif args.workload == "admm":
         # ADMM on a max-cut relaxation of the size of the paper's n = 5000
         # instances (planted-bisection random graph), tracked basis K = 64
@@ -337,13 +552,13 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--baseline", action="store_true", help="time the undeflated filter (k = 0) instead")
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="run one plain 256 MiB device copy before timing (counter calibration)")
+    ap.add_argument("--no-counters", action="store_true", help="skip the rocprofv3 counter passes")
+    ap.add_argument("--counter-pass", default=None, help=argparse.SUPPRESS)
     ap.add_argument("--workload", default="headline",
-                    choices=["headline", "c2-step", "c3", "paper-step", "c4", "c5", "admm"],
+                    choices=["headline", "c1", "c2-step", "c3", "paper-step", "c4", "c5", "admm", "peaks"],
                     help="headline: the benchmark line; the others time further configurations "
                          "(one JSON line each, no roofline or CPU baseline)")
     ap.add_argument("--precision", default="f32", choices=["f32", "f16"],
@@ -359,6 +574,9 @@ def main() -> int:
             "(sharding the batch by matrix across GPUs is not implemented)")
         return 2
 
+    if args.counter_pass:
+        return counter_pass_child(args)
+
     import torch
     import paper_2609_21102_amd as sd
     import workloads
@@ -371,6 +589,13 @@ def main() -> int:
     k = 0 if args.baseline else case.k
     s, l = min(m, n), max(m, n)
     rp = min(s, k + case.oversample) if k else 0
+    # HBM traffic: two counter passes in child processes, before this
+    # process uses the GPU
+    traffic = None
+    if not args.no_counters and not args.baseline:
+        traffic = counter_traffic(case.x)
+        if "error" in traffic:
+            log(f"bench: counters unavailable: {traffic['error']}")
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     x = torch.from_numpy(case.x.view(np.int16).copy()).view(torch.bfloat16).to(dev)
@@ -383,19 +608,14 @@ def main() -> int:
                  gamma=case.gamma, out=out, workspace=ws)
 
     log(f"bench: {b} x {m} x {n} bf16, k={k}, warmup {args.warmup}, steps {args.steps}")
-    if args.copy_calibration:
-        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
+    # timed region: events around every update launch (on the library's
+    # stream) and after every call
     sd.profile_reset()
     sd.profile_set("ns_update")
-    # an event after every step on the call's stream: the per-step spread
     marks = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     marks[0].record()
@@ -410,21 +630,47 @@ def main() -> int:
     upd_ms, upd_n = sd.profile_read("ns_update")
     ms_per_step = ms_total / args.steps
     value = b * args.steps / (ms_total / 1e3)
-    flops = b * (ns_flops_per_matrix(s, l, case.steps) + (front_flops_per_matrix(s, l, k, rp, case.power_iters)
-                                                          if k else 0.0))
+    work = stage_work(s, l, k, rp, case.power_iters, case.steps)
+    flops = b * sum(w[0] for w in work.values()) if k else b * (work["ns_gram"][0] + work["ns_poly"][0] +
+                                                                 work["ns_update"][0])
     tflops = flops / (ms_per_step / 1e3) / 1e12
-    # totals over the timed calls, divided by the update launches they made
-    # (one per filter step, or two when a call runs its batch in two halves)
     n_launch = max(upd_n, 1)
-    upd_flops = 2.0 * s * s * l * b * case.steps * args.steps / n_launch
-    upd_bytes = update_bytes_per_matrix(s, l, case.steps) * b * case.steps * args.steps / n_launch
+    upd_flops = b * work["ns_update"][0] * args.steps / n_launch
+    upd_alg_bytes = b * work["ns_update"][1] * args.steps / n_launch
     upd_avg_ms = upd_ms / n_launch
     upd_tflops = upd_flops / (upd_avg_ms / 1e3) / 1e12
-    upd_gbs = upd_bytes / (upd_avg_ms / 1e3) / 1e9
-    log(f"bench: {ms_per_step:.3f} ms/step, {value:.0f} matrices/s, {tflops:.1f} TFLOP/s; "
-        f"update kernel {upd_avg_ms * 1e3:.1f} us avg over {upd_n} launches "
-        f"({upd_gbs:.0f} GB/s algorithmic, {upd_tflops:.1f} TFLOP/s)")
 
+    # every stage, from events around each launch over the same number of calls
+    names = ["ns_gram", "ns_poly", "ns_update"] + (["sketch", "cholqr", "small", "lowrank"] if k else ["lowrank"])
+    sd.profile_reset()
+    sd.profile_set(*names)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    sd.profile_set()
+    times = {nm: sd.profile_read(nm) for nm in names}
+    table = stage_table(times, work, b, args.steps, ms_per_step)
+    log(f"bench: {ms_per_step:.3f} ms/step, {value:.0f} matrices/s, {tflops:.1f} TFLOP/s; "
+        f"update {upd_avg_ms * 1e3:.1f} us avg over {upd_n} launches ({upd_tflops:.1f} TFLOP/s, "
+        f"{100 * upd_tflops / MFMA_BF16_PEAK_TFLOPS:.1f}% of bf16 MFMA); whole call "
+        f"{100 * table['whole_call_frac']:.1f}% of its roofline")
+    for nm, row in table["stages"].items():
+        log(f"  {nm:10s} {row['ms_per_call'] * 1e3:8.1f} us/call  {row['bound']:7s} "
+            + (f"{100 * row['frac']:5.1f}%" if "frac" in row else ""))
+
+    tr = None
+    if traffic and "per_kernel" in traffic and "ns_update" in traffic["per_kernel"]:
+        tr = traffic["per_kernel"]["ns_update"]["bytes_per_launch"]
+        for nm, row in traffic["per_kernel"].items():
+            if nm in table["stages"]:
+                table["stages"][nm]["traffic_bytes_per_launch"] = row["bytes_per_launch"]
+    roofline = {"bound": "mfma", "kernel": "iterate update X <- a X + B X (gemm_dma_kernel, EpiUpdateHL)",
+                "achieved": upd_tflops, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": upd_tflops / MFMA_BF16_PEAK_TFLOPS, "traffic": tr,
+                "flops_per_launch": upd_flops, "avg_launch_us": upd_avg_ms * 1e3, "launches": upd_n,
+                "algorithmic_bytes_per_launch": upd_alg_bytes,
+                "traffic_over_algorithmic": (tr / upd_alg_bytes) if tr else None,
+                "traffic_method": (traffic or {}).get("method") if tr else (traffic or {}).get("error")}
     result = {
         "metric": "deflated msign matrices/s + TFLOP/s (% MFMA peak), batched 768x3072 bf16",
         "value": value,
@@ -444,12 +690,9 @@ def main() -> int:
                    "batch": b, "m": m, "n": n, "k": k, "steps": case.steps, "parallelism": "single GPU"},
         "tflops": tflops,
         "mfma_frac": tflops / MFMA_BF16_PEAK_TFLOPS,
-        "roofline": {"bound": "hbm", "kernel": "iterate update X <- a X + B X (gemm_dma_kernel, EpiUpdateHL)",
-                     "achieved": upd_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": upd_gbs / HBM_PEAK_GBS, "traffic": measured_traffic(),
-                     "bytes_per_launch": upd_bytes, "avg_launch_us": upd_avg_ms * 1e3,
-                     "launches": upd_n, "tflops": upd_tflops,
-                     "mfma_frac": upd_tflops / MFMA_BF16_PEAK_TFLOPS, "kernel_hash": kernel_hash()},
+        "roofline": roofline,
+        "stages": table["stages"],
+        "whole_call_frac": table["whole_call_frac"],
     }
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")

@@ -11,6 +11,9 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsdeflate.so")
 SOURCES = ["msign.hip", "psd.hip"]
+# peak-rate microbenchmarks for the benchmark's roofline constants (not part of the library)
+PEAKS_LIB = os.path.join(HERE, "libsdpeaks.so")
+PEAKS_SOURCES = ["peaks.hip"]
 ARCH = os.environ.get("SDEFLATE_ARCH", "gfx950")
 
 # Packed fp32 instructions are disabled for every HIP translation unit.
@@ -28,9 +31,9 @@ def hipcc() -> str:
     return exe
 
 
-def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
-    tmp = LIB + ".tmp"
+def _compile(sources, lib, verbose):
+    srcs = [os.path.join(CSRC, s) for s in sources]
+    tmp = lib + ".tmp"
     cmd = [hipcc(), *FLAGS, "-I", os.path.join(ROOT, "include"), *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -41,8 +44,14 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError(f"hipcc failed ({res.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
+
+
+def build(verbose: bool = False) -> str:
+    """Build libsdeflate.so and the microbenchmark library libsdpeaks.so."""
+    _compile(PEAKS_SOURCES, PEAKS_LIB, verbose)
+    return _compile(SOURCES, LIB, verbose)
 
 
 if __name__ == "__main__":
