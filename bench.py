@@ -670,7 +670,8 @@ def main() -> int:
                 "flops_per_launch": upd_flops, "avg_launch_us": upd_avg_ms * 1e3, "launches": upd_n,
                 "algorithmic_bytes_per_launch": upd_alg_bytes,
                 "traffic_over_algorithmic": (tr / upd_alg_bytes) if tr else None,
-                "traffic_method": (traffic or {}).get("method") if tr else (traffic or {}).get("error")}
+                "traffic_method": (traffic or {}).get("method") if tr else (traffic or {}).get("error"),
+                "counter_factors": [(traffic or {}).get("fetch_factor"), (traffic or {}).get("write_factor")]}
     result = {
         "metric": "deflated msign matrices/s + TFLOP/s (% MFMA peak), batched 768x3072 bf16",
         "value": value,

@@ -9,6 +9,7 @@
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Each wave issues 8 * iters MFMAs of 32 x 32 x 16 (32768 flops each). The
 // results feed a comparison that is never true in practice, so the products
@@ -36,17 +37,32 @@ __global__ __launch_bounds__(256) void sdp_mfma_bf16_kernel(int iters, float* si
   if (s == -1.0f) sink[blockIdx.x] = s;
 }
 
-__global__ __launch_bounds__(256) void sdp_copy_kernel(const float4* __restrict__ src, float4* __restrict__ dst,
+// Streaming kernels: every thread moves U consecutive-stride float4 per
+// iteration with all loads issued before the stores (more bytes in flight);
+// the copy's stores are non-temporal. n is a multiple of the grid's stride
+// times U (the caller sizes the buffers so).
+constexpr int STREAM_U = 4;
+__global__ __launch_bounds__(256) void sdp_copy_kernel(const f32x4_t* __restrict__ src, f32x4_t* __restrict__ dst,
                                                        size_t n) {
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
-    dst[i] = src[i];
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride * STREAM_U) {
+    f32x4_t v[STREAM_U];
+#pragma unroll
+    for (int u = 0; u < STREAM_U; ++u) v[u] = src[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < STREAM_U; ++u) __builtin_nontemporal_store(v[u], &dst[i + u * stride]);
+  }
 }
 
 __global__ __launch_bounds__(256) void sdp_read_kernel(const float4* __restrict__ src, size_t n, float* sink) {
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
   float s = 0.f;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
-    const float4 v = src[i];
-    s += v.x + v.y + v.z + v.w;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride * STREAM_U) {
+    float4 v[STREAM_U];
+#pragma unroll
+    for (int u = 0; u < STREAM_U; ++u) v[u] = src[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < STREAM_U; ++u) s += v[u].x + v[u].y + v[u].z + v[u].w;
   }
   if (s == -1.0f) sink[blockIdx.x] = s;
 }
@@ -58,14 +74,15 @@ int sdp_mfma_bf16(int blocks, int iters, float* sink, hipStream_t stream) {
   hipLaunchKernelGGL(sdp_mfma_bf16_kernel, dim3(blocks), dim3(256), 0, stream, iters, sink);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
-// n float4 elements each way (src and dst do not overlap)
+// n float4 elements each way (src and dst do not overlap); n must be a
+// multiple of blocks * 256 * 4
 int sdp_copy(const void* src, void* dst, size_t n, int blocks, hipStream_t stream) {
-  if (!src || !dst || n == 0 || blocks < 1) return -1;
-  hipLaunchKernelGGL(sdp_copy_kernel, dim3(blocks), dim3(256), 0, stream, (const float4*)src, (float4*)dst, n);
+  if (!src || !dst || n == 0 || blocks < 1 || n % ((size_t)blocks * 256 * STREAM_U)) return -1;
+  hipLaunchKernelGGL(sdp_copy_kernel, dim3(blocks), dim3(256), 0, stream, (const f32x4_t*)src, (f32x4_t*)dst, n);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 int sdp_read(const void* src, size_t n, int blocks, float* sink, hipStream_t stream) {
-  if (!src || n == 0 || blocks < 1 || !sink) return -1;
+  if (!src || n == 0 || blocks < 1 || !sink || n % ((size_t)blocks * 256 * STREAM_U)) return -1;
   hipLaunchKernelGGL(sdp_read_kernel, dim3(blocks), dim3(256), 0, stream, (const float4*)src, n, sink);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
