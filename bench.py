@@ -468,10 +468,13 @@ def other_workload(args) -> int:
                             "flops_per_launch": fl}}
     elif args.workload == "admm":
         # ADMM on a max-cut relaxation of the size of the paper's n = 5000
-        # instances (planted-bisection random graph), tracked basis K = 64
-        # (the widest Rayleigh-Ritz block the library solves), r = 32, tau = 0.1;
-        # one step = 10 iterations with the gate open, continuing the state.
-        n, k, r, chunk = 5000, 64, 32, 10
+        # instances (planted-bisection random graph), tracked basis of the
+        # paper's width K = ceil(0.05 n) = 250 with window r = ceil(0.025 n) =
+        # 125 (--admm-k: another width, r = K / 2), tau = 0.1; one step = 10
+        # iterations with the gate open, continuing the state.
+        n, chunk = 5000, 10
+        k = args.admm_k
+        r = max(1, (k + 1) // 2)
         steps, table, degree = _filter_table(args)
         case = workloads.planted_maxcut(n, case_id=0)
         C = torch.from_numpy(case.c).to(dev)
@@ -489,6 +492,12 @@ def other_workload(args) -> int:
 
         ms = _timed(call, args.steps, args.warmup)
         roof = _psd_update_roofline(sd, call, args.steps, n, args.precision)
+        stage_ms = {}
+        for stg in ("ns_gram", "ns_poly", "ns_update", "restore", "sketch", "cholqr", "small", "lowrank", "lanczos"):
+            t_ms, t_n = _stage_time(sd, call, args.steps, stg)
+            if t_n:
+                stage_ms[stg] = {"ms_per_iteration": t_ms / (args.steps * chunk), "launches_per_iteration":
+                                 t_n / (args.steps * chunk)}
         # per step: X^2 and the update (n^3 each, symmetric), plus A^2 for a quintic
         flops = chunk * ((2.0 if degree == 3 else 3.0) * n ** 3 * steps + 2.0 * n ** 3)
         peak = 157.3 if args.precision == "f32" else MFMA_BF16_PEAK_TFLOPS
@@ -501,7 +510,7 @@ def other_workload(args) -> int:
                           "filter_degree": degree,
                           "iterations_per_step": chunk, "final_eta": float(last["eta"][-1]),
                           "final_n_deflated": int(last["ndef"][-1])},
-               "roofline": roof}
+               "roofline": roof, "stages": stage_ms}
     else:
         if args.workload == "c4":
             case = workloads.config4()
@@ -566,6 +575,7 @@ def main() -> int:
     ap.add_argument("--poly", default="cubic", choices=["cubic", "quintic7"],
                     help="c4 / c5 / admm: the filter: 10 cubic steps, or 7 steps of the degree-5 map "
                          "(the shape of the paper's T = 7 fp16 composite)")
+    ap.add_argument("--admm-k", type=int, default=250, help="admm: width K of the tracked basis")
     ap.add_argument("--sequential", action="store_true",
                     help="c2-step / paper-step: one call per group on one stream instead of sd_msign_groups")
     args = ap.parse_args()

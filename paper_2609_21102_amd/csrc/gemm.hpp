@@ -461,6 +461,33 @@ struct EpiStore {
   }
 };
 
+// out = alpha x + C, alpha read from device memory (null: 1), plus an
+// optional fp16 copy of alpha x in the same layout. x may alias out: each
+// element of x is read before the main loop by the lane that later writes it.
+struct EpiAxpyDev {
+  static constexpr bool PRE = true;
+  static constexpr bool ROWWISE = false;
+  static constexpr bool HI_FROM_B = false;
+  const float* x;
+  const float* alpha;
+  float* out;
+  f16_t* xs16;
+  int ld;
+  __device__ float pre(int, int r, int c) const { return x[(long long)r * ld + c]; }
+  __device__ void apply(int, int r0, int c, float v[4], int mode, const float* xv) const {
+    const float a = alpha ? *alpha : 1.f;
+    if (xs16) {
+      float w[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w[j] = a * xv[j];
+      emit4(xs16, ld, r0, c, w, mode);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) v[j] = fmaf(a, xv[j], v[j]);
+    emit4(out, ld, r0, c, v, mode);
+  }
+};
+
 // Plain fp32 store of C in the row-wise form (direct-to-LDS kernel).
 struct EpiStoreRows {
   static constexpr bool PRE = false;

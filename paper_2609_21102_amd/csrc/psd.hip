@@ -11,6 +11,7 @@
 // With nothing deflated the same kernels run with R = Z, which is the
 // baseline projection of eq:baseline_projection.
 #include "host.hpp"
+#include "wide.hpp"
 
 namespace sd {
 
@@ -514,6 +515,12 @@ struct PsdPlan {
   float* sumsq;    // [tiles] sums of R^2 per 128 x 128 tile (Frobenius scale)
   LanczosState* lst;
   double* lpart;   // Lanczos step partial sums: two blocks of LZ_MAX rows
+  // wide tracked bases (K > SM_MAX): K x K problems in global memory
+  bool wk;
+  int kp, kr;      // K rounded up to 32 (small matrices), to 128 (panel rows)
+  double *wpart, *g64, *hb0, *hb1, *eb0, *eb1, *e64, *mt, *lw;
+  float* us;       // scaled copy of U for the rank-K GEMMs
+  BjState* bst;
 };
 
 static void plan_psd(PsdPlan& p, Arena& ar) {
@@ -531,12 +538,26 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
   p.ah = p.f16 && p.quintic ? ar.take<f16_t>(nn) : nullptr;
   p.rh = p.f16 ? ar.take<f16_t>(nn) : nullptr;
   const int kq = p.K > 0 ? p.K : 1;
-  const int kr = round_up(kq, 32);
+  const int kr = p.wk ? p.kr : round_up(kq, 32);
   p.vt = ar.take<float>((size_t)kr * p.n_pad);
   p.zt = ar.take<float>((size_t)kr * p.n_pad);
   p.E = ar.take<float>((size_t)kq * kq);
   p.lam = ar.take<float>(kq);
-  p.ut = ar.take<float>((size_t)kq * p.n_pad);
+  p.ut = ar.take<float>((size_t)(p.wk ? kr : kq) * p.n_pad);
+  if (p.wk) {
+    const size_t kk = (size_t)p.kp * p.kp;
+    p.us = ar.take<float>((size_t)kr * p.n_pad);
+    p.wpart = ar.take<double>(kk * cdiv(p.n_pad, WG_CHUNK));
+    p.g64 = ar.take<double>(kk);
+    p.hb0 = ar.take<double>(kk);
+    p.hb1 = ar.take<double>(kk);
+    p.eb0 = ar.take<double>(kk);
+    p.eb1 = ar.take<double>(kk);
+    p.e64 = ar.take<double>(kk);
+    p.mt = ar.take<double>(kk);
+    p.lw = ar.take<double>(kk);
+    p.bst = ar.take<BjState>(1);
+  }
   p.coefR = ar.take<float>(kq);
   p.coefX = ar.take<float>(kq);
   p.coefP = ar.take<float>(kq);
@@ -557,7 +578,7 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
 static int validate_psd(int n, int k, int steps, const float* X, const float* Qwarm, const float* out,
                         const sd_psd_opts& o) {
   if (n < 1 || k < 0 || k >= n || steps < 0 || steps > 1000 || !X || !out) return SD_ERR_INVALID_ARG;
-  if (k > SM_MAX) return SD_ERR_UNSUPPORTED;
+  if (k > WIDE_MAX) return SD_ERR_UNSUPPORTED;
   if (k > 0 && !Qwarm) return SD_ERR_INVALID_ARG;
   if (o.subspace_iters < 1 || o.subspace_iters > 100) return SD_ERR_INVALID_ARG;
   if (o.lanczos_steps < 1 || o.lanczos_steps > LZ_MAX) return SD_ERR_INVALID_ARG;
@@ -590,6 +611,9 @@ static void make_psd_plan(PsdPlan& p, int n, int k, int steps, const float* X, c
   p.f16 = o.precision == SD_PREC_F16;
   p.wide = p.f16 && p.n_pad % 256 == 0 && p.n_pad >= 4096;
   p.frob = o.scale_mode == SD_SCALE_FROBENIUS;
+  p.wk = k > SM_MAX;
+  p.kp = round_up(k > 0 ? k : 1, 32);
+  p.kr = round_up(k > 0 ? k : 1, 128);
   const bool aligned = X && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
   p.copy_in = p.n != p.n_pad || !aligned;
 }
@@ -637,6 +661,81 @@ __global__ __launch_bounds__(WAVE) void frob_scale_kernel(const float* sumsq, in
   }
 }
 
+// ------------------------------------------- wide tracked bases ----------
+constexpr int BJ_MAX_SWEEPS = 16;   // block Jacobi sweep cap
+constexpr int BJ_TOL_EXP = -40;     // stop at off(H) <= 2^-40 ||H||_F
+
+// C = A B^T over the panel rows (kp x kp, float64), SYM: A == B.
+static void wide_products(const PsdPlan& p, const float* A, const float* B, bool sym, double* C, hipStream_t st) {
+  const int np = p.n_pad, kp = p.kp, nch = cdiv(np, WG_CHUNK), tk = cdiv(kp, 64);
+  const int tiles = sym ? tk * (tk + 1) / 2 : tk * tk;
+  const dim3 gr(cdiv(kp * kp, 256));
+  if (sym) {
+    hipLaunchKernelGGL(wide_gram_kernel<true>, dim3(tiles * nch), dim3(256), 0, st, A, np, B, np, kp, np, p.wpart);
+    hipLaunchKernelGGL(wide_gram_reduce_kernel<true>, gr, dim3(256), 0, st, p.wpart, nch, kp, C);
+  } else {
+    hipLaunchKernelGGL(wide_gram_kernel<false>, dim3(tiles * nch), dim3(256), 0, st, A, np, B, np, kp, np, p.wpart);
+    hipLaunchKernelGGL(wide_gram_reduce_kernel<false>, gr, dim3(256), 0, st, p.wpart, nch, kp, C);
+  }
+}
+
+// dst = CholQR(src) (K panel rows; rows K .. kr - 1 of dst written as zero).
+static void cholqr_wide(const PsdPlan& p, const float* src, float* dst, int* status, hipStream_t st) {
+  ProfScope ps(SD_STAGE_CHOLQR, st);
+  const int np = p.n_pad;
+  wide_products(p, src, src, true, p.g64, st);
+  hipLaunchKernelGGL(chol_inv_wide_kernel, dim3(1), dim3(CI_THREADS), 0, st, p.g64, p.K, p.kp, p.lw, p.mt, status);
+  hipLaunchKernelGGL(wide_rotate_kernel, dim3(cdiv(p.kr, 64) * (np / 64)), dim3(256), 0, st, p.mt, p.kp, src, np,
+                     p.kp, p.K, np, dst, np, p.kr);
+}
+
+// Zt = V^T Z^T = (Z V)^T on the float32 MFMA GEMM (Z symmetric: its rows).
+static void zv_wide(const PsdPlan& p, const float* z, const float* vt, float* zt, hipStream_t st) {
+  ProfScope ps(SD_STAGE_SKETCH, st);
+  const int np = p.n_pad;
+  GemmShape g{p.kr, np, np, np, np, 0, 0, 1};
+  EpiStore es{zt, 0, np};
+  launch_gemm<CfgTile128, float, false, false>(vt, z, g, es, st);
+}
+
+// out = alpha x + U^T diag(mult c) U over the deflated rows (float32 MFMA,
+// K = kp); x may be out.
+static void rankk_wide(const PsdPlan& p, const float* coef, float mult, const float* x, const float* alpha,
+                       float* out, f16_t* xs16, hipStream_t st) {
+  ProfScope ps(SD_STAGE_LOWRANK, st);
+  const int np = p.n_pad;
+  hipLaunchKernelGGL(scale_rows_kernel, grid1((long long)p.kp * np, 256), dim3(256), 0, st, p.ut, np, coef, p.ndef,
+                     mult, p.kp, p.us);
+  GemmShape g{np, np, p.kp, np, np, 0, 0, 1};
+  EpiAxpyDev e{x, alpha, out, xs16, np};
+  launch_gemm<CfgTile128, float, true, false, true>(p.us, p.ut, g, e, st);
+}
+
+// Rayleigh-Ritz on the wide basis: H = V^T (Z V) in float64, block Jacobi,
+// ordering / gate / coefficients, U = V E.
+static void ritz_wide(const PsdPlan& p, const float* vt, const float* zt, const sd_psd_opts& o, hipStream_t st) {
+  ProfScope ps(SD_STAGE_SMALL, st);
+  const int kp = p.kp, np = p.n_pad, nb = kp / BJ_B, P = nb / 2, rps = nb - 1;
+  wide_products(p, vt, zt, false, p.g64, st);
+  hipLaunchKernelGGL(bj_init_kernel, dim3(cdiv(kp * kp, 256)), dim3(256), 0, st, p.g64, kp, p.hb0, p.eb0, p.bst);
+  const dim3 grid(P * P + P * cdiv(kp, 64));
+  for (int sweep = 0; sweep < BJ_MAX_SWEEPS; ++sweep) {
+    for (int t = 0; t < rps; ++t) {
+      const long long g = (long long)sweep * rps + t;
+      const bool odd = g & 1;
+      hipLaunchKernelGGL(bj_round_kernel, grid, dim3(128), 0, st, odd ? p.hb1 : p.hb0, odd ? p.hb0 : p.hb1,
+                         odd ? p.eb1 : p.eb0, odd ? p.eb0 : p.eb1, kp, nb, t, 2 * BJ_B - 1, p.bst);
+    }
+    hipLaunchKernelGGL(bj_check_kernel, dim3(1), dim3(1024), 0, st, p.hb0, p.hb1, kp, rps, sweep, BJ_MAX_SWEEPS,
+                       BJ_TOL_EXP, p.bst);
+  }
+  hipLaunchKernelGGL(ritz_wide_kernel, dim3(1), dim3(1024), 0, st, p.hb0, p.hb1, p.eb0, p.eb1, rps, p.bst, p.K, kp,
+                     o.tau, o.window, o.gamma, p.e64, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out,
+                     o.n_deflated_out, o.n_positive_out);
+  hipLaunchKernelGGL(wide_rotate_kernel, dim3(cdiv(kp, 64) * (np / 64)), dim3(256), 0, st, p.e64, kp, vt, np, kp,
+                     kp, np, p.ut, np, kp);
+}
+
 static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, const sd_psd_opts& o,
                    hipStream_t st) {
   const int np = p.n_pad, n = p.n, K = p.K;
@@ -657,7 +756,22 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   la.ldx = np;
   la.ldo = np;
   la.ldl = la.ldr = np;
-  if (K > 0) {
+  if (K > 0 && p.wk) {
+    // wide basis: V panel (rows K .. kr - 1 zero), (J - 1) x [Z V, CholQR],
+    // Z V, Rayleigh-Ritz, R = Z - U lam U^T as a GEMM, next basis
+    fill(p.vt + (long long)K * np, (long long)(p.kr - K) * np, 0.f, st);
+    hipLaunchKernelGGL(rows_to_panel_kernel, grid1((long long)K * np, 256), dim3(256), 0, st, Qwarm, K, n, np, p.vt);
+    for (int j = 0; j + 1 < o.subspace_iters; ++j) {
+      zv_wide(p, z, p.vt, p.zt, st);
+      cholqr_wide(p, p.zt, p.vt, o.status_dev, st);
+    }
+    zv_wide(p, z, p.vt, p.zt, st);
+    ritz_wide(p, p.vt, p.zt, o, st);
+    rankk_wide(p, p.coefR, 1.f, z, nullptr, p.r, nullptr, st);
+    if (p.frob) hipLaunchKernelGGL(tile_sumsq_kernel, dim3((np / 128) * (np / 128)), dim3(256), 0, st, p.r, np, p.sumsq);
+    cholqr_wide(p, p.zt, p.vt, o.status_dev, st);
+    hipLaunchKernelGGL(panel_to_rows_kernel, grid1((long long)n * K, 256), dim3(256), 0, st, p.vt, np, K, n, Qwarm);
+  } else if (K > 0) {
     hipLaunchKernelGGL(rows_to_panel_kernel, grid1((long long)K * np, 256), dim3(256), 0, st, Qwarm, K, n, np, p.vt);
     float* vt = p.vt;
     float* zt = p.zt;
@@ -724,13 +838,17 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     lanczos(p, p.r, o.seed, o.theta_out, st);
   }
   // X0 = R / theta + gamma^-1 U sign(lam) U^T
-  la.x = p.r;
-  la.coef = p.coefX;
-  la.alpha = p.alpha_x0;
-  la.out = p.xa;
-  la.xs16 = p.rh;   // fp16 path: R / theta, the restore product's operand
-  lowrank<float, float>(la, st);
-  la.xs16 = nullptr;
+  if (K > 0 && p.wk) {
+    rankk_wide(p, p.coefX, 1.f, p.r, p.alpha_x0, p.xa, p.rh, st);
+  } else {
+    la.x = p.r;
+    la.coef = p.coefX;
+    la.alpha = p.alpha_x0;
+    la.out = p.xa;
+    la.xs16 = p.rh;   // fp16 path: R / theta, the restore product's operand
+    lowrank<float, float>(la, st);
+    la.xs16 = nullptr;
+  }
 
   float* cur = p.xa;
   float* nxt = p.xb;
@@ -862,9 +980,14 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     launch_gemm<CfgTile128, float, false, false>(p.r, cur, g, es, st);
   }
   const int tiles = (np / 64) * (np / 64);
-  const float* ut = K > 0 ? p.ut : nullptr;
-  const int* kk = K > 0 ? p.ndef : nullptr;
-  if (K <= 16)
+  if (K > 0 && p.wk) {
+    // the head as 2 U max(lam, 0) U^T added to C: the output's (C + C^T) / 4
+    // then carries (H + H^T) / 2, exactly symmetric
+    rankk_wide(p, p.coefP, 2.f, p.c, nullptr, p.c, nullptr, st);
+  }
+  const float* ut = (K > 0 && !p.wk) ? p.ut : nullptr;
+  const int* kk = (K > 0 && !p.wk) ? p.ndef : nullptr;
+  if (K <= 16 || p.wk)
     hipLaunchKernelGGL((psd_out_kernel<16>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
   else if (K <= 32)
     hipLaunchKernelGGL((psd_out_kernel<32>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
@@ -1011,7 +1134,7 @@ size_t sd_psd_workspace_bytes(int n, int k, const sd_psd_opts* opts) {
   sd_psd_opts o;
   sd_psd_opts_default(&o);
   if (opts) o = *opts;
-  if (n < 1 || k < 0 || k >= n || k > SM_MAX) return 0;
+  if (n < 1 || k < 0 || k >= n || k > WIDE_MAX) return 0;
   PsdPlan p{};
   make_psd_plan(p, n, k, 0, nullptr, o);
   Arena ar;
@@ -1084,7 +1207,7 @@ size_t sd_admm_workspace_bytes(int n, int k, int steps, const sd_psd_opts* opts)
   sd_psd_opts o;
   sd_psd_opts_default(&o);
   if (opts) o = *opts;
-  if (n < 1 || k < 0 || k >= n || k > SM_MAX || steps < 0) return 0;
+  if (n < 1 || k < 0 || k >= n || k > WIDE_MAX || steps < 0) return 0;
   PsdPlan p{};
   Arena ar;
   admm_plan(p, ar, n, k, steps, o);

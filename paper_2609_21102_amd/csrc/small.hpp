@@ -189,7 +189,10 @@ static __device__ __forceinline__ void jacobi_eig(SmallLds& s, int n, int tol_ex
 //     slots) is held as 2 x 2 units (rows 2p, 2p + 1; columns T_q, B_q).
 //   * The ring step goes through LDS (s.h2, s.e2): one round trip per round.
 //   * Stop after N - 1 consecutive rounds without a rotation (every pair was
-//     checked with nothing changed in between), or after 40 sweeps.
+//     checked with nothing changed in between), or after 40 sweeps (or
+//     max_rounds rounds when given: a partial solve whose accumulated
+//     rotation is s.e).
+//   * S: any LDS struct with h, e, h2, e2 of at least N x N (and red for NW > 1).
 // Input: s.h (n x n). Output as jacobi_eig: eigenvalues on the diagonal of
 // s.h (off-diagonal entries are left as they were) and eigenvectors as the
 // columns of s.e; returns the number of rounds. Only the calling wave may
@@ -223,8 +226,8 @@ __device__ __forceinline__ int jw_index(int slot, int R) {
   return k0 <= NP - 2 ? k0 + 1 : 3 * NP - 2 - k0;
 }
 
-template <int NP, int NW = 1>
-__device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) {
+template <int NP, int NW = 1, typename S = SmallLds>
+__device__ __forceinline__ int jacobi_eig_wave(S& s, int n, int tol_exp, int max_rounds = 0) {
   constexpr int N = 2 * NP, NB = NP * NP, L = WAVE * NW, U = (NB + L - 1) / L;
   static_assert(N <= SM_MAX && U <= 4, "at most four 2 x 2 blocks per lane");
   const int lane = NW == 1 ? (int)(threadIdx.x & (WAVE - 1)) : (int)threadIdx.x;
@@ -262,7 +265,8 @@ __device__ __forceinline__ int jacobi_eig_wave(SmallLds& s, int n, int tol_exp) 
   else fro = block_sum(fro, s.red);
   const double abs_floor = __builtin_amdgcn_ldexp(sqrt(fro), tol_exp);
   int idle = 0, R = 0;
-  while (idle < N - 1 && R < 40 * (N - 1)) {
+  const int round_cap = max_rounds > 0 ? max_rounds : 40 * (N - 1);
+  while (idle < N - 1 && R < round_cap) {
     // every lane chooses the angles of its own pairs p and q from their
     // diagonal blocks (the same inputs give the same angles in every lane)
     bool rot = false;

@@ -1,0 +1,606 @@
+// Wide tracked bases for the deflated PSD projection (Alg. 2 with the
+// paper's basis widths, K = ceil(0.05 n): 250 to 350 columns in its SDP runs,
+// Sec. 3.3). The K x K problems no longer fit one work-group's LDS, so this
+// path splits them:
+//   * float64 products of panel rows (the CholeskyQR Gram Z^T Z and the
+//     Rayleigh quotient V^T Z V) over position chunks, reduced in chunk order;
+//   * CholeskyQR's factor and the inverse of the triangular factor on one
+//     work-group, the K x K matrices in global memory (L2-resident), panels
+//     of 32 columns in LDS;
+//   * a block Jacobi eigensolver over 16-index blocks: every round pairs the
+//     blocks by the circle method and rotates each 32 x 32 pair problem with
+//     one sweep of the one-wave Jacobi (the same rotations a scalar cyclic
+//     Jacobi would apply in a block ordering), one launch per round, a
+//     convergence check after every sweep;
+//   * the rotations V E and Z L^-T as float64-accumulated products; the
+//     rank-K terms of the residual, the padded start and the restore as
+//     float32 MFMA GEMMs with an axpy epilogue (gemm.hpp).
+#pragma once
+
+#include "common.hpp"
+#include "small.hpp"
+#include "gemm.hpp"
+
+namespace sd {
+
+constexpr int WIDE_MAX = 512;     // widest tracked basis of this path
+constexpr int WG_CHUNK = 512;     // positions per partial of the float64 products
+constexpr int BJ_B = 16;          // block Jacobi: indices per block (pairs of 32)
+
+// -------------------------------------------- float64 panel products -----
+// part[ch][a][b] = sum over the positions x of chunk ch of A[a][x] B[b][x],
+// a, b < kp, in float64 and position order (one thread per output). Tiles of
+// 64 x 64 outputs (SYM: upper tiles only, A == B); thread (ty, tx) owns rows
+// a0 + ty + 16i and columns b0 + tx + 16j. Grid: tiles * nch; 256 threads.
+template <bool SYM>
+__global__ __launch_bounds__(256) void wide_gram_kernel(const float* __restrict__ A, int lda,
+                                                        const float* __restrict__ B, int ldb, int kp, int len,
+                                                        double* __restrict__ part) {
+  __shared__ double as[32][65];
+  __shared__ double bs[32][65];
+  const int tk = cdiv(kp, 64);
+  const int ntiles = SYM ? tk * (tk + 1) / 2 : tk * tk;
+  const int ch = blockIdx.x / ntiles;
+  int t = blockIdx.x - ch * ntiles, ta, tb;
+  if (SYM) {
+    sym_tile(t, tk, ta, tb);
+  } else {
+    ta = t / tk;
+    tb = t - ta * tk;
+  }
+  const int a0 = ta * 64, b0 = tb * 64;
+  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  const int x_begin = ch * WG_CHUNK, x_end = min(len, x_begin + WG_CHUNK);
+  double acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int x0 = x_begin; x0 < x_end; x0 += 32) {
+    float va[8], vb[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + 256 * u, r = e >> 5, x = e & 31;
+      va[u] = a0 + r < kp ? A[(long long)(a0 + r) * lda + x0 + x] : 0.f;
+      vb[u] = b0 + r < kp ? B[(long long)(b0 + r) * ldb + x0 + x] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = tid + 256 * u, r = e >> 5, x = e & 31;
+      as[x][r] = (double)va[u];
+      bs[x][r] = (double)vb[u];
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int x = 0; x < 32; ++x) {
+      double av[4], bv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        av[i] = as[x][ty + 16 * i];
+        bv[i] = bs[x][tx + 16 * i];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fma(av[i], bv[j], acc[i][j]);
+    }
+  }
+  double* out = part + (long long)ch * kp * kp;
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int a = a0 + ty + 16 * i, b = b0 + tx + 16 * j;
+      if (a < kp && b < kp) out[(long long)a * kp + b] = acc[i][j];
+    }
+}
+
+// C[a][b] = sum of the chunk partials in chunk order (SYM: entries below the
+// tile diagonal read their mirror, so C is exactly symmetric: a diagonal
+// tile's (a, b) and (b, a) sum the same products in the same order).
+template <bool SYM>
+__global__ __launch_bounds__(256) void wide_gram_reduce_kernel(const double* __restrict__ part, int nch, int kp,
+                                                               double* __restrict__ C) {
+  const long long e = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (long long)kp * kp) return;
+  int a = (int)(e / kp), b = (int)(e - (long long)a * kp);
+  if (SYM && a / 64 > b / 64) {
+    const int t = a;
+    a = b;
+    b = t;
+  }
+  const long long src = (long long)a * kp + b, step = (long long)kp * kp;
+  double t = 0.0;
+  for (int c = 0; c < nch; ++c) t += part[c * step + src];
+  C[e] = t;
+}
+
+// ---------------------------------- CholeskyQR factor and its inverse -----
+// Gram = L L^T for the leading c x c block of G (kp x kp, float64), right-
+// looking by panels of 32 columns, pivots below c u tr(Gram) raised to that
+// floor (flag 2 in status) as in the narrow path; then M = L^-1 by block
+// rows, written transposed: MT[j][i] = M[i][j] (zero outside the c x c lower
+// triangle), so that Q^T = M Z^T is the float64 rotation MT^T Z^T. A zero
+// trace gives MT = 0 (a zero panel). One work-group of 1024 threads; L and
+// MT live in global memory (L2), the current panel in LDS.
+constexpr int CI_THREADS = 1024;
+
+__global__ __launch_bounds__(CI_THREADS) void chol_inv_wide_kernel(const double* __restrict__ G, int c, int kp,
+                                                                   double* __restrict__ L, double* __restrict__ MT,
+                                                                   int* status) {
+  __shared__ double D[32][33];
+  __shared__ double Dinv[32][33];
+  __shared__ double P[WIDE_MAX * 32];   // panel rows below the diagonal block; then the block products T
+  __shared__ double red[CI_THREADS / WAVE];
+  __shared__ int floored;
+  const int tid = threadIdx.x;
+  double tr = 0.0;
+  for (int a = tid; a < c; a += CI_THREADS) tr += G[(long long)a * kp + a];
+  tr = block_sum(tr, red);
+  for (long long e = tid; e < (long long)kp * kp; e += CI_THREADS) {
+    MT[e] = 0.0;
+    L[e] = G[e];
+  }
+  if (tid == 0) floored = 0;
+  __syncthreads();
+  if (tr == 0.0) return;
+  const double floor_ = (double)c * 1.1102230246251565e-16 * tr;
+  // ---- factor
+  for (int j0 = 0; j0 < c; j0 += 32) {
+    const int w = min(32, c - j0);
+    for (int e = tid; e < 32 * 32; e += CI_THREADS) {
+      const int r = e >> 5, q = e & 31;
+      D[r][q] = (r < w && q < w) ? L[(long long)(j0 + r) * kp + j0 + q] : 0.0;
+    }
+    __syncthreads();
+    if (tid < WAVE) {
+      const int lane = tid;
+      for (int jj = 0; jj < w; ++jj) {
+        double d = D[jj][jj];
+        if (d <= floor_) {
+          d = floor_;
+          if (lane == 0) floored = 1;
+        }
+        const double piv = sqrt(d);
+        wave_sync();
+        if (lane == jj) D[jj][jj] = piv;
+        if (lane > jj && lane < w) D[lane][jj] = D[lane][jj] / piv;
+        wave_sync();
+        if (lane > jj && lane < w) {
+          const double lij = D[lane][jj];
+          for (int k = jj + 1; k <= lane; ++k) D[lane][k] -= lij * D[k][jj];
+        }
+        wave_sync();
+      }
+    }
+    __syncthreads();
+    // panel below the block: row i solves P[i] D^T = G'[i] (one row per thread)
+    const int m = c - j0 - w;
+    for (int rr = tid; rr < m; rr += CI_THREADS) {
+      const long long row = (long long)(j0 + w + rr) * kp + j0;
+      double* pr = P + rr * 32;   // this thread's row, solved in place
+      for (int t = 0; t < 32; ++t) pr[t] = t < w ? L[row + t] : 0.0;
+      for (int t = 0; t < w; ++t) {
+        double v = pr[t];
+        for (int u = 0; u < t; ++u) v -= pr[u] * D[t][u];
+        pr[t] = v / D[t][t];
+        L[row + t] = pr[t];
+      }
+    }
+    for (int e = tid; e < w * w; e += CI_THREADS) {
+      const int r = e / w, q = e - r * w;
+      if (q <= r) L[(long long)(j0 + r) * kp + j0 + q] = D[r][q];
+    }
+    __syncthreads();
+    // trailing update of the lower triangle, 4 x 4 blocks per thread
+    const int nbm = cdiv(m, 4);
+    const int nblk = nbm * (nbm + 1) / 2;
+    for (int blk = tid; blk < nblk; blk += CI_THREADS) {
+      int bi = (int)((sqrt(8.0 * blk + 1.0) - 1.0) * 0.5);
+      while (bi * (bi + 1) / 2 > blk) --bi;
+      while ((bi + 1) * (bi + 2) / 2 <= blk) ++bi;
+      const int bk = blk - bi * (bi + 1) / 2;
+      double acc[4][4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc[i][k] = 0.0;
+      for (int t = 0; t < w; ++t) {
+        double pi[4], pk[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          pi[i] = 4 * bi + i < m ? P[(4 * bi + i) * 32 + t] : 0.0;
+          pk[i] = 4 * bk + i < m ? P[(4 * bk + i) * 32 + t] : 0.0;
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int k = 0; k < 4; ++k) acc[i][k] = fma(pi[i], pk[k], acc[i][k]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int ii = 4 * bi + i, kk = 4 * bk + k;
+          if (ii < m && kk <= ii) L[(long long)(j0 + w + ii) * kp + j0 + w + kk] -= acc[i][k];
+        }
+    }
+    __syncthreads();
+  }
+  if (tid == 0 && floored && status) atomicOr(status, 2);
+  // ---- inverse by block rows: M_ii = L_ii^-1, M_ij = -L_ii^-1 sum_{j <= k < i} L_ik M_kj
+  for (int i0 = 0; i0 < c; i0 += 32) {
+    const int w = min(32, c - i0);
+    for (int e = tid; e < 32 * 32; e += CI_THREADS) {
+      const int r = e >> 5, q = e & 31;
+      D[r][q] = (r < w && q <= r) ? L[(long long)(i0 + r) * kp + i0 + q] : 0.0;
+    }
+    __syncthreads();
+    if (tid < 32) {   // column t of the diagonal block's inverse
+      const int t = tid;
+      for (int i = 0; i < 32; ++i) Dinv[i][t] = 0.0;
+      if (t < w) {
+        Dinv[t][t] = 1.0 / D[t][t];
+        for (int i = t + 1; i < w; ++i) {
+          double s = 0.0;
+          for (int u = t; u < i; ++u) s += D[i][u] * Dinv[u][t];
+          Dinv[i][t] = -s / D[i][i];
+        }
+      }
+    }
+    __syncthreads();
+    const int nbi = i0 / 32;
+    double* T = P;
+    for (int e = tid; e < nbi * 1024; e += CI_THREADS) {
+      const int jb = e >> 10, r = (e >> 5) & 31, q = e & 31;
+      double s = 0.0;
+      if (r < w) {
+        const double* lr = L + (long long)(i0 + r) * kp;
+        const double* mr = MT + (long long)(32 * jb + q) * kp;
+        for (int u = 32 * jb; u < i0; ++u) s = fma(lr[u], mr[u], s);
+      }
+      T[e] = s;
+    }
+    __syncthreads();
+    for (int e = tid; e < nbi * 1024; e += CI_THREADS) {
+      const int jb = e >> 10, r = (e >> 5) & 31, q = e & 31;
+      if (r < w) {
+        double v = 0.0;
+        for (int u = 0; u < w; ++u) v = fma(Dinv[r][u], T[(jb << 10) + u * 32 + q], v);
+        MT[(long long)(32 * jb + q) * kp + i0 + r] = -v;
+      }
+    }
+    for (int e = tid; e < 32 * 32; e += CI_THREADS) {
+      const int r = e >> 5, q = e & 31;
+      if (r < w && q <= r) MT[(long long)(i0 + q) * kp + i0 + r] = Dinv[r][q];
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------ float64 rotations -----
+// out[i][x] = sum_{j < kin} M[j][i] P[j][x] for i < kout (float64, j order,
+// rounded once), rows kout .. rows_out - 1 written as zero; len a multiple of
+// 64. Used for U = V E (M = E) and Q = Z L^-T (M = MT). Tiles of 64 outputs
+// x 64 positions; thread (ty, tx) owns rows i0 + ty + 16 ii and positions
+// x0 + 4 tx .. + 3. Grid: cdiv(rows_out, 64) * (len / 64); 256 threads.
+__global__ __launch_bounds__(256) void wide_rotate_kernel(const double* __restrict__ M, int ldm,
+                                                          const float* __restrict__ Pt, int ldp, int kin, int kout,
+                                                          int len, float* __restrict__ out, int ldo, int rows_out) {
+  __shared__ double ms[16][65];
+  __shared__ double ps[16][65];
+  const int tpx = len / 64;
+  const int ti = blockIdx.x / tpx, txb = blockIdx.x - ti * tpx;
+  const int i0 = ti * 64, x0 = txb * 64;
+  const int tid = threadIdx.x, ty = tid >> 4, tx = tid & 15;
+  if (i0 >= kout) {   // zero rows only
+#pragma unroll
+    for (int ii = 0; ii < 4; ++ii) {
+      const int i = i0 + ty + 16 * ii;
+      if (i < rows_out) *reinterpret_cast<float4*>(out + (long long)i * ldo + x0 + 4 * tx) = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    return;
+  }
+  double acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = 0.0;
+  for (int j0 = 0; j0 < kin; j0 += 16) {
+    double mv[4];
+    float pv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = tid + 256 * u, j = e >> 6, c = e & 63;
+      mv[u] = (j0 + j < kin && i0 + c < kout) ? M[(long long)(j0 + j) * ldm + i0 + c] : 0.0;
+      pv[u] = j0 + j < kin ? Pt[(long long)(j0 + j) * ldp + x0 + c] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int e = tid + 256 * u, j = e >> 6, c = e & 63;
+      ms[j][c] = mv[u];
+      ps[j][c] = (double)pv[u];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      double a[4], p[4];
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii) a[ii] = ms[j][ty + 16 * ii];
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) p[jj] = ps[j][4 * tx + jj];
+#pragma unroll
+      for (int ii = 0; ii < 4; ++ii)
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj) acc[ii][jj] = fma(a[ii], p[jj], acc[ii][jj]);
+    }
+  }
+#pragma unroll
+  for (int ii = 0; ii < 4; ++ii) {
+    const int i = i0 + ty + 16 * ii;
+    if (i < rows_out) {
+      const bool v = i < kout;
+      *reinterpret_cast<float4*>(out + (long long)i * ldo + x0 + 4 * tx) =
+          v ? make_float4((float)acc[ii][0], (float)acc[ii][1], (float)acc[ii][2], (float)acc[ii][3])
+            : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+}
+
+// --------------------------------------------------- block Jacobi --------
+struct BjState {
+  int done;     // converged (or the sweep cap reached): later launches return at once
+  int sweeps;   // sweeps applied when done was set
+};
+
+struct PairLds {
+  double h[2 * BJ_B][2 * BJ_B + 1];
+  double e[2 * BJ_B][2 * BJ_B + 1];
+  double h2[2 * BJ_B][2 * BJ_B + 1];
+  double e2[2 * BJ_B][2 * BJ_B + 1];
+};
+
+// Blocks of pair j in round t of the circle method over nb (even) blocks
+// (the ordering of jacobi_eig): over nb - 1 rounds every two blocks meet once.
+__device__ __forceinline__ void bj_pair(int t, int j, int nb, int& pa, int& pb) {
+  const int m = nb - 1;
+  int u = t + j - 1, w = t + m - 1 - j;
+  u -= u >= m ? m : 0;
+  w -= w >= m ? m : 0;
+  pa = j == 0 ? 0 : u + 1;
+  pb = w + 1;
+}
+// Global index of local index l (0..31) of the pair of blocks (pa, pb).
+__device__ __forceinline__ int bj_index(int l, int pa, int pb) {
+  return l < BJ_B ? BJ_B * pa + l : BJ_B * pb + (l - BJ_B);
+}
+
+// H0 = (H + H^T) / 2 (exactly symmetric), E0 = I, solver state reset.
+__global__ __launch_bounds__(256) void bj_init_kernel(const double* __restrict__ H, int kp, double* __restrict__ H0,
+                                                      double* __restrict__ E0, BjState* st) {
+  const long long e = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (e == 0) {
+    st->done = 0;
+    st->sweeps = 0;
+  }
+  if (e >= (long long)kp * kp) return;
+  const int i = (int)(e / kp), j = (int)(e - (long long)i * kp);
+  H0[e] = i == j ? H[e] : 0.5 * (H[e] + H[(long long)j * kp + i]);
+  E0[e] = i == j ? 1.0 : 0.0;
+}
+
+// One wave: the 32 x 32 problem of blocks (pa, pb) into s.h, then `rounds`
+// rounds of the one-wave Jacobi; s.e is the accumulated rotation J.
+__device__ __forceinline__ void bj_solve(const double* __restrict__ H, int kp, int pa, int pb, PairLds& s,
+                                         int rounds) {
+  const int lane = threadIdx.x & (WAVE - 1);
+#pragma unroll
+  for (int u = 0; u < 16; ++u) {
+    const int e = lane + WAVE * u, l = e >> 5, q = e & 31;
+    s.h[l][q] = H[(long long)bj_index(l, pa, pb) * kp + bj_index(q, pa, pb)];
+  }
+  wave_sync();
+  jacobi_eig_wave<BJ_B>(s, 2 * BJ_B, -48, rounds);
+}
+
+// One round: P = nb / 2 pairs. Work-groups 0 .. P^2 - 1 write the H block of
+// pairs (a, b), Hout[a][b] = J_a^T Hin[a][b] J_b (wave 0 solves pair a, wave 1
+// pair b); the next P * cdiv(kp, 64) update 64 rows of E on pair a's
+// columns, Eout = Ein J_a. Every work-group that needs J_a computes it from the
+// same entries in the same order, so all copies agree. Reads Hin/Ein, writes
+// Hout/Eout (the caller alternates the buffers). 128 threads.
+__global__ __launch_bounds__(128) void bj_round_kernel(const double* __restrict__ Hin, double* __restrict__ Hout,
+                                                       const double* __restrict__ Ein, double* __restrict__ Eout,
+                                                       int kp, int nb, int t, int rounds, const BjState* st) {
+  __shared__ PairLds sa, sb;
+  if (st->done) return;
+  const int P = nb / 2, nh = P * P;
+  const int tid = threadIdx.x, wave = tid / WAVE;
+  const int bid = blockIdx.x;
+  if (bid < nh) {
+    const int a = bid / P, b = bid - a * P;
+    int pa, qa, pb, qb;
+    bj_pair(t, a, nb, pa, qa);
+    bj_pair(t, b, nb, pb, qb);
+    if (wave == 0) bj_solve(Hin, kp, pa, qa, sa, rounds);
+    else if (a != b) bj_solve(Hin, kp, pb, qb, sb, rounds);
+    __syncthreads();
+    const PairLds& jb = a == b ? sa : sb;
+    for (int e = tid; e < 1024; e += 128) {
+      const int l = e >> 5, q = e & 31;
+      sa.h[l][q] = Hin[(long long)bj_index(l, pa, qa) * kp + bj_index(q, pb, qb)];
+    }
+    __syncthreads();
+    for (int e = tid; e < 1024; e += 128) {   // T = H_ab J_b
+      const int l = e >> 5, m = e & 31;
+      double v = 0.0;
+#pragma unroll 8
+      for (int q = 0; q < 32; ++q) v = fma(sa.h[l][q], jb.e[q][m], v);
+      sa.h2[l][m] = v;
+    }
+    __syncthreads();
+    for (int e = tid; e < 1024; e += 128) {   // J_a^T T
+      const int l = e >> 5, m = e & 31;
+      double v = 0.0;
+#pragma unroll 8
+      for (int q = 0; q < 32; ++q) v = fma(sa.e[q][l], sa.h2[q][m], v);
+      Hout[(long long)bj_index(l, pa, qa) * kp + bj_index(m, pb, qb)] = v;
+    }
+    return;
+  }
+  const int idx = bid - nh;
+  const int a = idx % P, r0 = (idx / P) * 64;
+  int pa, qa;
+  bj_pair(t, a, nb, pa, qa);
+  if (wave == 0) bj_solve(Hin, kp, pa, qa, sa, rounds);
+  __syncthreads();
+  // rows r0 .. r0 + 63 of E on the pair's columns, staged in sa.h (rows 0-31)
+  // and sa.h2 (rows 32-63)
+  for (int e = tid; e < 2048; e += 128) {
+    const int rr = e >> 5, q = e & 31, r = r0 + rr;
+    const double v = r < kp ? Ein[(long long)r * kp + bj_index(q, pa, qa)] : 0.0;
+    if (rr < 32) sa.h[rr][q] = v;
+    else sa.h2[rr - 32][q] = v;
+  }
+  __syncthreads();
+  for (int e = tid; e < 2048; e += 128) {
+    const int rr = e >> 5, m = e & 31, r = r0 + rr;
+    if (r >= kp) continue;
+    const double* er = rr < 32 ? sa.h[rr] : sa.h2[rr - 32];
+    double v = 0.0;
+#pragma unroll 8
+    for (int q = 0; q < 32; ++q) v = fma(er[q], sa.e[q][m], v);
+    Eout[(long long)r * kp + bj_index(m, pa, qa)] = v;
+  }
+}
+
+// After sweep `sweep` (rounds_per_sweep rounds each): done when the
+// off-diagonal mass is at most 2^(2 tol_exp) of the total, or at the sweep
+// cap. Round g reads buffer g % 2 and writes (g + 1) % 2, so after G rounds
+// the current matrices are buffer G % 2. One work-group.
+__global__ __launch_bounds__(1024) void bj_check_kernel(const double* __restrict__ H0, const double* __restrict__ H1,
+                                                        int kp, int rounds_per_sweep, int sweep, int max_sweeps,
+                                                        int tol_exp, BjState* st) {
+  __shared__ double red[1024 / WAVE];
+  if (st->done) return;
+  const long long g = (long long)(sweep + 1) * rounds_per_sweep;
+  const double* H = (g & 1) ? H1 : H0;
+  double off = 0.0, tot = 0.0;
+  for (long long e = threadIdx.x; e < (long long)kp * kp; e += 1024) {
+    const int i = (int)(e / kp), j = (int)(e - (long long)i * kp);
+    const double v = H[e] * H[e];
+    tot += v;
+    if (i != j) off += v;
+  }
+  off = block_sum(off, red);
+  tot = block_sum(tot, red);
+  if (threadIdx.x == 0 && (off <= __builtin_amdgcn_ldexp(tot, 2 * tol_exp) || sweep + 1 >= max_sweeps)) {
+    st->done = 1;
+    st->sweeps = sweep + 1;
+  }
+}
+
+// Rayleigh-Ritz finish (as ritz_kernel, from the block Jacobi's result):
+// Ritz values lam = diag(H) of the current buffers, ordered by |lam|
+// descending (ties: larger lam, then lower index); E64[a][j] = E[a][perm[j]]
+// for j < K (zero columns K .. kp - 1); the deflated count (all K, or the
+// gate of Alg. 2 with window r) and the coefficients of the residual (-lam),
+// the padded start (sign(lam) / gamma) and the restore (max(lam, 0)). One
+// work-group; K <= WIDE_MAX.
+__global__ __launch_bounds__(1024) void ritz_wide_kernel(const double* __restrict__ H0, const double* __restrict__ H1,
+                                                         const double* __restrict__ E0, const double* __restrict__ E1,
+                                                         int rounds_per_sweep, const BjState* st, int K, int kp,
+                                                         float tau, int window, float gamma,
+                                                         double* __restrict__ E64, float* lam_sorted, int* ndef,
+                                                         float* coef_r, float* coef_x, float* coef_p, float* ritz_user,
+                                                         int* ndef_user, int* npos_user) {
+  __shared__ double lam[WIDE_MAX], key[WIDE_MAX];
+  __shared__ int perm[WIDE_MAX];
+  __shared__ int count;
+  const int tid = threadIdx.x;
+  const long long g = (long long)st->sweeps * rounds_per_sweep;
+  const double* H = (g & 1) ? H1 : H0;
+  const double* E = (g & 1) ? E1 : E0;
+  if (tid < K) {
+    lam[tid] = H[(long long)tid * kp + tid];
+    key[tid] = fabs(lam[tid]);
+  }
+  __syncthreads();
+  if (tid < K) {
+    const double k0 = key[tid], l0 = lam[tid];
+    int rank = 0;
+    for (int j = 0; j < K; ++j) {
+      const double kj = key[j], lj = lam[j];
+      if (kj > k0 || (kj == k0 && (lj > l0 || (lj == l0 && j < tid)))) ++rank;
+    }
+    perm[rank] = tid;
+  }
+  __syncthreads();
+  for (long long e = tid; e < (long long)kp * kp; e += 1024) {
+    const int a = (int)(e / kp), j = (int)(e - (long long)a * kp);
+    E64[e] = j < K ? E[(long long)a * kp + perm[j]] : 0.0;
+  }
+  if (tid == 0) {
+    const double l0 = fabs(lam[perm[0]]);
+    int nd = K;
+    if (tau > 0.f) {
+      const double thr = (double)tau * l0;
+      const int r = window < 1 ? 1 : (window > K ? K : window);
+      nd = 0;
+      if (fabs(lam[perm[r - 1]]) < thr)
+        for (int j = 0; j < K; ++j) nd += (fabs(lam[perm[j]]) > thr) ? 1 : 0;
+    }
+    int np = 0;
+    for (int j = 0; j < nd; ++j) np += lam[perm[j]] > 0.0 ? 1 : 0;
+    *ndef = nd;
+    if (ndef_user) *ndef_user = nd;
+    if (npos_user) *npos_user = np;
+    count = nd;
+  }
+  __syncthreads();
+  const int nd = count;
+  if (tid < K) {
+    const double l = lam[perm[tid]];
+    const bool on = tid < nd;
+    lam_sorted[tid] = (float)l;
+    if (ritz_user) ritz_user[tid] = (float)l;
+    coef_r[tid] = on ? (float)(-l) : 0.f;
+    coef_x[tid] = on ? (float)((l > 0.0 ? 1.0 : (l < 0.0 ? -1.0 : 0.0)) / (double)gamma) : 0.f;
+    coef_p[tid] = (on && l > 0.0) ? (float)l : 0.f;
+  }
+}
+
+// --------------------------------------------- rank-K terms as GEMMs -----
+// Us[j][x] = mult c[j] U[j][x] for j < kdef (device count), 0 for kdef <= j < rows.
+__global__ __launch_bounds__(256) void scale_rows_kernel(const float* __restrict__ U, int ld, const float* __restrict__ c,
+                                                         const int* __restrict__ kdef, float mult, int rows,
+                                                         float* __restrict__ Us) {
+  const long long e = (long long)blockIdx.x * 256 + threadIdx.x;
+  if (e >= (long long)rows * ld) return;
+  const int j = (int)(e / ld);
+  Us[e] = j < *kdef ? (mult * c[j]) * U[e] : 0.f;
+}
+
+// Per 128 x 128 tile sums of R^2 (the Frobenius scale's partials, the layout
+// of the residual pass's tile sums). Grid: (n_pad / 128)^2; 256 threads.
+__global__ __launch_bounds__(256) void tile_sumsq_kernel(const float* __restrict__ R, int ld, float* __restrict__ sumsq) {
+  __shared__ float red[4];
+  const int tc = ld / 128;
+  const int i0 = (blockIdx.x / tc) * 128, n0 = (blockIdx.x % tc) * 128;
+  const int rg = threadIdx.x >> 4, cg = threadIdx.x & 15;
+  float ss = 0.f;
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const float* p = R + (long long)(i0 + rg * 8 + r) * ld + n0 + cg * 8;
+    const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int c = 0; c < 8; ++c) ss = fmaf(v[c], v[c], ss);
+  }
+  ss = block_sum(ss, red);
+  if (threadIdx.x == 0) sumsq[blockIdx.x] = ss;
+}
+
+}  // namespace sd

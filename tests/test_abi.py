@@ -142,8 +142,8 @@ def test_psd_invalid_arguments(lib):
     assert lib.sd_psd_project_deflated_ex(16, 16, 5, FAKE, FAKE, FAKE, None, None) == -1   # k >= n
     assert lib.sd_psd_project_deflated_ex(16, 4, 5, FAKE, None, FAKE, None, None) == -1    # no basis
     assert lib.sd_psd_project_deflated_ex(16, 4, -1, FAKE, FAKE, FAKE, None, None) == -1
-    assert lib.sd_psd_project_deflated_ex(200, 65, 5, ctypes.c_void_p(0x100000), ctypes.c_void_p(0x200000),
-                                          ctypes.c_void_p(0x300000), None, None) == -2
+    assert lib.sd_psd_project_deflated_ex(600, 513, 5, ctypes.c_void_p(0x100000), ctypes.c_void_p(0x200000),
+                                          ctypes.c_void_p(0x300000), None, None) == -2   # K > 512
     # the basis may not overlap X or out
     assert lib.sd_psd_project_deflated_ex(16, 4, 5, ctypes.c_void_p(0x10000), ctypes.c_void_p(0x10040),
                                           ctypes.c_void_p(0x20000), None, None) == -1
@@ -169,7 +169,7 @@ def test_admm_invalid_arguments_and_empty_run(lib):
     assert call(16, 3, 1.0, 16, Q) == -1                  # k >= n
     assert call(16, 3, 1.0, 0, None, warmup=-1) == -1
     assert call(16, 3, 1.0, 0, None, C=None) == -1        # missing matrix
-    assert call(200, 3, 1.0, 65, Q) == -2                 # K beyond the supported Rayleigh-Ritz block
+    assert call(600, 3, 1.0, 513, Q) == -2                # K beyond the widest tracked basis (512)
     bad = sd.psd_opts(tau=0.1, window=0)
     assert call(64, 3, 1.0, 4, Q, opts=ctypes.byref(bad)) == -1
     # zero iterations: validated, nothing launched, success

@@ -467,3 +467,118 @@ def test_admm_split_calls_equal_one_call_bitwise():
     for u, v in ((X1, X2), (S1, S2), (y1, y2), (q1, q2)):
         assert torch.equal(u, v)
     assert torch.equal(e1, torch.cat([e2a, e2b])) and torch.equal(d1, torch.cat([d2a, d2b]))
+
+
+# ---------------------------------------------------------------- wide bases
+# K > 64: the K x K problems leave LDS (block Jacobi, one-work-group Cholesky
+# and inverse in global memory, float64 panel products, rank-K terms as
+# float32 GEMMs). Same contract as the narrow path: 1e-4 against the float64
+# oracle, counts exact, Ritz values to 1e-5, the next basis to 1e-4, output
+# exactly symmetric. With every Ritz pair deflated (tau = 0) the outputs do
+# not depend on the eigenvector choice inside clusters of Ritz values.
+@pytest.mark.parametrize("n,k", [(260, 65), (300, 100), (600, 200), (800, 352)])
+def test_wide_basis(n, k):
+    case = workloads.small_psd(n, k=k, case_id=n + 31)
+    say(f"psd wide n={n} k={k}")
+    out, info, q = gpu_psd(case, k)
+    want, vnext, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm[:, :k].astype(np.float64),
+                                                   steps=case.steps, gamma=case.gamma,
+                                                   subspace_iters=case.subspace_iters)
+    err = rel_fro(host64(out), want)
+    say(f"  rel err {err:.3e}  next basis {rel_fro(host64(q), vnext):.3e}  theta {float(info['theta']):.6g} "
+        f"vs {oinfo.theta:.6g}")
+    assert int(info["n_deflated"]) == oinfo.n_deflated == k
+    assert int(info["n_positive"]) == oinfo.n_positive
+    np.testing.assert_allclose(info["ritz"].cpu().numpy(), oinfo.ritz, rtol=1e-5, atol=1e-5 * abs(oinfo.ritz[0]))
+    assert rel_fro(host64(q), vnext) < 1e-4
+    assert err < TOL
+    assert abs(float(info["theta"]) - oinfo.theta) <= 1e-5 * oinfo.theta
+    o = out.cpu().numpy()
+    assert np.array_equal(o, o.T)
+
+
+@pytest.mark.parametrize("scale,precision", [("lanczos", "f16"), ("frobenius", "f32"), ("frobenius", "f16")])
+def test_wide_basis_scale_and_precision(scale, precision):
+    n, k = 512, 100
+    case = workloads.small_psd(n, k=k, case_id=n + 37)
+    say(f"psd wide n={n} k={k} {scale} {precision}")
+    out, info, q = gpu_psd(case, k, scale=scale, precision=precision)
+    want, vnext, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm[:, :k].astype(np.float64),
+                                                   steps=case.steps, gamma=case.gamma,
+                                                   subspace_iters=case.subspace_iters, scale=scale,
+                                                   mode="f16" if precision == "f16" else "exact")
+    err = rel_fro(host64(out), want)
+    say(f"  rel err {err:.3e}")
+    assert int(info["n_deflated"]) == oinfo.n_deflated
+    assert err < (F16_TOL if precision == "f16" else TOL)
+    assert abs(float(info["theta"]) - oinfo.theta) <= 1e-5 * oinfo.theta
+
+
+def test_wide_basis_gate():
+    # the gate of Alg. 2 on a wide basis: 6 dominant pairs well above
+    # tau |lambda_1| and a bulk well below it
+    n, k = 400, 96
+    case = workloads.small_psd(n, k=k, n_dom=6, dom=(100.0, 300.0), case_id=n + 41)
+    out, info, _ = gpu_psd(case, k, tau=0.1, window=48)
+    want, _, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm.astype(np.float64),
+                                               steps=case.steps, gamma=case.gamma, tau=0.1, window=48,
+                                               subspace_iters=case.subspace_iters)
+    err = rel_fro(host64(out), want)
+    say(f"psd wide gate: deflated {int(info['n_deflated'])} vs {oinfo.n_deflated}, rel err {err:.3e}")
+    assert int(info["n_deflated"]) == oinfo.n_deflated == 6
+    assert int(info["n_positive"]) == oinfo.n_positive
+    assert err < TOL
+
+
+@pytest.mark.parametrize("precision", ["f32", "f16"])
+def test_wide_basis_rank_deficient(precision):
+    # rank(Z) = 3 < K = 80: CholeskyQR floors pivots (flag 2); the output is
+    # the exact projection to float32 rounding on both sides
+    g = np.random.default_rng(6)
+    n, k = 300, 80
+    u, _ = np.linalg.qr(g.standard_normal((n, 3)))
+    z = ((u * np.array([5.0, -3.0, 2.0])) @ u.T).astype(np.float32)
+    z = np.triu(z) + np.triu(z, 1).T
+    v0 = np.linalg.qr(g.standard_normal((n, k)))[0].astype(np.float32)
+    say(f"psd wide rank-deficient {precision}")
+    out, info = sd.psd_project(torch.from_numpy(z).cuda(), k, 10, torch.from_numpy(v0).cuda(), subspace_iters=2,
+                               gamma=1.1, info=True, precision=precision)
+    torch.cuda.synchronize()
+    assert int(info["status"][0]) & 2
+    exact = opsd.psd_exact(z.astype(np.float64))
+    assert rel_fro(host64(out), exact) < TOL
+    np.testing.assert_allclose(info["ritz"].cpu().numpy()[:3], [5.0, -3.0, 2.0], rtol=1e-5)
+    o = out.cpu().numpy()
+    assert np.isfinite(o).all() and np.array_equal(o, o.T)
+
+
+@pytest.mark.parametrize("precision", ["f32", "f16"])
+def test_admm_paper_width_against_oracle(precision):
+    """ADMM at the paper's basis width: planted max-cut n = 2000, K =
+    ceil(0.05 n) = 100, r = 50, every Ritz pair deflated (tau = 0, so no
+    gate decision sits near a tie), 4 iterations from zero against the
+    oracle."""
+    from oracle import admm as oadmm
+    case = workloads.planted_maxcut(2000, case_id=11)
+    assert case.k == 100
+    n = case.c.shape[0]
+    say(f"admm n={n} K={case.k} {precision}")
+    C = torch.from_numpy(case.c).cuda()
+    b = torch.from_numpy(case.b).cuda()
+    q = torch.from_numpy(np.ascontiguousarray(case.basis0)).cuda()
+    iters = 4
+    X, S, y, eta, ndef = sd.admm_diag(C, b, iters, case.k, q, warmup=0, tau=0.0, window=case.window,
+                                      precision=precision)
+    torch.cuda.synchronize()
+    proj = oadmm.DeflatedProjector(case.basis0.astype(np.float64), tau=0.0, window=case.window, warmup=0,
+                                   mode="f16" if precision == "f16" else "exact")
+    xo, so, yo, etas = oadmm.admm_diag(case.c.astype(np.float64), case.b.astype(np.float64), iters, proj)
+    ex, es, ey = rel_fro(host64(X), xo), rel_fro(host64(S), so), rel_fro(host64(y), yo)
+    say(f"  X {ex:.2e} S {es:.2e} y {ey:.2e}; eta {float(eta[-1]):.4e} vs {etas[-1]:.4e}; deflated {ndef.tolist()}")
+    assert ndef.cpu().tolist() == proj.n_deflated == [case.k] * iters
+    # the basis is CholQR(Z V) of the last projection's input, which carries
+    # the iterates' accumulated differences: the same bound as X and S
+    tol = ADMM_F32_TOL if precision == "f32" else admm_f16_tol(iters)
+    assert rel_fro(host64(q), proj.basis) < tol
+    assert max(ex, es, ey) < tol
+    np.testing.assert_allclose(eta.cpu().numpy(), etas, rtol=1e-2)
