@@ -519,7 +519,9 @@ struct PsdPlan {
   bool wk;
   int kp, kr;      // K rounded up to 32 (small matrices), to 128 (panel rows)
   double *wpart, *g64, *hb0, *hb1, *eb0, *eb1, *e64, *mt, *lw;
+  double *wpart2, *g64b;   // the next basis' CholeskyQR (side stream)
   float* us;       // scaled copy of U for the rank-K GEMMs
+  float* qn;       // the next basis, CholQR(Z V), panel rows
   BjState* bst;
 };
 
@@ -547,8 +549,11 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
   if (p.wk) {
     const size_t kk = (size_t)p.kp * p.kp;
     p.us = ar.take<float>((size_t)kr * p.n_pad);
+    p.qn = ar.take<float>((size_t)kr * p.n_pad);
     p.wpart = ar.take<double>(kk * cdiv(p.n_pad, WG_CHUNK));
+    p.wpart2 = ar.take<double>(kk * cdiv(p.n_pad, WG_CHUNK));
     p.g64 = ar.take<double>(kk);
+    p.g64b = ar.take<double>(kk);
     p.hb0 = ar.take<double>(kk);
     p.hb1 = ar.take<double>(kk);
     p.eb0 = ar.take<double>(kk);
@@ -664,27 +669,32 @@ __global__ __launch_bounds__(WAVE) void frob_scale_kernel(const float* sumsq, in
 // ------------------------------------------- wide tracked bases ----------
 constexpr int BJ_MAX_SWEEPS = 16;   // block Jacobi sweep cap
 constexpr int BJ_TOL_EXP = -40;     // stop at off(H) <= 2^-40 ||H||_F
+constexpr int BJ_INNER_ROUNDS = BJ_P - 1;   // one sweep of the pair problem per round
 
-// C = A B^T over the panel rows (kp x kp, float64), SYM: A == B.
-static void wide_products(const PsdPlan& p, const float* A, const float* B, bool sym, double* C, hipStream_t st) {
+// C = A B^T over the panel rows (kp x kp, float64), SYM: A == B; part: the
+// chunk partials' scratch.
+static void wide_products(const PsdPlan& p, const float* A, const float* B, bool sym, double* part, double* C,
+                          hipStream_t st) {
   const int np = p.n_pad, kp = p.kp, nch = cdiv(np, WG_CHUNK), tk = cdiv(kp, 64);
   const int tiles = sym ? tk * (tk + 1) / 2 : tk * tk;
   const dim3 gr(cdiv(kp * kp, 256));
   if (sym) {
-    hipLaunchKernelGGL(wide_gram_kernel<true>, dim3(tiles * nch), dim3(256), 0, st, A, np, B, np, kp, np, p.wpart);
-    hipLaunchKernelGGL(wide_gram_reduce_kernel<true>, gr, dim3(256), 0, st, p.wpart, nch, kp, C);
+    hipLaunchKernelGGL(wide_gram_kernel<true>, dim3(tiles * nch), dim3(256), 0, st, A, np, B, np, kp, np, part);
+    hipLaunchKernelGGL(wide_gram_reduce_kernel<true>, gr, dim3(256), 0, st, part, nch, kp, C);
   } else {
-    hipLaunchKernelGGL(wide_gram_kernel<false>, dim3(tiles * nch), dim3(256), 0, st, A, np, B, np, kp, np, p.wpart);
-    hipLaunchKernelGGL(wide_gram_reduce_kernel<false>, gr, dim3(256), 0, st, p.wpart, nch, kp, C);
+    hipLaunchKernelGGL(wide_gram_kernel<false>, dim3(tiles * nch), dim3(256), 0, st, A, np, B, np, kp, np, part);
+    hipLaunchKernelGGL(wide_gram_reduce_kernel<false>, gr, dim3(256), 0, st, part, nch, kp, C);
   }
 }
 
-// dst = CholQR(src) (K panel rows; rows K .. kr - 1 of dst written as zero).
-static void cholqr_wide(const PsdPlan& p, const float* src, float* dst, int* status, hipStream_t st) {
+// dst = CholQR(src) (K panel rows; rows K .. kr - 1 of dst written as zero),
+// with the partials' scratch `part` and the Gram buffer `g`.
+static void cholqr_wide(const PsdPlan& p, const float* src, float* dst, int* status, double* part, double* g,
+                        hipStream_t st) {
   ProfScope ps(SD_STAGE_CHOLQR, st);
   const int np = p.n_pad;
-  wide_products(p, src, src, true, p.g64, st);
-  hipLaunchKernelGGL(chol_inv_wide_kernel, dim3(1), dim3(CI_THREADS), 0, st, p.g64, p.K, p.kp, p.lw, p.mt, status);
+  wide_products(p, src, src, true, part, g, st);
+  hipLaunchKernelGGL(chol_inv_wide_kernel, dim3(1), dim3(CI_THREADS), 0, st, g, p.K, p.kp, p.lw, p.mt, status);
   hipLaunchKernelGGL(wide_rotate_kernel, dim3(cdiv(p.kr, 64) * (np / 64)), dim3(256), 0, st, p.mt, p.kp, src, np,
                      p.kp, p.K, np, dst, np, p.kr);
 }
@@ -716,15 +726,15 @@ static void rankk_wide(const PsdPlan& p, const float* coef, float mult, const fl
 static void ritz_wide(const PsdPlan& p, const float* vt, const float* zt, const sd_psd_opts& o, hipStream_t st) {
   ProfScope ps(SD_STAGE_SMALL, st);
   const int kp = p.kp, np = p.n_pad, nb = kp / BJ_B, P = nb / 2, rps = nb - 1;
-  wide_products(p, vt, zt, false, p.g64, st);
+  wide_products(p, vt, zt, false, p.wpart, p.g64, st);
   hipLaunchKernelGGL(bj_init_kernel, dim3(cdiv(kp * kp, 256)), dim3(256), 0, st, p.g64, kp, p.hb0, p.eb0, p.bst);
-  const dim3 grid(P * P + P * cdiv(kp, 64));
+  const dim3 grid(P * P + P * (kp / BJ_P));
   for (int sweep = 0; sweep < BJ_MAX_SWEEPS; ++sweep) {
     for (int t = 0; t < rps; ++t) {
       const long long g = (long long)sweep * rps + t;
       const bool odd = g & 1;
       hipLaunchKernelGGL(bj_round_kernel, grid, dim3(128), 0, st, odd ? p.hb1 : p.hb0, odd ? p.hb0 : p.hb1,
-                         odd ? p.eb1 : p.eb0, odd ? p.eb0 : p.eb1, kp, nb, t, 2 * BJ_B - 1, p.bst);
+                         odd ? p.eb1 : p.eb0, odd ? p.eb0 : p.eb1, kp, nb, t, BJ_INNER_ROUNDS, p.bst);
     }
     hipLaunchKernelGGL(bj_check_kernel, dim3(1), dim3(1024), 0, st, p.hb0, p.hb1, kp, rps, sweep, BJ_MAX_SWEEPS,
                        BJ_TOL_EXP, p.bst);
@@ -734,6 +744,34 @@ static void ritz_wide(const PsdPlan& p, const float* vt, const float* zt, const 
                      o.n_deflated_out, o.n_positive_out);
   hipLaunchKernelGGL(wide_rotate_kernel, dim3(cdiv(kp, 64) * (np / 64)), dim3(256), 0, st, p.e64, kp, vt, np, kp,
                      kp, np, p.ut, np, kp);
+}
+
+// Library-owned side stream per device (non-blocking, default priority,
+// kept until the process ends) for the wide path's next-basis CholeskyQR,
+// which only the final basis write waits for: it runs beside the
+// Rayleigh-Ritz step. Enqueues that use it hold `mu`.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+  std::mutex mu;
+  bool ready = false;
+};
+
+static int side_stream(SideStream*& ss) {
+  static std::mutex mu;
+  static SideStream per_dev[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return SD_ERR_HIP;
+  std::lock_guard<std::mutex> g(mu);
+  SideStream& d = per_dev[dev];
+  if (!d.ready) {
+    if (hipStreamCreateWithFlags(&d.s, hipStreamNonBlocking) != hipSuccess) return SD_ERR_HIP;
+    if (hipEventCreateWithFlags(&d.fork, hipEventDisableTiming) != hipSuccess) return SD_ERR_HIP;
+    if (hipEventCreateWithFlags(&d.join, hipEventDisableTiming) != hipSuccess) return SD_ERR_HIP;
+    d.ready = true;
+  }
+  ss = &d;
+  return SD_OK;
 }
 
 static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, const sd_psd_opts& o,
@@ -756,21 +794,30 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   la.ldx = np;
   la.ldo = np;
   la.ldl = la.ldr = np;
+  SideStream* ss = nullptr;
+  std::unique_lock<std::mutex> side_lock;
   if (K > 0 && p.wk) {
     // wide basis: V panel (rows K .. kr - 1 zero), (J - 1) x [Z V, CholQR],
-    // Z V, Rayleigh-Ritz, R = Z - U lam U^T as a GEMM, next basis
+    // Z V, then the next basis CholQR(Z V) on the side stream beside
+    // Rayleigh-Ritz and R = Z - U lam U^T (a GEMM); the basis is written
+    // back at the end of the call
+    const int rc = side_stream(ss);
+    if (rc != SD_OK) return rc;
+    side_lock = std::unique_lock<std::mutex>(ss->mu);
     fill(p.vt + (long long)K * np, (long long)(p.kr - K) * np, 0.f, st);
     hipLaunchKernelGGL(rows_to_panel_kernel, grid1((long long)K * np, 256), dim3(256), 0, st, Qwarm, K, n, np, p.vt);
     for (int j = 0; j + 1 < o.subspace_iters; ++j) {
       zv_wide(p, z, p.vt, p.zt, st);
-      cholqr_wide(p, p.zt, p.vt, o.status_dev, st);
+      cholqr_wide(p, p.zt, p.vt, o.status_dev, p.wpart, p.g64, st);
     }
     zv_wide(p, z, p.vt, p.zt, st);
+    if (hipEventRecord(ss->fork, st) != hipSuccess || hipStreamWaitEvent(ss->s, ss->fork, 0) != hipSuccess)
+      return SD_ERR_HIP;
+    cholqr_wide(p, p.zt, p.qn, o.status_dev, p.wpart2, p.g64b, ss->s);
+    if (hipEventRecord(ss->join, ss->s) != hipSuccess) return SD_ERR_HIP;
     ritz_wide(p, p.vt, p.zt, o, st);
     rankk_wide(p, p.coefR, 1.f, z, nullptr, p.r, nullptr, st);
     if (p.frob) hipLaunchKernelGGL(tile_sumsq_kernel, dim3((np / 128) * (np / 128)), dim3(256), 0, st, p.r, np, p.sumsq);
-    cholqr_wide(p, p.zt, p.vt, o.status_dev, st);
-    hipLaunchKernelGGL(panel_to_rows_kernel, grid1((long long)n * K, 256), dim3(256), 0, st, p.vt, np, K, n, Qwarm);
   } else if (K > 0) {
     hipLaunchKernelGGL(rows_to_panel_kernel, grid1((long long)K * np, 256), dim3(256), 0, st, Qwarm, K, n, np, p.vt);
     float* vt = p.vt;
@@ -993,6 +1040,10 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     hipLaunchKernelGGL((psd_out_kernel<32>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
   else
     hipLaunchKernelGGL((psd_out_kernel<64>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
+  if (ss) {   // wide basis: join the side stream, write the next basis
+    if (hipStreamWaitEvent(st, ss->join, 0) != hipSuccess) return SD_ERR_HIP;
+    hipLaunchKernelGGL(panel_to_rows_kernel, grid1((long long)n * K, 256), dim3(256), 0, st, p.qn, np, K, n, Qwarm);
+  }
   return hip_status();
 }
 

@@ -7,8 +7,8 @@
 //   * CholeskyQR's factor and the inverse of the triangular factor on one
 //     work-group, the K x K matrices in global memory (L2-resident), panels
 //     of 32 columns in LDS;
-//   * a block Jacobi eigensolver over 16-index blocks: every round pairs the
-//     blocks by the circle method and rotates each 32 x 32 pair problem with
+//   * a block Jacobi eigensolver over 8-index blocks: every round pairs the
+//     blocks by the circle method and rotates each 16 x 16 pair problem with
 //     one sweep of the one-wave Jacobi (the same rotations a scalar cyclic
 //     Jacobi would apply in a block ordering), one launch per round, a
 //     convergence check after every sweep;
@@ -25,7 +25,8 @@ namespace sd {
 
 constexpr int WIDE_MAX = 512;     // widest tracked basis of this path
 constexpr int WG_CHUNK = 512;     // positions per partial of the float64 products
-constexpr int BJ_B = 16;          // block Jacobi: indices per block (pairs of 32)
+constexpr int BJ_B = 8;           // block Jacobi: indices per block
+constexpr int BJ_P = 2 * BJ_B;    // indices per pair problem
 
 // -------------------------------------------- float64 panel products -----
 // part[ch][a][b] = sum over the positions x of chunk ch of A[a][x] B[b][x],
@@ -356,10 +357,10 @@ struct BjState {
 };
 
 struct PairLds {
-  double h[2 * BJ_B][2 * BJ_B + 1];
-  double e[2 * BJ_B][2 * BJ_B + 1];
-  double h2[2 * BJ_B][2 * BJ_B + 1];
-  double e2[2 * BJ_B][2 * BJ_B + 1];
+  double h[BJ_P][BJ_P + 1];
+  double e[BJ_P][BJ_P + 1];
+  double h2[BJ_P][BJ_P + 1];
+  double e2[BJ_P][BJ_P + 1];
 };
 
 // Blocks of pair j in round t of the circle method over nb (even) blocks
@@ -372,7 +373,7 @@ __device__ __forceinline__ void bj_pair(int t, int j, int nb, int& pa, int& pb) 
   pa = j == 0 ? 0 : u + 1;
   pb = w + 1;
 }
-// Global index of local index l (0..31) of the pair of blocks (pa, pb).
+// Global index of local index l (0 .. BJ_P - 1) of the pair of blocks (pa, pb).
 __device__ __forceinline__ int bj_index(int l, int pa, int pb) {
   return l < BJ_B ? BJ_B * pa + l : BJ_B * pb + (l - BJ_B);
 }
@@ -391,23 +392,23 @@ __global__ __launch_bounds__(256) void bj_init_kernel(const double* __restrict__
   E0[e] = i == j ? 1.0 : 0.0;
 }
 
-// One wave: the 32 x 32 problem of blocks (pa, pb) into s.h, then `rounds`
-// rounds of the one-wave Jacobi; s.e is the accumulated rotation J.
+// One wave: the BJ_P x BJ_P problem of blocks (pa, pb) into s.h, then
+// `rounds` rounds of the one-wave Jacobi (0: until converged); s.e is the
+// accumulated rotation J.
 __device__ __forceinline__ void bj_solve(const double* __restrict__ H, int kp, int pa, int pb, PairLds& s,
                                          int rounds) {
   const int lane = threadIdx.x & (WAVE - 1);
-#pragma unroll
-  for (int u = 0; u < 16; ++u) {
-    const int e = lane + WAVE * u, l = e >> 5, q = e & 31;
+  for (int e = lane; e < BJ_P * BJ_P; e += WAVE) {
+    const int l = e / BJ_P, q = e - l * BJ_P;
     s.h[l][q] = H[(long long)bj_index(l, pa, pb) * kp + bj_index(q, pa, pb)];
   }
   wave_sync();
-  jacobi_eig_wave<BJ_B>(s, 2 * BJ_B, -48, rounds);
+  jacobi_eig_wave<BJ_B>(s, BJ_P, -48, rounds);
 }
 
 // One round: P = nb / 2 pairs. Work-groups 0 .. P^2 - 1 write the H block of
 // pairs (a, b), Hout[a][b] = J_a^T Hin[a][b] J_b (wave 0 solves pair a, wave 1
-// pair b); the next P * cdiv(kp, 64) update 64 rows of E on pair a's
+// pair b); the next P * (kp / BJ_P) update BJ_P rows of E on pair a's
 // columns, Eout = Ein J_a. Every work-group that needs J_a computes it from the
 // same entries in the same order, so all copies agree. Reads Hin/Ein, writes
 // Hout/Eout (the caller alternates the buffers). 128 threads.
@@ -428,50 +429,46 @@ __global__ __launch_bounds__(128) void bj_round_kernel(const double* __restrict_
     else if (a != b) bj_solve(Hin, kp, pb, qb, sb, rounds);
     __syncthreads();
     const PairLds& jb = a == b ? sa : sb;
-    for (int e = tid; e < 1024; e += 128) {
-      const int l = e >> 5, q = e & 31;
+    for (int e = tid; e < BJ_P * BJ_P; e += 128) {
+      const int l = e / BJ_P, q = e - l * BJ_P;
       sa.h[l][q] = Hin[(long long)bj_index(l, pa, qa) * kp + bj_index(q, pb, qb)];
     }
     __syncthreads();
-    for (int e = tid; e < 1024; e += 128) {   // T = H_ab J_b
-      const int l = e >> 5, m = e & 31;
+    for (int e = tid; e < BJ_P * BJ_P; e += 128) {   // T = H_ab J_b
+      const int l = e / BJ_P, m = e - l * BJ_P;
       double v = 0.0;
 #pragma unroll 8
-      for (int q = 0; q < 32; ++q) v = fma(sa.h[l][q], jb.e[q][m], v);
+      for (int q = 0; q < BJ_P; ++q) v = fma(sa.h[l][q], jb.e[q][m], v);
       sa.h2[l][m] = v;
     }
     __syncthreads();
-    for (int e = tid; e < 1024; e += 128) {   // J_a^T T
-      const int l = e >> 5, m = e & 31;
+    for (int e = tid; e < BJ_P * BJ_P; e += 128) {   // J_a^T T
+      const int l = e / BJ_P, m = e - l * BJ_P;
       double v = 0.0;
 #pragma unroll 8
-      for (int q = 0; q < 32; ++q) v = fma(sa.e[q][l], sa.h2[q][m], v);
+      for (int q = 0; q < BJ_P; ++q) v = fma(sa.e[q][l], sa.h2[q][m], v);
       Hout[(long long)bj_index(l, pa, qa) * kp + bj_index(m, pb, qb)] = v;
     }
     return;
   }
   const int idx = bid - nh;
-  const int a = idx % P, r0 = (idx / P) * 64;
+  const int a = idx % P, r0 = (idx / P) * BJ_P;
   int pa, qa;
   bj_pair(t, a, nb, pa, qa);
   if (wave == 0) bj_solve(Hin, kp, pa, qa, sa, rounds);
   __syncthreads();
-  // rows r0 .. r0 + 63 of E on the pair's columns, staged in sa.h (rows 0-31)
-  // and sa.h2 (rows 32-63)
-  for (int e = tid; e < 2048; e += 128) {
-    const int rr = e >> 5, q = e & 31, r = r0 + rr;
-    const double v = r < kp ? Ein[(long long)r * kp + bj_index(q, pa, qa)] : 0.0;
-    if (rr < 32) sa.h[rr][q] = v;
-    else sa.h2[rr - 32][q] = v;
+  // rows r0 .. r0 + BJ_P - 1 of E on the pair's columns, staged in sa.h
+  for (int e = tid; e < BJ_P * BJ_P; e += 128) {
+    const int rr = e / BJ_P, q = e - rr * BJ_P, r = r0 + rr;
+    sa.h[rr][q] = r < kp ? Ein[(long long)r * kp + bj_index(q, pa, qa)] : 0.0;
   }
   __syncthreads();
-  for (int e = tid; e < 2048; e += 128) {
-    const int rr = e >> 5, m = e & 31, r = r0 + rr;
+  for (int e = tid; e < BJ_P * BJ_P; e += 128) {
+    const int rr = e / BJ_P, m = e - rr * BJ_P, r = r0 + rr;
     if (r >= kp) continue;
-    const double* er = rr < 32 ? sa.h[rr] : sa.h2[rr - 32];
     double v = 0.0;
 #pragma unroll 8
-    for (int q = 0; q < 32; ++q) v = fma(er[q], sa.e[q][m], v);
+    for (int q = 0; q < BJ_P; ++q) v = fma(sa.h[rr][q], sa.e[q][m], v);
     Eout[(long long)r * kp + bj_index(m, pa, qa)] = v;
   }
 }
