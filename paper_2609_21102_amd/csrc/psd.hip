@@ -518,7 +518,8 @@ struct PsdPlan {
   // wide tracked bases (K > SM_MAX): K x K problems in global memory
   bool wk;
   int kp, kr;      // K rounded up to 32 (small matrices), to 128 (panel rows)
-  double *wpart, *g64, *hb0, *hb1, *eb0, *eb1, *e64, *mt, *lw;
+  double *wpart, *g64, *hb0, *hb1, *eb0, *eb1, *e64, *lw, *dinv, *q64;
+  int* czero;      // CholeskyQR: zero-trace flag
   double *wpart2, *g64b;   // the next basis' CholeskyQR (side stream)
   float* us;       // scaled copy of U for the rank-K GEMMs
   float* qn;       // the next basis, CholQR(Z V), panel rows
@@ -559,8 +560,10 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
     p.eb0 = ar.take<double>(kk);
     p.eb1 = ar.take<double>(kk);
     p.e64 = ar.take<double>(kk);
-    p.mt = ar.take<double>(kk);
     p.lw = ar.take<double>(kk);
+    p.dinv = ar.take<double>((size_t)p.kp * CW);
+    p.q64 = ar.take<double>((size_t)p.kp * p.n_pad);
+    p.czero = ar.take<int>(1);
     p.bst = ar.take<BjState>(1);
   }
   p.coefR = ar.take<float>(kq);
@@ -688,15 +691,18 @@ static void wide_products(const PsdPlan& p, const float* A, const float* B, bool
 }
 
 // dst = CholQR(src) (K panel rows; rows K .. kr - 1 of dst written as zero),
-// with the partials' scratch `part` and the Gram buffer `g`.
+// with the partials' scratch `part` and the Gram buffer `g`. src and dst may
+// not overlap.
 static void cholqr_wide(const PsdPlan& p, const float* src, float* dst, int* status, double* part, double* g,
                         hipStream_t st) {
   ProfScope ps(SD_STAGE_CHOLQR, st);
-  const int np = p.n_pad;
+  const int np = p.n_pad, nbk = cdiv(p.K, CW);
   wide_products(p, src, src, true, part, g, st);
-  hipLaunchKernelGGL(chol_inv_wide_kernel, dim3(1), dim3(CI_THREADS), 0, st, g, p.K, p.kp, p.lw, p.mt, status);
-  hipLaunchKernelGGL(wide_rotate_kernel, dim3(cdiv(p.kr, 64) * (np / 64)), dim3(256), 0, st, p.mt, p.kp, src, np,
-                     p.kp, p.K, np, dst, np, p.kr);
+  hipLaunchKernelGGL(chol_wide_kernel, dim3(1), dim3(CF_THREADS), 0, st, g, p.K, p.kp, p.lw, p.dinv, p.czero, status);
+  fill(dst + (long long)p.K * np, (long long)(p.kr - p.K) * np, 0.f, st);
+  for (int ib = 0; ib < nbk; ++ib)
+    hipLaunchKernelGGL(chol_solve_wide_kernel, dim3(np / 64), dim3(256), 0, st, src, np, p.K, p.kp, p.lw, p.dinv,
+                       p.czero, ib, p.q64, dst);
 }
 
 // Zt = V^T Z^T = (Z V)^T on the float32 MFMA GEMM (Z symmetric: its rows).

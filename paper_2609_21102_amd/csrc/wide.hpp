@@ -4,15 +4,15 @@
 // path splits them:
 //   * float64 products of panel rows (the CholeskyQR Gram Z^T Z and the
 //     Rayleigh quotient V^T Z V) over position chunks, reduced in chunk order;
-//   * CholeskyQR's factor and the inverse of the triangular factor on one
-//     work-group, the K x K matrices in global memory (L2-resident), panels
-//     of 32 columns in LDS;
+//   * CholeskyQR's factor on one work-group, the K x K matrix in global
+//     memory (L2-resident), panels of 16 columns in LDS and registers; the
+//     panel Q^T = L^-1 Z^T by block rows of 16 over all positions;
 //   * a block Jacobi eigensolver over 8-index blocks: every round pairs the
 //     blocks by the circle method and rotates each 16 x 16 pair problem with
 //     one sweep of the one-wave Jacobi (the same rotations a scalar cyclic
 //     Jacobi would apply in a block ordering), one launch per round, a
 //     convergence check after every sweep;
-//   * the rotations V E and Z L^-T as float64-accumulated products; the
+//   * the rotation V E as a float64-accumulated product; the
 //     rank-K terms of the residual, the padded start and the restore as
 //     float32 MFMA GEMMs with an axpy epilogue (gemm.hpp).
 #pragma once
@@ -117,87 +117,115 @@ __global__ __launch_bounds__(256) void wide_gram_reduce_kernel(const double* __r
   C[e] = t;
 }
 
-// ---------------------------------- CholeskyQR factor and its inverse -----
-// Gram = L L^T for the leading c x c block of G (kp x kp, float64), right-
-// looking by panels of 32 columns, pivots below c u tr(Gram) raised to that
-// floor (flag 2 in status) as in the narrow path; then M = L^-1 by block
-// rows, written transposed: MT[j][i] = M[i][j] (zero outside the c x c lower
-// triangle), so that Q^T = M Z^T is the float64 rotation MT^T Z^T. A zero
-// trace gives MT = 0 (a zero panel). One work-group of 1024 threads; L and
-// MT live in global memory (L2), the current panel in LDS.
-constexpr int CI_THREADS = 1024;
+// ------------------------------------------------------ CholeskyQR -----
+// Factor: Gram = L L^T for the leading c x c block of G (kp x kp, float64),
+// right-looking by panels of CW = 16 columns, pivots below c u tr(Gram) raised to
+// that floor (flag 2 in status) as in the narrow path. One work-group of 512
+// threads; L lives in global memory (L2), the panel in LDS:
+//   * the CW x CW diagonal block on one wave, row i in lane i's registers; at
+//     step j every lane publishes its entry of column j in LDS and reads the
+//     column back (one round trip per step), then updates its own row;
+//   * the inverse of the diagonal block, column t in lane t's registers
+//     (forward substitution), written to Dinv[jb] for the solve below;
+//   * the rows below: one row per thread in registers, P D^-T by forward
+//     substitution, kept in LDS for the trailing update (4 x 4 blocks).
+// A zero trace sets *zero (the solve then writes a zero panel).
+constexpr int CF_THREADS = 512;
+constexpr int CW = 16;   // panel width (rows of the solve's blocks)
+constexpr int CPS = CW + 1;   // LDS row stride of the panel (odd: rows fall in distinct banks)
 
-__global__ __launch_bounds__(CI_THREADS) void chol_inv_wide_kernel(const double* __restrict__ G, int c, int kp,
-                                                                   double* __restrict__ L, double* __restrict__ MT,
-                                                                   int* status) {
-  __shared__ double D[32][33];
-  __shared__ double Dinv[32][33];
-  __shared__ double P[WIDE_MAX * 32];   // panel rows below the diagonal block; then the block products T
-  __shared__ double red[CI_THREADS / WAVE];
-  __shared__ int floored;
+__global__ __launch_bounds__(CF_THREADS) void chol_wide_kernel(const double* __restrict__ G, int c, int kp,
+                                                               double* __restrict__ L, double* __restrict__ Dinv,
+                                                               int* zero, int* status) {
+  __shared__ double colv[CW];
+  __shared__ double D[CW][CW + 1];
+  __shared__ double P[WIDE_MAX * CPS];
+  __shared__ double red[CF_THREADS / WAVE];
   const int tid = threadIdx.x;
   double tr = 0.0;
-  for (int a = tid; a < c; a += CI_THREADS) tr += G[(long long)a * kp + a];
+  for (int a = tid; a < c; a += CF_THREADS) tr += G[(long long)a * kp + a];
   tr = block_sum(tr, red);
-  for (long long e = tid; e < (long long)kp * kp; e += CI_THREADS) {
-    MT[e] = 0.0;
-    L[e] = G[e];
-  }
-  if (tid == 0) floored = 0;
+  for (int i = 0; i < kp; ++i)
+    for (int k = tid; k < kp; k += CF_THREADS) L[(long long)i * kp + k] = G[(long long)i * kp + k];
+  if (tid == 0) *zero = tr == 0.0;
   __syncthreads();
   if (tr == 0.0) return;
   const double floor_ = (double)c * 1.1102230246251565e-16 * tr;
-  // ---- factor
-  for (int j0 = 0; j0 < c; j0 += 32) {
-    const int w = min(32, c - j0);
-    for (int e = tid; e < 32 * 32; e += CI_THREADS) {
-      const int r = e >> 5, q = e & 31;
-      D[r][q] = (r < w && q < w) ? L[(long long)(j0 + r) * kp + j0 + q] : 0.0;
-    }
-    __syncthreads();
+  bool floored = false;
+  for (int j0 = 0; j0 < c; j0 += CW) {
+    const int w = min(CW, c - j0);
     if (tid < WAVE) {
+      // rows past w are identity rows (unit pivot, no coupling)
       const int lane = tid;
-      for (int jj = 0; jj < w; ++jj) {
-        double d = D[jj][jj];
-        if (d <= floor_) {
+      double h[CW];
+#pragma unroll
+      for (int k = 0; k < CW; ++k)
+        h[k] = (lane < w && k <= lane) ? L[(long long)(j0 + lane) * kp + j0 + k] : (k == lane ? 1.0 : 0.0);
+#pragma unroll
+      for (int j = 0; j < CW; ++j) {
+        if (lane < CW) colv[lane] = h[j];
+        wave_sync();
+        double cv[CW];
+#pragma unroll
+        for (int k = j; k < CW; ++k) cv[k] = colv[k];
+        wave_sync();
+        double d = cv[j];
+        if (j < w && d <= floor_) {
           d = floor_;
-          if (lane == 0) floored = 1;
+          floored = true;
         }
-        const double piv = sqrt(d);
-        wave_sync();
-        if (lane == jj) D[jj][jj] = piv;
-        if (lane > jj && lane < w) D[lane][jj] = D[lane][jj] / piv;
-        wave_sync();
-        if (lane > jj && lane < w) {
-          const double lij = D[lane][jj];
-          for (int k = jj + 1; k <= lane; ++k) D[lane][k] -= lij * D[k][jj];
+        const double piv = sqrt(d), r = 1.0 / piv;
+        const double lij = lane > j ? h[j] * r : (lane == j ? piv : 0.0);
+        h[j] = lij;
+#pragma unroll
+        for (int k = j + 1; k < CW; ++k)
+          if (lane >= k) h[k] -= lij * (cv[k] * r);
+        __builtin_amdgcn_sched_barrier(0);   // keep each step's loads in its step (register pressure)
+      }
+      if (lane < CW) {
+#pragma unroll
+        for (int k = 0; k < CW; ++k) {
+          D[lane][k] = k <= lane ? h[k] : 0.0;
+          if (lane < w && k <= lane) L[(long long)(j0 + lane) * kp + j0 + k] = h[k];
         }
-        wave_sync();
+      }
+      wave_sync();
+      if (lane < CW) {   // column t = lane of the block's inverse
+        const int t = lane;
+        double x[CW];
+#pragma unroll
+        for (int i = 0; i < CW; ++i) {
+          double v = i == t ? 1.0 : 0.0;
+#pragma unroll
+          for (int u = 0; u < i; ++u) v -= D[i][u] * x[u];
+          x[i] = i < t ? 0.0 : v / D[i][i];
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        double* di = Dinv + (long long)(j0 / CW) * CW * CW;
+#pragma unroll
+        for (int i = 0; i < CW; ++i) di[i * CW + t] = x[i];
       }
     }
     __syncthreads();
-    // panel below the block: row i solves P[i] D^T = G'[i] (one row per thread)
     const int m = c - j0 - w;
-    for (int rr = tid; rr < m; rr += CI_THREADS) {
+    for (int rr = tid; rr < m; rr += CF_THREADS) {
+      // this thread's row, solved in place in LDS (column-oriented forward
+      // substitution; D is read by every thread alike: broadcast)
       const long long row = (long long)(j0 + w + rr) * kp + j0;
-      double* pr = P + rr * 32;   // this thread's row, solved in place
-      for (int t = 0; t < 32; ++t) pr[t] = t < w ? L[row + t] : 0.0;
+      double* pr = P + rr * CPS;
+      for (int t = 0; t < CW; ++t) pr[t] = t < w ? L[row + t] : 0.0;
       for (int t = 0; t < w; ++t) {
-        double v = pr[t];
-        for (int u = 0; u < t; ++u) v -= pr[u] * D[t][u];
-        pr[t] = v / D[t][t];
-        L[row + t] = pr[t];
+        const double v = pr[t] / D[t][t];
+        pr[t] = v;
+        L[row + t] = v;
+        for (int u = t + 1; u < w; ++u) pr[u] -= v * D[u][t];
       }
-    }
-    for (int e = tid; e < w * w; e += CI_THREADS) {
-      const int r = e / w, q = e - r * w;
-      if (q <= r) L[(long long)(j0 + r) * kp + j0 + q] = D[r][q];
     }
     __syncthreads();
     // trailing update of the lower triangle, 4 x 4 blocks per thread
     const int nbm = cdiv(m, 4);
     const int nblk = nbm * (nbm + 1) / 2;
-    for (int blk = tid; blk < nblk; blk += CI_THREADS) {
+    for (int blk = tid; blk < nblk; blk += CF_THREADS) {
       int bi = (int)((sqrt(8.0 * blk + 1.0) - 1.0) * 0.5);
       while (bi * (bi + 1) / 2 > blk) --bi;
       while ((bi + 1) * (bi + 2) / 2 <= blk) ++bi;
@@ -211,8 +239,8 @@ __global__ __launch_bounds__(CI_THREADS) void chol_inv_wide_kernel(const double*
         double pi[4], pk[4];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          pi[i] = 4 * bi + i < m ? P[(4 * bi + i) * 32 + t] : 0.0;
-          pk[i] = 4 * bk + i < m ? P[(4 * bk + i) * 32 + t] : 0.0;
+          pi[i] = 4 * bi + i < m ? P[(4 * bi + i) * CPS + t] : 0.0;
+          pk[i] = 4 * bk + i < m ? P[(4 * bk + i) * CPS + t] : 0.0;
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -230,60 +258,74 @@ __global__ __launch_bounds__(CI_THREADS) void chol_inv_wide_kernel(const double*
     __syncthreads();
   }
   if (tid == 0 && floored && status) atomicOr(status, 2);
-  // ---- inverse by block rows: M_ii = L_ii^-1, M_ij = -L_ii^-1 sum_{j <= k < i} L_ik M_kj
-  for (int i0 = 0; i0 < c; i0 += 32) {
-    const int w = min(32, c - i0);
-    for (int e = tid; e < 32 * 32; e += CI_THREADS) {
-      const int r = e >> 5, q = e & 31;
-      D[r][q] = (r < w && q <= r) ? L[(long long)(i0 + r) * kp + i0 + q] : 0.0;
+}
+
+// Solve: rows i0 .. i0 + CW - 1 (block ib, i0 = CW ib) of Q^T = L^-1 Z^T,
+//   Q_ib = Dinv_ib (Z_ib - sum_{u < i0} L[i0 + r][u] Q[u]),
+// by block rows, one launch per block (the blocks before it are done).
+// Q64 keeps the float64 rows for the later blocks, Q the float32 rows (rows
+// at or past c are not written). Work-group: CW rows x 64 positions; thread
+// (r, g) owns row r and positions x0 + 4 g .. + 3. Grid: len / 64; 256 threads.
+__global__ __launch_bounds__(256) void chol_solve_wide_kernel(const float* __restrict__ Zt, int ld, int c, int kp,
+                                                              const double* __restrict__ L,
+                                                              const double* __restrict__ Dinv, const int* zero,
+                                                              int ib, double* __restrict__ Q64,
+                                                              float* __restrict__ Q) {
+  static_assert(CW == 16, "thread layout: 16 rows x 16 position groups");
+  __shared__ double ls[CW][33];
+  __shared__ double qs[32][65];
+  const int tid = threadIdx.x, r = tid >> 4, g = tid & 15;
+  const int i0 = CW * ib, x0 = blockIdx.x * 64 + 4 * g;
+  const bool live = i0 + r < c;
+  double acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) acc[j] = live ? (double)Zt[(long long)(i0 + r) * ld + x0 + j] : 0.0;
+  for (int u0 = 0; u0 < i0; u0 += 32) {
+    const int uw = min(32, i0 - u0);   // i0 is a multiple of 16: 16 or 32
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int e = tid + 256 * q, rr = e >> 5, uu = e & 31;
+      ls[rr][uu] = (i0 + rr < c && uu < uw) ? L[(long long)(i0 + rr) * kp + u0 + uu] : 0.0;
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + 256 * q, uu = e >> 6, xx = e & 63;
+      qs[uu][xx] = uu < uw ? Q64[(long long)(u0 + uu) * ld + blockIdx.x * 64 + xx] : 0.0;
     }
     __syncthreads();
-    if (tid < 32) {   // column t of the diagonal block's inverse
-      const int t = tid;
-      for (int i = 0; i < 32; ++i) Dinv[i][t] = 0.0;
-      if (t < w) {
-        Dinv[t][t] = 1.0 / D[t][t];
-        for (int i = t + 1; i < w; ++i) {
-          double s = 0.0;
-          for (int u = t; u < i; ++u) s += D[i][u] * Dinv[u][t];
-          Dinv[i][t] = -s / D[i][i];
-        }
-      }
+#pragma unroll 4
+    for (int uu = 0; uu < 32; ++uu) {
+      const double l = ls[r][uu];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[j] = fma(-l, qs[uu][4 * g + j], acc[j]);
     }
     __syncthreads();
-    const int nbi = i0 / 32;
-    double* T = P;
-    for (int e = tid; e < nbi * 1024; e += CI_THREADS) {
-      const int jb = e >> 10, r = (e >> 5) & 31, q = e & 31;
-      double s = 0.0;
-      if (r < w) {
-        const double* lr = L + (long long)(i0 + r) * kp;
-        const double* mr = MT + (long long)(32 * jb + q) * kp;
-        for (int u = 32 * jb; u < i0; ++u) s = fma(lr[u], mr[u], s);
-      }
-      T[e] = s;
-    }
-    __syncthreads();
-    for (int e = tid; e < nbi * 1024; e += CI_THREADS) {
-      const int jb = e >> 10, r = (e >> 5) & 31, q = e & 31;
-      if (r < w) {
-        double v = 0.0;
-        for (int u = 0; u < w; ++u) v = fma(Dinv[r][u], T[(jb << 10) + u * 32 + q], v);
-        MT[(long long)(32 * jb + q) * kp + i0 + r] = -v;
-      }
-    }
-    for (int e = tid; e < 32 * 32; e += CI_THREADS) {
-      const int r = e >> 5, q = e & 31;
-      if (r < w && q <= r) MT[(long long)(i0 + q) * kp + i0 + r] = Dinv[r][q];
-    }
-    __syncthreads();
+  }
+  // diagonal block: q = Dinv_ib acc over the block's rows
+#pragma unroll
+  for (int j = 0; j < 4; ++j) qs[r][4 * g + j] = acc[j];
+  __syncthreads();
+  const double* di = Dinv + (long long)ib * CW * CW + r * CW;
+  double out[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int v = 0; v <= r; ++v) {
+    const double dv = di[v];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[j] = fma(dv, qs[v][4 * g + j], out[j]);
+  }
+  if (!live) return;
+  const bool z = *zero != 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const double v = z ? 0.0 : out[j];
+    Q64[(long long)(i0 + r) * ld + x0 + j] = v;
+    Q[(long long)(i0 + r) * ld + x0 + j] = (float)v;
   }
 }
 
 // ------------------------------------------------ float64 rotations -----
 // out[i][x] = sum_{j < kin} M[j][i] P[j][x] for i < kout (float64, j order,
 // rounded once), rows kout .. rows_out - 1 written as zero; len a multiple of
-// 64. Used for U = V E (M = E) and Q = Z L^-T (M = MT). Tiles of 64 outputs
+// 64. Used for U = V E (M = E). Tiles of 64 outputs
 // x 64 positions; thread (ty, tx) owns rows i0 + ty + 16 ii and positions
 // x0 + 4 tx .. + 3. Grid: cdiv(rows_out, 64) * (len / 64); 256 threads.
 __global__ __launch_bounds__(256) void wide_rotate_kernel(const double* __restrict__ M, int ldm,
@@ -485,8 +527,8 @@ __global__ __launch_bounds__(1024) void bj_check_kernel(const double* __restrict
   const long long g = (long long)(sweep + 1) * rounds_per_sweep;
   const double* H = (g & 1) ? H1 : H0;
   double off = 0.0, tot = 0.0;
-  for (long long e = threadIdx.x; e < (long long)kp * kp; e += 1024) {
-    const int i = (int)(e / kp), j = (int)(e - (long long)i * kp);
+  for (int e = threadIdx.x; e < kp * kp; e += 1024) {   // kp <= 512: 32-bit indices
+    const int i = e / kp, j = e - i * kp;
     const double v = H[e] * H[e];
     tot += v;
     if (i != j) off += v;
