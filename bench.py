@@ -353,7 +353,25 @@ def other_workload(args) -> int:
             cases = [workloads.config3("768x3072")]
         groups, flops = muon_groups(cases)
         nmat = sum(c.x.shape[0] for c in cases)
-        if args.sequential:
+        if args.param_list:
+            # the same matrices as a parameter list (every other non-square
+            # member as its transpose), grouped inside the library
+            c0 = cases[0]
+            if any((c.k, c.steps, c.oversample, c.power_iters, c.gamma) != (c0.k, c0.steps, c0.oversample,
+                                                                          c0.power_iters, c0.gamma) or
+                   not np.array_equal(c.coeffs, c0.coeffs) for c in cases):
+                raise SystemExit("--param-list needs one k, filter and option set across the groups")
+            xs = []
+            for g in groups:
+                for b_ in range(g["x"].shape[0]):
+                    mat = g["x"][b_]
+                    xs.append(mat.t().contiguous() if (b_ % 2 and mat.shape[0] != mat.shape[1]) else mat)
+            outs = [torch.empty_like(x_) for x_ in xs]
+
+            def step():
+                sd.msign_params(xs, c0.k, c0.steps, c0.coeffs, outs=outs, oversample=c0.oversample,
+                                power_iters=c0.power_iters, gamma=c0.gamma)
+        elif args.sequential:
             def step():
                 for g in groups:
                     sd.msign(g["x"], g["k"], g["steps"], g["coeffs"], oversample=g["oversample"],
@@ -384,7 +402,8 @@ def other_workload(args) -> int:
                "mfma_frac": flops / (ms / 1e3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, "steps": args.steps,
                "warmup": args.warmup, "dtype": "bf16", "data": "synthetic",
                "config": {"workload": args.workload, "groups": desc,
-                          "launch": "one call per group" if args.sequential else "sd_msign_groups",
+                          "launch": ("sd_msign_params (parameter list)" if args.param_list else
+                                     "one call per group" if args.sequential else "sd_msign_groups"),
                           "k": [c.k for c in cases], "filter_steps": [c.steps for c in cases]},
                "roofline": roof}
     elif args.workload == "peaks":
@@ -576,6 +595,8 @@ def main() -> int:
                     help="c4 / c5 / admm: the filter: 10 cubic steps, or 7 steps of the degree-5 map "
                          "(the shape of the paper's T = 7 fp16 composite)")
     ap.add_argument("--admm-k", type=int, default=250, help="admm: width K of the tracked basis")
+    ap.add_argument("--param-list", action="store_true",
+                    help="c2-step / paper-step: the matrices as a parameter list through sd_msign_params")
     ap.add_argument("--sequential", action="store_true",
                     help="c2-step / paper-step: one call per group on one stream instead of sd_msign_groups")
     args = ap.parse_args()

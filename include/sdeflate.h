@@ -156,8 +156,9 @@ typedef struct {
 } sd_msign_group;
 
 /* The deflated polar factors of a whole Muon step: a parameter list grouped
- * by shape, one batched call per group (App. D, "Grouping"; the grouping
- * itself, wide vs tall and equal shapes, is the caller's). Every group is
+ * by shape, one batched call per group (App. D, "Grouping"; here the
+ * grouping itself, wide vs tall and equal shapes, is the caller's:
+ * sd_msign_params below does it in the library). Every group is
  * validated first: on an argument error nothing is enqueued and the error of
  * the first bad group is returned. The groups then run concurrently on
  * library-owned streams (default priority, at most three per device) that
@@ -167,6 +168,34 @@ typedef struct {
  * from the pool on the group's stream unless its opts bring a workspace.
  * The output buffers of different groups must not overlap. */
 int sd_msign_groups(int ngroups, const sd_msign_group* groups, hipStream_t stream);
+
+/* One matrix of a Muon step's parameter list: in and out are m x n row-major
+ * of the call's dtype, device memory; out may equal in (updated in place)
+ * but may not otherwise overlap any other parameter's in or out. */
+typedef struct sd_msign_param {
+  const void* in;
+  void* out;
+  int m, n;
+} sd_msign_param;
+
+/* The deflated polar factors of a parameter list with the grouping done by
+ * the library (App. D, "Grouping"): parameters are bucketed by shape with
+ * wide ones transposed (polar(M^T) = polar(M)^T), so an m x n and an n x m
+ * matrix share the group of s x l, s = min(m, n), l = max(m, n); groups are
+ * formed in order of first appearance in the list, and a group's batch holds
+ * its members in list order (member b is matrix b of that batch: its sketch
+ * is Philox matrix b of the call). Each group is gathered into one s x l batch
+ * (tall members transposed), runs as one batched sd_msign_deflated_ex call
+ * with k, steps, coeffs, dtype and opts, and is scattered back (transposed
+ * back where it was gathered transposed); groups run concurrently as in
+ * sd_msign_groups, joined back into `stream`. Every parameter's result is
+ * bit for bit the one of that batched call. All parameters are validated
+ * first (SD_ERR_INVALID_ARG: count < 1, a null pointer, m or n < 1,
+ * k >= min(m, n), or invalid opts; nothing is enqueued then). Staging
+ * buffers (two per group, batch x s x l elements) and each group's scratch
+ * come from the pool on the group's stream; opts->workspace must be NULL. */
+int sd_msign_params(int count, const sd_msign_param* params, int k, int steps, const float* coeffs, int dtype,
+                    const sd_msign_opts* opts, hipStream_t stream);
 
 /* Workspace an _ex call with these arguments needs (0 on invalid arguments). */
 size_t sd_msign_workspace_bytes(int batch, int m, int n, int k, int dtype, const sd_msign_opts* opts);

@@ -93,6 +93,15 @@ class PsdOpts(ctypes.Structure):
 _LIB = None
 
 
+class MsignParam(ctypes.Structure):
+    _fields_ = [
+        ("input", ctypes.c_void_p),
+        ("out", ctypes.c_void_p),
+        ("m", ctypes.c_int),
+        ("n", ctypes.c_int),
+    ]
+
+
 def _declare(lib):
     vp, i, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
     sig = {
@@ -104,6 +113,7 @@ def _declare(lib):
         "sd_msign_workspace_bytes": (sz, [i, i, i, i, i, ctypes.POINTER(MsignOpts)]),
         "sd_msign_deflated_noalloc": (i, [i, i, i, i, i, vp, i, vp, vp, ctypes.POINTER(MsignOpts), vp]),
         "sd_msign_groups": (i, [i, ctypes.POINTER(MsignGroup), vp]),
+        "sd_msign_params": (i, [i, ctypes.POINTER(MsignParam), i, i, vp, i, ctypes.POINTER(MsignOpts), vp]),
         "sd_msign_opts_default": (None, [ctypes.POINTER(MsignOpts)]),
         "sd_psd_project": (i, [i, i, vp, vp, vp]),
         "sd_psd_project_deflated": (i, [i, i, i, vp, vp, vp, vp]),
@@ -283,6 +293,40 @@ def msign_groups(groups, *, stream=None):
         outs.append(out)
     _check(lib().sd_msign_groups(n, arr, _stream(stream)), "sd_msign_groups")
     del keep
+    return outs
+
+
+def msign_params(xs, k: int = 0, steps: int = 5, coeffs=None, *, outs=None, stream=None, **opts):
+    """One Muon step over a parameter list (sd_msign_params): xs is a list of
+    2-D CUDA tensors (all bfloat16 or all float32, contiguous), grouped by
+    shape inside the library (m x n and n x m together); outs (optional) the
+    output tensors, one per input (an output may be its own input). Options as
+    in msign (oversample, power_iters, gamma, tau, seed, window, restore).
+    Returns the outputs."""
+    import torch
+    if not xs:
+        raise ValueError("empty parameter list")
+    dt = xs[0].dtype
+    if dt == torch.bfloat16:
+        dtype = SD_DTYPE_BF16
+    elif dt == torch.float32:
+        dtype = SD_DTYPE_F32
+    else:
+        raise TypeError("parameters must be bfloat16 or float32")
+    outs = [torch.empty_like(x) for x in xs] if outs is None else list(outs)
+    arr = (MsignParam * len(xs))()
+    for i, (x, y) in enumerate(zip(xs, outs)):
+        if x.dim() != 2 or not x.is_cuda or not x.is_contiguous() or x.dtype != dt:
+            raise ValueError("every parameter must be a contiguous 2-D CUDA tensor of one dtype")
+        if y.shape != x.shape or y.dtype != dt or not y.is_contiguous():
+            raise ValueError("every output must match its parameter's shape and dtype")
+        arr[i] = MsignParam(x.data_ptr(), y.data_ptr(), x.shape[0], x.shape[1])
+    table, tptr = _host_table(coeffs, steps, 3)
+    o = msign_opts(**{key: v for key, v in opts.items() if key != "restore"})
+    o.restore = SD_RESTORE[opts.get("restore", "padded")]
+    _check(lib().sd_msign_params(len(xs), arr, k, steps, tptr, dtype, ctypes.byref(o), _stream(stream)),
+           "sd_msign_params")
+    del table
     return outs
 
 

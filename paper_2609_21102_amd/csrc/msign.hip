@@ -578,6 +578,82 @@ static int group_streams(GroupStreams*& gs) {
   gs = &d;
   return SD_OK;
 }
+// one host thread at a time enqueues on the shared group streams and events
+static std::mutex group_enqueue_mu;
+
+// ------------------------------------------- parameter-list grouping -----
+// Gather (staging is the destination, s x l row-major per member) or scatter
+// (staging is the source) for up to PL_MAX members per launch; a member whose
+// own layout is l x s (tall) is transposed through a 32 x 32 LDS tile so
+// that both its reads and its writes are coalesced. Grid: (cdiv(s, 32) *
+// cdiv(l, 32), members); 256 threads.
+constexpr int PL_MAX = 32;
+struct ParamTable {
+  const void* src[PL_MAX];
+  void* dst[PL_MAX];
+  int transpose[PL_MAX];
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void param_copy_kernel(ParamTable t, int s, int l, int gather) {
+  __shared__ T tile[32][33];
+  const int b = blockIdx.y;
+  const int tl = (l + 31) / 32;
+  const int i0 = (blockIdx.x / tl) * 32, j0 = (blockIdx.x % tl) * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;
+  const T* src = reinterpret_cast<const T*>(t.src[b]);
+  T* dst = reinterpret_cast<T*>(t.dst[b]);
+  if (!t.transpose[b]) {   // both sides s x l
+    for (int r = ty; r < 32; r += 8) {
+      const int i = i0 + r, j = j0 + tx;
+      if (i < s && j < l) dst[(long long)i * l + j] = src[(long long)i * l + j];
+    }
+    return;
+  }
+  if (gather) {   // src l x s: staging[i][j] = src[j][i]
+    for (int r = ty; r < 32; r += 8) {
+      const int j = j0 + r, i = i0 + tx;
+      tile[r][tx] = (j < l && i < s) ? src[(long long)j * s + i] : T{};
+    }
+    __syncthreads();
+    for (int r = ty; r < 32; r += 8) {
+      const int i = i0 + r, j = j0 + tx;
+      if (i < s && j < l) dst[(long long)i * l + j] = tile[tx][r];
+    }
+  } else {        // dst l x s: dst[j][i] = staging[i][j]
+    for (int r = ty; r < 32; r += 8) {
+      const int i = i0 + r, j = j0 + tx;
+      tile[r][tx] = (i < s && j < l) ? src[(long long)i * l + j] : T{};
+    }
+    __syncthreads();
+    for (int r = ty; r < 32; r += 8) {
+      const int j = j0 + r, i = i0 + tx;
+      if (j < l && i < s) dst[(long long)j * s + i] = tile[tx][r];
+    }
+  }
+}
+
+// Gather or scatter one group's members (param indices `idx`) against the
+// staging batch `stg` (s x l per member, esz bytes per element).
+static void param_copy(const sd_msign_param* params, const std::vector<int>& idx, char* stg, int s, int l,
+                       size_t esz, bool gather, hipStream_t st) {
+  const size_t per = (size_t)s * l * esz;
+  const dim3 blk(256);
+  for (size_t c0 = 0; c0 < idx.size(); c0 += PL_MAX) {
+    ParamTable t{};
+    const int nb = (int)std::min<size_t>(PL_MAX, idx.size() - c0);
+    for (int u = 0; u < nb; ++u) {
+      const sd_msign_param& q = params[idx[c0 + u]];
+      char* mine = stg + (c0 + u) * per;
+      t.src[u] = gather ? q.in : mine;
+      t.dst[u] = gather ? static_cast<void*>(mine) : q.out;
+      t.transpose[u] = q.m > q.n;
+    }
+    const dim3 grid((unsigned)(cdiv(s, 32) * cdiv(l, 32)), (unsigned)nb);
+    if (esz == 2) hipLaunchKernelGGL(param_copy_kernel<uint16_t>, grid, blk, 0, st, t, s, l, gather ? 1 : 0);
+    else hipLaunchKernelGGL(param_copy_kernel<float>, grid, blk, 0, st, t, s, l, gather ? 1 : 0);
+  }
+}
 }  // namespace sd
 
 extern "C" {
@@ -599,9 +675,7 @@ int sd_msign_groups(int ngroups, const sd_msign_group* groups, hipStream_t strea
   GroupStreams* gs = nullptr;
   int rc = group_streams(gs);
   if (rc != SD_OK) return rc;
-  // one host thread at a time enqueues on the shared streams and events
-  static std::mutex enqueue_mu;
-  std::lock_guard<std::mutex> lock(enqueue_mu);
+  std::lock_guard<std::mutex> lock(group_enqueue_mu);
   const int used = ngroups < GroupStreams::N ? ngroups : GroupStreams::N;
   if (hipEventRecord(gs->fork, stream) != hipSuccess) return SD_ERR_HIP;
   for (int i = 0; i < used; ++i)
@@ -616,6 +690,66 @@ int sd_msign_groups(int ngroups, const sd_msign_group* groups, hipStream_t strea
     if (hipEventRecord(gs->join[i], gs->s[i]) != hipSuccess || hipStreamWaitEvent(stream, gs->join[i], 0) != hipSuccess)
       return SD_ERR_HIP;
   }
+  return rc;
+}
+
+int sd_msign_params(int count, const sd_msign_param* params, int k, int steps, const float* coeffs, int dtype,
+                    const sd_msign_opts* opts, hipStream_t stream) {
+  if (count < 1 || !params) return SD_ERR_INVALID_ARG;
+  sd_msign_opts o;
+  sd_msign_opts_default(&o);
+  if (opts) o = *opts;
+  if (o.workspace) return SD_ERR_INVALID_ARG;
+  // buckets by (s, l) in order of first appearance, members in list order
+  std::vector<std::pair<int, int>> keys;
+  std::vector<std::vector<int>> members;
+  for (int i = 0; i < count; ++i) {
+    const sd_msign_param& q = params[i];
+    if (!q.in || !q.out || q.m < 1 || q.n < 1) return SD_ERR_INVALID_ARG;
+    const std::pair<int, int> key(std::min(q.m, q.n), std::max(q.m, q.n));
+    size_t g = 0;
+    while (g < keys.size() && keys[g] != key) ++g;
+    if (g == keys.size()) {
+      keys.push_back(key);
+      members.emplace_back();
+    }
+    members[g].push_back(i);
+  }
+  const char probe[16] __attribute__((aligned(16))) = {0};
+  for (size_t g = 0; g < keys.size(); ++g) {
+    const int rc = validate_msign((int)members[g].size(), keys[g].first, keys[g].second, k, steps, dtype, probe,
+                                  probe, o);
+    if (rc != SD_OK) return rc;
+  }
+  const size_t esz = dtype == SD_DTYPE_BF16 ? 2 : 4;
+  GroupStreams* gs = nullptr;
+  int rc = group_streams(gs);
+  if (rc != SD_OK) return rc;
+  std::lock_guard<std::mutex> lock(group_enqueue_mu);
+  const int used = (int)std::min<size_t>(keys.size(), GroupStreams::N);
+  if (hipEventRecord(gs->fork, stream) != hipSuccess) return SD_ERR_HIP;
+  for (int i = 0; i < used; ++i)
+    if (hipStreamWaitEvent(gs->s[i], gs->fork, 0) != hipSuccess) return SD_ERR_HIP;
+  for (size_t g = 0; g < keys.size() && rc == SD_OK; ++g) {
+    hipStream_t st = gs->s[g % GroupStreams::N];
+    const int s = keys[g].first, l = keys[g].second, b = (int)members[g].size();
+    const size_t bytes = (size_t)b * s * l * esz, half = (bytes + 255) / 256 * 256;
+    Scratch stg;
+    rc = stg.acquire(nullptr, 0, 2 * half, st);
+    if (rc != SD_OK) break;
+    char* in = reinterpret_cast<char*>(stg.ptr);
+    char* out = in + half;
+    param_copy(params, members[g], in, s, l, esz, true, st);
+    rc = msign_enqueue(b, s, l, k, steps, coeffs, dtype, in, out, o, st);
+    if (rc == SD_OK) param_copy(params, members[g], out, s, l, esz, false, st);
+    stg.release();
+  }
+  // join every used stream back, also after a failure, so `stream` never runs ahead
+  for (int i = 0; i < used; ++i) {
+    if (hipEventRecord(gs->join[i], gs->s[i]) != hipSuccess || hipStreamWaitEvent(stream, gs->join[i], 0) != hipSuccess)
+      return SD_ERR_HIP;
+  }
+  if (rc == SD_OK) rc = hip_status();
   return rc;
 }
 

@@ -128,6 +128,22 @@ def test_msign_invalid_options_and_pointers(lib):
     assert lib.sd_msign_workspace_bytes(1, 8, 8, 2, 0, ctypes.byref(o)) > 0
 
 
+def test_params_invalid_arguments(lib):
+    P = sd.MsignParam
+    ok = P(FAKE.value, FAKE.value, 8, 20)
+    arr = (P * 2)(ok, P(FAKE.value, FAKE.value, 20, 8))
+    assert lib.sd_msign_params(0, arr, 2, 5, None, 0, None, None) == -1           # empty list
+    assert lib.sd_msign_params(1, None, 2, 5, None, 0, None, None) == -1          # no list
+    assert lib.sd_msign_params(2, arr, 8, 5, None, 0, None, None) == -1           # k >= min(m, n)
+    for bad in (P(None, FAKE.value, 8, 20), P(FAKE.value, None, 8, 20), P(FAKE.value, FAKE.value, 0, 20)):
+        a2 = (P * 2)(ok, bad)
+        assert lib.sd_msign_params(2, a2, 2, 5, None, 0, None, None) == -1
+    o = sd.msign_opts()
+    o.workspace = FAKE.value                                                       # the list takes no workspace
+    assert lib.sd_msign_params(2, arr, 2, 5, None, 0, ctypes.byref(o), None) == -1
+    assert lib.sd_msign_params(2, arr, 2, 5, None, 7, None, None) == -1           # dtype
+
+
 def test_groups_invalid_arguments(lib):
     ok = sd.MsignGroup(1, 8, 8, 2, 5, None, 0, FAKE.value, FAKE.value, None)
     bad = sd.MsignGroup(1, 8, 8, 8, 5, None, 0, FAKE.value, FAKE.value, None)   # k >= min(m, n)

@@ -409,6 +409,37 @@ def _group_args(case):
                 oversample=case.oversample, power_iters=case.power_iters, gamma=case.gamma)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_param_list_grouping_bitwise(dtype):
+    """sd_msign_params buckets a parameter list by shape with wide and tall
+    sharing a group (polar(M^T) = polar(M)^T): every output equals, bit for
+    bit, the batched call on its group stacked in list order with tall members
+    transposed; also in place (outputs on the inputs)."""
+    rng = np.random.default_rng([21102, 41, 0 if dtype == "bf16" else 1])
+    shapes = [(64, 200), (200, 64), (96, 96), (64, 200), (128, 300), (300, 128), (96, 96), (33, 70), (70, 33)]
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    xs = [torch.from_numpy(rng.standard_normal(sh).astype(np.float32)).to(tdt).cuda().contiguous() for sh in shapes]
+    say(f"param list {dtype}: {len(xs)} matrices")
+    outs = sd.msign_params(xs, 4, 5)
+    torch.cuda.synchronize()
+    groups = {}
+    for i, x in enumerate(xs):
+        groups.setdefault((min(x.shape), max(x.shape)), []).append(i)
+    assert list(groups) == [(64, 200), (96, 96), (128, 300), (33, 70)]
+    for key, idx in groups.items():
+        stack = torch.stack([xs[i] if xs[i].shape[0] <= xs[i].shape[1] else xs[i].t() for i in idx]).contiguous()
+        want = sd.msign(stack, 4, 5)
+        torch.cuda.synchronize()
+        for b, i in enumerate(idx):
+            w = want[b] if xs[i].shape[0] <= xs[i].shape[1] else want[b].t()
+            assert torch.equal(outs[i], w), (key, i)
+    copies = [x.clone() for x in xs]
+    sd.msign_params(copies, 4, 5, outs=copies)
+    torch.cuda.synchronize()
+    for a, b in zip(copies, outs):
+        assert torch.equal(a, b)
+
+
 def test_groups_match_single_calls_bitwise():
     """sd_msign_groups runs the groups concurrently on the library's streams;
     each group's result must be the single call's, bit for bit."""
