@@ -33,6 +33,7 @@ from __future__ import annotations
 import argparse
 import hashlib
 import json
+import math
 import os
 import sys
 import time
@@ -487,13 +488,14 @@ def other_workload(args) -> int:
                             "flops_per_launch": fl}}
     elif args.workload == "admm":
         # ADMM on a max-cut relaxation of the size of the paper's n = 5000
-        # instances (planted-bisection random graph), tracked basis of the
-        # paper's width K = ceil(0.05 n) = 250 with window r = ceil(0.025 n) =
-        # 125 (--admm-k: another width, r = K / 2), tau = 0.1; one step = 10
-        # iterations with the gate open, continuing the state.
-        n, chunk = 5000, 10
-        k = args.admm_k
-        r = max(1, (k + 1) // 2)
+        # instances (--admm-n: another size; planted-bisection random graph),
+        # tracked basis of the paper's width K = ceil(0.05 n) with window
+        # r = ceil(0.025 n) (--admm-k: another width, r = ceil(K / 2)),
+        # tau = 0.1; one step = 10 iterations with the gate open, continuing
+        # the state.
+        n, chunk = args.admm_n, 10
+        k = args.admm_k if args.admm_k else math.ceil(0.05 * n)
+        r = math.ceil(0.025 * n) if not args.admm_k else max(1, (k + 1) // 2)
         steps, table, degree = _filter_table(args)
         case = workloads.planted_maxcut(n, case_id=0)
         C = torch.from_numpy(case.c).to(dev)
@@ -594,7 +596,8 @@ def main() -> int:
     ap.add_argument("--poly", default="cubic", choices=["cubic", "quintic7"],
                     help="c4 / c5 / admm: the filter: 10 cubic steps, or 7 steps of the degree-5 map "
                          "(the shape of the paper's T = 7 fp16 composite)")
-    ap.add_argument("--admm-k", type=int, default=250, help="admm: width K of the tracked basis")
+    ap.add_argument("--admm-n", type=int, default=5000, help="admm: order n of the SDP")
+    ap.add_argument("--admm-k", type=int, default=0, help="admm: width K of the tracked basis (default ceil(0.05 n))")
     ap.add_argument("--param-list", action="store_true",
                     help="c2-step / paper-step: the matrices as a parameter list through sd_msign_params")
     ap.add_argument("--sequential", action="store_true",

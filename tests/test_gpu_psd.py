@@ -476,7 +476,7 @@ def test_admm_split_calls_equal_one_call_bitwise():
 # oracle, counts exact, Ritz values to 1e-5, the next basis to 1e-4, output
 # exactly symmetric. With every Ritz pair deflated (tau = 0) the outputs do
 # not depend on the eigenvector choice inside clusters of Ritz values.
-@pytest.mark.parametrize("n,k", [(260, 65), (300, 100), (600, 200), (800, 352)])
+@pytest.mark.parametrize("n,k", [(260, 65), (300, 100), (600, 200), (800, 352), (700, 512)])
 def test_wide_basis(n, k):
     case = workloads.small_psd(n, k=k, case_id=n + 31)
     say(f"psd wide n={n} k={k}")
