@@ -244,7 +244,13 @@ int sd_sketch_host(int batch, int s, int rp, uint64_t seed, float* out);
  *     (eq:baseline_projection);
  *   - Qwarm <- CholeskyQR(Zt) (the basis for the next call).
  * Everything is float32 (MFMA fp32), small factorizations float64.
- * Requirements: n >= 1, 0 <= k < n, k <= 64, 0 <= steps <= 1000; Qwarm is
+ * Tracked bases up to 64 columns keep their K x K problems in one
+ * work-group's LDS; wider ones (up to 512, the paper's K = ceil(0.05 n) at
+ * its SDP sizes) take float64 panel products, a one-work-group Cholesky
+ * with a block-row solve, a block Jacobi Rayleigh-Ritz and float32 MFMA
+ * GEMMs for the rank-K terms, and compute the next basis on a
+ * library-owned side stream (default priority) joined back into `stream`.
+ * Requirements: n >= 1, 0 <= k < n, k <= 512, 0 <= steps <= 1000; Qwarm is
  * required when k > 0 and must not overlap X or out. k = 0 is the baseline
  * (Qwarm unused, may be NULL).
  */
@@ -318,7 +324,7 @@ size_t sd_psd_workspace_bytes(int n, int k, const sd_psd_opts* opts);
  * enqueued: SD_ERR_INVALID_ARG for n < 1, iters < 0, warmup < 0, sigma <= 0,
  * steps outside 0..1000,
  * a null C, b, X, S or y, k < 0 or k >= n, k > 0 without Qwarm, a basis
- * overlapping C or S, or invalid opts; SD_ERR_UNSUPPORTED for k > 64.
+ * overlapping C or S, or invalid opts; SD_ERR_UNSUPPORTED for k > 512.
  * iters = 0 validates and returns SD_OK. */
 int sd_admm_diag(int n, int iters, int steps, float sigma, const float* C, const float* b, float* X, float* S,
                  float* y, int k, float* Qwarm, int warmup, const sd_psd_opts* opts, float* eta_out, int* ndef_out,
