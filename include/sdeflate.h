@@ -193,7 +193,9 @@ typedef struct sd_msign_param {
  * first (SD_ERR_INVALID_ARG: count < 1, a null pointer, m or n < 1,
  * k >= min(m, n), or invalid opts; nothing is enqueued then). Staging
  * buffers (two per group, batch x s x l elements) and each group's scratch
- * come from the pool on the group's stream; opts->workspace must be NULL. */
+ * come from the pool on the group's stream; opts->workspace must be NULL.
+ * A pool allocation that fails (SD_ERR_HIP) stops the enqueueing there: the
+ * groups enqueued before it still run and are joined into `stream`. */
 int sd_msign_params(int count, const sd_msign_param* params, int k, int steps, const float* coeffs, int dtype,
                     const sd_msign_opts* opts, hipStream_t stream);
 

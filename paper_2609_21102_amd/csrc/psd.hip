@@ -820,7 +820,10 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     if (hipEventRecord(ss->fork, st) != hipSuccess || hipStreamWaitEvent(ss->s, ss->fork, 0) != hipSuccess)
       return SD_ERR_HIP;
     cholqr_wide(p, p.zt, p.qn, o.status_dev, p.wpart2, p.g64b, ss->s);
-    if (hipEventRecord(ss->join, ss->s) != hipSuccess) return SD_ERR_HIP;
+    if (hipEventRecord(ss->join, ss->s) != hipSuccess) {
+      (void)hipStreamSynchronize(ss->s);   // no join point: the caller may free the workspace on return
+      return SD_ERR_HIP;
+    }
     ritz_wide(p, p.vt, p.zt, o, st);
     rankk_wide(p, p.coefR, 1.f, z, nullptr, p.r, nullptr, st);
     if (p.frob) hipLaunchKernelGGL(tile_sumsq_kernel, dim3((np / 128) * (np / 128)), dim3(256), 0, st, p.r, np, p.sumsq);
@@ -1047,7 +1050,10 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   else
     hipLaunchKernelGGL((psd_out_kernel<64>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
   if (ss) {   // wide basis: join the side stream, write the next basis
-    if (hipStreamWaitEvent(st, ss->join, 0) != hipSuccess) return SD_ERR_HIP;
+    if (hipStreamWaitEvent(st, ss->join, 0) != hipSuccess) {
+      (void)hipStreamSynchronize(ss->s);
+      return SD_ERR_HIP;
+    }
     hipLaunchKernelGGL(panel_to_rows_kernel, grid1((long long)n * K, 256), dim3(256), 0, st, p.qn, np, K, n, Qwarm);
   }
   return hip_status();
