@@ -409,8 +409,9 @@ def _group_args(case):
                 oversample=case.oversample, power_iters=case.power_iters, gamma=case.gamma)
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_param_list_grouping_bitwise(dtype):
+@pytest.mark.parametrize("dtype,k,restore", [("bf16", 4, "padded"), ("f32", 4, "padded"), ("f32", 0, "padded"),
+                                             ("bf16", 3, "explicit")])
+def test_param_list_grouping_bitwise(dtype, k, restore):
     """sd_msign_params buckets a parameter list by shape with wide and tall
     sharing a group (polar(M^T) = polar(M)^T): every output equals, bit for
     bit, the batched call on its group stacked in list order with tall members
@@ -419,8 +420,8 @@ def test_param_list_grouping_bitwise(dtype):
     shapes = [(64, 200), (200, 64), (96, 96), (64, 200), (128, 300), (300, 128), (96, 96), (33, 70), (70, 33)]
     tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
     xs = [torch.from_numpy(rng.standard_normal(sh).astype(np.float32)).to(tdt).cuda().contiguous() for sh in shapes]
-    say(f"param list {dtype}: {len(xs)} matrices")
-    outs = sd.msign_params(xs, 4, 5)
+    say(f"param list {dtype} k={k} {restore}: {len(xs)} matrices")
+    outs = sd.msign_params(xs, k, 5, restore=restore)
     torch.cuda.synchronize()
     groups = {}
     for i, x in enumerate(xs):
@@ -428,13 +429,13 @@ def test_param_list_grouping_bitwise(dtype):
     assert list(groups) == [(64, 200), (96, 96), (128, 300), (33, 70)]
     for key, idx in groups.items():
         stack = torch.stack([xs[i] if xs[i].shape[0] <= xs[i].shape[1] else xs[i].t() for i in idx]).contiguous()
-        want = sd.msign(stack, 4, 5)
+        want = sd.msign(stack, k, 5, restore=restore)
         torch.cuda.synchronize()
         for b, i in enumerate(idx):
             w = want[b] if xs[i].shape[0] <= xs[i].shape[1] else want[b].t()
             assert torch.equal(outs[i], w), (key, i)
     copies = [x.clone() for x in xs]
-    sd.msign_params(copies, 4, 5, outs=copies)
+    sd.msign_params(copies, k, 5, outs=copies, restore=restore)
     torch.cuda.synchronize()
     for a, b in zip(copies, outs):
         assert torch.equal(a, b)
