@@ -59,7 +59,10 @@ enum {
   SD_FLAG_RESIDUAL_FLOOR = 4 /* Muon: a residual at the float32 rounding level of the head
                                 was dropped (nu <= 2^-20 ||X||_F: the input has rank
                                 <= k_eff, outside Alg. 1's k < rank(M)); X0 is then
-                                gamma^-1 U_k V_k^T (0 with the explicit restore) */
+                                gamma^-1 U_k V_k^T (0 with the explicit restore) */,
+  SD_FLAG_EIG_UNCONVERGED = 8 /* PSD, tracked bases wider than 64: the block Jacobi
+                                Rayleigh-Ritz reached its cap of 16 sweeps with the
+                                off-diagonal mass above 2^-40 of the norm */
 };
 
 /* ------------------------------------------------------------------ Muon --

@@ -743,7 +743,7 @@ static void ritz_wide(const PsdPlan& p, const float* vt, const float* zt, const 
                          odd ? p.eb1 : p.eb0, odd ? p.eb0 : p.eb1, kp, nb, t, BJ_INNER_ROUNDS, p.bst);
     }
     hipLaunchKernelGGL(bj_check_kernel, dim3(1), dim3(1024), 0, st, p.hb0, p.hb1, kp, rps, sweep, BJ_MAX_SWEEPS,
-                       BJ_TOL_EXP, p.bst);
+                       BJ_TOL_EXP, p.bst, o.status_dev);
   }
   hipLaunchKernelGGL(ritz_wide_kernel, dim3(1), dim3(1024), 0, st, p.hb0, p.hb1, p.eb0, p.eb1, rps, p.bst, p.K, kp,
                      o.tau, o.window, o.gamma, p.e64, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out,

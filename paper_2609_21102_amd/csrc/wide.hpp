@@ -517,11 +517,12 @@ __global__ __launch_bounds__(128) void bj_round_kernel(const double* __restrict_
 
 // After sweep `sweep` (rounds_per_sweep rounds each): done when the
 // off-diagonal mass is at most 2^(2 tol_exp) of the total, or at the sweep
-// cap. Round g reads buffer g % 2 and writes (g + 1) % 2, so after G rounds
-// the current matrices are buffer G % 2. One work-group.
+// cap (then flag 8 in status: not converged). Round g reads buffer g % 2 and
+// writes (g + 1) % 2, so after G rounds the current matrices are buffer
+// G % 2. One work-group.
 __global__ __launch_bounds__(1024) void bj_check_kernel(const double* __restrict__ H0, const double* __restrict__ H1,
                                                         int kp, int rounds_per_sweep, int sweep, int max_sweeps,
-                                                        int tol_exp, BjState* st) {
+                                                        int tol_exp, BjState* st, int* status) {
   __shared__ double red[1024 / WAVE];
   if (st->done) return;
   const long long g = (long long)(sweep + 1) * rounds_per_sweep;
@@ -535,9 +536,11 @@ __global__ __launch_bounds__(1024) void bj_check_kernel(const double* __restrict
   }
   off = block_sum(off, red);
   tot = block_sum(tot, red);
-  if (threadIdx.x == 0 && (off <= __builtin_amdgcn_ldexp(tot, 2 * tol_exp) || sweep + 1 >= max_sweeps)) {
+  const bool conv = off <= __builtin_amdgcn_ldexp(tot, 2 * tol_exp);
+  if (threadIdx.x == 0 && (conv || sweep + 1 >= max_sweeps)) {
     st->done = 1;
     st->sweeps = sweep + 1;
+    if (!conv && status) atomicOr(status, 8);
   }
 }
 
