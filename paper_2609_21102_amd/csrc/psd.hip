@@ -705,13 +705,15 @@ static void cholqr_wide(const PsdPlan& p, const float* src, float* dst, int* sta
                        p.czero, ib, p.q64, dst);
 }
 
-// Zt = V^T Z^T = (Z V)^T on the float32 MFMA GEMM (Z symmetric: its rows).
+// Zt = V^T Z^T = (Z V)^T on the float32 MFMA GEMM (Z symmetric: its rows),
+// on 64 x 64 tiles: with only kr / 128 tile rows, 128 x 128 tiles would leave
+// most CUs idle (K = 250, n = 5000: 80 work-groups; 366 -> 193 us).
 static void zv_wide(const PsdPlan& p, const float* z, const float* vt, float* zt, hipStream_t st) {
   ProfScope ps(SD_STAGE_SKETCH, st);
   const int np = p.n_pad;
   GemmShape g{p.kr, np, np, np, np, 0, 0, 1};
   EpiStore es{zt, 0, np};
-  launch_gemm<CfgTile128, float, false, false>(vt, z, g, es, st);
+  launch_gemm<GemmCfg<2, 2, 1, 1>, float, false, false>(vt, z, g, es, st);
 }
 
 // out = alpha x + U^T diag(mult c) U over the deflated rows (float32 MFMA,

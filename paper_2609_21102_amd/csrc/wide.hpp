@@ -3,7 +3,7 @@
 // Sec. 3.3). The K x K problems no longer fit one work-group's LDS, so this
 // path splits them:
 //   * float64 products of panel rows (the CholeskyQR Gram Z^T Z and the
-//     Rayleigh quotient V^T Z V) over position chunks, reduced in chunk order;
+//     Rayleigh quotient V^T Z V) over 128-position chunks, reduced in chunk order;
 //   * CholeskyQR's factor on one work-group, the K x K matrix in global
 //     memory (L2-resident), panels of 16 columns in LDS and registers; the
 //     panel Q^T = L^-1 Z^T by block rows of 16 over all positions;
@@ -24,7 +24,7 @@
 namespace sd {
 
 constexpr int WIDE_MAX = 512;     // widest tracked basis of this path
-constexpr int WG_CHUNK = 512;     // positions per partial of the float64 products
+constexpr int WG_CHUNK = 128;     // positions per partial of the float64 products (more chunks: more work-groups)
 constexpr int BJ_B = 8;           // block Jacobi: indices per block
 constexpr int BJ_P = 2 * BJ_B;    // indices per pair problem
 
