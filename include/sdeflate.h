@@ -60,7 +60,7 @@ enum {
                                 was dropped (nu <= 2^-20 ||X||_F: the input has rank
                                 <= k_eff, outside Alg. 1's k < rank(M)); X0 is then
                                 gamma^-1 U_k V_k^T (0 with the explicit restore) */,
-  SD_FLAG_EIG_UNCONVERGED = 8 /* PSD, tracked bases wider than 64: the block Jacobi
+  SD_FLAG_EIG_UNCONVERGED = 8 /* PSD, tracked bases wider than 32: the block Jacobi
                                 Rayleigh-Ritz reached its cap of 16 sweeps with the
                                 off-diagonal mass above 2^-40 of the norm */
 };
@@ -249,7 +249,7 @@ int sd_sketch_host(int batch, int s, int rp, uint64_t seed, float* out);
  *     (eq:baseline_projection);
  *   - Qwarm <- CholeskyQR(Zt) (the basis for the next call).
  * Everything is float32 (MFMA fp32), small factorizations float64.
- * Tracked bases up to 64 columns keep their K x K problems in one
+ * Tracked bases up to 32 columns keep their K x K problems in one
  * work-group's LDS; wider ones (up to 512, the paper's K = ceil(0.05 n) at
  * its SDP sizes) take float64 panel products, a one-work-group Cholesky
  * with a block-row solve, a block Jacobi Rayleigh-Ritz and float32 MFMA

@@ -16,6 +16,7 @@
 namespace sd {
 
 constexpr int LZ_MAX = 64;   // largest Lanczos step count
+constexpr int PSD_NARROW_MAX = 32;   // widest tracked basis whose K x K problems stay in one work-group
 
 // y[i] = sum_j A[i][j] x[j]; one wave per row, four rows per work-group.
 __global__ __launch_bounds__(256) void gemv_kernel(const float* __restrict__ A, int ld, int n_pad,
@@ -515,7 +516,7 @@ struct PsdPlan {
   float* sumsq;    // [tiles] sums of R^2 per 128 x 128 tile (Frobenius scale)
   LanczosState* lst;
   double* lpart;   // Lanczos step partial sums: two blocks of LZ_MAX rows
-  // wide tracked bases (K > SM_MAX): K x K problems in global memory
+  // wide tracked bases (K > PSD_NARROW_MAX): K x K problems in global memory
   bool wk;
   int kp, kr;      // K rounded up to 32 (small matrices), to 128 (panel rows)
   double *wpart, *g64, *hb0, *hb1, *eb0, *eb1, *e64, *lw, *dinv, *q64;
@@ -619,7 +620,11 @@ static void make_psd_plan(PsdPlan& p, int n, int k, int steps, const float* X, c
   p.f16 = o.precision == SD_PREC_F16;
   p.wide = p.f16 && p.n_pad % 256 == 0 && p.n_pad >= 4096;
   p.frob = o.scale_mode == SD_SCALE_FROBENIUS;
-  p.wk = k > SM_MAX;
+  // bases wider than 32 take the wide path: at K = 64 it measured 7.49
+  // against 7.73 ms per ADMM iteration (n = 5000, fp16) for the four-wave
+  // one-work-group Jacobi; at K = 32 the one-wave Jacobi is faster (6.61
+  // against 6.92 ms)
+  p.wk = k > PSD_NARROW_MAX;
   p.kp = round_up(k > 0 ? k : 1, 32);
   p.kr = round_up(k > 0 ? k : 1, 128);
   const bool aligned = X && (reinterpret_cast<uintptr_t>(X) % 16 == 0);
@@ -848,13 +853,11 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   hipLaunchKernelGGL(ritz_kernel<NPV>, dim3(1), dim3(SM_THREADS), 0, st, p.part, np / GP_CHUNK, K, o.tau, o.window, \
                      o.gamma, p.E, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out, o.n_deflated_out,          \
                      o.n_positive_out)
-      switch (jacobi_class(K)) {
+      switch (jacobi_class(K)) {   // K <= PSD_NARROW_MAX: one wave
         case 4: SD_RITZ(4); break;
         case 8: SD_RITZ(8); break;
         case 12: SD_RITZ(12); break;
-        case 16: SD_RITZ(16); break;
-        case 32: SD_RITZ(32); break;
-        default: SD_RITZ(0); break;
+        default: SD_RITZ(16); break;
       }
 #undef SD_RITZ
     }
@@ -1047,10 +1050,8 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   const int* kk = (K > 0 && !p.wk) ? p.ndef : nullptr;
   if (K <= 16 || p.wk)
     hipLaunchKernelGGL((psd_out_kernel<16>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
-  else if (K <= 32)
+  else   // narrow: K <= PSD_NARROW_MAX = 32
     hipLaunchKernelGGL((psd_out_kernel<32>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
-  else
-    hipLaunchKernelGGL((psd_out_kernel<64>), dim3(tiles), dim3(256), 0, st, p.r, p.c, np, ut, np, p.coefP, kk, n, np, out);
   if (ss) {   // wide basis: join the side stream, write the next basis
     if (hipStreamWaitEvent(st, ss->join, 0) != hipSuccess) {
       (void)hipStreamSynchronize(ss->s);
