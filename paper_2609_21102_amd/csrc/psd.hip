@@ -525,6 +525,7 @@ struct PsdPlan {
   float* us;       // scaled copy of U for the rank-K GEMMs
   float* qn;       // the next basis, CholQR(Z V), panel rows
   BjState* bst;
+  double* bjpart;  // block Jacobi: (off-diagonal, total) sums of squares per H block of a sweep's last round
 };
 
 static void plan_psd(PsdPlan& p, Arena& ar) {
@@ -566,6 +567,8 @@ static void plan_psd(PsdPlan& p, Arena& ar) {
     p.q64 = ar.take<double>((size_t)p.kp * p.n_pad);
     p.czero = ar.take<int>(1);
     p.bst = ar.take<BjState>(1);
+    const size_t pairs = (size_t)p.kp / BJ_B / 2;
+    p.bjpart = ar.take<double>(2 * pairs * pairs);
   }
   p.coefR = ar.take<float>(kq);
   p.coefX = ar.take<float>(kq);
@@ -746,12 +749,14 @@ static void ritz_wide(const PsdPlan& p, const float* vt, const float* zt, const 
     for (int t = 0; t < rps; ++t) {
       const long long g = (long long)sweep * rps + t;
       const bool odd = g & 1;
+      const int flags = (t == rps - 1 ? BJ_WRITE_PART : 0) | (t == 0 && sweep > 0 ? BJ_TEST_PART : 0);
       hipLaunchKernelGGL(bj_round_kernel, grid, dim3(128), 0, st, odd ? p.hb1 : p.hb0, odd ? p.hb0 : p.hb1,
-                         odd ? p.eb1 : p.eb0, odd ? p.eb0 : p.eb1, kp, nb, t, BJ_INNER_ROUNDS, p.bst);
+                         odd ? p.eb1 : p.eb0, odd ? p.eb0 : p.eb1, kp, nb, t, BJ_INNER_ROUNDS, sweep, flags,
+                         BJ_TOL_EXP, p.bjpart, p.bst);
     }
-    hipLaunchKernelGGL(bj_check_kernel, dim3(1), dim3(1024), 0, st, p.hb0, p.hb1, kp, rps, sweep, BJ_MAX_SWEEPS,
-                       BJ_TOL_EXP, p.bst, o.status_dev);
   }
+  hipLaunchKernelGGL(bj_final_kernel, dim3(1), dim3(128), 0, st, p.bjpart, P * P, BJ_MAX_SWEEPS, BJ_TOL_EXP, p.bst,
+                     o.status_dev);
   hipLaunchKernelGGL(ritz_wide_kernel, dim3(1), dim3(1024), 0, st, p.hb0, p.hb1, p.eb0, p.eb1, rps, p.bst, p.K, kp,
                      o.tau, o.window, o.gamma, p.e64, p.lam, p.ndef, p.coefR, p.coefX, p.coefP, o.ritz_out,
                      o.n_deflated_out, o.n_positive_out);

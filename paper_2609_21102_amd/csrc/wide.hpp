@@ -10,8 +10,9 @@
 //   * a block Jacobi eigensolver over 8-index blocks: every round pairs the
 //     blocks by the circle method and rotates each 16 x 16 pair problem with
 //     one sweep of the one-wave Jacobi (the same rotations a scalar cyclic
-//     Jacobi would apply in a block ordering), one launch per round, a
-//     convergence check after every sweep;
+//     Jacobi would apply in a block ordering), one launch per round; the
+//     last round of a sweep leaves per-block sums of squares that the next
+//     sweep's first round tests for convergence;
 //   * the rotation V E as a float64-accumulated product; the
 //     rank-K terms of the residual, the padded start and the restore as
 //     float32 MFMA GEMMs with an axpy epilogue (gemm.hpp).
@@ -434,46 +435,117 @@ __global__ __launch_bounds__(256) void bj_init_kernel(const double* __restrict__
   E0[e] = i == j ? 1.0 : 0.0;
 }
 
-// One wave: the BJ_P x BJ_P problem of blocks (pa, pb) into s.h, then
-// `rounds` rounds of the one-wave Jacobi (0: until converged); s.e is the
-// accumulated rotation J.
-__device__ __forceinline__ void bj_solve(const double* __restrict__ H, int kp, int pa, int pb, PairLds& s,
-                                         int rounds) {
+// Entries of the BJ_P x BJ_P pair problem held per lane (one wave) and of a
+// BJ_P x BJ_P block held per thread (128 threads).
+constexpr int BJ_PE = BJ_P * BJ_P / WAVE;
+constexpr int BJ_BE = BJ_P * BJ_P / 128;
+static_assert(BJ_PE * WAVE == BJ_P * BJ_P && BJ_BE * 128 == BJ_P * BJ_P, "pair blocks split evenly");
+
+// Lane's entries of the problem of blocks (pa, pb): entry e = lane + WAVE i
+// is (l, q) = (e / BJ_P, e % BJ_P).
+__device__ __forceinline__ void bj_load_pair(const double* __restrict__ H, int kp, int pa, int pb,
+                                             double (&v)[BJ_PE]) {
   const int lane = threadIdx.x & (WAVE - 1);
-  for (int e = lane; e < BJ_P * BJ_P; e += WAVE) {
-    const int l = e / BJ_P, q = e - l * BJ_P;
-    s.h[l][q] = H[(long long)bj_index(l, pa, pb) * kp + bj_index(q, pa, pb)];
+#pragma unroll
+  for (int i = 0; i < BJ_PE; ++i) {
+    const int e = lane + WAVE * i, l = e / BJ_P, q = e - l * BJ_P;
+    v[i] = H[(long long)bj_index(l, pa, pb) * kp + bj_index(q, pa, pb)];
+  }
+}
+
+// One wave: the pair problem (from bj_load_pair) into s.h, then `rounds`
+// rounds of the one-wave Jacobi (0: until converged); s.e is the accumulated
+// rotation J.
+__device__ __forceinline__ void bj_solve(const double (&v)[BJ_PE], PairLds& s, int rounds) {
+  const int lane = threadIdx.x & (WAVE - 1);
+#pragma unroll
+  for (int i = 0; i < BJ_PE; ++i) {
+    const int e = lane + WAVE * i, l = e / BJ_P, q = e - l * BJ_P;
+    s.h[l][q] = v[i];
   }
   wave_sync();
   jacobi_eig_wave<BJ_B>(s, BJ_P, -48, rounds);
 }
+
+// Convergence of the block Jacobi after a sweep, from the per-block sums of
+// squares (off-diagonal, total) that the sweep's last round wrote, summed in
+// one fixed order by a 128-thread work-group (every caller gets the same
+// decision): done when the off-diagonal mass is at most 2^(2 tol_exp) of the
+// total.
+__device__ __forceinline__ bool bj_converged(const double* __restrict__ part, int nparts, int tol_exp,
+                                             double* red) {
+  double off = 0.0, tot = 0.0;
+  for (int i = threadIdx.x; i < nparts; i += 128) {
+    off += part[2 * i];
+    tot += part[2 * i + 1];
+  }
+  off = block_sum(off, red);
+  tot = block_sum(tot, red);
+  return off <= __builtin_amdgcn_ldexp(tot, 2 * tol_exp);
+}
+
+// Round flags: BJ_WRITE_PART on the last round of a sweep (every H-block
+// work-group writes the sums of squares of its output block to part);
+// BJ_TEST_PART on the first round of sweep `sweep` > 0 (every work-group first
+// tests the previous sweep's sums and all return when it converged;
+// work-group 0 records it in the state, so later launches return at once).
+constexpr int BJ_WRITE_PART = 1, BJ_TEST_PART = 2;
 
 // One round: P = nb / 2 pairs. Work-groups 0 .. P^2 - 1 write the H block of
 // pairs (a, b), Hout[a][b] = J_a^T Hin[a][b] J_b (wave 0 solves pair a, wave 1
 // pair b); the next P * (kp / BJ_P) update BJ_P rows of E on pair a's
 // columns, Eout = Ein J_a. Every work-group that needs J_a computes it from the
 // same entries in the same order, so all copies agree. Reads Hin/Ein, writes
-// Hout/Eout (the caller alternates the buffers). 128 threads.
+// Hout/Eout (the caller alternates the buffers). Every global load of a round
+// (the state flag, the pair problem, the block to rotate) is issued before
+// the first wait, so a round costs one memory round trip before its solve
+// instead of three. 128 threads.
 __global__ __launch_bounds__(128) void bj_round_kernel(const double* __restrict__ Hin, double* __restrict__ Hout,
                                                        const double* __restrict__ Ein, double* __restrict__ Eout,
-                                                       int kp, int nb, int t, int rounds, const BjState* st) {
+                                                       int kp, int nb, int t, int rounds, int sweep, int flags,
+                                                       int tol_exp, double* __restrict__ part, BjState* st) {
   __shared__ PairLds sa, sb;
-  if (st->done) return;
+  __shared__ double red[128 / WAVE];
+  __shared__ int sdone;
   const int P = nb / 2, nh = P * P;
   const int tid = threadIdx.x, wave = tid / WAVE;
   const int bid = blockIdx.x;
+  double pv[BJ_PE], bv[BJ_BE];
+  // the state flag reaches every wave through LDS: work-group 0 of a testing
+  // round may set it while this work-group runs, and all waves of a
+  // work-group must take the same branch
+  const auto is_done = [&]() {
+    if (tid == 0) sdone = st->done;
+    __syncthreads();
+    if (sdone) return true;
+    if (!(flags & BJ_TEST_PART) || !bj_converged(part, nh, tol_exp, red)) return false;
+    if (bid == 0 && tid == 0) {
+      st->done = 1;
+      st->sweeps = sweep;
+    }
+    return true;
+  };
   if (bid < nh) {
     const int a = bid / P, b = bid - a * P;
     int pa, qa, pb, qb;
     bj_pair(t, a, nb, pa, qa);
     bj_pair(t, b, nb, pb, qb);
-    if (wave == 0) bj_solve(Hin, kp, pa, qa, sa, rounds);
-    else if (a != b) bj_solve(Hin, kp, pb, qb, sb, rounds);
+    if (wave == 0) bj_load_pair(Hin, kp, pa, qa, pv);
+    else bj_load_pair(Hin, kp, pb, qb, pv);
+#pragma unroll
+    for (int i = 0; i < BJ_BE; ++i) {
+      const int e = tid + 128 * i, l = e / BJ_P, q = e - l * BJ_P;
+      bv[i] = Hin[(long long)bj_index(l, pa, qa) * kp + bj_index(q, pb, qb)];
+    }
+    if (is_done()) return;
+    if (wave == 0) bj_solve(pv, sa, rounds);
+    else if (a != b) bj_solve(pv, sb, rounds);
     __syncthreads();
     const PairLds& jb = a == b ? sa : sb;
-    for (int e = tid; e < BJ_P * BJ_P; e += 128) {
-      const int l = e / BJ_P, q = e - l * BJ_P;
-      sa.h[l][q] = Hin[(long long)bj_index(l, pa, qa) * kp + bj_index(q, pb, qb)];
+#pragma unroll
+    for (int i = 0; i < BJ_BE; ++i) {
+      const int e = tid + 128 * i, l = e / BJ_P, q = e - l * BJ_P;
+      sa.h[l][q] = bv[i];
     }
     __syncthreads();
     for (int e = tid; e < BJ_P * BJ_P; e += 128) {   // T = H_ab J_b
@@ -484,12 +556,24 @@ __global__ __launch_bounds__(128) void bj_round_kernel(const double* __restrict_
       sa.h2[l][m] = v;
     }
     __syncthreads();
+    double off = 0.0, tot = 0.0;
     for (int e = tid; e < BJ_P * BJ_P; e += 128) {   // J_a^T T
       const int l = e / BJ_P, m = e - l * BJ_P;
       double v = 0.0;
 #pragma unroll 8
       for (int q = 0; q < BJ_P; ++q) v = fma(sa.e[q][l], sa.h2[q][m], v);
-      Hout[(long long)bj_index(l, pa, qa) * kp + bj_index(m, pb, qb)] = v;
+      const int gi = bj_index(l, pa, qa), gj = bj_index(m, pb, qb);
+      Hout[(long long)gi * kp + gj] = v;
+      tot = fma(v, v, tot);
+      off = gi != gj ? fma(v, v, off) : off;
+    }
+    if (flags & BJ_WRITE_PART) {
+      off = block_sum(off, red);
+      tot = block_sum(tot, red);
+      if (tid == 0) {
+        part[2 * bid] = off;
+        part[2 * bid + 1] = tot;
+      }
     }
     return;
   }
@@ -497,49 +581,48 @@ __global__ __launch_bounds__(128) void bj_round_kernel(const double* __restrict_
   const int a = idx % P, r0 = (idx / P) * BJ_P;
   int pa, qa;
   bj_pair(t, a, nb, pa, qa);
-  if (wave == 0) bj_solve(Hin, kp, pa, qa, sa, rounds);
+  if (wave == 0) bj_load_pair(Hin, kp, pa, qa, pv);
+  // rows r0 .. r0 + BJ_P - 1 of E on the pair's columns (r0 + BJ_P <= kp)
+#pragma unroll
+  for (int i = 0; i < BJ_BE; ++i) {
+    const int e = tid + 128 * i, rr = e / BJ_P, q = e - rr * BJ_P;
+    bv[i] = Ein[(long long)(r0 + rr) * kp + bj_index(q, pa, qa)];
+  }
+  if (is_done()) return;
+  if (wave == 0) bj_solve(pv, sa, rounds);
   __syncthreads();
-  // rows r0 .. r0 + BJ_P - 1 of E on the pair's columns, staged in sa.h
-  for (int e = tid; e < BJ_P * BJ_P; e += 128) {
-    const int rr = e / BJ_P, q = e - rr * BJ_P, r = r0 + rr;
-    sa.h[rr][q] = r < kp ? Ein[(long long)r * kp + bj_index(q, pa, qa)] : 0.0;
+  // the E rows staged in sa.h (free once the solve is done)
+#pragma unroll
+  for (int i = 0; i < BJ_BE; ++i) {
+    const int e = tid + 128 * i, rr = e / BJ_P, q = e - rr * BJ_P;
+    sa.h[rr][q] = bv[i];
   }
   __syncthreads();
   for (int e = tid; e < BJ_P * BJ_P; e += 128) {
-    const int rr = e / BJ_P, m = e - rr * BJ_P, r = r0 + rr;
-    if (r >= kp) continue;
+    const int rr = e / BJ_P, m = e - rr * BJ_P;
     double v = 0.0;
 #pragma unroll 8
     for (int q = 0; q < BJ_P; ++q) v = fma(sa.h[rr][q], sa.e[q][m], v);
-    Eout[(long long)r * kp + bj_index(m, pa, qa)] = v;
+    Eout[(long long)(r0 + rr) * kp + bj_index(m, pa, qa)] = v;
   }
 }
 
-// After sweep `sweep` (rounds_per_sweep rounds each): done when the
-// off-diagonal mass is at most 2^(2 tol_exp) of the total, or at the sweep
-// cap (then flag 8 in status: not converged). Round g reads buffer g % 2 and
-// writes (g + 1) % 2, so after G rounds the current matrices are buffer
-// G % 2. One work-group.
-__global__ __launch_bounds__(1024) void bj_check_kernel(const double* __restrict__ H0, const double* __restrict__ H1,
-                                                        int kp, int rounds_per_sweep, int sweep, int max_sweeps,
-                                                        int tol_exp, BjState* st, int* status) {
-  __shared__ double red[1024 / WAVE];
-  if (st->done) return;
-  const long long g = (long long)(sweep + 1) * rounds_per_sweep;
-  const double* H = (g & 1) ? H1 : H0;
-  double off = 0.0, tot = 0.0;
-  for (int e = threadIdx.x; e < kp * kp; e += 1024) {   // kp <= 512: 32-bit indices
-    const int i = e / kp, j = e - i * kp;
-    const double v = H[e] * H[e];
-    tot += v;
-    if (i != j) off += v;
-  }
-  off = block_sum(off, red);
-  tot = block_sum(tot, red);
-  const bool conv = off <= __builtin_amdgcn_ldexp(tot, 2 * tol_exp);
-  if (threadIdx.x == 0 && (conv || sweep + 1 >= max_sweeps)) {
+// After the last sweep's launches: when no round recorded convergence, test
+// the last sweep's sums (flag 8 in status when they have not converged: the
+// sweep cap was reached) and record max_sweeps. Round g reads buffer g % 2
+// and writes (g + 1) % 2, so after G rounds the current matrices are buffer
+// G % 2. One work-group of 128 threads.
+__global__ __launch_bounds__(128) void bj_final_kernel(const double* __restrict__ part, int nparts, int max_sweeps,
+                                                       int tol_exp, BjState* st, int* status) {
+  __shared__ double red[128 / WAVE];
+  __shared__ int sdone;
+  if (threadIdx.x == 0) sdone = st->done;
+  __syncthreads();
+  if (sdone) return;
+  const bool conv = bj_converged(part, nparts, tol_exp, red);
+  if (threadIdx.x == 0) {
     st->done = 1;
-    st->sweeps = sweep + 1;
+    st->sweeps = max_sweeps;
     if (!conv && status) atomicOr(status, 8);
   }
 }
