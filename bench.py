@@ -580,7 +580,8 @@ def other_workload(args) -> int:
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed calls (default: 50 for the Muon workloads, 20 for the PSD and ADMM ones)")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -603,6 +604,8 @@ def main() -> int:
     ap.add_argument("--sequential", action="store_true",
                     help="c2-step / paper-step: one call per group on one stream instead of sd_msign_groups")
     args = ap.parse_args()
+    if args.steps is None:
+        args.steps = 50 if args.workload in ("headline", "c1", "c2-step", "c3", "paper-step") else 20
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         log("bench.py: the library runs on a single GPU; --gpus must be 1 "
             "(sharding the batch by matrix across GPUs is not implemented)")
