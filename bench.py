@@ -73,8 +73,11 @@ def update_bytes_algorithmic(s: int, l: int) -> float:
 def stage_work(s: int, l: int, k: int, rp: int, power_iters: int, steps: int) -> dict:
     """Algorithmic work per matrix of one call, by stage: (flops, bytes)."""
     return {
-        "ns_gram": (steps * s * (s + 1.0) * l, 0.0),
-        "ns_poly": (steps * s * (s + 1.0) * s, 0.0),
+        # the chain's HBM bytes per step: X read by the Gram and the update and
+        # written by the update (bf16), A written by the Gram and read by the
+        # polynomial (fp32, the b A term), B written and read (bf16)
+        "ns_gram": (steps * s * (s + 1.0) * l, steps * (2.0 * s * l + 4.0 * s * s)),
+        "ns_poly": (steps * s * (s + 1.0) * s, steps * (4.0 * s * s + 2.0 * s * s)),
         "ns_update": (steps * 2.0 * s * s * l, steps * update_bytes_algorithmic(s, l)),
         # each pass over X reads it once (bf16); 2 s l r' flops
         "sketch": ((2 + 2 * power_iters) * 2.0 * s * l * rp, (2 + 2 * power_iters) * 2.0 * s * l),
