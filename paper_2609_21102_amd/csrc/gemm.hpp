@@ -23,6 +23,8 @@
 // and writes each value at (r, c) and (c, r); diagonal tiles write c >= r.
 #pragma once
 
+#include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "common.hpp"
@@ -47,6 +49,13 @@ struct GemmShape {
   // work-groups that share a B column panel run together on one XCD, so the
   // panel comes from HBM once and from L2 after that.
   int m_fast = 0;
+  // Tail split (register-staged kernel): space for partial accumulators that
+  // the caller may give (part_cap floats); launch_gemm then cuts the tiles of
+  // a last, mostly idle round of work-groups along K (tiles tail0 .. end, in
+  // `pieces` pieces each) and sums the pieces in a second launch.
+  float* part = nullptr;
+  long long part_cap = 0;
+  int tail0 = 0, pieces = 0;
 };
 
 enum { EMIT_FULL = 0, EMIT_SYM_OFF = 1, EMIT_SYM_DIAG = 2 };
@@ -741,7 +750,14 @@ __device__ __forceinline__ void sym_tile(int t, int nt, int& tm, int& tn) {
 // (fp32 sources feed bf16 MFMAs through rounding in the staging step).
 // A_KN: A is stored K x M (M contiguous) and transposed while staging, as B
 // is in NN form.
-template <typename Cfg, typename T, typename SA, typename SB, bool A_KN, bool B_NN, bool SYM, typename Epi>
+// Tail split (sh.pieces > 1): work-groups from sh.tail0 on each compute one
+// K piece of a tile of the last round and store the accumulators to sh.part
+// (piece u of tile t at unit (t - tail0) pieces + u, in the MFMA fragment
+// layout, element-major so that lanes store consecutive floats); FIXUP
+// launches one work-group per such tile, sums its pieces in piece order and
+// runs the epilogue.
+template <typename Cfg, typename T, typename SA, typename SB, bool A_KN, bool B_NN, bool SYM, typename Epi,
+          bool FIXUP = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void gemm_kernel(const SA* __restrict__ A, const SB* __restrict__ B,
                                                        GemmShape sh, Epi epi) {
   constexpr int BK = GemmK<T>::BK;
@@ -751,7 +767,18 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_
   __shared__ __attribute__((aligned(16))) char lds[Cfg::STAGES * STAGE];
   const int tiles_m = sh.M / BM, tiles_n = sh.N / BN;
   const int per = SYM ? tiles_m * (tiles_m + 1) / 2 : tiles_m * tiles_n;
-  const int lid = xcd_remap(blockIdx.x, per * sh.batch);
+  int lid, piece = 0;
+  bool tail = false;
+  if constexpr (FIXUP) {
+    lid = sh.tail0 + (int)blockIdx.x;
+  } else if (sh.pieces > 1 && (int)blockIdx.x >= sh.tail0) {
+    const int u = (int)blockIdx.x - sh.tail0;
+    lid = sh.tail0 + u / sh.pieces;
+    piece = u - (u / sh.pieces) * sh.pieces;
+    tail = true;
+  } else {
+    lid = xcd_remap(blockIdx.x, sh.pieces > 1 ? sh.tail0 : per * sh.batch);
+  }
   const int b = lid / per;
   int t = lid - b * per, tm, tn;
   if (SYM) {
@@ -780,54 +807,82 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_
   constexpr bool PRE = Epi::PRE;
   float px[PRE ? WM * WN * 16 : 1];
   if constexpr (PRE) {
+    if (!tail) {
 #pragma unroll
-    for (int mi = 0; mi < WM; ++mi)
+      for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
-      for (int ni = 0; ni < WN; ++ni)
+        for (int ni = 0; ni < WN; ++ni)
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < 4; ++i)
 #pragma unroll
-          for (int j = 0; j < 4; ++j)
-            px[(mi * WN + ni) * 16 + 4 * i + j] =
-                epi.pre(b, m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h + j, n0 + wn * WN * 32 + ni * 32 + r32);
+            for (int j = 0; j < 4; ++j)
+              px[(mi * WN + ni) * 16 + 4 * i + j] =
+                  epi.pre(b, m0 + wm * WM * 32 + mi * 32 + 8 * i + 4 * h + j, n0 + wn * WN * 32 + ni * 32 + r32);
+    }
   }
 
-  using AStager = typename std::conditional<A_KN, NNStager<BM, NT, T, SA>, RowStager<BM, NT, T, SA>>::type;
-  using BStager = typename std::conditional<B_NN, NNStager<BN, NT, T, SB>, RowStager<BN, NT, T, SB>>::type;
-  AStager sa;
-  BStager sb;
-  auto load_tiles = [&](int k0) {
-    if constexpr (A_KN) sa.load(Ab, sh.lda, k0, m0);
-    else sa.load(Ab, sh.lda, m0, k0);
-    if constexpr (B_NN) sb.load(Bb, sh.ldb, k0, n0);
-    else sb.load(Bb, sh.ldb, n0, k0);
-  };
-  const int nk = sh.K / BK;
-  load_tiles(0);
-  if constexpr (Cfg::STAGES == 2) {
-    sa.store(lds);
-    sb.store(lds + TA);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-      const int cur = kt & 1;
-      const bool more = kt + 1 < nk;
-      if (more) load_tiles((kt + 1) * BK);
-      tile_mma<T, WM, WN>(lds + cur * STAGE, lds + cur * STAGE + TA, acc, wm, wn, lane);
-      if (more) {
-        char* nxt = lds + (cur ^ 1) * STAGE;
-        sa.store(nxt);
-        sb.store(nxt + TA);
-      }
-      __syncthreads();
+  // the fragment layout of the partial accumulators
+  constexpr int TILE = BM * BN;
+  auto part_at = [&](int mi, int ni, int e) { return ((mi * WN + ni) * 16 + e) * NT + (int)threadIdx.x; };
+  if constexpr (FIXUP) {
+    const float* src = sh.part + (long long)(lid - sh.tail0) * sh.pieces * TILE;
+    for (int pc = 0; pc < sh.pieces; ++pc) {
+#pragma unroll
+      for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[mi][ni][e] += src[(long long)pc * TILE + part_at(mi, ni, e)];
     }
   } else {
-    for (int kt = 0; kt < nk; ++kt) {
+    using AStager = typename std::conditional<A_KN, NNStager<BM, NT, T, SA>, RowStager<BM, NT, T, SA>>::type;
+    using BStager = typename std::conditional<B_NN, NNStager<BN, NT, T, SB>, RowStager<BN, NT, T, SB>>::type;
+    AStager sa;
+    BStager sb;
+    auto load_tiles = [&](int k0) {
+      if constexpr (A_KN) sa.load(Ab, sh.lda, k0, m0);
+      else sa.load(Ab, sh.lda, m0, k0);
+      if constexpr (B_NN) sb.load(Bb, sh.ldb, k0, n0);
+      else sb.load(Bb, sh.ldb, n0, k0);
+    };
+    const int nk = sh.K / BK;
+    const int kb = tail ? piece * nk / sh.pieces : 0, ke = tail ? (piece + 1) * nk / sh.pieces : nk;
+    load_tiles(kb * BK);
+    if constexpr (Cfg::STAGES == 2) {
       sa.store(lds);
       sb.store(lds + TA);
       __syncthreads();
-      if (kt + 1 < nk) load_tiles((kt + 1) * BK);
-      tile_mma<T, WM, WN>(lds, lds + TA, acc, wm, wn, lane);
-      __syncthreads();
+      for (int kt = kb; kt < ke; ++kt) {
+        const int cur = (kt - kb) & 1;
+        const bool more = kt + 1 < ke;
+        if (more) load_tiles((kt + 1) * BK);
+        tile_mma<T, WM, WN>(lds + cur * STAGE, lds + cur * STAGE + TA, acc, wm, wn, lane);
+        if (more) {
+          char* nxt = lds + (cur ^ 1) * STAGE;
+          sa.store(nxt);
+          sb.store(nxt + TA);
+        }
+        __syncthreads();
+      }
+    } else {
+      for (int kt = kb; kt < ke; ++kt) {
+        sa.store(lds);
+        sb.store(lds + TA);
+        __syncthreads();
+        if (kt + 1 < ke) load_tiles((kt + 1) * BK);
+        tile_mma<T, WM, WN>(lds, lds + TA, acc, wm, wn, lane);
+        __syncthreads();
+      }
+    }
+    if (tail) {
+      float* dst = sh.part + (long long)((int)blockIdx.x - sh.tail0) * TILE;
+#pragma unroll
+      for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) dst[part_at(mi, ni, e)] = acc[mi][ni][e];
+      return;
     }
   }
 
@@ -1223,14 +1278,56 @@ void launch_gemm_dma(const T* A, const T* B, const GemmShape& sh, const Epi& epi
 
 // Host launcher (errors surface through hipGetLastError at the end of a call).
 // M, N must be multiples of the tile and K of the K step.
+// Work-groups of `kern` (nt threads) resident on the current device at once:
+// CUs x work-groups per CU, cached per device (0 when the runtime cannot tell).
+template <typename K>
+inline int gemm_slots(K kern, int nt, std::atomic<int> (&cache)[16]) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+  if (dev < 16) {
+    const int c = cache[dev].load(std::memory_order_relaxed);
+    if (c > 0) return c;
+  }
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, nt, 0) != hipSuccess) return 0;
+  const int slots = cus * per_cu;
+  if (dev < 16) cache[dev].store(slots, std::memory_order_relaxed);
+  return slots;
+}
+
 template <typename Cfg, typename T, bool B_NN, bool SYM, bool A_KN = false, typename SA, typename SB, typename Epi>
 void launch_gemm(const SA* A, const SB* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;
   const long long blocks = per * sh.batch;
   if (blocks <= 0) return;
-  hipLaunchKernelGGL((gemm_kernel<Cfg, T, SA, SB, A_KN, B_NN, SYM, Epi>), dim3((unsigned)blocks), dim3(Cfg::NT), 0,
-                     stream, A, B, sh, epi);
+  auto kern = gemm_kernel<Cfg, T, SA, SB, A_KN, B_NN, SYM, Epi>;
+  GemmShape s2 = sh;
+  s2.tail0 = 0;
+  s2.pieces = 0;
+  if (sh.part) {
+    // a last round of at most half the resident work-groups: cut its tiles
+    // along K into up to 16 pieces that fill one round
+    static std::atomic<int> slots_cache[16];
+    const int slots = gemm_slots(kern, Cfg::NT, slots_cache);
+    const long long rem = slots > 0 ? blocks % slots : 0;
+    const int nk = sh.K / GemmK<T>::BK;
+    if (slots > 0 && blocks >= slots && rem > 0 && 2 * rem <= slots) {
+      const long long pieces = std::min<long long>(
+          {slots / rem, 16ll, (long long)nk, sh.part_cap / (rem * Cfg::BM * Cfg::BN)});
+      if (pieces >= 2) {
+        s2.tail0 = (int)(blocks - rem);
+        s2.pieces = (int)pieces;
+        hipLaunchKernelGGL(kern, dim3((unsigned)(blocks - rem + rem * pieces)), dim3(Cfg::NT), 0, stream, A, B, s2,
+                           epi);
+        hipLaunchKernelGGL((gemm_kernel<Cfg, T, SA, SB, A_KN, B_NN, SYM, Epi, true>), dim3((unsigned)rem),
+                           dim3(Cfg::NT), 0, stream, A, B, s2, epi);
+        return;
+      }
+    }
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A, B, s2, epi);
 }
 
 }  // namespace sd

@@ -526,10 +526,15 @@ struct PsdPlan {
   float* qn;       // the next basis, CholQR(Z V), panel rows
   BjState* bst;
   double* bjpart;  // block Jacobi: (off-diagonal, total) sums of squares per H block of a sweep's last round
+  float* split;    // fp32 filter products: partial accumulators of a last round cut along K
+  long long split_cap;
 };
 
 static void plan_psd(PsdPlan& p, Arena& ar) {
   const size_t nn = (size_t)p.n_pad * p.n_pad;
+  // fp32 products: room for 512 partial 128 x 128 tiles (32 MB)
+  p.split_cap = p.f16 ? 0 : 512ll * 128 * 128;
+  p.split = p.split_cap ? ar.take<float>((size_t)p.split_cap) : nullptr;
   p.zp = p.copy_in ? ar.take<float>(nn) : nullptr;
   p.r = ar.take<float>(nn);
   p.xa = ar.take<float>(nn);
@@ -988,7 +993,9 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
       hn = th;
     }
   }
-  auto sym_gemm = [&](const float* A, const float* B, const GemmShape& g, const auto& epi) {
+  auto sym_gemm = [&](const float* A, const float* B, GemmShape g, const auto& epi) {
+    g.part = p.split;   // a mostly idle last round is cut along K
+    g.part_cap = p.split_cap;
     launch_gemm<CfgTile128, float, false, true>(A, B, g, epi, st);
   };
   for (int t = 0; t < (p.f16 ? 0 : p.steps); ++t) {
@@ -1043,6 +1050,8 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
     launch_gemm_dma<CfgDma128, false, false>(p.rh, p.steps % 2 ? p.xh1 : p.xh0, g, es, st);
   } else {
     EpiStore es{p.c, nn, np};
+    g.part = p.split;
+    g.part_cap = p.split_cap;
     launch_gemm<CfgTile128, float, false, false>(p.r, cur, g, es, st);
   }
   const int tiles = (np / 64) * (np / 64);
