@@ -821,18 +821,33 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_
     }
   }
 
-  // the fragment layout of the partial accumulators
+  // the fragment layout of the partial accumulators: 16-byte groups of four
+  // accumulators, consecutive threads at consecutive groups
   constexpr int TILE = BM * BN;
-  auto part_at = [&](int mi, int ni, int e) { return ((mi * WN + ni) * 16 + e) * NT + (int)threadIdx.x; };
+  auto part_at = [&](int mi, int ni, int q) { return (((mi * WN + ni) * 4 + q) * NT + (int)threadIdx.x) * 4; };
   if constexpr (FIXUP) {
     const float* src = sh.part + (long long)(lid - sh.tail0) * sh.pieces * TILE;
     for (int pc = 0; pc < sh.pieces; ++pc) {
+      f32x4_t v[WM][WN][4];
 #pragma unroll
       for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
         for (int ni = 0; ni < WN; ++ni)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) acc[mi][ni][e] += src[(long long)pc * TILE + part_at(mi, ni, e)];
+          for (int q = 0; q < 4; ++q)
+            v[mi][ni][q] = *reinterpret_cast<const f32x4_t*>(src + (long long)pc * TILE + part_at(mi, ni, q));
+      // every load of the piece is issued before the first sum (left to
+      // itself the scheduler interleaved loads, waits and sums, with two or
+      // three loads in flight)
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[mi][ni][4 * q + j] += v[mi][ni][q][j];
     }
   } else {
     using AStager = typename std::conditional<A_KN, NNStager<BM, NT, T, SA>, RowStager<BM, NT, T, SA>>::type;
@@ -881,7 +896,9 @@ __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_
 #pragma unroll
         for (int ni = 0; ni < WN; ++ni)
 #pragma unroll
-          for (int e = 0; e < 16; ++e) dst[part_at(mi, ni, e)] = acc[mi][ni][e];
+          for (int q = 0; q < 4; ++q)
+            *reinterpret_cast<f32x4_t*>(dst + part_at(mi, ni, q)) =
+                f32x4_t{acc[mi][ni][4 * q], acc[mi][ni][4 * q + 1], acc[mi][ni][4 * q + 2], acc[mi][ni][4 * q + 3]};
       return;
     }
   }
