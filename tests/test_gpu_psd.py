@@ -159,6 +159,27 @@ def test_config4_full():
     assert int(info["n_positive"]) == oinfo.n_positive
 
 
+@pytest.mark.slow
+def test_fp32_tail_split_full_tiling():
+    """n = 5000 (padded to 5120), fp32 products: the restore product's 1600
+    tiles leave a last round of 64 tiles for 512 resident work-groups, which
+    the library cuts along K and sums in a second launch; the symmetric
+    products (820 tiles) run whole. Two filter steps keep the oracle short.
+    Same contract as the other fp32 cases."""
+    case = workloads.small_psd(5000, k=16, steps=2, case_id=1)
+    say("psd n=5000 k=16 steps=2 (fp32, tail split of the restore product)")
+    out, info, q = gpu_psd(case)
+    want, vnext, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm.astype(np.float64),
+                                                   steps=case.steps, gamma=case.gamma,
+                                                   subspace_iters=case.subspace_iters)
+    err = rel_fro(host64(out), want)
+    say(f"  rel err {err:.3e}")
+    assert err < TOL
+    assert int(info["n_deflated"]) == oinfo.n_deflated
+    o = out.cpu().numpy()
+    assert np.array_equal(o, o.T)
+
+
 def test_config5_chain_scaled():
     """Config 5's call pattern at n = 1024 (same spectrum recipe, k = 32, one
     subspace step per call): 20 chained projections, each warm-started from
