@@ -1036,9 +1036,17 @@ struct DmaLds {
 
 // One output tile (linear tile id lid over the batch). T: the 16-bit operand
 // type (bf16 or fp16; the loads move bytes, only the MFMA differs).
-template <typename Cfg, typename T, bool B_NN, bool SYM, typename Epi>
+// SPLIT (epilogues in the MFMA layout only): DMA_PIECE computes K steps
+// kb .. ke - 1 and stores the accumulators to dst (the fragment layout of the
+// register-staged kernel's tail split); DMA_FIXUP sums the tile's `pieces`
+// partials at src in piece order and runs the epilogue.
+enum { DMA_WHOLE = 0, DMA_PIECE = 1, DMA_FIXUP = 2 };
+template <typename Cfg, typename T, bool B_NN, bool SYM, typename Epi, int SPLIT = DMA_WHOLE>
 __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* __restrict__ B,
-                                              const GemmShape& sh, const Epi& epi, char* lds, int lid) {
+                                              const GemmShape& sh, const Epi& epi, char* lds, int lid,
+                                              int kb = 0, int ke = 0, float* dst = nullptr,
+                                              const float* src = nullptr) {
+  static_assert(SPLIT == DMA_WHOLE || !Epi::ROWWISE, "K pieces need an epilogue in the MFMA layout");
   constexpr int BK = Cfg::BK, RB = 2 * BK, CH = BK / 8, RPL = 1024 / RB;   // rows per 1 KB load
   constexpr int BM = Cfg::BM, BN = Cfg::BN, WM = Cfg::WM, WN = Cfg::WN, S = Cfg::STAGES;
   constexpr int NW = Cfg::NWM * Cfg::NWN;
@@ -1078,7 +1086,7 @@ __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* 
   constexpr int RW_CH = BM * BN / 8 / Cfg::NT;     // row chunks per thread
   float px[PRE ? WM * WN * 16 : 1];
   u32x4_t rw_h[ROWWISE ? RW_CH : 1], rw_l[ROWWISE ? RW_CH : 1];
-  if constexpr (PRE) {
+  if constexpr (PRE && SPLIT != DMA_PIECE) {
 #pragma unroll
     for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
@@ -1144,13 +1152,45 @@ __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* 
 #pragma unroll
     for (int jj = 0; jj < WN; ++jj) acc[i][jj] = f32x16_t{};
 
-  const int nk = sh.K / BK;
+  // K steps k0 .. k0 + nk - 1 (all of them for a whole tile)
+  const int k0 = SPLIT == DMA_PIECE ? kb : 0;
+  const int nk = SPLIT == DMA_PIECE ? ke - kb : (SPLIT == DMA_FIXUP ? 0 : sh.K / BK);
+  if constexpr (SPLIT == DMA_FIXUP) {
+    // a piece's loads in groups of MH fragment rows (the accumulators and
+    // one group's values fit the registers), all of a group's loads before
+    // its sums
+    constexpr int TILE = BM * BN, MH = WM > 2 ? WM / 2 : WM;
+    for (int pc = 0; pc < sh.pieces; ++pc) {
+#pragma unroll
+      for (int m2 = 0; m2 < WM; m2 += MH) {
+        f32x4_t v[MH][WN][4];
+#pragma unroll
+        for (int mi = 0; mi < MH; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              v[mi][ni][q] = *reinterpret_cast<const f32x4_t*>(
+                  src + (long long)pc * TILE + ((((m2 + mi) * WN + ni) * 4 + q) * Cfg::NT + (int)threadIdx.x) * 4);
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int mi = 0; mi < MH; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+#pragma unroll
+              for (int j = 0; j < 4; ++j) acc[m2 + mi][ni][4 * q + j] += v[mi][ni][q][j];
+      }
+    }
+  }
 #pragma unroll
   for (int s0 = 0; s0 < S - 1; ++s0)
-    if (s0 < nk) issue(s0, s0);
-  for (int kt = 0; kt < nk; ++kt) {
-    // stage kt has landed once at most the later stages' loads are pending
-    const int later = nk - 1 - kt < S - 2 ? nk - 1 - kt : S - 2;
+    if (s0 < nk) issue(s0, k0 + s0);
+  for (int i = 0; i < nk; ++i) {
+    const int kt = k0 + i;
+    // stage i has landed once at most the later stages' loads are pending
+    const int later = nk - 1 - i < S - 2 ? nk - 1 - i : S - 2;
     if constexpr (S >= 5) {
       if (later >= 3) wait_vmcnt<LT * 3>();
       else if (later == 2) wait_vmcnt<LT * 2>();
@@ -1167,8 +1207,8 @@ __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* 
       wait_vmcnt<0>();
     }
     __builtin_amdgcn_s_barrier();
-    if (kt + S - 1 < nk) issue((kt + S - 1) % S, kt + S - 1);
-    const char* base = lds + (kt % S) * STAGE;
+    if (i + S - 1 < nk) issue((i + S - 1) % S, kt + S - 1);
+    const char* base = lds + (i % S) * STAGE;
     if constexpr (Epi::HI_FROM_B) {
       // rows [kt BK, kt BK + BK) of the B operand are rows of this tile's
       // output when they fall in [m0, m0 + BM): copy the epilogue's chunks
@@ -1185,6 +1225,17 @@ __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* 
       }
     }
     tile_mma_dma<T, WM, WN, BN, BK, B_NN>(base, base + A_BYTES, acc, wm, wn, lane);
+  }
+  if constexpr (SPLIT == DMA_PIECE) {
+#pragma unroll
+    for (int mi = 0; mi < WM; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          *reinterpret_cast<f32x4_t*>(dst + (((mi * WN + ni) * 4 + q) * Cfg::NT + (int)threadIdx.x) * 4) =
+              f32x4_t{acc[mi][ni][4 * q], acc[mi][ni][4 * q + 1], acc[mi][ni][4 * q + 2], acc[mi][ni][4 * q + 3]};
+    return;
   }
 
   if constexpr (ROWWISE) {
@@ -1273,28 +1324,32 @@ __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* 
 // tiles, so work-groups that share operand panels share an L2). A variant
 // that walked several tiles per work-group measured no faster and needed
 // about 20-100 more VGPRs.
-template <typename Cfg, bool B_NN, bool SYM, typename Epi, typename T>
+template <typename Cfg, bool B_NN, bool SYM, typename Epi, typename T, int SPLIT = DMA_WHOLE>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void
 gemm_dma_kernel(const T* __restrict__ A, const T* __restrict__ B, GemmShape sh, Epi epi) {
   __shared__ __attribute__((aligned(1024))) char lds[DmaLds<Cfg, Epi::ROWWISE>::BYTES];
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const int total = (SYM ? tm * (tm + 1) / 2 : tm * tn) * sh.batch;
-  gemm_dma_tile<Cfg, T, B_NN, SYM, Epi>(A, B, sh, epi, lds, xcd_remap(blockIdx.x, total));
+  constexpr long long TILE = (long long)Cfg::BM * Cfg::BN;
+  if constexpr (SPLIT == DMA_FIXUP) {
+    const int u = (int)blockIdx.x;   // tile tail0 + u
+    gemm_dma_tile<Cfg, T, B_NN, SYM, Epi, DMA_FIXUP>(A, B, sh, epi, lds, sh.tail0 + u, 0, 0, nullptr,
+                                                     sh.part + (long long)u * sh.pieces * TILE);
+  } else if constexpr (SPLIT == DMA_PIECE) {
+    // whole tiles 0 .. tail0 - 1, then the pieces of the tail tiles
+    if ((int)blockIdx.x < sh.tail0) {
+      gemm_dma_tile<Cfg, T, B_NN, SYM, Epi>(A, B, sh, epi, lds, xcd_remap(blockIdx.x, sh.tail0));
+      return;
+    }
+    const int u = (int)blockIdx.x - sh.tail0, tile = u / sh.pieces, piece = u - tile * sh.pieces;
+    const int nk = sh.K / Cfg::BK;
+    gemm_dma_tile<Cfg, T, B_NN, SYM, Epi, DMA_PIECE>(A, B, sh, epi, lds, sh.tail0 + tile, piece * nk / sh.pieces,
+                                                     (piece + 1) * nk / sh.pieces, sh.part + (long long)u * TILE);
+  } else {
+    gemm_dma_tile<Cfg, T, B_NN, SYM, Epi>(A, B, sh, epi, lds, xcd_remap(blockIdx.x, total));
+  }
 }
 
-template <typename Cfg, bool B_NN, bool SYM, typename Epi, typename T>
-void launch_gemm_dma(const T* A, const T* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
-  static_assert(sizeof(T) == 2, "16-bit operands");
-  const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
-  const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;
-  const long long blocks = per * sh.batch;
-  if (blocks <= 0) return;
-  hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi, T>), dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A,
-                     B, sh, epi);
-}
-
-// Host launcher (errors surface through hipGetLastError at the end of a call).
-// M, N must be multiples of the tile and K of the K step.
 // Work-groups of `kern` (nt threads) resident on the current device at once:
 // CUs x work-groups per CU, cached per device (0 when the runtime cannot tell).
 template <typename K>
@@ -1313,6 +1368,51 @@ inline int gemm_slots(K kern, int nt, std::atomic<int> (&cache)[16]) {
   return slots;
 }
 
+// Pieces for a last round of tiles: with `slots` work-groups resident at once
+// and a last round of rem = blocks % slots tiles that fills at most half of
+// them, up to 16 K pieces per tile that together fill one round (bounded by
+// the K steps and by the caller's space for partials); 0 when not worth it.
+inline int tail_pieces(long long blocks, int slots, int nk, long long part_cap, long long tile) {
+  if (slots <= 0 || blocks < slots) return 0;
+  const long long rem = blocks % slots;
+  if (rem == 0 || 2 * rem > slots) return 0;
+  const long long p = std::min<long long>({slots / rem, 16ll, (long long)nk, part_cap / (rem * tile)});
+  return p >= 2 ? (int)p : 0;
+}
+
+template <typename Cfg, bool B_NN, bool SYM, typename Epi, typename T>
+void launch_gemm_dma(const T* A, const T* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
+  static_assert(sizeof(T) == 2, "16-bit operands");
+  const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
+  const long long per = SYM ? (long long)tm * (tm + 1) / 2 : (long long)tm * tn;
+  const long long blocks = per * sh.batch;
+  if (blocks <= 0) return;
+  GemmShape s2 = sh;
+  s2.tail0 = 0;
+  s2.pieces = 0;
+  if constexpr (!Epi::ROWWISE) {
+    if (sh.part) {
+      static std::atomic<int> slots_cache[16];
+      const int slots = gemm_slots(gemm_dma_kernel<Cfg, B_NN, SYM, Epi, T>, Cfg::NT, slots_cache);
+      const int pieces = tail_pieces(blocks, slots, sh.K / Cfg::BK, sh.part_cap, (long long)Cfg::BM * Cfg::BN);
+      if (pieces) {
+        const long long rem = blocks % slots;
+        s2.tail0 = (int)(blocks - rem);
+        s2.pieces = pieces;
+        hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi, T, DMA_PIECE>),
+                           dim3((unsigned)(blocks - rem + rem * pieces)), dim3(Cfg::NT), 0, stream, A, B, s2, epi);
+        hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi, T, DMA_FIXUP>), dim3((unsigned)rem),
+                           dim3(Cfg::NT), 0, stream, A, B, s2, epi);
+        return;
+      }
+    }
+  }
+  hipLaunchKernelGGL((gemm_dma_kernel<Cfg, B_NN, SYM, Epi, T>), dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A,
+                     B, s2, epi);
+}
+
+// Host launcher (errors surface through hipGetLastError at the end of a call).
+// M, N must be multiples of the tile and K of the K step.
 template <typename Cfg, typename T, bool B_NN, bool SYM, bool A_KN = false, typename SA, typename SB, typename Epi>
 void launch_gemm(const SA* A, const SB* B, const GemmShape& sh, const Epi& epi, hipStream_t stream) {
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
@@ -1324,24 +1424,20 @@ void launch_gemm(const SA* A, const SB* B, const GemmShape& sh, const Epi& epi, 
   s2.tail0 = 0;
   s2.pieces = 0;
   if (sh.part) {
-    // a last round of at most half the resident work-groups: cut its tiles
-    // along K into up to 16 pieces that fill one round
+    // a last round of at most half the resident work-groups: its tiles cut
+    // along K (tail_pieces)
     static std::atomic<int> slots_cache[16];
     const int slots = gemm_slots(kern, Cfg::NT, slots_cache);
-    const long long rem = slots > 0 ? blocks % slots : 0;
-    const int nk = sh.K / GemmK<T>::BK;
-    if (slots > 0 && blocks >= slots && rem > 0 && 2 * rem <= slots) {
-      const long long pieces = std::min<long long>(
-          {slots / rem, 16ll, (long long)nk, sh.part_cap / (rem * Cfg::BM * Cfg::BN)});
-      if (pieces >= 2) {
-        s2.tail0 = (int)(blocks - rem);
-        s2.pieces = (int)pieces;
-        hipLaunchKernelGGL(kern, dim3((unsigned)(blocks - rem + rem * pieces)), dim3(Cfg::NT), 0, stream, A, B, s2,
-                           epi);
-        hipLaunchKernelGGL((gemm_kernel<Cfg, T, SA, SB, A_KN, B_NN, SYM, Epi, true>), dim3((unsigned)rem),
-                           dim3(Cfg::NT), 0, stream, A, B, s2, epi);
-        return;
-      }
+    const int pieces = tail_pieces(blocks, slots, sh.K / GemmK<T>::BK, sh.part_cap, (long long)Cfg::BM * Cfg::BN);
+    if (pieces) {
+      const long long rem = blocks % slots;
+      s2.tail0 = (int)(blocks - rem);
+      s2.pieces = pieces;
+      hipLaunchKernelGGL(kern, dim3((unsigned)(blocks - rem + rem * pieces)), dim3(Cfg::NT), 0, stream, A, B, s2,
+                         epi);
+      hipLaunchKernelGGL((gemm_kernel<Cfg, T, SA, SB, A_KN, B_NN, SYM, Epi, true>), dim3((unsigned)rem),
+                         dim3(Cfg::NT), 0, stream, A, B, s2, epi);
+      return;
     }
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)blocks), dim3(Cfg::NT), 0, stream, A, B, s2, epi);

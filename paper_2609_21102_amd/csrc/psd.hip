@@ -532,8 +532,9 @@ struct PsdPlan {
 
 static void plan_psd(PsdPlan& p, Arena& ar) {
   const size_t nn = (size_t)p.n_pad * p.n_pad;
-  // fp32 products: room for 512 partial 128 x 128 tiles (32 MB)
-  p.split_cap = p.f16 ? 0 : 512ll * 128 * 128;
+  // partial tiles of a last round cut along K: 512 of 128 x 128 for the
+  // fp32 products (32 MB), 256 of 256 x 256 for the fp16 ones (64 MB)
+  p.split_cap = p.f16 ? (p.wide ? 256ll * 256 * 256 : 0) : 512ll * 128 * 128;
   p.split = p.split_cap ? ar.take<float>((size_t)p.split_cap) : nullptr;
   p.zp = p.copy_in ? ar.take<float>(nn) : nullptr;
   p.r = ar.take<float>(nn);
@@ -943,6 +944,8 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
       const float b = o.poly ? o.poly[nc * t + 1] : -0.5f;
       const float c = (o.poly && nc == 3) ? o.poly[nc * t + 2] : 0.f;
       GemmShape g{np, np, np, np, np, nn, nn, 1};
+      g.part = p.split;   // a mostly idle last round is cut along K (256 x 256 tiles)
+      g.part_cap = p.split_cap;
       EpiGramT<f16_t> eg{};
       eg.stride = nn;
       eg.ld = np;
@@ -1044,6 +1047,8 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
   GemmShape g{np, np, np, np, np, nn, nn, 1};
   if (p.f16 && p.wide) {
     EpiScaleStore<false> es{p.c, p.theta, nn, np};
+    g.part = p.split;
+    g.part_cap = p.split_cap;
     launch_gemm_dma<CfgDma256, false, false>(p.rh, p.steps % 2 ? p.xh1 : p.xh0, g, es, st);
   } else if (p.f16) {
     EpiScaleStore<> es{p.c, p.theta, nn, np};

@@ -358,6 +358,25 @@ def test_config4_f16():
     assert int(info["n_deflated"]) == oinfo.n_deflated
 
 
+@pytest.mark.slow
+def test_f16_tail_split_symmetric():
+    """n = 5888 (23 tiles of 256 a side), fp16 products: the symmetric
+    products' 276 tiles leave a last round of 20 tiles for 256 resident
+    work-groups, which the library cuts along K into 8 pieces each and sums in
+    a second launch. Two filter steps keep the oracle short; the oracle's fp16
+    contract at the fp16 tolerance."""
+    case = workloads.small_psd(5888, k=16, steps=2, case_id=2)
+    say("psd n=5888 k=16 steps=2 (fp16, tail split of the symmetric products)")
+    out, info, _ = gpu_psd(case, precision="f16")
+    want, _, oinfo = opsd.psd_project_deflated(case.z.astype(np.float64), case.qwarm.astype(np.float64),
+                                               steps=case.steps, gamma=case.gamma,
+                                               subspace_iters=case.subspace_iters, mode="f16")
+    err = rel_fro(host64(out), want)
+    say(f"  rel err {err:.3e}")
+    assert err < F16_TOL
+    assert int(info["n_deflated"]) == oinfo.n_deflated
+
+
 def test_config4_f16_quintic_t7():
     # The shape of the paper's SDP filter: T = 7 degree-5 steps in fp16 (the
     # map (15/8, -5/4, 3/8); the paper's own composite is not printed). At
