@@ -1369,15 +1369,26 @@ inline int gemm_slots(K kern, int nt, std::atomic<int> (&cache)[16]) {
 }
 
 // Pieces for a last round of tiles: with `slots` work-groups resident at once
-// and a last round of rem = blocks % slots tiles that fills at most half of
-// them, up to 16 K pieces per tile that together fill one round (bounded by
-// the K steps and by the caller's space for partials); 0 when not worth it.
+// and a last round of rem = blocks % slots tiles, the number p of K pieces per
+// tile (2 .. 16, at most the K steps, bounded by the caller's space for
+// partials) for which the pieces' rounds, ceil(rem p / slots) / p of a
+// whole-tile round, take least time, if that is at most 0.8 of a round; 0
+// otherwise (no cut).
 inline int tail_pieces(long long blocks, int slots, int nk, long long part_cap, long long tile) {
   if (slots <= 0 || blocks < slots) return 0;
   const long long rem = blocks % slots;
-  if (rem == 0 || 2 * rem > slots) return 0;
-  const long long p = std::min<long long>({slots / rem, 16ll, (long long)nk, part_cap / (rem * tile)});
-  return p >= 2 ? (int)p : 0;
+  if (rem == 0) return 0;
+  int best = 0;
+  double best_t = 0.8;
+  for (int p = 2; p <= 16 && p <= nk; ++p) {
+    if (rem * p * tile > part_cap) break;
+    const double t = (double)((rem * p + slots - 1) / slots) / p;
+    if (t < best_t - 1e-9) {
+      best_t = t;
+      best = p;
+    }
+  }
+  return best;
 }
 
 template <typename Cfg, bool B_NN, bool SYM, typename Epi, typename T>
