@@ -20,6 +20,10 @@
  *     reported synchronously and nothing is enqueued. SD_ERR_HIP reports a
  *     failed allocation or launch. Numerical events found on the device are
  *     reported through the optional `status_dev` word of the options.
+ *   - Non-finite input (NaN, Inf) is not checked: it propagates to the output
+ *     of the matrix that holds it (other matrices of a batch are unaffected),
+ *     and the call completes; every index the kernels derive from values
+ *     (orderings of singular and Ritz values, deflation counts) stays in range.
  *   - Without a caller workspace the library allocates one per call from the
  *     device's stream-ordered memory pool (hipMallocAsync / hipFreeAsync on
  *     `stream`), so calls on different streams do not share scratch memory.

@@ -387,15 +387,21 @@ __host__ __device__ inline int jacobi_class(int n) {
   return n <= 8 ? 4 : n <= 16 ? 8 : n <= 24 ? 12 : n <= 32 ? 16 : n <= 64 ? 32 : 0;
 }
 
+// Sort keys of a descending order with NaN last: every comparison of the
+// rank loops below is then a total order, so the ranks form a permutation of
+// 0 .. n - 1 whatever the values (a NaN compares false both ways and would
+// give several entries one rank, leaving slots of perm unwritten).
+__device__ __forceinline__ double order_key(double v) { return v == v ? v : -__builtin_inf(); }
+
 // Rank of each key under "larger key first, then smaller index": s.perm[rank]
 // = index. Keys must be set in s.key[0..n).
 static __device__ __forceinline__ void sort_desc(SmallLds& s, int n) {
   const int tid = threadIdx.x;
   if (tid < n) {
-    const double k = s.key[tid];
+    const double k = order_key(s.key[tid]);
     int rank = 0;
     for (int j = 0; j < n; ++j) {
-      const double kj = s.key[j];
+      const double kj = order_key(s.key[j]);
       if (kj > k || (kj == k && j < tid)) ++rank;
     }
     s.perm[rank] = tid;
@@ -844,10 +850,10 @@ __global__ __launch_bounds__(SM_THREADS) void ritz_kernel(const double* part, in
   if (tid < K) s.key[tid] = fabs(s.h[tid][tid]);
   __syncthreads();
   if (tid < K) {
-    const double k0 = s.key[tid], lam = s.h[tid][tid];
+    const double k0 = order_key(s.key[tid]), lam = order_key(s.h[tid][tid]);
     int rank = 0;
     for (int j = 0; j < K; ++j) {
-      const double kj = s.key[j], lj = s.h[j][j];
+      const double kj = order_key(s.key[j]), lj = order_key(s.h[j][j]);
       if (kj > k0 || (kj == k0 && (lj > lam || (lj == lam && j < tid)))) ++rank;
     }
     s.perm[rank] = tid;

@@ -654,10 +654,12 @@ __global__ __launch_bounds__(1024) void ritz_wide_kernel(const double* __restric
   }
   __syncthreads();
   if (tid < K) {
-    const double k0 = key[tid], l0 = lam[tid];
+    // total order (order_key: NaN last), so perm is a permutation: it
+    // indexes global memory below
+    const double k0 = order_key(key[tid]), l0 = order_key(lam[tid]);
     int rank = 0;
     for (int j = 0; j < K; ++j) {
-      const double kj = key[j], lj = lam[j];
+      const double kj = order_key(key[j]), lj = order_key(lam[j]);
       if (kj > k0 || (kj == k0 && (lj > l0 || (lj == l0 && j < tid)))) ++rank;
     }
     perm[rank] = tid;

@@ -197,6 +197,23 @@ def test_config3_polar_express_table_sampled(group, batch):
         check_bf16_sample(f"config3 {group} matrix {idx[0]}", got[idx[0]], case, idx)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_nonfinite_input_completes(dtype):
+    """A NaN in one matrix of the batch: that matrix's output is not finite,
+    the call completes (the singular values are ordered with NaN last under a
+    total order, so the head's ordering stays a permutation), and the other
+    matrix is unaffected."""
+    case = workloads.small_muon(2, 96, 160, dtype=dtype, k=4, spikes=[50, 30, 20, 10])
+    xs = case.x.copy()
+    xs[0, 7, 11] = 0x7FC0 if dtype == "bf16" else np.nan   # bf16 quiet NaN bits / float32 NaN
+    out = sd.msign(dev_tensor(xs, dtype), 4, 5)
+    clean = sd.msign(dev_tensor(case.x, dtype), 4, 5)
+    torch.cuda.synchronize()
+    assert not torch.isfinite(out[0].float()).all()
+    assert torch.isfinite(clean.float()).all()
+    assert torch.equal(out[1], clean[1])
+
+
 def test_gate_off_equals_baseline_bitwise():
     # Sec. 2.2: when the gate does not fire the method reduces exactly to Muon.
     case = workloads.small_muon(2, 96, 160, k=3, spikes=[2.0, 1.9, 1.8])

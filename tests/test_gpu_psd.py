@@ -159,6 +159,25 @@ def test_config4_full():
     assert int(info["n_positive"]) == oinfo.n_positive
 
 
+@pytest.mark.parametrize("n,k", [(200, 8), (200, 40)])
+def test_nonfinite_input_completes(n, k):
+    """A NaN in the input propagates to the output; the call completes. The
+    Rayleigh-Ritz ordering of NaN Ritz values once gave a permutation with
+    unwritten slots, which the wide path (K > 32) used as global indices; the
+    ordering now puts NaN last under a total order."""
+    case = workloads.small_psd(n, k=k, case_id=n)
+    z = case.z.copy()
+    z[3, 5] = z[5, 3] = np.nan
+    say(f"psd n={n} k={k} with a NaN entry")
+    zt = torch.from_numpy(z).cuda()
+    q = torch.from_numpy(np.ascontiguousarray(case.qwarm[:, :k])).cuda()
+    out, info = sd.psd_project(zt, k, case.steps, q, subspace_iters=case.subspace_iters, gamma=case.gamma,
+                               info=True)
+    torch.cuda.synchronize()
+    assert not torch.isfinite(out).all()
+    assert 0 <= int(info["n_deflated"]) <= k
+
+
 @pytest.mark.slow
 def test_fp32_tail_split_full_tiling():
     """n = 5000 (padded to 5120), fp32 products: the restore product's 1600
