@@ -49,10 +49,10 @@ struct GemmShape {
   // work-groups that share a B column panel run together on one XCD, so the
   // panel comes from HBM once and from L2 after that.
   int m_fast = 0;
-  // Tail split (register-staged kernel): space for partial accumulators that
-  // the caller may give (part_cap floats); launch_gemm then cuts the tiles of
-  // a last, mostly idle round of work-groups along K (tiles tail0 .. end, in
-  // `pieces` pieces each) and sums the pieces in a second launch.
+  // Tail split: space for partial accumulators that the caller may give
+  // (part_cap floats); the launchers then cut the tiles of a last, partly
+  // idle round of work-groups along K (tiles tail0 .. end, in `pieces`
+  // pieces each; tail_pieces) and sum the pieces in a second launch.
   float* part = nullptr;
   long long part_cap = 0;
   int tail0 = 0, pieces = 0;
@@ -753,9 +753,9 @@ __device__ __forceinline__ void sym_tile(int t, int nt, int& tm, int& tn) {
 // Tail split (sh.pieces > 1): work-groups from sh.tail0 on each compute one
 // K piece of a tile of the last round and store the accumulators to sh.part
 // (piece u of tile t at unit (t - tail0) pieces + u, in the MFMA fragment
-// layout, element-major so that lanes store consecutive floats); FIXUP
-// launches one work-group per such tile, sums its pieces in piece order and
-// runs the epilogue.
+// layout as 16-byte groups of four accumulators, consecutive threads at
+// consecutive groups); FIXUP launches one work-group per such tile, sums its
+// pieces in piece order and runs the epilogue.
 template <typename Cfg, typename T, typename SA, typename SB, bool A_KN, bool B_NN, bool SYM, typename Epi,
           bool FIXUP = false>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void gemm_kernel(const SA* __restrict__ A, const SB* __restrict__ B,
