@@ -1099,14 +1099,15 @@ __global__ __launch_bounds__(256) void admm_y_kernel(const float* __restrict__ X
   y[i] = b[i] * inv_sigma - (X[d] * inv_sigma + S[d] - C[d]);
 }
 
-// Z = C - Diag(y) - X / sigma
+// Z = C - Diag(y) - X / sigma (row by row: work-group g takes rows g,
+// g + gridDim.x, ...; no division per element)
 __global__ __launch_bounds__(256) void admm_z_kernel(const float* __restrict__ C, const float* __restrict__ X,
                                                      const float* __restrict__ y, int n, float inv_sigma,
                                                      float* __restrict__ Z) {
-  const long long nn = (long long)n * n;
-  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < nn; e += (long long)gridDim.x * blockDim.x) {
-    const int i = (int)(e / n), j = (int)(e - (long long)i * n);
-    Z[e] = C[e] - (i == j ? y[i] : 0.f) - X[e] * inv_sigma;
+  for (int i = blockIdx.x; i < n; i += gridDim.x) {
+    const long long r = (long long)i * n;
+    for (int j = threadIdx.x; j < n; j += blockDim.x)
+      Z[r + j] = C[r + j] - (i == j ? y[i] : 0.f) - X[r + j] * inv_sigma;
   }
 }
 
@@ -1117,18 +1118,20 @@ __global__ __launch_bounds__(256) void admm_x_kernel(float* __restrict__ X, cons
                                                      const float* __restrict__ b, int n, float sigma,
                                                      double* __restrict__ part) {
   __shared__ double red[4];
-  const long long nn = (long long)n * n;
   double dual = 0.0, cx = 0.0, prim = 0.0;
-  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < nn; e += (long long)gridDim.x * blockDim.x) {
-    const int i = (int)(e / n), j = (int)(e - (long long)i * n);
-    const float r = S[e] + (i == j ? y[i] : 0.f) - C[e];
-    const float xn = X[e] + sigma * r;
-    X[e] = xn;
-    dual += (double)r * r;
-    cx += (double)C[e] * xn;
-    if (i == j) {
-      const double pr = (double)xn - b[i];
-      prim += pr * pr;
+  for (int i = blockIdx.x; i < n; i += gridDim.x) {   // rows g, g + gridDim.x, ...
+    const long long rw = (long long)i * n;
+    for (int j = threadIdx.x; j < n; j += blockDim.x) {
+      const long long e = rw + j;
+      const float r = S[e] + (i == j ? y[i] : 0.f) - C[e];
+      const float xn = X[e] + sigma * r;
+      X[e] = xn;
+      dual += (double)r * r;
+      cx += (double)C[e] * xn;
+      if (i == j) {
+        const double pr = (double)xn - b[i];
+        prim += pr * pr;
+      }
     }
   }
   dual = block_sum(dual, red);
@@ -1168,12 +1171,11 @@ static void admm_plan(PsdPlan& p, Arena& ar, int n, int k, int steps, const sd_p
 }
 
 // eta: the eigenvalue-free terms of eq:admm_eta from the partial sums. One
-// work-group; the partials are added in block order.
+// work-group; every sum in one fixed order (deterministic).
 __global__ __launch_bounds__(256) void admm_eta_kernel(const double* __restrict__ part, const double* __restrict__ cpart,
                                                        const float* __restrict__ b, const float* __restrict__ y, int n,
                                                        float* __restrict__ eta) {
   __shared__ double red[4];
-  __shared__ double sums[6];
   const int tid = threadIdx.x;
   double bb = 0.0, by = 0.0;
   for (int i = tid; i < n; i += 256) {
@@ -1182,14 +1184,19 @@ __global__ __launch_bounds__(256) void admm_eta_kernel(const double* __restrict_
   }
   bb = block_sum(bb, red);
   by = block_sum(by, red);
+  // the block partials: thread t adds blocks t, t + 256, ..., then a fixed tree
+  double dual = 0.0, cx = 0.0, prim = 0.0, cc = 0.0;
+  for (int k = tid; k < ADMM_BLOCKS; k += 256) {
+    dual += part[3 * k];
+    cx += part[3 * k + 1];
+    prim += part[3 * k + 2];
+    cc += cpart[k];
+  }
+  dual = block_sum(dual, red);
+  cx = block_sum(cx, red);
+  prim = block_sum(prim, red);
+  cc = block_sum(cc, red);
   if (tid == 0) {
-    double dual = 0.0, cx = 0.0, prim = 0.0, cc = 0.0;
-    for (int k = 0; k < ADMM_BLOCKS; ++k) {
-      dual += part[3 * k];
-      cx += part[3 * k + 1];
-      prim += part[3 * k + 2];
-      cc += cpart[k];
-    }
     const double nb = sqrt(bb), nc = sqrt(cc);
     const double e1 = sqrt(prim) / (1.0 + nb);
     const double e2 = sqrt(dual) / (1.0 + nc);
