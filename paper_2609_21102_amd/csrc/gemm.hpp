@@ -151,6 +151,27 @@ struct EpiGramT {
       emit4(out32 + b * stride, ld, r0, c, w, mode);
     }
   }
+  // Off-diagonal symmetric tiles, non-rowwise form (the kernel stages the
+  // transposed copy through LDS): `direct` stores rows r0..r0+3 at column c
+  // and hands back the values to mirror (here the raw product); `mirror8`
+  // stores eight of them along row r from column c0.
+  static constexpr bool MIRROR = !RW;
+  __device__ void direct(int b, int r0, int c, const float v[4], float w[4]) const {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = v[j];
+    operator()(b, r0, c, w, EMIT_FULL);
+  }
+  __device__ void mirror8(int b, int r, int c0, const float (&w)[8]) const {
+    const long long o = b * stride + (long long)r * ld + c0;
+    if (out16)
+      *reinterpret_cast<u32x4_t*>(out16 + o) =
+          u32x4_t{Op16<T16>::pack2(w[0] * scale16, w[1] * scale16), Op16<T16>::pack2(w[2] * scale16, w[3] * scale16),
+                  Op16<T16>::pack2(w[4] * scale16, w[5] * scale16), Op16<T16>::pack2(w[6] * scale16, w[7] * scale16)};
+    if (out32) {
+      *reinterpret_cast<f32x4_t*>(out32 + o) = f32x4_t{w[0], w[1], w[2], w[3]} * scale32;
+      *reinterpret_cast<f32x4_t*>(out32 + o + 4) = f32x4_t{w[4], w[5], w[6], w[7]} * scale32;
+    }
+  }
 };
 using EpiGram = EpiGramT<bf16_t>;
 
@@ -340,6 +361,23 @@ struct EpiUpdateSymNR {
     for (int j = 0; j < 4; ++j) w[j] = ac * xb[(long long)(r0 + j) * ld + c] + v[j];
     emit4(out + b * stride, ld, r0, c, w, mode);
     emit4(out16 + b * stride, ld, r0, c, w, mode);
+  }
+  // off-diagonal tiles: the transposed copy is staged through LDS (EpiGramT)
+  static constexpr bool MIRROR = true;
+  __device__ void direct(int b, int r0, int c, const float v[4], float w[4]) const {
+    const float* xb = x + b * stride;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = ac * xb[(long long)(r0 + j) * ld + c] + v[j];
+    st_col4(out + b * stride, ld, r0, c, w);
+    st_col4(out16 + b * stride, ld, r0, c, w);
+  }
+  __device__ void mirror8(int b, int r, int c0, const float (&w)[8]) const {
+    const long long o = b * stride + (long long)r * ld + c0;
+    *reinterpret_cast<f32x4_t*>(out + o) = f32x4_t{w[0], w[1], w[2], w[3]};
+    *reinterpret_cast<f32x4_t*>(out + o + 4) = f32x4_t{w[4], w[5], w[6], w[7]};
+    *reinterpret_cast<u32x4_t*>(out16 + o) =
+        u32x4_t{Op16<T16>::pack2(w[0], w[1]), Op16<T16>::pack2(w[2], w[3]), Op16<T16>::pack2(w[4], w[5]),
+                Op16<T16>::pack2(w[6], w[7])};
   }
 };
 
@@ -548,6 +586,17 @@ struct EpiSplit {
 template <typename E>
 struct EpiSplit<E, std::void_t<decltype(E::SPLIT)>> {
   static constexpr bool value = E::SPLIT;
+};
+
+// Epilogues whose off-diagonal symmetric tiles take the LDS-staged transposed
+// copy declare MIRROR = true (with `direct` and `mirror8`).
+template <typename E, typename = void>
+struct EpiMirror {
+  static constexpr bool value = false;
+};
+template <typename E>
+struct EpiMirror<E, std::void_t<decltype(E::MIRROR)>> {
+  static constexpr bool value = E::MIRROR;
 };
 
 // ------------------------------------------------------- staging ----------
@@ -1026,12 +1075,14 @@ __device__ __forceinline__ void tile_mma_dma(const char* la, const char* lb, f32
 // LDS bytes of gemm_dma_kernel: the ring, or the row-wise epilogue's C tile
 // (rows padded to BN + 8 floats, so the two row groups a store instruction
 // covers fall in different banks) where that is larger.
-template <typename Cfg, bool ROWWISE>
+template <typename Cfg, bool ROWWISE, bool MIRROR = false>
 struct DmaLds {
   static constexpr int RW_LD = Cfg::BN + 8;
+  static constexpr int MIR_LD = Cfg::BM + 4;   // floats per row of the staged transposed half-tile
   static constexpr int RING = Cfg::STAGES * (Cfg::BM + Cfg::BN) * 2 * Cfg::BK;
   static constexpr int CT = ROWWISE ? Cfg::BM * RW_LD * 4 : 0;
-  static constexpr int BYTES = RING > CT ? RING : CT;
+  static constexpr int MIR = MIRROR ? (Cfg::BN / 2) * MIR_LD * 4 : 0;
+  static constexpr int BYTES = RING > CT ? (RING > MIR ? RING : MIR) : (CT > MIR ? CT : MIR);
 };
 
 // One output tile (linear tile id lid over the batch). T: the 16-bit operand
@@ -1304,6 +1355,53 @@ __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* 
     }
   } else {
     const int mode = SYM ? (tm == tn ? EMIT_SYM_DIAG : EMIT_SYM_OFF) : EMIT_FULL;
+    if constexpr (SYM && EpiMirror<Epi>::value) {
+      if (mode == EMIT_SYM_OFF) {
+        // the transposed copy goes through LDS, half the tile's columns at a
+        // time, so that it leaves as 32-byte row chunks instead of scattered
+        // 16-byte pieces. A wave's columns lie in one half: in that half's
+        // pass it stores its own positions straight from the MFMA layout
+        // (rows r0..r0+3 at column c: coalesced across lanes) and puts the
+        // same values, transposed, into LDS; then every wave writes rows of
+        // the staged block.
+        constexpr int ML = DmaLds<Cfg, false, true>::MIR_LD, HC = BN / 2;
+        static_assert(HC % (WN * 32) == 0, "a wave's columns within one half");
+        float* lt = reinterpret_cast<float*>(lds);
+        const int wh = (wn * WN * 32) / HC;   // the half holding this wave's columns
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          __syncthreads();   // the ring (or the previous half) is no longer read
+          if (wh == half) {
+#pragma unroll
+            for (int mi = 0; mi < WM; ++mi) {
+#pragma unroll
+              for (int ni = 0; ni < WN; ++ni)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                  const int rl = wm * WM * 32 + mi * 32 + 8 * i + 4 * h, cl = wn * WN * 32 + ni * 32 + r32;
+                  const float v[4] = {acc[mi][ni][4 * i], acc[mi][ni][4 * i + 1], acc[mi][ni][4 * i + 2],
+                                      acc[mi][ni][4 * i + 3]};
+                  float w[4];
+                  epi.direct(b, m0 + rl, n0 + cl, v, w);
+                  *reinterpret_cast<f32x4_t*>(lt + (cl - half * HC) * ML + rl) = f32x4_t{w[0], w[1], w[2], w[3]};
+                }
+              // the epilogue's own loads one MFMA row of blocks at a time:
+              // all of them next to the live accumulators spilled registers
+              __builtin_amdgcn_sched_barrier(0);
+            }
+          }
+          __syncthreads();
+          for (int q = (int)threadIdx.x; q < HC * (BM / 8); q += Cfg::NT) {
+            const int row = q / (BM / 8), c8 = (q - row * (BM / 8)) * 8;
+            const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(lt + row * ML + c8);
+            const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(lt + row * ML + c8 + 4);
+            const float w8[8] = {a0[0], a0[1], a0[2], a0[3], a1[0], a1[1], a1[2], a1[3]};
+            epi.mirror8(b, n0 + half * HC + row, m0 + c8, w8);
+          }
+        }
+        return;
+      }
+    }
 #pragma unroll
     for (int mi = 0; mi < WM; ++mi)
 #pragma unroll
@@ -1327,7 +1425,7 @@ __device__ __forceinline__ void gemm_dma_tile(const T* __restrict__ A, const T* 
 template <typename Cfg, bool B_NN, bool SYM, typename Epi, typename T, int SPLIT = DMA_WHOLE>
 __global__ __attribute__((amdgpu_flat_work_group_size(1, Cfg::NT), amdgpu_waves_per_eu(Cfg::OCC))) void
 gemm_dma_kernel(const T* __restrict__ A, const T* __restrict__ B, GemmShape sh, Epi epi) {
-  __shared__ __attribute__((aligned(1024))) char lds[DmaLds<Cfg, Epi::ROWWISE>::BYTES];
+  __shared__ __attribute__((aligned(1024))) char lds[DmaLds<Cfg, Epi::ROWWISE, SYM && EpiMirror<Epi>::value>::BYTES];
   const int tm = sh.M / Cfg::BM, tn = sh.N / Cfg::BN;
   const int total = (SYM ? tm * (tm + 1) / 2 : tm * tn) * sh.batch;
   constexpr long long TILE = (long long)Cfg::BM * Cfg::BN;
