@@ -533,10 +533,10 @@ struct PsdPlan {
 static void plan_psd(PsdPlan& p, Arena& ar) {
   const size_t nn = (size_t)p.n_pad * p.n_pad;
   // partial tiles of a last round cut along K: 1024 of 128 x 128 for the
-  // fp32 products (64 MB), 256 of 256 x 256 for the fp16 ones (64 MB); none
+  // fp32 products (64 MB), 512 of 256 x 256 for the fp16 ones (128 MB); none
   // when even the full product has fewer tiles than a 256-CU device holds
   const long long m128 = p.n_pad / 128;
-  p.split_cap = p.f16 ? (p.wide ? 256ll * 256 * 256 : 0) : (m128 * m128 >= 256 ? 1024ll * 128 * 128 : 0);
+  p.split_cap = p.f16 ? (p.wide ? 512ll * 256 * 256 : 0) : (m128 * m128 >= 256 ? 1024ll * 128 * 128 : 0);
   p.split = p.split_cap ? ar.take<float>((size_t)p.split_cap) : nullptr;
   p.zp = p.copy_in ? ar.take<float>(nn) : nullptr;
   p.r = ar.take<float>(nn);
