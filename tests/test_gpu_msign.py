@@ -254,8 +254,11 @@ def test_gate_window_separate_from_k(dtype):
                 check_bf16_sample(f"gate window bf16 k={k} matrix {b}", got[b], case, [b], k=k, tau=0.1, window=6)
 
 
-def test_deterministic_and_transpose_exact():
-    case = workloads.small_muon(2, 100, 260, dtype="bf16", k=4)
+@pytest.mark.parametrize("m,n", [(100, 260), (96, 160)])
+def test_deterministic_and_transpose_exact(m, n):
+    # (96, 160): the tall transpose's short side is a multiple of 8, so its
+    # canonical copy takes 16-byte accesses; (100, 260): element accesses
+    case = workloads.small_muon(2, m, n, dtype="bf16", k=4)
     x = dev_tensor(case.x, "bf16")
     a = sd.msign(x, 4, 5)
     b = sd.msign(x, 4, 5)
