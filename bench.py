@@ -412,7 +412,8 @@ def other_workload(args) -> int:
                "roofline": roof}
     elif args.workload == "peaks":
         # re-measured roofline constants: dense bf16 MFMA rate, HBM copy and
-        # read bandwidth, and the vendor batched GEMM (torch.bmm) on the
+        # read bandwidth (grid-stride and chunk-per-work-group streams, the
+        # chunked read also with non-temporal loads), and the vendor batched GEMM (torch.bmm) on the
         # update's shape (24 x (768 x 768) x (768 x 3072) bf16) for scale
         import ctypes
         plib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_21102_amd", "libsdpeaks.so"))
@@ -420,8 +421,11 @@ def other_workload(args) -> int:
         plib.sdp_mfma_bf16.argtypes = [ctypes.c_int, ctypes.c_int, vp, vp]
         plib.sdp_copy.argtypes = [vp, vp, ctypes.c_size_t, ctypes.c_int, vp]
         plib.sdp_read.argtypes = [vp, ctypes.c_size_t, ctypes.c_int, vp, vp]
+        plib.sdp_copy_chunk.argtypes = [vp, vp, ctypes.c_size_t, vp]
+        plib.sdp_read_chunk.argtypes = [vp, ctypes.c_size_t, ctypes.c_int, vp, vp]
         st = vp(torch.cuda.current_stream().cuda_stream)
         sink = torch.zeros(1 << 16, dtype=torch.float32, device=dev)
+        csink = torch.zeros((1 << 30) // 16 // 1024, dtype=torch.float32, device=dev)   # one per chunk
 
         def timed_ms(fn, reps=5):
             fn()
@@ -442,6 +446,9 @@ def other_workload(args) -> int:
         dst = torch.empty_like(src)
         cp_ms = timed_ms(lambda: plib.sdp_copy(vp(src.data_ptr()), vp(dst.data_ptr()), n4, 256 * 32, st))
         rd_ms = timed_ms(lambda: plib.sdp_read(vp(src.data_ptr()), n4, 256 * 32, vp(sink.data_ptr()), st))
+        cpc_ms = timed_ms(lambda: plib.sdp_copy_chunk(vp(src.data_ptr()), vp(dst.data_ptr()), n4, st))
+        rdc_ms = timed_ms(lambda: plib.sdp_read_chunk(vp(src.data_ptr()), n4, 0, vp(csink.data_ptr()), st))
+        rdn_ms = timed_ms(lambda: plib.sdp_read_chunk(vp(src.data_ptr()), n4, 1, vp(csink.data_ptr()), st))
         del src, dst
         a16 = torch.randn(24, 768, 768, device=dev).to(torch.bfloat16)
         x16 = torch.randn(24, 768, 3072, device=dev).to(torch.bfloat16)
@@ -453,6 +460,9 @@ def other_workload(args) -> int:
                "measured_peaks": {"mfma_bf16_tflops": mf_tf, "mfma_bf16_frac_of_2500": mf_tf / 2500.0,
                                   "hbm_copy_gbs": 2.0 * (1 << 30) / (cp_ms / 1e3) / 1e9,
                                   "hbm_read_gbs": 1.0 * (1 << 30) / (rd_ms / 1e3) / 1e9,
+                                  "hbm_copy_chunk_gbs": 2.0 * (1 << 30) / (cpc_ms / 1e3) / 1e9,
+                                  "hbm_read_chunk_gbs": 1.0 * (1 << 30) / (rdc_ms / 1e3) / 1e9,
+                                  "hbm_read_chunk_nt_gbs": 1.0 * (1 << 30) / (rdn_ms / 1e3) / 1e9,
                                   "bmm_update_shape_us": bmm_ms * 1e3, "bmm_update_shape_tflops": bmm_tf},
                "roofline": {"bound": "mfma", "kernel": "sdp_mfma_bf16_kernel", "achieved": mf_tf, "peak": 2500.0,
                             "unit": "TFLOP/s", "frac": mf_tf / 2500.0, "traffic": None,

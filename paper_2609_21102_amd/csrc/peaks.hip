@@ -2,8 +2,9 @@
 // prices against, re-measured on the device: dense bf16 MFMA throughput
 // (v_mfma_f32_32x32x16_bf16 on register operands, eight independent
 // accumulators per wave) and HBM streaming bandwidth (a float4 copy and a
-// float4 read-and-reduce over buffers far larger than the caches). C entry
-// points; the caller times them.
+// float4 read-and-reduce over buffers far larger than the caches, each in a
+// grid-stride and a chunk-per-work-group form). C entry points; the caller
+// times them.
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 
@@ -67,6 +68,32 @@ __global__ __launch_bounds__(256) void sdp_read_kernel(const float4* __restrict_
   if (s == -1.0f) sink[blockIdx.x] = s;
 }
 
+// The same streams with one contiguous chunk of 256 U float4 per work-group
+// (every load of the chunk in flight before its first use; a grid of n /
+// (256 U) work-groups, n a multiple of 256 U): whole DRAM pages per work-group
+// instead of the grid-stride pattern above, and, for the read, optionally
+// non-temporal loads.
+template <bool NT>
+__global__ __launch_bounds__(256) void sdp_read_chunk_kernel(const f32x4_t* __restrict__ src, float* sink) {
+  const f32x4_t* p = src + (size_t)blockIdx.x * 256 * STREAM_U + threadIdx.x;
+  f32x4_t v[STREAM_U];
+#pragma unroll
+  for (int u = 0; u < STREAM_U; ++u) v[u] = NT ? __builtin_nontemporal_load(p + u * 256) : p[u * 256];
+  float s = 0.f;
+#pragma unroll
+  for (int u = 0; u < STREAM_U; ++u) s += v[u][0] + v[u][1] + v[u][2] + v[u][3];
+  if (s == -1.0f) sink[blockIdx.x] = s;
+}
+__global__ __launch_bounds__(256) void sdp_copy_chunk_kernel(const f32x4_t* __restrict__ src,
+                                                             f32x4_t* __restrict__ dst) {
+  const size_t o = (size_t)blockIdx.x * 256 * STREAM_U + threadIdx.x;
+  f32x4_t v[STREAM_U];
+#pragma unroll
+  for (int u = 0; u < STREAM_U; ++u) v[u] = src[o + u * 256];
+#pragma unroll
+  for (int u = 0; u < STREAM_U; ++u) __builtin_nontemporal_store(v[u], &dst[o + u * 256]);
+}
+
 extern "C" {
 // flops of one sdp_mfma_bf16 launch: blocks * 4 waves * 8 * iters * 32768
 int sdp_mfma_bf16(int blocks, int iters, float* sink, hipStream_t stream) {
@@ -84,6 +111,23 @@ int sdp_copy(const void* src, void* dst, size_t n, int blocks, hipStream_t strea
 int sdp_read(const void* src, size_t n, int blocks, float* sink, hipStream_t stream) {
   if (!src || n == 0 || blocks < 1 || !sink || n % ((size_t)blocks * 256 * STREAM_U)) return -1;
   hipLaunchKernelGGL(sdp_read_kernel, dim3(blocks), dim3(256), 0, stream, (const float4*)src, n, sink);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+// Chunked forms: n float4 elements, a multiple of 256 * 4; the grid is n / 1024
+// work-groups (at most 2^31 - 1), so sink must hold n / 1024 floats.
+int sdp_copy_chunk(const void* src, void* dst, size_t n, hipStream_t stream) {
+  const size_t chunk = (size_t)256 * STREAM_U;
+  if (!src || !dst || n == 0 || n % chunk || n / chunk > 0x7fffffffull) return -1;
+  hipLaunchKernelGGL(sdp_copy_chunk_kernel, dim3((unsigned)(n / chunk)), dim3(256), 0, stream, (const f32x4_t*)src,
+                     (f32x4_t*)dst);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+int sdp_read_chunk(const void* src, size_t n, int nontemporal, float* sink, hipStream_t stream) {
+  const size_t chunk = (size_t)256 * STREAM_U;
+  if (!src || !sink || n == 0 || n % chunk || n / chunk > 0x7fffffffull) return -1;
+  const dim3 g((unsigned)(n / chunk));
+  if (nontemporal) hipLaunchKernelGGL(sdp_read_chunk_kernel<true>, g, dim3(256), 0, stream, (const f32x4_t*)src, sink);
+  else hipLaunchKernelGGL(sdp_read_chunk_kernel<false>, g, dim3(256), 0, stream, (const f32x4_t*)src, sink);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 }
