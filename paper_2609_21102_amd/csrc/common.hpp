@@ -101,6 +101,15 @@ __device__ __forceinline__ void st16_nt(void* p, const u32x4_t& v) {
 __device__ __forceinline__ void st8_nt(void* p, const u32x2_t& v) {
   __builtin_nontemporal_store(v, reinterpret_cast<u32x2_t*>(p));
 }
+// Streaming when NT, else an ordinary store (for a result the next launch
+// reads at once and that fits in the last-level cache). A compile-time
+// choice: with a run-time flag the compiler merges the two stores into one
+// and the non-temporal hint is lost.
+template <bool NT>
+__device__ __forceinline__ void st16_pol(void* p, const u32x4_t& v) {
+  if constexpr (NT) st16_nt(p, v);
+  else st16(p, v);
+}
 
 // Element traits: storage type -> float and back.
 template <typename T> struct Cvt;

@@ -354,16 +354,30 @@ static int run_msign(const MsignPlan& p, const float* coeffs, const sd_msign_opt
       eg.out32 = reinterpret_cast<float*>(bm);
       eg.scale32 = b;
     }
+    // bf16 path: the Gram's copies and B stay cacheable for their reader
+    // when small enough (stream_outputs)
     {
       ProfScope ps(SD_STAGE_NS_GRAM, st);
-      sym_gemm<T>(xop(), g1, eg, st);
+      if constexpr (BF) {
+        if (stream_outputs((long long)B * ss * ((eg.out32 ? 4 : 0) + (eg.out16 ? 2 : 0))))
+          sym_gemm<T>(xop(), g1, eg, st);
+        else
+          sym_gemm<T>(xop(), g1, cached_stores(eg), st);
+      } else {
+        sym_gemm<T>(xop(), g1, eg, st);
+      }
     }
     if (c != 0.f) {
       GemmShape g2{p.s_pad, p.s_pad, p.s_pad, p.s_pad, p.s_pad, ss, ss, B};
       EpiPoly<T> ep{p.a32, bm, b, c, ss, p.s_pad};
       const T* aop = BF ? reinterpret_cast<const T*>(p.a16) : reinterpret_cast<const T*>(p.a32);
       ProfScope ps(SD_STAGE_NS_POLY, st);
-      sym_gemm<T>(aop, g2, ep, st);
+      if constexpr (BF) {
+        if (stream_outputs((long long)B * ss * 2)) sym_gemm<T>(aop, g2, ep, st);
+        else sym_gemm<T>(aop, g2, cached_stores(ep), st);
+      } else {
+        sym_gemm<T>(aop, g2, ep, st);
+      }
     }
     GemmShape g3{p.s_pad, p.l_pad, p.s_pad, p.s_pad, p.l_pad, ss, sl, B, 1};
     const bool last = t + 1 == p.steps;

@@ -970,14 +970,17 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
           ew.stride = eg.stride;
           ew.ld = eg.ld;
           launch_gemm_dma<CfgDma256, false, true>(hc, hc, g, ew, st);
-        } else {
+        } else if (stream_outputs(nn * ((eg.out32 ? 4 : 0) + (eg.out16 ? 2 : 0)))) {
           launch_gemm_dma<CfgDma128, false, true>(hc, hc, g, eg, st);
+        } else {   // small enough to stay cacheable for the next product
+          launch_gemm_dma<CfgDma128, false, true>(hc, hc, g, cached_stores(eg), st);
         }
       }
       if (c != 0.f) {
         ProfScope ps(SD_STAGE_NS_POLY, st);
         EpiPoly<f16_t> ep{p.s32, p.bh, b, c, nn, np};
-        launch_gemm_dma<CfgDma128, false, true>(p.ah, p.ah, g, ep, st);
+        if (stream_outputs(2 * nn)) launch_gemm_dma<CfgDma128, false, true>(p.ah, p.ah, g, ep, st);
+        else launch_gemm_dma<CfgDma128, false, true>(p.ah, p.ah, g, cached_stores(ep), st);
       }
       {
         ProfScope ps(SD_STAGE_NS_UPDATE, st);
