@@ -986,8 +986,14 @@ static int run_psd(const PsdPlan& p, const float* X, float* Qwarm, float* out, c
         ProfScope ps(SD_STAGE_NS_UPDATE, st);
         // B X = B X^T: the NT form on rows of X; symmetric tiles
         if (wide) {
-          EpiUpdateSymNR<f16_t> eu{cur, a, nxt, hn, nn, np};
-          launch_gemm_dma<CfgDma256, false, true>(p.bh, hc, g, eu, st);
+          // fp32 and fp16 outputs: 6 bytes per entry
+          if (stream_outputs(6 * nn)) {
+            EpiUpdateSymNR<f16_t, true> eu{cur, a, nxt, hn, nn, np};
+            launch_gemm_dma<CfgDma256, false, true>(p.bh, hc, g, eu, st);
+          } else {
+            EpiUpdateSymNR<f16_t> eu{cur, a, nxt, hn, nn, np};
+            launch_gemm_dma<CfgDma256, false, true>(p.bh, hc, g, eu, st);
+          }
         } else {
           EpiUpdateSym<f16_t> eu{cur, a, nxt, hn, nn, np};
           launch_gemm_dma<CfgDma128, false, true>(p.bh, hc, g, eu, st);
