@@ -189,9 +189,10 @@ static __device__ __forceinline__ void jacobi_eig(SmallLds& s, int n, int tol_ex
 //     slots) is held as 2 x 2 units (rows 2p, 2p + 1; columns T_q, B_q).
 //   * The ring step goes through LDS (s.h2, s.e2): one round trip per round.
 //   * Stop after N - 1 consecutive rounds without a rotation (every pair was
-//     checked with nothing changed in between), or after 40 sweeps (or
-//     max_rounds rounds when given: a partial solve whose accumulated
-//     rotation is s.e).
+//     checked with nothing changed in between), or at the first round without
+//     one in which no off-diagonal entry passes the rotation rule (the same
+//     values, sooner), or after 40 sweeps (or max_rounds rounds when given: a
+//     partial solve whose accumulated rotation is s.e).
 //   * S: any LDS struct with h, e, h2, e2 of at least N x N (and red for NW > 1).
 // Input: s.h (n x n). Output as jacobi_eig: eigenvalues on the diagonal of
 // s.h (off-diagonal entries are left as they were) and eigenvectors as the
@@ -266,6 +267,25 @@ __device__ __forceinline__ int jacobi_eig_wave(S& s, int n, int tol_exp, int max
   const double abs_floor = __builtin_amdgcn_ldexp(sqrt(fro), tol_exp);
   int idle = 0, R = 0;
   const int round_cap = max_rounds > 0 ? max_rounds : 40 * (N - 1);
+  // Would the rotation rule fire on any off-diagonal entry this lane holds
+  // (the entry with its own two diagonal entries, in either orientation)?
+  // When it fires on none in a round that rotated nothing, no later round can
+  // rotate either, as the values no longer change: the solve stops there,
+  // with the values the remaining idle rounds would have left.
+  auto pending = [&]() {
+    bool any = false;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int r1 = 0; r1 < 2; ++r1)
+#pragma unroll
+        for (int r2 = 0; r2 < 2; ++r2) {
+          const double x = h[u][2 * r1 + r2], a = tp[u][r1], d = tq[u][r2];
+          const bool off = bp[u] != bq[u] || r1 != r2;
+          any |= act[u] && off && x * x > 0x1p-100 * fabs(a * d) && fabs(x) > abs_floor;
+        }
+    return any;
+  };
   while (idle < N - 1 && R < round_cap) {
     // every lane chooses the angles of its own pairs p and q from their
     // diagonal blocks (the same inputs give the same angles in every lane)
@@ -303,6 +323,7 @@ __device__ __forceinline__ int jacobi_eig_wave(S& s, int n, int tol_exp, int max
       }
     } else if constexpr (NW == 1) {
       ++idle;
+      if (!__any(pending())) break;
     }
     // ring step; each lane also picks up the diagonal blocks of its new p, q
 #pragma unroll
@@ -321,6 +342,8 @@ __device__ __forceinline__ int jacobi_eig_wave(S& s, int n, int tol_exp, int max
     } else {
       const bool any = __syncthreads_or(rot);
       idle = any ? 0 : idle + 1;
+      // (the skipped pairs' unit rotations left the values as they were)
+      if (!any && !__syncthreads_or(pending())) break;
     }
 #pragma unroll
     for (int u = 0; u < U; ++u)
