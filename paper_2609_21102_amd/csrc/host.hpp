@@ -206,6 +206,13 @@ inline void gram_partials(const float* A, long long sa, int lda, const float* B,
                           int cb, int len_pad, bool sym, double* part, int batch, hipStream_t st) {
   const dim3 g((len_pad / GP_CHUNK) * batch), b(256);
   const int cm = ca > cb ? ca : cb;
+  if (cm > 16 && sym && A == B && sa == sb && lda == ldb && ca == cb) {
+    // one panel of more than 16 rows: the blocked kernel (at 16 rows and
+    // fewer its one-entry blocks measured slower than the kernel below)
+    if (cm <= 32) hipLaunchKernelGGL((gram_partial_sym_kernel<32, 2>), g, b, 0, st, A, sa, lda, ca, len_pad, part, batch);
+    else hipLaunchKernelGGL((gram_partial_sym_kernel<64, 4>), g, b, 0, st, A, sa, lda, ca, len_pad, part, batch);
+    return;
+  }
   if (cm <= 16) hipLaunchKernelGGL((gram_partial_kernel<16>), g, b, 0, st, A, sa, lda, B, sb, ldb, ca, cb, len_pad, sym, part, batch);
   else if (cm <= 32) hipLaunchKernelGGL((gram_partial_kernel<32>), g, b, 0, st, A, sa, lda, B, sb, ldb, ca, cb, len_pad, sym, part, batch);
   else hipLaunchKernelGGL((gram_partial_kernel<64>), g, b, 0, st, A, sa, lda, B, sb, ldb, ca, cb, len_pad, sym, part, batch);

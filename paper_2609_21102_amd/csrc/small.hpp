@@ -495,6 +495,78 @@ __global__ __launch_bounds__(256) void gram_partial_kernel(const float* A, long 
   }
 }
 
+// The symmetric case (A = B) with the same results: the chunk's rows are
+// converted to float64 once, into LDS (the product of two float32 values is
+// exact in float64, so converting per product or per value gives the same
+// terms), and each thread forms a BS x BS block of entries (a, bb) of the
+// upper block triangle, every entry one running sum over the positions in
+// order, as above. The blocks share their row loads and give BS^2
+// independent sums per thread. Grid: (len_pad / 128) * batch; 256 threads;
+// CM / BS = 16 block rows (136 blocks). Used for panels of 17 to 64 rows.
+template <int CM, int BS>
+__global__ __launch_bounds__(256) void gram_partial_sym_kernel(const float* A, long long sa, int lda, int ca,
+                                                               int len_pad, double* part, int batch) {
+  constexpr int PD = GP_CHUNK + 2;   // doubles per row: rows start 16 bytes apart in the banks
+  constexpr int NB = CM / BS, NBLK = NB * (NB + 1) / 2;
+  static_assert(NBLK <= 256 && GP_CHUNK % 2 == 0, "one block per thread");
+  __shared__ __attribute__((aligned(16))) double td[CM][PD];
+  const int nch = len_pad / GP_CHUNK;
+  const int b = blockIdx.x / nch, ch = blockIdx.x - b * nch;
+  const int x0 = ch * GP_CHUNK;
+  constexpr int PER = CM * GP_CHUNK / 256;
+  const float* Ab = A + b * sa;
+  float va[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + 256 * u, a = e / GP_CHUNK, x = e - a * GP_CHUNK;
+    va[u] = a < ca ? Ab[(long long)a * lda + x0 + x] : 0.f;
+  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + 256 * u, a = e / GP_CHUNK, x = e - a * GP_CHUNK;
+    td[a][x] = (double)va[u];
+  }
+  __syncthreads();
+  const int blk = threadIdx.x;
+  if (blk >= NBLK) return;
+  int I = 0, q = blk;   // block (I, J), I <= J, row-major over the upper block triangle
+  while (q >= NB - I) {
+    q -= NB - I;
+    ++I;
+  }
+  const int J = I + q;
+  if (I * BS >= ca || J * BS >= ca) return;
+  double t[BS][BS];
+#pragma unroll
+  for (int i = 0; i < BS; ++i)
+#pragma unroll
+    for (int j = 0; j < BS; ++j) t[i][j] = 0.0;
+#pragma unroll 4
+  for (int x = 0; x < GP_CHUNK; x += 2) {
+    f64x2_t ra[BS], rb[BS];   // positions x and x + 1 of the block's rows
+#pragma unroll
+    for (int i = 0; i < BS; ++i) ra[i] = *reinterpret_cast<const f64x2_t*>(&td[I * BS + i][x]);
+#pragma unroll
+    for (int j = 0; j < BS; ++j) rb[j] = *reinterpret_cast<const f64x2_t*>(&td[J * BS + j][x]);
+#pragma unroll
+    for (int i = 0; i < BS; ++i)
+#pragma unroll
+      for (int j = 0; j < BS; ++j) {
+        t[i][j] += ra[i][0] * rb[j][0];
+        t[i][j] += ra[i][1] * rb[j][1];
+      }
+  }
+  const int items = gram_items(ca, ca, true);
+  double* out = part + ((long long)b * nch + ch) * items;
+#pragma unroll
+  for (int i = 0; i < BS; ++i)
+#pragma unroll
+    for (int j = 0; j < BS; ++j) {
+      const int a = I * BS + i, bb = J * BS + j;
+      if (a <= bb && bb < ca) out[a * ca - a * (a - 1) / 2 + (bb - a)] = t[i][j];
+    }
+}
+
 // s.h[a][bb] = sum of the chunk partials in chunk order (mirrored when sym).
 // Loads are issued 32 chunks at a time (one round trip for up to 4096
 // positions); the additions keep chunk order.
