@@ -664,7 +664,7 @@ template <int CM>
 __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp, int ld, int c, int len_pad,
                                                          const double* fac, int batch, bf16_t* Pt16, int c16,
                                                          long long sp16) {
-  __shared__ double L[CM][CM + 1];
+  __shared__ __attribute__((aligned(16))) double L[CM][CM + 2];   // even pitch: 16-byte pairs
   __shared__ double inv_d[CM];
   const int per = len_pad / 128;
   const int b = blockIdx.x / per;
@@ -681,7 +681,12 @@ __global__ __launch_bounds__(128) void chol_apply_kernel(float* Pt, long long sp
     if (jj < c) {
       double v = (double)P[(long long)jj * ld + x];
 #pragma unroll
-      for (int i = 0; i < jj; ++i) v -= q[i] * L[jj][i];
+      for (int i = 0; i + 1 < jj; i += 2) {   // the same terms in the same order, two per LDS read
+        const f64x2_t l2 = *reinterpret_cast<const f64x2_t*>(&L[jj][i]);
+        v -= q[i] * l2[0];
+        v -= q[i + 1] * l2[1];
+      }
+      if (jj & 1) v -= q[jj - 1] * L[jj][jj - 1];
       q[jj] = v * inv_d[jj];
     }
   }
@@ -712,7 +717,7 @@ __global__ __launch_bounds__(128) void chol_qr_kernel(float* Pt, long long sp, i
                                                       int c16, long long sp16) {
   static_assert(CM <= 16, "rows in registers: wider panels use the two-kernel path");
   __shared__ double G[CM][CM + 1];
-  __shared__ double L[CM][CM + 1];
+  __shared__ __attribute__((aligned(16))) double L[CM][CM + 2];   // even pitch: 16-byte pairs
   __shared__ double inv_d[CM];
   __shared__ double colv[CM];
   const int per = len_pad / 128;
@@ -806,7 +811,12 @@ __global__ __launch_bounds__(128) void chol_qr_kernel(float* Pt, long long sp, i
     if (jj < c) {
       double v = (double)pv[jj];
 #pragma unroll
-      for (int i = 0; i < jj; ++i) v -= q[i] * L[jj][i];
+      for (int i = 0; i + 1 < jj; i += 2) {   // the same terms in the same order, two per LDS read
+        const f64x2_t l2 = *reinterpret_cast<const f64x2_t*>(&L[jj][i]);
+        v -= q[i] * l2[0];
+        v -= q[i + 1] * l2[1];
+      }
+      if (jj & 1) v -= q[jj - 1] * L[jj][jj - 1];
       q[jj] = v * inv_d[jj];
     }
   }
